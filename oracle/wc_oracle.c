@@ -1,0 +1,789 @@
+/*
+ * wc_oracle.c -- CPU ORACLE for the chunked rANS weight codec.
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the plain, slow, single-threaded
+ * statement of what the GPU decode path must reproduce.  Only the tests, the
+ * package smoke check and the benchmark's CPU-baseline leg load it.  It shares
+ * no code, header, table or constant with the HIP library; everything below
+ * is written out from the paper and from the format readings documented next
+ * to each function.
+ *
+ * Paper: "Approaching Shannon Bound with Lossless LLM Weight Compression".
+ *   Sec. II-B   per-tensor empirical entropy over format-defined symbols,
+ *               element-weighted model entropy.
+ *   Sec. IV-A   tile-partitioned, independently decodable ANS substreams with
+ *               an offset index table.
+ *   Sec. V-B    offline compression: static frequency table, independent
+ *               initial state per tile.
+ *   Alg. 2      warp-cooperative rANS decode: slot = state mod 2^b, table
+ *               lookup (symbol, freq, cumfreq), state <- f*floor(s/2^b)+slot-c,
+ *               renormalise from the interleaved stream.
+ *   Sec. VI-F   metadata closed form 4 B * N_tiles + 2^b * 4 B (Table 3).
+ *
+ * Every arithmetic step is integer except the entropy (fp64).  Nothing here
+ * is blocked, fused or reordered beyond what the definitions state.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ------------------------------------------------------------------------ */
+/* Constants of the format (own copy; see the format readings).              */
+
+#define ORC_DT_BF16 1
+#define ORC_DT_FP16 2
+#define ORC_DT_U8 3
+#define ORC_DT_U4 4
+
+#define ORC_PROB_BITS 12u
+#define ORC_M (1u << ORC_PROB_BITS)   /* table total 2^12 (Sec. VI-F, b = 12) */
+#define ORC_STATE_LOW (1u << 16)       /* rANS lower bound of the state        */
+#define ORC_MAGIC 0x31424357u          /* bytes 'W','C','B','1'                */
+#define ORC_VERSION 1u
+
+#define ORC_OK 0
+#define ORC_EINVAL (-1)
+#define ORC_ENOMEM (-2)
+#define ORC_ECORRUPT (-3)
+
+/* ------------------------------------------------------------------------ */
+/* Little-endian byte access, written out so the layout is explicit.         */
+
+static void put16(uint8_t* p, uint32_t v) { p[0] = (uint8_t)v; p[1] = (uint8_t)(v >> 8); }
+static void put32(uint8_t* p, uint32_t v) {
+  for (int i = 0; i < 4; i++) p[i] = (uint8_t)(v >> (8 * i));
+}
+static void put64(uint8_t* p, uint64_t v) {
+  for (int i = 0; i < 8; i++) p[i] = (uint8_t)(v >> (8 * i));
+}
+static uint32_t get16(const uint8_t* p) { return (uint32_t)p[0] | ((uint32_t)p[1] << 8); }
+static uint32_t get32(const uint8_t* p) {
+  uint32_t v = 0;
+  for (int i = 3; i >= 0; i--) v = (v << 8) | p[i];
+  return v;
+}
+static uint64_t get64(const uint8_t* p) {
+  uint64_t v = 0;
+  for (int i = 7; i >= 0; i--) v = (v << 8) | p[i];
+  return v;
+}
+static uint64_t round16(uint64_t x) { return (x + 15) / 16 * 16; }
+
+/* ------------------------------------------------------------------------ */
+/* Field split (Sec. II-B: symbols are determined by the numeric format).    */
+/*
+ * A 16-bit float word w (bf16, or fp16 with the same bit positions) is split
+ * into a coded byte -- bits 14..7, i.e. the bf16 exponent -- and a raw byte
+ * holding the sign (bit 15) in its top bit and bits 6..0 below it.  The split
+ * is a bit permutation, so every pattern (NaN, Inf, subnormal, -0) survives.
+ */
+uint8_t orc_coded16(uint16_t w) { return (uint8_t)((w >> 7) & 0xFF); }
+uint8_t orc_raw16(uint16_t w) { return (uint8_t)(((w >> 15) & 1) << 7 | (w & 0x7F)); }
+uint16_t orc_merge16(uint8_t coded, uint8_t raw) {
+  uint32_t sign = (raw >> 7) & 1;
+  uint32_t low7 = raw & 0x7F;
+  return (uint16_t)((sign << 15) | ((uint32_t)coded << 7) | low7);
+}
+
+static int dtype_ok(uint32_t dt) { return dt >= ORC_DT_BF16 && dt <= ORC_DT_U4; }
+static int has_raw(uint32_t dt) { return dt == ORC_DT_BF16 || dt == ORC_DT_FP16; }
+static uint32_t alphabet_of(uint32_t dt) { return dt == ORC_DT_U4 ? 16u : 256u; }
+/* Symbols per lane-group: a lane-group always covers 4 output bytes. */
+static uint32_t group_of(uint32_t dt) {
+  return dt == ORC_DT_U4 ? 8u : (dt == ORC_DT_U8 ? 4u : 2u);
+}
+
+/* Number of coded symbols of a tensor of `nbytes` storage bytes. */
+static uint64_t n_symbols_of(uint32_t dt, uint64_t nbytes) {
+  if (dt == ORC_DT_U4) return 2 * nbytes;
+  if (dt == ORC_DT_U8) return nbytes;
+  return nbytes / 2;
+}
+
+/*
+ * Coded symbol stream (and raw bytes for 16-bit types) of a tensor.
+ * int8: one symbol per byte.  int4: two symbols per byte, low nibble first.
+ */
+int orc_symbols(uint32_t dt, const uint8_t* data, uint64_t nbytes, uint8_t* coded,
+                uint8_t* raw) {
+  if (!dtype_ok(dt)) return ORC_EINVAL;
+  if (has_raw(dt) && (nbytes % 2) != 0) return ORC_EINVAL;
+  uint64_t n = n_symbols_of(dt, nbytes);
+  for (uint64_t i = 0; i < n; i++) {
+    if (dt == ORC_DT_U8) {
+      coded[i] = data[i];
+    } else if (dt == ORC_DT_U4) {
+      uint8_t byte = data[i / 2];
+      coded[i] = (i % 2 == 0) ? (byte & 0x0F) : (byte >> 4);
+    } else {
+      uint16_t w = (uint16_t)(data[2 * i] | (data[2 * i + 1] << 8));
+      coded[i] = orc_coded16(w);
+      raw[i] = orc_raw16(w);
+    }
+  }
+  return ORC_OK;
+}
+
+/* Inverse of orc_symbols: write tensor bytes for symbol range [s0, s0+n). */
+static void put_symbols(uint32_t dt, const uint8_t* coded, const uint8_t* raw, uint64_t s0,
+                        uint64_t n, uint8_t* out) {
+  for (uint64_t k = 0; k < n; k++) {
+    uint64_t i = s0 + k;
+    if (dt == ORC_DT_U8) {
+      out[i] = coded[k];
+    } else if (dt == ORC_DT_U4) {
+      if (i % 2 == 0)
+        out[i / 2] = (uint8_t)((out[i / 2] & 0xF0) | (coded[k] & 0x0F));
+      else
+        out[i / 2] = (uint8_t)((out[i / 2] & 0x0F) | ((coded[k] & 0x0F) << 4));
+    } else {
+      uint16_t w = orc_merge16(coded[k], raw[k]);
+      out[2 * i] = (uint8_t)(w & 0xFF);
+      out[2 * i + 1] = (uint8_t)(w >> 8);
+    }
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Histogram and empirical Shannon entropy (Sec. II-B).                      */
+
+void orc_histogram(const uint8_t* sym, uint64_t n, uint64_t* hist /*[256]*/) {
+  for (int s = 0; s < 256; s++) hist[s] = 0;
+  for (uint64_t i = 0; i < n; i++) hist[sym[i]]++;
+}
+
+/* H = -sum_i p_i log2 p_i with p_i = count_i / n, over `alphabet` bins. */
+double orc_entropy(const uint64_t* hist, uint32_t alphabet) {
+  uint64_t n = 0;
+  for (uint32_t s = 0; s < alphabet; s++) n += hist[s];
+  if (n == 0) return 0.0;
+  double h = 0.0;
+  for (uint32_t s = 0; s < alphabet; s++) {
+    if (hist[s] == 0) continue;
+    double p = (double)hist[s] / (double)n;
+    h -= p * log2(p);
+  }
+  return h;
+}
+
+/* Per-field statistics of one tensor. */
+typedef struct {
+  uint32_t n_fields;       /* 1 (int8/int4) or 2 (coded byte + raw byte) */
+  uint32_t alphabet[2];
+  uint64_t count[2];
+  uint64_t hist[2][256];
+  double H[2];             /* bits per symbol */
+  double H_joint16;        /* over whole 16-bit words; NaN for 8/4-bit types */
+  double bound_bytes;      /* sum over fields of count * H / 8 */
+  double bound_bytes_raw8; /* coded field at H, raw field at 8 bits */
+} orc_stats;
+
+int orc_analyze(uint32_t dt, const uint8_t* data, uint64_t nbytes, orc_stats* st) {
+  if (!dtype_ok(dt) || !st) return ORC_EINVAL;
+  if (has_raw(dt) && nbytes % 2) return ORC_EINVAL;
+  memset(st, 0, sizeof(*st));
+  uint64_t n = n_symbols_of(dt, nbytes);
+  uint8_t* coded = (uint8_t*)malloc(n ? n : 1);
+  uint8_t* raw = (uint8_t*)malloc(n ? n : 1);
+  if (!coded || !raw) {
+    free(coded);
+    free(raw);
+    return ORC_ENOMEM;
+  }
+  orc_symbols(dt, data, nbytes, coded, raw);
+  st->n_fields = has_raw(dt) ? 2 : 1;
+  st->alphabet[0] = alphabet_of(dt);
+  st->count[0] = n;
+  orc_histogram(coded, n, st->hist[0]);
+  st->H[0] = orc_entropy(st->hist[0], st->alphabet[0]);
+  st->bound_bytes = (double)n * st->H[0] / 8.0;
+  st->bound_bytes_raw8 = st->bound_bytes;
+  st->H_joint16 = NAN;
+  if (has_raw(dt)) {
+    st->alphabet[1] = 256;
+    st->count[1] = n;
+    orc_histogram(raw, n, st->hist[1]);
+    st->H[1] = orc_entropy(st->hist[1], 256);
+    st->bound_bytes += (double)n * st->H[1] / 8.0;
+    st->bound_bytes_raw8 += (double)n;
+    uint64_t* h16 = (uint64_t*)calloc(65536, sizeof(uint64_t));
+    if (!h16) {
+      free(coded);
+      free(raw);
+      return ORC_ENOMEM;
+    }
+    for (uint64_t i = 0; i < n; i++) h16[data[2 * i] | (data[2 * i + 1] << 8)]++;
+    st->H_joint16 = 0.0;
+    for (uint32_t w = 0; w < 65536; w++) {
+      if (!h16[w]) continue;
+      double p = (double)h16[w] / (double)n;
+      st->H_joint16 -= p * log2(p);
+    }
+    free(h16);
+  }
+  free(coded);
+  free(raw);
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Normalisation of counts to a 2^12 total (Sec. VI-F: b = 12 probability    */
+/* bits).  The paper does not give the rounding rule; the reading used is an */
+/* integer largest-remainder rule:                                           */
+/*   f_s = floor(c_s * 4096 / n), remainder r_s = c_s * 4096 mod n;          */
+/*   a present symbol rounded to 0 is forced to 1;                           */
+/*   a shortfall d > 0 is handed out +1 each to the d non-forced symbols     */
+/*   with the largest remainder (ties: lower symbol first);                  */
+/*   an excess is removed -1 at a time from the largest f (ties: lower).     */
+
+int orc_normalise(const uint64_t* hist, uint32_t alphabet, uint32_t* freq) {
+  if (alphabet == 0 || alphabet > 256) return ORC_EINVAL;
+  uint64_t n = 0;
+  for (uint32_t s = 0; s < alphabet; s++) n += hist[s];
+  for (uint32_t s = 0; s < alphabet; s++) freq[s] = 0;
+  if (n == 0) return ORC_OK; /* empty field: no table */
+  uint64_t rem[256];
+  int forced[256], chosen[256];
+  int64_t total = 0;
+  for (uint32_t s = 0; s < alphabet; s++) {
+    /* c * 4096 fits in 64 bits for any c < 2^52 */
+    freq[s] = (uint32_t)((hist[s] * ORC_M) / n);
+    rem[s] = (hist[s] * ORC_M) % n;
+    forced[s] = 0;
+    chosen[s] = 0;
+    if (hist[s] > 0 && freq[s] == 0) {
+      freq[s] = 1;
+      forced[s] = 1;
+    }
+    total += freq[s];
+  }
+  int64_t d = (int64_t)ORC_M - total;
+  while (d > 0) {
+    int best = -1;
+    for (uint32_t s = 0; s < alphabet; s++) {
+      if (hist[s] == 0 || forced[s] || chosen[s]) continue;
+      if (best < 0 || rem[s] > rem[best]) best = (int)s;
+    }
+    if (best < 0) return ORC_EINVAL;
+    freq[best] += 1;
+    chosen[best] = 1; /* each symbol receives at most one extra unit */
+    d--;
+  }
+  while (d < 0) {
+    int best = 0;
+    for (uint32_t s = 1; s < alphabet; s++)
+      if (freq[s] > freq[best]) best = (int)s;
+    freq[best] -= 1;
+    d++;
+  }
+  return ORC_OK;
+}
+
+/* cum_s = sum_{t < s} f_t */
+static void cumulative(const uint32_t* freq, uint32_t alphabet, uint32_t* cum) {
+  uint32_t c = 0;
+  for (uint32_t s = 0; s < alphabet; s++) {
+    cum[s] = c;
+    c += freq[s];
+  }
+}
+
+/* ------------------------------------------------------------------------ */
+/* Lane interleave of one chunk (Sec. V-C-3: R substreams, one per lane;    */
+/* indices follow the interleaved decode order).  Reading used: symbol i of */
+/* a chunk belongs to lane (i mod L*W) div W, at step                        */
+/* (i div L*W) * W + (i mod W).  So W consecutive symbols (4 output bytes)  */
+/* belong to one lane, and a row of L*W symbols is spread over the lanes.   */
+
+static uint64_t symbol_at(uint64_t t, uint32_t lane, uint32_t L, uint32_t W) {
+  return (t / W) * (uint64_t)L * W + (uint64_t)lane * W + (t % W);
+}
+
+static uint64_t steps_of(uint64_t n, uint32_t L, uint32_t W) {
+  uint64_t rows = (n + (uint64_t)L * W - 1) / ((uint64_t)L * W);
+  return rows * W;
+}
+
+static uint32_t states_of(uint64_t n, uint32_t L, uint32_t W) {
+  uint64_t groups = (n + W - 1) / W;
+  return (uint32_t)(groups < L ? groups : L);
+}
+
+/* ------------------------------------------------------------------------ */
+/* rANS coding of one chunk.                                                 */
+/*
+ * State x is a 32-bit integer kept in [2^16, 2^32); 16-bit words are moved
+ * in and out; probabilities are f_s / 2^12.
+ *   encode s:  if x >= f_s * 2^20: emit x mod 2^16, x = floor(x / 2^16)
+ *              x = floor(x / f_s) * 2^12 + (x mod f_s) + cum_s
+ *   decode:    slot = x mod 2^12; s = the symbol with cum_s <= slot < cum_s+f_s
+ *              x = f_s * floor(x / 2^12) + slot - cum_s          (Alg. 2)
+ *              if x < 2^16: x = x * 2^16 + next word
+ * Every lane starts the encoder at 2^16, so a correct decode ends with every
+ * lane back at 2^16 and the whole word stream consumed.
+ *
+ * Word order: the encoder runs steps T-1..0 and, within a step, lanes L-1..0,
+ * pushing words on a stack; the stream is that stack read from the top, so
+ * the decoder, running steps 0..T-1 and lanes 0..L-1, meets the words in
+ * stream order.
+ */
+
+int orc_encode_stream(const uint8_t* sym, uint64_t n, const uint32_t* freq, uint32_t alphabet,
+                      uint32_t L, uint32_t W, uint32_t* states /*[L]*/, uint16_t* words,
+                      uint64_t words_cap, uint64_t* n_words, uint32_t* n_states) {
+  if (L == 0 || W == 0) return ORC_EINVAL;
+  uint32_t cum[256];
+  cumulative(freq, alphabet, cum);
+  uint32_t A = states_of(n, L, W);
+  uint64_t T = steps_of(n, L, W);
+  for (uint32_t l = 0; l < A; l++) states[l] = ORC_STATE_LOW;
+  /* the stack is written top-down at the end of `words` and moved later */
+  uint64_t pushed = 0;
+  for (uint64_t tt = T; tt-- > 0;) {
+    for (uint32_t l = A; l-- > 0;) {
+      uint64_t i = symbol_at(tt, l, L, W);
+      if (i >= n) continue;
+      uint32_t s = sym[i];
+      if (s >= alphabet || freq[s] == 0) return ORC_EINVAL;
+      uint64_t x = states[l];
+      uint64_t f = freq[s];
+      if (x >= (f << 20)) {
+        if (pushed >= words_cap) return ORC_ENOMEM;
+        words[words_cap - 1 - pushed] = (uint16_t)(x & 0xFFFF);
+        pushed++;
+        x >>= 16;
+      }
+      x = (x / f) * ORC_M + (x % f) + cum[s];
+      states[l] = (uint32_t)x;
+    }
+  }
+  /* stack top (last pushed) is at words[words_cap - pushed]: stream order */
+  memmove(words, words + (words_cap - pushed), pushed * sizeof(uint16_t));
+  *n_words = pushed;
+  *n_states = A;
+  return ORC_OK;
+}
+
+int orc_decode_stream(const uint32_t* states_in, uint32_t n_states, const uint16_t* words,
+                      uint64_t n_words, uint64_t n, const uint32_t* freq, uint32_t alphabet,
+                      uint32_t L, uint32_t W, uint8_t* sym_out) {
+  if (L == 0 || W == 0 || L > 4096) return ORC_EINVAL;
+  uint32_t A = states_of(n, L, W);
+  if (n_states != A) return ORC_ECORRUPT;
+  uint32_t cum[256];
+  cumulative(freq, alphabet, cum);
+  uint32_t total = 0;
+  for (uint32_t s = 0; s < alphabet; s++) total += freq[s];
+  if (n > 0 && total != ORC_M) return ORC_EINVAL;
+  /* slot -> symbol: symbol s owns slots cum_s .. cum_s + f_s - 1 */
+  uint8_t slot_sym[ORC_M];
+  memset(slot_sym, 0, sizeof(slot_sym));
+  for (uint32_t s = 0; s < alphabet; s++)
+    for (uint32_t k = 0; k < freq[s] && cum[s] + k < ORC_M; k++) slot_sym[cum[s] + k] = (uint8_t)s;
+  uint32_t x[4096];
+  for (uint32_t l = 0; l < A; l++) x[l] = states_in[l];
+  uint64_t cursor = 0;
+  uint64_t T = steps_of(n, L, W);
+  int bad = 0;
+  for (uint64_t t = 0; t < T; t++) {
+    for (uint32_t l = 0; l < A; l++) {
+      uint64_t i = symbol_at(t, l, L, W);
+      if (i >= n) continue;
+      uint32_t slot = x[l] & (ORC_M - 1);
+      uint32_t s = slot_sym[slot];
+      sym_out[i] = (uint8_t)s;
+      x[l] = freq[s] * (x[l] >> ORC_PROB_BITS) + slot - cum[s];
+      if (x[l] < ORC_STATE_LOW) {
+        uint32_t w = 0;
+        if (cursor < n_words)
+          w = words[cursor];
+        else
+          bad = 1;
+        cursor++;
+        x[l] = (x[l] << 16) | w;
+      }
+    }
+  }
+  for (uint32_t l = 0; l < A; l++)
+    if (x[l] != ORC_STATE_LOW) bad = 1;
+  if (cursor != n_words) bad = 1;
+  return bad ? ORC_ECORRUPT : ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Blob: header, tensor descriptors, tables, chunk index, chunk records and  */
+/* the raw bytes (layout readings in the design notes; Sec. IV-A / V-B give  */
+/* per-tile substreams plus an offset table).                                */
+
+typedef struct {
+  const uint8_t* data;
+  uint64_t nbytes;
+  uint32_t dtype;
+} orc_tensor;
+
+static uint64_t symbols_per_chunk(uint32_t dt, uint32_t chunk_bytes) {
+  return n_symbols_of(dt, chunk_bytes);
+}
+
+static uint64_t chunks_of(uint64_t n_sym, uint64_t per) { return (n_sym + per - 1) / per; }
+
+void orc_free(void* p) { free(p); }
+
+int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_bytes, uint32_t L,
+                    uint8_t** blob_out, uint64_t* size_out) {
+  if (!ts || !blob_out || !size_out) return ORC_EINVAL;
+  if (n_tensors == 0 || n_tensors > 4096) return ORC_EINVAL;
+  if (chunk_bytes < 256 || chunk_bytes > (1u << 20) || chunk_bytes % 256) return ORC_EINVAL;
+  if (L < 1 || L > 64) return ORC_EINVAL;
+
+  /* pass 1: symbols, tables, chunk records (kept separately), sizes */
+  uint64_t n_chunks = 0;
+  for (uint32_t t = 0; t < n_tensors; t++) {
+    if (!dtype_ok(ts[t].dtype)) return ORC_EINVAL;
+    if (has_raw(ts[t].dtype) && ts[t].nbytes % 2) return ORC_EINVAL;
+    uint64_t n = n_symbols_of(ts[t].dtype, ts[t].nbytes);
+    n_chunks += chunks_of(n, symbols_per_chunk(ts[t].dtype, chunk_bytes));
+  }
+  if (n_chunks > 0xFFFFFFFEull) return ORC_EINVAL;
+
+  uint8_t** rec = (uint8_t**)calloc(n_chunks ? n_chunks : 1, sizeof(uint8_t*));
+  uint64_t* rec_size = (uint64_t*)calloc(n_chunks ? n_chunks : 1, sizeof(uint64_t));
+  uint32_t* freqs = (uint32_t*)calloc((size_t)n_tensors * 256, sizeof(uint32_t));
+  uint8_t** raws = (uint8_t**)calloc(n_tensors, sizeof(uint8_t*));
+  if (!rec || !rec_size || !freqs || !raws) return ORC_ENOMEM;
+
+  int rc = ORC_OK;
+  uint64_t c_glob = 0;
+  for (uint32_t t = 0; t < n_tensors && rc == ORC_OK; t++) {
+    uint32_t dt = ts[t].dtype;
+    uint64_t n = n_symbols_of(dt, ts[t].nbytes);
+    uint32_t alpha = alphabet_of(dt), W = group_of(dt);
+    uint8_t* coded = (uint8_t*)malloc(n ? n : 1);
+    uint8_t* raw = (uint8_t*)malloc(n ? n : 1);
+    if (!coded || !raw) {
+      rc = ORC_ENOMEM;
+      free(coded);
+      free(raw);
+      break;
+    }
+    orc_symbols(dt, ts[t].data, ts[t].nbytes, coded, raw);
+    uint64_t hist[256];
+    orc_histogram(coded, n, hist);
+    orc_normalise(hist, alpha, freqs + (size_t)t * 256);
+    uint64_t per = symbols_per_chunk(dt, chunk_bytes);
+    uint64_t nc = chunks_of(n, per);
+    for (uint64_t c = 0; c < nc; c++, c_glob++) {
+      uint64_t s0 = c * per;
+      uint64_t len = (n - s0) < per ? (n - s0) : per;
+      /* each symbol pushes at most one word */
+      uint64_t cap = len + 1;
+      uint16_t* words = (uint16_t*)malloc(cap * sizeof(uint16_t));
+      uint32_t states[64];
+      uint64_t nw = 0;
+      uint32_t A = 0;
+      if (!words) {
+        rc = ORC_ENOMEM;
+        break;
+      }
+      rc = orc_encode_stream(coded + s0, len, freqs + (size_t)t * 256, alpha, L, W, states, words,
+                             cap, &nw, &A);
+      if (rc != ORC_OK) {
+        free(words);
+        break;
+      }
+      uint64_t sz = 16 + round16(4ull * A) + round16(2ull * nw);
+      uint8_t* r = (uint8_t*)calloc(sz, 1);
+      if (!r) {
+        free(words);
+        rc = ORC_ENOMEM;
+        break;
+      }
+      put32(r + 0, (uint32_t)nw);
+      put32(r + 4, A);
+      put32(r + 8, (uint32_t)len);
+      put32(r + 12, 0);
+      for (uint32_t l = 0; l < A; l++) put32(r + 16 + 4 * l, states[l]);
+      uint8_t* wp = r + 16 + round16(4ull * A);
+      for (uint64_t k = 0; k < nw; k++) put16(wp + 2 * k, words[k]);
+      free(words);
+      rec[c_glob] = r;
+      rec_size[c_glob] = sz;
+    }
+    if (has_raw(dt) && rc == ORC_OK) {
+      raws[t] = raw;
+      raw = NULL;
+    }
+    free(coded);
+    free(raw);
+  }
+
+  /* pass 2: lay out the blob */
+  uint64_t off_desc = 64;
+  uint64_t off_tables = off_desc + 64ull * n_tensors;
+  uint64_t* freq_off = (uint64_t*)calloc(n_tensors, sizeof(uint64_t));
+  uint64_t* raw_off_t = (uint64_t*)calloc(n_tensors, sizeof(uint64_t));
+  if (!freq_off || !raw_off_t) rc = ORC_ENOMEM;
+  uint64_t pos = off_tables;
+  for (uint32_t t = 0; t < n_tensors && rc == ORC_OK; t++) {
+    freq_off[t] = pos;
+    pos += round16(2ull * alphabet_of(ts[t].dtype));
+  }
+  uint64_t off_index = round16(pos);
+  uint64_t off_records = round16(off_index + 4ull * (n_chunks + 1));
+  pos = off_records;
+  for (uint64_t c = 0; c < n_chunks && rc == ORC_OK; c++) pos += rec_size[c];
+  uint64_t off_raw = pos;
+  for (uint32_t t = 0; t < n_tensors && rc == ORC_OK; t++) {
+    if (has_raw(ts[t].dtype)) {
+      raw_off_t[t] = pos;
+      pos += round16(n_symbols_of(ts[t].dtype, ts[t].nbytes));
+    }
+  }
+  uint64_t total = pos;
+  if (rc == ORC_OK && total / 16 > 0xFFFFFFFFull) rc = ORC_EINVAL;
+
+  uint8_t* b = NULL;
+  if (rc == ORC_OK) {
+    b = (uint8_t*)calloc(total, 1);
+    if (!b) rc = ORC_ENOMEM;
+  }
+  if (rc == ORC_OK) {
+    put32(b + 0, ORC_MAGIC);
+    put16(b + 4, ORC_VERSION);
+    put16(b + 6, 64);
+    put32(b + 8, n_tensors);
+    put32(b + 12, 64);
+    put64(b + 16, n_chunks);
+    put64(b + 24, total);
+    put64(b + 32, off_index);
+    put64(b + 40, off_records);
+    put64(b + 48, off_raw);
+    put64(b + 56, 0);
+    uint64_t first = 0;
+    for (uint32_t t = 0; t < n_tensors; t++) {
+      uint32_t dt = ts[t].dtype;
+      uint64_t n = n_symbols_of(dt, ts[t].nbytes);
+      uint64_t nc = chunks_of(n, symbols_per_chunk(dt, chunk_bytes));
+      uint8_t* d = b + off_desc + 64ull * t;
+      put32(d + 0, dt);
+      put32(d + 4, chunk_bytes);
+      put64(d + 8, n);
+      put64(d + 16, ts[t].nbytes);
+      put64(d + 24, first);
+      put64(d + 32, nc);
+      put16(d + 40, L);
+      d[42] = (uint8_t)group_of(dt);
+      d[43] = (uint8_t)ORC_PROB_BITS;
+      put16(d + 44, alphabet_of(dt));
+      put16(d + 46, 0);
+      put64(d + 48, freq_off[t]);
+      put64(d + 56, raw_off_t[t]);
+      for (uint32_t s = 0; s < alphabet_of(dt); s++)
+        put16(b + freq_off[t] + 2 * s, freqs[(size_t)t * 256 + s]);
+      if (has_raw(dt)) memcpy(b + raw_off_t[t], raws[t], n);
+      first += nc;
+    }
+    pos = off_records;
+    for (uint64_t c = 0; c < n_chunks; c++) {
+      put32(b + off_index + 4 * c, (uint32_t)(pos / 16));
+      memcpy(b + pos, rec[c], rec_size[c]);
+      pos += rec_size[c];
+    }
+    put32(b + off_index + 4 * n_chunks, (uint32_t)(pos / 16));
+  }
+
+  for (uint64_t c = 0; c < n_chunks; c++) free(rec[c]);
+  for (uint32_t t = 0; t < n_tensors; t++) free(raws[t]);
+  free(rec);
+  free(rec_size);
+  free(freqs);
+  free(raws);
+  free(freq_off);
+  free(raw_off_t);
+  if (rc != ORC_OK) {
+    free(b);
+    return rc;
+  }
+  *blob_out = b;
+  *size_out = total;
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Blob reading and validation.                                              */
+
+typedef struct {
+  uint32_t dtype, chunk_bytes, L, W, prob_bits, alphabet;
+  uint64_t n_sym, out_bytes, first_chunk, n_chunks, freq_off, raw_off;
+} orc_desc;
+
+static int read_desc(const uint8_t* b, uint64_t size, uint32_t t, orc_desc* d) {
+  uint32_t n_t = get32(b + 8);
+  if (t >= n_t) return ORC_EINVAL;
+  const uint8_t* p = b + 64 + 64ull * t;
+  d->dtype = get32(p + 0);
+  d->chunk_bytes = get32(p + 4);
+  d->n_sym = get64(p + 8);
+  d->out_bytes = get64(p + 16);
+  d->first_chunk = get64(p + 24);
+  d->n_chunks = get64(p + 32);
+  d->L = get16(p + 40);
+  d->W = p[42];
+  d->prob_bits = p[43];
+  d->alphabet = get16(p + 44);
+  d->freq_off = get64(p + 48);
+  d->raw_off = get64(p + 56);
+  if (!dtype_ok(d->dtype)) return ORC_EINVAL;
+  if (d->prob_bits != ORC_PROB_BITS) return ORC_EINVAL;
+  if (d->W != group_of(d->dtype) || d->alphabet != alphabet_of(d->dtype)) return ORC_EINVAL;
+  if (d->L < 1 || d->L > 64) return ORC_EINVAL;
+  if (d->chunk_bytes < 256 || d->chunk_bytes > (1u << 20) || d->chunk_bytes % 256)
+    return ORC_EINVAL;
+  if (d->n_sym != n_symbols_of(d->dtype, d->out_bytes)) return ORC_EINVAL;
+  if (has_raw(d->dtype) && d->out_bytes % 2) return ORC_EINVAL;
+  if (d->n_chunks != chunks_of(d->n_sym, symbols_per_chunk(d->dtype, d->chunk_bytes)))
+    return ORC_EINVAL;
+  if (d->freq_off + 2ull * d->alphabet > size) return ORC_EINVAL;
+  if (has_raw(d->dtype) && (d->raw_off > size || d->n_sym > size - d->raw_off))
+    return ORC_EINVAL;
+  return ORC_OK;
+}
+
+static int check_header(const uint8_t* b, uint64_t size) {
+  if (!b || size < 64) return ORC_EINVAL;
+  if (get32(b) != ORC_MAGIC || get16(b + 4) != ORC_VERSION || get16(b + 6) != 64 ||
+      get32(b + 12) != 64)
+    return ORC_EINVAL;
+  if (get64(b + 24) != size) return ORC_EINVAL;
+  uint32_t n_t = get32(b + 8);
+  uint64_t n_c = get64(b + 16);
+  uint64_t off_index = get64(b + 32), off_rec = get64(b + 40), off_raw = get64(b + 48);
+  if (n_t == 0 || 64 + 64ull * n_t > size) return ORC_EINVAL;
+  if (off_index > size || n_c + 1 > (size - off_index) / 4) return ORC_EINVAL;
+  if (off_rec > off_raw || off_raw > size) return ORC_EINVAL;
+  uint64_t first = 0;
+  for (uint32_t t = 0; t < n_t; t++) {
+    orc_desc d;
+    int rc = read_desc(b, size, t, &d);
+    if (rc) return rc;
+    if (d.first_chunk != first) return ORC_EINVAL;
+    first += d.n_chunks;
+    if (d.n_sym > 0) {
+      uint32_t sum = 0;
+      for (uint32_t s = 0; s < d.alphabet; s++) sum += get16(b + d.freq_off + 2 * s);
+      if (sum != ORC_M) return ORC_EINVAL;
+    }
+  }
+  if (first != n_c) return ORC_EINVAL;
+  for (uint64_t c = 0; c <= n_c; c++) {
+    uint64_t o = 16ull * get32(b + off_index + 4 * c);
+    if (o < off_rec || o > off_raw) return ORC_EINVAL;
+    if (c > 0 && o < 16ull * get32(b + off_index + 4 * (c - 1))) return ORC_EINVAL;
+  }
+  return ORC_OK;
+}
+
+/* Decode chunk `c` (index within tensor `t`) into the tensor buffer `out`. */
+static int decode_one(const uint8_t* b, uint64_t size, const orc_desc* d, uint64_t c,
+                      uint8_t* out) {
+  uint64_t off_index = get64(b + 32);
+  uint64_t g = d->first_chunk + c;
+  uint64_t o0 = 16ull * get32(b + off_index + 4 * g);
+  uint64_t o1 = 16ull * get32(b + off_index + 4 * (g + 1));
+  if (o1 < o0 + 16 || o1 > size) return ORC_ECORRUPT;
+  const uint8_t* r = b + o0;
+  uint64_t per = symbols_per_chunk(d->dtype, d->chunk_bytes);
+  uint64_t s0 = c * per;
+  uint64_t len = (d->n_sym - s0) < per ? (d->n_sym - s0) : per;
+  uint32_t nw = get32(r + 0), A = get32(r + 4), nsym = get32(r + 8);
+  if (nsym != len || A != states_of(len, d->L, d->W)) return ORC_ECORRUPT;
+  if (16 + round16(4ull * A) + round16(2ull * nw) != o1 - o0) return ORC_ECORRUPT;
+  uint32_t states[64];
+  for (uint32_t l = 0; l < A; l++) states[l] = get32(r + 16 + 4 * l);
+  const uint8_t* wp = r + 16 + round16(4ull * A);
+  uint16_t* words = (uint16_t*)malloc((nw ? nw : 1) * sizeof(uint16_t));
+  uint8_t* sym = (uint8_t*)malloc(len ? len : 1);
+  if (!words || !sym) {
+    free(words);
+    free(sym);
+    return ORC_ENOMEM;
+  }
+  for (uint32_t k = 0; k < nw; k++) words[k] = (uint16_t)get16(wp + 2 * k);
+  uint32_t freq[256];
+  for (uint32_t s = 0; s < d->alphabet; s++) freq[s] = get16(b + d->freq_off + 2 * s);
+  int rc = orc_decode_stream(states, A, words, nw, len, freq, d->alphabet, d->L, d->W, sym);
+  if (rc == ORC_OK || rc == ORC_ECORRUPT) {
+    const uint8_t* raw = has_raw(d->dtype) ? b + d->raw_off + s0 : NULL;
+    put_symbols(d->dtype, sym, raw, s0, len, out);
+  }
+  free(words);
+  free(sym);
+  return rc;
+}
+
+int orc_blob_tensors(const uint8_t* b, uint64_t size, uint32_t* n_tensors) {
+  int rc = check_header(b, size);
+  if (rc) return rc;
+  *n_tensors = get32(b + 8);
+  return ORC_OK;
+}
+
+/* out_bytes, dtype and chunk count of tensor t */
+int orc_blob_tensor_info(const uint8_t* b, uint64_t size, uint32_t t, uint64_t* out_bytes,
+                         uint32_t* dtype, uint64_t* n_chunks) {
+  int rc = check_header(b, size);
+  if (rc) return rc;
+  orc_desc d;
+  rc = read_desc(b, size, t, &d);
+  if (rc) return rc;
+  *out_bytes = d.out_bytes;
+  *dtype = d.dtype;
+  *n_chunks = d.n_chunks;
+  return ORC_OK;
+}
+
+/* Decode every tensor; outs[t] must hold out_bytes of tensor t. */
+int orc_decode_blob(const uint8_t* b, uint64_t size, uint8_t* const* outs) {
+  int rc = check_header(b, size);
+  if (rc) return rc;
+  uint32_t n_t = get32(b + 8);
+  int worst = ORC_OK;
+  for (uint32_t t = 0; t < n_t; t++) {
+    orc_desc d;
+    read_desc(b, size, t, &d);
+    for (uint64_t c = 0; c < d.n_chunks; c++) {
+      rc = decode_one(b, size, &d, c, outs[t]);
+      if (rc != ORC_OK) worst = rc;
+    }
+  }
+  return worst;
+}
+
+/* Decode chunks [c0, c1) of tensor t into `out` (the whole tensor buffer). */
+int orc_decode_chunks(const uint8_t* b, uint64_t size, uint32_t t, uint64_t c0, uint64_t c1,
+                      uint8_t* out) {
+  int rc = check_header(b, size);
+  if (rc) return rc;
+  orc_desc d;
+  rc = read_desc(b, size, t, &d);
+  if (rc) return rc;
+  if (c0 > c1 || c1 > d.n_chunks) return ORC_EINVAL;
+  int worst = ORC_OK;
+  for (uint64_t c = c0; c < c1; c++) {
+    rc = decode_one(b, size, &d, c, out);
+    if (rc != ORC_OK) worst = rc;
+  }
+  return worst;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Metadata closed form (Sec. VI-F): a 4-byte offset per tile plus one      */
+/* shared codebook of 2^b entries of 4 bytes, for a rows x cols matrix cut   */
+/* into tile_r x tile_c tiles.                                               */
+
+double orc_metadata_bytes(uint64_t rows, uint64_t cols, uint64_t tile_r, uint64_t tile_c,
+                          uint32_t b) {
+  double tiles = ((double)rows / (double)tile_r) * ((double)cols / (double)tile_c);
+  return 4.0 * tiles + (double)(1ull << b) * 4.0;
+}

@@ -1,0 +1,133 @@
+"""Oracle blob round trips, edge cases, validation and the size bound.
+
+The method is lossless (Sec. I, Sec. V-B: each tile an independently decodable
+substream), so decode(encode(x)) must return x byte for byte for every bit
+pattern; the compressed payload must sit close to the order-0 entropy bound
+(Sec. VI-B reports 0.01-0.1 bits/weight; the target here is 1 % of the bound
+with table and index overhead stated separately).
+"""
+import struct
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_15789_amd import synth
+
+
+def roundtrip(tensors, **kw):
+    blob = oracle.encode(tensors, **kw)
+    outs = oracle.decode(blob)
+    for (dt, data), out in zip(tensors, outs):
+        assert np.array_equal(out, np.ascontiguousarray(data).view(np.uint8).reshape(-1)), dt
+    return blob
+
+
+def test_every_bit_pattern():
+    rng = np.random.default_rng(0)
+    allw = rng.permutation(np.arange(65536, dtype=np.uint32)).astype(np.uint16)
+    tens = [("bf16", allw), ("fp16", allw[::-1].copy()),
+            ("u8", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40))),
+            ("u4", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40)))]
+    for lanes in (1, 32, 64):
+        for cb in (256, 16384, 65536):
+            roundtrip(tens, chunk_bytes=cb, lanes=lanes)
+
+
+@pytest.mark.parametrize("dtype,esize", [("bf16", 2), ("fp16", 2), ("u8", 1), ("u4", 1)])
+@pytest.mark.parametrize("cb", [256, 16384])
+def test_edge_sizes(dtype, esize, cb):
+    rng = np.random.default_rng(1)
+    E = cb // esize                       # storage units per chunk
+    sizes = [0, 1, 2, 3, 5, 63, 64, 65, E - 1, E, E + 1, 2 * E + 7, 3 * E]
+    for n in sizes:
+        if esize == 2:
+            data = (rng.normal(0, 0.02, n).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        else:
+            data = rng.integers(0, 256, n).astype(np.uint8)
+            data[: n // 2] = 7                  # skewed
+        for lanes in (32, 64):
+            roundtrip([(dtype, data)], chunk_bytes=cb, lanes=lanes)
+
+
+def test_single_symbol_tensor_has_no_words():
+    blob = roundtrip([("u8", np.full(100_000, 42, np.uint8))], chunk_bytes=65536, lanes=64)
+    # 2 chunks: each record is 16 B header + 64 states, no words
+    n_c = struct.unpack_from("<Q", blob, 16)[0]
+    idx = struct.unpack_from("<Q", blob, 32)[0]
+    for c in range(n_c):
+        off = struct.unpack_from("<I", blob, idx + 4 * c)[0] * 16
+        nw, A, ns, _ = struct.unpack_from("<IIII", blob, off)
+        assert nw == 0
+        states = struct.unpack_from(f"<{A}I", blob, off + 16)
+        assert all(s == 65536 for s in states)
+
+
+def test_multi_tensor_layer_and_chunk_decode():
+    ts = synth.config(3, div=16)
+    pairs = [(t.dtype, t.data) for t in ts]
+    blob = roundtrip(pairs, chunk_bytes=16384, lanes=64)
+    info = oracle.tensor_info(blob)
+    for t, (dt, data) in enumerate(pairs):
+        ref = np.ascontiguousarray(data).view(np.uint8).reshape(-1)
+        nc = info[t]["n_chunks"]
+        if nc == 0:
+            continue
+        out = oracle.decode_chunks(blob, t, nc // 2, nc)
+        lo = (nc // 2) * 16384
+        assert np.array_equal(out[lo:], ref[lo:])
+        assert not out[:lo].any()
+
+
+def test_header_validation():
+    blob = bytearray(oracle.encode([("bf16", np.arange(1000, dtype=np.uint16))]))
+    for mutate in [lambda b: b.__setitem__(0, 0),                      # magic
+                   lambda b: b.__setitem__(4, 9),                      # version
+                   lambda b: struct.pack_into("<I", b, 64 + 4, 1000),  # chunk_bytes not k*256
+                   lambda b: b.__setitem__(64 + 43, 11)]:              # prob_bits
+        b = bytearray(blob)
+        mutate(b)
+        with pytest.raises(oracle.OracleError) as e:
+            oracle.decode(bytes(b))
+        assert e.value.rc == -1
+    with pytest.raises(oracle.OracleError):
+        oracle.decode(bytes(blob[:-16]))                              # truncated
+
+
+def test_corrupt_payload_is_reported():
+    data = synth.config(1, div=16)[0].data
+    blob = bytearray(oracle.encode([("bf16", data)], chunk_bytes=16384))
+    idx = struct.unpack_from("<Q", blob, 32)[0]
+    off = struct.unpack_from("<I", blob, idx + 4)[0] * 16           # chunk 1
+    nw, A = struct.unpack_from("<II", blob, off)
+    wpos = off + 16 + ((4 * A + 15) // 16) * 16 + 2 * (nw // 2)
+    blob[wpos] ^= 0x40
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.decode(bytes(blob))
+    assert e.value.rc == -3
+
+
+def _payload(blob):
+    n_c = struct.unpack_from("<Q", blob, 16)[0]
+    idx, rec, raw = struct.unpack_from("<QQQ", blob, 32)
+    states = words = 0
+    for c in range(n_c):
+        off = struct.unpack_from("<I", blob, idx + 4 * c)[0] * 16
+        nw, A = struct.unpack_from("<II", blob, off)
+        states += 4 * A
+        words += 2 * nw
+    return states + words + (len(blob) - raw)
+
+
+@pytest.mark.parametrize("cfg,div", [(1, 1), (2, 4), (3, 4), (4, 4)])
+def test_size_within_one_percent_of_entropy_bound(cfg, div):
+    ts = synth.config(cfg, div=div)
+    pairs = [(t.dtype, t.data) for t in ts]
+    bound = sum(oracle.analyze(d, a)["bound_bytes"] for d, a in pairs)
+    for lanes in (32, 64):
+        blob = oracle.encode(pairs, chunk_bytes=65536, lanes=lanes)
+        # payload = lane states + words + raw bytes; header, tables, index and
+        # record padding are the stated metadata overhead
+        assert _payload(blob) <= 1.01 * bound, (cfg, lanes)
+        if lanes == 32:
+            assert len(blob) <= 1.01 * bound, (cfg, lanes)
