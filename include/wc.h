@@ -1,0 +1,170 @@
+/*
+ * wc.h -- C ABI of libwc, the MI355X chunked rANS weight decoder.
+ *
+ * The library turns near-entropy-bound compressed weight streams back into
+ * bit-identical bf16 / fp16 / int8 / int4 tensors in GPU memory.
+ *
+ * Paper: "Approaching Shannon Bound with Lossless LLM Weight Compression"
+ * (Tan, Chen, Alonso, Wong, He).
+ *   - Sec. II-B: per-tensor empirical entropy over format-defined symbols.
+ *   - Sec. IV-A, V-B: weights cut into independently decodable ANS
+ *     substreams with a static frequency table and an offset index; the
+ *     compression is offline.
+ *   - Alg. 2, Sec. V-C-3: lane-parallel rANS decode with a table lookup of
+ *     (symbol, frequency, cumulative frequency) in on-chip memory and
+ *     coalesced renormalisation reads.
+ *   - Sec. VI-F: metadata = 4 B per tile offset + one 2^12-entry codebook.
+ *
+ * All functions return a wc_status; no C++ exception crosses the ABI.  No
+ * PyTorch or HIP type appears in a signature: device memory and streams are
+ * passed as plain pointers (`void*`), so any allocator (torch, hipMalloc)
+ * can own them.
+ *
+ * Blob format (little-endian; every offset absolute from the blob start):
+ *   header 64 B, then one 64-B descriptor per tensor, then each tensor's
+ *   u16 frequency table (16-B padded), the chunk index (u32 per chunk + 1:
+ *   record offset / 16), the chunk records and the raw bytes.  A chunk covers
+ *   `chunk_bytes` of decoded output; its record is
+ *     u32 n_words, u32 n_states (A), u32 n_symbols, u32 0,
+ *     u32 state[A] (16-B padded), u16 word[n_words] (16-B padded).
+ *   Symbol i of a chunk belongs to lane (i mod L*W) div W at step
+ *   (i div L*W)*W + i mod W, with W symbols = 4 output bytes per lane-group.
+ */
+#ifndef WC_H_
+#define WC_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  WC_OK = 0,
+  WC_EINVAL = -1,       /* bad argument, malformed or inconsistent blob */
+  WC_ENOMEM = -2,       /* host allocation failed */
+  WC_ECORRUPT = -3,     /* reserved for host-side stream checks */
+  WC_EHIP = -4,         /* a HIP runtime call or kernel launch failed */
+  WC_EUNSUPPORTED = -5  /* valid blob the GPU path does not handle (e.g. lanes) */
+} wc_status;
+
+/* Storage formats.  WC_BF16 / WC_FP16: the 16-bit word is split into a coded
+ * byte (bits 14..7) and a raw byte (bit 15, bits 6..0) -- Sec. II-B symbols
+ * "determined by the chosen numeric format".  WC_U8: one coded symbol per byte
+ * (int8 or fp8 codes).  WC_U4: two coded nibbles per byte, low nibble first. */
+typedef enum { WC_BF16 = 1, WC_FP16 = 2, WC_U8 = 3, WC_U4 = 4 } wc_dtype;
+
+/* A host tensor to analyse or encode: `nbytes` bytes of raw storage. */
+typedef struct {
+  const void* host_ptr;
+  uint64_t nbytes;
+  int32_t dtype; /* wc_dtype */
+  int32_t reserved;
+} wc_tensor;
+
+/* Encoder parameters.  chunk_bytes: decoded bytes per chunk, a multiple of
+ * 256 in [256, 1 MiB] (16, 32 or 64 KiB in practice).  lanes: interleaved
+ * rANS lanes per chunk, 1..64 (the GPU decoder takes 64).  prob_bits: must be
+ * 12 (Sec. VI-F, b = 12).  n_threads: host encoder threads, 0 = all cores. */
+typedef struct {
+  uint32_t chunk_bytes;
+  uint32_t lanes;
+  uint32_t prob_bits;
+  uint32_t n_threads;
+} wc_params;
+
+/* Per-field statistics of one tensor (Sec. II-B).  Field 0 is the coded
+ * symbol stream; field 1 (16-bit formats only) the raw byte stream.
+ * H[f] = -sum p log2 p over the field's empirical histogram, in bits per
+ * symbol.  H_joint16 is the entropy over whole 16-bit words (NaN for 8/4-bit
+ * formats).  bound_bytes = sum_f count[f] * H[f] / 8, the order-0 bound that
+ * compressed payloads are compared with; bound_bytes_raw8 charges the raw
+ * field at 8 bits, which is what a raw-stored field can reach. */
+typedef struct {
+  uint32_t n_fields;
+  uint32_t alphabet[2];
+  uint64_t count[2];
+  uint64_t hist[2][256];
+  double H[2];
+  double H_joint16;
+  double bound_bytes;
+  double bound_bytes_raw8;
+} wc_stats;
+
+/* An encoded blob held in host memory, plus its parsed description.
+ * Owned by the library; release with wc_free.  The fields below are
+ * read-only for the caller. */
+typedef struct wc_blob {
+  const uint8_t* data;       /* blob bytes (host) */
+  uint64_t size;             /* bytes */
+  uint32_t n_tensors;
+  uint32_t reserved;
+  uint64_t n_chunks;         /* over all tensors */
+  const uint64_t* out_bytes; /* [n_tensors] decoded bytes per tensor */
+  /* size breakdown (sums to size): */
+  uint64_t meta_bytes;       /* header, descriptors, tables, chunk index */
+  uint64_t record_hdr_bytes; /* 16 B per chunk record */
+  uint64_t state_bytes;      /* final lane states */
+  uint64_t word_bytes;       /* rANS words */
+  uint64_t pad_bytes;        /* 16-B alignment padding */
+  uint64_t raw_bytes;        /* raw byte region (16-bit formats), incl. padding */
+  void* priv;                /* library-internal */
+} wc_blob;
+
+/* Device-side error bits ORed into *dev_err by wc_decode. */
+#define WC_DERR_INDEX 1u  /* chunk record offset or header inconsistent */
+#define WC_DERR_STATE 2u  /* a lane did not end at the initial state 2^16 */
+#define WC_DERR_CURSOR 4u /* a chunk's word stream was not consumed exactly */
+#define WC_DERR_TABLE 8u  /* a frequency table does not sum to 2^12 */
+
+/* wc_analyze -- histogram and empirical entropy of one tensor (Sec. II-B).
+ * Host only, single pass, allocates nothing on the heap except transient
+ * 16-bit histogram storage.  Returns WC_EINVAL for a NULL argument, an
+ * unknown dtype or an odd byte count of a 16-bit format. */
+wc_status wc_analyze(const wc_tensor* t, wc_stats* out);
+
+/* wc_encode -- offline compression of n tensors into one blob (Sec. V-B):
+ * per-tensor static table normalised to 2^12, chunks of chunk_bytes of
+ * output, each coded as `lanes` interleaved rANS lanes from independent
+ * initial states, plus the chunk offset index.  Host only; threads over
+ * chunks.  On success *out receives a library-owned blob (release with
+ * wc_free).  Deterministic: the bytes depend only on the inputs and on
+ * chunk_bytes / lanes, never on n_threads.  Errors: WC_EINVAL (bad params,
+ * dtype, sizes, blob over 64 GiB), WC_ENOMEM. */
+wc_status wc_encode(const wc_tensor* t, uint32_t n, const wc_params* p, wc_blob** out);
+
+/* wc_open -- parse and validate an existing blob (e.g. one written by another
+ * encoder or read from disk).  Copies the `size` bytes at `data`; on success
+ * *out is library-owned (wc_free).  Returns WC_EINVAL for any malformed field
+ * (magic, version, sizes, offsets, table sums, index order). */
+wc_status wc_open(const void* data, uint64_t size, wc_blob** out);
+
+/* wc_decode -- GPU decode of every tensor of a blob (Alg. 2), one launch.
+ *   desc     host description from wc_encode / wc_open (supplies the grid and
+ *            per-tensor layout, so no device-to-host copy is needed);
+ *   dev_blob device copy of desc->data (desc->size bytes), caller-owned;
+ *   dev_dst  host array of n device pointers; dev_dst[i] receives
+ *            desc->out_bytes[i] decoded bytes (caller-owned; the pointer for
+ *            an empty tensor may be NULL);
+ *   n        must equal desc->n_tensors;
+ *   stream   hipStream_t to launch on (NULL = null stream);
+ *   dev_err  NULL, or a device int32 into which WC_DERR_* bits are ORed
+ *            (the caller clears it; read it after synchronising the stream).
+ * Asynchronous with respect to the host; allocates nothing.  Reads only
+ * inside [dev_blob, dev_blob + desc->size) and writes only the decoded byte
+ * ranges.  Returns WC_EINVAL (argument mismatch), WC_EUNSUPPORTED (a tensor
+ * coded with a lane count other than 64), WC_EHIP (launch failure). */
+wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_dst, uint32_t n,
+                    void* stream, int32_t* dev_err);
+
+/* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
+void wc_free(wc_blob* b);
+
+/* wc_version -- ABI version of this header (1). */
+int32_t wc_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* WC_H_ */

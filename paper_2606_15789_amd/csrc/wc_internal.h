@@ -1,0 +1,55 @@
+// wc_internal.h -- definitions shared by the host half (wc_host.cpp) and the
+// device half (wc_decode.hip) of libwc.  Not part of the public ABI.
+#pragma once
+
+#include <stdint.h>
+
+#include <vector>
+
+#include "../../include/wc.h"
+
+namespace wc {
+
+constexpr uint32_t kMagic = 0x31424357u;  // "WCB1"
+constexpr uint32_t kVersion = 1;
+constexpr uint32_t kProbBits = 12;        // b = 12 (Sec. VI-F)
+constexpr uint32_t kTableSize = 1u << kProbBits;
+constexpr uint32_t kStateLow = 1u << 16;  // lower end of the state interval
+constexpr uint32_t kHeaderBytes = 64;
+constexpr uint32_t kDescBytes = 64;
+constexpr uint32_t kMaxLanes = 64;
+
+inline bool has_raw(uint32_t dt) { return dt == WC_BF16 || dt == WC_FP16; }
+inline uint32_t alphabet_of(uint32_t dt) { return dt == WC_U4 ? 16u : 256u; }
+// W: symbols per lane-group; a lane-group is always 4 decoded bytes.
+inline uint32_t group_of(uint32_t dt) { return dt == WC_U4 ? 8u : (dt == WC_U8 ? 4u : 2u); }
+inline uint64_t symbols_of(uint32_t dt, uint64_t bytes) {
+  return dt == WC_U4 ? 2 * bytes : (dt == WC_U8 ? bytes : bytes / 2);
+}
+inline uint64_t pad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
+
+struct TensorInfo {
+  uint32_t dtype = 0, chunk_bytes = 0, lanes = 0, group = 0, alphabet = 0;
+  uint64_t n_sym = 0, out_bytes = 0, first_chunk = 0, n_chunks = 0;
+  uint64_t freq_off = 0, raw_off = 0;
+  uint64_t sym_per_chunk() const { return symbols_of(dtype, chunk_bytes); }
+};
+
+struct BlobPriv {
+  std::vector<uint8_t> bytes;
+  std::vector<uint64_t> out_bytes;
+  std::vector<TensorInfo> tensors;
+  uint64_t n_chunks = 0, index_off = 0, records_off = 0, raw_off = 0;
+};
+
+// What a wc_blob's `priv` points at: the public struct and the parsed blob.
+struct BlobHandle {
+  wc_blob pub;
+  BlobPriv priv;
+};
+
+// Validate `size` bytes at `p` and describe them.  Host-side checks of every
+// header field, table sum and index entry; WC_EINVAL on the first failure.
+wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out);
+
+}  // namespace wc

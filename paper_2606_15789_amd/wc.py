@@ -1,0 +1,219 @@
+"""Python binding of libwc (ctypes): argument marshalling only.
+
+Every step of the decode runs in libwc's HIP kernel; this module converts
+numpy / torch objects to the plain pointers and sizes of the C ABI declared in
+``include/wc.h`` and raises on any non-zero status.  There is no fallback: if
+``libwc.so`` is missing or fails to load, every call raises.
+"""
+
+from __future__ import annotations
+
+import ctypes as C
+import os
+
+import numpy as np
+
+from . import build as _build
+
+DTYPES = {"bf16": 1, "fp16": 2, "u8": 3, "u4": 4}
+STATUS = {0: "WC_OK", -1: "WC_EINVAL", -2: "WC_ENOMEM", -3: "WC_ECORRUPT", -4: "WC_EHIP",
+          -5: "WC_EUNSUPPORTED"}
+DERR = {1: "WC_DERR_INDEX", 2: "WC_DERR_STATE", 4: "WC_DERR_CURSOR", 8: "WC_DERR_TABLE"}
+
+# Every function the header declares; the library must export all of them.
+EXPORTS = ["wc_analyze", "wc_encode", "wc_open", "wc_decode", "wc_free", "wc_version"]
+
+
+class WcError(RuntimeError):
+    def __init__(self, what, rc):
+        super().__init__(f"{what} failed: {STATUS.get(rc, rc)}")
+        self.rc = rc
+
+
+class _Tensor(C.Structure):
+    _fields_ = [("host_ptr", C.c_void_p), ("nbytes", C.c_uint64), ("dtype", C.c_int32),
+                ("reserved", C.c_int32)]
+
+
+class _Params(C.Structure):
+    _fields_ = [("chunk_bytes", C.c_uint32), ("lanes", C.c_uint32), ("prob_bits", C.c_uint32),
+                ("n_threads", C.c_uint32)]
+
+
+class _Stats(C.Structure):
+    _fields_ = [("n_fields", C.c_uint32), ("alphabet", C.c_uint32 * 2),
+                ("count", C.c_uint64 * 2), ("hist", (C.c_uint64 * 256) * 2),
+                ("H", C.c_double * 2), ("H_joint16", C.c_double),
+                ("bound_bytes", C.c_double), ("bound_bytes_raw8", C.c_double)]
+
+
+class _Blob(C.Structure):
+    _fields_ = [("data", C.POINTER(C.c_uint8)), ("size", C.c_uint64),
+                ("n_tensors", C.c_uint32), ("reserved", C.c_uint32),
+                ("n_chunks", C.c_uint64), ("out_bytes", C.POINTER(C.c_uint64)),
+                ("meta_bytes", C.c_uint64), ("record_hdr_bytes", C.c_uint64),
+                ("state_bytes", C.c_uint64), ("word_bytes", C.c_uint64),
+                ("pad_bytes", C.c_uint64), ("raw_bytes", C.c_uint64),
+                ("priv", C.c_void_p)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libwc.so (building it first only if nothing is built)."""
+    global _lib
+    if _lib is None:
+        path = _build.ensure_built()
+        L = C.CDLL(path)
+        L.wc_analyze.argtypes = [C.POINTER(_Tensor), C.POINTER(_Stats)]
+        L.wc_analyze.restype = C.c_int
+        L.wc_encode.argtypes = [C.POINTER(_Tensor), C.c_uint32, C.POINTER(_Params),
+                                C.POINTER(C.POINTER(_Blob))]
+        L.wc_encode.restype = C.c_int
+        L.wc_open.argtypes = [C.c_void_p, C.c_uint64, C.POINTER(C.POINTER(_Blob))]
+        L.wc_open.restype = C.c_int
+        L.wc_decode.argtypes = [C.POINTER(_Blob), C.c_void_p, C.POINTER(C.c_void_p), C.c_uint32,
+                                C.c_void_p, C.c_void_p]
+        L.wc_decode.restype = C.c_int
+        L.wc_free.argtypes = [C.POINTER(_Blob)]
+        L.wc_free.restype = None
+        L.wc_version.restype = C.c_int32
+        _lib = L
+    return _lib
+
+
+def library_path() -> str:
+    return _build.LIB
+
+
+def _bytes(data) -> np.ndarray:
+    a = np.ascontiguousarray(data)
+    return a.view(np.uint8).reshape(-1)
+
+
+def analyze(dtype: str, data) -> dict:
+    """wc_analyze: per-field histograms and empirical entropy of one tensor."""
+    b = _bytes(data)
+    t = _Tensor(b.ctypes.data if b.size else None, b.size, DTYPES[dtype], 0)
+    st = _Stats()
+    rc = lib().wc_analyze(C.byref(t), C.byref(st))
+    if rc:
+        raise WcError("wc_analyze", rc)
+    nf = st.n_fields
+    return {"n_fields": nf, "alphabet": [st.alphabet[i] for i in range(nf)],
+            "count": [st.count[i] for i in range(nf)],
+            "hist": [np.array(st.hist[i][:st.alphabet[i]], np.uint64) for i in range(nf)],
+            "H": [st.H[i] for i in range(nf)], "H_joint16": st.H_joint16,
+            "bound_bytes": st.bound_bytes, "bound_bytes_raw8": st.bound_bytes_raw8}
+
+
+class Blob:
+    """Owner of a wc_blob (released with wc_free)."""
+
+    def __init__(self, ptr):
+        self._p = ptr
+        b = ptr.contents
+        self.size = int(b.size)
+        self.n_tensors = int(b.n_tensors)
+        self.n_chunks = int(b.n_chunks)
+        self.out_bytes = [int(b.out_bytes[i]) for i in range(self.n_tensors)]
+        self.breakdown = {k: int(getattr(b, k)) for k in
+                          ("meta_bytes", "record_hdr_bytes", "state_bytes", "word_bytes",
+                           "pad_bytes", "raw_bytes")}
+
+    @property
+    def ptr(self):
+        if self._p is None:
+            raise ValueError("blob already freed")
+        return self._p
+
+    def array(self) -> np.ndarray:
+        """Zero-copy numpy view of the host blob bytes (valid until free)."""
+        b = self.ptr.contents
+        return np.ctypeslib.as_array(b.data, shape=(self.size,))
+
+    def tobytes(self) -> bytes:
+        return C.string_at(self.ptr.contents.data, self.size)
+
+    def payload_bytes(self) -> int:
+        """Lane states + words + raw bytes (what the entropy bound is compared with)."""
+        d = self.breakdown
+        return d["state_bytes"] + d["word_bytes"] + d["raw_bytes"]
+
+    def free(self):
+        if self._p is not None:
+            lib().wc_free(self._p)
+            self._p = None
+
+    def __del__(self):
+        try:
+            self.free()
+        except Exception:
+            pass
+
+
+def encode(tensors, chunk_bytes: int = 65536, lanes: int = 64, threads: int = 0) -> Blob:
+    """wc_encode of a list of (dtype, host array) pairs."""
+    keep = [_bytes(d) for _, d in tensors]
+    arr = (_Tensor * len(tensors))()
+    for i, ((dt, _), b) in enumerate(zip(tensors, keep)):
+        arr[i] = _Tensor(b.ctypes.data if b.size else None, b.size, DTYPES[dt], 0)
+    prm = _Params(chunk_bytes, lanes, 12, threads)
+    out = C.POINTER(_Blob)()
+    rc = lib().wc_encode(arr, len(tensors), C.byref(prm), C.byref(out))
+    if rc:
+        raise WcError("wc_encode", rc)
+    return Blob(out)
+
+
+def open_blob(data) -> Blob:
+    """wc_open: validate and take a copy of blob bytes made elsewhere."""
+    b = _bytes(np.frombuffer(data, np.uint8) if isinstance(data, (bytes, bytearray)) else data)
+    out = C.POINTER(_Blob)()
+    rc = lib().wc_open(b.ctypes.data, b.size, C.byref(out))
+    if rc:
+        raise WcError("wc_open", rc)
+    return Blob(out)
+
+
+def decode(blob: Blob, dev_blob: int, dev_dst, stream: int = 0, dev_err: int = 0) -> None:
+    """wc_decode with raw device pointers (ints); asynchronous on `stream`."""
+    ptrs = (C.c_void_p * max(1, len(dev_dst)))(*[p or None for p in dev_dst])
+    rc = lib().wc_decode(blob.ptr, C.c_void_p(dev_blob), ptrs, len(dev_dst),
+                         C.c_void_p(stream or None), C.c_void_p(dev_err or None))
+    if rc:
+        raise WcError("wc_decode", rc)
+
+
+# --- torch plumbing: device memory and streams only ---------------------------
+
+def to_device(blob: Blob, device="cuda"):
+    """Copy the blob bytes into a new uint8 device tensor."""
+    import torch
+    host = torch.from_numpy(blob.array())
+    return host.to(device)
+
+
+def decode_torch(blob: Blob, dev_blob, outs=None, stream=None, err=None):
+    """Decode into uint8 device tensors (allocated if `outs` is None).
+
+    Returns the list of output tensors.  `err` (int32 device tensor of one
+    element) receives the WC_DERR_* bits; the caller reads it after syncing.
+    """
+    import torch
+    dev = dev_blob.device
+    if outs is None:
+        outs = [torch.empty(n, dtype=torch.uint8, device=dev) for n in blob.out_bytes]
+    for o, n in zip(outs, blob.out_bytes):
+        if o.numel() * o.element_size() < n or not o.is_contiguous():
+            raise ValueError("output tensor too small or not contiguous")
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    decode(blob, dev_blob.data_ptr(), [o.data_ptr() if n else 0 for o, n in zip(outs, blob.out_bytes)],
+           stream.cuda_stream, err.data_ptr() if err is not None else 0)
+    return outs
+
+
+def describe_errors(bits: int) -> list:
+    return [name for b, name in DERR.items() if bits & b]

@@ -1,0 +1,203 @@
+"""GPU parity: libwc's HIP decode against the oracle and the original bytes.
+
+Every case decodes through the C ABI (wc_decode) on cuda:0 and requires the
+output to be bit-identical to the original tensor and to the oracle's decode
+of the same blob (whole blob at small sizes; sampled chunks, decoded one by
+one by the oracle, at the full workload sizes).
+"""
+import os
+import struct
+import sys
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_15789_amd import synth, wc
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def gpu_decode(blob, dev, expect_err=0):
+    dblob = wc.to_device(blob, dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    outs = wc.decode_torch(blob, dblob, err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == expect_err, wc.describe_errors(int(err.item()))
+    return outs
+
+
+def check_exact(pairs, blob, outs, oracle_full=True):
+    ref = oracle.decode(blob.tobytes()) if oracle_full else None
+    for t, ((dt, data), out) in enumerate(zip(pairs, outs)):
+        got = out.cpu().numpy()
+        orig = np.ascontiguousarray(data).view(np.uint8).reshape(-1)
+        assert np.array_equal(got, orig), (t, dt)
+        if ref is not None:
+            assert np.array_equal(got, ref[t]), (t, dt)
+
+
+def test_every_bit_pattern(dev):
+    rng = np.random.default_rng(0)
+    allw = rng.permutation(np.arange(65536, dtype=np.uint32)).astype(np.uint16)
+    pairs = [("bf16", allw), ("fp16", allw[::-1].copy()),
+             ("u8", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40))),
+             ("u4", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40)))]
+    for cb in (256, 16384, 65536):
+        say("bit patterns, chunk", cb)
+        blob = wc.encode(pairs, chunk_bytes=cb)
+        check_exact(pairs, blob, gpu_decode(blob, dev))
+
+
+@pytest.mark.parametrize("dtype,esize", [("bf16", 2), ("fp16", 2), ("u8", 1), ("u4", 1)])
+@pytest.mark.parametrize("cb", [256, 16384, 65536])
+def test_edge_sizes(dev, dtype, esize, cb):
+    rng = np.random.default_rng(1)
+    E = cb // esize
+    sizes = [0, 1, 2, 3, 5, 63, 64, 65, 127, 128, 129, 255, 257, E - 1, E, E + 1, 2 * E + 7, 3 * E]
+    pairs = []
+    for n in sizes:
+        if esize == 2:
+            d = (rng.normal(0, 0.02, n).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        else:
+            d = rng.integers(0, 256, n).astype(np.uint8)
+            d[: n // 2] = 3
+        pairs.append((dtype, d))
+    say("edge sizes", dtype, cb)
+    blob = wc.encode(pairs, chunk_bytes=cb)
+    check_exact(pairs, blob, gpu_decode(blob, dev))
+
+
+def test_degenerate_tables(dev):
+    pairs = [("u8", np.full(200_000, 42, np.uint8)),                 # single symbol: f = 4096
+             ("u4", np.full(70_000, 0x77, np.uint8)),
+             ("bf16", np.full(50_000, 0x3F80, np.uint16)),
+             ("u8", np.concatenate([np.zeros(100_000, np.uint8), np.arange(256, dtype=np.uint8)])),
+             ("u8", np.arange(256, dtype=np.uint8).repeat(300))]     # uniform: 8 bits
+    blob = wc.encode(pairs)
+    check_exact(pairs, blob, gpu_decode(blob, dev))
+
+
+@pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16)])
+def test_workloads_scaled(dev, cfg, div):
+    say("workload", cfg, "div", div)
+    pairs = [(t.dtype, t.data) for t in synth.config(cfg, div=div)]
+    blob = wc.encode(pairs)
+    check_exact(pairs, blob, gpu_decode(blob, dev))
+
+
+def test_oracle_blob_decodes_on_gpu(dev):
+    pairs = [(t.dtype, t.data) for t in synth.config(3, div=8)]
+    blob = wc.open_blob(oracle.encode(pairs, chunk_bytes=32768))
+    check_exact(pairs, blob, gpu_decode(blob, dev), oracle_full=False)
+
+
+def test_many_tensors_split_over_launches(dev):
+    rng = np.random.default_rng(4)
+    pairs = []
+    for i in range(75):
+        dt = ["bf16", "u8", "u4", "fp16"][i % 4]
+        n = int(rng.integers(0, 70_000))
+        if dt in ("bf16", "fp16"):
+            d = (rng.normal(0, 0.05, n).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        else:
+            d = rng.integers(0, 40, n).astype(np.uint8)
+        pairs.append((dt, d))
+    blob = wc.encode(pairs, chunk_bytes=16384)
+    check_exact(pairs, blob, gpu_decode(blob, dev))
+
+
+def _sample_chunks(n, k, rng):
+    if n <= k:
+        return list(range(n))
+    pick = set([0, n - 1]) | set(int(c) for c in rng.choice(n, size=k - 2, replace=False))
+    return sorted(pick)
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
+def test_workloads_full_size(dev, cfg):
+    """Full workload sizes in the benchmark's launch configuration (one launch)."""
+    say("full workload", cfg)
+    ts = synth.config(cfg)
+    pairs = [(t.dtype, t.data) for t in ts]
+    blob = wc.encode(pairs, chunk_bytes=65536, lanes=64)
+    outs = gpu_decode(blob, dev)
+    rng = np.random.default_rng(cfg)
+    raw = blob.tobytes()
+    info = oracle.tensor_info(raw)
+    for t, ((dt, data), out) in enumerate(zip(pairs, outs)):
+        orig = torch.from_numpy(np.ascontiguousarray(data).view(np.uint8).reshape(-1)).to(dev)
+        assert torch.equal(out, orig), (cfg, t)
+        got = out.cpu().numpy()
+        for c in _sample_chunks(info[t]["n_chunks"], 12, rng):
+            ref = oracle.decode_chunks(raw, t, c, c + 1)
+            lo, hi = c * 65536, min((c + 1) * 65536, info[t]["out_bytes"])
+            assert np.array_equal(got[lo:hi], ref[lo:hi]), (cfg, t, c)
+    del outs
+    torch.cuda.empty_cache()
+
+
+def test_device_side_corruption_flags(dev):
+    """The kernel's own checks turn corrupted device bytes into error bits."""
+    pairs = [(t.dtype, t.data) for t in synth.config(1, div=8)]
+    blob = wc.encode(pairs, chunk_bytes=16384)
+    raw = blob.tobytes()
+    idx = struct.unpack_from("<Q", raw, 32)[0]
+    off1 = struct.unpack_from("<I", raw, idx + 4)[0] * 16
+    nw, A = struct.unpack_from("<II", raw, off1)
+    wpos = off1 + 16 + ((4 * A + 15) // 16) * 16 + 2 * (nw // 2)
+    foff = struct.unpack_from("<Q", raw, 64 + 48)[0]
+
+    def run(mutate):
+        d = wc.to_device(blob, dev)
+        mutate(d)
+        err = torch.zeros(1, dtype=torch.int32, device=dev)
+        wc.decode_torch(blob, d, err=err)
+        torch.cuda.synchronize()
+        return int(err.item())
+
+    def flip_word(d):
+        d[wpos] ^= 0x40
+
+    def bump_state(d):
+        d[off1 + 16 + 20] ^= 0x01
+
+    def break_index(d):
+        d[idx + 4: idx + 8] = 0
+
+    def bad_header(d):
+        d[off1: off1 + 4] = torch.tensor([0xFF, 0xFF, 0, 0], dtype=torch.uint8, device=dev)
+
+    def bad_table(d):
+        d[foff + 2] = (int(d[foff + 2].item()) + 1) & 0xFF
+
+    assert run(lambda d: None) == 0
+    assert run(flip_word) & 0x6
+    assert run(bump_state) & 0x6
+    assert run(break_index) & 0x1
+    assert run(bad_header) & 0x1
+    assert run(bad_table) & 0x8
+
+
+def test_null_error_pointer_and_stream(dev):
+    pairs = [(t.dtype, t.data) for t in synth.config(4, div=16)]
+    blob = wc.encode(pairs)
+    d = wc.to_device(blob, dev)
+    s = torch.cuda.Stream(dev)
+    with torch.cuda.stream(s):
+        outs = wc.decode_torch(blob, d, stream=s)
+    s.synchronize()
+    check_exact(pairs, blob, outs, oracle_full=False)

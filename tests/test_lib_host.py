@@ -1,0 +1,131 @@
+"""CPU tests of libwc's host half: exports, analysis, encoder, blob validation.
+
+No GPU call is made here.  The library's encoder is separate code from the
+oracle's; both follow the same format readings, so their blobs must be
+byte-identical, and the library's statistics must equal the oracle's.
+"""
+import ctypes
+import math
+import os
+import re
+import struct
+import subprocess
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_15789_amd import synth, wc
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "wc.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:wc_status|void|int32_t)\s+(wc_\w+)\s*\(", text, re.M)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert set(names) == set(wc.EXPORTS)
+    lib = wc.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    out = subprocess.run(["nm", "-D", "--defined-only", wc.library_path()], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (wc_\w+)", out))
+    assert set(names) <= exported
+    assert lib.wc_version() == 1
+
+
+@pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16)])
+@pytest.mark.parametrize("lanes", [64, 32])
+def test_blobs_identical_to_oracle(cfg, div, lanes):
+    ts = synth.config(cfg, div=div)
+    pairs = [(t.dtype, t.data) for t in ts]
+    for cb in (16384, 65536):
+        b = wc.encode(pairs, chunk_bytes=cb, lanes=lanes, threads=4)
+        assert b.tobytes() == oracle.encode(pairs, chunk_bytes=cb, lanes=lanes)
+        assert sum(b.breakdown.values()) == b.size
+        assert b.out_bytes == [t.nbytes for t in ts]
+
+
+def test_blob_identical_on_edge_sizes_and_patterns():
+    rng = np.random.default_rng(2)
+    allw = rng.permutation(np.arange(65536, dtype=np.uint32)).astype(np.uint16)
+    pairs = [("bf16", allw), ("fp16", allw[:1001]), ("u8", np.zeros(0, np.uint8)),
+             ("u4", rng.integers(0, 256, 777).astype(np.uint8)), ("u8", np.full(5, 9, np.uint8)),
+             ("bf16", allw[:1])]
+    for lanes in (1, 7, 64):
+        for cb in (256, 1024):
+            assert wc.encode(pairs, chunk_bytes=cb, lanes=lanes).tobytes() == \
+                oracle.encode(pairs, chunk_bytes=cb, lanes=lanes)
+
+
+def test_encoder_is_thread_count_invariant():
+    pairs = [(t.dtype, t.data) for t in synth.config(2, div=8)]
+    ref = wc.encode(pairs, threads=1).tobytes()
+    for th in (2, 3, 8):
+        assert wc.encode(pairs, threads=th).tobytes() == ref
+
+
+@pytest.mark.parametrize("cfg", [1, 3, 4])
+def test_analyze_matches_oracle(cfg):
+    for t in synth.config(cfg, div=8):
+        a, o = wc.analyze(t.dtype, t.data), oracle.analyze(t.dtype, t.data)
+        assert a["n_fields"] == o["n_fields"] and a["count"] == o["count"]
+        for f in range(a["n_fields"]):
+            assert np.array_equal(a["hist"][f], o["hist"][f])
+            assert a["H"][f] == pytest.approx(o["H"][f], rel=1e-12)
+        assert a["bound_bytes"] == pytest.approx(o["bound_bytes"], rel=1e-12)
+        if t.dtype in ("bf16", "fp16"):
+            assert a["H_joint16"] == pytest.approx(o["H_joint16"], rel=1e-12)
+        else:
+            assert math.isnan(a["H_joint16"])
+
+
+def test_open_accepts_oracle_blob_and_rejects_corruption():
+    pairs = [(t.dtype, t.data) for t in synth.config(3, div=16)]
+    ob = oracle.encode(pairs, chunk_bytes=16384)
+    b = wc.open_blob(ob)
+    assert b.tobytes() == ob and b.n_tensors == len(pairs)
+    bad_cases = []
+    for pos, val in [(0, 0x00), (4, 0x07), (64 + 43, 11), (64 + 40, 0)]:
+        x = bytearray(ob)
+        x[pos] = val
+        bad_cases.append(bytes(x))
+    x = bytearray(ob)                        # frequency table no longer sums to 4096
+    foff = struct.unpack_from("<Q", ob, 64 + 48)[0]
+    struct.pack_into("<H", x, foff, struct.unpack_from("<H", ob, foff)[0] + 1)
+    bad_cases.append(bytes(x))
+    x = bytearray(ob)                        # index entry out of order
+    idx = struct.unpack_from("<Q", ob, 32)[0]
+    struct.pack_into("<I", x, idx + 4, 0)
+    bad_cases.append(bytes(x))
+    bad_cases.append(ob[:-16])               # truncated
+    for bad in bad_cases:
+        with pytest.raises(wc.WcError) as e:
+            wc.open_blob(bad)
+        assert e.value.rc == -1
+
+
+def test_encode_rejects_bad_parameters():
+    d = np.zeros(100, np.uint16)
+    for kw in [dict(chunk_bytes=100), dict(chunk_bytes=1 << 21), dict(lanes=0), dict(lanes=65)]:
+        with pytest.raises(wc.WcError):
+            wc.encode([("bf16", d)], **kw)
+    with pytest.raises(wc.WcError):
+        wc.encode([("bf16", np.zeros(3, np.uint8))])   # odd byte count for a 16-bit format
+
+
+def test_decode_rejects_before_any_launch():
+    b = wc.encode([("bf16", np.zeros(1000, np.uint16))], lanes=32)
+    with pytest.raises(wc.WcError) as e:          # lane count the GPU path does not take
+        wc.decode(b, 1, [1])
+    assert e.value.rc == -5
+    b = wc.encode([("bf16", np.zeros(1000, np.uint16))])
+    with pytest.raises(wc.WcError) as e:          # tensor count mismatch
+        wc.decode(b, 1, [1, 1])
+    assert e.value.rc == -1
+    with pytest.raises(wc.WcError):
+        wc.decode(b, 0, [1])                      # no device blob
