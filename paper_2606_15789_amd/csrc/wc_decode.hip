@@ -13,9 +13,10 @@
 //    frequencies; an entry is {f | symbol << 24, slot - cum}, so the state
 //    update is a single 24-bit multiply-add (v_mad_u32_u24 ignores the symbol
 //    byte);
-//  * each wave streams its chunk's 16-bit words through a private 4 KiB LDS
-//    ring, refilled 1 KiB at a time with bounds-checked buffer loads (reads
+//  * each wave streams its chunk's 16-bit words through a private 2 KiB LDS
+//    ring, refilled 512 B at a time with bounds-checked buffer loads (reads
 //    past the chunk record return zero), one segment prefetched ahead;
+//  * the raw sign|mantissa bytes of bf16/fp16 rows are loaded 8 rows ahead;
 //  * renormalisation: ballot of lanes whose state fell below 2^16, mbcnt gives
 //    each such lane its word index (cursor + rank), the cursor advances by the
 //    ballot's popcount -- the lanes' words are consecutive in the stream;
@@ -31,8 +32,8 @@ namespace {
 
 constexpr int kWaves = 8;                  // chunks (waves) per workgroup
 constexpr int kThreads = kWaves * 64;
-constexpr int kSegWords = 512;             // refill unit: 1 KiB, 16 B per lane
-constexpr int kRingSegs = 4;
+constexpr int kSegWords = 256;             // refill unit: 512 B, 8 B per lane
+constexpr int kRingSegs = 4;               // 2 KiB word ring per wave
 constexpr int kRingWords = kRingSegs * kSegWords;
 constexpr int kMaxLaunchTensors = 32;
 
@@ -65,7 +66,7 @@ struct LaunchArgs {
   DevTensor t[kMaxLaunchTensors];
 };
 
-typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint64_t dpad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
 
@@ -141,6 +142,10 @@ __device__ __forceinline__ uint32_t assemble(const uint32_t (&s)[W], uint32_t ra
   }
 }
 
+// Raw-byte rows prefetched ahead of their use (16-bit formats): the loads of
+// rows r+1 .. r+kRawAhead are in flight while row r decodes.
+constexpr int kRawAhead = 8;
+
 template <int W>
 __device__ void decode_chunk(const LaunchArgs& a, const DevTensor& T, uint32_t chunk,
                              uint32_t lane, const uint2* __restrict__ tab,
@@ -148,7 +153,10 @@ __device__ void decode_chunk(const LaunchArgs& a, const DevTensor& T, uint32_t c
   const uint8_t* blob = reinterpret_cast<const uint8_t*>(a.blob);
   const uint32_t* index = reinterpret_cast<const uint32_t*>(blob + a.index_off);
   const uint32_t g = T.first_chunk + chunk;
-  const uint64_t o0 = 16ull * index[g], o1 = 16ull * index[g + 1];
+  // per-chunk values are wave-uniform; readfirstlane keeps them (and the
+  // buffer descriptors built from them) in scalar registers
+  const uint64_t o0 = 16ull * __builtin_amdgcn_readfirstlane(index[g]);
+  const uint64_t o1 = 16ull * __builtin_amdgcn_readfirstlane(index[g + 1]);
   const uint64_t s0 = uint64_t(chunk) * T.per;
   const uint32_t n_c = (uint32_t)min<uint64_t>(T.per, T.n_sym - s0);
   const uint32_t A = min<uint32_t>(64u, (n_c + W - 1) / W);
@@ -157,8 +165,10 @@ __device__ void decode_chunk(const LaunchArgs& a, const DevTensor& T, uint32_t c
     return;
   }
   const uint32_t* rec = reinterpret_cast<const uint32_t*>(blob + o0);
-  const uint32_t nw = rec[0], recA = rec[1], recN = rec[2];
-  const uint64_t wbase = 16 + dpad16(4ull * A);
+  const uint32_t nw = __builtin_amdgcn_readfirstlane(rec[0]);
+  const uint32_t recA = __builtin_amdgcn_readfirstlane(rec[1]);
+  const uint32_t recN = __builtin_amdgcn_readfirstlane(rec[2]);
+  const uint32_t wbase = 16u + (uint32_t)dpad16(4ull * A);
   if (recA != A || recN != n_c || wbase + dpad16(2ull * nw) != o1 - o0) {
     if (lane == 0) report(a, WC_DERR_INDEX);
     return;
@@ -167,18 +177,18 @@ __device__ void decode_chunk(const LaunchArgs& a, const DevTensor& T, uint32_t c
   uint32_t x = __builtin_amdgcn_raw_buffer_load_b32(rs, 16u + 4u * lane, 0, 0);
   if (lane >= A) x = wc::kStateLow;  // lanes without symbols keep the initial state
 
-  // --- word ring -----------------------------------------------------------
+  // --- word ring: segments of kSegWords words, kRingSegs of them per wave ---
   const uint32_t nseg = (nw + kSegWords - 1) / kSegWords;
   uint32_t next_seg = 0;  // first segment not yet in the ring
   bool pend = false;      // registers hold segment next_seg (load issued)
-  u32x4 pbuf = {0, 0, 0, 0};
+  u32x2 pbuf = {0, 0};
   uint32_t cursor = 0;
   auto issue = [&](uint32_t seg) {
-    pbuf = __builtin_amdgcn_raw_buffer_load_b128(rs, (uint32_t)wbase + seg * 1024u + lane * 16u,
-                                                 0, 0);
+    pbuf = __builtin_amdgcn_raw_buffer_load_b64(
+        rs, wbase + seg * (2u * kSegWords) + lane * 8u, 0, 0);
   };
   auto commit = [&](uint32_t seg) {
-    *reinterpret_cast<u32x4*>(ring + (seg % kRingSegs) * kSegWords + lane * 8) = pbuf;
+    *reinterpret_cast<u32x2*>(ring + (seg % kRingSegs) * kSegWords + lane * 4) = pbuf;
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
   };
@@ -197,10 +207,13 @@ __device__ void decode_chunk(const LaunchArgs& a, const DevTensor& T, uint32_t c
     }
   };
 
-  // --- raw bytes (16-bit formats) -------------------------------------------
-  const uint32_t raw_avail =
-      W == 2 ? (uint32_t)min<uint64_t>(T.per, T.raw_padded - s0) : 0u;
+  // --- raw bytes (16-bit formats): row r of lane l is the u16 at r*128 + 2l --
+  const uint32_t raw_avail = W == 2 ? (uint32_t)min<uint64_t>(T.per, T.raw_padded - s0) : 0u;
   const __amdgpu_buffer_rsrc_t rr = make_rsrc(blob + T.raw_off + s0, raw_avail);
+  auto raw_row = [&](uint32_t r) -> uint32_t {
+    // reads at or past raw_avail return 0 (buffer bounds)
+    return __builtin_amdgcn_raw_buffer_load_b16(rr, r * 128u + lane * 2u, 0, 0);
+  };
 
   // one decode step for every lane with `active` set
   auto step = [&](uint32_t& sym, bool active) {
@@ -222,22 +235,19 @@ __device__ void decode_chunk(const LaunchArgs& a, const DevTensor& T, uint32_t c
   uint32_t* out = reinterpret_cast<uint32_t*>(T.dst + uint64_t(chunk) * T.chunk_bytes);
   const uint32_t rows_full = n_c / (64u * W);
   const uint32_t rem = n_c % (64u * W);
-  for (uint32_t r = 0; r < rows_full; r++) {
+
+  // a full row: every lane decodes W symbols and stores one dword
+  auto full_row = [&](uint32_t r, uint32_t raw2) {
     refill(64u * W);
-    uint32_t raw2 = 0;
-    if constexpr (W == 2) raw2 = __builtin_amdgcn_raw_buffer_load_b16(rr, r * 128u + lane * 2u, 0, 0);
     uint32_t s[W];
 #pragma unroll
     for (int k = 0; k < W; k++) step(s[k], true);
     out[r * 64u + lane] = assemble<W>(s, raw2);
-  }
-  if (rem) {
+  };
+  // the last, partial row: lane l holds min(W, rem - l*W) symbols
+  auto tail_row = [&](uint32_t r, uint32_t raw2) {
     refill(64u * W);
-    const int v = max(0, min<int>(W, (int)rem - (int)(lane * W)));  // valid symbols of this lane
-    uint32_t raw2 = 0;
-    if constexpr (W == 2) {
-      if (v > 0) raw2 = __builtin_amdgcn_raw_buffer_load_b16(rr, rows_full * 128u + lane * 2u, 0, 0);
-    }
+    const int v = max(0, min<int>(W, (int)rem - (int)(lane * W)));
     uint32_t s[W];
 #pragma unroll
     for (int k = 0; k < W; k++) {
@@ -245,14 +255,39 @@ __device__ void decode_chunk(const LaunchArgs& a, const DevTensor& T, uint32_t c
       step(s[k], k < v);
     }
     const uint32_t word = assemble<W>(s, raw2);
-    uint8_t* ob = reinterpret_cast<uint8_t*>(out + rows_full * 64u + lane);
+    uint8_t* ob = reinterpret_cast<uint8_t*>(out + r * 64u + lane);
     const int nb = v * 4 / W;  // valid output bytes of this lane
     if (nb == 4) {
       *reinterpret_cast<uint32_t*>(ob) = word;
     } else {
       for (int b = 0; b < nb; b++) ob[b] = (uint8_t)(word >> (8 * b));
     }
+  };
+
+  if constexpr (W == 2) {
+    uint32_t q[kRawAhead];
+#pragma unroll
+    for (int j = 0; j < kRawAhead; j++) q[j] = raw_row(j);
+    uint32_t r0 = 0;
+    for (; r0 + kRawAhead <= rows_full; r0 += kRawAhead) {
+#pragma unroll
+      for (int j = 0; j < kRawAhead; j++) {
+        const uint32_t raw2 = q[j];
+        q[j] = raw_row(r0 + j + kRawAhead);
+        full_row(r0 + j, raw2);
+      }
+    }
+    // fewer than kRawAhead full rows left, then the partial row; q[j] holds row r0 + j
+#pragma unroll
+    for (int j = 0; j < kRawAhead; j++) {
+      if (r0 + j < rows_full) full_row(r0 + j, q[j]);
+      else if (r0 + j == rows_full && rem) tail_row(rows_full, q[j]);
+    }
+  } else {
+    for (uint32_t r = 0; r < rows_full; r++) full_row(r, 0u);
+    if (rem) tail_row(rows_full, 0u);
   }
+
   // --- end-of-chunk checks: every lane back at 2^16, every word consumed ----
   uint32_t bits = 0;
   if (__ballot(lane < A && x != wc::kStateLow)) bits |= WC_DERR_STATE;
@@ -273,7 +308,10 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
   const uint32_t tid = threadIdx.x;
   build_table(a, T, tab, cum, tid);
   __syncthreads();
-  const uint32_t wave = tid >> 6, lane = tid & 63;
+  // the wave index is uniform across the wave; say so, so chunk metadata and
+  // buffer descriptors live in scalar registers
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t lane = __lane_id();
   const uint32_t chunk = (wg - T.wg0) * kWaves + wave;
   if (chunk >= T.n_chunks) return;
   switch (T.kind) {
