@@ -64,7 +64,8 @@ def lib():
     """Load libwc.so (building it first only if nothing is built)."""
     global _lib
     if _lib is None:
-        path = _build.ensure_built()
+        # WC_LIB selects another build of libwc (for A/B measurements of kernel variants)
+        path = os.environ.get("WC_LIB") or _build.ensure_built()
         L = C.CDLL(path)
         L.wc_analyze.argtypes = [C.POINTER(_Tensor), C.POINTER(_Stats)]
         L.wc_analyze.restype = C.c_int
@@ -84,7 +85,7 @@ def lib():
 
 
 def library_path() -> str:
-    return _build.LIB
+    return os.environ.get("WC_LIB") or _build.LIB
 
 
 def _bytes(data) -> np.ndarray:
