@@ -15,7 +15,8 @@ HEADERS = [os.path.join(CSRC, "wc_internal.h"),
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = os.environ.get("WC_OFFLOAD_ARCH", "gfx950")
 
-FLAGS = ["-O3", "-std=c++17", "-fPIC", "-shared", f"--offload-arch={ARCH}",
+FLAGS = ["-O3", "-std=c++20", "-fno-strict-aliasing", "-fPIC", "-shared",
+         f"--offload-arch={ARCH}",
          # packed fp32 instructions stay off for every HIP object of this project
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
          "-Wall", "-lpthread"]

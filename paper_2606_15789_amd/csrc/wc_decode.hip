@@ -7,35 +7,53 @@
 // Sec. IV-A / V-B (independently decodable units located by an offset index).
 //
 // Mapping onto the MI355X:
-//  * one wave64 decodes one chunk, one rANS lane per wave lane (64 lanes);
-//  * a workgroup holds kWaves chunks of the same tensor and shares one
-//    4096-entry decode table in LDS, built from the tensor's 2^12-normalised
-//    frequencies; an entry is {f | symbol << 24, slot - cum}, so the state
-//    update is a single 24-bit multiply-add (v_mad_u32_u24 ignores the symbol
-//    byte);
-//  * each wave streams its chunk's 16-bit words through a private 2 KiB LDS
-//    ring, refilled 512 B at a time with bounds-checked buffer loads (reads
-//    past the chunk record return zero), one segment prefetched ahead;
+//  * a workgroup of kWaves wave64s decodes kWaves chunks of one tensor, one
+//    chunk per wave, one rANS lane per wave lane;
+//  * the workgroup shares one 4096-entry decode table in LDS, built from the
+//    tensor's 2^12-normalised frequencies; an entry is {f | symbol << 24,
+//    slot - cum}, so the state update is one v_mad_u32_u24 (the 24-bit multiply
+//    ignores the symbol byte);
+//  * words reach a per-chunk 2 KiB LDS ring through a fixed-rate pipeline: every
+//    two decode steps a chain commits the 128-word unit it loaded kPipe groups
+//    earlier and issues one new bounds-checked buffer load (the next unit, or a
+//    load past the record that returns zeros when the ring is full).  Two steps
+//    consume at most 128 words, so the decoder never waits for a unit, and the
+//    fixed load pattern gives the compiler exact vmcnt waits.  The ring's first
+//    64 words are mirrored past its end, so a lane's word address is one scalar
+//    base plus its rank;
+//  * renormalisation: ballot of the lanes whose state fell below 2^16, mbcnt
+//    gives each of them its rank, the cursor advances by the popcount -- the
+//    lanes' words are consecutive in the stream;
 //  * the raw sign|mantissa bytes of bf16/fp16 rows are loaded 8 rows ahead;
-//  * renormalisation: ballot of lanes whose state fell below 2^16, mbcnt gives
-//    each such lane its word index (cursor + rank), the cursor advances by the
-//    ballot's popcount -- the lanes' words are consecutive in the stream;
-//  * every W steps a lane has 4 decoded bytes (two bf16 re-interleaved with
-//    their raw sign|mantissa bytes, four int8, or eight int4) and the wave
-//    stores 256 contiguous bytes with one dword store per lane.
+//  * every W steps a lane holds 4 decoded bytes (two bf16 rebuilt from their
+//    coded and raw bytes with v_perm / v_bfi, four int8 or eight int4) and the
+//    wave stores 256 contiguous bytes, one dword per lane, as a non-temporal
+//    (streaming) store.
 // No MFMA: the work is integer table decoding, not a contraction.
 #include <hip/hip_runtime.h>
+
+#include <utility>
 
 #include "wc_internal.h"
 
 namespace {
 
-constexpr int kWaves = 8;                  // chunks (waves) per workgroup
+constexpr int kWaves = 8;                  // waves (chunks) per workgroup
 constexpr int kThreads = kWaves * 64;
-constexpr int kSegWords = 256;             // refill unit: 512 B, 8 B per lane
-constexpr int kRingSegs = 4;               // 2 KiB word ring per wave
-constexpr int kRingWords = kRingSegs * kSegWords;
+constexpr int kUnitWords = 128;            // one dword per lane
+constexpr int kRingUnits = 8;
+constexpr int kRingWords = kRingUnits * kUnitWords;  // 2 KiB
+constexpr int kMirrorWords = 64;
+constexpr int kPipe = 4;                   // groups between a unit's load and its commit
+constexpr int kRawAhead = 8;               // raw-byte rows in flight (16-bit formats)
+constexpr uint32_t kNoUnit = 0xFFFFFFFFu;
+// Offsets that can fall outside a buffer are always passed as the vector
+// offset, which the hardware range-checks against num_records; the scalar
+// offset carries only offsets that are in range by construction.
+constexpr uint32_t kFarOffset = 0x7FFFFF00u;  // past any record: loads return zeros
 constexpr int kMaxLaunchTensors = 32;
+constexpr int kStreamStore = 2;            // buffer-store cache policy: non-temporal
+static_assert(kPipe <= kRingUnits - 2, "the word pipeline needs two spare ring units");
 
 enum Kind : uint32_t { kSplit16 = 0, kByte = 1, kNibble = 2 };
 
@@ -45,6 +63,7 @@ struct DevTensor {
   uint64_t raw_off;      // raw bytes (blob offset), 16-bit formats only
   uint64_t n_sym;        // coded symbols in the tensor
   uint64_t raw_padded;   // bytes of the (16-B padded) raw region
+  uint64_t out_bytes;    // decoded bytes of the tensor
   uint32_t first_chunk;  // global index of the tensor's first chunk
   uint32_t n_chunks;
   uint32_t wg0;          // first workgroup of the tensor in this launch
@@ -65,8 +84,6 @@ struct LaunchArgs {
   uint32_t pad;
   DevTensor t[kMaxLaunchTensors];
 };
-
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
 __device__ __forceinline__ uint64_t dpad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
 
@@ -125,31 +142,47 @@ __device__ void build_table(const LaunchArgs& a, const DevTensor& T, uint2* tab,
   }
 }
 
+// Decoded bytes of a lane-group from the table entries' low words (symbol in
+// byte 3) and, for 16-bit formats, the group's two raw bytes.
 template <int W>
-__device__ __forceinline__ uint32_t assemble(const uint32_t (&s)[W], uint32_t raw2) {
+__device__ __forceinline__ uint32_t assemble(const uint32_t (&lo)[W], uint32_t raw2) {
   if constexpr (W == 2) {
-    // two 16-bit words: coded byte -> bits 14..7, raw bit 7 -> bit 15, raw bits 6..0 stay
-    uint32_t E = s[0] | (s[1] << 16);
-    uint32_t R = (raw2 & 0xFFu) | ((raw2 & 0xFF00u) << 8);
-    return (E << 7) | (R & 0x007F007Fu) | ((R & 0x00800080u) << 8);
+    // word = raw bit 7 -> bit 15 | coded byte -> bits 14..7 | raw bits 6..0
+    const uint32_t E = __builtin_amdgcn_perm(lo[1], lo[0], 0x0C070C03u);  // e0 | e1 << 16
+    const uint32_t P = __builtin_amdgcn_perm(0u, raw2, 0x01010000u);       // r0 r0 r1 r1
+    const uint32_t M = 0x807F807Fu;
+    return (P & M) | ((E << 7) & ~M);
   } else if constexpr (W == 4) {
-    return s[0] | (s[1] << 8) | (s[2] << 16) | (s[3] << 24);
+    const uint32_t b01 = __builtin_amdgcn_perm(lo[1], lo[0], 0x0C0C0703u);
+    const uint32_t b23 = __builtin_amdgcn_perm(lo[3], lo[2], 0x0C0C0703u);
+    return b01 | (b23 << 16);
   } else {
-    uint32_t v = 0;
-#pragma unroll
-    for (int k = 0; k < 8; k++) v |= s[k] << (4 * k);
-    return v;
+    // nibbles: even symbols gathered into bytes, odd ones shifted in above them
+    const uint32_t e01 = __builtin_amdgcn_perm(lo[2], lo[0], 0x0C0C0703u);
+    const uint32_t e23 = __builtin_amdgcn_perm(lo[6], lo[4], 0x0C0C0703u);
+    const uint32_t o01 = __builtin_amdgcn_perm(lo[3], lo[1], 0x0C0C0703u);
+    const uint32_t o23 = __builtin_amdgcn_perm(lo[7], lo[5], 0x0C0C0703u);
+    return (e01 | (e23 << 16)) | ((o01 | (o23 << 16)) << 4);
   }
 }
 
-// Raw-byte rows prefetched ahead of their use (16-bit formats): the loads of
-// rows r+1 .. r+kRawAhead are in flight while row r decodes.
-constexpr int kRawAhead = 8;
+// Everything a wave keeps about one chunk it decodes.
+struct Chain {
+  __amdgpu_buffer_rsrc_t rs;  // the chunk record
+  __amdgpu_buffer_rsrc_t rr;  // the chunk's raw bytes (16-bit formats)
+  __amdgpu_buffer_rsrc_t os;  // the chunk's decoded bytes
+  uint32_t* ring;             // LDS word ring (kRingWords + kMirrorWords u16)
+  uint32_t x;                 // this lane's rANS state
+  uint32_t cursor;            // words consumed
+  uint32_t issued;            // units loaded or in flight
+  uint32_t nunits, nw, A, n_c, wbase;
+  bool ok;
+};
 
-template <int W>
-__device__ void decode_chunk(const LaunchArgs& a, const DevTensor& T, uint32_t chunk,
-                             uint32_t lane, const uint2* __restrict__ tab,
-                             uint16_t* __restrict__ ring) {
+__device__ __forceinline__ Chain open_chain(const LaunchArgs& a, const DevTensor& T,
+                                            uint32_t chunk, uint32_t W, uint32_t lane,
+                                            uint32_t* ring) {
+  Chain c;
   const uint8_t* blob = reinterpret_cast<const uint8_t*>(a.blob);
   const uint32_t* index = reinterpret_cast<const uint32_t*>(blob + a.index_off);
   const uint32_t g = T.first_chunk + chunk;
@@ -158,147 +191,187 @@ __device__ void decode_chunk(const LaunchArgs& a, const DevTensor& T, uint32_t c
   const uint64_t o0 = 16ull * __builtin_amdgcn_readfirstlane(index[g]);
   const uint64_t o1 = 16ull * __builtin_amdgcn_readfirstlane(index[g + 1]);
   const uint64_t s0 = uint64_t(chunk) * T.per;
-  const uint32_t n_c = (uint32_t)min<uint64_t>(T.per, T.n_sym - s0);
-  const uint32_t A = min<uint32_t>(64u, (n_c + W - 1) / W);
-  if (o0 < a.records_off || o1 > a.records_end || o1 < o0 + 16) {
+  c.n_c = (uint32_t)min<uint64_t>(T.per, T.n_sym - s0);
+  c.A = min<uint32_t>(64u, (c.n_c + W - 1) / W);
+  c.ring = ring;
+  c.cursor = 0;
+  c.issued = 0;
+  c.nw = c.nunits = c.wbase = 0;
+  c.ok = o0 >= a.records_off && o1 <= a.records_end && o1 >= o0 + 16;
+  if (c.ok) {
+    const uint32_t* rec = reinterpret_cast<const uint32_t*>(blob + o0);
+    c.nw = __builtin_amdgcn_readfirstlane(rec[0]);
+    const uint32_t recA = __builtin_amdgcn_readfirstlane(rec[1]);
+    const uint32_t recN = __builtin_amdgcn_readfirstlane(rec[2]);
+    c.wbase = 16u + (uint32_t)dpad16(4ull * c.A);
+    c.ok = recA == c.A && recN == c.n_c && c.wbase + dpad16(2ull * c.nw) == o1 - o0;
+  }
+  c.rs = make_rsrc(blob + o0, c.ok ? (uint32_t)(o1 - o0) : 0u);
+  c.nunits = c.ok ? (c.nw + kUnitWords - 1) / kUnitWords : 0u;
+  c.x = __builtin_amdgcn_raw_buffer_load_b32(c.rs, 16u + 4u * lane, 0, 0);
+  if (lane >= c.A) c.x = wc::kStateLow;  // lanes without symbols keep the initial state
+  const uint32_t out_len =
+      (uint32_t)min<uint64_t>(T.chunk_bytes, T.out_bytes - uint64_t(chunk) * T.chunk_bytes);
+  c.os = make_rsrc(reinterpret_cast<const void*>(T.dst + uint64_t(chunk) * T.chunk_bytes),
+                   out_len);
+  const uint32_t raw_len = W == 2 ? (uint32_t)min<uint64_t>(T.per, T.raw_padded - s0) : 0u;
+  c.rr = make_rsrc(blob + T.raw_off + s0, raw_len);
+  return c;
+}
+
+// The unit load of one pipeline slot: unit `u` of the chain, or (kNoUnit) a
+// load past the record that returns zeros and touches no memory.
+__device__ __forceinline__ uint32_t load_unit(const Chain& c, uint32_t u, uint32_t lane) {
+  const uint32_t off = u == kNoUnit ? kFarOffset : c.wbase + u * (2u * kUnitWords);
+  return __builtin_amdgcn_raw_buffer_load_b32(c.rs, lane * 4u + off, 0, 0);
+}
+
+__device__ __forceinline__ void commit_unit(const Chain& c, uint32_t u, uint32_t v,
+                                            uint32_t lane) {
+  if (u == kNoUnit) return;
+  const uint32_t slot = u % kRingUnits;
+  c.ring[slot * (kUnitWords / 2) + lane] = v;
+  if (slot == 0 && lane < kMirrorWords / 2) c.ring[kRingWords / 2 + lane] = v;
+}
+
+// Next unit to issue, or kNoUnit when the stream is done or the ring is full.
+__device__ __forceinline__ uint32_t next_unit(Chain& c) {
+  if (c.issued < c.nunits && c.issued < c.cursor / kUnitWords + kRingUnits) return c.issued++;
+  return kNoUnit;
+}
+
+// One decode step for the lanes with `active` set; returns the table entry's
+// low word (symbol in byte 3).  Branch-free: every lane reads a word and v_perm
+// either shifts it in or keeps the state, so a whole group of steps stays one
+// basic block and the compiler can overlap one step's LDS reads with the
+// previous step's arithmetic.
+template <bool kAll>
+__device__ __forceinline__ uint32_t step(Chain& c, const uint2* __restrict__ tab, bool active) {
+  const uint2 e = tab[c.x & (wc::kTableSize - 1)];
+  uint32_t xn = __umul24(e.x, c.x >> wc::kProbBits) + e.y;
+  uint32_t lo = e.x;
+  if (!kAll) {
+    xn = active ? xn : c.x;
+    lo = active ? lo : 0u;
+  }
+  const bool need = (kAll || active) && xn < wc::kStateLow;
+  const uint64_t m = __ballot(need);
+  const uint32_t rank =
+      __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+  const uint16_t* words = reinterpret_cast<const uint16_t*>(c.ring);
+  const uint32_t w = words[(c.cursor & (kRingWords - 1)) + rank];
+  // bytes {w0, w1, x0, x1} = (x << 16) | w, or {x0, x1, x2, x3} = x
+  c.x = __builtin_amdgcn_perm(xn, w, need ? 0x05040100u : 0x07060504u);
+  c.cursor += (uint32_t)__popcll(m);
+  return lo;
+}
+
+// Decode one chunk with the whole wave, one rANS lane per wave lane.
+template <int W>
+__device__ __forceinline__ void decode_chunk(const LaunchArgs& a, const DevTensor& T,
+                                             uint32_t chunk, uint32_t lane,
+                                             const uint2* __restrict__ tab, uint32_t* ring) {
+  constexpr int kGroupsPerRow = W / 2;        // groups of two steps in a row
+  constexpr int kUnroll = W == 2 ? kRawAhead : kPipe;  // groups per loop body
+  static_assert(kUnroll % kPipe == 0 && kUnroll % kGroupsPerRow == 0, "pipeline shape");
+
+  Chain c = open_chain(a, T, chunk, W, lane, ring);
+  if (!c.ok) {
     if (lane == 0) report(a, WC_DERR_INDEX);
     return;
   }
-  const uint32_t* rec = reinterpret_cast<const uint32_t*>(blob + o0);
-  const uint32_t nw = __builtin_amdgcn_readfirstlane(rec[0]);
-  const uint32_t recA = __builtin_amdgcn_readfirstlane(rec[1]);
-  const uint32_t recN = __builtin_amdgcn_readfirstlane(rec[2]);
-  const uint32_t wbase = 16u + (uint32_t)dpad16(4ull * A);
-  if (recA != A || recN != n_c || wbase + dpad16(2ull * nw) != o1 - o0) {
-    if (lane == 0) report(a, WC_DERR_INDEX);
-    return;
-  }
-  const __amdgpu_buffer_rsrc_t rs = make_rsrc(blob + o0, (uint32_t)(o1 - o0));
-  uint32_t x = __builtin_amdgcn_raw_buffer_load_b32(rs, 16u + 4u * lane, 0, 0);
-  if (lane >= A) x = wc::kStateLow;  // lanes without symbols keep the initial state
-
-  // --- word ring: segments of kSegWords words, kRingSegs of them per wave ---
-  const uint32_t nseg = (nw + kSegWords - 1) / kSegWords;
-  uint32_t next_seg = 0;  // first segment not yet in the ring
-  bool pend = false;      // registers hold segment next_seg (load issued)
-  u32x2 pbuf = {0, 0};
-  uint32_t cursor = 0;
-  auto issue = [&](uint32_t seg) {
-    pbuf = __builtin_amdgcn_raw_buffer_load_b64(
-        rs, wbase + seg * (2u * kSegWords) + lane * 8u, 0, 0);
-  };
-  auto commit = [&](uint32_t seg) {
-    *reinterpret_cast<u32x2*>(ring + (seg % kRingSegs) * kSegWords + lane * 4) = pbuf;
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-  };
-  // make words [cursor, cursor + ahead) resident, then start the next segment
-  auto refill = [&](uint32_t ahead) {
-    uint32_t need = min((cursor + ahead + kSegWords - 1) / kSegWords, nseg);
-    while (next_seg < need) {
-      if (!pend) issue(next_seg);
-      commit(next_seg);
-      next_seg++;
-      pend = false;
-    }
-    if (!pend && next_seg < nseg) {
-      issue(next_seg);
-      pend = true;
-    }
-  };
-
-  // --- raw bytes (16-bit formats): row r of lane l is the u16 at r*128 + 2l --
-  const uint32_t raw_avail = W == 2 ? (uint32_t)min<uint64_t>(T.per, T.raw_padded - s0) : 0u;
-  const __amdgpu_buffer_rsrc_t rr = make_rsrc(blob + T.raw_off + s0, raw_avail);
-  auto raw_row = [&](uint32_t r) -> uint32_t {
-    // reads at or past raw_avail return 0 (buffer bounds)
-    return __builtin_amdgcn_raw_buffer_load_b16(rr, r * 128u + lane * 2u, 0, 0);
-  };
-
-  // one decode step for every lane with `active` set
-  auto step = [&](uint32_t& sym, bool active) {
-    if (active) {
-      uint2 e = tab[x & (wc::kTableSize - 1)];
-      sym = e.x >> 24;
-      x = __umul24(e.x, x >> wc::kProbBits) + e.y;
-    }
-    bool need = active && x < wc::kStateLow;
-    uint64_t m = __ballot(need);
-    if (need) {
-      uint32_t p = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
-                                             __builtin_amdgcn_mbcnt_lo((uint32_t)m, cursor));
-      x = (x << 16) | ring[p & (kRingWords - 1)];
-    }
-    cursor += (uint32_t)__popcll(m);
-  };
-
-  uint32_t* out = reinterpret_cast<uint32_t*>(T.dst + uint64_t(chunk) * T.chunk_bytes);
+  const uint32_t n_c = c.n_c;
   const uint32_t rows_full = n_c / (64u * W);
   const uint32_t rem = n_c % (64u * W);
+  const uint32_t rows = rows_full + (rem ? 1u : 0u);
+  const uint32_t groups = rows * kGroupsPerRow;
 
-  // a full row: every lane decodes W symbols and stores one dword
-  auto full_row = [&](uint32_t r, uint32_t raw2) {
-    refill(64u * W);
-    uint32_t s[W];
+  // prologue: unit 0 committed now, then kPipe units in flight
+  uint32_t pu[kPipe], pv[kPipe];
+  {
+    const uint32_t u0 = next_unit(c);
+    commit_unit(c, u0, load_unit(c, u0, lane), lane);
+  }
 #pragma unroll
-    for (int k = 0; k < W; k++) step(s[k], true);
-    out[r * 64u + lane] = assemble<W>(s, raw2);
-  };
-  // the last, partial row: lane l holds min(W, rem - l*W) symbols
-  auto tail_row = [&](uint32_t r, uint32_t raw2) {
-    refill(64u * W);
-    const int v = max(0, min<int>(W, (int)rem - (int)(lane * W)));
-    uint32_t s[W];
-#pragma unroll
-    for (int k = 0; k < W; k++) {
-      s[k] = 0;
-      step(s[k], k < v);
-    }
-    const uint32_t word = assemble<W>(s, raw2);
-    uint8_t* ob = reinterpret_cast<uint8_t*>(out + r * 64u + lane);
-    const int nb = v * 4 / W;  // valid output bytes of this lane
-    if (nb == 4) {
-      *reinterpret_cast<uint32_t*>(ob) = word;
-    } else {
-      for (int b = 0; b < nb; b++) ob[b] = (uint8_t)(word >> (8 * b));
-    }
-  };
+  for (int j = 0; j < kPipe; j++) {
+    pu[j] = next_unit(c);
+    pv[j] = load_unit(c, pu[j], lane);
+  }
+  __builtin_amdgcn_wave_barrier();
 
+  // raw bytes of the first kRawAhead rows (16-bit formats)
+  uint32_t rq[W == 2 ? kRawAhead : 1];
   if constexpr (W == 2) {
-    uint32_t q[kRawAhead];
 #pragma unroll
-    for (int j = 0; j < kRawAhead; j++) q[j] = raw_row(j);
-    uint32_t r0 = 0;
-    for (; r0 + kRawAhead <= rows_full; r0 += kRawAhead) {
+    for (int j = 0; j < kRawAhead; j++)
+      rq[j] = __builtin_amdgcn_raw_buffer_load_b16(c.rr, j * 128u + lane * 2u, 0, 0);
+  }
+  uint32_t lo[W];
+
+  // group g of the chunk, j = g mod kUnroll (static)
+  auto group = [&](uint32_t g, auto jc, auto tailc) {
+    constexpr int j = decltype(jc)::value;
+    constexpr bool kTail = decltype(tailc)::value;
+    constexpr int slot = j % kPipe;
+    constexpr int k0 = (j % kGroupsPerRow) * 2;  // first step of this group in its row
+    commit_unit(c, pu[slot], pv[slot], lane);
+    pu[slot] = next_unit(c);
+    pv[slot] = load_unit(c, pu[slot], lane);
+    __builtin_amdgcn_wave_barrier();
+    const int nv = kTail ? max(0, min<int>(W, (int)rem - (int)(lane * W))) : W;
 #pragma unroll
-      for (int j = 0; j < kRawAhead; j++) {
-        const uint32_t raw2 = q[j];
-        q[j] = raw_row(r0 + j + kRawAhead);
-        full_row(r0 + j, raw2);
+    for (int k = k0; k < k0 + 2; k++) lo[k] = step<!kTail>(c, tab, k < nv);
+    if constexpr (j % kGroupsPerRow == kGroupsPerRow - 1) {
+      const uint32_t r = g / kGroupsPerRow;
+      uint32_t raw2 = 0;
+      if constexpr (W == 2) {
+        raw2 = rq[j % kRawAhead];
+        rq[j % kRawAhead] =
+            __builtin_amdgcn_raw_buffer_load_b16(c.rr, (r + kRawAhead) * 128u + lane * 2u, 0, 0);
+      }
+      const uint32_t word = assemble<W>(lo, raw2);
+      if (!kTail) {
+        __builtin_amdgcn_raw_buffer_store_b32(word, c.os, lane * 4u, r * 256u, kStreamStore);
+      } else {
+        const int nb = nv * 4 / W;  // valid output bytes of this lane
+        if (nb == 4) {
+          __builtin_amdgcn_raw_buffer_store_b32(word, c.os, lane * 4u, r * 256u, kStreamStore);
+        } else {
+          for (int b = 0; b < nb; b++)
+            __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(word >> (8 * b)), c.os, lane * 4u + b,
+                                                 r * 256u, 0);
+        }
       }
     }
-    // fewer than kRawAhead full rows left, then the partial row; q[j] holds row r0 + j
-#pragma unroll
-    for (int j = 0; j < kRawAhead; j++) {
-      if (r0 + j < rows_full) full_row(r0 + j, q[j]);
-      else if (r0 + j == rows_full && rem) tail_row(rows_full, q[j]);
-    }
-  } else {
-    for (uint32_t r = 0; r < rows_full; r++) full_row(r, 0u);
-    if (rem) tail_row(rows_full, 0u);
+  };
+
+  const uint32_t groups_full = rows_full * kGroupsPerRow;
+  uint32_t g0 = 0;
+  for (; g0 + kUnroll <= groups_full; g0 += kUnroll) {
+    [&]<int... J>(std::integer_sequence<int, J...>) {
+      (group(g0 + J, std::integral_constant<int, J>{}, std::false_type{}), ...);
+    }(std::make_integer_sequence<int, kUnroll>{});
   }
+  // the remaining full rows and the partial last row
+  [&]<int... J>(std::integer_sequence<int, J...>) {
+    ((g0 + J < groups_full
+          ? group(g0 + J, std::integral_constant<int, J>{}, std::false_type{})
+          : (g0 + J < groups ? group(g0 + J, std::integral_constant<int, J>{}, std::true_type{})
+                             : void())),
+     ...);
+  }(std::make_integer_sequence<int, kUnroll>{});
 
   // --- end-of-chunk checks: every lane back at 2^16, every word consumed ----
   uint32_t bits = 0;
-  if (__ballot(lane < A && x != wc::kStateLow)) bits |= WC_DERR_STATE;
-  if (cursor != nw) bits |= WC_DERR_CURSOR;
+  if (__ballot(lane < c.A && c.x != wc::kStateLow)) bits |= WC_DERR_STATE;
+  if (c.cursor != c.nw) bits |= WC_DERR_CURSOR;
   if (lane == 0) report(a, bits);
 }
 
 __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
   __shared__ uint2 tab[wc::kTableSize];
   __shared__ uint32_t cum[260];
-  __shared__ __attribute__((aligned(16))) uint16_t ring[kWaves][kRingWords];
+  __shared__ uint32_t ring[kWaves][(kRingWords + kMirrorWords) / 2];
 
   const uint32_t wg = blockIdx.x;
   uint32_t ti = 0;
@@ -351,6 +424,7 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
       D.freq_off = T.freq_off;
       D.raw_off = T.raw_off;
       D.n_sym = T.n_sym;
+      D.out_bytes = T.out_bytes;
       D.raw_padded = wc::has_raw(T.dtype) ? wc::pad16(T.n_sym) : 0;
       D.first_chunk = (uint32_t)T.first_chunk;
       D.n_chunks = (uint32_t)T.n_chunks;
