@@ -1,22 +1,33 @@
 #!/usr/bin/env python3
-"""Sustained decode throughput of the chunked rANS weight decoder on one MI355X.
+"""Decode throughput of the chunked rANS weight decoder on one MI355X.
 
-Workload: Llama-3-70B-shaped decoder layers in bf16 (q/o 8192x8192, k/v
-1024x8192, gate/up 28672x8192, down 8192x28672; Normal(0, 0.015) with 0.1 %
-outlier input channels x20), 1.711 GB decoded per layer.  `--layers` distinct
-layer seeds are drawn on the GPU, encoded on the host with libwc's threaded
-encoder (64 KiB chunks, 64 lanes) and kept resident in HBM; every layer is
-decoded once and checked byte-exact against its original before timing.
+Workloads (`--workload`, seeded synthetic tensors with the shapes and
+statistics of the paper's models):
+  llama3-70b-layer-bf16 (default)  q/o 8192x8192, k/v 1024x8192, gate/up
+      28672x8192, down 8192x28672, Normal(0, 0.015) with 0.1 % outlier input
+      channels x20; 1.711 GB decoded per layer; `--layers` distinct layer
+      seeds are drawn on the GPU and kept resident;
+  bf16-matrix-4096        one 4096x4096 bf16 matrix, Normal(0, 0.02);
+  llama3-8b-layer-bf16    one Llama-3-8B layer in bf16 (outlier channels);
+  llama3-8b-layer-int4    the same shapes as int4 codes (group 128) + fp16
+      scales + bf16 norms;
+  llama3-8b-layer-int8    the same shapes as per-row int8 (Student-t weights)
+      + fp16 scales + bf16 norms.
+Blobs are encoded on the host with libwc's threaded encoder (64 KiB chunks,
+64 lanes by default) and kept resident in HBM; every resident blob is decoded
+once and checked byte-exact against its original before timing.
 
-A step is one wc_decode launch that decodes every tensor of one layer from its
-resident blob into a resident output buffer (two output sets are ping-ponged);
-step k decodes layer k mod --layers.  Each blob (~1.13 GB) is several times the
-256 MB Infinity Cache, so every step streams from HBM.  The JSON line reports
+A step is one wc_decode launch that decodes every tensor of one blob into a
+resident output set.  The 70B workload rotates over its layer seeds (each blob
+~1.13 GB, several times the 256 MB Infinity Cache); the smaller workloads
+rotate over enough resident copies of their blob and output set (at least
+1 GiB together) that every step streams from HBM.  The JSON line reports
 decoded GB/s over the K timed steps, the roofline of the decode kernel
 (algorithmic bytes = blob bytes read + decoded bytes written, per launch, over
 its mean event-timed duration, against 8 TB/s), the compression ratio next to
-the order-0 entropy bound, a device-to-device copy ceiling, and the CPU
-oracle's single-thread decode rate on the host cores.
+the order-0 entropy bound, a device-to-device copy ceiling, the same K steps
+issued alternately on two streams (so one launch's tail overlaps the next
+launch's start), and the CPU oracle's single-thread decode rate on the host.
 """
 
 from __future__ import annotations
@@ -33,6 +44,11 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decompressed GB/s on one MI355X (% of HBM roofline); ratio vs Shannon bound"
 HBM_PEAK_GBPS = 8000.0
+WORKLOAD_DEFAULT = "llama3-70b-layer-bf16"
+# workload name -> seeded recipe number in paper_2606_15789_amd.synth.config
+WORKLOADS = {WORKLOAD_DEFAULT: 5, "bf16-matrix-4096": 1, "llama3-8b-layer-bf16": 2,
+             "llama3-8b-layer-int4": 3, "llama3-8b-layer-int8": 4}
+ROTATE_BYTES = 1 << 30   # resident bytes the small workloads rotate over
 
 # HBM bytes per launch of the 70B-layer decode from rocprofv3 --pmc FETCH_SIZE and
 # WRITE_SIZE runs, each scaled by the same counter on a 470 MB device copy (FETCH_SIZE
@@ -57,8 +73,12 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def oracle_baseline(blob, host_tensors):
-    """Single-thread oracle decode of one whole layer blob on one host core."""
+def oracle_baseline(blob, host_tensors, workload: str, min_seconds: float = 3.0):
+    """Single-thread oracle decode of one whole blob on one host core.
+
+    The blob is decoded whole, repeatedly until `min_seconds` have elapsed
+    (at least once), timed around the decode calls only.
+    """
     import numpy as np
 
     import oracle
@@ -68,32 +88,55 @@ def oracle_baseline(blob, host_tensors):
     old = os.sched_getaffinity(0)
     core = min(old)
     os.sched_setaffinity(0, {core})
+    reps, dt = 0, 0.0
     try:
-        t0 = time.perf_counter()
-        for t, i in enumerate(info):
-            oracle.decode_chunks(raw, t, 0, i["n_chunks"], out=outs[t])
-        dt = time.perf_counter() - t0
+        while reps == 0 or dt < min_seconds:
+            t0 = time.perf_counter()
+            for t, i in enumerate(info):
+                oracle.decode_chunks(raw, t, 0, i["n_chunks"], out=outs[t])
+            dt += time.perf_counter() - t0
+            reps += 1
     finally:
         os.sched_setaffinity(0, old)
     for o, h in zip(outs, host_tensors):
-        if not np.array_equal(o, h):
-            raise RuntimeError("oracle baseline decoded a different layer")
+        if not np.array_equal(o, np.ascontiguousarray(h).view(np.uint8).reshape(-1)):
+            raise RuntimeError("oracle baseline decoded a different blob")
     n_out = sum(i["out_bytes"] for i in info)
-    return {"value": round(n_out / dt / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"layer 0 of the 70B bf16 workload: all {sum(i['n_chunks'] for i in info)} "
-                      f"chunks, {n_out} decoded bytes, single thread pinned to core {core}",
+    what = "layer 0 of the 70B bf16 workload" if workload == WORKLOAD_DEFAULT else workload
+    return {"value": round(reps * n_out / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"{what}: all {sum(i['n_chunks'] for i in info)} chunks, {n_out} decoded "
+                      f"bytes, decoded {reps}x, single thread pinned to core {core}",
             "seconds": round(dt, 3), "cpu": cpu_model(), "host_cpus": os.cpu_count()}
 
 
-def counted_traffic(chunk_bytes: int, lanes: int):
+def counted_traffic(workload: str, chunk_bytes: int, lanes: int):
     import hashlib
     src = os.path.join(ROOT, "paper_2606_15789_amd", "csrc", "wc_decode.hip")
     with open(src, "rb") as fh:
         sha = hashlib.sha256(fh.read()).hexdigest()[:16]
     c = COUNTED_TRAFFIC
-    if sha != c["kernel_sha256"] or chunk_bytes != c["chunk_bytes"] or lanes != c["lanes"]:
+    if (workload != WORKLOAD_DEFAULT or sha != c["kernel_sha256"]
+            or chunk_bytes != c["chunk_bytes"] or lanes != c["lanes"]):
         return None
     return c["fetch_bytes"] + c["write_bytes"]
+
+
+def compression_stats(blob, typed_host):
+    """Compressed size against the field-wise order-0 bound of every tensor."""
+    from paper_2606_15789_amd import wc
+    stats = [wc.analyze(dt, h) for dt, h in typed_host]
+    bound = sum(st["bound_bytes"] for st in stats)
+    raw8 = sum(st["bound_bytes_raw8"] for st in stats)
+    out_b = sum(blob.out_bytes)
+    return {"ratio": round(out_b / blob.size, 5),
+            "bound_ratio": round(out_b / bound, 5),
+            "payload_over_bound_pct": round(100 * (blob.payload_bytes() / bound - 1), 4),
+            "total_over_bound_pct": round(100 * (blob.size / bound - 1), 4),
+            "over_raw8_bound_pct": round(100 * (blob.payload_bytes() / raw8 - 1), 4),
+            "metadata_bytes": blob.breakdown["meta_bytes"]
+            + blob.breakdown["record_hdr_bytes"] + blob.breakdown["pad_bytes"],
+            "breakdown": blob.breakdown}
 
 
 def main() -> int:
@@ -101,11 +144,14 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=80)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--layers", type=int, default=8, help="distinct layer seeds resident in HBM")
+    ap.add_argument("--workload", choices=list(WORKLOADS), default=WORKLOAD_DEFAULT)
+    ap.add_argument("--layers", type=int, default=8,
+                    help="distinct 70B layer seeds resident in HBM")
     ap.add_argument("--chunk-bytes", type=int, default=65536)
     ap.add_argument("--lanes", type=int, default=64)
     ap.add_argument("--threads", type=int, default=int(os.environ.get("OMP_NUM_THREADS", "16")))
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-two-stream", action="store_true")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -123,90 +169,112 @@ def main() -> int:
         return 1
     dev = torch.device("cuda:0")
     wc.lib()
-    NL = max(1, args.layers)
+    cfg = WORKLOADS[args.workload]
+    big = cfg == 5
 
     # --- setup: draw, encode, upload, verify ---------------------------------
-    blobs, dblobs = [], []
-    layer_out = None
-    sets = None
+    # The 70B workload keeps `--layers` distinct layer blobs; the others keep
+    # copies of one blob.  Either way `n_res` blobs rotate through the steps.
     err = torch.zeros(1, dtype=torch.int32, device=dev)
+    blobs, dblobs, sets = [], [], []
     keep_orig = {}
-    last_layers = {(args.warmup + args.steps - 1) % NL, (args.warmup + args.steps - 2) % NL}
-    comp = None
-    cpu = None
+    comp = cpu = None
     t_setup = time.perf_counter()
-    for layer in range(NL):
-        t0 = time.perf_counter()
-        tens = synth.config_torch_device(5, layer, device="cuda")
-        host = [t.cpu().numpy() for _, t, _ in tens]
-        blob = wc.encode([("bf16", h) for h in host], chunk_bytes=args.chunk_bytes,
-                         lanes=args.lanes, threads=args.threads)
-        dblob = wc.to_device(blob, dev)
-        if sets is None:
-            layer_out = blob.out_bytes
-            sets = [[torch.empty(n, dtype=torch.uint8, device=dev) for n in layer_out]
-                    for _ in range(2)]
-        wc.decode_torch(blob, dblob, outs=sets[0], err=err)
+
+    def check(blob, dblob, outs, originals, what):
+        wc.decode_torch(blob, dblob, outs=outs, err=err)
         torch.cuda.synchronize()
         if int(err.item()) != 0:
-            raise RuntimeError(f"layer {layer}: device errors {wc.describe_errors(int(err.item()))}")
-        for (_, orig, _), out in zip(tens, sets[0]):
-            if not torch.equal(orig, out):
-                raise RuntimeError(f"layer {layer}: decoded bytes differ from the original")
-        if layer in last_layers:
-            keep_orig[layer] = [o for _, o, _ in tens]
-        if layer == 0:
-            stats = [wc.analyze("bf16", h) for h in host]
-            bound = sum(st["bound_bytes"] for st in stats)
-            raw8 = sum(st["bound_bytes_raw8"] for st in stats)
-            out_b = sum(blob.out_bytes)
-            comp = {"ratio": round(out_b / blob.size, 5),
-                    "bound_ratio": round(out_b / bound, 5),
-                    "payload_over_bound_pct": round(100 * (blob.payload_bytes() / bound - 1), 4),
-                    "total_over_bound_pct": round(100 * (blob.size / bound - 1), 4),
-                    "over_raw8_bound_pct": round(100 * (blob.payload_bytes() / raw8 - 1), 4),
-                    "metadata_bytes": blob.breakdown["meta_bytes"]
-                    + blob.breakdown["record_hdr_bytes"] + blob.breakdown["pad_bytes"],
-                    "breakdown": blob.breakdown}
-            if not args.no_cpu_baseline:
-                log("cpu baseline: oracle decode of layer 0 on one core ...")
-                cpu = oracle_baseline(blob, host)
-                log(f"cpu baseline: {cpu['value']} GB/s in {cpu['seconds']} s")
-        del tens, host
-        blobs.append(blob)
-        dblobs.append(dblob)
-        log(f"layer {layer + 1}/{NL}: {blob.size / 1e9:.3f} GB compressed, "
-            f"{sum(blob.out_bytes) / 1e9:.3f} GB decoded, verified, "
-            f"{time.perf_counter() - t0:.1f} s")
+            raise RuntimeError(f"{what}: device errors {wc.describe_errors(int(err.item()))}")
+        for orig, out in zip(originals, outs):
+            if not torch.equal(orig.reshape(-1).view(torch.uint8), out[:orig.numel() * orig.element_size()]):
+                raise RuntimeError(f"{what}: decoded bytes differ from the original")
+
+    def first_blob(typed_host):
+        nonlocal comp, cpu
+        comp = compression_stats(blobs[0], typed_host)
+        if not args.no_cpu_baseline:
+            log("cpu baseline: oracle decode on one core ...")
+            cpu = oracle_baseline(blobs[0], [h for _, h in typed_host], args.workload)
+            log(f"cpu baseline: {cpu['value']} GB/s in {cpu['seconds']} s")
+
+    if big:
+        n_res = max(1, args.layers)
+        last = {(args.warmup + args.steps - j) % n_res for j in (1, 2)}
+        for layer in range(n_res):
+            t0 = time.perf_counter()
+            tens = synth.config_torch_device(5, layer, device="cuda")
+            host = [("bf16", t.cpu().numpy()) for _, t, _ in tens]
+            blob = wc.encode(host, chunk_bytes=args.chunk_bytes, lanes=args.lanes,
+                             threads=args.threads)
+            blobs.append(blob)
+            dblobs.append(wc.to_device(blob, dev))
+            if len(sets) == 0:
+                sets = [[torch.empty(n, dtype=torch.uint8, device=dev) for n in blob.out_bytes]
+                        for _ in range(2)]
+            check(blob, dblobs[-1], sets[0], [o for _, o, _ in tens], f"layer {layer}")
+            if layer in last:
+                keep_orig[layer] = [o for _, o, _ in tens]
+            if layer == 0:
+                first_blob(host)
+            del tens, host
+            log(f"layer {layer + 1}/{n_res}: {blob.size / 1e9:.3f} GB compressed, "
+                f"{sum(blob.out_bytes) / 1e9:.3f} GB decoded, verified, "
+                f"{time.perf_counter() - t0:.1f} s")
+        out_sets = lambda k: sets[k % 2]          # noqa: E731
+        origs = lambda k: keep_orig[k % n_res]    # noqa: E731
+    else:
+        tens = synth.config(cfg)
+        host = [(t.dtype, t.data) for t in tens]
+        blob = wc.encode(host, chunk_bytes=args.chunk_bytes, lanes=args.lanes,
+                         threads=args.threads)
+        per = blob.size + sum(blob.out_bytes)
+        n_res = max(2, -(-ROTATE_BYTES // per))
+        dev_orig = [torch.from_numpy(np.ascontiguousarray(h).view(np.uint8).reshape(-1)).to(dev)
+                    for _, h in host]
+        for r in range(n_res):
+            blobs.append(blob)
+            dblobs.append(wc.to_device(blob, dev))
+            sets.append([torch.empty(n, dtype=torch.uint8, device=dev) for n in blob.out_bytes])
+            check(blob, dblobs[-1], sets[-1], dev_orig, f"copy {r}")
+        first_blob(host)
+        log(f"{args.workload}: {blob.size / 1e6:.1f} MB compressed, "
+            f"{sum(blob.out_bytes) / 1e6:.1f} MB decoded, {n_res} resident copies, verified")
+        out_sets = lambda k: sets[k % n_res]      # noqa: E731
+        origs = lambda k: dev_orig                # noqa: E731
+        del tens
     torch.cuda.empty_cache()
     setup_s = time.perf_counter() - t_setup
+    out_per_step = sum(blobs[0].out_bytes)
+    in_per_step = float(np.mean([b.size for b in blobs]))
 
-    # --- device-to-device copy ceiling ----------------------------------------
-    src = sets[0][4]
-    dst = sets[1][4]
+    # --- device-to-device copy ceiling (256 MB or the largest output) ----------
+    big_out = max(range(len(blobs[0].out_bytes)), key=lambda i: blobs[0].out_bytes[i])
+    src = sets[0][big_out]
+    dst = sets[1][big_out]
+    reps = max(10, int(4e9 // max(1, src.numel())))
     for _ in range(3):
         dst.copy_(src)
     torch.cuda.synchronize()
     c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     c0.record()
-    for _ in range(10):
+    for _ in range(reps):
         dst.copy_(src)
     c1.record()
     torch.cuda.synchronize()
-    copy_gbps = 10 * 2 * src.numel() / (c0.elapsed_time(c1) / 1e3) / 1e9
+    copy_gbps = reps * 2 * src.numel() / (c0.elapsed_time(c1) / 1e3) / 1e9
 
     # --- timed decode ---------------------------------------------------------
     stream = torch.cuda.current_stream(dev)
     err.zero_()
 
-    def step(k):
-        layer = k % NL
-        outs = sets[k % 2]
-        wc.decode(blobs[layer], dblobs[layer].data_ptr(), [o.data_ptr() for o in outs],
-                  stream.cuda_stream, err.data_ptr())
+    def step(k, s):
+        r = k % n_res
+        wc.decode(blobs[r], dblobs[r].data_ptr(), [o.data_ptr() for o in out_sets(k)],
+                  s.cuda_stream, err.data_ptr())
 
     for k in range(args.warmup):
-        step(k)
+        step(k, stream)
     torch.cuda.synchronize()
     K = args.steps
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -216,28 +284,55 @@ def main() -> int:
     start.record(stream)
     for k in range(K):
         ev[k][0].record(stream)
-        step(args.warmup + k)
+        step(args.warmup + k, stream)
         ev[k][1].record(stream)
     end.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
     launch_ms = [a.elapsed_time(b) for a, b in ev]
 
-    if int(err.item()) != 0:
-        raise RuntimeError(f"device errors during timing: {wc.describe_errors(int(err.item()))}")
-    for j in (1, 2):
-        k = args.warmup + K - j
-        if k < args.warmup:
-            continue
-        for o, r in zip(sets[k % 2], keep_orig[k % NL]):
-            if not torch.equal(o, r):
-                raise RuntimeError("timed decode output differs from the original")
+    def verify_last(what):
+        if int(err.item()) != 0:
+            raise RuntimeError(f"device errors during {what}: "
+                               f"{wc.describe_errors(int(err.item()))}")
+        for j in (1, 2):
+            k = args.warmup + K - j
+            if k < args.warmup:
+                continue
+            for o, r in zip(out_sets(k), origs(k)):
+                if not torch.equal(o[:r.numel() * r.element_size()], r.reshape(-1).view(torch.uint8)):
+                    raise RuntimeError(f"{what}: decode output differs from the original")
 
-    out_per_step = sum(layer_out)
-    in_per_step = float(np.mean([b.size for b in blobs]))
+    verify_last("the timed decode")
+
+    # --- the same steps on two streams (supplementary) --------------------------
+    two = None
+    if not args.no_two_stream:
+        streams = [torch.cuda.Stream(dev), torch.cuda.Stream(dev)]
+        for k in range(args.warmup):
+            step(k, streams[k % 2])
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(K):
+            step(args.warmup + k, streams[k % 2])
+        torch.cuda.synchronize()
+        dt2 = time.perf_counter() - t0
+        verify_last("the two-stream decode")
+        two = {"value": round(K * out_per_step / dt2 / 1e9, 2), "unit": "GB/s",
+               "ms_per_step": round(dt2 / K * 1e3, 4),
+               "timing": "host clock around K steps issued alternately on two streams"}
+
     value = K * out_per_step / (total_ms / 1e3) / 1e9
     mean_launch_s = float(np.mean(launch_ms)) / 1e3
     achieved = (in_per_step + out_per_step) / mean_launch_s / 1e9
+    config = {"workload": args.workload, "tensors_per_step": len(blobs[0].out_bytes),
+              "decoded_bytes_per_step": out_per_step,
+              "compressed_bytes_per_step": int(in_per_step),
+              "chunk_bytes": args.chunk_bytes, "lanes": args.lanes, "parallelism": "single-gpu"}
+    if big:
+        config["layers_resident"] = n_res
+    else:
+        config["copies_resident"] = n_res
     line = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -251,20 +346,16 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "u32",
         "data": "synthetic",
-        "config": {"workload": "llama3-70b-layer-bf16", "layers_resident": NL,
-                   "tensors_per_layer": len(layer_out),
-                   "decoded_bytes_per_step": out_per_step,
-                   "compressed_bytes_per_step": int(in_per_step),
-                   "chunk_bytes": args.chunk_bytes, "lanes": args.lanes,
-                   "parallelism": "single-gpu"},
+        "config": config,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": counted_traffic(args.chunk_bytes, args.lanes),
+                     "traffic": counted_traffic(args.workload, args.chunk_bytes, args.lanes),
                      "kernel": "wc_decode_kernel",
                      "mean_launch_us": round(mean_launch_s * 1e6, 2),
                      "algorithmic_bytes_per_launch": int(in_per_step + out_per_step)},
         "hbm_pct": round(100 * achieved / HBM_PEAK_GBPS, 2),
         "d2d_copy_GBps": round(copy_gbps, 1),
+        "two_stream": two,
         "compression": comp,
         "cpu_baseline": cpu,
         "setup_s": round(setup_s, 1),
