@@ -64,7 +64,7 @@ typedef struct {
 
 /* Encoder parameters.  chunk_bytes: decoded bytes per chunk, a multiple of
  * 256 in [256, 1 MiB] (16, 32 or 64 KiB in practice).  lanes: interleaved
- * rANS lanes per chunk, 1..64 (the GPU decoder takes 64).  prob_bits: must be
+ * rANS lanes per chunk, 1..64 (the GPU decoder takes 64 or 32).  prob_bits: must be
  * 12 (Sec. VI-F, b = 12).  n_threads: host encoder threads, 0 = all cores. */
 typedef struct {
   uint32_t chunk_bytes;
@@ -139,7 +139,8 @@ wc_status wc_encode(const wc_tensor* t, uint32_t n, const wc_params* p, wc_blob*
  * (magic, version, sizes, offsets, table sums, index order). */
 wc_status wc_open(const void* data, uint64_t size, wc_blob** out);
 
-/* wc_decode -- GPU decode of every tensor of a blob (Alg. 2), one launch.
+/* wc_decode -- GPU decode of every tensor of a blob (Alg. 2), one launch per
+ * 32 non-empty tensors.
  *   desc     host description from wc_encode / wc_open (supplies the grid and
  *            per-tensor layout, so no device-to-host copy is needed);
  *   dev_blob device copy of desc->data (desc->size bytes), caller-owned;
@@ -152,8 +153,9 @@ wc_status wc_open(const void* data, uint64_t size, wc_blob** out);
  *            (the caller clears it; read it after synchronising the stream).
  * Asynchronous with respect to the host; allocates nothing.  Reads only
  * inside [dev_blob, dev_blob + desc->size) and writes only the decoded byte
- * ranges.  Returns WC_EINVAL (argument mismatch), WC_EUNSUPPORTED (a tensor
- * coded with a lane count other than 64), WC_EHIP (launch failure). */
+ * ranges.  A wave decodes one 64-lane chunk, or two adjacent 32-lane chunks.
+ * Returns WC_EINVAL (argument mismatch), WC_EUNSUPPORTED (a tensor coded with
+ * a lane count other than 64 or 32), WC_EHIP (launch failure). */
 wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_dst, uint32_t n,
                     void* stream, int32_t* dev_err);
 

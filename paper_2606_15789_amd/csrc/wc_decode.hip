@@ -7,8 +7,11 @@
 // Sec. IV-A / V-B (independently decodable units located by an offset index).
 //
 // Mapping onto the MI355X:
-//  * a workgroup of kWaves wave64s decodes kWaves chunks of one tensor, one
-//    chunk per wave, one rANS lane per wave lane;
+//  * a workgroup of kWaves wave64s decodes chunks of one tensor, one rANS lane
+//    per wave lane: a wave decodes one 64-lane chunk, or two adjacent 32-lane
+//    chunks, one per half-wave (each half keeps its own word ring and cursor;
+//    a lane's rank within its half is the wave's mbcnt minus the lower half's
+//    popcount);
 //  * the workgroup shares one 4096-entry decode table in LDS, built from the
 //    tensor's 2^12-normalised frequencies; an entry is {f | symbol << 24,
 //    slot - cum}, so the state update is one v_mad_u32_u24 (the 24-bit multiply
@@ -71,7 +74,7 @@ struct DevTensor {
   uint32_t chunk_bytes;  // decoded bytes per full chunk
   uint32_t kind;
   uint32_t alphabet;
-  uint32_t pad;
+  uint32_t lanes;        // rANS lanes per chunk: 64, or 32 (two chunks per wave)
 };
 
 struct LaunchArgs {
@@ -166,87 +169,155 @@ __device__ __forceinline__ uint32_t assemble(const uint32_t (&lo)[W], uint32_t r
   }
 }
 
-// Everything a wave keeps about one chunk it decodes.
+// Everything a wave keeps about the kH chunks it decodes (kH = 64 / L: one
+// 64-lane chunk, or two adjacent 32-lane chunks, one per half-wave).  The
+// chunks' records, raw bytes and outputs are adjacent, so one buffer
+// descriptor spans both and a lane adds its half's base as a vector offset.
+template <int L>
 struct Chain {
-  __amdgpu_buffer_rsrc_t rs;  // the chunk record
-  __amdgpu_buffer_rsrc_t rr;  // the chunk's raw bytes (16-bit formats)
-  __amdgpu_buffer_rsrc_t os;  // the chunk's decoded bytes
-  uint32_t* ring;             // LDS word ring (kRingWords + kMirrorWords u16)
+  static constexpr int kH = 64 / L;
+  __amdgpu_buffer_rsrc_t rs;  // the chunks' records
+  __amdgpu_buffer_rsrc_t rr;  // the chunks' raw bytes (16-bit formats)
+  __amdgpu_buffer_rsrc_t os;  // the chunks' decoded bytes
+  uint32_t* ring;             // LDS word rings, one per half (kHalfRing32 u32 each)
   uint32_t x;                 // this lane's rANS state
-  uint32_t cursor;            // words consumed
-  uint32_t issued;            // units loaded or in flight
-  uint32_t nunits, nw, A, n_c, wbase;
+  uint32_t cursor[kH];        // words consumed, per half
+  uint32_t issued[kH];        // units loaded or in flight, per half
+  uint32_t nunits[kH], nw[kH], A[kH], n_c[kH], wbase[kH];
+  uint32_t rec1, raw1, out1;  // half 1's byte offsets within rs / rr / os
+  uint32_t n_exist;           // halves with a chunk
   bool ok;
 };
 
-__device__ __forceinline__ Chain open_chain(const LaunchArgs& a, const DevTensor& T,
-                                            uint32_t chunk, uint32_t W, uint32_t lane,
-                                            uint32_t* ring) {
-  Chain c;
+template <int L>
+struct Shape {
+  static constexpr int kH = 64 / L;
+  static constexpr uint32_t kUnitWords = 2 * L;               // one dword per lane of a half
+  static constexpr uint32_t kRingWords = 1024 / kH;           // per half
+  static constexpr uint32_t kMirrorWords = 64 / kH;           // a step reads at most L words
+  static constexpr uint32_t kHalfRing32 = (kRingWords + kMirrorWords) / 2;
+  static_assert(kRingWords == kRingUnits * kUnitWords, "ring shape");
+};
+
+template <int L>
+__device__ __forceinline__ Chain<L> open_chain(const LaunchArgs& a, const DevTensor& T,
+                                               uint32_t chunk0, uint32_t W, uint32_t lane,
+                                               uint32_t* ring) {
+  constexpr int kH = Chain<L>::kH;
+  Chain<L> c;
   const uint8_t* blob = reinterpret_cast<const uint8_t*>(a.blob);
   const uint32_t* index = reinterpret_cast<const uint32_t*>(blob + a.index_off);
-  const uint32_t g = T.first_chunk + chunk;
+  const uint32_t g = T.first_chunk + chunk0;
+  c.n_exist = min<uint32_t>(kH, T.n_chunks - chunk0);
   // per-chunk values are wave-uniform; readfirstlane keeps them (and the
   // buffer descriptors built from them) in scalar registers
-  const uint64_t o0 = 16ull * __builtin_amdgcn_readfirstlane(index[g]);
-  const uint64_t o1 = 16ull * __builtin_amdgcn_readfirstlane(index[g + 1]);
-  const uint64_t s0 = uint64_t(chunk) * T.per;
-  c.n_c = (uint32_t)min<uint64_t>(T.per, T.n_sym - s0);
-  c.A = min<uint32_t>(64u, (c.n_c + W - 1) / W);
+  uint64_t o[kH + 1];
+#pragma unroll
+  for (int h = 0; h <= kH; h++)
+    o[h] = 16ull * __builtin_amdgcn_readfirstlane(index[g + min<uint32_t>(h, c.n_exist)]);
   c.ring = ring;
-  c.cursor = 0;
-  c.issued = 0;
-  c.nw = c.nunits = c.wbase = 0;
-  c.ok = o0 >= a.records_off && o1 <= a.records_end && o1 >= o0 + 16;
-  if (c.ok) {
-    const uint32_t* rec = reinterpret_cast<const uint32_t*>(blob + o0);
-    c.nw = __builtin_amdgcn_readfirstlane(rec[0]);
-    const uint32_t recA = __builtin_amdgcn_readfirstlane(rec[1]);
-    const uint32_t recN = __builtin_amdgcn_readfirstlane(rec[2]);
-    c.wbase = 16u + (uint32_t)dpad16(4ull * c.A);
-    c.ok = recA == c.A && recN == c.n_c && c.wbase + dpad16(2ull * c.nw) == o1 - o0;
+  c.ok = true;
+  uint64_t end = o[0];
+#pragma unroll
+  for (int h = 0; h < kH; h++) {
+    c.cursor[h] = c.issued[h] = 0;
+    c.nw[h] = c.nunits[h] = c.wbase[h] = c.A[h] = c.n_c[h] = 0;
+    if ((uint32_t)h >= c.n_exist) continue;
+    const uint64_t s0 = uint64_t(chunk0 + h) * T.per;
+    c.n_c[h] = (uint32_t)min<uint64_t>(T.per, T.n_sym - s0);
+    c.A[h] = min<uint32_t>(L, (c.n_c[h] + W - 1) / W);
+    bool ok = o[h] >= a.records_off && o[h + 1] <= a.records_end && o[h + 1] >= o[h] + 16;
+    if (ok) {
+      const uint32_t* rec = reinterpret_cast<const uint32_t*>(blob + o[h]);
+      c.nw[h] = __builtin_amdgcn_readfirstlane(rec[0]);
+      const uint32_t recA = __builtin_amdgcn_readfirstlane(rec[1]);
+      const uint32_t recN = __builtin_amdgcn_readfirstlane(rec[2]);
+      c.wbase[h] = (uint32_t)(o[h] - o[0]) + 16u + (uint32_t)dpad16(4ull * c.A[h]);
+      ok = recA == c.A[h] && recN == c.n_c[h] &&
+           c.wbase[h] + dpad16(2ull * c.nw[h]) == o[h + 1] - o[0];
+    }
+    c.nunits[h] = ok ? (c.nw[h] + Shape<L>::kUnitWords - 1) / Shape<L>::kUnitWords : 0u;
+    c.ok = c.ok && ok;
+    end = o[h + 1];
   }
-  c.rs = make_rsrc(blob + o0, c.ok ? (uint32_t)(o1 - o0) : 0u);
-  c.nunits = c.ok ? (c.nw + kUnitWords - 1) / kUnitWords : 0u;
-  c.x = __builtin_amdgcn_raw_buffer_load_b32(c.rs, 16u + 4u * lane, 0, 0);
-  if (lane >= c.A) c.x = wc::kStateLow;  // lanes without symbols keep the initial state
-  const uint32_t out_len =
-      (uint32_t)min<uint64_t>(T.chunk_bytes, T.out_bytes - uint64_t(chunk) * T.chunk_bytes);
-  c.os = make_rsrc(reinterpret_cast<const void*>(T.dst + uint64_t(chunk) * T.chunk_bytes),
-                   out_len);
-  const uint32_t raw_len = W == 2 ? (uint32_t)min<uint64_t>(T.per, T.raw_padded - s0) : 0u;
+  c.rs = make_rsrc(blob + o[0], c.ok ? (uint32_t)(end - o[0]) : 0u);
+  c.rec1 = kH == 2 ? (uint32_t)(o[1] - o[0]) : 0u;
+  // lane -> half h, lane within the half
+  const uint32_t h = kH == 2 ? lane / L : 0u;
+  const uint32_t sub = lane % L;
+  const uint32_t A_h = kH == 2 && h ? c.A[kH - 1] : c.A[0];
+  c.x = __builtin_amdgcn_raw_buffer_load_b32(c.rs, (h ? c.rec1 : 0u) + 16u + 4u * sub, 0, 0);
+  if (sub >= A_h) c.x = wc::kStateLow;  // lanes without symbols keep the initial state
+  const uint64_t s0 = uint64_t(chunk0) * T.per;
+  const uint64_t out0 = uint64_t(chunk0) * T.chunk_bytes;
+  const uint32_t out_len = (uint32_t)min<uint64_t>(uint64_t(kH) * T.chunk_bytes, T.out_bytes - out0);
+  c.os = make_rsrc(reinterpret_cast<const void*>(T.dst + out0), out_len);
+  c.out1 = T.chunk_bytes;
+  const uint32_t raw_len =
+      W == 2 ? (uint32_t)min<uint64_t>(uint64_t(kH) * T.per, T.raw_padded - s0) : 0u;
   c.rr = make_rsrc(blob + T.raw_off + s0, raw_len);
+  c.raw1 = T.per;
   return c;
 }
 
-// The unit load of one pipeline slot: unit `u` of the chain, or (kNoUnit) a
-// load past the record that returns zeros and touches no memory.
-__device__ __forceinline__ uint32_t load_unit(const Chain& c, uint32_t u, uint32_t lane) {
-  const uint32_t off = u == kNoUnit ? kFarOffset : c.wbase + u * (2u * kUnitWords);
-  return __builtin_amdgcn_raw_buffer_load_b32(c.rs, lane * 4u + off, 0, 0);
-}
-
-__device__ __forceinline__ void commit_unit(const Chain& c, uint32_t u, uint32_t v,
-                                            uint32_t lane) {
-  if (u == kNoUnit) return;
-  const uint32_t slot = u % kRingUnits;
-  c.ring[slot * (kUnitWords / 2) + lane] = v;
-  if (slot == 0 && lane < kMirrorWords / 2) c.ring[kRingWords / 2 + lane] = v;
-}
-
-// Next unit to issue, or kNoUnit when the stream is done or the ring is full.
-__device__ __forceinline__ uint32_t next_unit(Chain& c) {
-  if (c.issued < c.nunits && c.issued < c.cursor / kUnitWords + kRingUnits) return c.issued++;
+// Next unit of half h to issue, or kNoUnit when its stream is done or its
+// ring is full.
+template <int L>
+__device__ __forceinline__ uint32_t next_unit(Chain<L>& c, int h) {
+  if (c.issued[h] < c.nunits[h] &&
+      c.issued[h] < c.cursor[h] / Shape<L>::kUnitWords + kRingUnits)
+    return c.issued[h]++;
   return kNoUnit;
 }
 
+// The unit load of one pipeline slot, per lane: unit `u` of the lane's half,
+// or (kNoUnit) a load past the records that returns zeros and touches no memory.
+template <int L>
+__device__ __forceinline__ uint32_t load_unit(const Chain<L>& c, uint32_t u, uint32_t wb,
+                                              uint32_t sub) {
+  const uint32_t off = u == kNoUnit ? kFarOffset : wb + u * (4u * L);
+  return __builtin_amdgcn_raw_buffer_load_b32(c.rs, sub * 4u + off, 0, 0);
+}
+
+template <int L>
+__device__ __forceinline__ void commit_unit(const Chain<L>& c, uint32_t u, uint32_t v,
+                                            uint32_t h, uint32_t sub) {
+  if (u == kNoUnit) return;
+  const uint32_t slot = u % kRingUnits;
+  uint32_t* r = c.ring + h * Shape<L>::kHalfRing32;
+  r[slot * L + sub] = v;
+  if (slot == 0 && sub < Shape<L>::kMirrorWords / 2) r[Shape<L>::kRingWords / 2 + sub] = v;
+}
+
+// One pipeline slot: the unit of each half issued together (one load).
+template <int L>
+struct Slot {
+  uint32_t u;  // this lane's unit (its half's), or kNoUnit
+  uint32_t v;  // the loaded dword
+};
+
+template <int L>
+__device__ __forceinline__ Slot<L> issue(Chain<L>& c, uint32_t h, uint32_t sub) {
+  Slot<L> s;
+  if constexpr (Chain<L>::kH == 1) {
+    s.u = next_unit(c, 0);
+    s.v = load_unit(c, s.u, c.wbase[0], sub);
+  } else {
+    const uint32_t u0 = next_unit(c, 0), u1 = next_unit(c, 1);
+    s.u = h ? u1 : u0;
+    s.v = load_unit(c, s.u, h ? c.wbase[1] : c.wbase[0], sub);
+  }
+  return s;
+}
+
 // One decode step for the lanes with `active` set; returns the table entry's
-// low word (symbol in byte 3).  Branch-free: every lane reads a word and v_perm
-// either shifts it in or keeps the state, so a whole group of steps stays one
-// basic block and the compiler can overlap one step's LDS reads with the
-// previous step's arithmetic.
-template <bool kAll>
-__device__ __forceinline__ uint32_t step(Chain& c, const uint2* __restrict__ tab, bool active) {
+// low word (symbol in byte 3).  Branch-free: every lane reads a word and
+// v_perm either shifts it in or keeps the state, so a group of steps stays
+// one basic block.
+template <bool kAll, int L>
+__device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ tab, bool active,
+                                         uint32_t h) {
+  using S = Shape<L>;
   const uint2 e = tab[c.x & (wc::kTableSize - 1)];
   uint32_t xn = __umul24(e.x, c.x >> wc::kProbBits) + e.y;
   uint32_t lo = e.x;
@@ -259,44 +330,62 @@ __device__ __forceinline__ uint32_t step(Chain& c, const uint2* __restrict__ tab
   const uint32_t rank =
       __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
   const uint16_t* words = reinterpret_cast<const uint16_t*>(c.ring);
-  const uint32_t w = words[(c.cursor & (kRingWords - 1)) + rank];
+  uint32_t idx;
+  if constexpr (Chain<L>::kH == 1) {
+    idx = (c.cursor[0] & (S::kRingWords - 1)) + rank;
+    c.cursor[0] += (uint32_t)__popcll(m);
+  } else {
+    // the upper half's rank counts the lower half's lanes too: subtract them
+    const uint32_t p0 = (uint32_t)__popc((uint32_t)m);
+    const uint32_t b0 = c.cursor[0] & (S::kRingWords - 1);
+    const uint32_t b1 = 2 * S::kHalfRing32 + (c.cursor[1] & (S::kRingWords - 1)) - p0;
+    idx = (h ? b1 : b0) + rank;
+    c.cursor[0] += p0;
+    c.cursor[1] += (uint32_t)__popc((uint32_t)(m >> 32));
+  }
+  const uint32_t w = words[idx];
   // bytes {w0, w1, x0, x1} = (x << 16) | w, or {x0, x1, x2, x3} = x
   c.x = __builtin_amdgcn_perm(xn, w, need ? 0x05040100u : 0x07060504u);
-  c.cursor += (uint32_t)__popcll(m);
   return lo;
 }
 
-// Decode one chunk with the whole wave, one rANS lane per wave lane.
-template <int W>
-__device__ __forceinline__ void decode_chunk(const LaunchArgs& a, const DevTensor& T,
-                                             uint32_t chunk, uint32_t lane,
-                                             const uint2* __restrict__ tab, uint32_t* ring) {
+// Decode the chunk(s) of one wave, one rANS lane per wave lane.
+template <int W, int L>
+__device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
+                                              uint32_t chunk0, uint32_t lane,
+                                              const uint2* __restrict__ tab, uint32_t* ring) {
+  constexpr int kH = Chain<L>::kH;
   constexpr int kGroupsPerRow = W / 2;        // groups of two steps in a row
   constexpr int kUnroll = W == 2 ? kRawAhead : kPipe;  // groups per loop body
+  constexpr uint32_t kRowSym = L * W;          // symbols of one half-row
   static_assert(kUnroll % kPipe == 0 && kUnroll % kGroupsPerRow == 0, "pipeline shape");
 
-  Chain c = open_chain(a, T, chunk, W, lane, ring);
+  Chain<L> c = open_chain<L>(a, T, chunk0, W, lane, ring);
   if (!c.ok) {
     if (lane == 0) report(a, WC_DERR_INDEX);
     return;
   }
-  const uint32_t n_c = c.n_c;
-  const uint32_t rows_full = n_c / (64u * W);
-  const uint32_t rem = n_c % (64u * W);
-  const uint32_t rows = rows_full + (rem ? 1u : 0u);
+  const uint32_t h = kH == 2 ? lane / L : 0u;
+  const uint32_t sub = lane % L;
+  // rows every lane of every half decodes in full, and rows in total
+  uint32_t rows_full = c.n_c[0] / kRowSym, rows = (c.n_c[0] + kRowSym - 1) / kRowSym;
+  if constexpr (kH == 2) {
+    rows_full = min(rows_full, c.n_c[1] / kRowSym);
+    rows = max(rows, (c.n_c[1] + kRowSym - 1) / kRowSym);
+  }
+  const uint32_t n_lane = kH == 2 && h ? c.n_c[kH - 1] : c.n_c[0];  // symbols of this lane's chunk
   const uint32_t groups = rows * kGroupsPerRow;
+  const uint32_t out_v = (kH == 2 && h ? c.out1 : 0u) + sub * 4u;   // lane's output offset
+  const uint32_t raw_v = (kH == 2 && h ? c.raw1 : 0u) + sub * 2u;   // lane's raw offset
 
   // prologue: unit 0 committed now, then kPipe units in flight
-  uint32_t pu[kPipe], pv[kPipe];
+  Slot<L> pipe[kPipe];
   {
-    const uint32_t u0 = next_unit(c);
-    commit_unit(c, u0, load_unit(c, u0, lane), lane);
+    const Slot<L> s0 = issue(c, h, sub);
+    commit_unit(c, s0.u, s0.v, h, sub);
   }
 #pragma unroll
-  for (int j = 0; j < kPipe; j++) {
-    pu[j] = next_unit(c);
-    pv[j] = load_unit(c, pu[j], lane);
-  }
+  for (int j = 0; j < kPipe; j++) pipe[j] = issue(c, h, sub);
   __builtin_amdgcn_wave_barrier();
 
   // raw bytes of the first kRawAhead rows (16-bit formats)
@@ -304,7 +393,7 @@ __device__ __forceinline__ void decode_chunk(const LaunchArgs& a, const DevTenso
   if constexpr (W == 2) {
 #pragma unroll
     for (int j = 0; j < kRawAhead; j++)
-      rq[j] = __builtin_amdgcn_raw_buffer_load_b16(c.rr, j * 128u + lane * 2u, 0, 0);
+      rq[j] = __builtin_amdgcn_raw_buffer_load_b16(c.rr, j * (2u * L) + raw_v, 0, 0);
   }
   uint32_t lo[W];
 
@@ -314,32 +403,31 @@ __device__ __forceinline__ void decode_chunk(const LaunchArgs& a, const DevTenso
     constexpr bool kTail = decltype(tailc)::value;
     constexpr int slot = j % kPipe;
     constexpr int k0 = (j % kGroupsPerRow) * 2;  // first step of this group in its row
-    commit_unit(c, pu[slot], pv[slot], lane);
-    pu[slot] = next_unit(c);
-    pv[slot] = load_unit(c, pu[slot], lane);
+    commit_unit(c, pipe[slot].u, pipe[slot].v, h, sub);
+    pipe[slot] = issue(c, h, sub);
     __builtin_amdgcn_wave_barrier();
-    const int nv = kTail ? max(0, min<int>(W, (int)rem - (int)(lane * W))) : W;
+    const uint32_t r = g / kGroupsPerRow;
+    const int nv = kTail ? max(0, min<int>(W, (int)n_lane - (int)(r * kRowSym + sub * W))) : W;
 #pragma unroll
-    for (int k = k0; k < k0 + 2; k++) lo[k] = step<!kTail>(c, tab, k < nv);
+    for (int k = k0; k < k0 + 2; k++) lo[k] = step<!kTail, L>(c, tab, k < nv, h);
     if constexpr (j % kGroupsPerRow == kGroupsPerRow - 1) {
-      const uint32_t r = g / kGroupsPerRow;
       uint32_t raw2 = 0;
       if constexpr (W == 2) {
         raw2 = rq[j % kRawAhead];
-        rq[j % kRawAhead] =
-            __builtin_amdgcn_raw_buffer_load_b16(c.rr, (r + kRawAhead) * 128u + lane * 2u, 0, 0);
+        rq[j % kRawAhead] = __builtin_amdgcn_raw_buffer_load_b16(
+            c.rr, (r + kRawAhead) * (2u * L) + raw_v, 0, 0);
       }
       const uint32_t word = assemble<W>(lo, raw2);
       if (!kTail) {
-        __builtin_amdgcn_raw_buffer_store_b32(word, c.os, lane * 4u, r * 256u, kStreamStore);
+        __builtin_amdgcn_raw_buffer_store_b32(word, c.os, out_v, r * (4u * L), kStreamStore);
       } else {
         const int nb = nv * 4 / W;  // valid output bytes of this lane
         if (nb == 4) {
-          __builtin_amdgcn_raw_buffer_store_b32(word, c.os, lane * 4u, r * 256u, kStreamStore);
+          __builtin_amdgcn_raw_buffer_store_b32(word, c.os, out_v, r * (4u * L), kStreamStore);
         } else {
           for (int b = 0; b < nb; b++)
-            __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(word >> (8 * b)), c.os, lane * 4u + b,
-                                                 r * 256u, 0);
+            __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(word >> (8 * b)), c.os, out_v + b,
+                                                 r * (4u * L), 0);
         }
       }
     }
@@ -352,19 +440,34 @@ __device__ __forceinline__ void decode_chunk(const LaunchArgs& a, const DevTenso
       (group(g0 + J, std::integral_constant<int, J>{}, std::false_type{}), ...);
     }(std::make_integer_sequence<int, kUnroll>{});
   }
-  // the remaining full rows and the partial last row
-  [&]<int... J>(std::integer_sequence<int, J...>) {
-    ((g0 + J < groups_full
-          ? group(g0 + J, std::integral_constant<int, J>{}, std::false_type{})
-          : (g0 + J < groups ? group(g0 + J, std::integral_constant<int, J>{}, std::true_type{})
-                             : void())),
-     ...);
-  }(std::make_integer_sequence<int, kUnroll>{});
+  // the remaining full groups, then the rows some lanes decode only in part
+  // (the last row of a chunk; with two chunks per wave, every row past the
+  // shorter chunk's full rows)
+  if constexpr (kH == 1) {
+    [&]<int... J>(std::integer_sequence<int, J...>) {
+      ((g0 + J < groups_full
+            ? group(g0 + J, std::integral_constant<int, J>{}, std::false_type{})
+            : (g0 + J < groups ? group(g0 + J, std::integral_constant<int, J>{}, std::true_type{})
+                               : void())),
+       ...);
+    }(std::make_integer_sequence<int, kUnroll>{});
+  } else {
+    for (; g0 < groups; g0 += kUnroll) {
+      [&]<int... J>(std::integer_sequence<int, J...>) {
+        ((g0 + J < groups ? group(g0 + J, std::integral_constant<int, J>{}, std::true_type{})
+                          : void()),
+         ...);
+      }(std::make_integer_sequence<int, kUnroll>{});
+    }
+  }
 
   // --- end-of-chunk checks: every lane back at 2^16, every word consumed ----
   uint32_t bits = 0;
-  if (__ballot(lane < c.A && c.x != wc::kStateLow)) bits |= WC_DERR_STATE;
-  if (c.cursor != c.nw) bits |= WC_DERR_CURSOR;
+  const uint32_t A_h = kH == 2 && h ? c.A[kH - 1] : c.A[0];
+  if (__ballot(sub < A_h && c.x != wc::kStateLow)) bits |= WC_DERR_STATE;
+#pragma unroll
+  for (int k = 0; k < kH; k++)
+    if (c.cursor[k] != c.nw[k]) bits |= WC_DERR_CURSOR;
   if (lane == 0) report(a, bits);
 }
 
@@ -385,12 +488,21 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
   // buffer descriptors live in scalar registers
   const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const uint32_t lane = __lane_id();
-  const uint32_t chunk = (wg - T.wg0) * kWaves + wave;
-  if (chunk >= T.n_chunks) return;
-  switch (T.kind) {
-    case kSplit16: decode_chunk<2>(a, T, chunk, lane, tab, ring[wave]); break;
-    case kByte: decode_chunk<4>(a, T, chunk, lane, tab, ring[wave]); break;
-    default: decode_chunk<8>(a, T, chunk, lane, tab, ring[wave]); break;
+  const uint32_t per_wave = T.lanes == 32 ? 2u : 1u;
+  const uint32_t chunk0 = ((wg - T.wg0) * kWaves + wave) * per_wave;
+  if (chunk0 >= T.n_chunks) return;
+  if (T.lanes == 32) {
+    switch (T.kind) {
+      case kSplit16: decode_chunks<2, 32>(a, T, chunk0, lane, tab, ring[wave]); break;
+      case kByte: decode_chunks<4, 32>(a, T, chunk0, lane, tab, ring[wave]); break;
+      default: decode_chunks<8, 32>(a, T, chunk0, lane, tab, ring[wave]); break;
+    }
+  } else {
+    switch (T.kind) {
+      case kSplit16: decode_chunks<2, 64>(a, T, chunk0, lane, tab, ring[wave]); break;
+      case kByte: decode_chunks<4, 64>(a, T, chunk0, lane, tab, ring[wave]); break;
+      default: decode_chunks<8, 64>(a, T, chunk0, lane, tab, ring[wave]); break;
+    }
   }
 }
 
@@ -404,7 +516,7 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
   for (uint32_t t = 0; t < n; t++) {
     const wc::TensorInfo& T = P.tensors[t];
     if (T.n_chunks == 0) continue;
-    if (T.lanes != 64) return WC_EUNSUPPORTED;
+    if (T.lanes != 64 && T.lanes != 32) return WC_EUNSUPPORTED;
     if (!dev_dst[t]) return WC_EINVAL;
   }
   LaunchArgs args{};
@@ -433,7 +545,9 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
       D.chunk_bytes = T.chunk_bytes;
       D.kind = T.dtype == WC_U4 ? kNibble : (T.dtype == WC_U8 ? kByte : kSplit16);
       D.alphabet = T.alphabet;
-      wgs += (uint32_t)((T.n_chunks + kWaves - 1) / kWaves);
+      D.lanes = T.lanes;
+      const uint64_t per_group = uint64_t(kWaves) * (T.lanes == 32 ? 2u : 1u);
+      wgs += (uint32_t)((T.n_chunks + per_group - 1) / per_group);
     }
     if (nt == 0) break;
     args.n_tensors = nt;

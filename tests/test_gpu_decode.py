@@ -50,21 +50,23 @@ def check_exact(pairs, blob, outs, oracle_full=True):
             assert np.array_equal(got, ref[t]), (t, dt)
 
 
-def test_every_bit_pattern(dev):
+@pytest.mark.parametrize("lanes", [64, 32])
+def test_every_bit_pattern(dev, lanes):
     rng = np.random.default_rng(0)
     allw = rng.permutation(np.arange(65536, dtype=np.uint32)).astype(np.uint16)
     pairs = [("bf16", allw), ("fp16", allw[::-1].copy()),
              ("u8", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40))),
              ("u4", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40)))]
     for cb in (256, 16384, 65536):
-        say("bit patterns, chunk", cb)
-        blob = wc.encode(pairs, chunk_bytes=cb)
+        say("bit patterns, chunk", cb, "lanes", lanes)
+        blob = wc.encode(pairs, chunk_bytes=cb, lanes=lanes)
         check_exact(pairs, blob, gpu_decode(blob, dev))
 
 
 @pytest.mark.parametrize("dtype,esize", [("bf16", 2), ("fp16", 2), ("u8", 1), ("u4", 1)])
 @pytest.mark.parametrize("cb", [256, 16384, 65536])
-def test_edge_sizes(dev, dtype, esize, cb):
+@pytest.mark.parametrize("lanes", [64, 32])
+def test_edge_sizes(dev, dtype, esize, cb, lanes):
     rng = np.random.default_rng(1)
     E = cb // esize
     sizes = [0, 1, 2, 3, 5, 63, 64, 65, 127, 128, 129, 255, 257, E - 1, E, E + 1, 2 * E + 7, 3 * E]
@@ -76,26 +78,28 @@ def test_edge_sizes(dev, dtype, esize, cb):
             d = rng.integers(0, 256, n).astype(np.uint8)
             d[: n // 2] = 3
         pairs.append((dtype, d))
-    say("edge sizes", dtype, cb)
-    blob = wc.encode(pairs, chunk_bytes=cb)
+    say("edge sizes", dtype, cb, "lanes", lanes)
+    blob = wc.encode(pairs, chunk_bytes=cb, lanes=lanes)
     check_exact(pairs, blob, gpu_decode(blob, dev))
 
 
-def test_degenerate_tables(dev):
+@pytest.mark.parametrize("lanes", [64, 32])
+def test_degenerate_tables(dev, lanes):
     pairs = [("u8", np.full(200_000, 42, np.uint8)),                 # single symbol: f = 4096
              ("u4", np.full(70_000, 0x77, np.uint8)),
              ("bf16", np.full(50_000, 0x3F80, np.uint16)),
              ("u8", np.concatenate([np.zeros(100_000, np.uint8), np.arange(256, dtype=np.uint8)])),
              ("u8", np.arange(256, dtype=np.uint8).repeat(300))]     # uniform: 8 bits
-    blob = wc.encode(pairs)
+    blob = wc.encode(pairs, lanes=lanes)
     check_exact(pairs, blob, gpu_decode(blob, dev))
 
 
 @pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16)])
-def test_workloads_scaled(dev, cfg, div):
-    say("workload", cfg, "div", div)
+@pytest.mark.parametrize("lanes", [64, 32])
+def test_workloads_scaled(dev, cfg, div, lanes):
+    say("workload", cfg, "div", div, "lanes", lanes)
     pairs = [(t.dtype, t.data) for t in synth.config(cfg, div=div)]
-    blob = wc.encode(pairs)
+    blob = wc.encode(pairs, lanes=lanes)
     check_exact(pairs, blob, gpu_decode(blob, dev))
 
 
@@ -105,7 +109,8 @@ def test_oracle_blob_decodes_on_gpu(dev):
     check_exact(pairs, blob, gpu_decode(blob, dev), oracle_full=False)
 
 
-def test_many_tensors_split_over_launches(dev):
+@pytest.mark.parametrize("lanes", [64, 32])
+def test_many_tensors_split_over_launches(dev, lanes):
     rng = np.random.default_rng(4)
     pairs = []
     for i in range(75):
@@ -116,7 +121,7 @@ def test_many_tensors_split_over_launches(dev):
         else:
             d = rng.integers(0, 40, n).astype(np.uint8)
         pairs.append((dt, d))
-    blob = wc.encode(pairs, chunk_bytes=16384)
+    blob = wc.encode(pairs, chunk_bytes=16384, lanes=lanes)
     check_exact(pairs, blob, gpu_decode(blob, dev))
 
 
@@ -127,13 +132,14 @@ def _sample_chunks(n, k, rng):
     return sorted(pick)
 
 
-@pytest.mark.parametrize("cfg", [1, 2, 3, 4, 5])
-def test_workloads_full_size(dev, cfg):
+@pytest.mark.parametrize("cfg,lanes", [(1, 64), (2, 64), (3, 64), (4, 64), (5, 64), (4, 32),
+                                       (5, 32)])
+def test_workloads_full_size(dev, cfg, lanes):
     """Full workload sizes in the benchmark's launch configuration (one launch)."""
-    say("full workload", cfg)
+    say("full workload", cfg, "lanes", lanes)
     ts = synth.config(cfg)
     pairs = [(t.dtype, t.data) for t in ts]
-    blob = wc.encode(pairs, chunk_bytes=65536, lanes=64)
+    blob = wc.encode(pairs, chunk_bytes=65536, lanes=lanes)
     outs = gpu_decode(blob, dev)
     rng = np.random.default_rng(cfg)
     raw = blob.tobytes()
@@ -150,10 +156,11 @@ def test_workloads_full_size(dev, cfg):
     torch.cuda.empty_cache()
 
 
-def test_device_side_corruption_flags(dev):
+@pytest.mark.parametrize("lanes", [64, 32])
+def test_device_side_corruption_flags(dev, lanes):
     """The kernel's own checks turn corrupted device bytes into error bits."""
     pairs = [(t.dtype, t.data) for t in synth.config(1, div=8)]
-    blob = wc.encode(pairs, chunk_bytes=16384)
+    blob = wc.encode(pairs, chunk_bytes=16384, lanes=lanes)
     raw = blob.tobytes()
     idx = struct.unpack_from("<Q", raw, 32)[0]
     off1 = struct.unpack_from("<I", raw, idx + 4)[0] * 16

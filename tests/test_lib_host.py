@@ -119,10 +119,11 @@ def test_encode_rejects_bad_parameters():
 
 
 def test_decode_rejects_before_any_launch():
-    b = wc.encode([("bf16", np.zeros(1000, np.uint16))], lanes=32)
-    with pytest.raises(wc.WcError) as e:          # lane count the GPU path does not take
-        wc.decode(b, 1, [1])
-    assert e.value.rc == -5
+    for lanes in (1, 16, 48, 63):
+        b = wc.encode([("bf16", np.zeros(1000, np.uint16))], lanes=lanes)
+        with pytest.raises(wc.WcError) as e:      # lane count the GPU path does not take
+            wc.decode(b, 1, [1])
+        assert e.value.rc == -5
     b = wc.encode([("bf16", np.zeros(1000, np.uint16))])
     with pytest.raises(wc.WcError) as e:          # tensor count mismatch
         wc.decode(b, 1, [1, 1])
