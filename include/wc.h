@@ -28,7 +28,7 @@
  *     u32 n_words, u32 n_states (A), u32 n_symbols, u32 0,
  *     u32 state[A] (16-B padded), u16 word[n_words] (16-B padded).
  *   Symbol i of a chunk belongs to lane (i mod L*W) div W at step
- *   (i div L*W)*W + i mod W, with W symbols = 4 output bytes per lane-group.
+ *   (i div L*W)*W + i mod W, with W symbols = 16 output bytes per lane-group.
  */
 #ifndef WC_H_
 #define WC_H_

@@ -40,7 +40,7 @@
 #define ORC_M (1u << ORC_PROB_BITS)   /* table total 2^12 (Sec. VI-F, b = 12) */
 #define ORC_STATE_LOW (1u << 16)       /* rANS lower bound of the state        */
 #define ORC_MAGIC 0x31424357u          /* bytes 'W','C','B','1'                */
-#define ORC_VERSION 1u
+#define ORC_VERSION 2u
 
 #define ORC_OK 0
 #define ORC_EINVAL (-1)
@@ -89,9 +89,9 @@ uint16_t orc_merge16(uint8_t coded, uint8_t raw) {
 static int dtype_ok(uint32_t dt) { return dt >= ORC_DT_BF16 && dt <= ORC_DT_U4; }
 static int has_raw(uint32_t dt) { return dt == ORC_DT_BF16 || dt == ORC_DT_FP16; }
 static uint32_t alphabet_of(uint32_t dt) { return dt == ORC_DT_U4 ? 16u : 256u; }
-/* Symbols per lane-group: a lane-group always covers 4 output bytes. */
+/* Symbols per lane-group: a lane-group always covers 16 output bytes. */
 static uint32_t group_of(uint32_t dt) {
-  return dt == ORC_DT_U4 ? 8u : (dt == ORC_DT_U8 ? 4u : 2u);
+  return dt == ORC_DT_U4 ? 32u : (dt == ORC_DT_U8 ? 16u : 8u);
 }
 
 /* Number of coded symbols of a tensor of `nbytes` storage bytes. */
@@ -293,7 +293,7 @@ static void cumulative(const uint32_t* freq, uint32_t alphabet, uint32_t* cum) {
 /* Lane interleave of one chunk (Sec. V-C-3: R substreams, one per lane;    */
 /* indices follow the interleaved decode order).  Reading used: symbol i of */
 /* a chunk belongs to lane (i mod L*W) div W, at step                        */
-/* (i div L*W) * W + (i mod W).  So W consecutive symbols (4 output bytes)  */
+/* (i div L*W) * W + (i mod W).  So W consecutive symbols (16 output bytes) */
 /* belong to one lane, and a row of L*W symbols is spread over the lanes.   */
 
 static uint64_t symbol_at(uint64_t t, uint32_t lane, uint32_t L, uint32_t W) {

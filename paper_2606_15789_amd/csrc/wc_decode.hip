@@ -27,11 +27,12 @@
 //  * renormalisation: ballot of the lanes whose state fell below 2^16, mbcnt
 //    gives each of them its rank, the cursor advances by the popcount -- the
 //    lanes' words are consecutive in the stream;
-//  * the raw sign|mantissa bytes of bf16/fp16 rows are loaded 8 rows ahead;
-//  * every W steps a lane holds 4 decoded bytes (two bf16 rebuilt from their
-//    coded and raw bytes with v_perm / v_bfi, four int8 or eight int4) and the
-//    wave stores 256 contiguous bytes, one dword per lane, as a non-temporal
-//    (streaming) store.
+//  * a lane-group is 16 decoded bytes: every G steps a lane assembles a dword
+//    (two bf16 rebuilt from their coded and raw bytes with v_perm / v_bfi,
+//    four int8 or eight int4), and every 4G steps it stores the four with one
+//    16-byte non-temporal (streaming) store, so a wave writes a 1 KiB row;
+//  * the raw sign|mantissa bytes of bf16/fp16 rows (8 per lane per row) are
+//    loaded two rows ahead with one 8-byte load per lane;
 // No MFMA: the work is integer table decoding, not a contraction.
 #include <hip/hip_runtime.h>
 
@@ -48,7 +49,7 @@ constexpr int kRingUnits = 8;
 constexpr int kRingWords = kRingUnits * kUnitWords;  // 2 KiB
 constexpr int kMirrorWords = 64;
 constexpr int kPipe = 4;                   // groups between a unit's load and its commit
-constexpr int kRawAhead = 8;               // raw-byte rows in flight (16-bit formats)
+constexpr int kRawRows = 2;                // raw-byte rows in flight (16-bit formats)
 constexpr uint32_t kNoUnit = 0xFFFFFFFFu;
 // Offsets that can fall outside a buffer are always passed as the vector
 // offset, which the hardware range-checks against num_records; the scalar
@@ -145,17 +146,17 @@ __device__ void build_table(const LaunchArgs& a, const DevTensor& T, uint2* tab,
   }
 }
 
-// Decoded bytes of a lane-group from the table entries' low words (symbol in
-// byte 3) and, for 16-bit formats, the group's two raw bytes.
-template <int W>
-__device__ __forceinline__ uint32_t assemble(const uint32_t (&lo)[W], uint32_t raw2) {
-  if constexpr (W == 2) {
+// One decoded dword (G symbols) from the table entries' low words (symbol in
+// byte 3) and, for 16-bit formats, its two raw bytes.
+template <int G>
+__device__ __forceinline__ uint32_t assemble(const uint32_t (&lo)[G], uint32_t raw2) {
+  if constexpr (G == 2) {
     // word = raw bit 7 -> bit 15 | coded byte -> bits 14..7 | raw bits 6..0
     const uint32_t E = __builtin_amdgcn_perm(lo[1], lo[0], 0x0C070C03u);  // e0 | e1 << 16
     const uint32_t P = __builtin_amdgcn_perm(0u, raw2, 0x01010000u);       // r0 r0 r1 r1
     const uint32_t M = 0x807F807Fu;
     return (P & M) | ((E << 7) & ~M);
-  } else if constexpr (W == 4) {
+  } else if constexpr (G == 4) {
     const uint32_t b01 = __builtin_amdgcn_perm(lo[1], lo[0], 0x0C0C0703u);
     const uint32_t b23 = __builtin_amdgcn_perm(lo[3], lo[2], 0x0C0C0703u);
     return b01 | (b23 << 16);
@@ -253,8 +254,9 @@ __device__ __forceinline__ Chain<L> open_chain(const LaunchArgs& a, const DevTen
   const uint32_t out_len = (uint32_t)min<uint64_t>(uint64_t(kH) * T.chunk_bytes, T.out_bytes - out0);
   c.os = make_rsrc(reinterpret_cast<const void*>(T.dst + out0), out_len);
   c.out1 = T.chunk_bytes;
-  const uint32_t raw_len =
-      W == 2 ? (uint32_t)min<uint64_t>(uint64_t(kH) * T.per, T.raw_padded - s0) : 0u;
+  const uint32_t raw_len = T.kind == kSplit16
+                               ? (uint32_t)min<uint64_t>(uint64_t(kH) * T.per, T.raw_padded - s0)
+                               : 0u;
   c.rr = make_rsrc(blob + T.raw_off + s0, raw_len);
   c.raw1 = T.per;
   return c;
@@ -349,15 +351,20 @@ __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ 
   return lo;
 }
 
-// Decode the chunk(s) of one wave, one rANS lane per wave lane.
-template <int W, int L>
+// Decode the chunk(s) of one wave, one rANS lane per wave lane.  G symbols
+// make one output dword; a lane-group is 4G symbols, 16 output bytes, so a
+// lane's share of a row is stored with one 16-byte store.
+template <int G, int L>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
                                               const uint2* __restrict__ tab, uint32_t* ring) {
   constexpr int kH = Chain<L>::kH;
+  constexpr int W = 4 * G;                    // symbols per lane-group
   constexpr int kGroupsPerRow = W / 2;        // groups of two steps in a row
-  constexpr int kUnroll = W == 2 ? kRawAhead : kPipe;  // groups per loop body
+  constexpr int kUnroll = G == 2 ? kGroupsPerRow * kRawRows : kGroupsPerRow;  // groups per body
   constexpr uint32_t kRowSym = L * W;          // symbols of one half-row
+  constexpr uint32_t kRowBytes = 16u * L;      // decoded bytes of one half-row
+  constexpr uint32_t kRawRowBytes = 8u * L;    // raw bytes of one half-row (16-bit formats)
   static_assert(kUnroll % kPipe == 0 && kUnroll % kGroupsPerRow == 0, "pipeline shape");
 
   Chain<L> c = open_chain<L>(a, T, chunk0, W, lane, ring);
@@ -375,8 +382,8 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   }
   const uint32_t n_lane = kH == 2 && h ? c.n_c[kH - 1] : c.n_c[0];  // symbols of this lane's chunk
   const uint32_t groups = rows * kGroupsPerRow;
-  const uint32_t out_v = (kH == 2 && h ? c.out1 : 0u) + sub * 4u;   // lane's output offset
-  const uint32_t raw_v = (kH == 2 && h ? c.raw1 : 0u) + sub * 2u;   // lane's raw offset
+  const uint32_t out_v = (kH == 2 && h ? c.out1 : 0u) + sub * 16u;  // lane's output offset
+  const uint32_t raw_v = (kH == 2 && h ? c.raw1 : 0u) + sub * 8u;   // lane's raw offset
 
   // prologue: unit 0 committed now, then kPipe units in flight
   Slot<L> pipe[kPipe];
@@ -388,46 +395,61 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   for (int j = 0; j < kPipe; j++) pipe[j] = issue(c, h, sub);
   __builtin_amdgcn_wave_barrier();
 
-  // raw bytes of the first kRawAhead rows (16-bit formats)
-  uint32_t rq[W == 2 ? kRawAhead : 1];
-  if constexpr (W == 2) {
+  // raw bytes (8 per lane per row) of the first kRawRows rows (16-bit formats)
+  uint2 rq[G == 2 ? kRawRows : 1];
+  if constexpr (G == 2) {
 #pragma unroll
-    for (int j = 0; j < kRawAhead; j++)
-      rq[j] = __builtin_amdgcn_raw_buffer_load_b16(c.rr, j * (2u * L) + raw_v, 0, 0);
+    for (int j = 0; j < kRawRows; j++)
+      rq[j] = __builtin_bit_cast(
+          uint2, __builtin_amdgcn_raw_buffer_load_b64(c.rr, j * kRawRowBytes + raw_v, 0, 0));
   }
-  uint32_t lo[W];
+  uint32_t lo[G];   // entries of the dword being assembled
+  uint32_t ow[4];   // the row's four output dwords
 
   // group g of the chunk, j = g mod kUnroll (static)
   auto group = [&](uint32_t g, auto jc, auto tailc) {
     constexpr int j = decltype(jc)::value;
     constexpr bool kTail = decltype(tailc)::value;
     constexpr int slot = j % kPipe;
-    constexpr int k0 = (j % kGroupsPerRow) * 2;  // first step of this group in its row
+    constexpr int k0 = (j % kGroupsPerRow) * 2;  // first step of this group in its lane-group
     commit_unit(c, pipe[slot].u, pipe[slot].v, h, sub);
     pipe[slot] = issue(c, h, sub);
     __builtin_amdgcn_wave_barrier();
     const uint32_t r = g / kGroupsPerRow;
     const int nv = kTail ? max(0, min<int>(W, (int)n_lane - (int)(r * kRowSym + sub * W))) : W;
 #pragma unroll
-    for (int k = k0; k < k0 + 2; k++) lo[k] = step<!kTail, L>(c, tab, k < nv, h);
-    if constexpr (j % kGroupsPerRow == kGroupsPerRow - 1) {
+    for (int k = k0; k < k0 + 2; k++) lo[k % G] = step<!kTail, L>(c, tab, k < nv, h);
+    if constexpr ((k0 + 2) % G == 0) {
+      constexpr int d = (k0 + 1) / G;             // the dword these G steps complete
       uint32_t raw2 = 0;
-      if constexpr (W == 2) {
-        raw2 = rq[j % kRawAhead];
-        rq[j % kRawAhead] = __builtin_amdgcn_raw_buffer_load_b16(
-            c.rr, (r + kRawAhead) * (2u * L) + raw_v, 0, 0);
+      if constexpr (G == 2) {
+        const uint2 rv = rq[(j / kGroupsPerRow) % kRawRows];
+        const uint32_t src = d < 2 ? rv.x : rv.y;
+        raw2 = d & 1 ? src >> 16 : src;
       }
-      const uint32_t word = assemble<W>(lo, raw2);
-      if (!kTail) {
-        __builtin_amdgcn_raw_buffer_store_b32(word, c.os, out_v, r * (4u * L), kStreamStore);
+      ow[d] = assemble<G>(lo, raw2);
+    }
+    if constexpr (j % kGroupsPerRow == kGroupsPerRow - 1) {
+      if constexpr (G == 2) {
+        rq[(j / kGroupsPerRow) % kRawRows] = __builtin_bit_cast(
+            uint2, __builtin_amdgcn_raw_buffer_load_b64(c.rr, (r + kRawRows) * kRawRowBytes + raw_v,
+                                                        0, 0));
+      }
+      using v4u = __attribute__((ext_vector_type(4))) unsigned int;
+      const v4u o = {ow[0], ow[1], ow[2], ow[3]};
+      const int nb = nv * 4 / G;  // valid output bytes of this lane
+      if (!kTail || nb == 16) {
+        __builtin_amdgcn_raw_buffer_store_b128(o, c.os, out_v, r * kRowBytes, kStreamStore);
       } else {
-        const int nb = nv * 4 / W;  // valid output bytes of this lane
-        if (nb == 4) {
-          __builtin_amdgcn_raw_buffer_store_b32(word, c.os, out_v, r * (4u * L), kStreamStore);
-        } else {
-          for (int b = 0; b < nb; b++)
-            __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(word >> (8 * b)), c.os, out_v + b,
-                                                 r * (4u * L), 0);
+#pragma unroll
+        for (int d = 0; d < 4; d++) {
+          if (4 * d + 4 <= nb) {
+            __builtin_amdgcn_raw_buffer_store_b32(ow[d], c.os, out_v + 4u * d, r * kRowBytes, 0);
+          } else {
+            for (int b = 4 * d; b < nb; b++)
+              __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(ow[d] >> (8 * (b - 4 * d))), c.os,
+                                                   out_v + b, r * kRowBytes, 0);
+          }
         }
       }
     }
@@ -443,22 +465,12 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   // the remaining full groups, then the rows some lanes decode only in part
   // (the last row of a chunk; with two chunks per wave, every row past the
   // shorter chunk's full rows)
-  if constexpr (kH == 1) {
+  for (; g0 < groups; g0 += kUnroll) {
     [&]<int... J>(std::integer_sequence<int, J...>) {
-      ((g0 + J < groups_full
-            ? group(g0 + J, std::integral_constant<int, J>{}, std::false_type{})
-            : (g0 + J < groups ? group(g0 + J, std::integral_constant<int, J>{}, std::true_type{})
-                               : void())),
+      ((g0 + J < groups ? group(g0 + J, std::integral_constant<int, J>{}, std::true_type{})
+                        : void()),
        ...);
     }(std::make_integer_sequence<int, kUnroll>{});
-  } else {
-    for (; g0 < groups; g0 += kUnroll) {
-      [&]<int... J>(std::integer_sequence<int, J...>) {
-        ((g0 + J < groups ? group(g0 + J, std::integral_constant<int, J>{}, std::true_type{})
-                          : void()),
-         ...);
-      }(std::make_integer_sequence<int, kUnroll>{});
-    }
   }
 
   // --- end-of-chunk checks: every lane back at 2^16, every word consumed ----

@@ -11,7 +11,7 @@
 namespace wc {
 
 constexpr uint32_t kMagic = 0x31424357u;  // "WCB1"
-constexpr uint32_t kVersion = 1;
+constexpr uint32_t kVersion = 2;        // blob format version
 constexpr uint32_t kProbBits = 12;        // b = 12 (Sec. VI-F)
 constexpr uint32_t kTableSize = 1u << kProbBits;
 constexpr uint32_t kStateLow = 1u << 16;  // lower end of the state interval
@@ -21,8 +21,8 @@ constexpr uint32_t kMaxLanes = 64;
 
 inline bool has_raw(uint32_t dt) { return dt == WC_BF16 || dt == WC_FP16; }
 inline uint32_t alphabet_of(uint32_t dt) { return dt == WC_U4 ? 16u : 256u; }
-// W: symbols per lane-group; a lane-group is always 4 decoded bytes.
-inline uint32_t group_of(uint32_t dt) { return dt == WC_U4 ? 8u : (dt == WC_U8 ? 4u : 2u); }
+// W: symbols per lane-group; a lane-group is always 16 decoded bytes.
+inline uint32_t group_of(uint32_t dt) { return dt == WC_U4 ? 32u : (dt == WC_U8 ? 16u : 8u); }
 inline uint64_t symbols_of(uint32_t dt, uint64_t bytes) {
   return dt == WC_U4 ? 2 * bytes : (dt == WC_U8 ? bytes : bytes / 2);
 }
