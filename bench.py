@@ -12,7 +12,10 @@ statistics of the paper's models):
   llama3-8b-layer-int4    the same shapes as int4 codes (group 128) + fp16
       scales + bf16 norms;
   llama3-8b-layer-int8    the same shapes as per-row int8 (Student-t weights)
-      + fp16 scales + bf16 norms.
+      + fp16 scales + bf16 norms;
+  llama3-8b-layer-fp8-e4m3  fp8 e4m3 codes with per-row bf16 scales;
+  llama3-8b-layer-mxfp4   fp4 e2m1 codes + e8m0 scales per 32 inputs;
+  llama3-8b-layer-awq4    4-bit codes + 4-bit zero points + fp16 scales, g128.
 Blobs are encoded on the host with libwc's threaded encoder (64 KiB chunks,
 64 lanes by default) and kept resident in HBM; every resident blob is decoded
 once and checked byte-exact against its original before timing.
@@ -47,7 +50,9 @@ HBM_PEAK_GBPS = 8000.0
 WORKLOAD_DEFAULT = "llama3-70b-layer-bf16"
 # workload name -> seeded recipe number in paper_2606_15789_amd.synth.config
 WORKLOADS = {WORKLOAD_DEFAULT: 5, "bf16-matrix-4096": 1, "llama3-8b-layer-bf16": 2,
-             "llama3-8b-layer-int4": 3, "llama3-8b-layer-int8": 4}
+             "llama3-8b-layer-int4": 3, "llama3-8b-layer-int8": 4,
+             "llama3-8b-layer-fp8-e4m3": 6, "llama3-8b-layer-mxfp4": 7,
+             "llama3-8b-layer-awq4": 8}
 ROTATE_BYTES = 1 << 30   # resident bytes the small workloads rotate over
 
 # HBM bytes per launch of the 70B-layer decode from rocprofv3 --pmc FETCH_SIZE and

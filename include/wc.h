@@ -48,11 +48,22 @@ typedef enum {
   WC_EUNSUPPORTED = -5  /* valid blob the GPU path does not handle (e.g. lanes) */
 } wc_status;
 
-/* Storage formats.  WC_BF16 / WC_FP16: the 16-bit word is split into a coded
- * byte (bits 14..7) and a raw byte (bit 15, bits 6..0) -- Sec. II-B symbols
- * "determined by the chosen numeric format".  WC_U8: one coded symbol per byte
- * (int8 or fp8 codes).  WC_U4: two coded nibbles per byte, low nibble first. */
-typedef enum { WC_BF16 = 1, WC_FP16 = 2, WC_U8 = 3, WC_U4 = 4 } wc_dtype;
+/* Storage formats.  The symbols follow from the numeric format (Sec. II-B):
+ *   WC_BF16 / WC_FP16: the 16-bit word is split into a coded byte (bits 14..7)
+ *     and a raw byte (bit 15, bits 6..0);
+ *   WC_U8, WC_FP8_E4M3, WC_FP8_E5M2: one coded symbol per byte (int8 or fp8
+ *     codes; the three differ only in the recorded type);
+ *   WC_U4, WC_FP4_E2M1: two coded nibbles per byte, low nibble first (int4 or
+ *     fp4 e2m1 codes). */
+typedef enum {
+  WC_BF16 = 1,
+  WC_FP16 = 2,
+  WC_U8 = 3,
+  WC_U4 = 4,
+  WC_FP8_E4M3 = 5,
+  WC_FP8_E5M2 = 6,
+  WC_FP4_E2M1 = 7
+} wc_dtype;
 
 /* A host tensor to analyse or encode: `nbytes` bytes of raw storage. */
 typedef struct {

@@ -20,7 +20,9 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "wc_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-DTYPES = {"bf16": 1, "fp16": 2, "u8": 3, "u4": 4}
+DTYPES = {"bf16": 1, "fp16": 2, "u8": 3, "u4": 4, "fp8_e4m3": 5, "fp8_e5m2": 6, "fp4_e2m1": 7}
+_NIBBLE = ("u4", "fp4_e2m1")
+_BYTE = ("u8", "fp8_e4m3", "fp8_e5m2")
 
 
 def build(force: bool = False) -> str:
@@ -123,7 +125,7 @@ def symbols(dtype: str, data):
     """(coded symbols, raw bytes or None) of a tensor's storage bytes."""
     b = _bytes_view(data)
     dt = DTYPES[dtype]
-    n = {"u4": 2 * b.size, "u8": b.size}.get(dtype, b.size // 2)
+    n = 2 * b.size if dtype in _NIBBLE else (b.size if dtype in _BYTE else b.size // 2)
     coded = np.empty(max(n, 1), np.uint8)
     raw = np.empty(max(n, 1), np.uint8)
     rc = lib().orc_symbols(dt, _ptr(b), b.size, _ptr(coded), _ptr(raw))

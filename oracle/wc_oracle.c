@@ -35,6 +35,9 @@
 #define ORC_DT_FP16 2
 #define ORC_DT_U8 3
 #define ORC_DT_U4 4
+#define ORC_DT_FP8_E4M3 5   /* 1-byte codes: coded as byte symbols, like ORC_DT_U8 */
+#define ORC_DT_FP8_E5M2 6
+#define ORC_DT_FP4_E2M1 7   /* packed 4-bit codes: nibble symbols, like ORC_DT_U4 */
 
 #define ORC_PROB_BITS 12u
 #define ORC_M (1u << ORC_PROB_BITS)   /* table total 2^12 (Sec. VI-F, b = 12) */
@@ -86,24 +89,31 @@ uint16_t orc_merge16(uint8_t coded, uint8_t raw) {
   return (uint16_t)((sign << 15) | ((uint32_t)coded << 7) | low7);
 }
 
-static int dtype_ok(uint32_t dt) { return dt >= ORC_DT_BF16 && dt <= ORC_DT_U4; }
+static int dtype_ok(uint32_t dt) { return dt >= ORC_DT_BF16 && dt <= ORC_DT_FP4_E2M1; }
 static int has_raw(uint32_t dt) { return dt == ORC_DT_BF16 || dt == ORC_DT_FP16; }
-static uint32_t alphabet_of(uint32_t dt) { return dt == ORC_DT_U4 ? 16u : 256u; }
+/* Every byte of the tensor is one symbol (int8, fp8). */
+static int is_byte(uint32_t dt) {
+  return dt == ORC_DT_U8 || dt == ORC_DT_FP8_E4M3 || dt == ORC_DT_FP8_E5M2;
+}
+/* Every nibble is one symbol, low nibble first (int4, fp4). */
+static int is_nibble(uint32_t dt) { return dt == ORC_DT_U4 || dt == ORC_DT_FP4_E2M1; }
+static uint32_t alphabet_of(uint32_t dt) { return is_nibble(dt) ? 16u : 256u; }
 /* Symbols per lane-group: a lane-group always covers 16 output bytes. */
 static uint32_t group_of(uint32_t dt) {
-  return dt == ORC_DT_U4 ? 32u : (dt == ORC_DT_U8 ? 16u : 8u);
+  return is_nibble(dt) ? 32u : (is_byte(dt) ? 16u : 8u);
 }
 
 /* Number of coded symbols of a tensor of `nbytes` storage bytes. */
 static uint64_t n_symbols_of(uint32_t dt, uint64_t nbytes) {
-  if (dt == ORC_DT_U4) return 2 * nbytes;
-  if (dt == ORC_DT_U8) return nbytes;
+  if (is_nibble(dt)) return 2 * nbytes;
+  if (is_byte(dt)) return nbytes;
   return nbytes / 2;
 }
 
 /*
  * Coded symbol stream (and raw bytes for 16-bit types) of a tensor.
- * int8: one symbol per byte.  int4: two symbols per byte, low nibble first.
+ * int8 / fp8: one symbol per byte.  int4 / fp4: two symbols per byte, low
+ * nibble first.
  */
 int orc_symbols(uint32_t dt, const uint8_t* data, uint64_t nbytes, uint8_t* coded,
                 uint8_t* raw) {
@@ -111,9 +121,9 @@ int orc_symbols(uint32_t dt, const uint8_t* data, uint64_t nbytes, uint8_t* code
   if (has_raw(dt) && (nbytes % 2) != 0) return ORC_EINVAL;
   uint64_t n = n_symbols_of(dt, nbytes);
   for (uint64_t i = 0; i < n; i++) {
-    if (dt == ORC_DT_U8) {
+    if (is_byte(dt)) {
       coded[i] = data[i];
-    } else if (dt == ORC_DT_U4) {
+    } else if (is_nibble(dt)) {
       uint8_t byte = data[i / 2];
       coded[i] = (i % 2 == 0) ? (byte & 0x0F) : (byte >> 4);
     } else {
@@ -130,9 +140,9 @@ static void put_symbols(uint32_t dt, const uint8_t* coded, const uint8_t* raw, u
                         uint64_t n, uint8_t* out) {
   for (uint64_t k = 0; k < n; k++) {
     uint64_t i = s0 + k;
-    if (dt == ORC_DT_U8) {
+    if (is_byte(dt)) {
       out[i] = coded[k];
-    } else if (dt == ORC_DT_U4) {
+    } else if (is_nibble(dt)) {
       if (i % 2 == 0)
         out[i / 2] = (uint8_t)((out[i / 2] & 0xF0) | (coded[k] & 0x0F));
       else

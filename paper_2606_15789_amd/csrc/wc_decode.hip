@@ -555,7 +555,7 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
       D.wg0 = wgs;
       D.per = (uint32_t)T.sym_per_chunk();
       D.chunk_bytes = T.chunk_bytes;
-      D.kind = T.dtype == WC_U4 ? kNibble : (T.dtype == WC_U8 ? kByte : kSplit16);
+      D.kind = wc::is_nibble(T.dtype) ? kNibble : (wc::is_byte(T.dtype) ? kByte : kSplit16);
       D.alphabet = T.alphabet;
       D.lanes = T.lanes;
       const uint64_t per_group = uint64_t(kWaves) * (T.lanes == 32 ? 2u : 1u);

@@ -57,14 +57,15 @@ void parallel_for(uint64_t n, unsigned threads, F&& fn) {
 
 // ---------------------------------------------------------------------------
 // Field split (Sec. II-B): 16-bit words -> coded byte (bits 14..7) and raw
-// byte (bit 15 -> bit 7, bits 6..0); int8 -> byte; int4 -> nibbles, low first.
+// byte (bit 15 -> bit 7, bits 6..0); int8 / fp8 -> byte; int4 / fp4 -> nibbles,
+// low first.
 
 // Symbols [s0, s1) of the tensor at `src`; coded[k] / raw[k] receive symbol s0 + k.
 void split_range(uint32_t dt, const uint8_t* src, uint64_t s0, uint64_t s1, uint8_t* coded,
                  uint8_t* raw) {
-  if (dt == WC_U8) {
+  if (is_byte(dt)) {
     memcpy(coded, src + s0, s1 - s0);
-  } else if (dt == WC_U4) {
+  } else if (is_nibble(dt)) {
     for (uint64_t i = s0; i < s1; i++) {
       uint8_t b = src[i >> 1];
       coded[i - s0] = (i & 1) ? (b >> 4) : (b & 15);
@@ -279,7 +280,7 @@ wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out) {
     T.alphabet = ld16(d + 44);
     T.freq_off = ld64(d + 48);
     T.raw_off = ld64(d + 56);
-    if (T.dtype < WC_BF16 || T.dtype > WC_U4) return WC_EINVAL;
+    if (!dtype_ok(T.dtype)) return WC_EINVAL;
     if (pb != kProbBits || T.group != group_of(T.dtype) || T.alphabet != alphabet_of(T.dtype))
       return WC_EINVAL;
     if (T.lanes < 1 || T.lanes > kMaxLanes) return WC_EINVAL;
@@ -341,7 +342,7 @@ int32_t wc_version(void) { return 1; }
 wc_status wc_analyze(const wc_tensor* t, wc_stats* out) {
   if (!t || !out || (!t->host_ptr && t->nbytes)) return WC_EINVAL;
   uint32_t dt = uint32_t(t->dtype);
-  if (dt < WC_BF16 || dt > WC_U4) return WC_EINVAL;
+  if (!dtype_ok(dt)) return WC_EINVAL;
   if (has_raw(dt) && t->nbytes % 2) return WC_EINVAL;
   try {
     memset(out, 0, sizeof(*out));
@@ -393,7 +394,7 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
     return WC_EINVAL;
   for (uint32_t t = 0; t < n; t++) {
     uint32_t dt = uint32_t(ts[t].dtype);
-    if (dt < WC_BF16 || dt > WC_U4) return WC_EINVAL;
+    if (!dtype_ok(dt)) return WC_EINVAL;
     if (has_raw(dt) && ts[t].nbytes % 2) return WC_EINVAL;
     if (!ts[t].host_ptr && ts[t].nbytes) return WC_EINVAL;
   }

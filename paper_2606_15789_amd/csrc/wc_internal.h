@@ -19,12 +19,16 @@ constexpr uint32_t kHeaderBytes = 64;
 constexpr uint32_t kDescBytes = 64;
 constexpr uint32_t kMaxLanes = 64;
 
+inline bool dtype_ok(uint32_t dt) { return dt >= WC_BF16 && dt <= WC_FP4_E2M1; }
 inline bool has_raw(uint32_t dt) { return dt == WC_BF16 || dt == WC_FP16; }
-inline uint32_t alphabet_of(uint32_t dt) { return dt == WC_U4 ? 16u : 256u; }
+// one symbol per byte (int8, fp8) / per nibble, low first (int4, fp4)
+inline bool is_byte(uint32_t dt) { return dt == WC_U8 || dt == WC_FP8_E4M3 || dt == WC_FP8_E5M2; }
+inline bool is_nibble(uint32_t dt) { return dt == WC_U4 || dt == WC_FP4_E2M1; }
+inline uint32_t alphabet_of(uint32_t dt) { return is_nibble(dt) ? 16u : 256u; }
 // W: symbols per lane-group; a lane-group is always 16 decoded bytes.
-inline uint32_t group_of(uint32_t dt) { return dt == WC_U4 ? 32u : (dt == WC_U8 ? 16u : 8u); }
+inline uint32_t group_of(uint32_t dt) { return is_nibble(dt) ? 32u : (is_byte(dt) ? 16u : 8u); }
 inline uint64_t symbols_of(uint32_t dt, uint64_t bytes) {
-  return dt == WC_U4 ? 2 * bytes : (dt == WC_U8 ? bytes : bytes / 2);
+  return is_nibble(dt) ? 2 * bytes : (is_byte(dt) ? bytes : bytes / 2);
 }
 inline uint64_t pad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
 

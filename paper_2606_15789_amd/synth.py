@@ -187,6 +187,100 @@ def quant_int8_rows(w: np.ndarray):
     return codes.view(np.uint8), scales.view(np.uint16)
 
 
+def quant_fp8_rows(w: np.ndarray, fmt: str = "e4m3"):
+    """Per-output-row scaled fp8 codes (OCP e4m3 'fn' or e5m2) and bf16 scales.
+
+    scale = absmax_row / max_finite (448 for e4m3, 57344 for e5m2); the codes
+    are torch's round-to-nearest-even conversion of w / scale.
+    """
+    import torch
+    dt, fmax = {"e4m3": (torch.float8_e4m3fn, 448.0), "e5m2": (torch.float8_e5m2, 57344.0)}[fmt]
+    rows, cols = w.shape
+    codes = np.empty((rows, cols), dtype=np.uint8)
+    scales = np.empty(rows, dtype=np.float32)
+
+    def q(rr):
+        r0, r1 = rr
+        blk = torch.from_numpy(np.ascontiguousarray(w[r0:r1]))
+        amax = blk.abs().amax(dim=1)
+        sc = torch.where(amax > 0, amax / fmax, torch.ones_like(amax))
+        scales[r0:r1] = sc.numpy()
+        codes[r0:r1] = (blk / sc[:, None]).to(dt).view(torch.uint8).numpy()
+
+    _pool_map(q, _row_blocks(rows, cols))
+    return codes, to_bf16(scales)
+
+
+_E2M1 = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0], dtype=np.float32)
+
+
+_E2M1_MID = (_E2M1[1:] + _E2M1[:-1]) / 2
+
+
+def fp4_e2m1_codes(x: np.ndarray) -> np.ndarray:
+    """4-bit e2m1 codes (sign << 3 | magnitude index) of x, round to nearest,
+    ties to the even code, saturating at 6."""
+    a = np.minimum(np.abs(x), np.float32(6.0))
+    lo = np.searchsorted(_E2M1_MID, a, side="left")    # midpoints strictly below a
+    hi = np.searchsorted(_E2M1_MID, a, side="right")   # midpoints at or below a
+    idx = np.where(lo == hi, lo, np.where(lo % 2 == 0, lo, hi)).astype(np.uint8)
+    sign = (np.signbit(x) & (idx > 0)).astype(np.uint8)
+    return (sign << 3) | idx
+
+
+def quant_mxfp4(w: np.ndarray, block: int = 32):
+    """MXFP4 (OCP microscaling): e2m1 codes, packed two per byte (low nibble =
+    even element), and one e8m0 scale byte per `block` inputs:
+    scale = 2^(floor(log2(amax)) - 2), stored as its biased exponent."""
+    rows, cols = w.shape
+    assert cols % block == 0
+    packed = np.empty((rows, cols // 2), dtype=np.uint8)
+    scales = np.empty((rows, cols // block), dtype=np.uint8)
+
+    def q(rr):
+        r0, r1 = rr
+        g = w[r0:r1].reshape(r1 - r0, cols // block, block)
+        amax = np.abs(g).max(axis=2)
+        e = np.where(amax > 0, np.floor(np.log2(np.maximum(amax, 1e-30))) - 2, -127)
+        e = np.clip(e, -127, 127).astype(np.int32)
+        scales[r0:r1] = (e + 127).astype(np.uint8)
+        x = g / np.exp2(e.astype(np.float32))[..., None]
+        c = fp4_e2m1_codes(x).reshape(r1 - r0, cols)
+        packed[r0:r1] = c[:, 0::2] | (c[:, 1::2] << 4)
+
+    _pool_map(q, _row_blocks(rows, cols))
+    return packed, scales
+
+
+def quant_awq4(w: np.ndarray, group: int = 128):
+    """Asymmetric per-group 4-bit codes with zero points (AWQ-style storage):
+    scale = (max - min) / 15 (fp16), zero = clamp(rint(-min / scale), 0, 15),
+    q = clamp(rint(w / scale) + zero, 0, 15).  Codes and zeros are packed
+    nibbles (low nibble = even element)."""
+    rows, cols = w.shape
+    assert cols % group == 0 and (cols // group) % 2 == 0
+    packed = np.empty((rows, cols // 2), dtype=np.uint8)
+    zeros = np.empty((rows, cols // group // 2), dtype=np.uint8)
+    scales = np.empty((rows, cols // group), dtype=np.float16)
+
+    def q(rr):
+        r0, r1 = rr
+        g = w[r0:r1].reshape(r1 - r0, cols // group, group)
+        lo, hi = g.min(axis=2), g.max(axis=2)
+        s16 = ((hi - lo) / np.float32(15.0)).astype(np.float16)
+        s16[s16 == 0] = np.float16(1.0)
+        s32 = s16.astype(np.float32)
+        z = np.clip(np.rint(-lo / s32), 0, 15).astype(np.uint8)
+        qq = np.clip(np.rint(g / s32[..., None]) + z[..., None], 0, 15).astype(np.uint8)
+        qq = qq.reshape(r1 - r0, cols)
+        packed[r0:r1] = qq[:, 0::2] | (qq[:, 1::2] << 4)
+        zeros[r0:r1] = z[:, 0::2] | (z[:, 1::2] << 4)
+        scales[r0:r1] = s16
+
+    _pool_map(q, _row_blocks(rows, cols))
+    return packed, zeros, scales.view(np.uint16)
+
+
 # --------------------------------------------------------------------------
 # Layer shapes ([out, in], PyTorch Linear layout).
 
@@ -261,6 +355,31 @@ def config(cfg: int, layer: int = 0, div: int = 1) -> list:
             w = normal_weight(o, i, 0.015, _key(4, layer, j), outliers=True)
             ts.append(Tensor(name, "bf16", to_bf16(w), (o, i)))
         return ts
+    if cfg == 6:
+        ts = []
+        for j, (name, o, i) in enumerate(_scaled(LLAMA3_8B, div)):
+            w = normal_weight(o, i, 0.02, _key(6, j), outliers=True)
+            codes, scales = quant_fp8_rows(w, "e4m3")
+            ts.append(Tensor(name + ".weight", "fp8_e4m3", codes.reshape(-1), (o, i)))
+            ts.append(Tensor(name + ".scale", "bf16", scales.reshape(-1), (o,)))
+        return ts + _norms(6, div)
+    if cfg == 7:
+        ts = []
+        for j, (name, o, i) in enumerate(_scaled(LLAMA3_8B, div)):
+            w = normal_weight(o, i, 0.02, _key(7, j), outliers=True)
+            codes, scales = quant_mxfp4(w)
+            ts.append(Tensor(name + ".blocks", "fp4_e2m1", codes.reshape(-1), (o, i)))
+            ts.append(Tensor(name + ".scales", "u8", scales.reshape(-1), (o, i // 32)))
+        return ts + _norms(7, div)
+    if cfg == 8:
+        ts = []
+        for j, (name, o, i) in enumerate(_scaled(LLAMA3_8B, div)):
+            w = normal_weight(o, i, 0.02, _key(8, j))
+            codes, zeros, scales = quant_awq4(w)
+            ts.append(Tensor(name + ".qweight", "u4", codes.reshape(-1), (o, i)))
+            ts.append(Tensor(name + ".qzeros", "u4", zeros.reshape(-1), (o, i // 128)))
+            ts.append(Tensor(name + ".scales", "fp16", scales.reshape(-1), (o, i // 128)))
+        return ts + _norms(8, div)
     raise ValueError(f"unknown workload {cfg}")
 
 
@@ -270,6 +389,9 @@ CONFIG_NAMES = {
     3: "Llama-3-8B layer int4 g128 + fp16 scales",
     4: "Llama-3-8B layer int8 per-row (Student-t nu=5) + fp16 scales",
     5: "Llama-3-70B layer bf16 (outlier channels)",
+    6: "Llama-3-8B layer fp8 e4m3, per-row bf16 scales (outlier channels)",
+    7: "Llama-3-8B layer MXFP4: e2m1 codes + e8m0 scales per 32 inputs",
+    8: "Llama-3-8B layer AWQ-style int4 g128: codes + 4-bit zero points + fp16 scales",
 }
 
 

@@ -15,7 +15,7 @@ import numpy as np
 
 from . import build as _build
 
-DTYPES = {"bf16": 1, "fp16": 2, "u8": 3, "u4": 4}
+DTYPES = {"bf16": 1, "fp16": 2, "u8": 3, "u4": 4, "fp8_e4m3": 5, "fp8_e5m2": 6, "fp4_e2m1": 7}
 STATUS = {0: "WC_OK", -1: "WC_EINVAL", -2: "WC_ENOMEM", -3: "WC_ECORRUPT", -4: "WC_EHIP",
           -5: "WC_EUNSUPPORTED"}
 DERR = {1: "WC_DERR_INDEX", 2: "WC_DERR_STATE", 4: "WC_DERR_CURSOR", 8: "WC_DERR_TABLE"}

@@ -56,14 +56,18 @@ def test_every_bit_pattern(dev, lanes):
     allw = rng.permutation(np.arange(65536, dtype=np.uint32)).astype(np.uint16)
     pairs = [("bf16", allw), ("fp16", allw[::-1].copy()),
              ("u8", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40))),
-             ("u4", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40)))]
+             ("u4", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40))),
+             ("fp8_e4m3", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 30))),
+             ("fp8_e5m2", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 20))),
+             ("fp4_e2m1", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 25)))]
     for cb in (256, 16384, 65536):
         say("bit patterns, chunk", cb, "lanes", lanes)
         blob = wc.encode(pairs, chunk_bytes=cb, lanes=lanes)
         check_exact(pairs, blob, gpu_decode(blob, dev))
 
 
-@pytest.mark.parametrize("dtype,esize", [("bf16", 2), ("fp16", 2), ("u8", 1), ("u4", 1)])
+@pytest.mark.parametrize("dtype,esize", [("bf16", 2), ("fp16", 2), ("u8", 1), ("u4", 1),
+                                         ("fp8_e4m3", 1), ("fp4_e2m1", 1)])
 @pytest.mark.parametrize("cb", [256, 16384, 65536])
 @pytest.mark.parametrize("lanes", [64, 32])
 def test_edge_sizes(dev, dtype, esize, cb, lanes):
@@ -94,7 +98,8 @@ def test_degenerate_tables(dev, lanes):
     check_exact(pairs, blob, gpu_decode(blob, dev))
 
 
-@pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16)])
+@pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16), (6, 8), (7, 8),
+                                     (8, 8)])
 @pytest.mark.parametrize("lanes", [64, 32])
 def test_workloads_scaled(dev, cfg, div, lanes):
     say("workload", cfg, "div", div, "lanes", lanes)
@@ -133,7 +138,7 @@ def _sample_chunks(n, k, rng):
 
 
 @pytest.mark.parametrize("cfg,lanes", [(1, 64), (2, 64), (3, 64), (4, 64), (5, 64), (4, 32),
-                                       (5, 32)])
+                                       (5, 32), (6, 64), (7, 64), (8, 64)])
 def test_workloads_full_size(dev, cfg, lanes):
     """Full workload sizes in the benchmark's launch configuration (one launch)."""
     say("full workload", cfg, "lanes", lanes)

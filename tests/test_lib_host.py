@@ -38,7 +38,8 @@ def test_library_exports_every_declared_symbol():
     assert lib.wc_version() == 1
 
 
-@pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16)])
+@pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16), (6, 8), (7, 8),
+                                     (8, 8)])
 @pytest.mark.parametrize("lanes", [64, 32])
 def test_blobs_identical_to_oracle(cfg, div, lanes):
     ts = synth.config(cfg, div=div)
@@ -55,7 +56,9 @@ def test_blob_identical_on_edge_sizes_and_patterns():
     allw = rng.permutation(np.arange(65536, dtype=np.uint32)).astype(np.uint16)
     pairs = [("bf16", allw), ("fp16", allw[:1001]), ("u8", np.zeros(0, np.uint8)),
              ("u4", rng.integers(0, 256, 777).astype(np.uint8)), ("u8", np.full(5, 9, np.uint8)),
-             ("bf16", allw[:1])]
+             ("bf16", allw[:1]), ("fp8_e5m2", rng.integers(0, 256, 3001).astype(np.uint8)),
+             ("fp4_e2m1", rng.integers(0, 256, 513).astype(np.uint8)),
+             ("fp8_e4m3", np.zeros(0, np.uint8))]
     for lanes in (1, 7, 64):
         for cb in (256, 1024):
             assert wc.encode(pairs, chunk_bytes=cb, lanes=lanes).tobytes() == \
@@ -69,7 +72,7 @@ def test_encoder_is_thread_count_invariant():
         assert wc.encode(pairs, threads=th).tobytes() == ref
 
 
-@pytest.mark.parametrize("cfg", [1, 3, 4])
+@pytest.mark.parametrize("cfg", [1, 3, 4, 6, 7])
 def test_analyze_matches_oracle(cfg):
     for t in synth.config(cfg, div=8):
         a, o = wc.analyze(t.dtype, t.data), oracle.analyze(t.dtype, t.data)

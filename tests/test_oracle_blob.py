@@ -28,13 +28,17 @@ def test_every_bit_pattern():
     allw = rng.permutation(np.arange(65536, dtype=np.uint32)).astype(np.uint16)
     tens = [("bf16", allw), ("fp16", allw[::-1].copy()),
             ("u8", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40))),
-            ("u4", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40)))]
+            ("u4", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 40))),
+            ("fp8_e4m3", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 30))),
+            ("fp8_e5m2", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 20))),
+            ("fp4_e2m1", rng.permutation(np.repeat(np.arange(256, dtype=np.uint8), 25)))]
     for lanes in (1, 32, 64):
         for cb in (256, 16384, 65536):
             roundtrip(tens, chunk_bytes=cb, lanes=lanes)
 
 
-@pytest.mark.parametrize("dtype,esize", [("bf16", 2), ("fp16", 2), ("u8", 1), ("u4", 1)])
+@pytest.mark.parametrize("dtype,esize", [("bf16", 2), ("fp16", 2), ("u8", 1), ("u4", 1),
+                                         ("fp8_e4m3", 1), ("fp4_e2m1", 1)])
 @pytest.mark.parametrize("cb", [256, 16384])
 def test_edge_sizes(dtype, esize, cb):
     rng = np.random.default_rng(1)
@@ -119,7 +123,7 @@ def _payload(blob):
     return states + words + (len(blob) - raw)
 
 
-@pytest.mark.parametrize("cfg,div", [(1, 1), (2, 4), (3, 4), (4, 4)])
+@pytest.mark.parametrize("cfg,div", [(1, 1), (2, 4), (3, 4), (4, 4), (6, 4), (7, 4), (8, 4)])
 def test_size_within_one_percent_of_entropy_bound(cfg, div):
     ts = synth.config(cfg, div=div)
     pairs = [(t.dtype, t.data) for t in ts]
@@ -131,3 +135,16 @@ def test_size_within_one_percent_of_entropy_bound(cfg, div):
         assert _payload(blob) <= 1.01 * bound, (cfg, lanes)
         if lanes == 32:
             assert len(blob) <= 1.01 * bound, (cfg, lanes)
+
+
+def test_fp8_and_fp4_code_like_bytes_and_nibbles():
+    """fp8 tensors produce the byte symbol stream of int8, fp4 the nibble
+    stream of int4; only the recorded type differs."""
+    rng = np.random.default_rng(9)
+    d = rng.integers(0, 256, 4099).astype(np.uint8)
+    for a, b in (("fp8_e4m3", "u8"), ("fp8_e5m2", "u8"), ("fp4_e2m1", "u4")):
+        ca, ra = oracle.symbols(a, d)
+        cb, rb = oracle.symbols(b, d)
+        assert np.array_equal(ca, cb) and ra is None and rb is None
+        assert oracle.analyze(a, d)["H"] == oracle.analyze(b, d)["H"]
+    assert len(oracle.symbols("fp4_e2m1", d)[0]) == 2 * d.size
