@@ -115,13 +115,13 @@ def oracle_baseline(blob, host_tensors, workload: str, min_seconds: float = 3.0)
             "seconds": round(dt, 3), "cpu": cpu_model(), "host_cpus": os.cpu_count()}
 
 
-def counted_traffic(workload: str, chunk_bytes: int, lanes: int):
+def counted_traffic(workload: str, chunk_bytes: int, lanes: int, tiled: bool = False):
     import hashlib
     src = os.path.join(ROOT, "paper_2606_15789_amd", "csrc", "wc_decode.hip")
     with open(src, "rb") as fh:
         sha = hashlib.sha256(fh.read()).hexdigest()[:16]
     c = COUNTED_TRAFFIC
-    if (workload != WORKLOAD_DEFAULT or sha != c["kernel_sha256"]
+    if (workload != WORKLOAD_DEFAULT or tiled or sha != c["kernel_sha256"]
             or chunk_bytes != c["chunk_bytes"] or lanes != c["lanes"]):
         return None
     return c["fetch_bytes"] + c["write_bytes"]
@@ -157,6 +157,9 @@ def main() -> int:
     ap.add_argument("--threads", type=int, default=int(os.environ.get("OMP_NUM_THREADS", "16")))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-two-stream", action="store_true")
+    ap.add_argument("--tile", default="", help="ROWSxCOLS 2-D tiles, e.g. 128x256 (default: "
+                    "flat chunks of --chunk-bytes)")
+    ap.add_argument("--codebook", choices=["tensor", "layer"], default="tensor")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -176,6 +179,8 @@ def main() -> int:
     wc.lib()
     cfg = WORKLOADS[args.workload]
     big = cfg == 5
+    tile = tuple(int(v) for v in args.tile.lower().split("x")) if args.tile else (0, 0)
+    shaped = lambda t, d, shape: (t, d, shape if len(shape) == 2 else None)  # noqa: E731
 
     # --- setup: draw, encode, upload, verify ---------------------------------
     # The 70B workload keeps `--layers` distinct layer blobs; the others keep
@@ -210,8 +215,9 @@ def main() -> int:
             t0 = time.perf_counter()
             tens = synth.config_torch_device(5, layer, device="cuda")
             host = [("bf16", t.cpu().numpy()) for _, t, _ in tens]
-            blob = wc.encode(host, chunk_bytes=args.chunk_bytes, lanes=args.lanes,
-                             threads=args.threads)
+            blob = wc.encode([shaped(dt, h, shape) for (dt, h), (_, _, shape) in zip(host, tens)],
+                             chunk_bytes=args.chunk_bytes, lanes=args.lanes,
+                             threads=args.threads, tile=tile, codebook=args.codebook)
             blobs.append(blob)
             dblobs.append(wc.to_device(blob, dev))
             if len(sets) == 0:
@@ -231,8 +237,9 @@ def main() -> int:
     else:
         tens = synth.config(cfg)
         host = [(t.dtype, t.data) for t in tens]
-        blob = wc.encode(host, chunk_bytes=args.chunk_bytes, lanes=args.lanes,
-                         threads=args.threads)
+        blob = wc.encode([shaped(t.dtype, t.data, t.shape) for t in tens],
+                         chunk_bytes=args.chunk_bytes, lanes=args.lanes,
+                         threads=args.threads, tile=tile, codebook=args.codebook)
         per = blob.size + sum(blob.out_bytes)
         n_res = max(2, -(-ROTATE_BYTES // per))
         dev_orig = [torch.from_numpy(np.ascontiguousarray(h).view(np.uint8).reshape(-1)).to(dev)
@@ -334,6 +341,10 @@ def main() -> int:
               "decoded_bytes_per_step": out_per_step,
               "compressed_bytes_per_step": int(in_per_step),
               "chunk_bytes": args.chunk_bytes, "lanes": args.lanes, "parallelism": "single-gpu"}
+    if args.tile:
+        config["tile"] = args.tile
+    if args.codebook != "tensor":
+        config["codebook"] = args.codebook
     if big:
         config["layers_resident"] = n_res
     else:
@@ -354,7 +365,8 @@ def main() -> int:
         "config": config,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                     "traffic": counted_traffic(args.workload, args.chunk_bytes, args.lanes),
+                     "traffic": counted_traffic(args.workload, args.chunk_bytes, args.lanes,
+                                                bool(args.tile) or args.codebook != "tensor"),
                      "kernel": "wc_decode_kernel",
                      "mean_launch_us": round(mean_launch_s * 1e6, 2),
                      "algorithmic_bytes_per_launch": int(in_per_step + out_per_step)},

@@ -20,11 +20,14 @@
  * passed as plain pointers (`void*`), so any allocator (torch, hipMalloc)
  * can own them.
  *
- * Blob format (little-endian; every offset absolute from the blob start):
- *   header 64 B, then one 64-B descriptor per tensor, then each tensor's
- *   u16 frequency table (16-B padded), the chunk index (u32 per chunk + 1:
- *   record offset / 16), the chunk records and the raw bytes.  A chunk covers
- *   `chunk_bytes` of decoded output; its record is
+ * Blob format version 3 (little-endian; every offset absolute from the blob
+ * start): header 64 B, then one 96-B descriptor per tensor (type, chunk size,
+ * sizes, lanes, table and raw offsets, shape and tile), then the u16 frequency
+ * tables (16-B padded; tensors sharing a codebook point to one table), the
+ * chunk index (u32 per chunk + 1: record offset / 16), the chunk records and
+ * the raw bytes.  A chunk covers `chunk_bytes` of decoded output (a tile of a
+ * tiled tensor, whose symbols and raw bytes are stored tile by tile); its
+ * record is
  *     u32 n_words, u32 n_states (A), u32 n_symbols, u32 0,
  *     u32 state[A] (16-B padded), u16 word[n_words] (16-B padded).
  *   Symbol i of a chunk belongs to lane (i mod L*W) div W at step
@@ -65,24 +68,44 @@ typedef enum {
   WC_FP4_E2M1 = 7
 } wc_dtype;
 
-/* A host tensor to analyse or encode: `nbytes` bytes of raw storage. */
+/* A host tensor to analyse or encode: `nbytes` bytes of raw storage.
+ * rows, cols: optional matrix shape in symbol elements (16-bit words, bytes,
+ * or nibbles for 4-bit formats), row-major; 0, 0 when the tensor is only a
+ * byte run.  A shape is what lets wc_encode cut the tensor into 2-D tiles. */
 typedef struct {
   const void* host_ptr;
   uint64_t nbytes;
   int32_t dtype; /* wc_dtype */
   int32_t reserved;
+  uint64_t rows;
+  uint64_t cols;
 } wc_tensor;
 
 /* Encoder parameters.  chunk_bytes: decoded bytes per chunk, a multiple of
  * 256 in [256, 1 MiB] (16, 32 or 64 KiB in practice).  lanes: interleaved
- * rANS lanes per chunk, 1..64 (the GPU decoder takes 64 or 32).  prob_bits: must be
- * 12 (Sec. VI-F, b = 12).  n_threads: host encoder threads, 0 = all cores. */
+ * rANS lanes per chunk, 1..64 (the GPU decoder takes 64 or 32).  prob_bits:
+ * must be 12 (Sec. VI-F, b = 12).  n_threads: host encoder threads, 0 = all
+ * cores.
+ * tile_rows, tile_cols: 2-D tiles (Sec. IV-A), both 0 for none.  A tensor
+ * whose shape they divide exactly is coded one chunk per tile, tiles in
+ * row-major order and each tile's symbols row-major; tile_cols must be a power
+ * of two.  Tensors without a shape, or with one the tile does not divide, or
+ * a tile narrower than a 16-byte lane-group, keep chunk_bytes chunks.
+ * codebook: WC_CODEBOOK_TENSOR (one table per tensor) or WC_CODEBOOK_LAYER
+ * (one table per dtype for the whole blob, Sec. IV / V-B). */
 typedef struct {
   uint32_t chunk_bytes;
   uint32_t lanes;
   uint32_t prob_bits;
   uint32_t n_threads;
+  uint32_t tile_rows;
+  uint32_t tile_cols;
+  uint32_t codebook;
+  uint32_t reserved;
 } wc_params;
+
+#define WC_CODEBOOK_TENSOR 0u
+#define WC_CODEBOOK_LAYER 1u
 
 /* Per-field statistics of one tensor (Sec. II-B).  Field 0 is the coded
  * symbol stream; field 1 (16-bit formats only) the raw byte stream.
@@ -173,7 +196,7 @@ wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);
 
-/* wc_version -- ABI version of this header (1). */
+/* wc_version -- ABI version of this header (2). */
 int32_t wc_version(void);
 
 #ifdef __cplusplus

@@ -46,7 +46,8 @@ class Stats(C.Structure):
 
 
 class _Tensor(C.Structure):
-    _fields_ = [("data", C.c_void_p), ("nbytes", C.c_uint64), ("dtype", C.c_uint32)]
+    _fields_ = [("data", C.c_void_p), ("nbytes", C.c_uint64), ("dtype", C.c_uint32),
+                ("rows", C.c_uint64), ("cols", C.c_uint64)]
 
 
 def lib():
@@ -76,13 +77,14 @@ def lib():
                                         C.c_uint64, C.c_void_p, C.c_uint32, C.c_uint32,
                                         C.c_uint32, C.c_void_p]
         L.orc_encode_blob.argtypes = [C.POINTER(_Tensor), C.c_uint32, C.c_uint32, C.c_uint32,
+                                      C.c_uint32, C.c_uint32, C.c_uint32,
                                       C.POINTER(u8p), C.POINTER(C.c_uint64)]
         L.orc_free.argtypes = [C.c_void_p]
         L.orc_free.restype = None
         L.orc_blob_tensors.argtypes = [C.c_void_p, C.c_uint64, C.POINTER(C.c_uint32)]
         L.orc_blob_tensor_info.argtypes = [C.c_void_p, C.c_uint64, C.c_uint32,
                                            C.POINTER(C.c_uint64), C.POINTER(C.c_uint32),
-                                           C.POINTER(C.c_uint64)]
+                                           C.POINTER(C.c_uint64), C.POINTER(C.c_uint32)]
         L.orc_decode_blob.argtypes = [C.c_void_p, C.c_uint64, C.POINTER(C.c_void_p)]
         L.orc_decode_chunks.argtypes = [C.c_void_p, C.c_uint64, C.c_uint32, C.c_uint64,
                                         C.c_uint64, C.c_void_p]
@@ -210,20 +212,31 @@ def decode_stream(states, words, n: int, freq, lanes: int, group: int):
 
 # --- blobs -------------------------------------------------------------------
 
-def encode(tensors, chunk_bytes: int = 65536, lanes: int = 64) -> bytes:
-    """Blob bytes of a list of (dtype, storage array) pairs."""
+def encode(tensors, chunk_bytes: int = 65536, lanes: int = 64, tile=(0, 0),
+           codebook: str = "tensor") -> bytes:
+    """Blob bytes of a list of (dtype, storage array[, (rows, cols)]) entries.
+
+    `tile` = (rows, cols) cuts every tensor whose shape (in symbol elements:
+    16-bit words, bytes or nibbles) the tile divides into one chunk per tile;
+    the others use `chunk_bytes`.  codebook "layer" shares one table among all
+    tensors of a dtype.
+    """
     keep = []
     arr = (_Tensor * len(tensors))()
-    for i, (dt, data) in enumerate(tensors):
+    for i, entry in enumerate(tensors):
+        dt, data = entry[0], entry[1]
+        rows, cols = entry[2] if len(entry) > 2 and entry[2] is not None else (0, 0)
         b = _bytes_view(data)
         keep.append(b)
         arr[i].data = b.ctypes.data if b.size else None
         arr[i].nbytes = b.size
         arr[i].dtype = DTYPES[dt]
+        arr[i].rows, arr[i].cols = rows, cols
     out = C.POINTER(C.c_uint8)()
     size = C.c_uint64()
-    rc = lib().orc_encode_blob(arr, len(tensors), chunk_bytes, lanes, C.byref(out),
-                               C.byref(size))
+    shared = {"tensor": 0, "layer": 1}[codebook]
+    rc = lib().orc_encode_blob(arr, len(tensors), chunk_bytes, lanes, tile[0], tile[1], shared,
+                               C.byref(out), C.byref(size))
     if rc:
         raise OracleError(rc, "encode")
     try:
@@ -245,11 +258,13 @@ def tensor_info(blob):
     info = []
     for t in range(n.value):
         ob, dt, nc = C.c_uint64(), C.c_uint32(), C.c_uint64()
+        tile = (C.c_uint32 * 3)()
         rc = lib().orc_blob_tensor_info(_ptr(b), b.size, t, C.byref(ob), C.byref(dt),
-                                        C.byref(nc))
+                                        C.byref(nc), tile)
         if rc:
             raise OracleError(rc, "tensor info")
-        info.append({"out_bytes": ob.value, "dtype": dt.value, "n_chunks": nc.value})
+        info.append({"out_bytes": ob.value, "dtype": dt.value, "n_chunks": nc.value,
+                     "tile": (tile[0], tile[1]), "chunk_bytes": tile[2]})
     return info
 
 

@@ -43,7 +43,7 @@
 #define ORC_M (1u << ORC_PROB_BITS)   /* table total 2^12 (Sec. VI-F, b = 12) */
 #define ORC_STATE_LOW (1u << 16)       /* rANS lower bound of the state        */
 #define ORC_MAGIC 0x31424357u          /* bytes 'W','C','B','1'                */
-#define ORC_VERSION 2u
+#define ORC_VERSION 3u
 
 #define ORC_OK 0
 #define ORC_EINVAL (-1)
@@ -110,6 +110,29 @@ static uint64_t n_symbols_of(uint32_t dt, uint64_t nbytes) {
   return nbytes / 2;
 }
 
+/* ---- 2-D tiles (Sec. IV-A: each tile of the weight matrix is its own     */
+/* substream).  A tensor is tiled when it has a shape the tile divides       */
+/* exactly, the tile width is a power of two covering whole lane-groups, and */
+/* a tile's bytes are a valid chunk size.  Its symbols are then coded in     */
+/* tile-major order (tiles row by row, each tile row-major) with one chunk   */
+/* per tile; the raw bytes follow the same order.                            */
+
+static int pow2(uint64_t x) { return x && !(x & (x - 1)); }
+
+static int tile_ok(uint32_t dt, uint64_t rows, uint64_t cols, uint32_t tr, uint32_t tc) {
+  if (!tr || !tc || !rows || !cols) return 0;
+  if (rows % tr || cols % tc || !pow2(tc) || tc < group_of(dt)) return 0;
+  uint64_t cb = (uint64_t)tr * tc * 16 / group_of(dt); /* 16 bytes per lane-group */
+  return cb >= 256 && cb <= (1u << 20) && cb % 256 == 0;
+}
+
+/* Element index (row-major in the tensor) of tile-major symbol k. */
+static uint64_t tile_element(uint64_t k, uint64_t cols, uint32_t tr, uint32_t tc) {
+  uint64_t per = (uint64_t)tr * tc, t = k / per, in = k % per;
+  uint64_t ntc = cols / tc, a = t / ntc, bcol = t % ntc;
+  return (a * tr + in / tc) * cols + bcol * tc + in % tc;
+}
+
 /*
  * Coded symbol stream (and raw bytes for 16-bit types) of a tensor.
  * int8 / fp8: one symbol per byte.  int4 / fp4: two symbols per byte, low
@@ -136,10 +159,12 @@ int orc_symbols(uint32_t dt, const uint8_t* data, uint64_t nbytes, uint8_t* code
 }
 
 /* Inverse of orc_symbols: write tensor bytes for symbol range [s0, s0+n). */
+/* Symbol s0 + k is written to element map(s0 + k): the identity, or the     */
+/* tile-major order when cols > 0.                                           */
 static void put_symbols(uint32_t dt, const uint8_t* coded, const uint8_t* raw, uint64_t s0,
-                        uint64_t n, uint8_t* out) {
+                        uint64_t n, uint8_t* out, uint64_t cols, uint32_t tr, uint32_t tc) {
   for (uint64_t k = 0; k < n; k++) {
-    uint64_t i = s0 + k;
+    uint64_t i = cols ? tile_element(s0 + k, cols, tr, tc) : s0 + k;
     if (is_byte(dt)) {
       out[i] = coded[k];
     } else if (is_nibble(dt)) {
@@ -430,7 +455,12 @@ typedef struct {
   const uint8_t* data;
   uint64_t nbytes;
   uint32_t dtype;
+  uint64_t rows, cols; /* shape in symbol elements (0, 0 = none) */
 } orc_tensor;
+
+#define ORC_DESC 96u /* bytes per tensor descriptor */
+
+
 
 static uint64_t symbols_per_chunk(uint32_t dt, uint32_t chunk_bytes) {
   return n_symbols_of(dt, chunk_bytes);
@@ -441,47 +471,122 @@ static uint64_t chunks_of(uint64_t n_sym, uint64_t per) { return (n_sym + per - 
 void orc_free(void* p) { free(p); }
 
 int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_bytes, uint32_t L,
+                    uint32_t tile_r, uint32_t tile_c, uint32_t shared_tables,
                     uint8_t** blob_out, uint64_t* size_out) {
   if (!ts || !blob_out || !size_out) return ORC_EINVAL;
   if (n_tensors == 0 || n_tensors > 4096) return ORC_EINVAL;
   if (chunk_bytes < 256 || chunk_bytes > (1u << 20) || chunk_bytes % 256) return ORC_EINVAL;
   if (L < 1 || L > 64) return ORC_EINVAL;
+  if ((tile_r == 0) != (tile_c == 0) || (tile_c && !pow2(tile_c))) return ORC_EINVAL;
 
-  /* pass 1: symbols, tables, chunk records (kept separately), sizes */
-  uint64_t n_chunks = 0;
   for (uint32_t t = 0; t < n_tensors; t++) {
-    if (!dtype_ok(ts[t].dtype)) return ORC_EINVAL;
-    if (has_raw(ts[t].dtype) && ts[t].nbytes % 2) return ORC_EINVAL;
-    uint64_t n = n_symbols_of(ts[t].dtype, ts[t].nbytes);
-    n_chunks += chunks_of(n, symbols_per_chunk(ts[t].dtype, chunk_bytes));
+    uint32_t dt = ts[t].dtype;
+    if (!dtype_ok(dt)) return ORC_EINVAL;
+    if (has_raw(dt) && ts[t].nbytes % 2) return ORC_EINVAL;
+    if ((ts[t].rows || ts[t].cols) && ts[t].rows * ts[t].cols != n_symbols_of(dt, ts[t].nbytes))
+      return ORC_EINVAL;
   }
-  if (n_chunks > 0xFFFFFFFEull) return ORC_EINVAL;
+
+  /* pass 0: per tensor, chunk size (tile or flat) and chunk count */
+  uint64_t n_chunks = 0;
+  uint32_t* cbytes = (uint32_t*)calloc(n_tensors, sizeof(uint32_t));
+  uint8_t* tiled = (uint8_t*)calloc(n_tensors, 1);
+  if (!cbytes || !tiled) {
+    free(cbytes);
+    free(tiled);
+    return ORC_ENOMEM;
+  }
+  for (uint32_t t = 0; t < n_tensors; t++) {
+    uint32_t dt = ts[t].dtype;
+    uint64_t n = n_symbols_of(dt, ts[t].nbytes);
+    tiled[t] = (uint8_t)tile_ok(dt, ts[t].rows, ts[t].cols, tile_r, tile_c);
+    cbytes[t] = tiled[t] ? (uint32_t)((uint64_t)tile_r * tile_c * 16 / group_of(dt)) : chunk_bytes;
+    n_chunks += chunks_of(n, symbols_per_chunk(dt, cbytes[t]));
+  }
+  int rc = n_chunks > 0xFFFFFFFEull ? ORC_EINVAL : ORC_OK;
 
   uint8_t** rec = (uint8_t**)calloc(n_chunks ? n_chunks : 1, sizeof(uint8_t*));
   uint64_t* rec_size = (uint64_t*)calloc(n_chunks ? n_chunks : 1, sizeof(uint64_t));
   uint32_t* freqs = (uint32_t*)calloc((size_t)n_tensors * 256, sizeof(uint32_t));
   uint8_t** raws = (uint8_t**)calloc(n_tensors, sizeof(uint8_t*));
-  if (!rec || !rec_size || !freqs || !raws) return ORC_ENOMEM;
+  uint8_t** codeds = (uint8_t**)calloc(n_tensors, sizeof(uint8_t*));
+  uint32_t* table_of = (uint32_t*)calloc(n_tensors, sizeof(uint32_t)); /* tensor -> table */
+  uint64_t(*hist)[256] = (uint64_t(*)[256])calloc(n_tensors, sizeof(uint64_t[256]));
+  if (!rec || !rec_size || !freqs || !raws || !codeds || !table_of || !hist) rc = ORC_ENOMEM;
+  if (rc != ORC_OK) n_chunks = 0; /* nothing to free per chunk */
 
-  int rc = ORC_OK;
+  /* pass 1: symbols in coding order (tile-major when tiled), histograms */
+  for (uint32_t t = 0; t < n_tensors && rc == ORC_OK; t++) {
+    uint32_t dt = ts[t].dtype;
+    uint64_t n = n_symbols_of(dt, ts[t].nbytes);
+    uint8_t* coded = (uint8_t*)malloc(n ? n : 1);
+    uint8_t* raw = (uint8_t*)malloc(n ? n : 1);
+    if (!coded || !raw) {
+      free(coded);
+      free(raw);
+      rc = ORC_ENOMEM;
+      break;
+    }
+    orc_symbols(dt, ts[t].data, ts[t].nbytes, coded, raw);
+    if (tiled[t]) {
+      uint8_t* c2 = (uint8_t*)malloc(n ? n : 1);
+      uint8_t* r2 = (uint8_t*)malloc(n ? n : 1);
+      if (!c2 || !r2) {
+        free(c2);
+        free(r2);
+        free(coded);
+        free(raw);
+        rc = ORC_ENOMEM;
+        break;
+      }
+      for (uint64_t k = 0; k < n; k++) {
+        uint64_t e = tile_element(k, ts[t].cols, tile_r, tile_c);
+        c2[k] = coded[e];
+        r2[k] = raw[e];
+      }
+      free(coded);
+      free(raw);
+      coded = c2;
+      raw = r2;
+    }
+    orc_histogram(coded, n, hist[t]);
+    codeds[t] = coded;
+    raws[t] = raw;
+  }
+
+  /* tables: one per tensor, or (layer codebook) one per dtype, normalised
+     from the summed histogram of every tensor of that dtype */
+  uint32_t n_tables = 0;
+  for (uint32_t t = 0; t < n_tensors && rc == ORC_OK; t++) {
+    uint32_t owner = t;
+    if (shared_tables)
+      for (uint32_t u = 0; u < t; u++)
+        if (ts[u].dtype == ts[t].dtype) {
+          owner = u;
+          break;
+        }
+    if (owner == t) {
+      uint64_t sum[256];
+      memcpy(sum, hist[t], sizeof(sum));
+      if (shared_tables)
+        for (uint32_t u = t + 1; u < n_tensors; u++)
+          if (ts[u].dtype == ts[t].dtype)
+            for (int k = 0; k < 256; k++) sum[k] += hist[u][k];
+      orc_normalise(sum, alphabet_of(ts[t].dtype), freqs + (size_t)t * 256);
+      table_of[t] = n_tables++;
+    } else {
+      memcpy(freqs + (size_t)t * 256, freqs + (size_t)owner * 256, 256 * sizeof(uint32_t));
+      table_of[t] = table_of[owner];
+    }
+  }
+
+  /* pass 2: chunk records */
   uint64_t c_glob = 0;
   for (uint32_t t = 0; t < n_tensors && rc == ORC_OK; t++) {
     uint32_t dt = ts[t].dtype;
     uint64_t n = n_symbols_of(dt, ts[t].nbytes);
     uint32_t alpha = alphabet_of(dt), W = group_of(dt);
-    uint8_t* coded = (uint8_t*)malloc(n ? n : 1);
-    uint8_t* raw = (uint8_t*)malloc(n ? n : 1);
-    if (!coded || !raw) {
-      rc = ORC_ENOMEM;
-      free(coded);
-      free(raw);
-      break;
-    }
-    orc_symbols(dt, ts[t].data, ts[t].nbytes, coded, raw);
-    uint64_t hist[256];
-    orc_histogram(coded, n, hist);
-    orc_normalise(hist, alpha, freqs + (size_t)t * 256);
-    uint64_t per = symbols_per_chunk(dt, chunk_bytes);
+    uint64_t per = symbols_per_chunk(dt, cbytes[t]);
     uint64_t nc = chunks_of(n, per);
     for (uint64_t c = 0; c < nc; c++, c_glob++) {
       uint64_t s0 = c * per;
@@ -496,8 +601,8 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
         rc = ORC_ENOMEM;
         break;
       }
-      rc = orc_encode_stream(coded + s0, len, freqs + (size_t)t * 256, alpha, L, W, states, words,
-                             cap, &nw, &A);
+      rc = orc_encode_stream(codeds[t] + s0, len, freqs + (size_t)t * 256, alpha, L, W, states,
+                             words, cap, &nw, &A);
       if (rc != ORC_OK) {
         free(words);
         break;
@@ -520,24 +625,28 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
       rec[c_glob] = r;
       rec_size[c_glob] = sz;
     }
-    if (has_raw(dt) && rc == ORC_OK) {
-      raws[t] = raw;
-      raw = NULL;
-    }
-    free(coded);
-    free(raw);
   }
 
-  /* pass 2: lay out the blob */
+  /* pass 3: lay out the blob */
   uint64_t off_desc = 64;
-  uint64_t off_tables = off_desc + 64ull * n_tensors;
+  uint64_t off_tables = off_desc + (uint64_t)ORC_DESC * n_tensors;
   uint64_t* freq_off = (uint64_t*)calloc(n_tensors, sizeof(uint64_t));
   uint64_t* raw_off_t = (uint64_t*)calloc(n_tensors, sizeof(uint64_t));
   if (!freq_off || !raw_off_t) rc = ORC_ENOMEM;
   uint64_t pos = off_tables;
   for (uint32_t t = 0; t < n_tensors && rc == ORC_OK; t++) {
-    freq_off[t] = pos;
-    pos += round16(2ull * alphabet_of(ts[t].dtype));
+    uint32_t owner = t;
+    for (uint32_t u = 0; u < t; u++)
+      if (table_of[u] == table_of[t]) {
+        owner = u;
+        break;
+      }
+    if (owner == t) {
+      freq_off[t] = pos;
+      pos += round16(2ull * alphabet_of(ts[t].dtype));
+    } else {
+      freq_off[t] = freq_off[owner];
+    }
   }
   uint64_t off_index = round16(pos);
   uint64_t off_records = round16(off_index + 4ull * (n_chunks + 1));
@@ -563,7 +672,7 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
     put16(b + 4, ORC_VERSION);
     put16(b + 6, 64);
     put32(b + 8, n_tensors);
-    put32(b + 12, 64);
+    put32(b + 12, ORC_DESC);
     put64(b + 16, n_chunks);
     put64(b + 24, total);
     put64(b + 32, off_index);
@@ -574,10 +683,10 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
     for (uint32_t t = 0; t < n_tensors; t++) {
       uint32_t dt = ts[t].dtype;
       uint64_t n = n_symbols_of(dt, ts[t].nbytes);
-      uint64_t nc = chunks_of(n, symbols_per_chunk(dt, chunk_bytes));
-      uint8_t* d = b + off_desc + 64ull * t;
+      uint64_t nc = chunks_of(n, symbols_per_chunk(dt, cbytes[t]));
+      uint8_t* d = b + off_desc + (uint64_t)ORC_DESC * t;
       put32(d + 0, dt);
-      put32(d + 4, chunk_bytes);
+      put32(d + 4, cbytes[t]);
       put64(d + 8, n);
       put64(d + 16, ts[t].nbytes);
       put64(d + 24, first);
@@ -589,6 +698,11 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
       put16(d + 46, 0);
       put64(d + 48, freq_off[t]);
       put64(d + 56, raw_off_t[t]);
+      put64(d + 64, ts[t].rows);
+      put64(d + 72, ts[t].cols);
+      put32(d + 80, tiled[t] ? tile_r : 0);
+      put32(d + 84, tiled[t] ? tile_c : 0);
+      put64(d + 88, 0);
       for (uint32_t s = 0; s < alphabet_of(dt); s++)
         put16(b + freq_off[t] + 2 * s, freqs[(size_t)t * 256 + s]);
       if (has_raw(dt)) memcpy(b + raw_off_t[t], raws[t], n);
@@ -603,12 +717,20 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
     put32(b + off_index + 4 * n_chunks, (uint32_t)(pos / 16));
   }
 
-  for (uint64_t c = 0; c < n_chunks; c++) free(rec[c]);
-  for (uint32_t t = 0; t < n_tensors; t++) free(raws[t]);
+  for (uint64_t c = 0; rec && c < n_chunks; c++) free(rec[c]);
+  for (uint32_t t = 0; t < n_tensors; t++) {
+    if (raws) free(raws[t]);
+    if (codeds) free(codeds[t]);
+  }
   free(rec);
   free(rec_size);
   free(freqs);
   free(raws);
+  free(codeds);
+  free(hist);
+  free(table_of);
+  free(cbytes);
+  free(tiled);
   free(freq_off);
   free(raw_off_t);
   if (rc != ORC_OK) {
@@ -624,14 +746,14 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
 /* Blob reading and validation.                                              */
 
 typedef struct {
-  uint32_t dtype, chunk_bytes, L, W, prob_bits, alphabet;
-  uint64_t n_sym, out_bytes, first_chunk, n_chunks, freq_off, raw_off;
+  uint32_t dtype, chunk_bytes, L, W, prob_bits, alphabet, tile_r, tile_c;
+  uint64_t n_sym, out_bytes, first_chunk, n_chunks, freq_off, raw_off, rows, cols;
 } orc_desc;
 
 static int read_desc(const uint8_t* b, uint64_t size, uint32_t t, orc_desc* d) {
   uint32_t n_t = get32(b + 8);
   if (t >= n_t) return ORC_EINVAL;
-  const uint8_t* p = b + 64 + 64ull * t;
+  const uint8_t* p = b + 64 + (uint64_t)ORC_DESC * t;
   d->dtype = get32(p + 0);
   d->chunk_bytes = get32(p + 4);
   d->n_sym = get64(p + 8);
@@ -644,6 +766,10 @@ static int read_desc(const uint8_t* b, uint64_t size, uint32_t t, orc_desc* d) {
   d->alphabet = get16(p + 44);
   d->freq_off = get64(p + 48);
   d->raw_off = get64(p + 56);
+  d->rows = get64(p + 64);
+  d->cols = get64(p + 72);
+  d->tile_r = get32(p + 80);
+  d->tile_c = get32(p + 84);
   if (!dtype_ok(d->dtype)) return ORC_EINVAL;
   if (d->prob_bits != ORC_PROB_BITS) return ORC_EINVAL;
   if (d->W != group_of(d->dtype) || d->alphabet != alphabet_of(d->dtype)) return ORC_EINVAL;
@@ -654,6 +780,12 @@ static int read_desc(const uint8_t* b, uint64_t size, uint32_t t, orc_desc* d) {
   if (has_raw(d->dtype) && d->out_bytes % 2) return ORC_EINVAL;
   if (d->n_chunks != chunks_of(d->n_sym, symbols_per_chunk(d->dtype, d->chunk_bytes)))
     return ORC_EINVAL;
+  if ((d->rows || d->cols) && d->rows * d->cols != d->n_sym) return ORC_EINVAL;
+  if (d->tile_r || d->tile_c) {
+    if (!tile_ok(d->dtype, d->rows, d->cols, d->tile_r, d->tile_c)) return ORC_EINVAL;
+    if (n_symbols_of(d->dtype, d->chunk_bytes) != (uint64_t)d->tile_r * d->tile_c)
+      return ORC_EINVAL;
+  }
   if (d->freq_off + 2ull * d->alphabet > size) return ORC_EINVAL;
   if (has_raw(d->dtype) && (d->raw_off > size || d->n_sym > size - d->raw_off))
     return ORC_EINVAL;
@@ -663,13 +795,13 @@ static int read_desc(const uint8_t* b, uint64_t size, uint32_t t, orc_desc* d) {
 static int check_header(const uint8_t* b, uint64_t size) {
   if (!b || size < 64) return ORC_EINVAL;
   if (get32(b) != ORC_MAGIC || get16(b + 4) != ORC_VERSION || get16(b + 6) != 64 ||
-      get32(b + 12) != 64)
+      get32(b + 12) != ORC_DESC)
     return ORC_EINVAL;
   if (get64(b + 24) != size) return ORC_EINVAL;
   uint32_t n_t = get32(b + 8);
   uint64_t n_c = get64(b + 16);
   uint64_t off_index = get64(b + 32), off_rec = get64(b + 40), off_raw = get64(b + 48);
-  if (n_t == 0 || 64 + 64ull * n_t > size) return ORC_EINVAL;
+  if (n_t == 0 || 64 + (uint64_t)ORC_DESC * n_t > size) return ORC_EINVAL;
   if (off_index > size || n_c + 1 > (size - off_index) / 4) return ORC_EINVAL;
   if (off_rec > off_raw || off_raw > size) return ORC_EINVAL;
   uint64_t first = 0;
@@ -725,7 +857,7 @@ static int decode_one(const uint8_t* b, uint64_t size, const orc_desc* d, uint64
   int rc = orc_decode_stream(states, A, words, nw, len, freq, d->alphabet, d->L, d->W, sym);
   if (rc == ORC_OK || rc == ORC_ECORRUPT) {
     const uint8_t* raw = has_raw(d->dtype) ? b + d->raw_off + s0 : NULL;
-    put_symbols(d->dtype, sym, raw, s0, len, out);
+    put_symbols(d->dtype, sym, raw, s0, len, out, d->tile_r ? d->cols : 0, d->tile_r, d->tile_c);
   }
   free(words);
   free(sym);
@@ -741,7 +873,7 @@ int orc_blob_tensors(const uint8_t* b, uint64_t size, uint32_t* n_tensors) {
 
 /* out_bytes, dtype and chunk count of tensor t */
 int orc_blob_tensor_info(const uint8_t* b, uint64_t size, uint32_t t, uint64_t* out_bytes,
-                         uint32_t* dtype, uint64_t* n_chunks) {
+                         uint32_t* dtype, uint64_t* n_chunks, uint32_t* tile) {
   int rc = check_header(b, size);
   if (rc) return rc;
   orc_desc d;
@@ -750,6 +882,11 @@ int orc_blob_tensor_info(const uint8_t* b, uint64_t size, uint32_t t, uint64_t* 
   *out_bytes = d.out_bytes;
   *dtype = d.dtype;
   *n_chunks = d.n_chunks;
+  if (tile) {
+    tile[0] = d.tile_r;
+    tile[1] = d.tile_c;
+    tile[2] = d.chunk_bytes;
+  }
   return ORC_OK;
 }
 

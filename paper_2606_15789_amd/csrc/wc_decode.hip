@@ -76,6 +76,12 @@ struct DevTensor {
   uint32_t kind;
   uint32_t alphabet;
   uint32_t lanes;        // rANS lanes per chunk: 64, or 32 (two chunks per wave)
+  uint32_t tiled;        // 1: chunk c is tile (c / ntc, c % ntc) of a row-major matrix
+  uint32_t tile_r;       // tile rows
+  uint32_t log_tc;       // log2 of the tile columns (symbols)
+  uint32_t ntc;          // tiles per band of tile_r rows
+  uint32_t pitch;        // decoded bytes of one matrix row
+  uint32_t tile_row_bytes;  // decoded bytes of one tile row
 };
 
 struct LaunchArgs {
@@ -250,10 +256,23 @@ __device__ __forceinline__ Chain<L> open_chain(const LaunchArgs& a, const DevTen
   c.x = __builtin_amdgcn_raw_buffer_load_b32(c.rs, (h ? c.rec1 : 0u) + 16u + 4u * sub, 0, 0);
   if (sub >= A_h) c.x = wc::kStateLow;  // lanes without symbols keep the initial state
   const uint64_t s0 = uint64_t(chunk0) * T.per;
-  const uint64_t out0 = uint64_t(chunk0) * T.chunk_bytes;
-  const uint32_t out_len = (uint32_t)min<uint64_t>(uint64_t(kH) * T.chunk_bytes, T.out_bytes - out0);
-  c.os = make_rsrc(reinterpret_cast<const void*>(T.dst + out0), out_len);
-  c.out1 = T.chunk_bytes;
+  if (T.tiled) {
+    // a tile's bytes start at its band's first row plus its column offset;
+    // the descriptor spans from the first tile's start to the last one's end
+    auto base = [&](uint32_t ch) {
+      return uint64_t(ch / T.ntc) * T.tile_r * T.pitch + uint64_t(ch % T.ntc) * T.tile_row_bytes;
+    };
+    const uint64_t out0 = base(chunk0);
+    c.out1 = c.n_exist == 2 ? (uint32_t)(base(chunk0 + 1) - out0) : 0u;
+    const uint32_t span = c.out1 + (T.tile_r - 1) * T.pitch + T.tile_row_bytes;
+    c.os = make_rsrc(reinterpret_cast<const void*>(T.dst + out0), span);
+  } else {
+    const uint64_t out0 = uint64_t(chunk0) * T.chunk_bytes;
+    const uint32_t out_len =
+        (uint32_t)min<uint64_t>(uint64_t(kH) * T.chunk_bytes, T.out_bytes - out0);
+    c.os = make_rsrc(reinterpret_cast<const void*>(T.dst + out0), out_len);
+    c.out1 = T.chunk_bytes;
+  }
   const uint32_t raw_len = T.kind == kSplit16
                                ? (uint32_t)min<uint64_t>(uint64_t(kH) * T.per, T.raw_padded - s0)
                                : 0u;
@@ -354,7 +373,7 @@ __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ 
 // Decode the chunk(s) of one wave, one rANS lane per wave lane.  G symbols
 // make one output dword; a lane-group is 4G symbols, 16 output bytes, so a
 // lane's share of a row is stored with one 16-byte store.
-template <int G, int L>
+template <int G, int L, bool kTiled>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
                                               const uint2* __restrict__ tab, uint32_t* ring) {
@@ -365,6 +384,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   constexpr uint32_t kRowSym = L * W;          // symbols of one half-row
   constexpr uint32_t kRowBytes = 16u * L;      // decoded bytes of one half-row
   constexpr uint32_t kRawRowBytes = 8u * L;    // raw bytes of one half-row (16-bit formats)
+  constexpr uint32_t kLogW = G == 2 ? 3 : (G == 4 ? 4 : 5);
   static_assert(kUnroll % kPipe == 0 && kUnroll % kGroupsPerRow == 0, "pipeline shape");
 
   Chain<L> c = open_chain<L>(a, T, chunk0, W, lane, ring);
@@ -383,6 +403,20 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   const uint32_t n_lane = kH == 2 && h ? c.n_c[kH - 1] : c.n_c[0];  // symbols of this lane's chunk
   const uint32_t groups = rows * kGroupsPerRow;
   const uint32_t out_v = (kH == 2 && h ? c.out1 : 0u) + sub * 16u;  // lane's output offset
+  const uint32_t half_v = kH == 2 && h ? c.out1 : 0u;                // tiled: half's base
+  const uint32_t tc_mask = (1u << T.log_tc) - 1u;
+  // output offset (voffset, soffset) of this lane's lane-group in row r: a
+  // byte run, or the lane-group's place in the tile of a row-major matrix
+  auto out_at = [&](uint32_t r, uint32_t& vo, uint32_t& so) {
+    if constexpr (kTiled) {
+      const uint32_t i0 = r * kRowSym + sub * W;
+      vo = half_v + (i0 >> T.log_tc) * T.pitch + ((i0 & tc_mask) >> kLogW) * 16u;
+      so = 0;
+    } else {
+      vo = out_v;
+      so = r * kRowBytes;
+    }
+  };
   const uint32_t raw_v = (kH == 2 && h ? c.raw1 : 0u) + sub * 8u;   // lane's raw offset
 
   // prologue: unit 0 committed now, then kPipe units in flight
@@ -438,17 +472,19 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
       using v4u = __attribute__((ext_vector_type(4))) unsigned int;
       const v4u o = {ow[0], ow[1], ow[2], ow[3]};
       const int nb = nv * 4 / G;  // valid output bytes of this lane
+      uint32_t vo, so;
+      out_at(r, vo, so);
       if (!kTail || nb == 16) {
-        __builtin_amdgcn_raw_buffer_store_b128(o, c.os, out_v, r * kRowBytes, kStreamStore);
+        __builtin_amdgcn_raw_buffer_store_b128(o, c.os, vo, so, kStreamStore);
       } else {
 #pragma unroll
         for (int d = 0; d < 4; d++) {
           if (4 * d + 4 <= nb) {
-            __builtin_amdgcn_raw_buffer_store_b32(ow[d], c.os, out_v + 4u * d, r * kRowBytes, 0);
+            __builtin_amdgcn_raw_buffer_store_b32(ow[d], c.os, vo + 4u * d, so, 0);
           } else {
             for (int b = 4 * d; b < nb; b++)
               __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(ow[d] >> (8 * (b - 4 * d))), c.os,
-                                                   out_v + b, r * kRowBytes, 0);
+                                                   vo + b, so, 0);
           }
         }
       }
@@ -503,19 +539,25 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
   const uint32_t per_wave = T.lanes == 32 ? 2u : 1u;
   const uint32_t chunk0 = ((wg - T.wg0) * kWaves + wave) * per_wave;
   if (chunk0 >= T.n_chunks) return;
-  if (T.lanes == 32) {
+  // instantiate one decoder per (format, lanes, tiling)
+  auto run = [&](auto gc, auto lc) {
+    constexpr int G = decltype(gc)::value, L = decltype(lc)::value;
+    if (T.tiled)
+      decode_chunks<G, L, true>(a, T, chunk0, lane, tab, ring[wave]);
+    else
+      decode_chunks<G, L, false>(a, T, chunk0, lane, tab, ring[wave]);
+  };
+  auto by_kind = [&](auto lc) {
     switch (T.kind) {
-      case kSplit16: decode_chunks<2, 32>(a, T, chunk0, lane, tab, ring[wave]); break;
-      case kByte: decode_chunks<4, 32>(a, T, chunk0, lane, tab, ring[wave]); break;
-      default: decode_chunks<8, 32>(a, T, chunk0, lane, tab, ring[wave]); break;
+      case kSplit16: run(std::integral_constant<int, 2>{}, lc); break;
+      case kByte: run(std::integral_constant<int, 4>{}, lc); break;
+      default: run(std::integral_constant<int, 8>{}, lc); break;
     }
-  } else {
-    switch (T.kind) {
-      case kSplit16: decode_chunks<2, 64>(a, T, chunk0, lane, tab, ring[wave]); break;
-      case kByte: decode_chunks<4, 64>(a, T, chunk0, lane, tab, ring[wave]); break;
-      default: decode_chunks<8, 64>(a, T, chunk0, lane, tab, ring[wave]); break;
-    }
-  }
+  };
+  if (T.lanes == 32)
+    by_kind(std::integral_constant<int, 32>{});
+  else
+    by_kind(std::integral_constant<int, 64>{});
 }
 
 }  // namespace
@@ -558,6 +600,17 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
       D.kind = wc::is_nibble(T.dtype) ? kNibble : (wc::is_byte(T.dtype) ? kByte : kSplit16);
       D.alphabet = T.alphabet;
       D.lanes = T.lanes;
+      D.tiled = T.tile_r ? 1u : 0u;
+      if (D.tiled) {
+        const uint64_t pitch = T.cols * 16 / T.group, trb = uint64_t(T.tile_c) * 16 / T.group;
+        // the widest output descriptor (two tiles of a 32-lane wave) must fit 32 bits
+        if ((2 * uint64_t(T.tile_r) + 1) * pitch >= (1ull << 31)) return WC_EUNSUPPORTED;
+        D.tile_r = T.tile_r;
+        D.log_tc = uint32_t(__builtin_ctz(T.tile_c));
+        D.ntc = uint32_t(T.cols / T.tile_c);
+        D.pitch = uint32_t(pitch);
+        D.tile_row_bytes = uint32_t(trb);
+      }
       const uint64_t per_group = uint64_t(kWaves) * (T.lanes == 32 ? 2u : 1u);
       wgs += (uint32_t)((T.n_chunks + per_group - 1) / per_group);
     }

@@ -9,6 +9,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <array>
 #include <atomic>
 #include <memory>
 #include <new>
@@ -280,6 +281,10 @@ wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out) {
     T.alphabet = ld16(d + 44);
     T.freq_off = ld64(d + 48);
     T.raw_off = ld64(d + 56);
+    T.rows = ld64(d + 64);
+    T.cols = ld64(d + 72);
+    T.tile_r = ld32(d + 80);
+    T.tile_c = ld32(d + 84);
     if (!dtype_ok(T.dtype)) return WC_EINVAL;
     if (pb != kProbBits || T.group != group_of(T.dtype) || T.alphabet != alphabet_of(T.dtype))
       return WC_EINVAL;
@@ -288,6 +293,10 @@ wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out) {
       return WC_EINVAL;
     if (has_raw(T.dtype) && T.out_bytes % 2) return WC_EINVAL;
     if (T.n_sym != symbols_of(T.dtype, T.out_bytes)) return WC_EINVAL;
+    if ((T.rows || T.cols) && T.rows * T.cols != T.n_sym) return WC_EINVAL;
+    if ((T.tile_r || T.tile_c) && (!tile_ok(T.dtype, T.rows, T.cols, T.tile_r, T.tile_c) ||
+                                   T.chunk_bytes != tile_bytes(T.dtype, T.tile_r, T.tile_c)))
+      return WC_EINVAL;
     uint64_t per = T.sym_per_chunk();
     if (T.n_chunks != (T.n_sym + per - 1) / per || T.first_chunk != first) return WC_EINVAL;
     if (T.freq_off < kHeaderBytes + uint64_t(kDescBytes) * nt ||
@@ -337,7 +346,7 @@ using namespace wc;
 
 extern "C" {
 
-int32_t wc_version(void) { return 1; }
+int32_t wc_version(void) { return 2; }
 
 wc_status wc_analyze(const wc_tensor* t, wc_stats* out) {
   if (!t || !out || (!t->host_ptr && t->nbytes)) return WC_EINVAL;
@@ -389,14 +398,20 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
   if (!ts || !prm || !out || n == 0 || n > 65536) return WC_EINVAL;
   *out = nullptr;
   const uint32_t CB = prm->chunk_bytes, L = prm->lanes;
+  const uint32_t TR = prm->tile_rows, TC = prm->tile_cols;
   if (CB < 256 || CB > (1u << 20) || CB % 256 || L < 1 || L > kMaxLanes ||
       prm->prob_bits != kProbBits)
     return WC_EINVAL;
+  if ((TR == 0) != (TC == 0) || (TC && !pow2(TC)) || prm->codebook > WC_CODEBOOK_LAYER)
+    return WC_EINVAL;
+  const bool shared = prm->codebook == WC_CODEBOOK_LAYER;
   for (uint32_t t = 0; t < n; t++) {
     uint32_t dt = uint32_t(ts[t].dtype);
     if (!dtype_ok(dt)) return WC_EINVAL;
     if (has_raw(dt) && ts[t].nbytes % 2) return WC_EINVAL;
     if (!ts[t].host_ptr && ts[t].nbytes) return WC_EINVAL;
+    if ((ts[t].rows || ts[t].cols) && ts[t].rows * ts[t].cols != symbols_of(dt, ts[t].nbytes))
+      return WC_EINVAL;
   }
   const unsigned threads = thread_count(prm->n_threads);
   try {
@@ -409,7 +424,13 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
     for (uint32_t t = 0; t < n; t++) {
       TensorInfo& T = P.tensors[t];
       T.dtype = uint32_t(ts[t].dtype);
-      T.chunk_bytes = CB;
+      T.rows = ts[t].rows;
+      T.cols = ts[t].cols;
+      if (tile_ok(T.dtype, T.rows, T.cols, TR, TC)) {
+        T.tile_r = TR;
+        T.tile_c = TC;
+      }
+      T.chunk_bytes = T.tile_r ? uint32_t(tile_bytes(T.dtype, TR, TC)) : CB;
       T.lanes = L;
       T.group = group_of(T.dtype);
       T.alphabet = alphabet_of(T.dtype);
@@ -423,17 +444,64 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
     if (nc_total >= 0xFFFFFFFFull) return WC_EINVAL;
     recs.resize(nc_total);
 
+    // symbols in coding order (tile-major for tiled tensors) and histograms
+    std::vector<std::vector<uint8_t>> codeds(n);
+    std::vector<std::array<uint64_t, 256>> hists(n);
     for (uint32_t t = 0; t < n; t++) {
       TensorInfo& T = P.tensors[t];
       const uint8_t* src = static_cast<const uint8_t*>(ts[t].host_ptr);
-      std::vector<uint8_t> coded(T.n_sym);
+      std::vector<uint8_t>& coded = codeds[t];
+      coded.resize(T.n_sym);
       if (has_raw(T.dtype)) raws[t].resize(T.n_sym);
       split_tensor(T.dtype, src, T.n_sym, coded.data(),
                    has_raw(T.dtype) ? raws[t].data() : nullptr, threads);
-      uint64_t hist[256];
-      histogram(coded.data(), T.n_sym, hist, threads);
-      freqs[t].assign(T.alphabet, 0);
-      normalise(hist, T.alphabet, freqs[t].data());
+      if (T.tile_r) {
+        // tile (a, b) is chunk a * (cols / tile_c) + b; its rows follow each other
+        const uint64_t ntc = T.cols / T.tile_c, per = uint64_t(T.tile_r) * T.tile_c;
+        std::vector<uint8_t> c2(T.n_sym), r2(has_raw(T.dtype) ? T.n_sym : 0);
+        parallel_for(T.n_chunks, threads, [&](uint64_t tile) {
+          const uint64_t a = tile / ntc, bcol = tile % ntc;
+          for (uint32_t i = 0; i < T.tile_r; i++) {
+            const uint64_t e = (a * T.tile_r + i) * T.cols + bcol * T.tile_c;
+            const uint64_t k = tile * per + uint64_t(i) * T.tile_c;
+            memcpy(c2.data() + k, coded.data() + e, T.tile_c);
+            if (!r2.empty()) memcpy(r2.data() + k, raws[t].data() + e, T.tile_c);
+          }
+        });
+        coded.swap(c2);
+        if (!r2.empty()) raws[t].swap(r2);
+      }
+      histogram(coded.data(), T.n_sym, hists[t].data(), threads);
+    }
+
+    // tables: one per tensor, or one per dtype normalised from the summed
+    // histogram of every tensor of that dtype (layer codebook)
+    std::vector<uint32_t> owner(n);
+    for (uint32_t t = 0; t < n; t++) {
+      owner[t] = t;
+      if (shared)
+        for (uint32_t u = 0; u < t; u++)
+          if (P.tensors[u].dtype == P.tensors[t].dtype) {
+            owner[t] = u;
+            break;
+          }
+      if (owner[t] != t) {
+        freqs[t] = freqs[owner[t]];
+        continue;
+      }
+      uint64_t sum[256];
+      memcpy(sum, hists[t].data(), sizeof(sum));
+      if (shared)
+        for (uint32_t u = t + 1; u < n; u++)
+          if (P.tensors[u].dtype == P.tensors[t].dtype)
+            for (int k = 0; k < 256; k++) sum[k] += hists[u][k];
+      freqs[t].assign(P.tensors[t].alphabet, 0);
+      normalise(sum, P.tensors[t].alphabet, freqs[t].data());
+    }
+
+    for (uint32_t t = 0; t < n; t++) {
+      TensorInfo& T = P.tensors[t];
+      const std::vector<uint8_t>& coded = codeds[t];
       EncSym tab[256];
       uint32_t cum = 0;
       for (uint32_t s = 0; s < 256; s++) {
@@ -451,11 +519,16 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
         uint64_t s0 = c * per, len = std::min(per, T.n_sym - s0);
         encode_chunk(coded.data() + s0, len, tab, L, T.group, recs[T.first_chunk + c], stack);
       });
+      std::vector<uint8_t>().swap(codeds[t]);
     }
 
     // layout
     uint64_t pos = kHeaderBytes + uint64_t(kDescBytes) * n;
     for (uint32_t t = 0; t < n; t++) {
+      if (owner[t] != t) {
+        P.tensors[t].freq_off = P.tensors[owner[t]].freq_off;
+        continue;
+      }
       P.tensors[t].freq_off = pos;
       pos += pad16(2ull * P.tensors[t].alphabet);
     }
@@ -499,6 +572,10 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
       st16(d + 44, T.alphabet);
       st64(d + 48, T.freq_off);
       st64(d + 56, T.raw_off);
+      st64(d + 64, T.rows);
+      st64(d + 72, T.cols);
+      st32(d + 80, T.tile_r);
+      st32(d + 84, T.tile_c);
       for (uint32_t s = 0; s < T.alphabet; s++) st16(b + T.freq_off + 2 * s, freqs[t][s]);
     }
     std::vector<uint64_t> rec_off(nc_total + 1);

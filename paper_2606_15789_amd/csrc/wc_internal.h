@@ -11,12 +11,12 @@
 namespace wc {
 
 constexpr uint32_t kMagic = 0x31424357u;  // "WCB1"
-constexpr uint32_t kVersion = 2;        // blob format version
+constexpr uint32_t kVersion = 3;        // blob format version
 constexpr uint32_t kProbBits = 12;        // b = 12 (Sec. VI-F)
 constexpr uint32_t kTableSize = 1u << kProbBits;
 constexpr uint32_t kStateLow = 1u << 16;  // lower end of the state interval
 constexpr uint32_t kHeaderBytes = 64;
-constexpr uint32_t kDescBytes = 64;
+constexpr uint32_t kDescBytes = 96;
 constexpr uint32_t kMaxLanes = 64;
 
 inline bool dtype_ok(uint32_t dt) { return dt >= WC_BF16 && dt <= WC_FP4_E2M1; }
@@ -31,11 +31,26 @@ inline uint64_t symbols_of(uint32_t dt, uint64_t bytes) {
   return is_nibble(dt) ? 2 * bytes : (is_byte(dt) ? bytes : bytes / 2);
 }
 inline uint64_t pad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
+inline bool pow2(uint64_t x) { return x && !(x & (x - 1)); }
+
+// A tensor is cut into tile_r x tile_c tiles (one chunk each) when its shape
+// is divided exactly, tile_c is a power of two covering whole lane-groups,
+// and a tile's decoded bytes are a valid chunk size.
+inline uint64_t tile_bytes(uint32_t dt, uint32_t tr, uint32_t tc) {
+  return uint64_t(tr) * tc * 16 / group_of(dt);
+}
+inline bool tile_ok(uint32_t dt, uint64_t rows, uint64_t cols, uint32_t tr, uint32_t tc) {
+  if (!tr || !tc || !rows || !cols || rows % tr || cols % tc || !pow2(tc) || tc < group_of(dt))
+    return false;
+  const uint64_t cb = tile_bytes(dt, tr, tc);
+  return cb >= 256 && cb <= (1u << 20) && cb % 256 == 0;
+}
 
 struct TensorInfo {
   uint32_t dtype = 0, chunk_bytes = 0, lanes = 0, group = 0, alphabet = 0;
+  uint32_t tile_r = 0, tile_c = 0;  // 0, 0: chunks are byte runs
   uint64_t n_sym = 0, out_bytes = 0, first_chunk = 0, n_chunks = 0;
-  uint64_t freq_off = 0, raw_off = 0;
+  uint64_t freq_off = 0, raw_off = 0, rows = 0, cols = 0;
   uint64_t sym_per_chunk() const { return symbols_of(dtype, chunk_bytes); }
 };
 

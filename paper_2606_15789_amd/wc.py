@@ -32,12 +32,16 @@ class WcError(RuntimeError):
 
 class _Tensor(C.Structure):
     _fields_ = [("host_ptr", C.c_void_p), ("nbytes", C.c_uint64), ("dtype", C.c_int32),
-                ("reserved", C.c_int32)]
+                ("reserved", C.c_int32), ("rows", C.c_uint64), ("cols", C.c_uint64)]
 
 
 class _Params(C.Structure):
     _fields_ = [("chunk_bytes", C.c_uint32), ("lanes", C.c_uint32), ("prob_bits", C.c_uint32),
-                ("n_threads", C.c_uint32)]
+                ("n_threads", C.c_uint32), ("tile_rows", C.c_uint32), ("tile_cols", C.c_uint32),
+                ("codebook", C.c_uint32), ("reserved", C.c_uint32)]
+
+
+CODEBOOKS = {"tensor": 0, "layer": 1}
 
 
 class _Stats(C.Structure):
@@ -96,7 +100,7 @@ def _bytes(data) -> np.ndarray:
 def analyze(dtype: str, data) -> dict:
     """wc_analyze: per-field histograms and empirical entropy of one tensor."""
     b = _bytes(data)
-    t = _Tensor(b.ctypes.data if b.size else None, b.size, DTYPES[dtype], 0)
+    t = _Tensor(b.ctypes.data if b.size else None, b.size, DTYPES[dtype], 0, 0, 0)
     st = _Stats()
     rc = lib().wc_analyze(C.byref(t), C.byref(st))
     if rc:
@@ -154,13 +158,20 @@ class Blob:
             pass
 
 
-def encode(tensors, chunk_bytes: int = 65536, lanes: int = 64, threads: int = 0) -> Blob:
-    """wc_encode of a list of (dtype, host array) pairs."""
-    keep = [_bytes(d) for _, d in tensors]
+def encode(tensors, chunk_bytes: int = 65536, lanes: int = 64, threads: int = 0, tile=(0, 0),
+           codebook: str = "tensor") -> Blob:
+    """wc_encode of a list of (dtype, host array[, (rows, cols)]) entries.
+
+    The shape is in symbol elements (16-bit words, bytes or nibbles); `tile`
+    = (tile_rows, tile_cols) cuts every tensor it divides into one chunk per
+    tile.  codebook "layer" shares one table among the tensors of a dtype.
+    """
+    keep = [_bytes(e[1]) for e in tensors]
     arr = (_Tensor * len(tensors))()
-    for i, ((dt, _), b) in enumerate(zip(tensors, keep)):
-        arr[i] = _Tensor(b.ctypes.data if b.size else None, b.size, DTYPES[dt], 0)
-    prm = _Params(chunk_bytes, lanes, 12, threads)
+    for i, (e, b) in enumerate(zip(tensors, keep)):
+        rows, cols = e[2] if len(e) > 2 and e[2] is not None else (0, 0)
+        arr[i] = _Tensor(b.ctypes.data if b.size else None, b.size, DTYPES[e[0]], 0, rows, cols)
+    prm = _Params(chunk_bytes, lanes, 12, threads, tile[0], tile[1], CODEBOOKS[codebook], 0)
     out = C.POINTER(_Blob)()
     rc = lib().wc_encode(arr, len(tensors), C.byref(prm), C.byref(out))
     if rc:

@@ -213,3 +213,43 @@ def test_null_error_pointer_and_stream(dev):
         outs = wc.decode_torch(blob, d, stream=s)
     s.synchronize()
     check_exact(pairs, blob, outs, oracle_full=False)
+
+
+def _shaped(ts):
+    return [(t.dtype, t.data, t.shape if len(t.shape) == 2 else None) for t in ts]
+
+
+@pytest.mark.parametrize("tile", [(32, 128), (64, 256), (128, 256), (1, 256)])
+@pytest.mark.parametrize("lanes", [64, 32])
+def test_tiled_workloads_scaled(dev, tile, lanes):
+    """2-D tiles (one chunk per tile) with a layer codebook: every tensor the
+    tile divides is written through the tile addressing, the rest stay flat."""
+    say("tiles", tile, "lanes", lanes)
+    ts = synth.config(2, div=8) + synth.config(3, div=8) + synth.config(7, div=8)
+    pairs = _shaped(ts)
+    blob = wc.encode(pairs, chunk_bytes=16384, lanes=lanes, tile=tile, codebook="layer")
+    assert any(i["tile"] == tile for i in oracle.tensor_info(blob.tobytes()))
+    check_exact([(d, a) for d, a, _ in pairs], blob, gpu_decode(blob, dev))
+
+
+def test_tiled_full_size_70b_layer(dev):
+    """The 70B layer in 128 x 256 tiles (64 KiB each) with one bf16 codebook."""
+    ts = synth.config(5)
+    pairs = _shaped(ts)
+    blob = wc.encode(pairs, lanes=64, tile=(128, 256), codebook="layer")
+    outs = gpu_decode(blob, dev)
+    raw = blob.tobytes()
+    info = oracle.tensor_info(raw)
+    rng = np.random.default_rng(5)
+    for t, ((dt, data, shape), out) in enumerate(zip(pairs, outs)):
+        orig = torch.from_numpy(np.ascontiguousarray(data).view(np.uint8).reshape(-1)).to(dev)
+        assert torch.equal(out, orig), t
+        got = out.cpu().numpy().view(np.uint16).reshape(shape)
+        ntc = shape[1] // 256
+        for c in _sample_chunks(info[t]["n_chunks"], 6, rng):
+            ref = oracle.decode_chunks(raw, t, c, c + 1).view(np.uint16).reshape(shape)
+            a, b = divmod(c, ntc)
+            rs, cs = slice(a * 128, (a + 1) * 128), slice(b * 256, (b + 1) * 256)
+            assert np.array_equal(got[rs, cs], ref[rs, cs]), (t, c)
+    del outs
+    torch.cuda.empty_cache()

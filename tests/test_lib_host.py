@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (wc_\w+)", out))
     assert set(names) <= exported
-    assert lib.wc_version() == 1
+    assert lib.wc_version() == 2
 
 
 @pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16), (6, 8), (7, 8),
@@ -133,3 +133,27 @@ def test_decode_rejects_before_any_launch():
     assert e.value.rc == -1
     with pytest.raises(wc.WcError):
         wc.decode(b, 0, [1])                      # no device blob
+
+
+@pytest.mark.parametrize("tile", [(32, 128), (64, 256), (128, 256)])
+@pytest.mark.parametrize("codebook", ["tensor", "layer"])
+@pytest.mark.parametrize("lanes", [64, 32])
+def test_tiled_blobs_identical_to_oracle(tile, codebook, lanes):
+    ts = synth.config(2, div=8) + synth.config(3, div=8)
+    pairs = [(t.dtype, t.data, t.shape if len(t.shape) == 2 else None) for t in ts]
+    a = wc.encode(pairs, chunk_bytes=16384, lanes=lanes, tile=tile, codebook=codebook)
+    b = oracle.encode(pairs, chunk_bytes=16384, lanes=lanes, tile=tile, codebook=codebook)
+    assert a.tobytes() == b
+    info = oracle.tensor_info(b)
+    assert any(i["tile"] == tile for i in info)            # some tensors were tiled
+
+
+def test_open_rejects_inconsistent_tile_fields():
+    d = np.arange(64 * 256, dtype=np.uint16).reshape(64, 256)
+    raw = bytearray(oracle.encode([("bf16", d, (64, 256))], tile=(32, 128)))
+    assert wc.open_blob(bytes(raw)).n_chunks == 4
+    for off, val in ((64 + 80, 33), (64 + 84, 96), (64 + 72, 255)):   # rows, tile_c, cols
+        bad = bytearray(raw)
+        struct.pack_into("<I", bad, off, val)
+        with pytest.raises(wc.WcError):
+            wc.open_blob(bytes(bad))

@@ -1,0 +1,130 @@
+"""Oracle: 2-D tile chunks and the layer codebook (Sec. IV-A, V-B, VI-F).
+
+The tile definition is pinned with numpy slicing, independently of the
+oracle's own index arithmetic: decoding one tile into a sentinel-filled
+buffer must rebuild exactly W[a*tr:(a+1)*tr, b*tc:(b+1)*tc] and nothing else.
+The shared table is pinned against the (separately pinned) histogram and
+normaliser applied to the concatenated symbols of every tensor of the dtype.
+"""
+import struct
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_15789_amd import synth
+
+DESC = 96
+
+
+def _desc(blob, t):
+    d = 64 + DESC * t
+    return {"chunk_bytes": struct.unpack_from("<I", blob, d + 4)[0],
+            "freq_off": struct.unpack_from("<Q", blob, d + 48)[0],
+            "rows": struct.unpack_from("<Q", blob, d + 64)[0],
+            "cols": struct.unpack_from("<Q", blob, d + 72)[0],
+            "tile": struct.unpack_from("<II", blob, d + 80)}
+
+
+def _matrix(dtype, rows, cols, seed):
+    """Storage array and symbol-element shape of a random matrix."""
+    rng = np.random.default_rng(seed)
+    if dtype in ("bf16", "fp16"):
+        w = (rng.normal(0, 0.02, (rows, cols)).astype(np.float32).view(np.uint32) >> 16)
+        return w.astype(np.uint16), (rows, cols)
+    if dtype in ("u4", "fp4_e2m1"):
+        return rng.integers(0, 256, (rows, cols // 2)).astype(np.uint8), (rows, cols)
+    return np.clip(rng.normal(128, 12, (rows, cols)), 0, 255).astype(np.uint8), (rows, cols)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp16", "u8", "u4", "fp8_e4m3", "fp4_e2m1"])
+@pytest.mark.parametrize("tile", [(32, 128), (64, 256), (16, 512)])
+def test_tile_decodes_to_its_slice(dtype, tile):
+    tr, tc = tile
+    rows, cols = 4 * tr, 3 * tc
+    data, shape = _matrix(dtype, rows, cols, 1)
+    blob = oracle.encode([(dtype, data, shape)], chunk_bytes=65536, lanes=64, tile=tile)
+    info = oracle.tensor_info(blob)[0]
+    assert info["tile"] == tile and info["n_chunks"] == 12
+    assert _desc(blob, 0)["rows"] == rows and _desc(blob, 0)["cols"] == cols
+    nib = dtype in ("u4", "fp4_e2m1")
+    for c in (0, 1, 4, 11):
+        a, b = divmod(c, cols // tc)
+        buf = np.full(data.nbytes, 0xA5, np.uint8)
+        oracle.decode_chunks(blob, 0, c, c + 1, out=buf)
+        got = buf.view(data.dtype).reshape(data.shape)
+        cs = slice(b * tc // 2, (b + 1) * tc // 2) if nib else slice(b * tc, (b + 1) * tc)
+        rs = slice(a * tr, (a + 1) * tr)
+        assert np.array_equal(got[rs, cs], data[rs, cs]), (dtype, tile, c)
+        mask = np.ones(data.shape, bool)
+        mask[rs, cs] = False
+        sentinel = np.full(1, 0xA5A5, np.uint16)[0] if data.dtype == np.uint16 else 0xA5
+        assert np.all(got[mask] == sentinel), (dtype, tile, c)
+    assert np.array_equal(oracle.decode(blob)[0], data.view(np.uint8).reshape(-1))
+
+
+def test_untileable_tensors_stay_flat():
+    """A shape the tile does not divide, or no shape, keeps 1-D chunks."""
+    d1, s1 = _matrix("bf16", 100, 256, 2)           # 100 rows: not a multiple of 64
+    d2, s2 = _matrix("u8", 64, 96, 3)               # 96 cols: not a multiple of 256
+    d3, _ = _matrix("bf16", 64, 256, 4)             # no shape given
+    d4, s4 = _matrix("u4", 64, 256, 5)              # tiled
+    blob = oracle.encode([("bf16", d1, s1), ("u8", d2, s2), ("bf16", d3), ("u4", d4, s4)],
+                         chunk_bytes=4096, tile=(64, 256))
+    info = oracle.tensor_info(blob)
+    assert [i["tile"] for i in info] == [(0, 0), (0, 0), (0, 0), (64, 256)]
+    assert [i["chunk_bytes"] for i in info] == [4096, 4096, 4096, 64 * 256 // 2]
+    for (d, out) in zip((d1, d2, d3, d4), oracle.decode(blob)):
+        assert np.array_equal(out, d.view(np.uint8).reshape(-1))
+
+
+def test_tile_narrower_than_a_lane_group_is_flat():
+    d, s = _matrix("u4", 64, 256, 6)                # int4 lane-group: 32 nibbles
+    blob = oracle.encode([("u4", d, s)], chunk_bytes=4096, tile=(64, 16))
+    assert oracle.tensor_info(blob)[0]["tile"] == (0, 0)
+
+
+def test_bad_tile_parameters_and_shapes_are_rejected():
+    d, s = _matrix("bf16", 64, 256, 7)
+    with pytest.raises(oracle.OracleError):
+        oracle.encode([("bf16", d, s)], tile=(64, 0))
+    with pytest.raises(oracle.OracleError):
+        oracle.encode([("bf16", d, s)], tile=(64, 96))   # not a power of two
+    with pytest.raises(oracle.OracleError):
+        oracle.encode([("bf16", d, (64, 255))], tile=(64, 256))   # shape != element count
+
+
+def test_layer_codebook_shares_one_table_per_dtype():
+    ts = synth.config(3, div=16)                    # int4 codes, fp16 scales, bf16 norms
+    pairs = [(t.dtype, t.data) for t in ts]
+    blob = oracle.encode(pairs, codebook="layer")
+    offs = {}
+    for t, (dt, _) in enumerate(pairs):
+        offs.setdefault(dt, set()).add(_desc(blob, t)["freq_off"])
+    assert all(len(v) == 1 for v in offs.values())
+    assert len({o for v in offs.values() for o in v}) == 3
+    for dt in offs:
+        syms = np.concatenate([oracle.symbols(d, a)[0] for d, a in pairs if d == dt])
+        alpha = 16 if dt == "u4" else 256
+        want = oracle.normalise(oracle.histogram(syms)[:alpha], alpha)
+        off = next(iter(offs[dt]))
+        got = np.frombuffer(blob, np.uint16, count=alpha, offset=off)
+        assert np.array_equal(got, want), dt
+    for (dt, d), out in zip(pairs, oracle.decode(blob)):
+        assert np.array_equal(out, np.ascontiguousarray(d).view(np.uint8).reshape(-1))
+    per_tensor = oracle.encode(pairs)
+    assert len({_desc(per_tensor, t)["freq_off"] for t in range(len(pairs))}) == len(pairs)
+
+
+def test_tiled_index_matches_the_per_tile_metadata_term():
+    """Table 3 charges 4 B per tile; the index holds one u32 per tile plus an
+    end sentinel."""
+    d, s = _matrix("bf16", 256, 1024, 8)
+    for tr, tc in ((32, 128), (64, 256)):
+        blob = oracle.encode([("bf16", d, s)], tile=(tr, tc), codebook="layer")
+        off_index, off_rec = struct.unpack_from("<QQ", blob, 32)
+        n_tiles = (256 // tr) * (1024 // tc)
+        index_bytes = 4 * (n_tiles + 1)
+        assert off_rec - off_index == (index_bytes + 15) // 16 * 16
+        closed = oracle.metadata_bytes(256, 1024, tr, tc, 12) - (1 << 12) * 4
+        assert index_bytes - 4 == closed
