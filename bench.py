@@ -56,11 +56,11 @@ WORKLOADS = {WORKLOAD_DEFAULT: 5, "bf16-matrix-4096": 1, "llama3-8b-layer-bf16":
 ROTATE_BYTES = 1 << 30   # resident bytes the small workloads rotate over
 
 # HBM bytes per launch of the 70B-layer decode from rocprofv3 --pmc FETCH_SIZE and
-# WRITE_SIZE runs, each scaled by the same counter on a 470 MB device copy (FETCH_SIZE
+# WRITE_SIZE runs, each scaled by the same counter on a 512 MiB device copy (FETCH_SIZE
 # reads half the copied bytes: factor 2.0; WRITE_SIZE is exact).  Valid only for
 # the kernel source they were taken on (sha256 prefix); otherwise reported as null.
-COUNTED_TRAFFIC = {"kernel_sha256": "0db788798814ef10", "fetch_bytes": 1142385792,
-                   "write_bytes": 1711291296, "chunk_bytes": 65536, "lanes": 64}
+COUNTED_TRAFFIC = {"kernel_sha256": "e94d6c1053cea04e", "fetch_bytes": 1142324288,
+                   "write_bytes": 1711277680, "chunk_bytes": 65536, "lanes": 64}
 
 
 def log(*a):
