@@ -77,8 +77,10 @@ def lib():
                                         C.c_uint64, C.c_void_p, C.c_uint32, C.c_uint32,
                                         C.c_uint32, C.c_void_p]
         L.orc_encode_blob.argtypes = [C.POINTER(_Tensor), C.c_uint32, C.c_uint32, C.c_uint32,
-                                      C.c_uint32, C.c_uint32, C.c_uint32,
+                                      C.c_uint32, C.c_uint32, C.c_uint32, C.c_uint32,
                                       C.POINTER(u8p), C.POINTER(C.c_uint64)]
+        L.orc_gemv_bf16.argtypes = [C.c_void_p, C.c_uint64, C.c_uint64, C.c_void_p, C.c_uint32,
+                                    C.c_void_p, C.c_void_p]
         L.orc_free.argtypes = [C.c_void_p]
         L.orc_free.restype = None
         L.orc_blob_tensors.argtypes = [C.c_void_p, C.c_uint64, C.POINTER(C.c_uint32)]
@@ -213,13 +215,14 @@ def decode_stream(states, words, n: int, freq, lanes: int, group: int):
 # --- blobs -------------------------------------------------------------------
 
 def encode(tensors, chunk_bytes: int = 65536, lanes: int = 64, tile=(0, 0),
-           codebook: str = "tensor") -> bytes:
+           codebook: str = "tensor", tile_order: int = 0) -> bytes:
     """Blob bytes of a list of (dtype, storage array[, (rows, cols)]) entries.
 
     `tile` = (rows, cols) cuts every tensor whose shape (in symbol elements:
     16-bit words, bytes or nibbles) the tile divides into one chunk per tile;
-    the others use `chunk_bytes`.  codebook "layer" shares one table among all
-    tensors of a dtype.
+    the others use `chunk_bytes`.  tile_order 0 keeps each tile row-major, 1
+    lists its lane-groups k-block by k-block (column blocks).  codebook
+    "layer" shares one table among all tensors of a dtype.
     """
     keep = []
     arr = (_Tensor * len(tensors))()
@@ -235,8 +238,8 @@ def encode(tensors, chunk_bytes: int = 65536, lanes: int = 64, tile=(0, 0),
     out = C.POINTER(C.c_uint8)()
     size = C.c_uint64()
     shared = {"tensor": 0, "layer": 1}[codebook]
-    rc = lib().orc_encode_blob(arr, len(tensors), chunk_bytes, lanes, tile[0], tile[1], shared,
-                               C.byref(out), C.byref(size))
+    rc = lib().orc_encode_blob(arr, len(tensors), chunk_bytes, lanes, tile[0], tile[1],
+                               tile_order, shared, C.byref(out), C.byref(size))
     if rc:
         raise OracleError(rc, "encode")
     try:
@@ -258,13 +261,14 @@ def tensor_info(blob):
     info = []
     for t in range(n.value):
         ob, dt, nc = C.c_uint64(), C.c_uint32(), C.c_uint64()
-        tile = (C.c_uint32 * 3)()
+        tile = (C.c_uint32 * 4)()
         rc = lib().orc_blob_tensor_info(_ptr(b), b.size, t, C.byref(ob), C.byref(dt),
                                         C.byref(nc), tile)
         if rc:
             raise OracleError(rc, "tensor info")
         info.append({"out_bytes": ob.value, "dtype": dt.value, "n_chunks": nc.value,
-                     "tile": (tile[0], tile[1]), "chunk_bytes": tile[2]})
+                     "tile": (tile[0], tile[1]), "chunk_bytes": tile[2],
+                     "tile_order": tile[3]})
     return info
 
 
@@ -295,3 +299,19 @@ def decode_chunks(blob, tensor: int, c0: int, c1: int, out: np.ndarray | None = 
 def metadata_bytes(rows: int, cols: int, tile_r: int, tile_c: int, b: int = 12) -> float:
     return lib().orc_metadata_bytes(rows, cols, tile_r, tile_c, b)
 
+
+
+def gemv_bf16(w, x):
+    """(y, sum |x w|) in fp64: y[m, n] = sum_k x[m, k] * w[n, k] for bf16 storage
+    words w (rows x cols) and x (M x cols), summed in k order."""
+    w = np.ascontiguousarray(w, dtype=np.uint16)
+    x = np.ascontiguousarray(x, dtype=np.uint16)
+    rows, cols = w.shape
+    M = x.shape[0]
+    assert x.shape[1] == cols
+    y = np.empty((M, rows), np.float64)
+    a = np.empty((M, rows), np.float64)
+    rc = lib().orc_gemv_bf16(_ptr(w), rows, cols, _ptr(x), M, _ptr(y), _ptr(a))
+    if rc:
+        raise OracleError(rc, "gemv")
+    return y, a

@@ -119,18 +119,29 @@ static uint64_t n_symbols_of(uint32_t dt, uint64_t nbytes) {
 
 static int pow2(uint64_t x) { return x && !(x & (x - 1)); }
 
-static int tile_ok(uint32_t dt, uint64_t rows, uint64_t cols, uint32_t tr, uint32_t tc) {
-  if (!tr || !tc || !rows || !cols) return 0;
+/* Within a tile, order 0 is row-major.  Order 1 (column blocks) lists the   */
+/* tile's lane-groups of W elements k-block by k-block, every row of the     */
+/* tile per block: lane-group g is row g mod tile_r, columns                 */
+/* [(g div tile_r) W, (g div tile_r) W + W).  With tile_r rANS lanes, lane l */
+/* then always decodes row l, which lets a decoder form whole dot products   */
+/* per lane.  Order 1 needs tile_r to be a power of two.                     */
+static int tile_ok(uint32_t dt, uint64_t rows, uint64_t cols, uint32_t tr, uint32_t tc,
+                   uint32_t order) {
+  if (!tr || !tc || !rows || !cols || order > 1) return 0;
   if (rows % tr || cols % tc || !pow2(tc) || tc < group_of(dt)) return 0;
+  if (order == 1 && !pow2(tr)) return 0;
   uint64_t cb = (uint64_t)tr * tc * 16 / group_of(dt); /* 16 bytes per lane-group */
   return cb >= 256 && cb <= (1u << 20) && cb % 256 == 0;
 }
 
 /* Element index (row-major in the tensor) of tile-major symbol k. */
-static uint64_t tile_element(uint64_t k, uint64_t cols, uint32_t tr, uint32_t tc) {
+static uint64_t tile_element(uint64_t k, uint64_t cols, uint32_t tr, uint32_t tc, uint32_t order,
+                             uint32_t W) {
   uint64_t per = (uint64_t)tr * tc, t = k / per, in = k % per;
   uint64_t ntc = cols / tc, a = t / ntc, bcol = t % ntc;
-  return (a * tr + in / tc) * cols + bcol * tc + in % tc;
+  if (order == 0) return (a * tr + in / tc) * cols + bcol * tc + in % tc;
+  uint64_t g = in / W, kb = g / tr, n = g % tr;
+  return (a * tr + n) * cols + bcol * tc + kb * W + in % W;
 }
 
 /*
@@ -160,11 +171,12 @@ int orc_symbols(uint32_t dt, const uint8_t* data, uint64_t nbytes, uint8_t* code
 
 /* Inverse of orc_symbols: write tensor bytes for symbol range [s0, s0+n). */
 /* Symbol s0 + k is written to element map(s0 + k): the identity, or the     */
-/* tile-major order when cols > 0.                                           */
+/* tile order when cols > 0.                                                 */
 static void put_symbols(uint32_t dt, const uint8_t* coded, const uint8_t* raw, uint64_t s0,
-                        uint64_t n, uint8_t* out, uint64_t cols, uint32_t tr, uint32_t tc) {
+                        uint64_t n, uint8_t* out, uint64_t cols, uint32_t tr, uint32_t tc,
+                        uint32_t order) {
   for (uint64_t k = 0; k < n; k++) {
-    uint64_t i = cols ? tile_element(s0 + k, cols, tr, tc) : s0 + k;
+    uint64_t i = cols ? tile_element(s0 + k, cols, tr, tc, order, group_of(dt)) : s0 + k;
     if (is_byte(dt)) {
       out[i] = coded[k];
     } else if (is_nibble(dt)) {
@@ -471,13 +483,14 @@ static uint64_t chunks_of(uint64_t n_sym, uint64_t per) { return (n_sym + per - 
 void orc_free(void* p) { free(p); }
 
 int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_bytes, uint32_t L,
-                    uint32_t tile_r, uint32_t tile_c, uint32_t shared_tables,
+                    uint32_t tile_r, uint32_t tile_c, uint32_t tile_order, uint32_t shared_tables,
                     uint8_t** blob_out, uint64_t* size_out) {
   if (!ts || !blob_out || !size_out) return ORC_EINVAL;
   if (n_tensors == 0 || n_tensors > 4096) return ORC_EINVAL;
   if (chunk_bytes < 256 || chunk_bytes > (1u << 20) || chunk_bytes % 256) return ORC_EINVAL;
   if (L < 1 || L > 64) return ORC_EINVAL;
-  if ((tile_r == 0) != (tile_c == 0) || (tile_c && !pow2(tile_c))) return ORC_EINVAL;
+  if ((tile_r == 0) != (tile_c == 0) || (tile_c && !pow2(tile_c)) || tile_order > 1)
+    return ORC_EINVAL;
 
   for (uint32_t t = 0; t < n_tensors; t++) {
     uint32_t dt = ts[t].dtype;
@@ -499,7 +512,7 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
   for (uint32_t t = 0; t < n_tensors; t++) {
     uint32_t dt = ts[t].dtype;
     uint64_t n = n_symbols_of(dt, ts[t].nbytes);
-    tiled[t] = (uint8_t)tile_ok(dt, ts[t].rows, ts[t].cols, tile_r, tile_c);
+    tiled[t] = (uint8_t)tile_ok(dt, ts[t].rows, ts[t].cols, tile_r, tile_c, tile_order);
     cbytes[t] = tiled[t] ? (uint32_t)((uint64_t)tile_r * tile_c * 16 / group_of(dt)) : chunk_bytes;
     n_chunks += chunks_of(n, symbols_per_chunk(dt, cbytes[t]));
   }
@@ -540,7 +553,7 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
         break;
       }
       for (uint64_t k = 0; k < n; k++) {
-        uint64_t e = tile_element(k, ts[t].cols, tile_r, tile_c);
+        uint64_t e = tile_element(k, ts[t].cols, tile_r, tile_c, tile_order, group_of(dt));
         c2[k] = coded[e];
         r2[k] = raw[e];
       }
@@ -702,7 +715,8 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
       put64(d + 72, ts[t].cols);
       put32(d + 80, tiled[t] ? tile_r : 0);
       put32(d + 84, tiled[t] ? tile_c : 0);
-      put64(d + 88, 0);
+      put32(d + 88, tiled[t] ? tile_order : 0);
+      put32(d + 92, 0);
       for (uint32_t s = 0; s < alphabet_of(dt); s++)
         put16(b + freq_off[t] + 2 * s, freqs[(size_t)t * 256 + s]);
       if (has_raw(dt)) memcpy(b + raw_off_t[t], raws[t], n);
@@ -746,7 +760,7 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
 /* Blob reading and validation.                                              */
 
 typedef struct {
-  uint32_t dtype, chunk_bytes, L, W, prob_bits, alphabet, tile_r, tile_c;
+  uint32_t dtype, chunk_bytes, L, W, prob_bits, alphabet, tile_r, tile_c, tile_order;
   uint64_t n_sym, out_bytes, first_chunk, n_chunks, freq_off, raw_off, rows, cols;
 } orc_desc;
 
@@ -770,6 +784,7 @@ static int read_desc(const uint8_t* b, uint64_t size, uint32_t t, orc_desc* d) {
   d->cols = get64(p + 72);
   d->tile_r = get32(p + 80);
   d->tile_c = get32(p + 84);
+  d->tile_order = get32(p + 88);
   if (!dtype_ok(d->dtype)) return ORC_EINVAL;
   if (d->prob_bits != ORC_PROB_BITS) return ORC_EINVAL;
   if (d->W != group_of(d->dtype) || d->alphabet != alphabet_of(d->dtype)) return ORC_EINVAL;
@@ -781,8 +796,10 @@ static int read_desc(const uint8_t* b, uint64_t size, uint32_t t, orc_desc* d) {
   if (d->n_chunks != chunks_of(d->n_sym, symbols_per_chunk(d->dtype, d->chunk_bytes)))
     return ORC_EINVAL;
   if ((d->rows || d->cols) && d->rows * d->cols != d->n_sym) return ORC_EINVAL;
+  if (!(d->tile_r || d->tile_c) && d->tile_order) return ORC_EINVAL;
   if (d->tile_r || d->tile_c) {
-    if (!tile_ok(d->dtype, d->rows, d->cols, d->tile_r, d->tile_c)) return ORC_EINVAL;
+    if (!tile_ok(d->dtype, d->rows, d->cols, d->tile_r, d->tile_c, d->tile_order))
+      return ORC_EINVAL;
     if (n_symbols_of(d->dtype, d->chunk_bytes) != (uint64_t)d->tile_r * d->tile_c)
       return ORC_EINVAL;
   }
@@ -857,7 +874,8 @@ static int decode_one(const uint8_t* b, uint64_t size, const orc_desc* d, uint64
   int rc = orc_decode_stream(states, A, words, nw, len, freq, d->alphabet, d->L, d->W, sym);
   if (rc == ORC_OK || rc == ORC_ECORRUPT) {
     const uint8_t* raw = has_raw(d->dtype) ? b + d->raw_off + s0 : NULL;
-    put_symbols(d->dtype, sym, raw, s0, len, out, d->tile_r ? d->cols : 0, d->tile_r, d->tile_c);
+    put_symbols(d->dtype, sym, raw, s0, len, out, d->tile_r ? d->cols : 0, d->tile_r, d->tile_c,
+                d->tile_order);
   }
   free(words);
   free(sym);
@@ -886,6 +904,7 @@ int orc_blob_tensor_info(const uint8_t* b, uint64_t size, uint32_t t, uint64_t* 
     tile[0] = d.tile_r;
     tile[1] = d.tile_c;
     tile[2] = d.chunk_bytes;
+    tile[3] = d.tile_order;
   }
   return ORC_OK;
 }
@@ -933,4 +952,35 @@ double orc_metadata_bytes(uint64_t rows, uint64_t cols, uint64_t tile_r, uint64_
                           uint32_t b) {
   double tiles = ((double)rows / (double)tile_r) * ((double)cols / (double)tile_c);
   return 4.0 * tiles + (double)(1ull << b) * 4.0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* What the fused decode-GEMM path computes (Alg. 1 / 3: the decoded tile is */
+/* multiplied with the activations): y[m][n] = sum_k x[m][k] * w[n][k] for  */
+/* bf16 w (rows x cols, row-major storage words) and bf16 x (M x cols), in  */
+/* fp64, summed in k order.  abs_out[m][n] = sum_k |x[m][k] * w[n][k]|, the */
+/* scale of any floating-point summation error.                             */
+
+static double bf16_value(uint16_t h) {
+  uint32_t u = (uint32_t)h << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return (double)f;
+}
+
+int orc_gemv_bf16(const uint16_t* w, uint64_t rows, uint64_t cols, const uint16_t* x, uint32_t M,
+                  double* y, double* abs_out) {
+  if (!w || !x || !y || M == 0) return ORC_EINVAL;
+  for (uint32_t m = 0; m < M; m++)
+    for (uint64_t n = 0; n < rows; n++) {
+      double s = 0.0, a = 0.0;
+      for (uint64_t k = 0; k < cols; k++) {
+        double p = bf16_value(x[(uint64_t)m * cols + k]) * bf16_value(w[n * cols + k]);
+        s += p;
+        a += fabs(p);
+      }
+      y[(uint64_t)m * rows + n] = s;
+      if (abs_out) abs_out[(uint64_t)m * rows + n] = a;
+    }
+  return ORC_OK;
 }

@@ -128,3 +128,67 @@ def test_tiled_index_matches_the_per_tile_metadata_term():
         assert off_rec - off_index == (index_bytes + 15) // 16 * 16
         closed = oracle.metadata_bytes(256, 1024, tr, tc, 12) - (1 << 12) * 4
         assert index_bytes - 4 == closed
+
+
+def _raw_bytes(words):
+    w = words.astype(np.uint32)
+    return (((w >> 8) & 0x80) | (w & 0x7F)).astype(np.uint8)
+
+
+@pytest.mark.parametrize("order", [0, 1])
+@pytest.mark.parametrize("tile", [(64, 256), (32, 128)])
+def test_tile_symbol_order_in_the_raw_region(order, tile):
+    """The raw bytes of a tile appear in the tile's symbol order: row-major
+    (order 0), or k-block by k-block with every row of the tile per block
+    (order 1, lane-groups of W = 8 bf16) -- computed here with numpy."""
+    tr, tc = tile
+    data, shape = _matrix("bf16", 2 * tr, 3 * tc, 11)
+    blob = oracle.encode([("bf16", data, shape)], tile=tile, tile_order=order)
+    info = oracle.tensor_info(blob)[0]
+    assert info["tile_order"] == order
+    raw_off = struct.unpack_from("<Q", blob, 64 + 56)[0]
+    per = tr * tc
+    for c in (0, 2, 5):
+        a, b = divmod(c, 3)
+        t = data[a * tr:(a + 1) * tr, b * tc:(b + 1) * tc]
+        seq = t.reshape(-1) if order == 0 else t.reshape(tr, tc // 8, 8).transpose(1, 0, 2).reshape(-1)
+        got = np.frombuffer(blob, np.uint8, count=per, offset=raw_off + c * per)
+        assert np.array_equal(got, _raw_bytes(seq)), (order, tile, c)
+    assert np.array_equal(oracle.decode(blob)[0], data.view(np.uint8).reshape(-1))
+
+
+def test_column_order_needs_power_of_two_tile_rows():
+    d, s = _matrix("bf16", 96, 256, 12)
+    blob = oracle.encode([("bf16", d, s)], chunk_bytes=4096, tile=(48, 256), tile_order=1)
+    assert oracle.tensor_info(blob)[0]["tile"] == (0, 0)       # stays flat
+    blob = oracle.encode([("bf16", d, s)], chunk_bytes=4096, tile=(48, 256), tile_order=0)
+    assert oracle.tensor_info(blob)[0]["tile"] == (48, 256)
+
+
+def _bf16_of(v):
+    return (np.asarray(v, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
+def test_gemv_reference_one_hot_rows_pick_columns():
+    rng = np.random.default_rng(13)
+    w = _bf16_of(rng.normal(0, 0.02, (40, 96)))
+    ks = [0, 7, 95]
+    x = np.zeros((3, 96), np.float32)
+    for m, k in enumerate(ks):
+        x[m, k] = 1.0
+    y, a = oracle.gemv_bf16(w, _bf16_of(x))
+    wf = (w.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    for m, k in enumerate(ks):
+        assert np.array_equal(y[m], wf[:, k])
+        assert np.array_equal(a[m], np.abs(wf[:, k]))
+
+
+def test_gemv_reference_exact_on_small_integers():
+    """bf16 holds integers up to 256 exactly; their products and sums are
+    exact in fp64, so the reference must equal an integer matmul."""
+    rng = np.random.default_rng(14)
+    wi = rng.integers(-100, 101, (33, 300))
+    xi = rng.integers(-50, 51, (5, 300))
+    y, a = oracle.gemv_bf16(_bf16_of(wi.astype(np.float32)), _bf16_of(xi.astype(np.float32)))
+    assert np.array_equal(y, (xi @ wi.T).astype(np.float64))
+    assert np.array_equal(a, (np.abs(xi) @ np.abs(wi).T).astype(np.float64))
