@@ -88,9 +88,14 @@ typedef struct {
  * cores.
  * tile_rows, tile_cols: 2-D tiles (Sec. IV-A), both 0 for none.  A tensor
  * whose shape they divide exactly is coded one chunk per tile, tiles in
- * row-major order and each tile's symbols row-major; tile_cols must be a power
- * of two.  Tensors without a shape, or with one the tile does not divide, or
- * a tile narrower than a 16-byte lane-group, keep chunk_bytes chunks.
+ * row-major order; tile_cols must be a power of two.  Tensors without a
+ * shape, or with one the tile does not divide, or a tile narrower than a
+ * 16-byte lane-group, keep chunk_bytes chunks.
+ * tile_order: WC_TILE_ROWS (each tile's symbols row-major) or
+ * WC_TILE_COLUMN_BLOCKS (the tile's lane-groups of W elements k-block by
+ * k-block, every tile row per block; tile_rows must be a power of two).  With
+ * tile_rows = lanes, lane l of a chunk decodes tile row l, the layout
+ * wc_gemv consumes.
  * codebook: WC_CODEBOOK_TENSOR (one table per tensor) or WC_CODEBOOK_LAYER
  * (one table per dtype for the whole blob, Sec. IV / V-B). */
 typedef struct {
@@ -101,11 +106,13 @@ typedef struct {
   uint32_t tile_rows;
   uint32_t tile_cols;
   uint32_t codebook;
-  uint32_t reserved;
+  uint32_t tile_order;
 } wc_params;
 
 #define WC_CODEBOOK_TENSOR 0u
 #define WC_CODEBOOK_LAYER 1u
+#define WC_TILE_ROWS 0u
+#define WC_TILE_COLUMN_BLOCKS 1u
 
 /* Per-field statistics of one tensor (Sec. II-B).  Field 0 is the coded
  * symbol stream; field 1 (16-bit formats only) the raw byte stream.
@@ -192,6 +199,24 @@ wc_status wc_open(const void* data, uint64_t size, wc_blob** out);
  * a lane count other than 64 or 32), WC_EHIP (launch failure). */
 wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_dst, uint32_t n,
                     void* stream, int32_t* dev_err);
+
+/* wc_gemv -- fused decode-GEMM (Alg. 1 / 3): dev_y += dev_x * W^T for one
+ * bf16 tensor W of a blob, decoded on the fly and never written to memory.
+ *   tensor  index of W in the blob; W must have a shape (N = rows, K = cols),
+ *           be coded with 64 lanes in column-block tiles of 64 rows
+ *           (wc_params.tile_rows = 64, tile_order = WC_TILE_COLUMN_BLOCKS);
+ *   dev_x   device bf16 activations, m x K row-major, 16-byte aligned;
+ *   m       1..8 rows of activations (decode-phase batch);
+ *   dev_y   device float, m x N row-major; the products are added to it
+ *           (clear it first for a plain product).  Tiles of one band of 64
+ *           rows add with fp32 atomics, so the summation order, and the last
+ *           bits of y, can differ from run to run.
+ *   stream, dev_err as for wc_decode.
+ * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument), or
+ * WC_EUNSUPPORTED (W is not a bf16 64-lane column-block tensor of 64 rows
+ * per tile). */
+wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t tensor, const void* dev_x,
+                  uint32_t m, float* dev_y, void* stream, int32_t* dev_err);
 
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);

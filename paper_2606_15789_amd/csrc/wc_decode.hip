@@ -82,6 +82,15 @@ struct DevTensor {
   uint32_t ntc;          // tiles per band of tile_r rows
   uint32_t pitch;        // decoded bytes of one matrix row
   uint32_t tile_row_bytes;  // decoded bytes of one tile row
+  uint32_t order;        // tile order: 0 row-major, 1 column blocks
+  uint32_t log_tr;       // log2 of the tile rows (column-block order)
+};
+
+// The fused decode-GEMM of one tensor: y[M][N] += x[M][K] * W^T.
+struct GemvArgs {
+  uint64_t x;            // const bf16* (M x K, row-major)
+  uint64_t y;            // float* (M x N, row-major)
+  uint32_t M, K, N, pad;
 };
 
 struct LaunchArgs {
@@ -373,10 +382,21 @@ __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ 
 // Decode the chunk(s) of one wave, one rANS lane per wave lane.  G symbols
 // make one output dword; a lane-group is 4G symbols, 16 output bytes, so a
 // lane's share of a row is stored with one 16-byte store.
-template <int G, int L, bool kTiled>
+//
+// kGemv: instead of storing a row, multiply it into y (the fused decode-GEMM,
+// Alg. 1 / 3).  It needs column-block tiles of 64 rows decoded by 64 lanes:
+// lane l then holds 8 consecutive weights of tile row l in every wave row r
+// (columns b * tile_c + 8 r ..), so each lane accumulates whole dot products
+// of its row with v_dot2_f32_bf16, reading the matching x columns as scalar
+// (wave-uniform) loads, and adds them to y once per tile (fp32 atomics: the
+// tiles of one row band split K).
+template <int G, int L, bool kTiled, int kM = 0>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
-                                              const uint2* __restrict__ tab, uint32_t* ring) {
+                                              const uint2* __restrict__ tab, uint32_t* ring,
+                                              const GemvArgs* ga = nullptr) {
+  constexpr bool kGemv = kM > 0;  // fused GEMM with kM rows of x
+  static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
   constexpr int kH = Chain<L>::kH;
   constexpr int W = 4 * G;                    // symbols per lane-group
   constexpr int kGroupsPerRow = W / 2;        // groups of two steps in a row
@@ -410,7 +430,13 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   auto out_at = [&](uint32_t r, uint32_t& vo, uint32_t& so) {
     if constexpr (kTiled) {
       const uint32_t i0 = r * kRowSym + sub * W;
-      vo = half_v + (i0 >> T.log_tc) * T.pitch + ((i0 & tc_mask) >> kLogW) * 16u;
+      if (T.order == 0) {
+        vo = half_v + (i0 >> T.log_tc) * T.pitch + ((i0 & tc_mask) >> kLogW) * 16u;
+      } else {
+        // lane-group g = i0 / W is row g mod tile_r of k-block g div tile_r
+        const uint32_t g = i0 >> kLogW;
+        vo = half_v + (g & ((1u << T.log_tr) - 1u)) * T.pitch + (g >> T.log_tr) * 16u;
+      }
       so = 0;
     } else {
       vo = out_v;
@@ -439,6 +465,16 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   }
   uint32_t lo[G];   // entries of the dword being assembled
   uint32_t ow[4];   // the row's four output dwords
+  float acc[kGemv ? kM : 1];
+  // x columns of this tile (fused GEMM), read through the constant address
+  // space: the addresses are wave-uniform, so the loads are scalar
+  typedef __attribute__((address_space(4))) const uint32_t cu32;
+  uint64_t xrow = 0;
+  if constexpr (kGemv) {
+#pragma unroll
+    for (int m = 0; m < kM; m++) acc[m] = 0.0f;
+    xrow = ga->x + 2ull * (chunk0 % T.ntc) * (1u << T.log_tc);
+  }
 
   // group g of the chunk, j = g mod kUnroll (static)
   auto group = [&](uint32_t g, auto jc, auto tailc) {
@@ -468,6 +504,25 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
         rq[(j / kGroupsPerRow) % kRawRows] = __builtin_bit_cast(
             uint2, __builtin_amdgcn_raw_buffer_load_b64(c.rr, (r + kRawRows) * kRawRowBytes + raw_v,
                                                         0, 0));
+      }
+      if constexpr (kGemv) {
+        // this lane: weights [8 r, 8 r + 8) of its tile row; x rows m < M
+        typedef __attribute__((ext_vector_type(2))) __bf16 bf2;
+        uint32_t xv[kM][4];
+#pragma unroll
+        for (int m = 0; m < kM; m++) {
+          cu32* xp = reinterpret_cast<cu32*>(xrow + 2ull * (uint64_t(m) * ga->K + r * 8u));
+#pragma unroll
+          for (int d = 0; d < 4; d++) xv[m][d] = xp[d];
+        }
+#pragma unroll
+        for (int m = 0; m < kM; m++)
+#pragma unroll
+          for (int d = 0; d < 4; d++)
+            acc[m] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf2, ow[d]),
+                                                     __builtin_bit_cast(bf2, xv[m][d]), acc[m],
+                                                     false);
+        return;
       }
       using v4u = __attribute__((ext_vector_type(4))) unsigned int;
       const v4u o = {ow[0], ow[1], ow[2], ow[3]};
@@ -507,6 +562,14 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
                         : void()),
        ...);
     }(std::make_integer_sequence<int, kUnroll>{});
+  }
+
+  if constexpr (kGemv) {
+    // tile (band, column) adds its partial dot products to y
+    const uint32_t n = (chunk0 / T.ntc) * 64u + sub;
+    float* y = reinterpret_cast<float*>(ga->y);
+#pragma unroll
+    for (int m = 0; m < kM; m++) unsafeAtomicAdd(y + uint64_t(m) * ga->N + n, acc[m]);
   }
 
   // --- end-of-chunk checks: every lane back at 2^16, every word consumed ----
@@ -560,6 +623,72 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
     by_kind(std::integral_constant<int, 64>{});
 }
 
+// The fused decode-GEMM of one tensor (column-block tiles of 64 x tile_c
+// bf16, 64 lanes): one wave per tile, y += x * W^T.
+template <int kM>
+__global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a, GemvArgs g) {
+  __shared__ uint2 tab[wc::kTableSize];
+  __shared__ uint32_t cum[260];
+  __shared__ uint32_t ring[kWaves][(kRingWords + kMirrorWords) / 2];
+  const DevTensor& T = a.t[0];
+  const uint32_t tid = threadIdx.x;
+  build_table(a, T, tab, cum, tid);
+  __syncthreads();
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t lane = __lane_id();
+  const uint32_t chunk = blockIdx.x * kWaves + wave;
+  if (chunk >= T.n_chunks) return;
+  decode_chunks<2, 64, true, kM>(a, T, chunk, lane, tab, ring[wave], &g);
+}
+
+}  // namespace
+
+namespace {
+
+// A tiled tensor whose widest output descriptor (two tiles of a 32-lane wave)
+// would not fit the 32-bit range the buffer descriptors address.
+bool tile_span_ok(const wc::TensorInfo& T) {
+  if (!T.tile_r) return true;
+  const uint64_t pitch = T.cols * 16 / T.group;
+  return (2 * uint64_t(T.tile_r) + 1) * pitch < (1ull << 31);
+}
+
+void fill_tensor(DevTensor& D, const wc::TensorInfo& T, const void* dst, uint32_t wg0) {
+  D = DevTensor{};
+  D.dst = reinterpret_cast<uint64_t>(dst);
+  D.freq_off = T.freq_off;
+  D.raw_off = T.raw_off;
+  D.n_sym = T.n_sym;
+  D.out_bytes = T.out_bytes;
+  D.raw_padded = wc::has_raw(T.dtype) ? wc::pad16(T.n_sym) : 0;
+  D.first_chunk = (uint32_t)T.first_chunk;
+  D.n_chunks = (uint32_t)T.n_chunks;
+  D.wg0 = wg0;
+  D.per = (uint32_t)T.sym_per_chunk();
+  D.chunk_bytes = T.chunk_bytes;
+  D.kind = wc::is_nibble(T.dtype) ? kNibble : (wc::is_byte(T.dtype) ? kByte : kSplit16);
+  D.alphabet = T.alphabet;
+  D.lanes = T.lanes;
+  D.tiled = T.tile_r ? 1u : 0u;
+  if (D.tiled) {
+    D.tile_r = T.tile_r;
+    D.log_tc = uint32_t(__builtin_ctz(T.tile_c));
+    D.ntc = uint32_t(T.cols / T.tile_c);
+    D.pitch = uint32_t(T.cols * 16 / T.group);
+    D.tile_row_bytes = uint32_t(uint64_t(T.tile_c) * 16 / T.group);
+    D.order = T.tile_order;
+    D.log_tr = T.tile_order == WC_TILE_COLUMN_BLOCKS ? uint32_t(__builtin_ctz(T.tile_r)) : 0u;
+  }
+}
+
+void fill_common(LaunchArgs& args, const wc::BlobPriv& P, const void* dev_blob, int32_t* dev_err) {
+  args.blob = reinterpret_cast<uint64_t>(dev_blob);
+  args.index_off = P.index_off;
+  args.records_off = P.records_off;
+  args.records_end = P.raw_off;
+  args.err = reinterpret_cast<uint64_t>(dev_err);
+}
+
 }  // namespace
 
 extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_dst,
@@ -571,46 +700,18 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
     const wc::TensorInfo& T = P.tensors[t];
     if (T.n_chunks == 0) continue;
     if (T.lanes != 64 && T.lanes != 32) return WC_EUNSUPPORTED;
+    if (!tile_span_ok(T)) return WC_EUNSUPPORTED;
     if (!dev_dst[t]) return WC_EINVAL;
   }
   LaunchArgs args{};
-  args.blob = reinterpret_cast<uint64_t>(dev_blob);
-  args.index_off = P.index_off;
-  args.records_off = P.records_off;
-  args.records_end = P.raw_off;
-  args.err = reinterpret_cast<uint64_t>(dev_err);
+  fill_common(args, P, dev_blob, dev_err);
   uint32_t t = 0;
   while (t < n) {
     uint32_t nt = 0, wgs = 0;
     for (; t < n && nt < kMaxLaunchTensors; t++) {
       const wc::TensorInfo& T = P.tensors[t];
       if (T.n_chunks == 0) continue;
-      DevTensor& D = args.t[nt++];
-      D.dst = reinterpret_cast<uint64_t>(dev_dst[t]);
-      D.freq_off = T.freq_off;
-      D.raw_off = T.raw_off;
-      D.n_sym = T.n_sym;
-      D.out_bytes = T.out_bytes;
-      D.raw_padded = wc::has_raw(T.dtype) ? wc::pad16(T.n_sym) : 0;
-      D.first_chunk = (uint32_t)T.first_chunk;
-      D.n_chunks = (uint32_t)T.n_chunks;
-      D.wg0 = wgs;
-      D.per = (uint32_t)T.sym_per_chunk();
-      D.chunk_bytes = T.chunk_bytes;
-      D.kind = wc::is_nibble(T.dtype) ? kNibble : (wc::is_byte(T.dtype) ? kByte : kSplit16);
-      D.alphabet = T.alphabet;
-      D.lanes = T.lanes;
-      D.tiled = T.tile_r ? 1u : 0u;
-      if (D.tiled) {
-        const uint64_t pitch = T.cols * 16 / T.group, trb = uint64_t(T.tile_c) * 16 / T.group;
-        // the widest output descriptor (two tiles of a 32-lane wave) must fit 32 bits
-        if ((2 * uint64_t(T.tile_r) + 1) * pitch >= (1ull << 31)) return WC_EUNSUPPORTED;
-        D.tile_r = T.tile_r;
-        D.log_tc = uint32_t(__builtin_ctz(T.tile_c));
-        D.ntc = uint32_t(T.cols / T.tile_c);
-        D.pitch = uint32_t(pitch);
-        D.tile_row_bytes = uint32_t(trb);
-      }
+      fill_tensor(args.t[nt++], T, dev_dst[t], wgs);
       const uint64_t per_group = uint64_t(kWaves) * (T.lanes == 32 ? 2u : 1u);
       wgs += (uint32_t)((T.n_chunks + per_group - 1) / per_group);
     }
@@ -621,4 +722,41 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
     if (hipGetLastError() != hipSuccess) return WC_EHIP;
   }
   return WC_OK;
+}
+
+extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t tensor,
+                             const void* dev_x, uint32_t m, float* dev_y, void* stream,
+                             int32_t* dev_err) {
+  if (!desc || !desc->priv || tensor >= desc->n_tensors || !dev_blob || !dev_x || !dev_y)
+    return WC_EINVAL;
+  if (m < 1 || m > 8 || reinterpret_cast<uintptr_t>(dev_x) % 16) return WC_EINVAL;
+  const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
+  const wc::TensorInfo& T = P.tensors[tensor];
+  if (T.dtype != WC_BF16 || T.lanes != 64 || T.tile_r != 64 ||
+      T.tile_order != WC_TILE_COLUMN_BLOCKS)
+    return WC_EUNSUPPORTED;
+  if (T.rows > 0xFFFFFFFFull || T.cols > 0xFFFFFFFFull) return WC_EUNSUPPORTED;
+  LaunchArgs args{};
+  fill_common(args, P, dev_blob, dev_err);
+  args.n_tensors = 1;
+  fill_tensor(args.t[0], T, nullptr, 0);
+  GemvArgs g{};
+  g.x = reinterpret_cast<uint64_t>(dev_x);
+  g.y = reinterpret_cast<uint64_t>(dev_y);
+  g.M = m;
+  g.K = uint32_t(T.cols);
+  g.N = uint32_t(T.rows);
+  const uint32_t wgs = uint32_t((T.n_chunks + kWaves - 1) / kWaves);
+  const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  switch (m) {
+    case 1: hipLaunchKernelGGL(wc_gemv_kernel<1>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
+    case 2: hipLaunchKernelGGL(wc_gemv_kernel<2>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
+    case 3: hipLaunchKernelGGL(wc_gemv_kernel<3>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
+    case 4: hipLaunchKernelGGL(wc_gemv_kernel<4>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
+    case 5: hipLaunchKernelGGL(wc_gemv_kernel<5>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
+    case 6: hipLaunchKernelGGL(wc_gemv_kernel<6>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
+    case 7: hipLaunchKernelGGL(wc_gemv_kernel<7>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
+    default: hipLaunchKernelGGL(wc_gemv_kernel<8>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
+  }
+  return hipGetLastError() == hipSuccess ? WC_OK : WC_EHIP;
 }

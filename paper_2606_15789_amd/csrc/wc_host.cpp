@@ -285,7 +285,8 @@ wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out) {
     T.cols = ld64(d + 72);
     T.tile_r = ld32(d + 80);
     T.tile_c = ld32(d + 84);
-    if (!dtype_ok(T.dtype)) return WC_EINVAL;
+    T.tile_order = ld32(d + 88);
+    if (!dtype_ok(T.dtype) || ld32(d + 92)) return WC_EINVAL;
     if (pb != kProbBits || T.group != group_of(T.dtype) || T.alphabet != alphabet_of(T.dtype))
       return WC_EINVAL;
     if (T.lanes < 1 || T.lanes > kMaxLanes) return WC_EINVAL;
@@ -294,8 +295,10 @@ wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out) {
     if (has_raw(T.dtype) && T.out_bytes % 2) return WC_EINVAL;
     if (T.n_sym != symbols_of(T.dtype, T.out_bytes)) return WC_EINVAL;
     if ((T.rows || T.cols) && T.rows * T.cols != T.n_sym) return WC_EINVAL;
-    if ((T.tile_r || T.tile_c) && (!tile_ok(T.dtype, T.rows, T.cols, T.tile_r, T.tile_c) ||
-                                   T.chunk_bytes != tile_bytes(T.dtype, T.tile_r, T.tile_c)))
+    if (!(T.tile_r || T.tile_c) && T.tile_order) return WC_EINVAL;
+    if ((T.tile_r || T.tile_c) &&
+        (!tile_ok(T.dtype, T.rows, T.cols, T.tile_r, T.tile_c, T.tile_order) ||
+         T.chunk_bytes != tile_bytes(T.dtype, T.tile_r, T.tile_c)))
       return WC_EINVAL;
     uint64_t per = T.sym_per_chunk();
     if (T.n_chunks != (T.n_sym + per - 1) / per || T.first_chunk != first) return WC_EINVAL;
@@ -402,7 +405,9 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
   if (CB < 256 || CB > (1u << 20) || CB % 256 || L < 1 || L > kMaxLanes ||
       prm->prob_bits != kProbBits)
     return WC_EINVAL;
-  if ((TR == 0) != (TC == 0) || (TC && !pow2(TC)) || prm->codebook > WC_CODEBOOK_LAYER)
+  const uint32_t TO = prm->tile_order;
+  if ((TR == 0) != (TC == 0) || (TC && !pow2(TC)) || prm->codebook > WC_CODEBOOK_LAYER ||
+      TO > WC_TILE_COLUMN_BLOCKS)
     return WC_EINVAL;
   const bool shared = prm->codebook == WC_CODEBOOK_LAYER;
   for (uint32_t t = 0; t < n; t++) {
@@ -426,9 +431,10 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
       T.dtype = uint32_t(ts[t].dtype);
       T.rows = ts[t].rows;
       T.cols = ts[t].cols;
-      if (tile_ok(T.dtype, T.rows, T.cols, TR, TC)) {
+      if (tile_ok(T.dtype, T.rows, T.cols, TR, TC, TO)) {
         T.tile_r = TR;
         T.tile_c = TC;
+        T.tile_order = TO;
       }
       T.chunk_bytes = T.tile_r ? uint32_t(tile_bytes(T.dtype, TR, TC)) : CB;
       T.lanes = L;
@@ -459,13 +465,21 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
         // tile (a, b) is chunk a * (cols / tile_c) + b; its rows follow each other
         const uint64_t ntc = T.cols / T.tile_c, per = uint64_t(T.tile_r) * T.tile_c;
         std::vector<uint8_t> c2(T.n_sym), r2(has_raw(T.dtype) ? T.n_sym : 0);
+        const uint32_t W = T.group;
         parallel_for(T.n_chunks, threads, [&](uint64_t tile) {
           const uint64_t a = tile / ntc, bcol = tile % ntc;
-          for (uint32_t i = 0; i < T.tile_r; i++) {
-            const uint64_t e = (a * T.tile_r + i) * T.cols + bcol * T.tile_c;
-            const uint64_t k = tile * per + uint64_t(i) * T.tile_c;
-            memcpy(c2.data() + k, coded.data() + e, T.tile_c);
-            if (!r2.empty()) memcpy(r2.data() + k, raws[t].data() + e, T.tile_c);
+          // a run is tile_c elements of one tile row (row-major order) or one
+          // lane-group of W elements (column blocks: k-block kb, row i at
+          // position kb * tile_r + i)
+          const bool rows_order = T.tile_order == WC_TILE_ROWS;
+          const uint64_t runs = rows_order ? T.tile_r : per / W;
+          const uint32_t len = rows_order ? T.tile_c : W;
+          for (uint64_t g = 0; g < runs; g++) {
+            const uint64_t i = rows_order ? g : g % T.tile_r, kb = rows_order ? 0 : g / T.tile_r;
+            const uint64_t e = (a * T.tile_r + i) * T.cols + bcol * T.tile_c + kb * W;
+            const uint64_t k = tile * per + g * len;
+            memcpy(c2.data() + k, coded.data() + e, len);
+            if (!r2.empty()) memcpy(r2.data() + k, raws[t].data() + e, len);
           }
         });
         coded.swap(c2);
@@ -576,6 +590,7 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
       st64(d + 72, T.cols);
       st32(d + 80, T.tile_r);
       st32(d + 84, T.tile_c);
+      st32(d + 88, T.tile_order);
       for (uint32_t s = 0; s < T.alphabet; s++) st16(b + T.freq_off + 2 * s, freqs[t][s]);
     }
     std::vector<uint64_t> rec_off(nc_total + 1);

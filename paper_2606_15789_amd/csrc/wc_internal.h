@@ -35,13 +35,16 @@ inline bool pow2(uint64_t x) { return x && !(x & (x - 1)); }
 
 // A tensor is cut into tile_r x tile_c tiles (one chunk each) when its shape
 // is divided exactly, tile_c is a power of two covering whole lane-groups,
-// and a tile's decoded bytes are a valid chunk size.
+// and a tile's decoded bytes are a valid chunk size; the column-block order
+// also needs tile_r to be a power of two.
 inline uint64_t tile_bytes(uint32_t dt, uint32_t tr, uint32_t tc) {
   return uint64_t(tr) * tc * 16 / group_of(dt);
 }
-inline bool tile_ok(uint32_t dt, uint64_t rows, uint64_t cols, uint32_t tr, uint32_t tc) {
+inline bool tile_ok(uint32_t dt, uint64_t rows, uint64_t cols, uint32_t tr, uint32_t tc,
+                    uint32_t order) {
   if (!tr || !tc || !rows || !cols || rows % tr || cols % tc || !pow2(tc) || tc < group_of(dt))
     return false;
+  if (order > WC_TILE_COLUMN_BLOCKS || (order == WC_TILE_COLUMN_BLOCKS && !pow2(tr))) return false;
   const uint64_t cb = tile_bytes(dt, tr, tc);
   return cb >= 256 && cb <= (1u << 20) && cb % 256 == 0;
 }
@@ -49,6 +52,7 @@ inline bool tile_ok(uint32_t dt, uint64_t rows, uint64_t cols, uint32_t tr, uint
 struct TensorInfo {
   uint32_t dtype = 0, chunk_bytes = 0, lanes = 0, group = 0, alphabet = 0;
   uint32_t tile_r = 0, tile_c = 0;  // 0, 0: chunks are byte runs
+  uint32_t tile_order = 0;          // WC_TILE_ROWS or WC_TILE_COLUMN_BLOCKS
   uint64_t n_sym = 0, out_bytes = 0, first_chunk = 0, n_chunks = 0;
   uint64_t freq_off = 0, raw_off = 0, rows = 0, cols = 0;
   uint64_t sym_per_chunk() const { return symbols_of(dtype, chunk_bytes); }

@@ -21,7 +21,8 @@ STATUS = {0: "WC_OK", -1: "WC_EINVAL", -2: "WC_ENOMEM", -3: "WC_ECORRUPT", -4: "
 DERR = {1: "WC_DERR_INDEX", 2: "WC_DERR_STATE", 4: "WC_DERR_CURSOR", 8: "WC_DERR_TABLE"}
 
 # Every function the header declares; the library must export all of them.
-EXPORTS = ["wc_analyze", "wc_encode", "wc_open", "wc_decode", "wc_free", "wc_version"]
+EXPORTS = ["wc_analyze", "wc_encode", "wc_open", "wc_decode", "wc_gemv", "wc_free",
+           "wc_version"]
 
 
 class WcError(RuntimeError):
@@ -38,7 +39,7 @@ class _Tensor(C.Structure):
 class _Params(C.Structure):
     _fields_ = [("chunk_bytes", C.c_uint32), ("lanes", C.c_uint32), ("prob_bits", C.c_uint32),
                 ("n_threads", C.c_uint32), ("tile_rows", C.c_uint32), ("tile_cols", C.c_uint32),
-                ("codebook", C.c_uint32), ("reserved", C.c_uint32)]
+                ("codebook", C.c_uint32), ("tile_order", C.c_uint32)]
 
 
 CODEBOOKS = {"tensor": 0, "layer": 1}
@@ -81,6 +82,9 @@ def lib():
         L.wc_decode.argtypes = [C.POINTER(_Blob), C.c_void_p, C.POINTER(C.c_void_p), C.c_uint32,
                                 C.c_void_p, C.c_void_p]
         L.wc_decode.restype = C.c_int
+        L.wc_gemv.argtypes = [C.POINTER(_Blob), C.c_void_p, C.c_uint32, C.c_void_p, C.c_uint32,
+                              C.c_void_p, C.c_void_p, C.c_void_p]
+        L.wc_gemv.restype = C.c_int
         L.wc_free.argtypes = [C.POINTER(_Blob)]
         L.wc_free.restype = None
         L.wc_version.restype = C.c_int32
@@ -159,19 +163,21 @@ class Blob:
 
 
 def encode(tensors, chunk_bytes: int = 65536, lanes: int = 64, threads: int = 0, tile=(0, 0),
-           codebook: str = "tensor") -> Blob:
+           codebook: str = "tensor", tile_order: int = 0) -> Blob:
     """wc_encode of a list of (dtype, host array[, (rows, cols)]) entries.
 
     The shape is in symbol elements (16-bit words, bytes or nibbles); `tile`
     = (tile_rows, tile_cols) cuts every tensor it divides into one chunk per
-    tile.  codebook "layer" shares one table among the tensors of a dtype.
+    tile (tile_order 0: row-major tiles, 1: column blocks, the wc_gemv layout).
+    codebook "layer" shares one table among the tensors of a dtype.
     """
     keep = [_bytes(e[1]) for e in tensors]
     arr = (_Tensor * len(tensors))()
     for i, (e, b) in enumerate(zip(tensors, keep)):
         rows, cols = e[2] if len(e) > 2 and e[2] is not None else (0, 0)
         arr[i] = _Tensor(b.ctypes.data if b.size else None, b.size, DTYPES[e[0]], 0, rows, cols)
-    prm = _Params(chunk_bytes, lanes, 12, threads, tile[0], tile[1], CODEBOOKS[codebook], 0)
+    prm = _Params(chunk_bytes, lanes, 12, threads, tile[0], tile[1], CODEBOOKS[codebook],
+                  tile_order)
     out = C.POINTER(_Blob)()
     rc = lib().wc_encode(arr, len(tensors), C.byref(prm), C.byref(out))
     if rc:
@@ -196,6 +202,16 @@ def decode(blob: Blob, dev_blob: int, dev_dst, stream: int = 0, dev_err: int = 0
                          C.c_void_p(stream or None), C.c_void_p(dev_err or None))
     if rc:
         raise WcError("wc_decode", rc)
+
+
+def gemv(blob: Blob, dev_blob: int, tensor: int, dev_x: int, m: int, dev_y: int,
+         stream: int = 0, dev_err: int = 0) -> None:
+    """wc_gemv with raw device pointers: y (m x N fp32) += x (m x K bf16) * W^T."""
+    rc = lib().wc_gemv(blob.ptr, C.c_void_p(dev_blob), tensor, C.c_void_p(dev_x or None), m,
+                       C.c_void_p(dev_y or None), C.c_void_p(stream or None),
+                       C.c_void_p(dev_err or None))
+    if rc:
+        raise WcError("wc_gemv", rc)
 
 
 # --- torch plumbing: device memory and streams only ---------------------------
@@ -229,3 +245,19 @@ def decode_torch(blob: Blob, dev_blob, outs=None, stream=None, err=None):
 
 def describe_errors(bits: int) -> list:
     return [name for b, name in DERR.items() if bits & b]
+
+
+def gemv_torch(blob: Blob, dev_blob, tensor: int, x, y=None, stream=None, err=None):
+    """Fused decode-GEMM into a float32 tensor: y += x @ W^T (y zeroed if None)."""
+    import torch
+    if x.dtype != torch.bfloat16 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous bfloat16 tensor")
+    m = x.shape[0]
+    if y is None:
+        n = int(blob.out_bytes[tensor] // 2 // x.shape[1])
+        y = torch.zeros((m, n), dtype=torch.float32, device=x.device)
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device)
+    gemv(blob, dev_blob.data_ptr(), tensor, x.data_ptr(), m, y.data_ptr(), stream.cuda_stream,
+         err.data_ptr() if err is not None else 0)
+    return y

@@ -1,0 +1,129 @@
+"""GPU parity of the fused decode-GEMM (wc_gemv) and of column-block tiles.
+
+wc_gemv adds x * W^T to y, decoding W on the fly.  The reference is the
+oracle's fp64 product of the same bf16 values (orc_gemv_bf16, pinned on
+one-hot and small-integer inputs).  The GPU sums in fp32 (v_dot2_f32_bf16,
+then fp32 atomics across the tiles of a row band); with at most K roundings
+of relative size 2^-24 each, |y - y_ref| <= K * 2^-24 * sum_k |x_k w_k|.  The
+test allows twice that.
+"""
+import struct
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2606_15789_amd import synth, wc
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def dev():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    return torch.device("cuda:0")
+
+
+def say(*a):
+    print(*a, flush=True)
+
+
+def _bf16(a):
+    return (np.asarray(a, np.float32).view(np.uint32) >> 16).astype(np.uint16)
+
+
+def _run_gemv(blob, dev, t, x_bits, y0=None, expect_err=0):
+    d = wc.to_device(blob, dev)
+    x = torch.from_numpy(x_bits.view(np.int16)).to(dev).view(torch.bfloat16)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    y = None if y0 is None else torch.from_numpy(y0).to(dev)
+    y = wc.gemv_torch(blob, d, t, x, y=y, err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == expect_err, wc.describe_errors(int(err.item()))
+    return y.cpu().numpy().astype(np.float64)
+
+
+def _check(y, w, x, scale=1.0):
+    ref, absref = oracle.gemv_bf16(w, x)
+    K = w.shape[1]
+    tol = 2.0 * K * 2.0 ** -24 * absref * scale + 1e-30
+    bad = np.abs(y - scale * ref) > tol
+    assert not bad.any(), (np.argwhere(bad)[:5], float(np.abs(y - scale * ref).max()))
+
+
+@pytest.mark.parametrize("tile", [(64, 256), (64, 512), (32, 128)])
+@pytest.mark.parametrize("lanes", [64, 32])
+def test_column_block_tiles_decode_exactly(dev, tile, lanes):
+    say("column blocks", tile, "lanes", lanes)
+    ts = synth.config(2, div=8)
+    pairs = [(t.dtype, t.data, t.shape if len(t.shape) == 2 else None) for t in ts]
+    blob = wc.encode(pairs, lanes=lanes, tile=tile, tile_order=1)
+    assert any(i["tile_order"] == 1 for i in oracle.tensor_info(blob.tobytes()))
+    d = wc.to_device(blob, dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    outs = wc.decode_torch(blob, d, err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    ref = oracle.decode(blob.tobytes())
+    for (_, data, _), o, r in zip(pairs, outs, ref):
+        got = o.cpu().numpy()
+        assert np.array_equal(got, np.ascontiguousarray(data).view(np.uint8).reshape(-1))
+        assert np.array_equal(got, r)
+
+
+@pytest.mark.parametrize("shape,tile", [((256, 512), (64, 256)), ((192, 1024), (64, 512)),
+                                        ((1024, 4096), (64, 512)), ((64, 256), (64, 256))])
+@pytest.mark.parametrize("m", [1, 3, 8])
+def test_gemv_matches_the_reference(dev, shape, tile, m):
+    say("gemv", shape, tile, m)
+    rng = np.random.default_rng(shape[0] + m)
+    w = _bf16(rng.normal(0, 0.02, shape))
+    x = _bf16(rng.normal(0, 1.0, (m, shape[1])))
+    blob = wc.encode([("bf16", w, shape)], tile=tile, tile_order=1)
+    y = _run_gemv(blob, dev, 0, x)
+    _check(y, w, x)
+
+
+def test_gemv_adds_to_y_and_picks_the_tensor(dev):
+    rng = np.random.default_rng(21)
+    w0 = _bf16(rng.normal(0, 0.02, (128, 512)))
+    w1 = _bf16(rng.normal(0, 0.05, (256, 1024)))
+    norm = _bf16(rng.normal(1, 0.02, 512))
+    blob = wc.encode([("bf16", norm), ("bf16", w0, (128, 512)), ("bf16", w1, (256, 1024))],
+                     tile=(64, 512), tile_order=1, codebook="layer")
+    x = _bf16(rng.normal(0, 1.0, (2, 1024)))
+    y = _run_gemv(blob, dev, 2, x)
+    _check(y, w1, x)
+    ref, _ = oracle.gemv_bf16(w1, x)
+    y2 = _run_gemv(blob, dev, 2, x, y0=ref.astype(np.float32))    # y += x W^T
+    _check(y2, w1, x, scale=2.0)
+    x0 = np.ascontiguousarray(x[:, :512])
+    _check(_run_gemv(blob, dev, 1, x0), w0, x0)
+
+
+def test_gemv_full_size_projection(dev):
+    """A Llama-3-70B q_proj (8192 x 8192) in 64 x 512 column-block tiles."""
+    w = synth.config(5)[0].data
+    assert w.shape == (8192, 8192)
+    blob = wc.encode([("bf16", w, (8192, 8192))], tile=(64, 512), tile_order=1)
+    x = _bf16(np.random.default_rng(22).normal(0, 1.0, (4, 8192)))
+    y = _run_gemv(blob, dev, 0, x)
+    _check(y, w, x)
+
+
+def test_gemv_reports_corruption(dev):
+    rng = np.random.default_rng(23)
+    w = _bf16(rng.normal(0, 0.02, (128, 512)))
+    blob = wc.encode([("bf16", w, (128, 512))], tile=(64, 256), tile_order=1)
+    raw = blob.tobytes()
+    idx = struct.unpack_from("<Q", raw, 32)[0]
+    off1 = struct.unpack_from("<I", raw, idx + 4)[0] * 16
+    d = wc.to_device(blob, dev)
+    d[off1 + 16 + 20] ^= 0x01                      # a lane state of tile 1
+    x = torch.from_numpy(_bf16(rng.normal(0, 1, (1, 512))).view(np.int16)).to(dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    wc.gemv_torch(blob, d, 0, x.view(torch.bfloat16), err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) & 0x6

@@ -138,11 +138,14 @@ def test_decode_rejects_before_any_launch():
 @pytest.mark.parametrize("tile", [(32, 128), (64, 256), (128, 256)])
 @pytest.mark.parametrize("codebook", ["tensor", "layer"])
 @pytest.mark.parametrize("lanes", [64, 32])
-def test_tiled_blobs_identical_to_oracle(tile, codebook, lanes):
+@pytest.mark.parametrize("order", [0, 1])
+def test_tiled_blobs_identical_to_oracle(tile, codebook, lanes, order):
     ts = synth.config(2, div=8) + synth.config(3, div=8)
     pairs = [(t.dtype, t.data, t.shape if len(t.shape) == 2 else None) for t in ts]
-    a = wc.encode(pairs, chunk_bytes=16384, lanes=lanes, tile=tile, codebook=codebook)
-    b = oracle.encode(pairs, chunk_bytes=16384, lanes=lanes, tile=tile, codebook=codebook)
+    a = wc.encode(pairs, chunk_bytes=16384, lanes=lanes, tile=tile, codebook=codebook,
+                  tile_order=order)
+    b = oracle.encode(pairs, chunk_bytes=16384, lanes=lanes, tile=tile, codebook=codebook,
+                      tile_order=order)
     assert a.tobytes() == b
     info = oracle.tensor_info(b)
     assert any(i["tile"] == tile for i in info)            # some tensors were tiled
@@ -157,3 +160,25 @@ def test_open_rejects_inconsistent_tile_fields():
         struct.pack_into("<I", bad, off, val)
         with pytest.raises(wc.WcError):
             wc.open_blob(bytes(bad))
+
+
+def test_gemv_rejects_before_any_launch():
+    w = (np.random.default_rng(3).normal(0, 0.02, (128, 512)).astype(np.float32)
+         .view(np.uint32) >> 16).astype(np.uint16)
+    good = wc.encode([("bf16", w, (128, 512))], tile=(64, 256), tile_order=1)
+    rows = wc.encode([("bf16", w, (128, 512))], tile=(64, 256), tile_order=0)
+    flat = wc.encode([("bf16", w, (128, 512))])
+    for m in (0, 9):
+        with pytest.raises(wc.WcError) as e:
+            wc.gemv(good, 16, 0, 16, m, 16)
+        assert e.value.rc == -1
+    with pytest.raises(wc.WcError) as e:
+        wc.gemv(good, 16, 0, 8, 1, 16)          # x not 16-byte aligned
+    assert e.value.rc == -1
+    with pytest.raises(wc.WcError) as e:
+        wc.gemv(good, 16, 1, 16, 1, 16)         # no such tensor
+    assert e.value.rc == -1
+    for b in (rows, flat):                      # not the column-block layout
+        with pytest.raises(wc.WcError) as e:
+            wc.gemv(b, 16, 0, 16, 1, 16)
+        assert e.value.rc == -5
