@@ -160,6 +160,10 @@ def main() -> int:
     ap.add_argument("--tile", default="", help="ROWSxCOLS 2-D tiles, e.g. 128x256 (default: "
                     "flat chunks of --chunk-bytes)")
     ap.add_argument("--codebook", choices=["tensor", "layer"], default="tensor")
+    ap.add_argument("--gemv", type=int, default=0, metavar="M",
+                    help="time the fused decode-GEMM y += x W^T (x: M rows) over the 70B "
+                         "layer instead of the decode, next to the same product unfused "
+                         "(wc_decode, then torch.matmul) and uncompressed (torch.matmul)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -177,6 +181,8 @@ def main() -> int:
         return 1
     dev = torch.device("cuda:0")
     wc.lib()
+    if args.gemv:
+        return gemv_bench(args, dev)
     cfg = WORKLOADS[args.workload]
     big = cfg == 5
     tile = tuple(int(v) for v in args.tile.lower().split("x")) if args.tile else (0, 0)
@@ -375,6 +381,120 @@ def main() -> int:
         "two_stream": two,
         "compression": comp,
         "cpu_baseline": cpu,
+        "setup_s": round(setup_s, 1),
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def gemv_bench(args, dev) -> int:
+    """Fused decode-GEMM over the seven projections of one 70B layer."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15789_amd import synth, wc
+    M = args.gemv
+    if not 1 <= M <= 8:
+        print("--gemv takes 1..8 rows of activations", file=sys.stderr)
+        return 2
+    tile = (64, 512)
+    t0 = time.perf_counter()
+    tens = synth.config_torch_device(5, 0, device="cuda")
+    shapes = [shape for _, _, shape in tens]
+    host = [t.cpu().numpy() for _, t, _ in tens]
+    blob = wc.encode([("bf16", h, shp) for h, shp in zip(host, shapes)], lanes=64, tile=tile,
+                     tile_order=1, threads=args.threads)
+    del host
+    dblob = wc.to_device(blob, dev)
+    W = [t.view(torch.bfloat16).reshape(shp) for _, t, shp in tens]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(12345)
+    xs = [torch.randn(M, shp[1], generator=gen, device=dev).to(torch.bfloat16) for shp in shapes]
+    ys = [torch.zeros(M, shp[0], dtype=torch.float32, device=dev) for shp in shapes]
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def fused():
+        # one launch for the seven projections
+        wc.gemv(blob, dblob.data_ptr(), list(range(len(W))), [x.data_ptr() for x in xs], M,
+                [y.data_ptr() for y in ys], stream.cuda_stream, err.data_ptr())
+
+    # correctness: y against torch's fp32 product of the same bf16 values,
+    # within the fp32 summation bound K * 2^-23 * sum |x w|
+    fused()
+    torch.cuda.synchronize()
+    if int(err.item()):
+        raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
+    for t, (w, x, y) in enumerate(zip(W, xs, ys)):
+        ref = x.float() @ w.float().t()
+        bound = x.float().abs() @ w.float().abs().t()
+        if torch.any((y - ref).abs() > w.shape[1] * 2.0 ** -23 * bound + 1e-30):
+            raise RuntimeError(f"fused GEMM tensor {t} outside the fp32 summation bound")
+    setup_s = time.perf_counter() - t0
+
+    # the unfused path decodes a byte-run blob of the same layer (the decode's
+    # fastest layout: 1 KiB rows) into memory, then multiplies
+    flat = wc.encode([("bf16", w.view(torch.uint8).reshape(-1).cpu().numpy()) for w in W],
+                     lanes=64, threads=args.threads)
+    dflat = wc.to_device(flat, dev)
+    outs = [torch.empty(n, dtype=torch.uint8, device=dev) for n in flat.out_bytes]
+
+    def unfused():
+        wc.decode(flat, dflat.data_ptr(), [o.data_ptr() for o in outs], stream.cuda_stream,
+                  err.data_ptr())
+        for t, (o, x, shp) in enumerate(zip(outs, xs, shapes)):
+            torch.matmul(x, o.view(torch.bfloat16).view(shp).t())
+
+    def uncompressed():
+        for w, x in zip(W, xs):
+            torch.matmul(x, w.t())
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / args.steps / 1e3
+
+    s_fused, s_unfused, s_plain = timed(fused), timed(unfused), timed(uncompressed)
+    if int(err.item()):
+        raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
+    wbytes = sum(blob.out_bytes)
+    alg = blob.size + sum(x.numel() * 2 for x in xs) + sum(2 * y.numel() * 4 for y in ys)
+    achieved = alg / s_fused / 1e9
+    line = {
+        "metric": METRIC + " [fused decode-GEMM]",
+        "value": round(wbytes / s_fused / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(s_fused * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16 x bf16 -> fp32",
+        "data": "synthetic",
+        "config": {"workload": "llama3-70b-layer-bf16", "mode": "fused-gemv", "m": M,
+                   "tile": f"{tile[0]}x{tile[1]}", "tile_order": "column-blocks",
+                   "lanes": 64, "weight_bytes_per_step": wbytes,
+                   "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "wc_gemv_kernel", "mean_step_us": round(s_fused * 1e6, 2),
+                     "algorithmic_bytes_per_step": int(alg)},
+        "unfused": {"value": round(wbytes / s_unfused / 1e9, 2), "unit": "GB/s",
+                    "ms_per_step": round(s_unfused * 1e3, 4),
+                    "what": "wc_decode of the layer (64 KiB byte-run chunks) into memory, then "
+                            "torch.matmul per tensor"},
+        "uncompressed": {"value": round(wbytes / s_plain / 1e9, 2), "unit": "GB/s",
+                         "ms_per_step": round(s_plain * 1e3, 4),
+                         "what": "torch.matmul on the bf16 weights"},
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line), flush=True)

@@ -200,23 +200,28 @@ wc_status wc_open(const void* data, uint64_t size, wc_blob** out);
 wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_dst, uint32_t n,
                     void* stream, int32_t* dev_err);
 
-/* wc_gemv -- fused decode-GEMM (Alg. 1 / 3): dev_y += dev_x * W^T for one
- * bf16 tensor W of a blob, decoded on the fly and never written to memory.
- *   tensor  index of W in the blob; W must have a shape (N = rows, K = cols),
- *           be coded with 64 lanes in column-block tiles of 64 rows
- *           (wc_params.tile_rows = 64, tile_order = WC_TILE_COLUMN_BLOCKS);
- *   dev_x   device bf16 activations, m x K row-major, 16-byte aligned;
- *   m       1..8 rows of activations (decode-phase batch);
- *   dev_y   device float, m x N row-major; the products are added to it
- *           (clear it first for a plain product).  Tiles of one band of 64
- *           rows add with fp32 atomics, so the summation order, and the last
- *           bits of y, can differ from run to run.
+/* wc_gemv -- fused decode-GEMM (Alg. 1 / 3): for each of n jobs i,
+ * dev_y[i] += dev_x[i] * W^T with W = tensor tensors[i] of the blob, decoded
+ * on the fly and never written to memory.  All jobs run in one launch.
+ *   n        1..32 jobs;
+ *   tensors  host array of n tensor indices; each W must be bf16 with a shape
+ *            (N = rows, K = cols), coded with 64 lanes in column-block tiles
+ *            of 64 rows (wc_params.tile_rows = 64, tile_order =
+ *            WC_TILE_COLUMN_BLOCKS);
+ *   dev_x    host array of n device pointers to bf16 activations, m x K
+ *            row-major, 16-byte aligned (jobs may share one x);
+ *   m        1..8 rows of activations, the same for every job;
+ *   dev_y    host array of n device pointers to float, m x N row-major; the
+ *            products are added (clear y first for a plain product).  The
+ *            tiles of one band of 64 rows add with fp32 atomics, so the
+ *            summation order, and the last bits of y, can differ between runs;
  *   stream, dev_err as for wc_decode.
  * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument), or
- * WC_EUNSUPPORTED (W is not a bf16 64-lane column-block tensor of 64 rows
- * per tile). */
-wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t tensor, const void* dev_x,
-                  uint32_t m, float* dev_y, void* stream, int32_t* dev_err);
+ * WC_EUNSUPPORTED (a tensor is not a bf16 64-lane column-block tensor of 64
+ * rows per tile). */
+wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n, const uint32_t* tensors,
+                  const void* const* dev_x, uint32_t m, float* const* dev_y, void* stream,
+                  int32_t* dev_err);
 
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);

@@ -84,13 +84,7 @@ struct DevTensor {
   uint32_t tile_row_bytes;  // decoded bytes of one tile row
   uint32_t order;        // tile order: 0 row-major, 1 column blocks
   uint32_t log_tr;       // log2 of the tile rows (column-block order)
-};
-
-// The fused decode-GEMM of one tensor: y[M][N] += x[M][K] * W^T.
-struct GemvArgs {
-  uint64_t x;            // const bf16* (M x K, row-major)
-  uint64_t y;            // float* (M x N, row-major)
-  uint32_t M, K, N, pad;
+  uint64_t x;            // fused GEMM: const bf16 x[M][K]; y[M][N] is float* dst
 };
 
 struct LaunchArgs {
@@ -393,8 +387,7 @@ __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ 
 template <int G, int L, bool kTiled, int kM = 0>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
-                                              const uint2* __restrict__ tab, uint32_t* ring,
-                                              const GemvArgs* ga = nullptr) {
+                                              const uint2* __restrict__ tab, uint32_t* ring) {
   constexpr bool kGemv = kM > 0;  // fused GEMM with kM rows of x
   static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
   constexpr int kH = Chain<L>::kH;
@@ -473,7 +466,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   if constexpr (kGemv) {
 #pragma unroll
     for (int m = 0; m < kM; m++) acc[m] = 0.0f;
-    xrow = ga->x + 2ull * (chunk0 % T.ntc) * (1u << T.log_tc);
+    xrow = T.x + 2ull * (chunk0 % T.ntc) * (1u << T.log_tc);
   }
 
   // group g of the chunk, j = g mod kUnroll (static)
@@ -511,7 +504,8 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
         uint32_t xv[kM][4];
 #pragma unroll
         for (int m = 0; m < kM; m++) {
-          cu32* xp = reinterpret_cast<cu32*>(xrow + 2ull * (uint64_t(m) * ga->K + r * 8u));
+          cu32* xp = reinterpret_cast<cu32*>(
+              xrow + 2ull * (uint64_t(m) * (T.ntc << T.log_tc) + r * 8u));
 #pragma unroll
           for (int d = 0; d < 4; d++) xv[m][d] = xp[d];
         }
@@ -567,9 +561,10 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   if constexpr (kGemv) {
     // tile (band, column) adds its partial dot products to y
     const uint32_t n = (chunk0 / T.ntc) * 64u + sub;
-    float* y = reinterpret_cast<float*>(ga->y);
+    const uint64_t N = uint64_t(T.n_chunks / T.ntc) * 64u;
+    float* y = reinterpret_cast<float*>(T.dst);
 #pragma unroll
-    for (int m = 0; m < kM; m++) unsafeAtomicAdd(y + uint64_t(m) * ga->N + n, acc[m]);
+    for (int m = 0; m < kM; m++) unsafeAtomicAdd(y + uint64_t(m) * N + n, acc[m]);
   }
 
   // --- end-of-chunk checks: every lane back at 2^16, every word consumed ----
@@ -623,22 +618,27 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
     by_kind(std::integral_constant<int, 64>{});
 }
 
-// The fused decode-GEMM of one tensor (column-block tiles of 64 x tile_c
-// bf16, 64 lanes): one wave per tile, y += x * W^T.
+// The fused decode-GEMM of up to kMaxLaunchTensors tensors (column-block
+// tiles of 64 x tile_c bf16, 64 lanes) in one launch: one wave per tile,
+// y += x * W^T for each tensor's own x and y.
 template <int kM>
-__global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a, GemvArgs g) {
+__global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   __shared__ uint2 tab[wc::kTableSize];
   __shared__ uint32_t cum[260];
   __shared__ uint32_t ring[kWaves][(kRingWords + kMirrorWords) / 2];
-  const DevTensor& T = a.t[0];
+  const uint32_t wg = blockIdx.x;
+  uint32_t ti = 0;
+  for (uint32_t k = 1; k < a.n_tensors; k++)
+    if (wg >= a.t[k].wg0) ti = k;
+  const DevTensor& T = a.t[ti];
   const uint32_t tid = threadIdx.x;
   build_table(a, T, tab, cum, tid);
   __syncthreads();
   const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const uint32_t lane = __lane_id();
-  const uint32_t chunk = blockIdx.x * kWaves + wave;
+  const uint32_t chunk = (wg - T.wg0) * kWaves + wave;
   if (chunk >= T.n_chunks) return;
-  decode_chunks<2, 64, true, kM>(a, T, chunk, lane, tab, ring[wave], &g);
+  decode_chunks<2, 64, true, kM>(a, T, chunk, lane, tab, ring[wave]);
 }
 
 }  // namespace
@@ -724,39 +724,44 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
   return WC_OK;
 }
 
-extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t tensor,
-                             const void* dev_x, uint32_t m, float* dev_y, void* stream,
-                             int32_t* dev_err) {
-  if (!desc || !desc->priv || tensor >= desc->n_tensors || !dev_blob || !dev_x || !dev_y)
+extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n,
+                             const uint32_t* tensors, const void* const* dev_x, uint32_t m,
+                             float* const* dev_y, void* stream, int32_t* dev_err) {
+  if (!desc || !desc->priv || !dev_blob || !tensors || !dev_x || !dev_y || n == 0 ||
+      n > kMaxLaunchTensors)
     return WC_EINVAL;
-  if (m < 1 || m > 8 || reinterpret_cast<uintptr_t>(dev_x) % 16) return WC_EINVAL;
+  if (m < 1 || m > 8) return WC_EINVAL;
   const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
-  const wc::TensorInfo& T = P.tensors[tensor];
-  if (T.dtype != WC_BF16 || T.lanes != 64 || T.tile_r != 64 ||
-      T.tile_order != WC_TILE_COLUMN_BLOCKS)
-    return WC_EUNSUPPORTED;
-  if (T.rows > 0xFFFFFFFFull || T.cols > 0xFFFFFFFFull) return WC_EUNSUPPORTED;
+  for (uint32_t i = 0; i < n; i++) {
+    if (tensors[i] >= desc->n_tensors || !dev_x[i] || !dev_y[i] ||
+        reinterpret_cast<uintptr_t>(dev_x[i]) % 16)
+      return WC_EINVAL;
+    const wc::TensorInfo& T = P.tensors[tensors[i]];
+    if (T.dtype != WC_BF16 || T.lanes != 64 || T.tile_r != 64 ||
+        T.tile_order != WC_TILE_COLUMN_BLOCKS)
+      return WC_EUNSUPPORTED;
+    if (T.rows > 0xFFFFFFFFull || T.cols > 0xFFFFFFFFull) return WC_EUNSUPPORTED;
+  }
   LaunchArgs args{};
   fill_common(args, P, dev_blob, dev_err);
-  args.n_tensors = 1;
-  fill_tensor(args.t[0], T, nullptr, 0);
-  GemvArgs g{};
-  g.x = reinterpret_cast<uint64_t>(dev_x);
-  g.y = reinterpret_cast<uint64_t>(dev_y);
-  g.M = m;
-  g.K = uint32_t(T.cols);
-  g.N = uint32_t(T.rows);
-  const uint32_t wgs = uint32_t((T.n_chunks + kWaves - 1) / kWaves);
+  uint32_t wgs = 0;
+  for (uint32_t i = 0; i < n; i++) {
+    const wc::TensorInfo& T = P.tensors[tensors[i]];
+    fill_tensor(args.t[i], T, dev_y[i], wgs);
+    args.t[i].x = reinterpret_cast<uint64_t>(dev_x[i]);
+    wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
+  }
+  args.n_tensors = n;
   const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   switch (m) {
-    case 1: hipLaunchKernelGGL(wc_gemv_kernel<1>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
-    case 2: hipLaunchKernelGGL(wc_gemv_kernel<2>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
-    case 3: hipLaunchKernelGGL(wc_gemv_kernel<3>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
-    case 4: hipLaunchKernelGGL(wc_gemv_kernel<4>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
-    case 5: hipLaunchKernelGGL(wc_gemv_kernel<5>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
-    case 6: hipLaunchKernelGGL(wc_gemv_kernel<6>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
-    case 7: hipLaunchKernelGGL(wc_gemv_kernel<7>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
-    default: hipLaunchKernelGGL(wc_gemv_kernel<8>, dim3(wgs), dim3(kThreads), 0, st, args, g); break;
+    case 1: hipLaunchKernelGGL(wc_gemv_kernel<1>, dim3(wgs), dim3(kThreads), 0, st, args); break;
+    case 2: hipLaunchKernelGGL(wc_gemv_kernel<2>, dim3(wgs), dim3(kThreads), 0, st, args); break;
+    case 3: hipLaunchKernelGGL(wc_gemv_kernel<3>, dim3(wgs), dim3(kThreads), 0, st, args); break;
+    case 4: hipLaunchKernelGGL(wc_gemv_kernel<4>, dim3(wgs), dim3(kThreads), 0, st, args); break;
+    case 5: hipLaunchKernelGGL(wc_gemv_kernel<5>, dim3(wgs), dim3(kThreads), 0, st, args); break;
+    case 6: hipLaunchKernelGGL(wc_gemv_kernel<6>, dim3(wgs), dim3(kThreads), 0, st, args); break;
+    case 7: hipLaunchKernelGGL(wc_gemv_kernel<7>, dim3(wgs), dim3(kThreads), 0, st, args); break;
+    default: hipLaunchKernelGGL(wc_gemv_kernel<8>, dim3(wgs), dim3(kThreads), 0, st, args); break;
   }
   return hipGetLastError() == hipSuccess ? WC_OK : WC_EHIP;
 }

@@ -82,8 +82,9 @@ def lib():
         L.wc_decode.argtypes = [C.POINTER(_Blob), C.c_void_p, C.POINTER(C.c_void_p), C.c_uint32,
                                 C.c_void_p, C.c_void_p]
         L.wc_decode.restype = C.c_int
-        L.wc_gemv.argtypes = [C.POINTER(_Blob), C.c_void_p, C.c_uint32, C.c_void_p, C.c_uint32,
-                              C.c_void_p, C.c_void_p, C.c_void_p]
+        L.wc_gemv.argtypes = [C.POINTER(_Blob), C.c_void_p, C.c_uint32,
+                              C.POINTER(C.c_uint32), C.POINTER(C.c_void_p), C.c_uint32,
+                              C.POINTER(C.c_void_p), C.c_void_p, C.c_void_p]
         L.wc_gemv.restype = C.c_int
         L.wc_free.argtypes = [C.POINTER(_Blob)]
         L.wc_free.restype = None
@@ -204,12 +205,16 @@ def decode(blob: Blob, dev_blob: int, dev_dst, stream: int = 0, dev_err: int = 0
         raise WcError("wc_decode", rc)
 
 
-def gemv(blob: Blob, dev_blob: int, tensor: int, dev_x: int, m: int, dev_y: int,
-         stream: int = 0, dev_err: int = 0) -> None:
-    """wc_gemv with raw device pointers: y (m x N fp32) += x (m x K bf16) * W^T."""
-    rc = lib().wc_gemv(blob.ptr, C.c_void_p(dev_blob), tensor, C.c_void_p(dev_x or None), m,
-                       C.c_void_p(dev_y or None), C.c_void_p(stream or None),
-                       C.c_void_p(dev_err or None))
+def gemv(blob: Blob, dev_blob: int, tensors, dev_x, m: int, dev_y, stream: int = 0,
+         dev_err: int = 0) -> None:
+    """wc_gemv with raw device pointers: y_i (m x N fp32) += x_i (m x K bf16) * W_i^T for
+    each job i (tensors, dev_x, dev_y: equal-length lists), in one launch."""
+    n = len(tensors)
+    ts = (C.c_uint32 * max(n, 1))(*tensors)
+    xs = (C.c_void_p * max(n, 1))(*[p or None for p in dev_x])
+    ys = (C.c_void_p * max(n, 1))(*[p or None for p in dev_y])
+    rc = lib().wc_gemv(blob.ptr, C.c_void_p(dev_blob), n, ts, xs, m, ys,
+                       C.c_void_p(stream or None), C.c_void_p(dev_err or None))
     if rc:
         raise WcError("wc_gemv", rc)
 
@@ -247,17 +252,19 @@ def describe_errors(bits: int) -> list:
     return [name for b, name in DERR.items() if bits & b]
 
 
-def gemv_torch(blob: Blob, dev_blob, tensor: int, x, y=None, stream=None, err=None):
-    """Fused decode-GEMM into a float32 tensor: y += x @ W^T (y zeroed if None)."""
+def gemv_torch(blob: Blob, dev_blob, tensors, xs, ys=None, stream=None, err=None):
+    """Fused decode-GEMM into float32 tensors, one launch: ys[i] += xs[i] @ W_i^T for
+    W_i = tensor tensors[i] (ys zeroed and returned if None)."""
     import torch
-    if x.dtype != torch.bfloat16 or not x.is_contiguous():
-        raise ValueError("x must be a contiguous bfloat16 tensor")
-    m = x.shape[0]
-    if y is None:
-        n = int(blob.out_bytes[tensor] // 2 // x.shape[1])
-        y = torch.zeros((m, n), dtype=torch.float32, device=x.device)
+    m = xs[0].shape[0]
+    for x in xs:
+        if x.dtype != torch.bfloat16 or not x.is_contiguous() or x.shape[0] != m:
+            raise ValueError("xs must be contiguous bfloat16 tensors with equal row counts")
+    if ys is None:
+        ys = [torch.zeros((m, int(blob.out_bytes[t] // 2 // x.shape[1])), dtype=torch.float32,
+                          device=x.device) for t, x in zip(tensors, xs)]
     if stream is None:
-        stream = torch.cuda.current_stream(x.device)
-    gemv(blob, dev_blob.data_ptr(), tensor, x.data_ptr(), m, y.data_ptr(), stream.cuda_stream,
-         err.data_ptr() if err is not None else 0)
-    return y
+        stream = torch.cuda.current_stream(xs[0].device)
+    gemv(blob, dev_blob.data_ptr(), list(tensors), [x.data_ptr() for x in xs], m,
+         [y.data_ptr() for y in ys], stream.cuda_stream, err.data_ptr() if err is not None else 0)
+    return ys

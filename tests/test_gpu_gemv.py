@@ -34,15 +34,18 @@ def _bf16(a):
     return (np.asarray(a, np.float32).view(np.uint32) >> 16).astype(np.uint16)
 
 
+def _dev_x(x_bits, dev):
+    return torch.from_numpy(x_bits.view(np.int16)).to(dev).view(torch.bfloat16)
+
+
 def _run_gemv(blob, dev, t, x_bits, y0=None, expect_err=0):
     d = wc.to_device(blob, dev)
-    x = torch.from_numpy(x_bits.view(np.int16)).to(dev).view(torch.bfloat16)
     err = torch.zeros(1, dtype=torch.int32, device=dev)
-    y = None if y0 is None else torch.from_numpy(y0).to(dev)
-    y = wc.gemv_torch(blob, d, t, x, y=y, err=err)
+    ys = None if y0 is None else [torch.from_numpy(y0).to(dev)]
+    ys = wc.gemv_torch(blob, d, [t], [_dev_x(x_bits, dev)], ys=ys, err=err)
     torch.cuda.synchronize()
     assert int(err.item()) == expect_err, wc.describe_errors(int(err.item()))
-    return y.cpu().numpy().astype(np.float64)
+    return ys[0].cpu().numpy().astype(np.float64)
 
 
 def _check(y, w, x, scale=1.0):
@@ -122,8 +125,29 @@ def test_gemv_reports_corruption(dev):
     off1 = struct.unpack_from("<I", raw, idx + 4)[0] * 16
     d = wc.to_device(blob, dev)
     d[off1 + 16 + 20] ^= 0x01                      # a lane state of tile 1
-    x = torch.from_numpy(_bf16(rng.normal(0, 1, (1, 512))).view(np.int16)).to(dev)
+    x = _dev_x(_bf16(rng.normal(0, 1, (1, 512))), dev)
     err = torch.zeros(1, dtype=torch.int32, device=dev)
-    wc.gemv_torch(blob, d, 0, x.view(torch.bfloat16), err=err)
+    wc.gemv_torch(blob, d, [0], [x], err=err)
     torch.cuda.synchronize()
     assert int(err.item()) & 0x6
+
+
+@pytest.mark.parametrize("m", [1, 5])
+def test_gemv_many_jobs_in_one_launch(dev, m):
+    """Every projection of a scaled 8B layer in one call; jobs with the same K
+    share one x, as q/k/v and gate/up do in a transformer layer."""
+    ts = [t for t in synth.config(2, div=4) if len(t.shape) == 2]
+    blob = wc.encode([(t.dtype, t.data, t.shape) for t in ts], tile=(64, 256), tile_order=1,
+                     codebook="layer")
+    d = wc.to_device(blob, dev)
+    rng = np.random.default_rng(31 + m)
+    xbits = {}
+    for t in ts:
+        xbits.setdefault(t.shape[1], _bf16(rng.normal(0, 1.0, (m, t.shape[1]))))
+    xdev = {k: _dev_x(v, dev) for k, v in xbits.items()}
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ys = wc.gemv_torch(blob, d, list(range(len(ts))), [xdev[t.shape[1]] for t in ts], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    for t, y in zip(ts, ys):
+        _check(y.cpu().numpy().astype(np.float64), t.data, xbits[t.shape[1]])

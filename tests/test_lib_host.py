@@ -170,15 +170,17 @@ def test_gemv_rejects_before_any_launch():
     flat = wc.encode([("bf16", w, (128, 512))])
     for m in (0, 9):
         with pytest.raises(wc.WcError) as e:
-            wc.gemv(good, 16, 0, 16, m, 16)
+            wc.gemv(good, 16, [0], [16], m, [16])
         assert e.value.rc == -1
-    with pytest.raises(wc.WcError) as e:
-        wc.gemv(good, 16, 0, 8, 1, 16)          # x not 16-byte aligned
-    assert e.value.rc == -1
-    with pytest.raises(wc.WcError) as e:
-        wc.gemv(good, 16, 1, 16, 1, 16)         # no such tensor
-    assert e.value.rc == -1
+    for args in (([0], [8], [16]),            # x not 16-byte aligned
+                 ([1], [16], [16]),           # no such tensor
+                 ([0], [16], [0]),            # no y
+                 ([], [], []),                # no jobs
+                 ([0] * 33, [16] * 33, [16] * 33)):   # more than one launch holds
+        with pytest.raises(wc.WcError) as e:
+            wc.gemv(good, 16, args[0], args[1], 1, args[2])
+        assert e.value.rc == -1, args
     for b in (rows, flat):                      # not the column-block layout
         with pytest.raises(wc.WcError) as e:
-            wc.gemv(b, 16, 0, 16, 1, 16)
+            wc.gemv(b, 16, [0], [16], 1, [16])
         assert e.value.rc == -5
