@@ -223,10 +223,68 @@ wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n, const u
                   const void* const* dev_x, uint32_t m, float* const* dev_y, void* stream,
                   int32_t* dev_err);
 
+/* A tensor in device memory, for the device-side analysis and encoder: the
+ * fields of wc_tensor, with dev_ptr a device pointer that must be 16-byte
+ * aligned (any torch or hipMalloc allocation is). */
+typedef struct {
+  const void* dev_ptr;
+  uint64_t nbytes;
+  int32_t dtype; /* wc_dtype */
+  int32_t reserved;
+  uint64_t rows;
+  uint64_t cols;
+} wc_dtensor;
+
+/* Device workspace wc_analyze_device needs: 65 536 u64 histogram bins. */
+#define WC_ANALYZE_WORKSPACE_BYTES 524288u
+
+/* wc_analyze_device -- wc_analyze of a tensor in device memory (Sec. II-B):
+ * the same wc_stats, bit for bit.  The histograms are counted on the GPU
+ * (16-bit formats: the histogram of whole 16-bit words, from which both
+ * fields and the joint entropy follow; other formats: the symbol histogram);
+ * the entropies are computed on the host from the counts.
+ *   dev_workspace  caller-owned device memory of at least
+ *                  WC_ANALYZE_WORKSPACE_BYTES (16-byte aligned), overwritten;
+ *   stream         hipStream_t (NULL = null stream).
+ * Synchronous: returns after the counts are back on the host.  Allocates
+ * nothing.  Returns WC_EINVAL (argument, dtype, odd size of a 16-bit format,
+ * misaligned pointer, workspace too small), WC_EHIP. */
+wc_status wc_analyze_device(const wc_dtensor* t, void* dev_workspace, uint64_t workspace_bytes,
+                            void* stream, wc_stats* out);
+
+/* wc_encode_device_bounds -- what wc_encode_device needs for these tensors and
+ * parameters (their pointers are not read): *blob_capacity, the largest blob
+ * they can give (every coded symbol emitting a word), and *workspace_bytes,
+ * the device scratch the encoder uses.  Host only.  WC_EINVAL as for
+ * wc_encode, and for a largest blob of 64 GiB or more. */
+wc_status wc_encode_device_bounds(const wc_dtensor* t, uint32_t n, const wc_params* p,
+                                  uint64_t* blob_capacity, uint64_t* workspace_bytes);
+
+/* wc_encode_device -- wc_encode on the GPU (Sec. V-B; the optional GPU-side
+ * compressor): the blob it writes to dev_blob is byte-identical to the one
+ * wc_encode makes from the same tensors and parameters (n_threads ignored).
+ * Histograms, table normalisation, the chunk encode (one wave per chunk, one
+ * rANS lane per wave lane, steps in reverse), the offset index and the final
+ * packing all run on the device, in order on `stream`.
+ *   t, n, p         the tensors (device memory, 16-byte aligned, not modified)
+ *                   and parameters, as for wc_encode;
+ *   dev_blob        caller-owned device buffer of blob_capacity >= the bound
+ *                   from wc_encode_device_bounds; bytes past the blob's size
+ *                   are left as they were;
+ *   dev_workspace   caller-owned device scratch of workspace_bytes >= the
+ *                   bound (16-byte aligned); overwritten;
+ *   dev_size        device u64 that receives the blob's size in bytes.
+ * Asynchronous: read *dev_size, and use the blob (e.g. wc_open on a host copy
+ * of it), after synchronising the stream.  Allocates nothing.  Returns
+ * WC_EINVAL (argument, parameters, sizes, alignment, capacity), WC_EHIP. */
+wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_params* p, void* dev_blob,
+                           uint64_t blob_capacity, void* dev_workspace, uint64_t workspace_bytes,
+                           void* stream, uint64_t* dev_size);
+
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);
 
-/* wc_version -- ABI version of this header (2). */
+/* wc_version -- ABI version of this header (3). */
 int32_t wc_version(void);
 
 #ifdef __cplusplus

@@ -1,0 +1,864 @@
+// wc_encode.hip -- device half of libwc's encoder and analysis for CDNA4 (gfx950).
+//
+// Paper: Sec. II-B (per-tensor histograms and empirical entropy over symbols
+// the numeric format defines), Sec. V-B (offline compression: a static table
+// per tensor or layer, every tile an independently decodable ANS substream
+// from its own initial state, an offset index), Sec. VI-F (b = 12).
+//
+// wc_encode_device writes, on the GPU, the same blob bytes as the host
+// encoder.  Its launches, in stream order:
+//   1. zero the histograms;
+//   2. histograms of the coded symbols (workgroup-private LDS histograms,
+//      replicated so that lanes with the same symbol hit different banks,
+//      flushed with 64-bit atomics), into the table each tensor uses;
+//   3. normalisation to 2^12 (one workgroup per table, integer largest
+//      remainder exactly as the host does it), the u16 tables written into the
+//      blob, and per symbol {f, cum, ceil(2^64 / f)} for the encoder;
+//   4. the chunk encoder: one wave per chunk, one rANS lane per wave lane,
+//      steps in reverse.  Within a step the lanes that emit a word push it in
+//      decreasing lane order (ballot; a lane's place is the number of emitting
+//      lanes above it), so the word stack, written downwards from the end of
+//      the chunk's worst-case workspace slot, is the chunk's stream in order;
+//   5. the offset index: one workgroup scans the record sizes and writes the
+//      index and the header;
+//   6. the descriptors (their raw-region offsets follow from the scan);
+//   7. packing: every chunk's record copied from its slot to its place, and
+//      the raw sign|mantissa bytes of 16-bit formats written in coding order.
+// The symbols' loads follow the decoder's layout: a lane-group of W symbols
+// is 16 bytes of the source, wherever the tiling puts it.
+#include <hip/hip_runtime.h>
+
+#include <string.h>
+
+#include <algorithm>
+#include <vector>
+
+#include "wc_internal.h"
+
+namespace {
+
+constexpr int kWaves = 8;  // chunks (waves) per encoder / packer workgroup
+constexpr int kThreads = kWaves * 64;
+constexpr int kHistThreads = 256;
+constexpr int kHistReps = 8;                 // LDS histogram copies (lane & 7)
+constexpr int kHistStride = 257;             // odd stride: copies of a bin in different banks
+constexpr uint64_t kHistSpan = 256u << 10;   // source bytes per histogram workgroup
+constexpr int kMaxLaunch = 16;               // tensors per launch
+constexpr int kScanThreads = 1024;
+
+enum Kind : uint32_t { kSplit16 = 0, kByte = 1, kNibble = 2 };
+
+struct EncTensor {
+  uint64_t src;             // device pointer of the tensor's bytes
+  uint64_t src_bytes;
+  uint64_t n_sym;
+  uint64_t slot_off;        // workspace offset of chunk 0's slot
+  uint64_t raw_rel;         // raw region, relative to the first raw region
+  uint64_t pitch;           // tiled: bytes of one matrix row
+  uint64_t tile_row_bytes;  // tiled: bytes of one tile row
+  uint32_t slot_bytes;      // bytes of one chunk's slot
+  uint32_t first_chunk, n_chunks, per, chunk_bytes;
+  uint32_t kind, logW, lanes;
+  uint32_t table;           // table index in the workspace
+  uint32_t wg0;             // first workgroup of the tensor in this launch
+  uint32_t tiled, tile_r, log_tc, ntc, order, log_tr;
+};
+
+struct EncArgs {
+  uint64_t blob, ws;
+  uint64_t hist_off, tab_off, rsz_off, misc_off;
+  uint64_t index_off;  // blob offset of the chunk index
+  uint32_t n_tensors, pad;
+  EncTensor t[kMaxLaunch];
+};
+
+__device__ __forceinline__ uint64_t dpad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
+
+// 16 source bytes at `off`, zeros past `bytes`.
+__device__ __forceinline__ uint4 load16(const uint8_t* base, uint64_t bytes, uint64_t off) {
+  if (off + 16 <= bytes) return *reinterpret_cast<const uint4*>(base + off);
+  uint32_t d[4] = {0u, 0u, 0u, 0u};
+  for (uint32_t b = 0; b < 16; b++)
+    if (off + b < bytes) d[b >> 2] |= uint32_t(base[off + b]) << (8 * (b & 3));
+  return make_uint4(d[0], d[1], d[2], d[3]);
+}
+
+__device__ __forceinline__ uint32_t dword(const uint4& v, uint32_t j) {
+  return j == 0 ? v.x : (j == 1 ? v.y : (j == 2 ? v.z : v.w));
+}
+
+// Coded symbol k of a lane-group (k a compile-time constant after unrolling).
+template <uint32_t K>
+__device__ __forceinline__ uint32_t symbol(const uint4& v, uint32_t k) {
+  if constexpr (K == kSplit16) return (dword(v, k >> 1) >> (16 * (k & 1) + 7)) & 0xFFu;
+  else if constexpr (K == kByte) return (dword(v, k >> 2) >> (8 * (k & 3))) & 0xFFu;
+  else return (dword(v, k >> 3) >> (4 * (k & 7))) & 0xFu;
+}
+
+// Byte offset in the source of the lane-group that starts at symbol i0 of
+// chunk c: a byte run, or the lane-group's place in its tile.
+__device__ __forceinline__ uint64_t group_offset(const EncTensor& T, uint32_t c, uint32_t i0) {
+  if (!T.tiled) return uint64_t(c) * T.chunk_bytes + uint64_t(i0 >> T.logW) * 16u;
+  const uint64_t base =
+      uint64_t(c / T.ntc) * T.tile_r * T.pitch + uint64_t(c % T.ntc) * T.tile_row_bytes;
+  if (T.order == 0)
+    return base + uint64_t(i0 >> T.log_tc) * T.pitch +
+           uint64_t((i0 & ((1u << T.log_tc) - 1u)) >> T.logW) * 16u;
+  const uint32_t g = i0 >> T.logW;  // row g mod tile_r of k-block g div tile_r
+  return base + uint64_t(g & ((1u << T.log_tr) - 1u)) * T.pitch + uint64_t(g >> T.log_tr) * 16u;
+}
+
+__device__ __forceinline__ uint32_t tensor_of(const EncArgs& a, uint32_t wg) {
+  uint32_t ti = 0;
+  for (uint32_t k = 1; k < a.n_tensors; k++)
+    if (wg >= a.t[k].wg0) ti = k;
+  return ti;
+}
+
+// ---------------------------------------------------------------------------
+// 1. zero fill (no memset node, so a captured graph can replay it)
+
+__global__ void zero_kernel(uint4* p, uint64_t n16) {
+  for (uint64_t i = blockIdx.x * uint64_t(blockDim.x) + threadIdx.x; i < n16;
+       i += uint64_t(gridDim.x) * blockDim.x)
+    p[i] = make_uint4(0u, 0u, 0u, 0u);
+}
+
+// ---------------------------------------------------------------------------
+// 2. coded-symbol histograms.  Workgroup w of a tensor counts source bytes
+// [w * kHistSpan, +kHistSpan); symbol order does not matter here.
+
+template <uint32_t K>
+__device__ void count_span(const EncTensor& T, uint64_t off0, uint64_t off1, uint32_t* h) {
+  const uint8_t* src = reinterpret_cast<const uint8_t*>(T.src);
+  const uint32_t rep = (threadIdx.x & (kHistReps - 1)) * kHistStride;
+  constexpr uint32_t W = K == kSplit16 ? 8u : (K == kByte ? 16u : 32u);
+  for (uint64_t off = off0 + threadIdx.x * 16ull; off < off1; off += kHistThreads * 16ull) {
+    const uint4 v = load16(src, T.src_bytes, off);
+    // symbols whose bytes lie inside the tensor
+    const uint64_t left = T.src_bytes - off;
+    const uint32_t nv = left >= 16 ? W : uint32_t(left * W / 16);
+#pragma unroll
+    for (uint32_t k = 0; k < W; k++)
+      if (k < nv) atomicAdd(&h[rep + symbol<K>(v, k)], 1u);
+  }
+}
+
+__global__ __launch_bounds__(kHistThreads) void hist_kernel(EncArgs a) {
+  __shared__ uint32_t h[kHistReps * kHistStride];
+  for (uint32_t i = threadIdx.x; i < kHistReps * kHistStride; i += kHistThreads) h[i] = 0;
+  __syncthreads();
+  const EncTensor& T = a.t[tensor_of(a, blockIdx.x)];
+  const uint64_t off0 = uint64_t(blockIdx.x - T.wg0) * kHistSpan;
+  const uint64_t off1 = min<uint64_t>(off0 + kHistSpan, T.src_bytes);
+  if (T.kind == kSplit16) count_span<kSplit16>(T, off0, off1, h);
+  else if (T.kind == kByte) count_span<kByte>(T, off0, off1, h);
+  else count_span<kNibble>(T, off0, off1, h);
+  __syncthreads();
+  uint32_t c = 0;
+  for (int r = 0; r < kHistReps; r++) c += h[r * kHistStride + threadIdx.x];
+  unsigned long long* g =
+      reinterpret_cast<unsigned long long*>(a.ws + a.hist_off) + uint64_t(T.table) * 256u;
+  if (c) atomicAdd(g + threadIdx.x, (unsigned long long)c);
+}
+
+// Whole 16-bit words of a 16-bit tensor, bins [part * 16384, +16384) counted
+// in LDS (the 65 536 bins of the joint histogram take four passes).
+__global__ __launch_bounds__(1024) void word_hist_kernel(uint64_t src, uint64_t bytes,
+                                                         uint64_t hist, uint32_t part) {
+  __shared__ uint32_t wh[16384];
+  for (uint32_t i = threadIdx.x; i < 16384; i += blockDim.x) wh[i] = 0;
+  __syncthreads();
+  const uint8_t* p = reinterpret_cast<const uint8_t*>(src);
+  const uint64_t stride = uint64_t(gridDim.x) * blockDim.x * 16;
+  for (uint64_t off = (uint64_t(blockIdx.x) * blockDim.x + threadIdx.x) * 16; off < bytes;
+       off += stride) {
+    const uint4 v = load16(p, bytes, off);
+    const uint32_t nw = bytes - off >= 16 ? 8u : uint32_t((bytes - off) / 2);
+#pragma unroll
+    for (uint32_t k = 0; k < 8; k++) {
+      const uint32_t w = (dword(v, k >> 1) >> (16 * (k & 1))) & 0xFFFFu;
+      if (k < nw && (w >> 14) == part) atomicAdd(&wh[w & 0x3FFFu], 1u);
+    }
+  }
+  __syncthreads();
+  unsigned long long* g = reinterpret_cast<unsigned long long*>(hist) + part * 16384u;
+  for (uint32_t i = threadIdx.x; i < 16384; i += blockDim.x)
+    if (wh[i]) atomicAdd(g + i, (unsigned long long)wh[i]);
+}
+
+// ---------------------------------------------------------------------------
+// 3. normalisation to 2^12 (Sec. VI-F): f = floor(c * 4096 / n); present
+// symbols at least 1 (forced); a shortfall d goes +1 each to the d largest
+// remainders among the unforced (lower symbol on ties); an excess comes off
+// the largest f one unit at a time (lower symbol on ties).
+
+struct NormTable {
+  uint64_t freq_off;  // blob offset of the u16 table
+  uint32_t table, alphabet;
+};
+
+struct NormArgs {
+  uint64_t blob, ws, hist_off, tab_off;
+  uint32_t n_tables, pad;
+  NormTable t[64];
+};
+
+__global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
+  __shared__ unsigned long long rem[256];
+  __shared__ uint32_t cand[256];
+  __shared__ uint32_t red[256];
+  __shared__ unsigned long long nsum;
+  const NormTable& NT = a.t[blockIdx.x];
+  const uint32_t s = threadIdx.x;
+  const unsigned long long* hg =
+      reinterpret_cast<const unsigned long long*>(a.ws + a.hist_off) + uint64_t(NT.table) * 256u;
+  const unsigned long long c = s < NT.alphabet ? hg[s] : 0ull;
+  if (s == 0) nsum = 0;
+  __syncthreads();
+  atomicAdd(&nsum, c);
+  __syncthreads();
+  const unsigned long long n = nsum;
+  uint32_t f = 0;
+  bool forced = false;
+  unsigned long long r = 0;
+  if (n && c) {
+    const unsigned long long scaled = c * wc::kTableSize;
+    f = uint32_t(scaled / n);
+    r = scaled % n;
+    if (f == 0) {
+      f = 1;
+      forced = true;
+    }
+  }
+  rem[s] = r;
+  cand[s] = (c && !forced) ? 1u : 0u;
+  red[s] = f;
+  __syncthreads();
+  for (uint32_t w = 128; w > 0; w >>= 1) {
+    if (s < w) red[s] += red[s + w];
+    __syncthreads();
+  }
+  int d = n ? int(wc::kTableSize) - int(red[0]) : 0;
+  __syncthreads();
+  if (d > 0 && cand[s]) {
+    // place of this candidate in (remainder descending, symbol ascending)
+    uint32_t rank = 0;
+    for (uint32_t t = 0; t < 256; t++)
+      rank += cand[t] && (rem[t] > r || (rem[t] == r && t < s)) ? 1u : 0u;
+    if (rank < uint32_t(d)) f += 1;
+  }
+  while (d < 0) {
+    // the largest f, lowest symbol on ties: reduce (f << 8 | 255 - s)
+    red[s] = (f << 8) | (255u - s);
+    __syncthreads();
+    for (uint32_t w = 128; w > 0; w >>= 1) {
+      if (s < w) red[s] = max(red[s], red[s + w]);
+      __syncthreads();
+    }
+    if (s == 255u - (red[0] & 0xFFu)) f -= 1;
+    d++;
+    __syncthreads();
+  }
+  // u16 table into the blob; cum and the reciprocal for the encoder
+  if (s < NT.alphabet) reinterpret_cast<uint16_t*>(a.blob + NT.freq_off)[s] = uint16_t(f);
+  red[s] = f;
+  __syncthreads();
+  uint32_t cum = 0;
+  for (uint32_t t = 0; t < s; t++) cum += red[t];
+  // ceil(2^64 / f) = floor((2^64 - 1) / f) + 1 for f >= 2; 0 marks f == 1
+  const unsigned long long rc = f > 1 ? ~0ull / f + 1 : 0ull;
+  uint4* tab = reinterpret_cast<uint4*>(a.ws + a.tab_off) + uint64_t(NT.table) * 256u;
+  tab[s] = make_uint4(f, cum, uint32_t(rc), uint32_t(rc >> 32));
+}
+
+// ---------------------------------------------------------------------------
+// 4. chunk encoder.  Symbol i of a chunk is lane (i mod L*W) div W's symbol at
+// step (i div L*W)*W + i mod W.  Steps run from the last to the first; in a
+// step every active lane with x >= f * 2^20 emits its low 16 bits (x >>= 16)
+// and then x = floor(x / f) * 2^12 + x mod f + cum.  The quotient uses the
+// 64-bit reciprocal r = ceil(2^64 / f): floor(x * r / 2^64) = floor(x / f) for
+// x < 2^32 (the error x * (r - 2^64 / f) / 2^64 is below 1 / f), computed as
+// (x * r_hi + mulhi(x, r_lo)) >> 32.
+
+template <uint32_t K>
+__device__ void encode_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, uint32_t lane,
+                             const uint4* __restrict__ tab) {
+  constexpr uint32_t W = K == kSplit16 ? 8u : (K == kByte ? 16u : 32u);
+  const uint8_t* src = reinterpret_cast<const uint8_t*>(T.src);
+  const uint64_t s0 = uint64_t(c) * T.per;
+  const uint32_t n_c = uint32_t(min<uint64_t>(T.per, T.n_sym - s0));
+  const uint32_t L = T.lanes;
+  const uint32_t A = min(L, (n_c + W - 1) / W);
+  const uint32_t LW = L * W;
+  const uint32_t rows = (n_c + LW - 1) / LW;
+  uint8_t* slot = reinterpret_cast<uint8_t*>(a.ws + T.slot_off) + uint64_t(c) * T.slot_bytes;
+  uint16_t* stack_end = reinterpret_cast<uint16_t*>(slot + T.slot_bytes);
+  uint32_t x = wc::kStateLow;
+  uint32_t top = 0;  // words pushed
+  for (uint32_t r = rows; r-- > 0;) {
+    const uint32_t i0 = r * LW + lane * W;
+    const bool lane_ok = lane < L && i0 < n_c;
+    const uint32_t nv = lane_ok ? min(W, n_c - i0) : 0u;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (lane_ok) v = load16(src, T.src_bytes, group_offset(T, c, i0));
+#pragma unroll
+    for (uint32_t kk = 0; kk < W; kk++) {
+      const uint32_t k = W - 1 - kk;
+      const bool active = k < nv;
+      const uint4 e = tab[symbol<K>(v, k)];  // {f, cum, r_lo, r_hi}
+      const bool emit = active && (x >> 20) >= e.x;
+      const uint64_t m = __ballot(emit);
+      const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+          uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
+      const uint32_t total = uint32_t(__popcll(m));
+      // pushed after the emitting lanes above this one (total - below - 1)
+      if (emit) stack_end[-int(top + total - below)] = uint16_t(x);
+      top += total;
+      const uint32_t v2 = emit ? x >> 16 : x;
+      const uint32_t q =
+          e.x == 1u ? v2 : uint32_t((uint64_t(v2) * e.w + __umulhi(v2, e.z)) >> 32);
+      const uint32_t xn = (q << wc::kProbBits) + (v2 - q * e.x) + e.y;
+      x = active ? xn : x;
+    }
+  }
+  // record header, states and their padding at the slot's start
+  uint32_t* hdr = reinterpret_cast<uint32_t*>(slot);
+  if (lane == 0) *reinterpret_cast<uint4*>(hdr) = make_uint4(top, A, n_c, 0u);
+  const uint32_t padA = uint32_t(dpad16(4ull * A) / 4);
+  if (lane < padA) hdr[4 + lane] = lane < A ? x : 0u;
+  if (lane == 0) {
+    const uint32_t bytes = 16u + 4u * padA + uint32_t(dpad16(2ull * top));
+    reinterpret_cast<uint32_t*>(a.ws + a.rsz_off)[T.first_chunk + c] = bytes / 16u;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void encode_kernel(EncArgs a) {
+  __shared__ uint4 tab[256];
+  const EncTensor& T = a.t[tensor_of(a, blockIdx.x)];
+  const uint4* tg = reinterpret_cast<const uint4*>(a.ws + a.tab_off) + uint64_t(T.table) * 256u;
+  if (threadIdx.x < 256) tab[threadIdx.x] = tg[threadIdx.x];
+  __syncthreads();
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t c = (blockIdx.x - T.wg0) * kWaves + wave;
+  if (c >= T.n_chunks) return;
+  const uint32_t lane = __lane_id();
+  if (T.kind == kSplit16) encode_chunk<kSplit16>(a, T, c, lane, tab);
+  else if (T.kind == kByte) encode_chunk<kByte>(a, T, c, lane, tab);
+  else encode_chunk<kNibble>(a, T, c, lane, tab);
+}
+
+// ---------------------------------------------------------------------------
+// 5. offset index: exclusive scan of the record sizes (16-byte units) from the
+// records' start; then the header, with the size and raw offset it implies.
+
+struct ScanArgs {
+  uint64_t blob, ws, rsz_off, misc_off, size_out;
+  uint64_t index_off, records_off, raw_region_bytes, n_chunks;
+  uint32_t header[16];  // the header with size and raw offset still 0
+};
+
+__global__ __launch_bounds__(kScanThreads) void scan_kernel(ScanArgs a) {
+  __shared__ uint32_t wsum[kScanThreads / 64];
+  __shared__ uint64_t carry_s;
+  const uint32_t tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const uint32_t* rsz = reinterpret_cast<const uint32_t*>(a.ws + a.rsz_off);
+  uint32_t* index = reinterpret_cast<uint32_t*>(a.blob + a.index_off);
+  const uint64_t rec16 = a.records_off / 16;
+  if (tid == 0) carry_s = 0;
+  __syncthreads();
+  for (uint64_t base = 0; base < a.n_chunks; base += kScanThreads) {
+    const uint64_t g = base + tid;
+    const uint32_t v = g < a.n_chunks ? rsz[g] : 0u;
+    uint32_t incl = v;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const uint32_t u = __shfl_up(incl, d, 64);
+      if ((int)lane >= d) incl += u;
+    }
+    if (lane == 63) wsum[wave] = incl;
+    __syncthreads();
+    uint32_t before = 0;
+    for (uint32_t w = 0; w < wave; w++) before += wsum[w];
+    const uint64_t carry = carry_s;
+    if (g < a.n_chunks) index[g] = uint32_t(rec16 + carry + before + incl - v);
+    __syncthreads();
+    if (tid == kScanThreads - 1) carry_s = carry + before + incl;
+    __syncthreads();
+  }
+  const uint64_t raw_start = a.records_off + 16 * carry_s;
+  const uint64_t size = raw_start + a.raw_region_bytes;
+  if (tid == 0) {
+    index[a.n_chunks] = uint32_t(raw_start / 16);
+    reinterpret_cast<uint64_t*>(a.ws + a.misc_off)[0] = raw_start;
+    *reinterpret_cast<uint64_t*>(a.size_out) = size;
+  }
+  // zeros between the index and the records
+  uint8_t* b = reinterpret_cast<uint8_t*>(a.blob);
+  for (uint64_t o = a.index_off + 4 * (a.n_chunks + 1) + tid; o < a.records_off; o += kScanThreads)
+    b[o] = 0;
+  if (tid < 16) {
+    uint32_t h = a.header[tid];
+    if (tid == 6) h = uint32_t(size);  // bytes 24..31: size
+    if (tid == 7) h = uint32_t(size >> 32);
+    if (tid == 12) h = uint32_t(raw_start);  // bytes 48..55: raw region
+    if (tid == 13) h = uint32_t(raw_start >> 32);
+    reinterpret_cast<uint32_t*>(a.blob)[tid] = h;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 6. descriptors: 96 bytes per tensor from the host, raw offsets rebased on
+// the raw regions' start.
+
+struct DescArgs {
+  uint64_t blob, ws, misc_off;
+  uint32_t first, n;
+  uint32_t raw_mask;  // tensors (bit i: first + i) with a raw region
+  uint32_t pad;
+  uint32_t d[kMaxLaunch * 2][24];
+};
+
+__global__ void desc_kernel(DescArgs a) {
+  const uint32_t t = threadIdx.x / 24, j = threadIdx.x % 24;
+  if (t >= a.n) return;
+  const uint64_t raw_start = reinterpret_cast<const uint64_t*>(a.ws + a.misc_off)[0];
+  uint32_t v = a.d[t][j];
+  if ((a.raw_mask >> t) & 1u) {
+    // bytes 56..63: raw offset (relative to the raw regions' start in d)
+    const uint64_t rel = uint64_t(a.d[t][14]) | (uint64_t(a.d[t][15]) << 32);
+    const uint64_t abs = raw_start + rel;
+    if (j == 14) v = uint32_t(abs);
+    if (j == 15) v = uint32_t(abs >> 32);
+  }
+  reinterpret_cast<uint32_t*>(a.blob + wc::kHeaderBytes + uint64_t(wc::kDescBytes) * (a.first + t))[j] =
+      v;
+}
+
+// ---------------------------------------------------------------------------
+// 7. packing: one wave per chunk moves its record from the slot to the offset
+// the index gives (words re-based from the stack's end, zero padding), and
+// for 16-bit formats writes the chunk's raw bytes at their coding-order place.
+
+template <uint32_t K>
+__device__ void pack_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, uint32_t lane) {
+  constexpr uint32_t W = K == kSplit16 ? 8u : (K == kByte ? 16u : 32u);
+  const uint32_t g = T.first_chunk + c;
+  uint8_t* blob = reinterpret_cast<uint8_t*>(a.blob);
+  const uint64_t o = 16ull * reinterpret_cast<const uint32_t*>(a.blob + a.index_off)[g];
+  const uint8_t* slot = reinterpret_cast<const uint8_t*>(a.ws + T.slot_off) + uint64_t(c) * T.slot_bytes;
+  const uint4 hdr = *reinterpret_cast<const uint4*>(slot);
+  const uint32_t nw = hdr.x, A = hdr.y, n_c = hdr.z;
+  const uint32_t head = 16u + uint32_t(dpad16(4ull * A));
+  // header and states (16-byte units)
+  for (uint32_t j = lane; j < head / 16; j += 64)
+    *reinterpret_cast<uint4*>(blob + o + 16ull * j) = reinterpret_cast<const uint4*>(slot)[j];
+  // words: the stack's last nw u16 of the slot, then zeros to 16 bytes
+  const uint16_t* words = reinterpret_cast<const uint16_t*>(slot + T.slot_bytes) - nw;
+  const uint32_t units = uint32_t(dpad16(2ull * nw) / 16);
+  for (uint32_t j = lane; j < units; j += 64) {
+    uint32_t d[4];
+#pragma unroll
+    for (uint32_t q = 0; q < 4; q++) {
+      const uint32_t k = 8 * j + 2 * q;
+      const uint32_t lo = k < nw ? words[k] : 0u, hi = k + 1 < nw ? words[k + 1] : 0u;
+      d[q] = lo | (hi << 16);
+    }
+    *reinterpret_cast<uint4*>(blob + o + head + 16ull * j) = make_uint4(d[0], d[1], d[2], d[3]);
+  }
+  if constexpr (K == kSplit16) {
+    // raw byte of a word: bit 15 -> bit 7, bits 6..0 kept
+    const uint64_t raw_start = reinterpret_cast<const uint64_t*>(a.ws + a.misc_off)[0];
+    uint8_t* raw = blob + raw_start + T.raw_rel + uint64_t(c) * T.per;
+    const uint8_t* src = reinterpret_cast<const uint8_t*>(T.src);
+    const uint32_t groups = (n_c + W - 1) / W;
+    for (uint32_t gi = lane; gi < groups; gi += 64) {
+      const uint32_t i0 = gi * W;
+      const uint4 v = load16(src, T.src_bytes, group_offset(T, c, i0));
+      uint32_t rb[2] = {0u, 0u};
+#pragma unroll
+      for (uint32_t k = 0; k < 8; k++) {
+        const uint32_t w = (dword(v, k >> 1) >> (16 * (k & 1))) & 0xFFFFu;
+        const uint32_t r = ((w >> 8) & 0x80u) | (w & 0x7Fu);
+        rb[k >> 2] |= r << (8 * (k & 3));
+      }
+      const uint32_t nv = min(W, n_c - i0);
+      if (nv == W) {
+        *reinterpret_cast<uint2*>(raw + i0) = make_uint2(rb[0], rb[1]);
+      } else {
+        for (uint32_t k = 0; k < nv; k++) raw[i0 + k] = uint8_t(rb[k >> 2] >> (8 * (k & 3)));
+      }
+    }
+    if (c + 1 == T.n_chunks) {
+      // the raw region's zero padding to 16 bytes
+      uint8_t* end = blob + raw_start + T.raw_rel;
+      const uint64_t padded = dpad16(T.n_sym);
+      if (lane < padded - T.n_sym) end[T.n_sym + lane] = 0;
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void pack_kernel(EncArgs a) {
+  const EncTensor& T = a.t[tensor_of(a, blockIdx.x)];
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const uint32_t c = (blockIdx.x - T.wg0) * kWaves + wave;
+  if (c >= T.n_chunks) return;
+  const uint32_t lane = __lane_id();
+  if (T.kind == kSplit16) pack_chunk<kSplit16>(a, T, c, lane);
+  else if (T.kind == kByte) pack_chunk<kByte>(a, T, c, lane);
+  else pack_chunk<kNibble>(a, T, c, lane);
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// Host side.
+
+namespace {
+
+using wc::Plan;
+using wc::TensorInfo;
+
+struct WsLayout {
+  uint64_t hist_off, tab_off, rsz_off, misc_off, slots_off, total;
+  std::vector<uint64_t> slot_off;     // per tensor
+  std::vector<uint32_t> table_of;     // per tensor: its table's index
+  uint32_t n_tables;
+};
+
+inline uint64_t up256(uint64_t x) { return (x + 255) & ~uint64_t(255); }
+
+uint32_t slot_bytes_of(const TensorInfo& T) { return uint32_t(wc::worst_record(T, T.sym_per_chunk())); }
+
+void layout_ws(const Plan& P, WsLayout& L) {
+  const uint32_t n = uint32_t(P.tensors.size());
+  L.table_of.assign(n, 0);
+  L.n_tables = 0;
+  for (uint32_t t = 0; t < n; t++)
+    L.table_of[t] = P.owner[t] == t ? L.n_tables++ : L.table_of[P.owner[t]];
+  uint64_t pos = 0;
+  L.hist_off = pos;
+  pos = up256(pos + 8ull * 256 * L.n_tables);
+  L.tab_off = pos;
+  pos = up256(pos + 16ull * 256 * L.n_tables);
+  L.rsz_off = pos;
+  pos = up256(pos + 4 * (P.n_chunks + 1));
+  L.misc_off = pos;
+  pos = up256(pos + 16);
+  L.slots_off = pos;
+  L.slot_off.assign(n, 0);
+  for (uint32_t t = 0; t < n; t++) {
+    L.slot_off[t] = pos;
+    pos = up256(pos + P.tensors[t].n_chunks * uint64_t(slot_bytes_of(P.tensors[t])));
+  }
+  L.total = pos;
+}
+
+uint32_t kind_of(uint32_t dt) {
+  return wc::is_nibble(dt) ? kNibble : (wc::is_byte(dt) ? kByte : kSplit16);
+}
+
+void fill_enc(EncTensor& E, const TensorInfo& T, const wc_dtensor& D, const WsLayout& L,
+              uint32_t t) {
+  E = EncTensor{};
+  E.src = reinterpret_cast<uint64_t>(D.dev_ptr);
+  E.src_bytes = T.out_bytes;
+  E.n_sym = T.n_sym;
+  E.slot_off = L.slot_off[t];
+  E.raw_rel = T.raw_off;  // relative in the plan
+  E.slot_bytes = slot_bytes_of(T);
+  E.first_chunk = uint32_t(T.first_chunk);
+  E.n_chunks = uint32_t(T.n_chunks);
+  E.per = uint32_t(T.sym_per_chunk());
+  E.chunk_bytes = T.chunk_bytes;
+  E.kind = kind_of(T.dtype);
+  E.logW = uint32_t(__builtin_ctz(T.group));
+  E.lanes = T.lanes;
+  E.table = L.table_of[t];
+  E.tiled = T.tile_r ? 1u : 0u;
+  if (E.tiled) {
+    E.tile_r = T.tile_r;
+    E.log_tc = uint32_t(__builtin_ctz(T.tile_c));
+    E.ntc = uint32_t(T.cols / T.tile_c);
+    E.pitch = T.cols * 16 / T.group;
+    E.tile_row_bytes = uint64_t(T.tile_c) * 16 / T.group;
+    E.order = T.tile_order;
+    E.log_tr = T.tile_order == WC_TILE_COLUMN_BLOCKS ? uint32_t(__builtin_ctz(T.tile_r)) : 0u;
+  }
+}
+
+void put32(uint32_t* d, uint32_t byte, uint32_t v) { d[byte / 4] = v; }
+void put64(uint32_t* d, uint32_t byte, uint64_t v) {
+  d[byte / 4] = uint32_t(v);
+  d[byte / 4 + 1] = uint32_t(v >> 32);
+}
+
+// The 96-byte descriptor of T as dwords (raw_off still relative).
+void descriptor(const TensorInfo& T, uint32_t* d) {
+  memset(d, 0, 96);
+  put32(d, 0, T.dtype);
+  put32(d, 4, T.chunk_bytes);
+  put64(d, 8, T.n_sym);
+  put64(d, 16, T.out_bytes);
+  put64(d, 24, T.first_chunk);
+  put64(d, 32, T.n_chunks);
+  d[10] = T.lanes | (T.group << 16) | (wc::kProbBits << 24);
+  d[11] = T.alphabet;
+  put64(d, 48, T.freq_off);
+  put64(d, 56, wc::has_raw(T.dtype) ? T.raw_off : 0);
+  put64(d, 64, T.rows);
+  put64(d, 72, T.cols);
+  put32(d, 80, T.tile_r);
+  put32(d, 84, T.tile_c);
+  put32(d, 88, T.tile_order);
+}
+
+wc_status plan_device(const wc_dtensor* t, uint32_t n, const wc_params* p, Plan& P,
+                      std::vector<wc_tensor>& hs) {
+  if (!t || !p || n == 0 || n > 65536) return WC_EINVAL;
+  hs.resize(n);
+  for (uint32_t i = 0; i < n; i++)
+    hs[i] = wc_tensor{t[i].dev_ptr, t[i].nbytes, t[i].dtype, 0, t[i].rows, t[i].cols};
+  return wc::plan_blob(hs.data(), n, p, P);
+}
+
+uint64_t capacity_of(const Plan& P) {
+  return P.records_off + P.worst_record_bytes + P.raw_region_bytes;
+}
+
+// Launch `kern` over the tensors in groups of kMaxLaunch, each tensor getting
+// `wgs_of(T)` workgroups.
+template <class WgsOf, class Launch>
+bool launch_groups(const Plan& P, const wc_dtensor* dt, const WsLayout& L, EncArgs& args,
+                   WgsOf wgs_of, Launch launch) {
+  const uint32_t n = uint32_t(P.tensors.size());
+  uint32_t t = 0;
+  while (t < n) {
+    uint32_t nt = 0, wgs = 0;
+    for (; t < n && nt < kMaxLaunch; t++) {
+      const TensorInfo& T = P.tensors[t];
+      const uint32_t w = wgs_of(T);
+      if (!w) continue;
+      fill_enc(args.t[nt], T, dt[t], L, t);
+      args.t[nt].wg0 = wgs;
+      nt++;
+      wgs += w;
+    }
+    if (!nt) break;
+    args.n_tensors = nt;
+    launch(wgs);
+    if (hipGetLastError() != hipSuccess) return false;
+  }
+  return true;
+}
+
+}  // namespace
+
+extern "C" wc_status wc_encode_device_bounds(const wc_dtensor* t, uint32_t n, const wc_params* p,
+                                             uint64_t* blob_capacity, uint64_t* workspace_bytes) {
+  if (!blob_capacity || !workspace_bytes) return WC_EINVAL;
+  try {
+    Plan P;
+    std::vector<wc_tensor> hs;
+    wc_status rc = plan_device(t, n, p, P, hs);
+    if (rc != WC_OK) return rc;
+    const uint64_t cap = capacity_of(P);
+    if (cap / 16 >= 0xFFFFFFFFull) return WC_EINVAL;
+    WsLayout L;
+    layout_ws(P, L);
+    *blob_capacity = cap;
+    *workspace_bytes = L.total;
+    return WC_OK;
+  } catch (...) {
+    return WC_ENOMEM;
+  }
+}
+
+extern "C" wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_params* p,
+                                      void* dev_blob, uint64_t blob_capacity, void* dev_workspace,
+                                      uint64_t workspace_bytes, void* stream, uint64_t* dev_size) {
+  if (!dev_blob || !dev_workspace || !dev_size) return WC_EINVAL;
+  if (reinterpret_cast<uintptr_t>(dev_blob) % 16 || reinterpret_cast<uintptr_t>(dev_workspace) % 16 ||
+      reinterpret_cast<uintptr_t>(dev_size) % 8)
+    return WC_EINVAL;
+  try {
+    Plan P;
+    std::vector<wc_tensor> hs;
+    wc_status rc = plan_device(t, n, p, P, hs);
+    if (rc != WC_OK) return rc;
+    for (uint32_t i = 0; i < n; i++)
+      if (t[i].nbytes && (!t[i].dev_ptr || reinterpret_cast<uintptr_t>(t[i].dev_ptr) % 16))
+        return WC_EINVAL;
+    const uint64_t cap = capacity_of(P);
+    if (cap / 16 >= 0xFFFFFFFFull || blob_capacity < cap) return WC_EINVAL;
+    WsLayout L;
+    layout_ws(P, L);
+    if (workspace_bytes < L.total) return WC_EINVAL;
+    const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    const uint64_t blob = reinterpret_cast<uint64_t>(dev_blob);
+    const uint64_t ws = reinterpret_cast<uint64_t>(dev_workspace);
+
+    // 1. histograms to zero
+    {
+      const uint64_t n16 = 8ull * 256 * L.n_tables / 16;
+      hipLaunchKernelGGL(zero_kernel, dim3(uint32_t(std::min<uint64_t>((n16 + 255) / 256, 4096))),
+                         dim3(256), 0, st, reinterpret_cast<uint4*>(ws + L.hist_off), n16);
+      if (hipGetLastError() != hipSuccess) return WC_EHIP;
+    }
+    EncArgs args{};
+    args.blob = blob;
+    args.ws = ws;
+    args.hist_off = L.hist_off;
+    args.tab_off = L.tab_off;
+    args.rsz_off = L.rsz_off;
+    args.misc_off = L.misc_off;
+    args.index_off = P.index_off;
+    // 2. histograms
+    if (!launch_groups(
+            P, t, L, args,
+            [](const TensorInfo& T) {
+              return uint32_t((T.out_bytes + kHistSpan - 1) / kHistSpan);
+            },
+            [&](uint32_t wgs) {
+              hipLaunchKernelGGL(hist_kernel, dim3(wgs), dim3(kHistThreads), 0, st, args);
+            }))
+      return WC_EHIP;
+    // 3. tables
+    {
+      NormArgs na{};
+      na.blob = blob;
+      na.ws = ws;
+      na.hist_off = L.hist_off;
+      na.tab_off = L.tab_off;
+      uint32_t k = 0;
+      for (uint32_t i = 0; i <= n; i++) {
+        // every table is written, all zeros when no symbol reaches it
+        if (i < n && P.owner[i] == i)
+          na.t[k++] = NormTable{P.tensors[i].freq_off, L.table_of[i], P.tensors[i].alphabet};
+        if (k == 64 || (i == n && k)) {
+          na.n_tables = k;
+          hipLaunchKernelGGL(norm_kernel, dim3(k), dim3(256), 0, st, na);
+          if (hipGetLastError() != hipSuccess) return WC_EHIP;
+          k = 0;
+        }
+      }
+    }
+    // 4. chunk encoder
+    if (!launch_groups(
+            P, t, L, args,
+            [](const TensorInfo& T) { return uint32_t((T.n_chunks + kWaves - 1) / kWaves); },
+            [&](uint32_t wgs) {
+              hipLaunchKernelGGL(encode_kernel, dim3(wgs), dim3(kThreads), 0, st, args);
+            }))
+      return WC_EHIP;
+    // 5. index and header
+    {
+      ScanArgs sa{};
+      sa.blob = blob;
+      sa.ws = ws;
+      sa.rsz_off = L.rsz_off;
+      sa.misc_off = L.misc_off;
+      sa.size_out = reinterpret_cast<uint64_t>(dev_size);
+      sa.index_off = P.index_off;
+      sa.records_off = P.records_off;
+      sa.raw_region_bytes = P.raw_region_bytes;
+      sa.n_chunks = P.n_chunks;
+      uint32_t* h = sa.header;
+      put32(h, 0, wc::kMagic);
+      h[1] = wc::kVersion | (wc::kHeaderBytes << 16);
+      put32(h, 8, n);
+      put32(h, 12, wc::kDescBytes);
+      put64(h, 16, P.n_chunks);
+      put64(h, 32, P.index_off);
+      put64(h, 40, P.records_off);
+      hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(kScanThreads), 0, st, sa);
+      if (hipGetLastError() != hipSuccess) return WC_EHIP;
+    }
+    // 6. descriptors
+    for (uint32_t t0 = 0; t0 < n; t0 += 2 * kMaxLaunch) {
+      DescArgs da{};
+      da.blob = blob;
+      da.ws = ws;
+      da.misc_off = L.misc_off;
+      da.first = t0;
+      da.n = std::min<uint32_t>(2 * kMaxLaunch, n - t0);
+      for (uint32_t i = 0; i < da.n; i++) {
+        const TensorInfo& T = P.tensors[t0 + i];
+        descriptor(T, da.d[i]);
+        if (wc::has_raw(T.dtype)) da.raw_mask |= 1u << i;
+      }
+      hipLaunchKernelGGL(desc_kernel, dim3(1), dim3(24 * 2 * kMaxLaunch), 0, st, da);
+      if (hipGetLastError() != hipSuccess) return WC_EHIP;
+    }
+    // 7. records and raw bytes
+    if (!launch_groups(
+            P, t, L, args,
+            [](const TensorInfo& T) { return uint32_t((T.n_chunks + kWaves - 1) / kWaves); },
+            [&](uint32_t wgs) {
+              hipLaunchKernelGGL(pack_kernel, dim3(wgs), dim3(kThreads), 0, st, args);
+            }))
+      return WC_EHIP;
+    return WC_OK;
+  } catch (...) {
+    return WC_ENOMEM;
+  }
+}
+
+extern "C" wc_status wc_analyze_device(const wc_dtensor* t, void* dev_workspace,
+                                       uint64_t workspace_bytes, void* stream, wc_stats* out) {
+  if (!t || !out || !dev_workspace || workspace_bytes < WC_ANALYZE_WORKSPACE_BYTES)
+    return WC_EINVAL;
+  const uint32_t dt = uint32_t(t->dtype);
+  if (!wc::dtype_ok(dt) || (wc::has_raw(dt) && t->nbytes % 2)) return WC_EINVAL;
+  if (t->nbytes && (!t->dev_ptr || reinterpret_cast<uintptr_t>(t->dev_ptr) % 16)) return WC_EINVAL;
+  if (reinterpret_cast<uintptr_t>(dev_workspace) % 16) return WC_EINVAL;
+  try {
+    const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+    const uint64_t ws = reinterpret_cast<uint64_t>(dev_workspace);
+    const bool words = wc::has_raw(dt);
+    const uint64_t bins = words ? 65536 : 256;
+    hipLaunchKernelGGL(zero_kernel, dim3(uint32_t((bins * 8 / 16 + 255) / 256)), dim3(256), 0, st,
+                       reinterpret_cast<uint4*>(ws), bins * 8 / 16);
+    if (hipGetLastError() != hipSuccess) return WC_EHIP;
+    if (t->nbytes) {
+      if (words) {
+        const uint32_t grid =
+            uint32_t(std::min<uint64_t>(std::max<uint64_t>((t->nbytes + kHistSpan - 1) / kHistSpan, 1), 1024));
+        for (uint32_t part = 0; part < 4; part++) {
+          hipLaunchKernelGGL(word_hist_kernel, dim3(grid), dim3(1024), 0, st,
+                             reinterpret_cast<uint64_t>(t->dev_ptr), t->nbytes, ws, part);
+          if (hipGetLastError() != hipSuccess) return WC_EHIP;
+        }
+      } else {
+        EncArgs a{};
+        a.ws = ws;
+        a.hist_off = 0;
+        a.n_tensors = 1;
+        EncTensor& E = a.t[0];
+        E.src = reinterpret_cast<uint64_t>(t->dev_ptr);
+        E.src_bytes = t->nbytes;
+        E.kind = kind_of(dt);
+        E.table = 0;
+        E.wg0 = 0;
+        hipLaunchKernelGGL(hist_kernel, dim3(uint32_t((t->nbytes + kHistSpan - 1) / kHistSpan)),
+                           dim3(kHistThreads), 0, st, a);
+        if (hipGetLastError() != hipSuccess) return WC_EHIP;
+      }
+    }
+    std::vector<uint64_t> h(bins);
+    if (hipMemcpyAsync(h.data(), dev_workspace, bins * 8, hipMemcpyDeviceToHost, st) != hipSuccess)
+      return WC_EHIP;
+    if (hipStreamSynchronize(st) != hipSuccess) return WC_EHIP;
+    memset(out, 0, sizeof(*out));
+    const uint64_t n_sym = wc::symbols_of(dt, t->nbytes);
+    if (words) {
+      wc::split_word_counts(h.data(), out);
+    } else {
+      for (uint32_t s = 0; s < 256; s++) out->hist[0][s] = h[s];
+    }
+    wc::finish_stats(dt, n_sym, words ? h.data() : nullptr, out);
+    return WC_OK;
+  } catch (...) {
+    return WC_ENOMEM;
+  }
+}

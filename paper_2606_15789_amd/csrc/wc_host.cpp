@@ -249,6 +249,115 @@ wc_blob* make_handle(BlobPriv&& bp) {
 }  // namespace
 
 // ---------------------------------------------------------------------------
+// Statistics from histograms (Sec. II-B).
+
+void finish_stats(uint32_t dt, uint64_t n, const uint64_t* joint16, wc_stats* out) {
+  out->n_fields = has_raw(dt) ? 2 : 1;
+  out->alphabet[0] = alphabet_of(dt);
+  out->alphabet[1] = has_raw(dt) ? 256 : 0;
+  out->count[0] = n;
+  out->count[1] = has_raw(dt) ? n : 0;
+  double bound = 0.0;
+  for (uint32_t f = 0; f < out->n_fields; f++) {
+    out->H[f] = entropy_bits(out->hist[f], out->alphabet[f]);
+    bound += double(n) * out->H[f] / 8.0;
+  }
+  out->bound_bytes = bound;
+  out->bound_bytes_raw8 = double(n) * out->H[0] / 8.0 + (has_raw(dt) ? double(n) : 0.0);
+  out->H_joint16 = joint16 ? entropy_bits(joint16, 65536) : NAN;
+}
+
+void split_word_counts(const uint64_t* joint16, wc_stats* out) {
+  for (uint32_t w = 0; w < 65536; w++) {
+    if (!joint16[w]) continue;
+    out->hist[0][(w >> 7) & 0xFF] += joint16[w];
+    out->hist[1][((w >> 8) & 0x80) | (w & 0x7F)] += joint16[w];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Blob layout (everything the data does not decide).
+
+wc_status plan_blob(const wc_tensor* ts, uint32_t n, const wc_params* prm, Plan& out) {
+  if (!ts || !prm || n == 0 || n > 65536) return WC_EINVAL;
+  const uint32_t CB = prm->chunk_bytes, L = prm->lanes;
+  const uint32_t TR = prm->tile_rows, TC = prm->tile_cols, TO = prm->tile_order;
+  if (CB < 256 || CB > (1u << 20) || CB % 256 || L < 1 || L > kMaxLanes ||
+      prm->prob_bits != kProbBits)
+    return WC_EINVAL;
+  if ((TR == 0) != (TC == 0) || (TC && !pow2(TC)) || prm->codebook > WC_CODEBOOK_LAYER ||
+      TO > WC_TILE_COLUMN_BLOCKS)
+    return WC_EINVAL;
+  for (uint32_t t = 0; t < n; t++) {
+    uint32_t dt = uint32_t(ts[t].dtype);
+    if (!dtype_ok(dt)) return WC_EINVAL;
+    if (has_raw(dt) && ts[t].nbytes % 2) return WC_EINVAL;
+    if ((ts[t].rows || ts[t].cols) && ts[t].rows * ts[t].cols != symbols_of(dt, ts[t].nbytes))
+      return WC_EINVAL;
+  }
+  const bool shared = prm->codebook == WC_CODEBOOK_LAYER;
+  out = Plan();
+  out.tensors.resize(n);
+  out.owner.resize(n);
+  uint64_t nc_total = 0;
+  for (uint32_t t = 0; t < n; t++) {
+    TensorInfo& T = out.tensors[t];
+    T.dtype = uint32_t(ts[t].dtype);
+    T.rows = ts[t].rows;
+    T.cols = ts[t].cols;
+    if (tile_ok(T.dtype, T.rows, T.cols, TR, TC, TO)) {
+      T.tile_r = TR;
+      T.tile_c = TC;
+      T.tile_order = TO;
+    }
+    T.chunk_bytes = T.tile_r ? uint32_t(tile_bytes(T.dtype, TR, TC)) : CB;
+    T.lanes = L;
+    T.group = group_of(T.dtype);
+    T.alphabet = alphabet_of(T.dtype);
+    T.out_bytes = ts[t].nbytes;
+    T.n_sym = symbols_of(T.dtype, T.out_bytes);
+    const uint64_t per = T.sym_per_chunk();
+    T.n_chunks = (T.n_sym + per - 1) / per;
+    T.first_chunk = nc_total;
+    nc_total += T.n_chunks;
+    // a full chunk's record, times the full chunks, plus the last one's
+    if (T.n_chunks)
+      out.worst_record_bytes += (T.n_chunks - 1) * worst_record(T, per) +
+                                worst_record(T, chunk_symbols(T, T.n_chunks - 1));
+  }
+  if (nc_total >= 0xFFFFFFFFull) return WC_EINVAL;
+  // tables: one per tensor, or the first tensor of each dtype owns its
+  // dtype's table (layer codebook)
+  uint64_t pos = kHeaderBytes + uint64_t(kDescBytes) * n;
+  for (uint32_t t = 0; t < n; t++) {
+    out.owner[t] = t;
+    if (shared)
+      for (uint32_t u = 0; u < t; u++)
+        if (out.tensors[u].dtype == out.tensors[t].dtype) {
+          out.owner[t] = u;
+          break;
+        }
+    TensorInfo& T = out.tensors[t];
+    if (out.owner[t] != t) {
+      T.freq_off = out.tensors[out.owner[t]].freq_off;
+      continue;
+    }
+    T.freq_off = pos;
+    pos += pad16(2ull * T.alphabet);
+  }
+  out.n_chunks = nc_total;
+  out.index_off = pad16(pos);
+  out.records_off = pad16(out.index_off + 4 * (nc_total + 1));
+  for (uint32_t t = 0; t < n; t++) {
+    TensorInfo& T = out.tensors[t];
+    if (!has_raw(T.dtype)) continue;
+    T.raw_off = out.raw_region_bytes;
+    out.raw_region_bytes += pad16(T.n_sym);
+  }
+  return WC_OK;
+}
+
+// ---------------------------------------------------------------------------
 // Blob validation.
 
 wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out) {
@@ -349,7 +458,7 @@ using namespace wc;
 
 extern "C" {
 
-int32_t wc_version(void) { return 2; }
+int32_t wc_version(void) { return 3; }
 
 wc_status wc_analyze(const wc_tensor* t, wc_stats* out) {
   if (!t || !out || (!t->host_ptr && t->nbytes)) return WC_EINVAL;
@@ -360,16 +469,8 @@ wc_status wc_analyze(const wc_tensor* t, wc_stats* out) {
     memset(out, 0, sizeof(*out));
     const uint8_t* src = static_cast<const uint8_t*>(t->host_ptr);
     uint64_t n = symbols_of(dt, t->nbytes);
-    out->n_fields = has_raw(dt) ? 2 : 1;
-    out->alphabet[0] = alphabet_of(dt);
-    out->count[0] = n;
-    out->H_joint16 = NAN;
     std::vector<uint64_t> h16;
-    if (has_raw(dt)) {
-      out->alphabet[1] = 256;
-      out->count[1] = n;
-      h16.assign(65536, 0);
-    }
+    if (has_raw(dt)) h16.assign(65536, 0);
     const uint64_t B = 1u << 16;
     uint8_t cbuf[1u << 16], rbuf[1u << 16];
     for (uint64_t s0 = 0; s0 < n; s0 += B) {
@@ -381,14 +482,7 @@ wc_status wc_analyze(const wc_tensor* t, wc_stats* out) {
         for (uint64_t i = s0; i < s1; i++) h16[src[2 * i] | (uint32_t(src[2 * i + 1]) << 8)]++;
       }
     }
-    double bound = 0.0;
-    for (uint32_t f = 0; f < out->n_fields; f++) {
-      out->H[f] = entropy_bits(out->hist[f], out->alphabet[f]);
-      bound += double(n) * out->H[f] / 8.0;
-    }
-    out->bound_bytes = bound;
-    out->bound_bytes_raw8 = double(n) * out->H[0] / 8.0 + (has_raw(dt) ? double(n) : 0.0);
-    if (has_raw(dt)) out->H_joint16 = entropy_bits(h16.data(), 65536);
+    finish_stats(dt, n, has_raw(dt) ? h16.data() : nullptr, out);
     return WC_OK;
   } catch (const std::bad_alloc&) {
     return WC_ENOMEM;
@@ -398,57 +492,23 @@ wc_status wc_analyze(const wc_tensor* t, wc_stats* out) {
 }
 
 wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_blob** out) {
-  if (!ts || !prm || !out || n == 0 || n > 65536) return WC_EINVAL;
+  if (!ts || !prm || !out) return WC_EINVAL;
   *out = nullptr;
-  const uint32_t CB = prm->chunk_bytes, L = prm->lanes;
-  const uint32_t TR = prm->tile_rows, TC = prm->tile_cols;
-  if (CB < 256 || CB > (1u << 20) || CB % 256 || L < 1 || L > kMaxLanes ||
-      prm->prob_bits != kProbBits)
-    return WC_EINVAL;
-  const uint32_t TO = prm->tile_order;
-  if ((TR == 0) != (TC == 0) || (TC && !pow2(TC)) || prm->codebook > WC_CODEBOOK_LAYER ||
-      TO > WC_TILE_COLUMN_BLOCKS)
-    return WC_EINVAL;
-  const bool shared = prm->codebook == WC_CODEBOOK_LAYER;
-  for (uint32_t t = 0; t < n; t++) {
-    uint32_t dt = uint32_t(ts[t].dtype);
-    if (!dtype_ok(dt)) return WC_EINVAL;
-    if (has_raw(dt) && ts[t].nbytes % 2) return WC_EINVAL;
+  for (uint32_t t = 0; t < n; t++)
     if (!ts[t].host_ptr && ts[t].nbytes) return WC_EINVAL;
-    if ((ts[t].rows || ts[t].cols) && ts[t].rows * ts[t].cols != symbols_of(dt, ts[t].nbytes))
-      return WC_EINVAL;
-  }
+  const uint32_t L = prm->lanes;
   const unsigned threads = thread_count(prm->n_threads);
   try {
+    Plan plan;
+    wc_status prc = plan_blob(ts, n, prm, plan);
+    if (prc != WC_OK) return prc;
     BlobPriv P;
-    P.tensors.resize(n);
+    P.tensors = plan.tensors;
+    const std::vector<uint32_t>& owner = plan.owner;
+    const uint64_t nc_total = plan.n_chunks;
     std::vector<std::vector<uint32_t>> freqs(n);
     std::vector<std::vector<uint8_t>> raws(n);
-    std::vector<Record> recs;
-    uint64_t nc_total = 0;
-    for (uint32_t t = 0; t < n; t++) {
-      TensorInfo& T = P.tensors[t];
-      T.dtype = uint32_t(ts[t].dtype);
-      T.rows = ts[t].rows;
-      T.cols = ts[t].cols;
-      if (tile_ok(T.dtype, T.rows, T.cols, TR, TC, TO)) {
-        T.tile_r = TR;
-        T.tile_c = TC;
-        T.tile_order = TO;
-      }
-      T.chunk_bytes = T.tile_r ? uint32_t(tile_bytes(T.dtype, TR, TC)) : CB;
-      T.lanes = L;
-      T.group = group_of(T.dtype);
-      T.alphabet = alphabet_of(T.dtype);
-      T.out_bytes = ts[t].nbytes;
-      T.n_sym = symbols_of(T.dtype, T.out_bytes);
-      uint64_t per = T.sym_per_chunk();
-      T.n_chunks = (T.n_sym + per - 1) / per;
-      T.first_chunk = nc_total;
-      nc_total += T.n_chunks;
-    }
-    if (nc_total >= 0xFFFFFFFFull) return WC_EINVAL;
-    recs.resize(nc_total);
+    std::vector<Record> recs(nc_total);
 
     // symbols in coding order (tile-major for tiled tensors) and histograms
     std::vector<std::vector<uint8_t>> codeds(n);
@@ -490,15 +550,8 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
 
     // tables: one per tensor, or one per dtype normalised from the summed
     // histogram of every tensor of that dtype (layer codebook)
-    std::vector<uint32_t> owner(n);
+    const bool shared = prm->codebook == WC_CODEBOOK_LAYER;
     for (uint32_t t = 0; t < n; t++) {
-      owner[t] = t;
-      if (shared)
-        for (uint32_t u = 0; u < t; u++)
-          if (P.tensors[u].dtype == P.tensors[t].dtype) {
-            owner[t] = u;
-            break;
-          }
       if (owner[t] != t) {
         freqs[t] = freqs[owner[t]];
         continue;
@@ -536,26 +589,16 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
       std::vector<uint8_t>().swap(codeds[t]);
     }
 
-    // layout
-    uint64_t pos = kHeaderBytes + uint64_t(kDescBytes) * n;
-    for (uint32_t t = 0; t < n; t++) {
-      if (owner[t] != t) {
-        P.tensors[t].freq_off = P.tensors[owner[t]].freq_off;
-        continue;
-      }
-      P.tensors[t].freq_off = pos;
-      pos += pad16(2ull * P.tensors[t].alphabet);
-    }
-    const uint64_t idx = pad16(pos);
-    const uint64_t rec = pad16(idx + 4 * (nc_total + 1));
-    pos = rec;
+    // layout: the plan fixed everything up to the records; the raw regions
+    // follow the records in tensor order
+    const uint64_t idx = plan.index_off;
+    const uint64_t rec = plan.records_off;
+    uint64_t pos = rec;
     for (auto& r : recs) pos += r.bytes.size();
     const uint64_t raw = pos;
     for (uint32_t t = 0; t < n; t++)
-      if (has_raw(P.tensors[t].dtype)) {
-        P.tensors[t].raw_off = pos;
-        pos += pad16(P.tensors[t].n_sym);
-      }
+      if (has_raw(P.tensors[t].dtype)) P.tensors[t].raw_off += raw;
+    pos = raw + plan.raw_region_bytes;
     const uint64_t total = pos;
     if (total / 16 >= 0xFFFFFFFFull) return WC_EINVAL;
 

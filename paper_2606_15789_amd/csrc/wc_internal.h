@@ -71,6 +71,44 @@ struct BlobHandle {
   BlobPriv priv;
 };
 
+// The data-independent part of a blob's layout, shared by the host encoder
+// (wc_encode) and the device encoder (wc_encode_device): per-tensor chunking
+// and tiling, the table each tensor uses and where it sits, the chunk index,
+// and where each raw region starts relative to the first one.  Everything
+// after the index depends on the coded data only through the records' total.
+struct Plan {
+  std::vector<TensorInfo> tensors;  // freq_off absolute; raw_off relative to the raw regions' start
+  std::vector<uint32_t> owner;      // tensor whose table a tensor uses (itself unless a layer codebook)
+  uint64_t n_chunks = 0, index_off = 0, records_off = 0;
+  uint64_t raw_region_bytes = 0;    // sum of pad16(n_sym) over the 16-bit tensors
+  uint64_t worst_record_bytes = 0;  // all records if every symbol emitted a word
+};
+
+// Validate the encoder parameters and tensor sizes (WC_EINVAL on any bad
+// field; the tensors' pointers are the caller's to check) and lay out the blob.
+wc_status plan_blob(const wc_tensor* ts, uint32_t n, const wc_params* p, Plan& out);
+
+// Symbols of chunk c of T, its lane-state count and its largest record.
+inline uint64_t chunk_symbols(const TensorInfo& T, uint64_t c) {
+  const uint64_t per = T.sym_per_chunk(), s0 = c * per;
+  return s0 >= T.n_sym ? 0 : (T.n_sym - s0 < per ? T.n_sym - s0 : per);
+}
+inline uint32_t chunk_states(const TensorInfo& T, uint64_t n_c) {
+  const uint64_t a = (n_c + T.group - 1) / T.group;
+  return uint32_t(a < T.lanes ? a : T.lanes);
+}
+inline uint64_t worst_record(const TensorInfo& T, uint64_t n_c) {
+  return 16 + pad16(4ull * chunk_states(T, n_c)) + pad16(2ull * n_c);
+}
+
+// Fill the rest of *out from out->hist (the field histograms of a tensor of
+// dtype dt with n symbols) and, for 16-bit formats, the 65 536 whole-word
+// counts `joint16` (NULL otherwise): entropies, bounds, joint entropy.
+void finish_stats(uint32_t dt, uint64_t n, const uint64_t* joint16, wc_stats* out);
+// Add whole-word counts of a 16-bit format into out->hist[0] (coded field,
+// bits 14..7) and out->hist[1] (raw field, bit 15 and bits 6..0).
+void split_word_counts(const uint64_t* joint16, wc_stats* out);
+
 // Validate `size` bytes at `p` and describe them.  Host-side checks of every
 // header field, table sum and index entry; WC_EINVAL on the first failure.
 wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out);

@@ -22,7 +22,9 @@ DERR = {1: "WC_DERR_INDEX", 2: "WC_DERR_STATE", 4: "WC_DERR_CURSOR", 8: "WC_DERR
 
 # Every function the header declares; the library must export all of them.
 EXPORTS = ["wc_analyze", "wc_encode", "wc_open", "wc_decode", "wc_gemv", "wc_free",
-           "wc_version"]
+           "wc_version", "wc_analyze_device", "wc_encode_device_bounds", "wc_encode_device"]
+
+ANALYZE_WORKSPACE_BYTES = 524288  # WC_ANALYZE_WORKSPACE_BYTES
 
 
 class WcError(RuntimeError):
@@ -86,6 +88,16 @@ def lib():
                               C.POINTER(C.c_uint32), C.POINTER(C.c_void_p), C.c_uint32,
                               C.POINTER(C.c_void_p), C.c_void_p, C.c_void_p]
         L.wc_gemv.restype = C.c_int
+        L.wc_analyze_device.argtypes = [C.POINTER(_Tensor), C.c_void_p, C.c_uint64, C.c_void_p,
+                                        C.POINTER(_Stats)]
+        L.wc_analyze_device.restype = C.c_int
+        L.wc_encode_device_bounds.argtypes = [C.POINTER(_Tensor), C.c_uint32, C.POINTER(_Params),
+                                              C.POINTER(C.c_uint64), C.POINTER(C.c_uint64)]
+        L.wc_encode_device_bounds.restype = C.c_int
+        L.wc_encode_device.argtypes = [C.POINTER(_Tensor), C.c_uint32, C.POINTER(_Params),
+                                       C.c_void_p, C.c_uint64, C.c_void_p, C.c_uint64,
+                                       C.c_void_p, C.c_void_p]
+        L.wc_encode_device.restype = C.c_int
         L.wc_free.argtypes = [C.POINTER(_Blob)]
         L.wc_free.restype = None
         L.wc_version.restype = C.c_int32
@@ -110,6 +122,10 @@ def analyze(dtype: str, data) -> dict:
     rc = lib().wc_analyze(C.byref(t), C.byref(st))
     if rc:
         raise WcError("wc_analyze", rc)
+    return _stats_dict(st)
+
+
+def _stats_dict(st) -> dict:
     nf = st.n_fields
     return {"n_fields": nf, "alphabet": [st.alphabet[i] for i in range(nf)],
             "count": [st.count[i] for i in range(nf)],
@@ -268,3 +284,88 @@ def gemv_torch(blob: Blob, dev_blob, tensors, xs, ys=None, stream=None, err=None
     gemv(blob, dev_blob.data_ptr(), list(tensors), [x.data_ptr() for x in xs], m,
          [y.data_ptr() for y in ys], stream.cuda_stream, err.data_ptr() if err is not None else 0)
     return ys
+
+
+# --- device-side analysis and encoder ----------------------------------------
+# wc_dtensor has wc_tensor's layout, with a device pointer in the first field.
+
+def _dtensors(entries):
+    """ctypes wc_dtensor array of (dtype, device tensor[, (rows, cols)]) entries."""
+    arr = (_Tensor * len(entries))()
+    for i, e in enumerate(entries):
+        x = e[1]
+        if not x.is_contiguous():
+            raise ValueError("device tensors must be contiguous")
+        nbytes = x.numel() * x.element_size()
+        rows, cols = e[2] if len(e) > 2 and e[2] is not None else (0, 0)
+        arr[i] = _Tensor(x.data_ptr() if nbytes else None, nbytes, DTYPES[e[0]], 0, rows, cols)
+    return arr
+
+
+def _params(chunk_bytes, lanes, tile, codebook, tile_order):
+    return _Params(chunk_bytes, lanes, 12, 0, tile[0], tile[1], CODEBOOKS[codebook], tile_order)
+
+
+def analyze_device(dtype: str, x, workspace=None, stream=None) -> dict:
+    """wc_analyze_device of a device tensor (synchronises `stream`)."""
+    import torch
+    t = _dtensors([(dtype, x)])
+    if workspace is None:
+        workspace = torch.empty(ANALYZE_WORKSPACE_BYTES, dtype=torch.uint8, device=x.device)
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device)
+    st = _Stats()
+    rc = lib().wc_analyze_device(t, C.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                 C.c_void_p(stream.cuda_stream or None), C.byref(st))
+    if rc:
+        raise WcError("wc_analyze_device", rc)
+    return _stats_dict(st)
+
+
+def encode_device_bounds(entries, chunk_bytes: int = 65536, lanes: int = 64, tile=(0, 0),
+                         codebook: str = "tensor", tile_order: int = 0):
+    """(blob capacity, workspace bytes) wc_encode_device needs.  `entries` are
+    (dtype, nbytes[, (rows, cols)]) or (dtype, tensor[, shape]) entries."""
+    arr = (_Tensor * len(entries))()
+    for i, e in enumerate(entries):
+        nb = e[1] if isinstance(e[1], int) else e[1].numel() * e[1].element_size()
+        rows, cols = e[2] if len(e) > 2 and e[2] is not None else (0, 0)
+        arr[i] = _Tensor(None, nb, DTYPES[e[0]], 0, rows, cols)
+    prm = _params(chunk_bytes, lanes, tile, codebook, tile_order)
+    cap, ws = C.c_uint64(), C.c_uint64()
+    rc = lib().wc_encode_device_bounds(arr, len(entries), C.byref(prm), C.byref(cap), C.byref(ws))
+    if rc:
+        raise WcError("wc_encode_device_bounds", rc)
+    return cap.value, ws.value
+
+
+def encode_device(entries, chunk_bytes: int = 65536, lanes: int = 64, tile=(0, 0),
+                  codebook: str = "tensor", tile_order: int = 0, blob=None, workspace=None,
+                  size=None, stream=None):
+    """wc_encode_device of (dtype, device tensor[, (rows, cols)]) entries.
+
+    Returns (blob, size): a uint8 device tensor of the capacity the bounds
+    give and an int64 device tensor of one element that receives the blob's
+    size; both are valid after `stream` (default: the current one) syncs.
+    """
+    import torch
+    dev = entries[0][1].device
+    cap, wsb = encode_device_bounds([(e[0], e[1]) + tuple(e[2:]) for e in entries], chunk_bytes,
+                                    lanes, tile, codebook, tile_order)
+    if blob is None:
+        blob = torch.empty(cap, dtype=torch.uint8, device=dev)
+    if workspace is None:
+        workspace = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    if size is None:
+        size = torch.zeros(1, dtype=torch.int64, device=dev)
+    if stream is None:
+        stream = torch.cuda.current_stream(dev)
+    arr = _dtensors(entries)
+    prm = _params(chunk_bytes, lanes, tile, codebook, tile_order)
+    rc = lib().wc_encode_device(arr, len(entries), C.byref(prm), C.c_void_p(blob.data_ptr()),
+                                blob.numel(), C.c_void_p(workspace.data_ptr()), workspace.numel(),
+                                C.c_void_p(stream.cuda_stream or None),
+                                C.c_void_p(size.data_ptr()))
+    if rc:
+        raise WcError("wc_encode_device", rc)
+    return blob, size

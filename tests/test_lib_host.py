@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (wc_\w+)", out))
     assert set(names) <= exported
-    assert lib.wc_version() == 2
+    assert lib.wc_version() == 3
 
 
 @pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16), (6, 8), (7, 8),
@@ -184,3 +184,44 @@ def test_gemv_rejects_before_any_launch():
         with pytest.raises(wc.WcError) as e:
             wc.gemv(b, 16, [0], [16], 1, [16])
         assert e.value.rc == -5
+
+
+def _pad16(x):
+    return (x + 15) // 16 * 16
+
+
+@pytest.mark.parametrize("lanes,cb,tile", [(64, 65536, (0, 0)), (32, 16384, (0, 0)),
+                                           (7, 256, (0, 0)), (64, 16384, (32, 128))])
+def test_device_encoder_bounds(lanes, cb, tile):
+    """wc_encode_device_bounds (host only): the capacity is the blob that every
+    coded symbol emitting a word would give, so any real blob fits in it."""
+    ts = synth.config(2, div=8) + synth.config(3, div=8)
+    entries = [(t.dtype, t.data, t.shape if len(t.shape) == 2 else None) for t in ts]
+    cap, ws = wc.encode_device_bounds([(d, a.nbytes, s) for d, a, s in entries], chunk_bytes=cb,
+                                      lanes=lanes, tile=tile)
+    b = wc.encode(entries, chunk_bytes=cb, lanes=lanes, tile=tile, threads=4)
+    assert b.size <= cap
+    worst = 0
+    W = {"bf16": 8, "fp16": 8, "u8": 16, "fp8_e4m3": 16, "fp8_e5m2": 16, "u4": 32,
+         "fp4_e2m1": 32}
+    for info, (dt, a, s) in zip(oracle.tensor_info(b.tobytes()), entries):
+        n_sym = a.nbytes * W[dt] // 16          # a lane-group of W symbols is 16 bytes
+        per = info["chunk_bytes"] * W[dt] // 16
+        for c in range(info["n_chunks"]):
+            n_c = min(per, n_sym - c * per)
+            A = min(lanes, -(-n_c // W[dt]))
+            worst += 16 + _pad16(4 * A) + _pad16(2 * n_c)
+    assert cap == b.breakdown["meta_bytes"] + worst + b.breakdown["raw_bytes"]
+    assert ws >= worst
+
+
+def test_device_encoder_bounds_rejects_bad_arguments():
+    e = [("u8", 1000)]
+    for kw in ({"chunk_bytes": 100}, {"lanes": 0}, {"lanes": 65}, {"tile": (3, 0)},
+               {"tile": (4, 96)}, {"codebook": "tensor", "tile_order": 2}):
+        with pytest.raises(wc.WcError):
+            wc.encode_device_bounds(e, **kw)
+    with pytest.raises(wc.WcError):
+        wc.encode_device_bounds([("bf16", 1001)])
+    with pytest.raises(wc.WcError):
+        wc.encode_device_bounds([("u8", 1000, (3, 7))])
