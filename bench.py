@@ -160,6 +160,9 @@ def main() -> int:
     ap.add_argument("--tile", default="", help="ROWSxCOLS 2-D tiles, e.g. 128x256 (default: "
                     "flat chunks of --chunk-bytes)")
     ap.add_argument("--codebook", choices=["tensor", "layer"], default="tensor")
+    ap.add_argument("--encode", action="store_true",
+                    help="time the device encoder (wc_encode_device) on the resident 70B "
+                         "layer instead of the decode")
     ap.add_argument("--gemv", type=int, default=0, metavar="M",
                     help="time the fused decode-GEMM y += x W^T (x: M rows) over the 70B "
                          "layer instead of the decode, next to the same product unfused "
@@ -183,6 +186,8 @@ def main() -> int:
     wc.lib()
     if args.gemv:
         return gemv_bench(args, dev)
+    if args.encode:
+        return encode_bench(args, dev)
     cfg = WORKLOADS[args.workload]
     big = cfg == 5
     tile = tuple(int(v) for v in args.tile.lower().split("x")) if args.tile else (0, 0)
@@ -495,6 +500,119 @@ def gemv_bench(args, dev) -> int:
         "uncompressed": {"value": round(wbytes / s_plain / 1e9, 2), "unit": "GB/s",
                          "ms_per_step": round(s_plain * 1e3, 4),
                          "what": "torch.matmul on the bf16 weights"},
+        "setup_s": round(setup_s, 1),
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def encode_bench(args, dev) -> int:
+    """Device encoder (histograms, tables, chunk encode, index, packing) over
+    one resident 70B layer: a step is one wc_encode_device call."""
+    import numpy as np
+    import torch
+
+    import oracle
+    from paper_2606_15789_amd import synth, wc
+    t0 = time.perf_counter()
+    tens = synth.config_torch_device(5, 0, device="cuda")
+    entries = [("bf16", t, shape) for _, t, shape in tens]
+    kw = dict(chunk_bytes=args.chunk_bytes, lanes=args.lanes)
+    cap, wsb = wc.encode_device_bounds(entries, **kw)
+    blob = torch.empty(cap, dtype=torch.uint8, device=dev)
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    size = torch.zeros(1, dtype=torch.int64, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def step():
+        wc.encode_device(entries, blob=blob, workspace=ws, size=size, stream=stream, **kw)
+
+    # correctness: the device blob is the host encoder's blob, and it decodes
+    step()
+    torch.cuda.synchronize()
+    n = int(size.item())
+    got = blob[:n].cpu().numpy()
+    host = [(dt, t.cpu().numpy(), shape) for dt, t, shape in entries]
+    h0 = time.perf_counter()
+    ref = wc.encode(host, threads=args.threads, **kw)
+    host_s = time.perf_counter() - h0
+    if n != ref.size or not np.array_equal(got, ref.array()):
+        raise RuntimeError("device blob differs from the host encoder's")
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    outs = wc.decode_torch(ref, blob, err=err)
+    torch.cuda.synchronize()
+    if int(err.item()) or any(not torch.equal(o, t) for o, (_, t, _) in zip(outs, entries)):
+        raise RuntimeError("device blob does not decode to the layer")
+    del outs, got
+    out_bytes = sum(ref.out_bytes)
+    setup_s = time.perf_counter() - t0
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    K = args.steps
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(K)]
+    for k in range(K):
+        ev[k][0].record(stream)
+        step()
+        ev[k][1].record(stream)
+    torch.cuda.synchronize()
+    ms = [a.elapsed_time(b) for a, b in ev]
+    if int(size.item()) != n:
+        raise RuntimeError("timed encodes gave another size")
+    mean_s = float(np.mean(ms)) / 1e3
+    alg = out_bytes + n  # the layer read once, the blob written once
+    cpu = None
+    if not args.no_cpu_baseline:
+        # oracle encode of the k and v projections on one core
+        sample = [(dt, h, shape) for dt, h, shape in host if shape[0] == 1024]
+        old = os.sched_getaffinity(0)
+        core = min(old)
+        os.sched_setaffinity(0, {core})
+        reps, dt = 0, 0.0
+        try:
+            while reps == 0 or dt < 3.0:
+                c0 = time.perf_counter()
+                ob = oracle.encode(sample, **kw)
+                dt += time.perf_counter() - c0
+                reps += 1
+        finally:
+            os.sched_setaffinity(0, old)
+        if ob != wc.encode(sample, threads=args.threads, **kw).tobytes():
+            raise RuntimeError("oracle sample blob differs")
+        sb = sum(h.nbytes for _, h, _ in sample)
+        cpu = {"value": round(reps * sb / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
+               "kind": "oracle",
+               "sample": f"oracle encode of the k_proj and v_proj tensors ({sb} bytes) of the "
+                         f"70B layer, {reps}x, single thread pinned to core {core}",
+               "seconds": round(dt, 3), "cpu": cpu_model(), "host_cpus": os.cpu_count()}
+    line = {
+        "metric": "encoded GB/s of weights on one MI355X (% of HBM roofline)",
+        "value": round(out_bytes / mean_s / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": args.warmup,
+        "ms_per_step": round(mean_s * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u32",
+        "data": "synthetic",
+        "config": {"workload": "llama3-70b-layer-bf16", "mode": "device-encode",
+                   "input_bytes_per_step": out_bytes, "blob_bytes_per_step": n,
+                   "chunk_bytes": args.chunk_bytes, "lanes": args.lanes,
+                   "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "achieved": round(alg / mean_s / 1e9, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(alg / mean_s / 1e9 / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "wc_encode_device (7 launches)",
+                     "mean_step_us": round(mean_s * 1e6, 2),
+                     "algorithmic_bytes_per_step": int(alg)},
+        "cpu_baseline": cpu,
+        "host_library_encode": {"value": round(out_bytes / host_s / 1e9, 3), "unit": "GB/s",
+                                "threads": args.threads, "seconds": round(host_s, 3)},
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line), flush=True)
