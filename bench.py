@@ -78,7 +78,7 @@ def cpu_model() -> str:
     return platform.processor() or "unknown"
 
 
-def oracle_baseline(blob, host_tensors, workload: str, min_seconds: float = 3.0):
+def oracle_baseline(blob, host_tensors, workload: str, min_seconds: float = 10.0):
     """Single-thread oracle decode of one whole blob on one host core.
 
     The blob is decoded whole, repeatedly until `min_seconds` have elapsed
