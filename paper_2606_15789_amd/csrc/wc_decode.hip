@@ -47,7 +47,7 @@ constexpr int kThreads = kWaves * 64;
 constexpr int kUnitWords = 128;            // one dword per lane
 constexpr int kRingUnits = 8;
 constexpr int kRingWords = kRingUnits * kUnitWords;  // 2 KiB
-constexpr int kMirrorWords = 64;
+constexpr int kMirrorWords = 128;           // a ring's first unit, mirrored past its end
 constexpr int kPipe = 4;                   // groups between a unit's load and its commit
 constexpr int kRawRows = 2;                // raw-byte rows in flight (16-bit formats)
 constexpr uint32_t kNoUnit = 0xFFFFFFFFu;
@@ -97,6 +97,8 @@ struct LaunchArgs {
   uint32_t pad;
   DevTensor t[kMaxLaunchTensors];
 };
+
+constexpr uint32_t wc_ring_words() { return kRingWords + kMirrorWords; }
 
 __device__ __forceinline__ uint64_t dpad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
 
@@ -205,26 +207,48 @@ struct Shape {
   static constexpr uint32_t kUnitWords = 2 * L;               // one dword per lane of a half
   static constexpr uint32_t kRingWords = 1024 / kH;           // per half
   static constexpr uint32_t kMirrorWords = 64 / kH;           // a step reads at most L words
+  // words one commit may write per half: a whole unit mirrored (one chunk per
+  // wave) or the 64 / kH words the reads need (two chunks per wave)
+  static constexpr uint32_t kMirrorWrite = kH == 1 ? kUnitWords : kMirrorWords;
+  static_assert(kH * (kRingWords + kMirrorWrite) <= wc_ring_words(), "ring shape");
   static constexpr uint32_t kHalfRing32 = (kRingWords + kMirrorWords) / 2;
   static_assert(kRingWords == kRingUnits * kUnitWords, "ring shape");
 };
 
+// The index entries of a wave's chunks: g, g + 1 and (two chunks per wave)
+// g + 2, clamped to the tensor's chunks.  Loaded before the table build so
+// that their latency overlaps it.
+struct IndexPre {
+  uint32_t v[3];
+};
+
+__device__ __forceinline__ IndexPre load_index(const LaunchArgs& a, const DevTensor& T,
+                                               uint32_t chunk0, uint32_t per_wave) {
+  IndexPre p{};
+  if (chunk0 < T.n_chunks) {
+    const uint32_t* index = reinterpret_cast<const uint32_t*>(a.blob + a.index_off);
+    const uint32_t g = T.first_chunk + chunk0;
+    const uint32_t n_exist = min<uint32_t>(per_wave, T.n_chunks - chunk0);
+#pragma unroll
+    for (uint32_t h = 0; h < 3; h++)
+      p.v[h] = __builtin_amdgcn_readfirstlane(index[g + min<uint32_t>(h, n_exist)]);
+  }
+  return p;
+}
+
 template <int L>
 __device__ __forceinline__ Chain<L> open_chain(const LaunchArgs& a, const DevTensor& T,
                                                uint32_t chunk0, uint32_t W, uint32_t lane,
-                                               uint32_t* ring) {
+                                               uint32_t* ring, const IndexPre& pre) {
   constexpr int kH = Chain<L>::kH;
   Chain<L> c;
   const uint8_t* blob = reinterpret_cast<const uint8_t*>(a.blob);
-  const uint32_t* index = reinterpret_cast<const uint32_t*>(blob + a.index_off);
-  const uint32_t g = T.first_chunk + chunk0;
   c.n_exist = min<uint32_t>(kH, T.n_chunks - chunk0);
   // per-chunk values are wave-uniform; readfirstlane keeps them (and the
   // buffer descriptors built from them) in scalar registers
   uint64_t o[kH + 1];
 #pragma unroll
-  for (int h = 0; h <= kH; h++)
-    o[h] = 16ull * __builtin_amdgcn_readfirstlane(index[g + min<uint32_t>(h, c.n_exist)]);
+  for (int h = 0; h <= kH; h++) o[h] = 16ull * pre.v[h];
   c.ring = ring;
   c.ok = true;
   uint64_t end = o[0];
@@ -308,9 +332,16 @@ __device__ __forceinline__ void commit_unit(const Chain<L>& c, uint32_t u, uint3
                                             uint32_t h, uint32_t sub) {
   if (u == kNoUnit) return;
   const uint32_t slot = u % kRingUnits;
-  uint32_t* r = c.ring + h * Shape<L>::kHalfRing32;
-  r[slot * L + sub] = v;
-  if (slot == 0 && sub < Shape<L>::kMirrorWords / 2) r[Shape<L>::kRingWords / 2 + sub] = v;
+  if constexpr (Chain<L>::kH == 1) {
+    // u is wave-uniform here, so both tests are scalar branches; the mirror
+    // takes the whole unit (the reads need its first 64 words)
+    c.ring[slot * L + sub] = v;
+    if (slot == 0) c.ring[Shape<L>::kRingWords / 2 + sub] = v;
+  } else {
+    uint32_t* r = c.ring + h * Shape<L>::kHalfRing32;
+    r[slot * L + sub] = v;
+    if (slot == 0 && sub < Shape<L>::kMirrorWords / 2) r[Shape<L>::kRingWords / 2 + sub] = v;
+  }
 }
 
 // One pipeline slot: the unit of each half issued together (one load).
@@ -324,8 +355,17 @@ template <int L>
 __device__ __forceinline__ Slot<L> issue(Chain<L>& c, uint32_t h, uint32_t sub) {
   Slot<L> s;
   if constexpr (Chain<L>::kH == 1) {
-    s.u = next_unit(c, 0);
-    s.v = load_unit(c, s.u, c.wbase[0], sub);
+    // wave-uniform, in integer arithmetic (no boolean, which the compiler
+    // would carry as a lane mask): the next unit while the stream has one and
+    // the ring room.  issued <= lim always: both only grow, issued only below lim.
+    const uint32_t lim = min(c.nunits[0], c.cursor[0] / Shape<L>::kUnitWords + kRingUnits);
+    const uint32_t take = (c.issued[0] - lim) >> 31;  // lim - issued < 2^31
+    const uint32_t none = take - 1u;  // 0, or all ones when nothing is issued
+    s.u = c.issued[0] | none;         // the unit, or kNoUnit
+    // the unit's offset (below 2^31), or one at least kFarOffset: zeros, no access
+    const uint32_t off = (c.wbase[0] + c.issued[0] * (4u * L)) | (none & kFarOffset);
+    c.issued[0] += take;
+    s.v = __builtin_amdgcn_raw_buffer_load_b32(c.rs, sub * 4u + off, 0, 0);
   } else {
     const uint32_t u0 = next_unit(c, 0), u1 = next_unit(c, 1);
     s.u = h ? u1 : u0;
@@ -387,7 +427,8 @@ __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ 
 template <int G, int L, bool kTiled, int kM = 0>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
-                                              const uint2* __restrict__ tab, uint32_t* ring) {
+                                              const uint2* __restrict__ tab, uint32_t* ring,
+                                              const IndexPre& pre) {
   constexpr bool kGemv = kM > 0;  // fused GEMM with kM rows of x
   static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
   constexpr int kH = Chain<L>::kH;
@@ -400,7 +441,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   constexpr uint32_t kLogW = G == 2 ? 3 : (G == 4 ? 4 : 5);
   static_assert(kUnroll % kPipe == 0 && kUnroll % kGroupsPerRow == 0, "pipeline shape");
 
-  Chain<L> c = open_chain<L>(a, T, chunk0, W, lane, ring);
+  Chain<L> c = open_chain<L>(a, T, chunk0, W, lane, ring, pre);
   if (!c.ok) {
     if (lane == 0) report(a, WC_DERR_INDEX);
     return;
@@ -588,22 +629,23 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
     if (wg >= a.t[k].wg0) ti = k;
   const DevTensor& T = a.t[ti];
   const uint32_t tid = threadIdx.x;
-  build_table(a, T, tab, cum, tid);
-  __syncthreads();
   // the wave index is uniform across the wave; say so, so chunk metadata and
   // buffer descriptors live in scalar registers
   const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const uint32_t lane = __lane_id();
   const uint32_t per_wave = T.lanes == 32 ? 2u : 1u;
   const uint32_t chunk0 = ((wg - T.wg0) * kWaves + wave) * per_wave;
+  const IndexPre pre = load_index(a, T, chunk0, per_wave);
+  build_table(a, T, tab, cum, tid);
+  __syncthreads();
   if (chunk0 >= T.n_chunks) return;
   // instantiate one decoder per (format, lanes, tiling)
   auto run = [&](auto gc, auto lc) {
     constexpr int G = decltype(gc)::value, L = decltype(lc)::value;
     if (T.tiled)
-      decode_chunks<G, L, true>(a, T, chunk0, lane, tab, ring[wave]);
+      decode_chunks<G, L, true>(a, T, chunk0, lane, tab, ring[wave], pre);
     else
-      decode_chunks<G, L, false>(a, T, chunk0, lane, tab, ring[wave]);
+      decode_chunks<G, L, false>(a, T, chunk0, lane, tab, ring[wave], pre);
   };
   auto by_kind = [&](auto lc) {
     switch (T.kind) {
@@ -632,13 +674,14 @@ __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
     if (wg >= a.t[k].wg0) ti = k;
   const DevTensor& T = a.t[ti];
   const uint32_t tid = threadIdx.x;
-  build_table(a, T, tab, cum, tid);
-  __syncthreads();
   const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const uint32_t lane = __lane_id();
   const uint32_t chunk = (wg - T.wg0) * kWaves + wave;
+  const IndexPre pre = load_index(a, T, chunk, 1u);
+  build_table(a, T, tab, cum, tid);
+  __syncthreads();
   if (chunk >= T.n_chunks) return;
-  decode_chunks<2, 64, true, kM>(a, T, chunk, lane, tab, ring[wave]);
+  decode_chunks<2, 64, true, kM>(a, T, chunk, lane, tab, ring[wave], pre);
 }
 
 }  // namespace
