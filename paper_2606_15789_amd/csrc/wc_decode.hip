@@ -17,13 +17,14 @@
 //    slot - cum}, so the state update is one v_mad_u32_u24 (the 24-bit multiply
 //    ignores the symbol byte);
 //  * words reach a per-chunk 2 KiB LDS ring through a fixed-rate pipeline: every
-//    two decode steps a chain commits the 128-word unit it loaded kPipe groups
-//    earlier and issues one new bounds-checked buffer load (the next unit, or a
-//    load past the record that returns zeros when the ring is full).  Two steps
-//    consume at most 128 words, so the decoder never waits for a unit, and the
-//    fixed load pattern gives the compiler exact vmcnt waits.  The ring's first
-//    64 words are mirrored past its end, so a lane's word address is one scalar
-//    base plus its rank;
+//    four decode steps a chain commits the 256-word unit (8 bytes per lane) it
+//    loaded eight steps earlier and issues one new bounds-checked buffer load
+//    (the next unit, or a load past the record that returns zeros when the ring
+//    is full).  Four steps consume at most 256 words, so the decoder never waits
+//    for a unit, and the fixed load pattern gives the compiler exact vmcnt
+//    waits.  The ring's first 64 words are mirrored past its end, so a lane's
+//    word address is one scalar base plus its rank (two 32-lane chunks per wave move
+//    one dword per lane of a half every two steps);
 //  * renormalisation: ballot of the lanes whose state fell below 2^16, mbcnt
 //    gives each of them its rank, the cursor advances by the popcount -- the
 //    lanes' words are consecutive in the stream;
@@ -44,11 +45,9 @@ namespace {
 
 constexpr int kWaves = 8;                  // waves (chunks) per workgroup
 constexpr int kThreads = kWaves * 64;
-constexpr int kUnitWords = 128;            // one dword per lane
-constexpr int kRingUnits = 8;
-constexpr int kRingWords = kRingUnits * kUnitWords;  // 2 KiB
-constexpr int kMirrorWords = 128;           // a ring's first unit, mirrored past its end
-constexpr int kPipe = 4;                   // groups between a unit's load and its commit
+constexpr int kWaveRingWords = 1024;       // words of a wave's ring (2 KiB)
+constexpr int kWaveMirrorWords = 64;       // a ring's first 64 words, mirrored past its end
+constexpr int kPipeSteps = 8;              // decode steps between a unit's load and its commit
 constexpr int kRawRows = 2;                // raw-byte rows in flight (16-bit formats)
 constexpr uint32_t kNoUnit = 0xFFFFFFFFu;
 // Offsets that can fall outside a buffer are always passed as the vector
@@ -57,7 +56,6 @@ constexpr uint32_t kNoUnit = 0xFFFFFFFFu;
 constexpr uint32_t kFarOffset = 0x7FFFFF00u;  // past any record: loads return zeros
 constexpr int kMaxLaunchTensors = 32;
 constexpr int kStreamStore = 2;            // buffer-store cache policy: non-temporal
-static_assert(kPipe <= kRingUnits - 2, "the word pipeline needs two spare ring units");
 
 enum Kind : uint32_t { kSplit16 = 0, kByte = 1, kNibble = 2 };
 
@@ -98,7 +96,7 @@ struct LaunchArgs {
   DevTensor t[kMaxLaunchTensors];
 };
 
-constexpr uint32_t wc_ring_words() { return kRingWords + kMirrorWords; }
+constexpr uint32_t wc_ring_words() { return kWaveRingWords + kWaveMirrorWords; }
 
 __device__ __forceinline__ uint64_t dpad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
 
@@ -201,18 +199,27 @@ struct Chain {
   bool ok;
 };
 
+// The word pipeline of a wave.  One chunk per wave: a unit is two dwords per
+// lane (256 words), loaded and committed every two groups (four steps, which
+// read at most 256 words).  Two chunks per wave: a unit is one dword per lane
+// of a half (64 words of that half), every group (two steps, at most 64 words
+// of a half).  Either way a unit is committed kPipeSteps steps after its load,
+// and the ring keeps two spare units.
 template <int L>
 struct Shape {
   static constexpr int kH = 64 / L;
-  static constexpr uint32_t kUnitWords = 2 * L;               // one dword per lane of a half
-  static constexpr uint32_t kRingWords = 1024 / kH;           // per half
+  static constexpr int kDw = kH == 1 ? 2 : 1;                 // dwords per lane per unit
+  static constexpr int kEvery = kDw;                          // groups per pipeline slot
+  static constexpr uint32_t kUnitWords = 2 * L * kDw;         // words per unit (per half)
+  static constexpr uint32_t kRingWords = kWaveRingWords / kH; // per half
+  static constexpr uint32_t kRingUnits = kRingWords / kUnitWords;
+  static constexpr int kPipe = kPipeSteps / (2 * kEvery);     // slots between load and commit
   static constexpr uint32_t kMirrorWords = 64 / kH;           // a step reads at most L words
-  // words one commit may write per half: a whole unit mirrored (one chunk per
-  // wave) or the 64 / kH words the reads need (two chunks per wave)
-  static constexpr uint32_t kMirrorWrite = kH == 1 ? kUnitWords : kMirrorWords;
-  static_assert(kH * (kRingWords + kMirrorWrite) <= wc_ring_words(), "ring shape");
+  // a step's reads run at most 64 / kH words past a half's ring: mirrored
+  static_assert(kH * (kRingWords + kMirrorWords) <= wc_ring_words(), "ring shape");
   static constexpr uint32_t kHalfRing32 = (kRingWords + kMirrorWords) / 2;
-  static_assert(kRingWords == kRingUnits * kUnitWords, "ring shape");
+  static_assert(kPipe >= 1 && kPipe <= int(kRingUnits) - 2, "two spare ring units");
+  static_assert(2 * kEvery * 64 <= kUnitWords * kH, "a slot's steps read at most one unit");
 };
 
 // The index entries of a wave's chunks: g, g + 1 and (two chunks per wave)
@@ -313,7 +320,7 @@ __device__ __forceinline__ Chain<L> open_chain(const LaunchArgs& a, const DevTen
 template <int L>
 __device__ __forceinline__ uint32_t next_unit(Chain<L>& c, int h) {
   if (c.issued[h] < c.nunits[h] &&
-      c.issued[h] < c.cursor[h] / Shape<L>::kUnitWords + kRingUnits)
+      c.issued[h] < c.cursor[h] / Shape<L>::kUnitWords + Shape<L>::kRingUnits)
     return c.issued[h]++;
   return kNoUnit;
 }
@@ -327,29 +334,32 @@ __device__ __forceinline__ uint32_t load_unit(const Chain<L>& c, uint32_t u, uin
   return __builtin_amdgcn_raw_buffer_load_b32(c.rs, sub * 4u + off, 0, 0);
 }
 
-template <int L>
-__device__ __forceinline__ void commit_unit(const Chain<L>& c, uint32_t u, uint32_t v,
-                                            uint32_t h, uint32_t sub) {
-  if (u == kNoUnit) return;
-  const uint32_t slot = u % kRingUnits;
-  if constexpr (Chain<L>::kH == 1) {
-    // u is wave-uniform here, so both tests are scalar branches; the mirror
-    // takes the whole unit (the reads need its first 64 words)
-    c.ring[slot * L + sub] = v;
-    if (slot == 0) c.ring[Shape<L>::kRingWords / 2 + sub] = v;
-  } else {
-    uint32_t* r = c.ring + h * Shape<L>::kHalfRing32;
-    r[slot * L + sub] = v;
-    if (slot == 0 && sub < Shape<L>::kMirrorWords / 2) r[Shape<L>::kRingWords / 2 + sub] = v;
-  }
-}
-
 // One pipeline slot: the unit of each half issued together (one load).
 template <int L>
 struct Slot {
-  uint32_t u;  // this lane's unit (its half's), or kNoUnit
-  uint32_t v;  // the loaded dword
+  uint32_t u;                  // this lane's unit (its half's), or kNoUnit
+  uint32_t v[Shape<L>::kDw];   // the loaded dwords
 };
+
+template <int L>
+__device__ __forceinline__ void commit_unit(const Chain<L>& c, const Slot<L>& s, uint32_t h,
+                                            uint32_t sub) {
+  const uint32_t u = s.u;
+  if (u == kNoUnit) return;
+  const uint32_t slot = u % Shape<L>::kRingUnits;
+  if constexpr (Chain<L>::kH == 1) {
+    // u is wave-uniform here, so both unit tests are scalar branches; the
+    // mirror takes the unit's first 64 words (lanes 0..15), all the reads need
+    uint2* r = reinterpret_cast<uint2*>(c.ring);
+    const uint2 v = make_uint2(s.v[0], s.v[1]);
+    r[slot * L + sub] = v;
+    if (slot == 0 && sub < Shape<L>::kMirrorWords / 4) r[Shape<L>::kRingWords / 4 + sub] = v;
+  } else {
+    uint32_t* r = c.ring + h * Shape<L>::kHalfRing32;
+    r[slot * L + sub] = s.v[0];
+    if (slot == 0 && sub < Shape<L>::kMirrorWords / 2) r[Shape<L>::kRingWords / 2 + sub] = s.v[0];
+  }
+}
 
 template <int L>
 __device__ __forceinline__ Slot<L> issue(Chain<L>& c, uint32_t h, uint32_t sub) {
@@ -358,18 +368,22 @@ __device__ __forceinline__ Slot<L> issue(Chain<L>& c, uint32_t h, uint32_t sub) 
     // wave-uniform, in integer arithmetic (no boolean, which the compiler
     // would carry as a lane mask): the next unit while the stream has one and
     // the ring room.  issued <= lim always: both only grow, issued only below lim.
-    const uint32_t lim = min(c.nunits[0], c.cursor[0] / Shape<L>::kUnitWords + kRingUnits);
+    using S = Shape<L>;
+    const uint32_t lim = min(c.nunits[0], c.cursor[0] / S::kUnitWords + S::kRingUnits);
     const uint32_t take = (c.issued[0] - lim) >> 31;  // lim - issued < 2^31
     const uint32_t none = take - 1u;  // 0, or all ones when nothing is issued
     s.u = c.issued[0] | none;         // the unit, or kNoUnit
     // the unit's offset (below 2^31), or one at least kFarOffset: zeros, no access
-    const uint32_t off = (c.wbase[0] + c.issued[0] * (4u * L)) | (none & kFarOffset);
+    const uint32_t off = (c.wbase[0] + c.issued[0] * (2u * S::kUnitWords)) | (none & kFarOffset);
     c.issued[0] += take;
-    s.v = __builtin_amdgcn_raw_buffer_load_b32(c.rs, sub * 4u + off, 0, 0);
+    const uint2 v = __builtin_bit_cast(
+        uint2, __builtin_amdgcn_raw_buffer_load_b64(c.rs, sub * 8u + off, 0, 0));
+    s.v[0] = v.x;
+    s.v[1] = v.y;
   } else {
     const uint32_t u0 = next_unit(c, 0), u1 = next_unit(c, 1);
     s.u = h ? u1 : u0;
-    s.v = load_unit(c, s.u, h ? c.wbase[1] : c.wbase[0], sub);
+    s.v[0] = load_unit(c, s.u, h ? c.wbase[1] : c.wbase[0], sub);
   }
   return s;
 }
@@ -439,7 +453,9 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   constexpr uint32_t kRowBytes = 16u * L;      // decoded bytes of one half-row
   constexpr uint32_t kRawRowBytes = 8u * L;    // raw bytes of one half-row (16-bit formats)
   constexpr uint32_t kLogW = G == 2 ? 3 : (G == 4 ? 4 : 5);
-  static_assert(kUnroll % kPipe == 0 && kUnroll % kGroupsPerRow == 0, "pipeline shape");
+  constexpr int kPipe = Shape<L>::kPipe, kEvery = Shape<L>::kEvery;
+  static_assert(kUnroll % (kPipe * kEvery) == 0 && kUnroll % kGroupsPerRow == 0,
+                "pipeline shape");
 
   Chain<L> c = open_chain<L>(a, T, chunk0, W, lane, ring, pre);
   if (!c.ok) {
@@ -483,7 +499,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   Slot<L> pipe[kPipe];
   {
     const Slot<L> s0 = issue(c, h, sub);
-    commit_unit(c, s0.u, s0.v, h, sub);
+    commit_unit(c, s0, h, sub);
   }
 #pragma unroll
   for (int j = 0; j < kPipe; j++) pipe[j] = issue(c, h, sub);
@@ -514,10 +530,13 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   auto group = [&](uint32_t g, auto jc, auto tailc) {
     constexpr int j = decltype(jc)::value;
     constexpr bool kTail = decltype(tailc)::value;
-    constexpr int slot = j % kPipe;
     constexpr int k0 = (j % kGroupsPerRow) * 2;  // first step of this group in its lane-group
-    commit_unit(c, pipe[slot].u, pipe[slot].v, h, sub);
-    pipe[slot] = issue(c, h, sub);
+    if constexpr (j % kEvery == 0) {
+      // every kEvery groups: commit the unit loaded kPipe slots ago, load the next
+      constexpr int slot = (j / kEvery) % kPipe;
+      commit_unit(c, pipe[slot], h, sub);
+      pipe[slot] = issue(c, h, sub);
+    }
     __builtin_amdgcn_wave_barrier();
     const uint32_t r = g / kGroupsPerRow;
     const int nv = kTail ? max(0, min<int>(W, (int)n_lane - (int)(r * kRowSym + sub * W))) : W;
@@ -621,7 +640,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
 __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
   __shared__ uint2 tab[wc::kTableSize];
   __shared__ uint32_t cum[260];
-  __shared__ uint32_t ring[kWaves][(kRingWords + kMirrorWords) / 2];
+  __shared__ uint32_t ring[kWaves][wc_ring_words() / 2];
 
   const uint32_t wg = blockIdx.x;
   uint32_t ti = 0;
@@ -667,7 +686,7 @@ template <int kM>
 __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   __shared__ uint2 tab[wc::kTableSize];
   __shared__ uint32_t cum[260];
-  __shared__ uint32_t ring[kWaves][(kRingWords + kMirrorWords) / 2];
+  __shared__ uint32_t ring[kWaves][wc_ring_words() / 2];
   const uint32_t wg = blockIdx.x;
   uint32_t ti = 0;
   for (uint32_t k = 1; k < a.n_tensors; k++)
