@@ -45,6 +45,7 @@ constexpr int kHistStride = 257;             // odd stride: copies of a bin in d
 constexpr uint64_t kHistSpan = 256u << 10;   // source bytes per histogram workgroup
 constexpr int kMaxLaunch = 16;               // tensors per launch
 constexpr int kScanThreads = 1024;
+constexpr uint32_t kFarOffset = 0x7FFFFF00u;  // past any slot: buffer stores are dropped
 
 enum Kind : uint32_t { kSplit16 = 0, kByte = 1, kNibble = 2 };
 
@@ -74,12 +75,19 @@ struct EncArgs {
 
 __device__ __forceinline__ uint64_t dpad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
 
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const v4u gu4;     // global memory: no flat access
+typedef __attribute__((address_space(1))) const uint8_t gu8;
+
 // 16 source bytes at `off`, zeros past `bytes`.
 __device__ __forceinline__ uint4 load16(const uint8_t* base, uint64_t bytes, uint64_t off) {
-  if (off + 16 <= bytes) return *reinterpret_cast<const uint4*>(base + off);
+  if (off + 16 <= bytes) {
+    const v4u v = *(gu4*)(uint64_t)(base + off);
+    return make_uint4(v.x, v.y, v.z, v.w);
+  }
   uint32_t d[4] = {0u, 0u, 0u, 0u};
   for (uint32_t b = 0; b < 16; b++)
-    if (off + b < bytes) d[b >> 2] |= uint32_t(base[off + b]) << (8 * (b & 3));
+    if (off + b < bytes) d[b >> 2] |= uint32_t(((gu8*)(uint64_t)base)[off + b]) << (8 * (b & 3));
   return make_uint4(d[0], d[1], d[2], d[3]);
 }
 
@@ -95,18 +103,31 @@ __device__ __forceinline__ uint32_t symbol(const uint4& v, uint32_t k) {
   else return (dword(v, k >> 3) >> (4 * (k & 7))) & 0xFu;
 }
 
-// Byte offset in the source of the lane-group that starts at symbol i0 of
-// chunk c: a byte run, or the lane-group's place in its tile.
-__device__ __forceinline__ uint64_t group_offset(const EncTensor& T, uint32_t c, uint32_t i0) {
-  if (!T.tiled) return uint64_t(c) * T.chunk_bytes + uint64_t(i0 >> T.logW) * 16u;
-  const uint64_t base =
-      uint64_t(c / T.ntc) * T.tile_r * T.pitch + uint64_t(c % T.ntc) * T.tile_row_bytes;
-  if (T.order == 0)
-    return base + uint64_t(i0 >> T.log_tc) * T.pitch +
-           uint64_t((i0 & ((1u << T.log_tc) - 1u)) >> T.logW) * 16u;
-  const uint32_t g = i0 >> T.logW;  // row g mod tile_r of k-block g div tile_r
-  return base + uint64_t(g & ((1u << T.log_tr) - 1u)) * T.pitch + uint64_t(g >> T.log_tr) * 16u;
-}
+// Byte offsets in the source of the lane-groups of one chunk: a byte run, or
+// a lane-group's place in its tile (row-major or column blocks).  The chunk's
+// part is worked out once; at(i0) is the lane-group that starts at symbol i0.
+struct GroupAddr {
+  uint64_t base, pitch;
+  uint32_t mode, logW, log_tc, log_tr;
+  __device__ __forceinline__ GroupAddr(const EncTensor& T, uint32_t c)
+      : pitch(T.pitch), logW(T.logW), log_tc(T.log_tc), log_tr(T.log_tr) {
+    if (!T.tiled) {
+      mode = 0;
+      base = uint64_t(c) * T.chunk_bytes;
+    } else {
+      mode = T.order == 0 ? 1u : 2u;
+      base = uint64_t(c / T.ntc) * T.tile_r * T.pitch + uint64_t(c % T.ntc) * T.tile_row_bytes;
+    }
+  }
+  __device__ __forceinline__ uint64_t at(uint32_t i0) const {
+    if (mode == 0) return base + (uint64_t(i0 >> logW) << 4);
+    if (mode == 1)
+      return base + uint64_t(i0 >> log_tc) * pitch +
+             (uint64_t((i0 & ((1u << log_tc) - 1u)) >> logW) << 4);
+    const uint32_t g = i0 >> logW;  // row g mod tile_r of k-block g div tile_r
+    return base + uint64_t(g & ((1u << log_tr) - 1u)) * pitch + (uint64_t(g >> log_tr) << 4);
+  }
+};
 
 __device__ __forceinline__ uint32_t tensor_of(const EncArgs& a, uint32_t wg) {
   uint32_t ti = 0;
@@ -266,10 +287,13 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
   __syncthreads();
   uint32_t cum = 0;
   for (uint32_t t = 0; t < s; t++) cum += red[t];
-  // ceil(2^64 / f) = floor((2^64 - 1) / f) + 1 for f >= 2; 0 marks f == 1
-  const unsigned long long rc = f > 1 ? ~0ull / f + 1 : 0ull;
+  // ceil(2^64 / f) = floor((2^64 - 1) / f) + 1 for f >= 2.  For f == 1 the
+  // reciprocal 2^64 - 1 gives the quotient x - 1 instead of x, which leaves
+  // the new state 2^12 - 1 short; the encoder's cum for that symbol carries it.
+  const unsigned long long rc = f > 1 ? ~0ull / f + 1 : (f == 1 ? ~0ull : 0ull);
+  const uint32_t cum_enc = f == 1 ? cum + wc::kTableSize - 1 : cum;
   uint4* tab = reinterpret_cast<uint4*>(a.ws + a.tab_off) + uint64_t(NT.table) * 256u;
-  tab[s] = make_uint4(f, cum, uint32_t(rc), uint32_t(rc >> 32));
+  tab[s] = make_uint4(f, cum_enc, uint32_t(rc), uint32_t(rc >> 32));
 }
 
 // ---------------------------------------------------------------------------
@@ -279,48 +303,62 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
 // and then x = floor(x / f) * 2^12 + x mod f + cum.  The quotient uses the
 // 64-bit reciprocal r = ceil(2^64 / f): floor(x * r / 2^64) = floor(x / f) for
 // x < 2^32 (the error x * (r - 2^64 / f) / 2^64 is below 1 / f), computed as
-// (x * r_hi + mulhi(x, r_lo)) >> 32.
+// (x * r_hi + mulhi(x, r_lo)) >> 32.  q < 2^20 and f <= 2^12, so q * f is a
+// 24-bit multiply.  Every step is branch-free: a lane that emits nothing
+// stores its word at an offset past the slot, which the buffer range check drops.
 
 template <uint32_t K>
 __device__ void encode_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, uint32_t lane,
                              const uint4* __restrict__ tab) {
   constexpr uint32_t W = K == kSplit16 ? 8u : (K == kByte ? 16u : 32u);
   const uint8_t* src = reinterpret_cast<const uint8_t*>(T.src);
+  const uint64_t src_bytes = T.src_bytes;
   const uint64_t s0 = uint64_t(c) * T.per;
   const uint32_t n_c = uint32_t(min<uint64_t>(T.per, T.n_sym - s0));
   const uint32_t L = T.lanes;
   const uint32_t A = min(L, (n_c + W - 1) / W);
   const uint32_t LW = L * W;
   const uint32_t rows = (n_c + LW - 1) / LW;
+  const GroupAddr ga(T, c);
   uint8_t* slot = reinterpret_cast<uint8_t*>(a.ws + T.slot_off) + uint64_t(c) * T.slot_bytes;
-  uint16_t* stack_end = reinterpret_cast<uint16_t*>(slot + T.slot_bytes);
+  // the slot as a buffer: word k from its end sits at byte slot_bytes - 2k
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(slot, (short)0, (int)T.slot_bytes, 0x00020000);
+  // this lane's lane-group of row r (zeros past the chunk's symbols)
+  auto load_row = [&](uint32_t r) {
+    const uint32_t i0 = r * LW + lane * W;
+    uint4 v = make_uint4(0u, 0u, 0u, 0u);
+    if (lane < L && i0 < n_c) v = load16(src, src_bytes, ga.at(i0));
+    return v;
+  };
   uint32_t x = wc::kStateLow;
   uint32_t top = 0;  // words pushed
+  uint4 cur = rows ? load_row(rows - 1) : make_uint4(0u, 0u, 0u, 0u);
   for (uint32_t r = rows; r-- > 0;) {
+    // the next row's load is in flight while this row is coded
+    const uint4 nxt = r ? load_row(r - 1) : make_uint4(0u, 0u, 0u, 0u);
     const uint32_t i0 = r * LW + lane * W;
-    const bool lane_ok = lane < L && i0 < n_c;
-    const uint32_t nv = lane_ok ? min(W, n_c - i0) : 0u;
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (lane_ok) v = load16(src, T.src_bytes, group_offset(T, c, i0));
+    const uint32_t nv = lane < L && i0 < n_c ? min(W, n_c - i0) : 0u;
 #pragma unroll
     for (uint32_t kk = 0; kk < W; kk++) {
       const uint32_t k = W - 1 - kk;
       const bool active = k < nv;
-      const uint4 e = tab[symbol<K>(v, k)];  // {f, cum, r_lo, r_hi}
+      const uint4 e = tab[symbol<K>(cur, k)];  // {f, cum, r_lo, r_hi}
       const bool emit = active && (x >> 20) >= e.x;
       const uint64_t m = __ballot(emit);
       const uint32_t below = __builtin_amdgcn_mbcnt_hi(
           uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
       const uint32_t total = uint32_t(__popcll(m));
       // pushed after the emitting lanes above this one (total - below - 1)
-      if (emit) stack_end[-int(top + total - below)] = uint16_t(x);
+      const uint32_t off = emit ? T.slot_bytes - 2u * (top + total - below) : kFarOffset;
+      __builtin_amdgcn_raw_buffer_store_b16(uint16_t(x), rs, off, 0, 0);
       top += total;
       const uint32_t v2 = emit ? x >> 16 : x;
-      const uint32_t q =
-          e.x == 1u ? v2 : uint32_t((uint64_t(v2) * e.w + __umulhi(v2, e.z)) >> 32);
-      const uint32_t xn = (q << wc::kProbBits) + (v2 - q * e.x) + e.y;
+      const uint32_t q = uint32_t((uint64_t(v2) * e.w + __umulhi(v2, e.z)) >> 32);
+      const uint32_t xn = (q << wc::kProbBits) + v2 - __umul24(q, e.x) + e.y;
       x = active ? xn : x;
     }
+    cur = nxt;
   }
   // record header, states and their padding at the slot's start
   uint32_t* hdr = reinterpret_cast<uint32_t*>(slot);
@@ -471,10 +509,11 @@ __device__ void pack_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, uin
     const uint64_t raw_start = reinterpret_cast<const uint64_t*>(a.ws + a.misc_off)[0];
     uint8_t* raw = blob + raw_start + T.raw_rel + uint64_t(c) * T.per;
     const uint8_t* src = reinterpret_cast<const uint8_t*>(T.src);
+    const GroupAddr ga(T, c);
     const uint32_t groups = (n_c + W - 1) / W;
     for (uint32_t gi = lane; gi < groups; gi += 64) {
       const uint32_t i0 = gi * W;
-      const uint4 v = load16(src, T.src_bytes, group_offset(T, c, i0));
+      const uint4 v = load16(src, T.src_bytes, ga.at(i0));
       uint32_t rb[2] = {0u, 0u};
 #pragma unroll
       for (uint32_t k = 0; k < 8; k++) {
