@@ -40,7 +40,7 @@ namespace {
 constexpr int kWaves = 8;  // chunks (waves) per encoder / packer workgroup
 constexpr int kThreads = kWaves * 64;
 constexpr int kHistThreads = 256;
-constexpr int kHistReps = 8;                 // LDS histogram copies (lane & 7)
+constexpr int kHistReps = 16;                // LDS histogram copies (lane & 15)
 constexpr int kHistStride = 257;             // odd stride: copies of a bin in different banks
 constexpr uint64_t kHistSpan = 256u << 10;   // source bytes per histogram workgroup
 constexpr int kMaxLaunch = 16;               // tensors per launch
@@ -154,7 +154,18 @@ __device__ void count_span(const EncTensor& T, uint64_t off0, uint64_t off1, uin
   const uint8_t* src = reinterpret_cast<const uint8_t*>(T.src);
   const uint32_t rep = (threadIdx.x & (kHistReps - 1)) * kHistStride;
   constexpr uint32_t W = K == kSplit16 ? 8u : (K == kByte ? 16u : 32u);
-  for (uint64_t off = off0 + threadIdx.x * 16ull; off < off1; off += kHistThreads * 16ull) {
+  constexpr uint64_t kStep = kHistThreads * 16ull;
+  // whole lane-groups, two loads in flight; then the tensor's last bytes
+  const uint64_t full_end = off0 + (off1 - off0) / 16 * 16;
+  uint64_t off = off0 + threadIdx.x * 16ull;
+  for (; off + kStep < full_end; off += 2 * kStep) {
+    const uint4 v0 = load16(src, full_end, off), v1 = load16(src, full_end, off + kStep);
+#pragma unroll
+    for (uint32_t k = 0; k < W; k++) atomicAdd(&h[rep + symbol<K>(v0, k)], 1u);
+#pragma unroll
+    for (uint32_t k = 0; k < W; k++) atomicAdd(&h[rep + symbol<K>(v1, k)], 1u);
+  }
+  for (; off < off1; off += kStep) {
     const uint4 v = load16(src, T.src_bytes, off);
     // symbols whose bytes lie inside the tensor
     const uint64_t left = T.src_bytes - off;
@@ -491,18 +502,24 @@ __device__ void pack_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, uin
   // header and states (16-byte units)
   for (uint32_t j = lane; j < head / 16; j += 64)
     *reinterpret_cast<uint4*>(blob + o + 16ull * j) = reinterpret_cast<const uint4*>(slot)[j];
-  // words: the stack's last nw u16 of the slot, then zeros to 16 bytes
-  const uint16_t* words = reinterpret_cast<const uint16_t*>(slot + T.slot_bytes) - nw;
+  // words: the stack's last nw u16 of the slot, then zeros to 16 bytes.  They
+  // start 2 bytes into a dword when nw is odd: five dword loads through the
+  // slot's buffer descriptor, realigned by 16 bits; the bytes past the slot's
+  // end (the padding) read as zero.
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(slot), (short)0, (int)T.slot_bytes, 0x00020000);
+  const uint32_t start = T.slot_bytes - 2u * nw;
+  const uint32_t a0 = start & ~3u, sh = (start & 2u) * 8u;
   const uint32_t units = uint32_t(dpad16(2ull * nw) / 16);
   for (uint32_t j = lane; j < units; j += 64) {
-    uint32_t d[4];
+    uint32_t d[5];
 #pragma unroll
-    for (uint32_t q = 0; q < 4; q++) {
-      const uint32_t k = 8 * j + 2 * q;
-      const uint32_t lo = k < nw ? words[k] : 0u, hi = k + 1 < nw ? words[k + 1] : 0u;
-      d[q] = lo | (hi << 16);
-    }
-    *reinterpret_cast<uint4*>(blob + o + head + 16ull * j) = make_uint4(d[0], d[1], d[2], d[3]);
+    for (uint32_t q = 0; q < 5; q++)
+      d[q] = __builtin_amdgcn_raw_buffer_load_b32(rs, a0 + 16u * j + 4u * q, 0, 0);
+    uint32_t w[4];
+#pragma unroll
+    for (uint32_t q = 0; q < 4; q++) w[q] = sh ? __builtin_amdgcn_alignbit(d[q + 1], d[q], 16) : d[q];
+    *reinterpret_cast<uint4*>(blob + o + head + 16ull * j) = make_uint4(w[0], w[1], w[2], w[3]);
   }
   if constexpr (K == kSplit16) {
     // raw byte of a word: bit 15 -> bit 7, bits 6..0 kept
@@ -511,13 +528,17 @@ __device__ void pack_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, uin
     const uint8_t* src = reinterpret_cast<const uint8_t*>(T.src);
     const GroupAddr ga(T, c);
     const uint32_t groups = (n_c + W - 1) / W;
-    for (uint32_t gi = lane; gi < groups; gi += 64) {
+    uint32_t gi = lane;
+    uint4 v = gi < groups ? load16(src, T.src_bytes, ga.at(gi * W)) : make_uint4(0u, 0u, 0u, 0u);
+    for (; gi < groups; gi += 64) {
       const uint32_t i0 = gi * W;
-      const uint4 v = load16(src, T.src_bytes, ga.at(i0));
+      // the next lane-group's load is in flight while this one is written
+      const uint4 cur = v;
+      if (gi + 64 < groups) v = load16(src, T.src_bytes, ga.at((gi + 64) * W));
       uint32_t rb[2] = {0u, 0u};
 #pragma unroll
       for (uint32_t k = 0; k < 8; k++) {
-        const uint32_t w = (dword(v, k >> 1) >> (16 * (k & 1))) & 0xFFFFu;
+        const uint32_t w = (dword(cur, k >> 1) >> (16 * (k & 1))) & 0xFFFFu;
         const uint32_t r = ((w >> 8) & 0x80u) | (w & 0x7Fu);
         rb[k >> 2] |= r << (8 * (k & 3));
       }
