@@ -160,6 +160,10 @@ def main() -> int:
     ap.add_argument("--tile", default="", help="ROWSxCOLS 2-D tiles, e.g. 128x256 (default: "
                     "flat chunks of --chunk-bytes)")
     ap.add_argument("--codebook", choices=["tensor", "layer"], default="tensor")
+    ap.add_argument("--sweep", action="store_true",
+                    help="one bf16 decoder layer of each model family of the paper (1.5B to "
+                         "405B parameters), drawn on the GPU and compressed with the device "
+                         "encoder: one JSON line per model")
     ap.add_argument("--encode", action="store_true",
                     help="time the device encoder (wc_encode_device) on the resident 70B "
                          "layer instead of the decode")
@@ -188,6 +192,8 @@ def main() -> int:
         return gemv_bench(args, dev)
     if args.encode:
         return encode_bench(args, dev)
+    if args.sweep:
+        return sweep_bench(args, dev)
     cfg = WORKLOADS[args.workload]
     big = cfg == 5
     tile = tuple(int(v) for v in args.tile.lower().split("x")) if args.tile else (0, 0)
@@ -616,6 +622,107 @@ def encode_bench(args, dev) -> int:
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line), flush=True)
+    return 0
+
+
+def sweep_bench(args, dev) -> int:
+    """Decode throughput and compression of one bf16 decoder layer per model
+    family (qwen2-1.5b .. llama3-405b).  Each layer is drawn on the GPU,
+    compressed by wc_encode_device, checked to decode back bit-exact, and
+    decoded K times from resident blobs (copies rotated so at least 1 GiB of
+    blobs and outputs is touched, as for the other small workloads)."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15789_amd import synth, wc
+    stream = torch.cuda.current_stream(dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ws = torch.empty(wc.ANALYZE_WORKSPACE_BYTES, dtype=torch.uint8, device=dev)
+    for seed, (model, (shapes, sigma)) in enumerate(synth.MODEL_LAYERS.items(), start=20):
+        t0 = time.perf_counter()
+        tens = synth.layer_torch_device(shapes, sigma, seed, device="cuda")
+        entries = [("bf16", t, shape) for _, t, shape in tens]
+        kw = dict(chunk_bytes=args.chunk_bytes, lanes=args.lanes)
+        dblob, size = wc.encode_device(entries, **kw)
+        torch.cuda.synchronize()
+        n = int(size.item())
+        dblob = dblob[:n].clone()
+        blob = wc.open_blob(dblob.cpu().numpy())
+        stats = [wc.analyze_device("bf16", t, workspace=ws) for _, t, _ in entries]
+        bound = sum(st["bound_bytes"] for st in stats)
+        out_b = sum(blob.out_bytes)
+        n_res = max(1, -(-ROTATE_BYTES // (n + out_b)))
+        dblobs = [dblob] + [dblob.clone() for _ in range(n_res - 1)]
+        outs = [[torch.empty(b, dtype=torch.uint8, device=dev) for b in blob.out_bytes]
+                for _ in range(n_res)]
+        for r in range(n_res):
+            wc.decode_torch(blob, dblobs[r], outs=outs[r], err=err)
+        torch.cuda.synchronize()
+        if int(err.item()) or any(not torch.equal(o, t) for r in range(n_res)
+                                  for o, (_, t, _) in zip(outs[r], entries)):
+            raise RuntimeError(f"{model}: decode differs from the original layer")
+        setup_s = time.perf_counter() - t0
+
+        def step(k):
+            r = k % n_res
+            wc.decode(blob, dblobs[r].data_ptr(), [o.data_ptr() for o in outs[r]],
+                      stream.cuda_stream, err.data_ptr())
+
+        for k in range(args.warmup):
+            step(k)
+        torch.cuda.synchronize()
+        K = args.steps
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(K)]
+        start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        start.record(stream)
+        for k in range(K):
+            ev[k][0].record(stream)
+            step(args.warmup + k)
+            ev[k][1].record(stream)
+        end.record(stream)
+        torch.cuda.synchronize()
+        if int(err.item()):
+            raise RuntimeError(f"{model}: device errors {wc.describe_errors(int(err.item()))}")
+        last = (args.warmup + K - 1) % n_res
+        if any(not torch.equal(o, t) for o, (_, t, _) in zip(outs[last], entries)):
+            raise RuntimeError(f"{model}: timed decode differs from the original layer")
+        total_ms = start.elapsed_time(end)
+        mean_s = float(np.mean([a.elapsed_time(b) for a, b in ev])) / 1e3
+        achieved = (n + out_b) / mean_s / 1e9
+        line = {
+            "metric": METRIC,
+            "value": round(K * out_b / (total_ms / 1e3) / 1e9, 2),
+            "unit": "GB/s",
+            "n_gpus": 1,
+            "steps": K,
+            "warmup": args.warmup,
+            "ms_per_step": round(total_ms / K, 4),
+            "higher_is_better": True,
+            "scaling": "weak",
+            "vs_baseline": None,
+            "dtype": "u32",
+            "data": "synthetic",
+            "config": {"workload": f"{model}-layer-bf16", "mode": "model-sweep",
+                       "tensors_per_step": len(entries), "params": out_b // 2,
+                       "decoded_bytes_per_step": out_b, "compressed_bytes_per_step": n,
+                       "sigma": sigma, "chunk_bytes": args.chunk_bytes, "lanes": args.lanes,
+                       "copies_resident": n_res, "parallelism": "single-gpu"},
+            "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                         "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                         "traffic": None, "kernel": "wc_decode_kernel",
+                         "mean_launch_us": round(mean_s * 1e6, 2),
+                         "algorithmic_bytes_per_launch": int(n + out_b)},
+            "compression": {"ratio": round(out_b / n, 5), "bound_ratio": round(out_b / bound, 5),
+                            "payload_over_bound_pct":
+                                round(100 * (blob.payload_bytes() / bound - 1), 4),
+                            "total_over_bound_pct": round(100 * (n / bound - 1), 4)},
+            "cpu_baseline": None,
+            "setup_s": round(setup_s, 1),
+        }
+        print(json.dumps(line), flush=True)
+        del tens, entries, dblob, dblobs, outs, blob
+        torch.cuda.empty_cache()
     return 0
 
 

@@ -395,6 +395,51 @@ CONFIG_NAMES = {
 }
 
 
+def _decoder_layer(d: int, f: int, kv: int, experts: int = 1, head: int = 128):
+    """Linear shapes of one decoder layer: hidden size d, intermediate size f,
+    kv key/value heads of `head` dims (grouped-query attention), `experts`
+    MLP experts."""
+    shapes = [("q_proj", d, d), ("k_proj", kv * head, d), ("v_proj", kv * head, d),
+              ("o_proj", d, d)]
+    for e in range(experts):
+        p = f"experts.{e}." if experts > 1 else ""
+        shapes += [(p + "gate_proj", f, d), (p + "up_proj", f, d), (p + "down_proj", d, f)]
+    return shapes
+
+
+# One bf16 decoder layer of each model family the paper evaluates (Sec. VI-A,
+# 1.5B to 405B parameters), with the sizes of the public model configurations,
+# and the sigma of the Normal draw (0.1 % outlier input columns x20 as above).
+MODEL_LAYERS = {
+    "qwen2-1.5b": (_decoder_layer(1536, 8960, 2), 0.02),
+    "mistral-7b": (_decoder_layer(4096, 14336, 8), 0.02),
+    "qwen2.5-14b": (_decoder_layer(5120, 13824, 8), 0.02),
+    "deepseek-67b": (_decoder_layer(8192, 22016, 8), 0.015),
+    "mixtral-8x22b": (_decoder_layer(6144, 16384, 8, experts=8), 0.015),
+    "llama3-405b": (_decoder_layer(16384, 53248, 8), 0.01),
+}
+
+
+def layer_torch_device(shapes, sigma: float, seed: int, layer: int = 0, device: str = "cuda"):
+    """bf16 Normal(0, sigma) tensors with 0.1 % outlier input columns x20, drawn
+    on the GPU with torch's Philox generator seeded (seed, layer, tensor).
+    Returns a list of (name, uint8 device tensor holding the bf16 storage,
+    shape)."""
+    import torch
+    out = []
+    for j, (name, o, i) in enumerate(shapes):
+        g = torch.Generator(device=device)
+        g.manual_seed((seed << 40) | (layer << 20) | j)
+        w = torch.randn((o, i), generator=g, device=device, dtype=torch.float32)
+        w.mul_(sigma)
+        mult = torch.from_numpy(_outlier_multiplier(i, _key(seed, layer, j))).to(device)
+        w.mul_(mult)
+        b = w.to(torch.bfloat16)
+        del w
+        out.append((name, b.view(torch.uint8).reshape(-1), (o, i)))
+    return out
+
+
 def config_torch_device(cfg: int, layer: int, device: str = "cuda"):
     """70B-layer bf16 tensors drawn on the GPU with torch's device generator.
 
@@ -403,18 +448,6 @@ def config_torch_device(cfg: int, layer: int, device: str = "cuda"):
     differ from the numpy recipe.  Returns a list of (name, uint8 device
     tensor holding the bf16 storage, shape).
     """
-    import torch
     if cfg != 5:
         raise ValueError("device-side drawing is provided for the 70B layer only")
-    out = []
-    for j, (name, o, i) in enumerate(LLAMA3_70B):
-        g = torch.Generator(device=device)
-        g.manual_seed((4 << 40) | (layer << 20) | j)
-        w = torch.randn((o, i), generator=g, device=device, dtype=torch.float32)
-        w.mul_(0.015)
-        mult = torch.from_numpy(_outlier_multiplier(i, _key(4, layer, j))).to(device)
-        w.mul_(mult)
-        b = w.to(torch.bfloat16)
-        del w
-        out.append((name, b.view(torch.uint8).reshape(-1), (o, i)))
-    return out
+    return layer_torch_device(LLAMA3_70B, 0.015, 4, layer, device)

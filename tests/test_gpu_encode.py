@@ -284,3 +284,25 @@ def test_analyze_device_edges(dev):
     for dt, d in cases:
         x = to_dev(d, dev) if d.size else torch.empty(0, dtype=torch.uint8, device=dev)
         _same_stats(wc.analyze_device(dt, x), oracle.analyze(dt, d))
+
+
+@pytest.mark.parametrize("model", ["qwen2-1.5b", "mistral-7b"])
+def test_model_family_layer(dev, model):
+    """A whole decoder layer of a model family (the benchmark's sweep draw):
+    the device blob equals the oracle's, and decodes on the GPU to the layer."""
+    say("model layer", model)
+    shapes, sigma = synth.MODEL_LAYERS[model]
+    tens = synth.layer_torch_device(shapes, sigma, 20, device="cuda")
+    dents = [("bf16", t, shape) for _, t, shape in tens]
+    blob, size = wc.encode_device(dents)
+    torch.cuda.synchronize()
+    got = blob[: int(size.item())].cpu().numpy().tobytes()
+    host = [("bf16", t.cpu().numpy(), shape) for _, t, shape in tens]
+    assert got == oracle.encode(host)
+    desc = wc.open_blob(got)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    outs = wc.decode_torch(desc, blob, err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    for (_, t, _), out in zip(tens, outs):
+        assert torch.equal(out, t)
