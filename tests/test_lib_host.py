@@ -4,7 +4,7 @@ No GPU call is made here.  The library's encoder is separate code from the
 oracle's; both follow the same format readings, so their blobs must be
 byte-identical, and the library's statistics must equal the oracle's.
 """
-import ctypes
+import ctypes as C
 import math
 import os
 import re
@@ -225,3 +225,37 @@ def test_device_encoder_bounds_rejects_bad_arguments():
         wc.encode_device_bounds([("bf16", 1001)])
     with pytest.raises(wc.WcError):
         wc.encode_device_bounds([("u8", 1000, (3, 7))])
+
+
+def test_device_encoder_rejects_before_any_launch():
+    """wc_encode_device / wc_analyze_device validate every argument on the host
+    before any HIP call; the fake device addresses below are never touched."""
+    lib = wc.lib()
+    fake = 1 << 40                      # 16-byte aligned, never dereferenced
+    n = 4096
+    t = (wc._Tensor * 1)(wc._Tensor(C.c_void_p(fake), n, wc.DTYPES["u8"], 0, 0, 0))
+    prm = wc._Params(65536, 64, 12, 0, 0, 0, 0, 0)
+    cap, wsb = wc.encode_device_bounds([("u8", n)])
+
+    def enc(tensors=t, blob=fake, capacity=cap, ws=fake, ws_bytes=wsb, size=fake, p=prm):
+        return lib.wc_encode_device(tensors, 1, C.byref(p), C.c_void_p(blob), capacity,
+                                    C.c_void_p(ws), ws_bytes, None, C.c_void_p(size))
+
+    assert enc(capacity=cap - 1) == -1          # blob one byte short
+    assert enc(ws_bytes=wsb - 1) == -1          # workspace too small
+    assert enc(blob=fake + 8) == -1             # misaligned blob
+    assert enc(ws=fake + 4) == -1               # misaligned workspace
+    assert enc(size=0) == -1                    # no size word
+    assert enc(blob=0) == -1
+    bad = (wc._Tensor * 1)(wc._Tensor(C.c_void_p(fake + 1), n, wc.DTYPES["u8"], 0, 0, 0))
+    assert enc(tensors=bad) == -1               # misaligned source
+    odd = (wc._Tensor * 1)(wc._Tensor(C.c_void_p(fake), n - 1, wc.DTYPES["bf16"], 0, 0, 0))
+    assert enc(tensors=odd) == -1               # odd byte count of a 16-bit format
+    assert enc(p=wc._Params(65536, 64, 11, 0, 0, 0, 0, 0)) == -1   # prob_bits must be 12
+    st = wc._Stats()
+    assert lib.wc_analyze_device(t, C.c_void_p(fake), wc.ANALYZE_WORKSPACE_BYTES - 1, None,
+                                 C.byref(st)) == -1
+    assert lib.wc_analyze_device(bad, C.c_void_p(fake), wc.ANALYZE_WORKSPACE_BYTES, None,
+                                 C.byref(st)) == -1
+    assert lib.wc_analyze_device(odd, C.c_void_p(fake), wc.ANALYZE_WORKSPACE_BYTES, None,
+                                 C.byref(st)) == -1
