@@ -202,23 +202,26 @@ wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_
 
 /* wc_gemv -- fused decode-GEMM (Alg. 1 / 3): for each of n jobs i,
  * dev_y[i] += dev_x[i] * W^T with W = tensor tensors[i] of the blob, decoded
- * on the fly and never written to memory.  All jobs run in one launch.
+ * on the fly and never written to memory.  Every job of one tile height runs
+ * in one launch.
  *   n        1..32 jobs;
  *   tensors  host array of n tensor indices; each W must be bf16 with a shape
- *            (N = rows, K = cols), coded with 64 lanes in column-block tiles
- *            of 64 rows (wc_params.tile_rows = 64, tile_order =
- *            WC_TILE_COLUMN_BLOCKS);
+ *            (N = rows, K = cols, 64 * K * 2 bytes below 2 GiB), coded with 64
+ *            lanes in column-block tiles (wc_params.tile_order =
+ *            WC_TILE_COLUMN_BLOCKS) of 64 rows (the products on the VALU,
+ *            m <= 8) or of 16 rows (the products on the matrix cores,
+ *            v_mfma_f32_16x16x32_bf16, m <= 64);
  *   dev_x    host array of n device pointers to bf16 activations, m x K
  *            row-major, 16-byte aligned (jobs may share one x);
- *   m        1..8 rows of activations, the same for every job;
+ *   m        1..64 rows of activations, the same for every job;
  *   dev_y    host array of n device pointers to float, m x N row-major; the
  *            products are added (clear y first for a plain product).  The
- *            tiles of one band of 64 rows add with fp32 atomics, so the
+ *            tiles of one band of rows add with fp32 atomics, so the
  *            summation order, and the last bits of y, can differ between runs;
  *   stream, dev_err as for wc_decode.
  * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument), or
  * WC_EUNSUPPORTED (a tensor is not a bf16 64-lane column-block tensor of 64
- * rows per tile). */
+ * or 16 rows per tile, m above its tile height's limit, or K too large). */
 wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n, const uint32_t* tensors,
                   const void* const* dev_x, uint32_t m, float* const* dev_y, void* stream,
                   int32_t* dev_err);

@@ -92,7 +92,7 @@ struct LaunchArgs {
   uint64_t records_end;
   uint64_t err;          // int32_t* or 0
   uint32_t n_tensors;
-  uint32_t pad;
+  uint32_t m;            // fused GEMM: rows of x (and of y) in every job
   DevTensor t[kMaxLaunchTensors];
 };
 
@@ -438,13 +438,26 @@ __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ 
 // of its row with v_dot2_f32_bf16, reading the matching x columns as scalar
 // (wave-uniform) loads, and adds them to y once per tile (fp32 atomics: the
 // tiles of one row band split K).
-template <int G, int L, bool kTiled, int kM = 0>
+//
+// kMB: the fused GEMM on the matrix cores, for up to 16 kMB rows of x.  It
+// needs column-block tiles of 16 rows decoded by 64 lanes: lane l then holds,
+// in every wave row r, the 8 weights of tile row l mod 16 at columns
+// b * tile_c + 32 r + 8 (l div 16) .., which is exactly the B operand of
+// v_mfma_f32_16x16x32_bf16 (B[k][n] = W[n][k], lane l holding column n = l
+// mod 16, rows 8 (l div 16) ..).  Each lane loads the matching 8 x values of
+// row l mod 16 of every block of 16 x rows (the A operand; rows past M read
+// as zeros through the buffer range check) one row of the wave ahead, and
+// every wave row issues one MFMA per x block.  At the end of the tile each
+// lane adds its 4 accumulators per block to y (fp32 atomics).
+template <int G, int L, bool kTiled, int kM = 0, int kMB = 0>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
                                               const uint2* __restrict__ tab, uint32_t* ring,
                                               const IndexPre& pre) {
-  constexpr bool kGemv = kM > 0;  // fused GEMM with kM rows of x
+  constexpr bool kGemv = kM > 0;   // fused GEMM with kM rows of x, dot products
+  constexpr bool kMfma = kMB > 0;  // fused GEMM with kMB blocks of 16 rows of x, MFMA
   static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
+  static_assert(!kMfma || (G == 2 && L == 64 && kTiled && !kGemv), "MFMA GEMM: bf16 tiles");
   constexpr int kH = Chain<L>::kH;
   constexpr int W = 4 * G;                    // symbols per lane-group
   constexpr int kGroupsPerRow = W / 2;        // groups of two steps in a row
@@ -525,6 +538,23 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
     for (int m = 0; m < kM; m++) acc[m] = 0.0f;
     xrow = T.x + 2ull * (chunk0 % T.ntc) * (1u << T.log_tc);
   }
+  typedef __attribute__((ext_vector_type(8))) __bf16 bf8;
+  typedef __attribute__((ext_vector_type(4))) float f4;
+  typedef __attribute__((ext_vector_type(4))) unsigned int u4v;
+  f4 macc[kMfma ? kMB : 1];
+  u4v xa[kMfma ? kMB : 1];
+  // the x rows (fused GEMM on the matrix cores): a.m rows of K bf16
+  const uint32_t K = T.ntc << T.log_tc;  // columns of W = length of an x row
+  const __amdgpu_buffer_rsrc_t xrs =
+      make_rsrc(reinterpret_cast<const void*>(T.x), kMfma ? a.m * K * 2u : 0u);
+  uint32_t xoff = 0, xblk = 0;
+  if constexpr (kMfma) {
+#pragma unroll
+    for (int mb = 0; mb < kMB; mb++) macc[mb] = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    // this lane's 8 x values of wave row 0: row sub mod 16, columns 8 (sub div 16) ..
+    xoff = ((sub & 15u) * K + (chunk0 % T.ntc) * (1u << T.log_tc) + 8u * (sub >> 4)) * 2u;
+    xblk = 32u * K;  // bytes of 16 rows of x
+  }
 
   // group g of the chunk, j = g mod kUnroll (static)
   auto group = [&](uint32_t g, auto jc, auto tailc) {
@@ -539,6 +569,13 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
     }
     __builtin_amdgcn_wave_barrier();
     const uint32_t r = g / kGroupsPerRow;
+    if constexpr (kMfma && j % kGroupsPerRow == 0) {
+      // the A operands of this wave row (32 columns = 64 bytes per row)
+#pragma unroll
+      for (int mb = 0; mb < kMB; mb++)
+        xa[mb] = __builtin_bit_cast(
+            u4v, __builtin_amdgcn_raw_buffer_load_b128(xrs, xoff + mb * xblk + r * 64u, 0, 0));
+    }
     const int nv = kTail ? max(0, min<int>(W, (int)n_lane - (int)(r * kRowSym + sub * W))) : W;
 #pragma unroll
     for (int k = k0; k < k0 + 2; k++) lo[k % G] = step<!kTail, L>(c, tab, k < nv, h);
@@ -557,6 +594,14 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
         rq[(j / kGroupsPerRow) % kRawRows] = __builtin_bit_cast(
             uint2, __builtin_amdgcn_raw_buffer_load_b64(c.rr, (r + kRawRows) * kRawRowBytes + raw_v,
                                                         0, 0));
+      }
+      if constexpr (kMfma) {
+        const bf8 b = __builtin_bit_cast(bf8, u4v{ow[0], ow[1], ow[2], ow[3]});
+#pragma unroll
+        for (int mb = 0; mb < kMB; mb++)
+          macc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, xa[mb]), b,
+                                                             macc[mb], 0, 0, 0);
+        return;
       }
       if constexpr (kGemv) {
         // this lane: weights [8 r, 8 r + 8) of its tile row; x rows m < M
@@ -626,6 +671,19 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
 #pragma unroll
     for (int m = 0; m < kM; m++) unsafeAtomicAdd(y + uint64_t(m) * N + n, acc[m]);
   }
+  if constexpr (kMfma) {
+    // D[4 (sub div 16) + i][sub mod 16] of every x block: y row, W row = y column
+    const uint32_t n = (chunk0 / T.ntc) * 16u + (sub & 15u);
+    const uint64_t N = uint64_t(T.n_chunks / T.ntc) * 16u;
+    float* y = reinterpret_cast<float*>(T.dst);
+#pragma unroll
+    for (int mb = 0; mb < kMB; mb++)
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        const uint32_t m = mb * 16u + 4u * (sub >> 4) + i;
+        if (m < a.m) unsafeAtomicAdd(y + uint64_t(m) * N + n, macc[mb][i]);
+      }
+  }
 
   // --- end-of-chunk checks: every lane back at 2^16, every word consumed ----
   uint32_t bits = 0;
@@ -679,10 +737,11 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
     by_kind(std::integral_constant<int, 64>{});
 }
 
-// The fused decode-GEMM of up to kMaxLaunchTensors tensors (column-block
-// tiles of 64 x tile_c bf16, 64 lanes) in one launch: one wave per tile,
-// y += x * W^T for each tensor's own x and y.
-template <int kM>
+// The fused decode-GEMM of up to kMaxLaunchTensors tensors in one launch: one
+// wave per tile, y += x * W^T for each tensor's own x and y.  kM > 0: column-
+// block tiles of 64 x tile_c bf16, kM rows of x, dot products on the VALU;
+// kMB > 0: column-block tiles of 16 x tile_c, up to 16 kMB rows of x, MFMA.
+template <int kM, int kMB>
 __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   __shared__ uint2 tab[wc::kTableSize];
   __shared__ uint32_t cum[260];
@@ -700,7 +759,7 @@ __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   build_table(a, T, tab, cum, tid);
   __syncthreads();
   if (chunk >= T.n_chunks) return;
-  decode_chunks<2, 64, true, kM>(a, T, chunk, lane, tab, ring[wave], pre);
+  decode_chunks<2, 64, true, kM, kMB>(a, T, chunk, lane, tab, ring[wave], pre);
 }
 
 }  // namespace
@@ -792,38 +851,60 @@ extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t
   if (!desc || !desc->priv || !dev_blob || !tensors || !dev_x || !dev_y || n == 0 ||
       n > kMaxLaunchTensors)
     return WC_EINVAL;
-  if (m < 1 || m > 8) return WC_EINVAL;
+  if (m < 1 || m > 64) return WC_EINVAL;
   const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
   for (uint32_t i = 0; i < n; i++) {
     if (tensors[i] >= desc->n_tensors || !dev_x[i] || !dev_y[i] ||
         reinterpret_cast<uintptr_t>(dev_x[i]) % 16)
       return WC_EINVAL;
     const wc::TensorInfo& T = P.tensors[tensors[i]];
-    if (T.dtype != WC_BF16 || T.lanes != 64 || T.tile_r != 64 ||
-        T.tile_order != WC_TILE_COLUMN_BLOCKS)
+    if (T.dtype != WC_BF16 || T.lanes != 64 || T.tile_order != WC_TILE_COLUMN_BLOCKS ||
+        !(T.tile_r == 64 || T.tile_r == 16))
       return WC_EUNSUPPORTED;
+    if (T.tile_r == 64 && m > 8) return WC_EUNSUPPORTED;  // dot-product path: m <= 8
     if (T.rows > 0xFFFFFFFFull || T.cols > 0xFFFFFFFFull) return WC_EUNSUPPORTED;
+    // x offsets of a lane reach 64 rows (4 blocks of 16) of 2 * cols bytes
+    if (64ull * T.cols * 2 > 0x7FFFFFFFull) return WC_EUNSUPPORTED;
   }
-  LaunchArgs args{};
-  fill_common(args, P, dev_blob, dev_err);
-  uint32_t wgs = 0;
-  for (uint32_t i = 0; i < n; i++) {
-    const wc::TensorInfo& T = P.tensors[tensors[i]];
-    fill_tensor(args.t[i], T, dev_y[i], wgs);
-    args.t[i].x = reinterpret_cast<uint64_t>(dev_x[i]);
-    wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
-  }
-  args.n_tensors = n;
   const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  switch (m) {
-    case 1: hipLaunchKernelGGL(wc_gemv_kernel<1>, dim3(wgs), dim3(kThreads), 0, st, args); break;
-    case 2: hipLaunchKernelGGL(wc_gemv_kernel<2>, dim3(wgs), dim3(kThreads), 0, st, args); break;
-    case 3: hipLaunchKernelGGL(wc_gemv_kernel<3>, dim3(wgs), dim3(kThreads), 0, st, args); break;
-    case 4: hipLaunchKernelGGL(wc_gemv_kernel<4>, dim3(wgs), dim3(kThreads), 0, st, args); break;
-    case 5: hipLaunchKernelGGL(wc_gemv_kernel<5>, dim3(wgs), dim3(kThreads), 0, st, args); break;
-    case 6: hipLaunchKernelGGL(wc_gemv_kernel<6>, dim3(wgs), dim3(kThreads), 0, st, args); break;
-    case 7: hipLaunchKernelGGL(wc_gemv_kernel<7>, dim3(wgs), dim3(kThreads), 0, st, args); break;
-    default: hipLaunchKernelGGL(wc_gemv_kernel<8>, dim3(wgs), dim3(kThreads), 0, st, args); break;
+  // one launch for the jobs of each path: 64-row tiles (VALU dot products)
+  // and 16-row tiles (MFMA)
+  for (uint32_t rows : {64u, 16u}) {
+    LaunchArgs args{};
+    fill_common(args, P, dev_blob, dev_err);
+    uint32_t wgs = 0, nt = 0;
+    for (uint32_t i = 0; i < n; i++) {
+      const wc::TensorInfo& T = P.tensors[tensors[i]];
+      if (T.tile_r != rows) continue;
+      fill_tensor(args.t[nt], T, dev_y[i], wgs);
+      args.t[nt].x = reinterpret_cast<uint64_t>(dev_x[i]);
+      wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
+      nt++;
+    }
+    if (!nt) continue;
+    args.n_tensors = nt;
+    args.m = m;
+    const dim3 grid(wgs), block(kThreads);
+    if (rows == 64) {
+      switch (m) {
+        case 1: hipLaunchKernelGGL((wc_gemv_kernel<1, 0>), grid, block, 0, st, args); break;
+        case 2: hipLaunchKernelGGL((wc_gemv_kernel<2, 0>), grid, block, 0, st, args); break;
+        case 3: hipLaunchKernelGGL((wc_gemv_kernel<3, 0>), grid, block, 0, st, args); break;
+        case 4: hipLaunchKernelGGL((wc_gemv_kernel<4, 0>), grid, block, 0, st, args); break;
+        case 5: hipLaunchKernelGGL((wc_gemv_kernel<5, 0>), grid, block, 0, st, args); break;
+        case 6: hipLaunchKernelGGL((wc_gemv_kernel<6, 0>), grid, block, 0, st, args); break;
+        case 7: hipLaunchKernelGGL((wc_gemv_kernel<7, 0>), grid, block, 0, st, args); break;
+        default: hipLaunchKernelGGL((wc_gemv_kernel<8, 0>), grid, block, 0, st, args); break;
+      }
+    } else {
+      switch ((m + 15) / 16) {
+        case 1: hipLaunchKernelGGL((wc_gemv_kernel<0, 1>), grid, block, 0, st, args); break;
+        case 2: hipLaunchKernelGGL((wc_gemv_kernel<0, 2>), grid, block, 0, st, args); break;
+        case 3: hipLaunchKernelGGL((wc_gemv_kernel<0, 3>), grid, block, 0, st, args); break;
+        default: hipLaunchKernelGGL((wc_gemv_kernel<0, 4>), grid, block, 0, st, args); break;
+      }
+    }
+    if (hipGetLastError() != hipSuccess) return WC_EHIP;
   }
-  return hipGetLastError() == hipSuccess ? WC_OK : WC_EHIP;
+  return WC_OK;
 }

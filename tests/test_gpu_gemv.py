@@ -2,10 +2,11 @@
 
 wc_gemv adds x * W^T to y, decoding W on the fly.  The reference is the
 oracle's fp64 product of the same bf16 values (orc_gemv_bf16, pinned on
-one-hot and small-integer inputs).  The GPU sums in fp32 (v_dot2_f32_bf16,
-then fp32 atomics across the tiles of a row band); with at most K roundings
-of relative size 2^-24 each, |y - y_ref| <= K * 2^-24 * sum_k |x_k w_k|.  The
-test allows twice that.
+one-hot and small-integer inputs).  The GPU sums in fp32 (v_dot2_f32_bf16 for
+64-row tiles, v_mfma_f32_16x16x32_bf16 for 16-row tiles, then fp32 atomics
+across the tiles of a row band); bf16 products are exact in fp32, so with at
+most K roundings of relative size 2^-24 each, |y - y_ref| <= K * 2^-24 *
+sum_k |x_k w_k|.  The test allows twice that.
 """
 import struct
 
@@ -151,3 +152,70 @@ def test_gemv_many_jobs_in_one_launch(dev, m):
     assert int(err.item()) == 0
     for t, y in zip(ts, ys):
         _check(y.cpu().numpy().astype(np.float64), t.data, xbits[t.shape[1]])
+
+
+# --- 16-row column-block tiles: the product on the matrix cores --------------
+
+@pytest.mark.parametrize("shape,tile", [((256, 512), (16, 256)), ((192, 1024), (16, 512)),
+                                        ((1024, 4096), (16, 2048)), ((16, 256), (16, 256))])
+@pytest.mark.parametrize("m", [1, 3, 16, 17, 40, 64])
+def test_mfma_gemm_matches_the_reference(dev, shape, tile, m):
+    say("mfma gemm", shape, tile, m)
+    rng = np.random.default_rng(shape[0] + 7 * m)
+    w = _bf16(rng.normal(0, 0.02, shape))
+    x = _bf16(rng.normal(0, 1.0, (m, shape[1])))
+    blob = wc.encode([("bf16", w, shape)], tile=tile, tile_order=1)
+    y = _run_gemv(blob, dev, 0, x)
+    _check(y, w, x)
+
+
+def test_mfma_gemm_small_integers_exact(dev):
+    """Small-integer x and W (exact in bf16, sums exact in fp32): y must equal
+    the oracle's product exactly, which pins the operand and output layouts."""
+    rng = np.random.default_rng(41)
+    shape, m = (64, 512), 37
+    w = _bf16(rng.integers(-4, 5, shape).astype(np.float32))
+    x = _bf16(rng.integers(-3, 4, (m, shape[1])).astype(np.float32))
+    blob = wc.encode([("bf16", w, shape)], tile=(16, 256), tile_order=1)
+    y = _run_gemv(blob, dev, 0, x)
+    ref, _ = oracle.gemv_bf16(w, x)
+    assert np.array_equal(y, ref)
+
+
+def test_mfma_gemm_full_size_layer(dev):
+    """All seven projections of a Llama-3-70B layer (numpy draw) in 16 x 2048
+    tiles, one launch, 64 rows of x: every y within the fp32 bound."""
+    ts = synth.config(5)
+    blob = wc.encode([(t.dtype, t.data, t.shape) for t in ts], tile=(16, 2048), tile_order=1)
+    d = wc.to_device(blob, dev)
+    rng = np.random.default_rng(42)
+    xbits = {}
+    for t in ts:
+        xbits.setdefault(t.shape[1], _bf16(rng.normal(0, 1.0, (64, t.shape[1]))))
+    xdev = {k: _dev_x(v, dev) for k, v in xbits.items()}
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ys = wc.gemv_torch(blob, d, list(range(len(ts))), [xdev[t.shape[1]] for t in ts], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    for t, y in zip(ts, ys):
+        # rows of W sampled (the fp64 reference of all 8192 x 8192 is slow)
+        rows = np.random.default_rng(t.shape[0]).choice(t.shape[0], 64, replace=False)
+        ref, absref = oracle.gemv_bf16(np.ascontiguousarray(t.data[rows]), xbits[t.shape[1]])
+        tol = 2.0 * t.shape[1] * 2.0 ** -24 * absref + 1e-30
+        got = y.cpu().numpy().astype(np.float64)[:, rows]
+        assert (np.abs(got - ref) <= tol).all(), t.name
+
+
+def test_gemv_row_limits(dev):
+    """64-row tiles take up to 8 rows of x, 16-row tiles up to 64."""
+    rng = np.random.default_rng(43)
+    w = _bf16(rng.normal(0, 0.02, (128, 512)))
+    b64 = wc.encode([("bf16", w, (128, 512))], tile=(64, 256), tile_order=1)
+    b16 = wc.encode([("bf16", w, (128, 512))], tile=(16, 256), tile_order=1)
+    x8, x9 = (_bf16(rng.normal(0, 1.0, (m, 512))) for m in (8, 9))
+    _check(_run_gemv(b64, dev, 0, x8), w, x8)
+    _check(_run_gemv(b16, dev, 0, x9), w, x9)
+    with pytest.raises(wc.WcError):
+        _run_gemv(b64, dev, 0, x9)
+    with pytest.raises(wc.WcError):
+        _run_gemv(b16, dev, 0, _bf16(rng.normal(0, 1.0, (65, 512))))
