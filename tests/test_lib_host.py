@@ -168,10 +168,13 @@ def test_gemv_rejects_before_any_launch():
     good = wc.encode([("bf16", w, (128, 512))], tile=(64, 256), tile_order=1)
     rows = wc.encode([("bf16", w, (128, 512))], tile=(64, 256), tile_order=0)
     flat = wc.encode([("bf16", w, (128, 512))])
-    for m in (0, 9):
+    for m in (0, 65):
         with pytest.raises(wc.WcError) as e:
             wc.gemv(good, 16, [0], [16], m, [16])
         assert e.value.rc == -1
+    with pytest.raises(wc.WcError) as e:          # 64-row tiles: dot products, m <= 8
+        wc.gemv(good, 16, [0], [16], 9, [16])
+    assert e.value.rc == -5
     for args in (([0], [8], [16]),            # x not 16-byte aligned
                  ([1], [16], [16]),           # no such tensor
                  ([0], [16], [0]),            # no y
