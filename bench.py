@@ -171,9 +171,10 @@ def main() -> int:
                     help="time the fused decode-GEMM y += x W^T (x: M rows, 1..64) over the "
                          "70B layer instead of the decode, next to the same product unfused "
                          "(wc_decode, then torch.matmul) and uncompressed (torch.matmul)")
-    ap.add_argument("--gemv-rows", type=int, choices=[64, 16], default=0,
-                    help="tile rows of the fused GEMM: 64 (VALU dot products, M <= 8) or 16 "
-                         "(matrix cores, M <= 64); default 64 for M <= 8, else 16")
+    ap.add_argument("--gemv-rows", type=int, choices=[64, 32, 16], default=0,
+                    help="tile rows of the fused GEMM: 64 (VALU dot products for M <= 5, "
+                         "matrix cores above), 32 or 16 (matrix cores); default 16 for "
+                         "M <= 16, else 64")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -408,14 +409,13 @@ def gemv_bench(args, dev) -> int:
 
     from paper_2606_15789_amd import synth, wc
     M = args.gemv
-    rows = args.gemv_rows or (64 if M <= 8 else 16)
-    if not 1 <= M <= (8 if rows == 64 else 64):
-        print("--gemv takes 1..8 rows of activations with 64-row tiles, 1..64 with 16-row "
-              "tiles", file=sys.stderr)
+    rows = args.gemv_rows or (16 if M <= 16 else 64)
+    if not 1 <= M <= 64:
+        print("--gemv takes 1..64 rows of activations", file=sys.stderr)
         return 2
-    # 64 KiB tiles: 64 x 512 (a lane per W row, VALU dot products) or 16 x 2048
-    # (a wave row per MFMA operand)
-    tile = (64, 512) if rows == 64 else (16, 2048)
+    # 64 KiB tiles: 64 x 512 (a lane per W row, VALU dot products), 32 x 1024 or
+    # 16 x 2048 (a wave row per MFMA operand)
+    tile = {64: (64, 512), 32: (32, 1024), 16: (16, 2048)}[rows]
     t0 = time.perf_counter()
     tens = synth.config_torch_device(5, 0, device="cuda")
     shapes = [shape for _, _, shape in tens]
@@ -500,7 +500,9 @@ def gemv_bench(args, dev) -> int:
         "data": "synthetic",
         "config": {"workload": "llama3-70b-layer-bf16", "mode": "fused-gemv", "m": M,
                    "tile": f"{tile[0]}x{tile[1]}", "tile_order": "column-blocks",
-                   "product": "v_dot2_f32_bf16" if rows == 64 else "v_mfma_f32_16x16x32_bf16",
+                   "product": ("v_dot2_f32_bf16" if rows == 64 and M <= 8 else
+                               "v_mfma_f32_16x16x32_bf16" if rows == 16 else
+                               "v_mfma_f32_32x32x16_bf16"),
                    "lanes": 64, "weight_bytes_per_step": wbytes,
                    "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,

@@ -208,9 +208,13 @@ wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_
  *   tensors  host array of n tensor indices; each W must be bf16 with a shape
  *            (N = rows, K = cols, 64 * K * 2 bytes below 2 GiB), coded with 64
  *            lanes in column-block tiles (wc_params.tile_order =
- *            WC_TILE_COLUMN_BLOCKS) of 64 rows (the products on the VALU,
- *            m <= 8) or of 16 rows (the products on the matrix cores,
- *            v_mfma_f32_16x16x32_bf16, m <= 64);
+ *            WC_TILE_COLUMN_BLOCKS) of 64, 32 or 16 rows.  64-row tiles take
+ *            the products on the VALU for m <= 5 and on the matrix cores above
+ *            (v_mfma_f32_32x32x16_bf16 on pairs of k-blocks, which needs at
+ *            least 16 columns per tile); 32-row tiles use
+ *            v_mfma_f32_32x32x16_bf16 and 16-row tiles
+ *            v_mfma_f32_16x16x32_bf16.  On MI355X 16-row tiles are the
+ *            fastest up to m = 16 and 64-row tiles from m = 32;
  *   dev_x    host array of n device pointers to bf16 activations, m x K
  *            row-major, 16-byte aligned (jobs may share one x);
  *   m        1..64 rows of activations, the same for every job;
@@ -220,8 +224,9 @@ wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_
  *            summation order, and the last bits of y, can differ between runs;
  *   stream, dev_err as for wc_decode.
  * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument), or
- * WC_EUNSUPPORTED (a tensor is not a bf16 64-lane column-block tensor of 64
- * or 16 rows per tile, m above its tile height's limit, or K too large). */
+ * WC_EUNSUPPORTED (a tensor is not a bf16 64-lane column-block tensor of 64,
+ * 32 or 16 rows per tile, has 64-row tiles of 8 columns with m > 5, or K is
+ * too large). */
 wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n, const uint32_t* tensors,
                   const void* const* dev_x, uint32_t m, float* const* dev_y, void* stream,
                   int32_t* dev_err);

@@ -439,17 +439,27 @@ __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ 
 // (wave-uniform) loads, and adds them to y once per tile (fp32 atomics: the
 // tiles of one row band split K).
 //
-// kMB: the fused GEMM on the matrix cores, for up to 16 kMB rows of x.  It
-// needs column-block tiles of 16 rows decoded by 64 lanes: lane l then holds,
-// in every wave row r, the 8 weights of tile row l mod 16 at columns
-// b * tile_c + 32 r + 8 (l div 16) .., which is exactly the B operand of
-// v_mfma_f32_16x16x32_bf16 (B[k][n] = W[n][k], lane l holding column n = l
-// mod 16, rows 8 (l div 16) ..).  Each lane loads the matching 8 x values of
-// row l mod 16 of every block of 16 x rows (the A operand; rows past M read
-// as zeros through the buffer range check) one row of the wave ahead, and
-// every wave row issues one MFMA per x block.  At the end of the tile each
-// lane adds its 4 accumulators per block to y (fp32 atomics).
-template <int G, int L, bool kTiled, int kM = 0, int kMB = 0>
+// kMB: the fused GEMM on the matrix cores, for up to kMR kMB rows of x.  It
+// needs column-block tiles of kMR (16 or 32) rows decoded by 64 lanes: lane l
+// then holds, in every wave row r, the 8 weights of tile row l mod kMR at
+// columns b * tile_c + (512 / kMR) r + 8 (l div kMR) .., which is exactly the
+// B operand of v_mfma_f32_16x16x32_bf16 (kMR = 16) or
+// v_mfma_f32_32x32x16_bf16 (kMR = 32): B[k][n] = W[n][k], lane l holding
+// column n = l mod kMR, rows 8 (l div kMR) ...  Each lane loads the matching
+// 8 x values of row l mod kMR of every block of kMR x rows (the A operand;
+// rows past M read as zeros through the buffer range check) at the start of
+// the wave row, and every wave row issues one MFMA per x block.  At the end
+// of the tile each lane adds its kMR * kMR / 64 accumulators per block to y
+// (fp32 atomics): lane l holds D[row][l mod kMR] with row = 4 (l div 16) + i
+// (kMR = 16) or 8 (i div 4) + 4 (l div 32) + i mod 4 (kMR = 32).
+//
+// kMR = 64: the same on column-block tiles of 64 rows (the dot-product
+// layout: lane l holds row l, columns 8 r ..).  Two wave rows r, r + 1 hold
+// 64 rows x 16 columns; one v_permlane32_swap per dword turns them into two
+// B operands of v_mfma_f32_32x32x16_bf16 (rows 0..31 and 32..63: lanes 0..31
+// keep row r, lanes 32..63 take row r + 1 of the same W rows), which share
+// one A operand of x, so every x value loaded feeds 64 W rows.
+template <int G, int L, bool kTiled, int kM = 0, int kMB = 0, int kMR = 16>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
                                               const uint2* __restrict__ tab, uint32_t* ring,
@@ -458,6 +468,9 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   constexpr bool kMfma = kMB > 0;  // fused GEMM with kMB blocks of 16 rows of x, MFMA
   static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
   static_assert(!kMfma || (G == 2 && L == 64 && kTiled && !kGemv), "MFMA GEMM: bf16 tiles");
+  static_assert(kMR == 16 || kMR == 32 || kMR == 64, "MFMA tiles of 16, 32 or 64 rows");
+  constexpr int kMM = kMR == 64 ? 32 : kMR;   // x rows per MFMA block
+  constexpr int kNB = kMR == 64 ? 2 : 1;      // MFMA output blocks of W rows per tile
   constexpr int kH = Chain<L>::kH;
   constexpr int W = 4 * G;                    // symbols per lane-group
   constexpr int kGroupsPerRow = W / 2;        // groups of two steps in a row
@@ -467,6 +480,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   constexpr uint32_t kRawRowBytes = 8u * L;    // raw bytes of one half-row (16-bit formats)
   constexpr uint32_t kLogW = G == 2 ? 3 : (G == 4 ? 4 : 5);
   constexpr int kPipe = Shape<L>::kPipe, kEvery = Shape<L>::kEvery;
+  static_assert(!kMfma || kMR != 64 || kUnroll == 2 * kGroupsPerRow, "row pairs per body");
   static_assert(kUnroll % (kPipe * kEvery) == 0 && kUnroll % kGroupsPerRow == 0,
                 "pipeline shape");
 
@@ -539,9 +553,11 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
     xrow = T.x + 2ull * (chunk0 % T.ntc) * (1u << T.log_tc);
   }
   typedef __attribute__((ext_vector_type(8))) __bf16 bf8;
-  typedef __attribute__((ext_vector_type(4))) float f4;
+  typedef __attribute__((ext_vector_type(kMM * kMM / 64))) float facc;
   typedef __attribute__((ext_vector_type(4))) unsigned int u4v;
-  f4 macc[kMfma ? kMB : 1];
+  constexpr uint32_t kRowXBytes = 1024u / kMR;  // bytes of an x row one wave row covers
+  facc macc[kMfma ? kMB : 1][kNB];
+  uint32_t prev[kMR == 64 ? 4 : 1];             // 64-row tiles: the even row's dwords
   u4v xa[kMfma ? kMB : 1];
   // the x rows (fused GEMM on the matrix cores): a.m rows of K bf16
   const uint32_t K = T.ntc << T.log_tc;  // columns of W = length of an x row
@@ -550,10 +566,12 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   uint32_t xoff = 0, xblk = 0;
   if constexpr (kMfma) {
 #pragma unroll
-    for (int mb = 0; mb < kMB; mb++) macc[mb] = f4{0.0f, 0.0f, 0.0f, 0.0f};
-    // this lane's 8 x values of wave row 0: row sub mod 16, columns 8 (sub div 16) ..
-    xoff = ((sub & 15u) * K + (chunk0 % T.ntc) * (1u << T.log_tc) + 8u * (sub >> 4)) * 2u;
-    xblk = 32u * K;  // bytes of 16 rows of x
+    for (int mb = 0; mb < kMB; mb++)
+#pragma unroll
+      for (int nb = 0; nb < kNB; nb++) macc[mb][nb] = facc{};
+    // this lane's 8 x values of wave row 0: row sub mod kMM, columns 8 (sub div kMM) ..
+    xoff = ((sub % kMM) * K + (chunk0 % T.ntc) * (1u << T.log_tc) + 8u * (sub / kMM)) * 2u;
+    xblk = 2u * kMM * K;  // bytes of kMM rows of x
   }
 
   // group g of the chunk, j = g mod kUnroll (static)
@@ -569,12 +587,14 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
     }
     __builtin_amdgcn_wave_barrier();
     const uint32_t r = g / kGroupsPerRow;
-    if constexpr (kMfma && j % kGroupsPerRow == 0) {
-      // the A operands of this wave row (32 columns = 64 bytes per row)
+    if constexpr (kMfma && j % kGroupsPerRow == 0 && (kMR != 64 || j < kGroupsPerRow)) {
+      // the A operands of this wave row (512 / kMR columns of each x row; for
+      // 64-row tiles, of the even row of a pair: 16 columns)
 #pragma unroll
       for (int mb = 0; mb < kMB; mb++)
         xa[mb] = __builtin_bit_cast(
-            u4v, __builtin_amdgcn_raw_buffer_load_b128(xrs, xoff + mb * xblk + r * 64u, 0, 0));
+            u4v, __builtin_amdgcn_raw_buffer_load_b128(xrs, xoff + mb * xblk + r * kRowXBytes,
+                                                       0, 0));
     }
     const int nv = kTail ? max(0, min<int>(W, (int)n_lane - (int)(r * kRowSym + sub * W))) : W;
 #pragma unroll
@@ -595,12 +615,40 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
             uint2, __builtin_amdgcn_raw_buffer_load_b64(c.rr, (r + kRawRows) * kRawRowBytes + raw_v,
                                                         0, 0));
       }
+      if constexpr (kMfma && kMR == 64) {
+        if constexpr (j < kGroupsPerRow) {
+#pragma unroll
+          for (int d = 0; d < 4; d++) prev[d] = ow[d];  // the even row waits for its pair
+        } else {
+          uint32_t b0[4], b1[4];
+#pragma unroll
+          for (int d = 0; d < 4; d++) {
+            const auto sw = __builtin_amdgcn_permlane32_swap(prev[d], ow[d], false, false);
+            b0[d] = sw[0];  // W rows 0..31: lanes 0..31 row r, lanes 32..63 row r + 1
+            b1[d] = sw[1];  // W rows 32..63
+          }
+          const bf8 B0 = __builtin_bit_cast(bf8, u4v{b0[0], b0[1], b0[2], b0[3]});
+          const bf8 B1 = __builtin_bit_cast(bf8, u4v{b1[0], b1[1], b1[2], b1[3]});
+#pragma unroll
+          for (int mb = 0; mb < kMB; mb++) {
+            const bf8 A = __builtin_bit_cast(bf8, xa[mb]);
+            macc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, B0, macc[mb][0], 0, 0, 0);
+            macc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, B1, macc[mb][1], 0, 0, 0);
+          }
+        }
+        return;
+      }
       if constexpr (kMfma) {
         const bf8 b = __builtin_bit_cast(bf8, u4v{ow[0], ow[1], ow[2], ow[3]});
 #pragma unroll
-        for (int mb = 0; mb < kMB; mb++)
-          macc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, xa[mb]), b,
-                                                             macc[mb], 0, 0, 0);
+        for (int mb = 0; mb < kMB; mb++) {
+          if constexpr (kMR == 16)
+            macc[mb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, xa[mb]),
+                                                                  b, macc[mb][0], 0, 0, 0);
+          else
+            macc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf8, xa[mb]),
+                                                                  b, macc[mb][0], 0, 0, 0);
+        }
         return;
       }
       if constexpr (kGemv) {
@@ -672,17 +720,22 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
     for (int m = 0; m < kM; m++) unsafeAtomicAdd(y + uint64_t(m) * N + n, acc[m]);
   }
   if constexpr (kMfma) {
-    // D[4 (sub div 16) + i][sub mod 16] of every x block: y row, W row = y column
-    const uint32_t n = (chunk0 / T.ntc) * 16u + (sub & 15u);
-    const uint64_t N = uint64_t(T.n_chunks / T.ntc) * 16u;
+    // D[row][sub mod kMM] of every x block and W block: y row, W row = y column
+    const uint64_t N = uint64_t(T.n_chunks / T.ntc) * kMR;
     float* y = reinterpret_cast<float*>(T.dst);
 #pragma unroll
-    for (int mb = 0; mb < kMB; mb++)
+    for (int nb = 0; nb < kNB; nb++) {
+      const uint32_t n = (chunk0 / T.ntc) * kMR + nb * kMM + (sub % kMM);
 #pragma unroll
-      for (int i = 0; i < 4; i++) {
-        const uint32_t m = mb * 16u + 4u * (sub >> 4) + i;
-        if (m < a.m) unsafeAtomicAdd(y + uint64_t(m) * N + n, macc[mb][i]);
-      }
+      for (int mb = 0; mb < kMB; mb++)
+#pragma unroll
+        for (int i = 0; i < kMM * kMM / 64; i++) {
+          const uint32_t row = kMM == 16 ? 4u * (sub >> 4) + i
+                                         : 8u * (i >> 2) + 4u * (sub >> 5) + (i & 3);
+          const uint32_t m = mb * kMM + row;
+          if (m < a.m) unsafeAtomicAdd(y + uint64_t(m) * N + n, macc[mb][nb][i]);
+        }
+    }
   }
 
   // --- end-of-chunk checks: every lane back at 2^16, every word consumed ----
@@ -740,8 +793,8 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
 // The fused decode-GEMM of up to kMaxLaunchTensors tensors in one launch: one
 // wave per tile, y += x * W^T for each tensor's own x and y.  kM > 0: column-
 // block tiles of 64 x tile_c bf16, kM rows of x, dot products on the VALU;
-// kMB > 0: column-block tiles of 16 x tile_c, up to 16 kMB rows of x, MFMA.
-template <int kM, int kMB>
+// kMB > 0: column-block tiles of kMR x tile_c, up to kMR kMB rows of x, MFMA.
+template <int kM, int kMB, int kMR = 16>
 __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   __shared__ uint2 tab[wc::kTableSize];
   __shared__ uint32_t cum[260];
@@ -759,7 +812,7 @@ __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   build_table(a, T, tab, cum, tid);
   __syncthreads();
   if (chunk >= T.n_chunks) return;
-  decode_chunks<2, 64, true, kM, kMB>(a, T, chunk, lane, tab, ring[wave], pre);
+  decode_chunks<2, 64, true, kM, kMB, kMR>(a, T, chunk, lane, tab, ring[wave], pre);
 }
 
 }  // namespace
@@ -845,6 +898,10 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
   return WC_OK;
 }
 
+// Rows of x up to which 64-row tiles take the VALU dot products; above, the
+// matrix cores (row pairs swapped into 32 x 32 x 16 MFMA operands).
+constexpr uint32_t kDotRows = 5;
+
 extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n,
                              const uint32_t* tensors, const void* const* dev_x, uint32_t m,
                              float* const* dev_y, void* stream, int32_t* dev_err) {
@@ -859,17 +916,19 @@ extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t
       return WC_EINVAL;
     const wc::TensorInfo& T = P.tensors[tensors[i]];
     if (T.dtype != WC_BF16 || T.lanes != 64 || T.tile_order != WC_TILE_COLUMN_BLOCKS ||
-        !(T.tile_r == 64 || T.tile_r == 16))
+        !(T.tile_r == 64 || T.tile_r == 32 || T.tile_r == 16))
       return WC_EUNSUPPORTED;
-    if (T.tile_r == 64 && m > 8) return WC_EUNSUPPORTED;  // dot-product path: m <= 8
+    // 64-row tiles past the dot-product rows pair k-blocks r and r+1 of one
+    // tile: at least two k-blocks (16 columns) per tile
+    if (T.tile_r == 64 && m > kDotRows && T.tile_c < 16) return WC_EUNSUPPORTED;
     if (T.rows > 0xFFFFFFFFull || T.cols > 0xFFFFFFFFull) return WC_EUNSUPPORTED;
     // x offsets of a lane reach 64 rows (4 blocks of 16) of 2 * cols bytes
     if (64ull * T.cols * 2 > 0x7FFFFFFFull) return WC_EUNSUPPORTED;
   }
   const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  // one launch for the jobs of each path: 64-row tiles (VALU dot products)
-  // and 16-row tiles (MFMA)
-  for (uint32_t rows : {64u, 16u}) {
+  // one launch for the jobs of each tile height: 64 rows (VALU dot products up
+  // to kDotRows rows of x, MFMA above), 32 or 16 rows (MFMA)
+  for (uint32_t rows : {64u, 32u, 16u}) {
     LaunchArgs args{};
     fill_common(args, P, dev_blob, dev_err);
     uint32_t wgs = 0, nt = 0;
@@ -885,23 +944,27 @@ extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t
     args.n_tensors = nt;
     args.m = m;
     const dim3 grid(wgs), block(kThreads);
-    if (rows == 64) {
+    if (rows == 64 && m > kDotRows) {
+      if (m <= 32) hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 64>), grid, block, 0, st, args);
+      else hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 64>), grid, block, 0, st, args);
+    } else if (rows == 64) {
       switch (m) {
         case 1: hipLaunchKernelGGL((wc_gemv_kernel<1, 0>), grid, block, 0, st, args); break;
         case 2: hipLaunchKernelGGL((wc_gemv_kernel<2, 0>), grid, block, 0, st, args); break;
         case 3: hipLaunchKernelGGL((wc_gemv_kernel<3, 0>), grid, block, 0, st, args); break;
         case 4: hipLaunchKernelGGL((wc_gemv_kernel<4, 0>), grid, block, 0, st, args); break;
-        case 5: hipLaunchKernelGGL((wc_gemv_kernel<5, 0>), grid, block, 0, st, args); break;
-        case 6: hipLaunchKernelGGL((wc_gemv_kernel<6, 0>), grid, block, 0, st, args); break;
-        case 7: hipLaunchKernelGGL((wc_gemv_kernel<7, 0>), grid, block, 0, st, args); break;
-        default: hipLaunchKernelGGL((wc_gemv_kernel<8, 0>), grid, block, 0, st, args); break;
+        default: hipLaunchKernelGGL((wc_gemv_kernel<5, 0>), grid, block, 0, st, args); break;
       }
+      static_assert(kDotRows == 5, "one dot-product instance per row count up to kDotRows");
+    } else if (rows == 32) {
+      if (m <= 32) hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 32>), grid, block, 0, st, args);
+      else hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 32>), grid, block, 0, st, args);
     } else {
       switch ((m + 15) / 16) {
-        case 1: hipLaunchKernelGGL((wc_gemv_kernel<0, 1>), grid, block, 0, st, args); break;
-        case 2: hipLaunchKernelGGL((wc_gemv_kernel<0, 2>), grid, block, 0, st, args); break;
-        case 3: hipLaunchKernelGGL((wc_gemv_kernel<0, 3>), grid, block, 0, st, args); break;
-        default: hipLaunchKernelGGL((wc_gemv_kernel<0, 4>), grid, block, 0, st, args); break;
+        case 1: hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 16>), grid, block, 0, st, args); break;
+        case 2: hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 16>), grid, block, 0, st, args); break;
+        case 3: hipLaunchKernelGGL((wc_gemv_kernel<0, 3, 16>), grid, block, 0, st, args); break;
+        default: hipLaunchKernelGGL((wc_gemv_kernel<0, 4, 16>), grid, block, 0, st, args); break;
       }
     }
     if (hipGetLastError() != hipSuccess) return WC_EHIP;

@@ -79,7 +79,7 @@ def test_column_block_tiles_decode_exactly(dev, tile, lanes):
 
 @pytest.mark.parametrize("shape,tile", [((256, 512), (64, 256)), ((192, 1024), (64, 512)),
                                         ((1024, 4096), (64, 512)), ((64, 256), (64, 256))])
-@pytest.mark.parametrize("m", [1, 3, 8])
+@pytest.mark.parametrize("m", [1, 3, 5, 6, 8])
 def test_gemv_matches_the_reference(dev, shape, tile, m):
     say("gemv", shape, tile, m)
     rng = np.random.default_rng(shape[0] + m)
@@ -157,8 +157,11 @@ def test_gemv_many_jobs_in_one_launch(dev, m):
 # --- 16-row column-block tiles: the product on the matrix cores --------------
 
 @pytest.mark.parametrize("shape,tile", [((256, 512), (16, 256)), ((192, 1024), (16, 512)),
-                                        ((1024, 4096), (16, 2048)), ((16, 256), (16, 256))])
-@pytest.mark.parametrize("m", [1, 3, 16, 17, 40, 64])
+                                        ((1024, 4096), (16, 2048)), ((16, 256), (16, 256)),
+                                        ((256, 512), (32, 256)), ((192, 1024), (32, 1024)),
+                                        ((32, 128), (32, 128)), ((256, 512), (64, 256)),
+                                        ((192, 1024), (64, 512)), ((64, 128), (64, 16))])
+@pytest.mark.parametrize("m", [1, 3, 16, 17, 33, 64])
 def test_mfma_gemm_matches_the_reference(dev, shape, tile, m):
     say("mfma gemm", shape, tile, m)
     rng = np.random.default_rng(shape[0] + 7 * m)
@@ -169,24 +172,28 @@ def test_mfma_gemm_matches_the_reference(dev, shape, tile, m):
     _check(y, w, x)
 
 
-def test_mfma_gemm_small_integers_exact(dev):
+@pytest.mark.parametrize("rows", [16, 32, 64])
+@pytest.mark.parametrize("m", [5, 6, 37])
+def test_mfma_gemm_small_integers_exact(dev, rows, m):
     """Small-integer x and W (exact in bf16, sums exact in fp32): y must equal
-    the oracle's product exactly, which pins the operand and output layouts."""
+    the oracle's product exactly, which pins the operand and output layouts
+    (64-row tiles: the VALU dot products at m = 5, the matrix cores above)."""
     rng = np.random.default_rng(41)
-    shape, m = (64, 512), 37
+    shape = (64, 512)
     w = _bf16(rng.integers(-4, 5, shape).astype(np.float32))
     x = _bf16(rng.integers(-3, 4, (m, shape[1])).astype(np.float32))
-    blob = wc.encode([("bf16", w, shape)], tile=(16, 256), tile_order=1)
+    blob = wc.encode([("bf16", w, shape)], tile=(rows, 256), tile_order=1)
     y = _run_gemv(blob, dev, 0, x)
     ref, _ = oracle.gemv_bf16(w, x)
     assert np.array_equal(y, ref)
 
 
-def test_mfma_gemm_full_size_layer(dev):
-    """All seven projections of a Llama-3-70B layer (numpy draw) in 16 x 2048
+@pytest.mark.parametrize("tile", [(16, 2048), (32, 1024), (64, 512)])
+def test_mfma_gemm_full_size_layer(dev, tile):
+    """All seven projections of a Llama-3-70B layer (numpy draw) in 64 KiB
     tiles, one launch, 64 rows of x: every y within the fp32 bound."""
     ts = synth.config(5)
-    blob = wc.encode([(t.dtype, t.data, t.shape) for t in ts], tile=(16, 2048), tile_order=1)
+    blob = wc.encode([(t.dtype, t.data, t.shape) for t in ts], tile=tile, tile_order=1)
     d = wc.to_device(blob, dev)
     rng = np.random.default_rng(42)
     xbits = {}
@@ -207,15 +214,22 @@ def test_mfma_gemm_full_size_layer(dev):
 
 
 def test_gemv_row_limits(dev):
-    """64-row tiles take up to 8 rows of x, 16-row tiles up to 64."""
+    """Up to 64 rows of x on every tile height (64-row tiles take the VALU dot
+    products up to 5 rows, the matrix cores above); 65 rows are refused, and
+    64-row tiles narrower than 16 columns take at most 5."""
     rng = np.random.default_rng(43)
     w = _bf16(rng.normal(0, 0.02, (128, 512)))
     b64 = wc.encode([("bf16", w, (128, 512))], tile=(64, 256), tile_order=1)
     b16 = wc.encode([("bf16", w, (128, 512))], tile=(16, 256), tile_order=1)
-    x8, x9 = (_bf16(rng.normal(0, 1.0, (m, 512))) for m in (8, 9))
-    _check(_run_gemv(b64, dev, 0, x8), w, x8)
-    _check(_run_gemv(b16, dev, 0, x9), w, x9)
+    narrow = wc.encode([("bf16", w, (128, 512))], tile=(64, 8), tile_order=1)
+    x5, x6, x64 = (_bf16(rng.normal(0, 1.0, (m, 512))) for m in (5, 6, 64))
+    _check(_run_gemv(b64, dev, 0, x5), w, x5)
+    _check(_run_gemv(b64, dev, 0, x6), w, x6)
+    _check(_run_gemv(b64, dev, 0, x64), w, x64)
+    _check(_run_gemv(b16, dev, 0, x6), w, x6)
+    _check(_run_gemv(narrow, dev, 0, x5), w, x5)
     with pytest.raises(wc.WcError):
-        _run_gemv(b64, dev, 0, x9)
-    with pytest.raises(wc.WcError):
-        _run_gemv(b16, dev, 0, _bf16(rng.normal(0, 1.0, (65, 512))))
+        _run_gemv(narrow, dev, 0, x6)
+    for b in (b64, b16):
+        with pytest.raises(wc.WcError):
+            _run_gemv(b, dev, 0, _bf16(rng.normal(0, 1.0, (65, 512))))

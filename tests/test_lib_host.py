@@ -172,8 +172,9 @@ def test_gemv_rejects_before_any_launch():
         with pytest.raises(wc.WcError) as e:
             wc.gemv(good, 16, [0], [16], m, [16])
         assert e.value.rc == -1
-    with pytest.raises(wc.WcError) as e:          # 64-row tiles: dot products, m <= 8
-        wc.gemv(good, 16, [0], [16], 9, [16])
+    narrow = wc.encode([("bf16", w, (128, 512))], tile=(64, 8), tile_order=1)
+    with pytest.raises(wc.WcError) as e:          # 64-row tiles past 5 rows pair k-blocks
+        wc.gemv(narrow, 16, [0], [16], 6, [16])
     assert e.value.rc == -5
     for args in (([0], [8], [16]),            # x not 16-byte aligned
                  ([1], [16], [16]),           # no such tensor
