@@ -47,6 +47,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "decompressed GB/s on one MI355X (% of HBM roofline); ratio vs Shannon bound"
 HBM_PEAK_GBPS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
 WORKLOAD_DEFAULT = "llama3-70b-layer-bf16"
 # workload name -> seeded recipe number in paper_2606_15789_amd.synth.config
 WORKLOADS = {WORKLOAD_DEFAULT: 5, "bf16-matrix-4096": 1, "llama3-8b-layer-bf16": 2,
@@ -168,7 +169,7 @@ def main() -> int:
                     help="time the device encoder (wc_encode_device) on the resident 70B "
                          "layer instead of the decode")
     ap.add_argument("--gemv", type=int, default=0, metavar="M",
-                    help="time the fused decode-GEMM y += x W^T (x: M rows, 1..64) over the "
+                    help="time the fused decode-GEMM y += x W^T (x: M rows, 1..4096) over the "
                          "70B layer instead of the decode, next to the same product unfused "
                          "(wc_decode, then torch.matmul) and uncompressed (torch.matmul)")
     ap.add_argument("--gemv-rows", type=int, choices=[64, 32, 16], default=0,
@@ -410,8 +411,9 @@ def gemv_bench(args, dev) -> int:
     from paper_2606_15789_amd import synth, wc
     M = args.gemv
     rows = args.gemv_rows or (16 if M <= 16 else 64)
-    if not 1 <= M <= 64:
-        print("--gemv takes 1..64 rows of activations", file=sys.stderr)
+    if not 1 <= M <= (4096 if rows == 64 else 64):
+        print("--gemv takes 1..4096 rows of activations on 64-row tiles, 1..64 on 32- or "
+              "16-row tiles", file=sys.stderr)
         return 2
     # 64 KiB tiles: 64 x 512 (a lane per W row, VALU dot products), 32 x 1024 or
     # 16 x 2048 (a wave row per MFMA operand)
@@ -432,10 +434,16 @@ def gemv_bench(args, dev) -> int:
     err = torch.zeros(1, dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream(dev)
 
+    # wc_gemm: wc_gemv up to 64 rows; above, x is packed into the workspace
+    # (inside every timed call) and the weights are decoded once per 256 rows
+    need = wc.gemm_workspace_bytes(blob, list(range(len(W))), [x.data_ptr() for x in xs], M)
+    ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
+
     def fused():
-        # one launch for the seven projections
-        wc.gemv(blob, dblob.data_ptr(), list(range(len(W))), [x.data_ptr() for x in xs], M,
-                [y.data_ptr() for y in ys], stream.cuda_stream, err.data_ptr())
+        # one launch per tile height for the seven projections (plus the x packing)
+        wc.gemm(blob, dblob.data_ptr(), list(range(len(W))), [x.data_ptr() for x in xs], M,
+                [y.data_ptr() for y in ys], ws.data_ptr(), ws.numel(), stream.cuda_stream,
+                err.data_ptr())
 
     # correctness: y against torch's fp32 product of the same bf16 values,
     # within the fp32 summation bound K * 2^-23 * sum |x w|
@@ -485,6 +493,11 @@ def gemv_bench(args, dev) -> int:
     wbytes = sum(blob.out_bytes)
     alg = blob.size + sum(x.numel() * 2 for x in xs) + sum(2 * y.numel() * 4 for y in ys)
     achieved = alg / s_fused / 1e9
+    flops = sum(2.0 * M * shp[0] * shp[1] for shp in shapes)
+    tflops = flops / s_fused / 1e12
+    shared = rows == 64 and M > 64
+    # the bound: HBM below the ridge point (peak flops / peak bytes), MFMA above
+    mfma_bound = flops / alg > MFMA_BF16_PEAK_TFLOPS * 1e12 / (HBM_PEAK_GBPS * 1e9)
     line = {
         "metric": METRIC + " [fused decode-GEMM]",
         "value": round(wbytes / s_fused / 1e9, 2),
@@ -500,15 +513,25 @@ def gemv_bench(args, dev) -> int:
         "data": "synthetic",
         "config": {"workload": "llama3-70b-layer-bf16", "mode": "fused-gemv", "m": M,
                    "tile": f"{tile[0]}x{tile[1]}", "tile_order": "column-blocks",
-                   "product": ("v_dot2_f32_bf16" if rows == 64 and M <= 8 else
+                   "product": ("v_dot2_f32_bf16" if rows == 64 and M <= 5 else
                                "v_mfma_f32_16x16x32_bf16" if rows == 16 else
                                "v_mfma_f32_32x32x16_bf16"),
+                   "decoded_once_per": ("256 rows of x (operands shared through LDS)"
+                                        if shared else "call"),
                    "lanes": 64, "weight_bytes_per_step": wbytes,
                    "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
-                     "kernel": "wc_gemv_kernel", "mean_step_us": round(s_fused * 1e6, 2),
-                     "algorithmic_bytes_per_step": int(alg)},
+        "roofline": ({"bound": "mfma", "achieved": round(tflops, 1),
+                      "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                      "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None}
+                     if mfma_bound else
+                     {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                      "traffic": None})
+                    | {"kernel": "wc_gemm_kernel" if shared else "wc_gemv_kernel",
+                       "mean_step_us": round(s_fused * 1e6, 2),
+                       "algorithmic_bytes_per_step": int(alg), "flops_per_step": flops,
+                       "hbm_frac": round(achieved / HBM_PEAK_GBPS, 4),
+                       "mfma_frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4)},
         "unfused": {"value": round(wbytes / s_unfused / 1e9, 2), "unit": "GB/s",
                     "ms_per_step": round(s_unfused * 1e3, 4),
                     "what": "wc_decode of the layer (64 KiB byte-run chunks) into memory, then "

@@ -231,6 +231,35 @@ wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n, const u
                   const void* const* dev_x, uint32_t m, float* const* dev_y, void* stream,
                   int32_t* dev_err);
 
+/* wc_gemm_workspace_bytes -- device workspace wc_gemm needs for these jobs
+ * (host only, nothing launched): 0 for m <= 64; above, one packed copy of
+ * each distinct x (jobs whose dev_x pointers and K are equal share it) of
+ * ceil(m / 32) * 32 * K * 2 bytes, each rounded up to 256 bytes.  dev_x is
+ * compared as pointers, never read.  Returns WC_EINVAL for a bad argument. */
+wc_status wc_gemm_workspace_bytes(const wc_blob* desc, uint32_t n, const uint32_t* tensors,
+                                  const void* const* dev_x, uint32_t m, uint64_t* bytes);
+
+/* wc_gemm -- the fused decode-GEMM of wc_gemv for any batch: m = 1..4096 rows
+ * of x (Alg. 1 / 3; Sec. V, the batch-size regime).  Up to m = 64 it is
+ * wc_gemv (the workspace is not used).  Above, the weights are decoded once
+ * per pass of 256 x rows: the 8 waves of a workgroup decode 8 consecutive
+ * tiles of one band of 64 W rows, exchange each pair of decoded wave rows
+ * (64 W rows x 16 columns, two v_mfma_f32_32x32x16_bf16 B operands) through
+ * LDS, and each wave multiplies all of them by its own 32 rows of x.  x is
+ * first packed into the workspace in MFMA operand order (one kernel per
+ * distinct x, on the same stream).  Jobs, arguments and y as for wc_gemv;
+ * above m = 64 every tensor must have 64-row tiles of at least 16 columns
+ * with rows % 64 == 0 and cols % tile_cols == 0 (full tiles).
+ *   dev_workspace  device memory of at least wc_gemm_workspace_bytes bytes,
+ *                  256-byte aligned, owned by the caller; overwritten; calls
+ *                  sharing a workspace must not overlap in time.
+ * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument, or a
+ * workspace too small or misaligned) or WC_EUNSUPPORTED (a tensor the path
+ * does not take). */
+wc_status wc_gemm(const wc_blob* desc, const void* dev_blob, uint32_t n, const uint32_t* tensors,
+                  const void* const* dev_x, uint32_t m, float* const* dev_y, void* dev_workspace,
+                  uint64_t workspace_bytes, void* stream, int32_t* dev_err);
+
 /* A tensor in device memory, for the device-side analysis and encoder: the
  * fields of wc_tensor, with dev_ptr a device pointer that must be 16-byte
  * aligned (any torch or hipMalloc allocation is). */
@@ -292,7 +321,7 @@ wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_params* p, 
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);
 
-/* wc_version -- ABI version of this header (3). */
+/* wc_version -- ABI version of this header (4). */
 int32_t wc_version(void);
 
 #ifdef __cplusplus

@@ -37,6 +37,7 @@
 // No MFMA: the work is integer table decoding, not a contraction.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <utility>
 
 #include "wc_internal.h"
@@ -439,6 +440,135 @@ __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ 
 // (wave-uniform) loads, and adds them to y once per tile (fp32 atomics: the
 // tiles of one row band split K).
 //
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+
+// The shared fused GEMM, for many rows of x on column-block tiles of 64 rows:
+// the waves of a workgroup decode up to kWaves consecutive tiles of one band
+// of 64 W rows (one tile each), so every weight is decoded once per pass over
+// the rows of x.  After each pair of wave rows a decoding wave leaves its two
+// v_mfma_f32_32x32x16_bf16 B operands (64 W rows x 16 columns) in LDS, and
+// every wave multiplies all of them by its own kXB blocks of 32 x rows.
+struct Share {
+  u32x4* frag;     // LDS [kWaves][2][64]: each wave's B operands of the current pair
+  uint32_t wave;   // this wave's slot
+  uint32_t n_act;  // waves of the workgroup that decode a tile (operands per pair)
+  uint32_t xoff;   // this lane's byte offset in packed x: tile 0, pair 0, x block 0
+  uint32_t xtile;  // packed x bytes between two consecutive tiles
+  uint32_t xblk;   // packed x bytes between blocks of 32 rows
+  uint32_t mrows;  // rows of x from this wave's first (0: none)
+  uint32_t first;  // this wave's first row of x (and of y)
+  uint32_t n0;     // first W row of the band (column of y)
+  uint32_t pairs;  // pairs of wave rows per tile
+  uint64_t N;      // columns of y (rows of W)
+};
+
+// LDS writes of every wave before the barrier are seen by every wave after it;
+// global loads in flight stay in flight.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Packed x: the A operands of v_mfma_f32_32x32x16_bf16 in the order the shared
+// GEMM reads them.  Unit (b, p, l) (16 bytes, at ((b K/16 + p) 64 + l) 16) holds
+// x row 32 b + l mod 32, columns 16 p + 8 (l div 32) .. + 8, zero past row M, so
+// the operand of one block of 32 rows and one pair of wave rows is 1 KiB in a
+// row: one fully used load per lane.
+__global__ __launch_bounds__(256) void pack_x_kernel(const uint16_t* __restrict__ x, uint32_t m,
+                                                    uint32_t K, u32x4* __restrict__ xp,
+                                                    uint64_t units) {
+  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, m * K * 2u);
+  const uint32_t pairs = K / 16u;
+  for (uint64_t u = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; u < units;
+       u += uint64_t(gridDim.x) * blockDim.x) {
+    const uint32_t l = uint32_t(u & 63u);
+    const uint64_t bp = u >> 6;
+    const uint32_t p = uint32_t(bp % pairs), b = uint32_t(bp / pairs);
+    const uint32_t row = 32u * b + (l & 31u), col = 16u * p + 8u * (l >> 5);
+    xp[u] = __builtin_bit_cast(
+        u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, (row * K + col) * 2u, 0, 0));
+  }
+}
+
+// A operands of one pair for every decoding wave's tile, from packed x: lane l
+// holds x row (first + l mod 32), columns 16 pair + 8 (l div 32) .. of the
+// tile; absent tiles and x blocks load nothing.
+template <int kXB>
+__device__ __forceinline__ void share_load_x(const Share& s, __amdgpu_buffer_rsrc_t xrs,
+                                             uint32_t pair, u32x4 (&xs)[kWaves][kXB]) {
+#pragma unroll
+  for (int f = 0; f < kWaves; f++)
+#pragma unroll
+    for (int xb = 0; xb < kXB; xb++) {
+      const bool use = uint32_t(f) < s.n_act && 32u * xb < s.mrows;
+      const uint32_t off = use ? s.xoff + f * s.xtile + xb * s.xblk + pair * 1024u : kFarOffset;
+      xs[f][xb] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xrs, off, 0, 0));
+    }
+}
+
+// acc[xb][nb] += x block xb times W rows 32 nb .. 32 nb + 31 of every tile's pair
+template <int kXB>
+__device__ __forceinline__ void share_mma(const Share& s, uint32_t lane,
+                                          const u32x4 (&xs)[kWaves][kXB],
+                                          f32x16 (&acc)[kXB][2]) {
+#pragma unroll
+  for (int f = 0; f < kWaves; f++) {
+    if (uint32_t(f) >= s.n_act) break;
+    const bf16x8 b0 = __builtin_bit_cast(bf16x8, s.frag[(2 * f) * 64 + lane]);
+    const bf16x8 b1 = __builtin_bit_cast(bf16x8, s.frag[(2 * f + 1) * 64 + lane]);
+#pragma unroll
+    for (int xb = 0; xb < kXB; xb++) {
+      if (32u * xb >= s.mrows) break;
+      const bf16x8 A = __builtin_bit_cast(bf16x8, xs[f][xb]);
+      acc[xb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, b0, acc[xb][0], 0, 0, 0);
+      acc[xb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, b1, acc[xb][1], 0, 0, 0);
+    }
+  }
+}
+
+// y[first + row][n0 + 32 nb + l mod 32] += acc: lane l holds rows
+// 8 (i div 4) + 4 (l div 32) + i mod 4 of each 32 x 32 block
+template <int kXB>
+__device__ __forceinline__ void share_store(const Share& s, uint32_t lane,
+                                            const f32x16 (&acc)[kXB][2], float* y) {
+#pragma unroll
+  for (int xb = 0; xb < kXB; xb++)
+#pragma unroll
+    for (int nb = 0; nb < 2; nb++)
+#pragma unroll
+      for (int i = 0; i < 16; i++) {
+        const uint32_t row = 32u * xb + 8u * (i >> 2) + 4u * (lane >> 5) + (i & 3);
+        if (row < s.mrows)
+          unsafeAtomicAdd(y + uint64_t(s.first + row) * s.N + s.n0 + 32u * nb + (lane & 31u),
+                          acc[xb][nb][i]);
+      }
+}
+
+// A wave of the workgroup with no tile to decode (or whose tile's index entry
+// is bad): it takes part in every pair's barriers and multiplies the decoding
+// waves' operands by its own rows of x.
+template <int kXB>
+__device__ void share_idle_wave(const LaunchArgs& a, const DevTensor& T, const Share& s,
+                                uint32_t lane) {
+  const uint32_t K = T.ntc << T.log_tc;
+  const __amdgpu_buffer_rsrc_t xrs =
+      make_rsrc(reinterpret_cast<const void*>(T.x), ((a.m + 31u) & ~31u) * K * 2u);
+  f32x16 acc[kXB][2];
+#pragma unroll
+  for (int xb = 0; xb < kXB; xb++) acc[xb][0] = acc[xb][1] = f32x16{};
+  u32x4 xs[kWaves][kXB];
+  for (uint32_t p = 0; p < s.pairs; p++) {
+    share_load_x<kXB>(s, xrs, p, xs);
+    lds_barrier();
+    share_mma<kXB>(s, lane, xs, acc);
+    lds_barrier();
+  }
+  share_store<kXB>(s, lane, acc, reinterpret_cast<float*>(T.dst));
+}
+
 // kMB: the fused GEMM on the matrix cores, for up to kMR kMB rows of x.  It
 // needs column-block tiles of kMR (16 or 32) rows decoded by 64 lanes: lane l
 // then holds, in every wave row r, the 8 weights of tile row l mod kMR at
@@ -459,13 +589,14 @@ __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ 
 // B operands of v_mfma_f32_32x32x16_bf16 (rows 0..31 and 32..63: lanes 0..31
 // keep row r, lanes 32..63 take row r + 1 of the same W rows), which share
 // one A operand of x, so every x value loaded feeds 64 W rows.
-template <int G, int L, bool kTiled, int kM = 0, int kMB = 0, int kMR = 16>
+template <int G, int L, bool kTiled, int kM = 0, int kMB = 0, int kMR = 16, bool kShare = false>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
                                               const uint2* __restrict__ tab, uint32_t* ring,
-                                              const IndexPre& pre) {
+                                              const IndexPre& pre, const Share* sh = nullptr) {
   constexpr bool kGemv = kM > 0;   // fused GEMM with kM rows of x, dot products
-  constexpr bool kMfma = kMB > 0;  // fused GEMM with kMB blocks of 16 rows of x, MFMA
+  constexpr bool kMfma = kMB > 0;  // fused GEMM with kMB blocks of x rows, MFMA
+  static_assert(!kShare || (kMfma && kMR == 64), "shared fused GEMM: 64-row tiles");
   static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
   static_assert(!kMfma || (G == 2 && L == 64 && kTiled && !kGemv), "MFMA GEMM: bf16 tiles");
   static_assert(kMR == 16 || kMR == 32 || kMR == 64, "MFMA tiles of 16, 32 or 64 rows");
@@ -487,6 +618,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   Chain<L> c = open_chain<L>(a, T, chunk0, W, lane, ring, pre);
   if (!c.ok) {
     if (lane == 0) report(a, WC_DERR_INDEX);
+    if constexpr (kShare) share_idle_wave<kMB>(a, T, *sh, lane);
     return;
   }
   const uint32_t h = kH == 2 ? lane / L : 0u;
@@ -556,15 +688,22 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   typedef __attribute__((ext_vector_type(kMM * kMM / 64))) float facc;
   typedef __attribute__((ext_vector_type(4))) unsigned int u4v;
   constexpr uint32_t kRowXBytes = 1024u / kMR;  // bytes of an x row one wave row covers
-  facc macc[kMfma ? kMB : 1][kNB];
+  facc macc[kMfma && !kShare ? kMB : 1][kNB];
+  f32x16 sacc[kShare ? kMB : 1][2];        // shared GEMM: this wave's x blocks x 64 W rows
+  u32x4 xs[kShare ? kWaves : 1][kShare ? kMB : 1];  // shared GEMM: A operands of the pair
   uint32_t prev[kMR == 64 ? 4 : 1];             // 64-row tiles: the even row's dwords
   u4v xa[kMfma ? kMB : 1];
   // the x rows (fused GEMM on the matrix cores): a.m rows of K bf16
   const uint32_t K = T.ntc << T.log_tc;  // columns of W = length of an x row
-  const __amdgpu_buffer_rsrc_t xrs =
-      make_rsrc(reinterpret_cast<const void*>(T.x), kMfma ? a.m * K * 2u : 0u);
+  // (the shared GEMM reads packed x: rows rounded up to blocks of 32)
+  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(
+      reinterpret_cast<const void*>(T.x),
+      kShare ? ((a.m + 31u) & ~31u) * K * 2u : (kMfma ? a.m * K * 2u : 0u));
   uint32_t xoff = 0, xblk = 0;
-  if constexpr (kMfma) {
+  if constexpr (kShare) {
+#pragma unroll
+    for (int xb = 0; xb < kMB; xb++) sacc[xb][0] = sacc[xb][1] = f32x16{};
+  } else if constexpr (kMfma) {
 #pragma unroll
     for (int mb = 0; mb < kMB; mb++)
 #pragma unroll
@@ -587,7 +726,11 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
     }
     __builtin_amdgcn_wave_barrier();
     const uint32_t r = g / kGroupsPerRow;
-    if constexpr (kMfma && j % kGroupsPerRow == 0 && (kMR != 64 || j < kGroupsPerRow)) {
+    if constexpr (kShare) {
+      if constexpr (j == 0) share_load_x<kMB>(*sh, xrs, r >> 1, xs);
+    }
+    if constexpr (kMfma && !kShare && j % kGroupsPerRow == 0 &&
+                  (kMR != 64 || j < kGroupsPerRow)) {
       // the A operands of this wave row (512 / kMR columns of each x row; for
       // 64-row tiles, of the even row of a pair: 16 columns)
 #pragma unroll
@@ -626,6 +769,16 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
             const auto sw = __builtin_amdgcn_permlane32_swap(prev[d], ow[d], false, false);
             b0[d] = sw[0];  // W rows 0..31: lanes 0..31 row r, lanes 32..63 row r + 1
             b1[d] = sw[1];  // W rows 32..63
+          }
+          if constexpr (kShare) {
+            // this wave's operands to every wave of the workgroup, then all of them
+            // times this wave's rows of x; the second barrier frees the slots
+            sh->frag[(2 * sh->wave) * 64 + lane] = u32x4{b0[0], b0[1], b0[2], b0[3]};
+            sh->frag[(2 * sh->wave + 1) * 64 + lane] = u32x4{b1[0], b1[1], b1[2], b1[3]};
+            lds_barrier();
+            share_mma<kMB>(*sh, lane, xs, sacc);
+            lds_barrier();
+            return;
           }
           const bf8 B0 = __builtin_bit_cast(bf8, u4v{b0[0], b0[1], b0[2], b0[3]});
           const bf8 B1 = __builtin_bit_cast(bf8, u4v{b1[0], b1[1], b1[2], b1[3]});
@@ -719,7 +872,8 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
 #pragma unroll
     for (int m = 0; m < kM; m++) unsafeAtomicAdd(y + uint64_t(m) * N + n, acc[m]);
   }
-  if constexpr (kMfma) {
+  if constexpr (kShare) share_store<kMB>(*sh, lane, sacc, reinterpret_cast<float*>(T.dst));
+  if constexpr (kMfma && !kShare) {
     // D[row][sub mod kMM] of every x block and W block: y row, W row = y column
     const uint64_t N = uint64_t(T.n_chunks / T.ntc) * kMR;
     float* y = reinterpret_cast<float*>(T.dst);
@@ -815,6 +969,58 @@ __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   decode_chunks<2, 64, true, kM, kMB, kMR>(a, T, chunk, lane, tab, ring[wave], pre);
 }
 
+// The shared fused GEMM: workgroup = (pass over 256 kXB rows of x, band of 64
+// W rows, segment of kWaves consecutive tiles of the band); wave w decodes tile
+// w of the segment (when the band has one) and owns x rows 32 kXB w .. of the
+// pass.  Every tile must be full: 64 rows, tile_c columns.  DevTensor::x is the
+// packed x of the job (pack_x_kernel).
+template <int kXB>
+__global__ __launch_bounds__(kThreads) void wc_gemm_kernel(LaunchArgs a) {
+  __shared__ uint2 tab[wc::kTableSize];
+  __shared__ uint32_t cum[260];
+  __shared__ uint32_t ring[kWaves][wc_ring_words() / 2];
+  __shared__ u32x4 frag[kWaves * 2 * 64];
+  const uint32_t wg = blockIdx.x;
+  uint32_t ti = 0;
+  for (uint32_t k = 1; k < a.n_tensors; k++)
+    if (wg >= a.t[k].wg0) ti = k;
+  const DevTensor& T = a.t[ti];
+  const uint32_t tid = threadIdx.x;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t lane = __lane_id();
+  const uint32_t bands = T.n_chunks / T.ntc;
+  const uint32_t segs = (T.ntc + kWaves - 1) / kWaves;
+  const uint32_t local = wg - T.wg0;
+  const uint32_t pass = local / (bands * segs), rest = local % (bands * segs);
+  const uint32_t band = rest / segs, seg = rest % segs;
+  Share s;
+  s.frag = frag;
+  s.wave = wave;
+  s.n_act = min<uint32_t>(kWaves, T.ntc - seg * kWaves);
+  const uint32_t K = T.ntc << T.log_tc;
+  s.first = (pass * kWaves + wave) * 32u * kXB;
+  s.mrows = s.first < a.m ? a.m - s.first : 0u;
+  // packed x: 1 KiB per (block of 32 rows, pair of columns 16 p ..)
+  s.xoff = s.mrows ? ((s.first / 32u) * (K / 16u) * 64u + lane) * 16u +
+                         seg * kWaves * ((1u << T.log_tc) / 16u) * 1024u
+                   : 0u;
+  s.xtile = (1u << T.log_tc) * 64u;
+  s.xblk = K * 64u;
+  s.n0 = band * 64u;
+  s.pairs = (1u << T.log_tc) / 16u;
+  s.N = uint64_t(bands) * 64u;
+  // waves past the band's last tile decode nothing; they index a tile that exists
+  const bool decodes = wave < s.n_act;
+  const uint32_t chunk = band * T.ntc + seg * kWaves + (decodes ? wave : 0u);
+  const IndexPre pre = load_index(a, T, chunk, 1u);
+  build_table(a, T, tab, cum, tid);
+  __syncthreads();
+  if (decodes)
+    decode_chunks<2, 64, true, 0, kXB, 64, true>(a, T, chunk, lane, tab, ring[wave], pre, &s);
+  else
+    share_idle_wave<kXB>(a, T, s, lane);
+}
+
 }  // namespace
 
 namespace {
@@ -901,14 +1107,25 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
 // Rows of x up to which 64-row tiles take the VALU dot products; above, the
 // matrix cores (row pairs swapped into 32 x 32 x 16 MFMA operands).
 constexpr uint32_t kDotRows = 5;
+// Rows of x up to which wc_gemm runs wc_gemv's kernels; above, the shared
+// fused GEMM (one decode of every tile per pass of kPassRows x rows) over
+// packed x.  kMaxGemmRows: the most rows of x wc_gemm takes.
+constexpr uint32_t kShareRows = 64;
+constexpr uint32_t kMaxGemmRows = 4096;
+constexpr uint32_t kPassRows = kWaves * 32u;
 
-extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n,
-                             const uint32_t* tensors, const void* const* dev_x, uint32_t m,
-                             float* const* dev_y, void* stream, int32_t* dev_err) {
+namespace {
+
+uint64_t pad256(uint64_t v) { return (v + 255) & ~uint64_t(255); }
+
+// Arguments of a fused GEMM call, before anything is launched.  share: the
+// jobs go to the shared fused GEMM (64-row tiles, every tile full).
+wc_status check_jobs(const wc_blob* desc, const void* dev_blob, uint32_t n,
+                     const uint32_t* tensors, const void* const* dev_x, uint32_t m,
+                     float* const* dev_y, bool share) {
   if (!desc || !desc->priv || !dev_blob || !tensors || !dev_x || !dev_y || n == 0 ||
       n > kMaxLaunchTensors)
     return WC_EINVAL;
-  if (m < 1 || m > 64) return WC_EINVAL;
   const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
   for (uint32_t i = 0; i < n; i++) {
     if (tensors[i] >= desc->n_tensors || !dev_x[i] || !dev_y[i] ||
@@ -924,10 +1141,22 @@ extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t
     if (T.rows > 0xFFFFFFFFull || T.cols > 0xFFFFFFFFull) return WC_EUNSUPPORTED;
     // x offsets of a lane reach 64 rows (4 blocks of 16) of 2 * cols bytes
     if (64ull * T.cols * 2 > 0x7FFFFFFFull) return WC_EUNSUPPORTED;
+    if (share) {
+      // every wave of a workgroup takes the same number of pairs of wave rows:
+      // 64-row tiles, all full; packed x addressed below kFarOffset
+      if (T.tile_r != 64 || T.rows % 64 || T.cols % T.tile_c) return WC_EUNSUPPORTED;
+      if (uint64_t((m + 31) / 32 * 32) * T.cols * 2 > kFarOffset) return WC_EUNSUPPORTED;
+    }
   }
-  const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  // one launch for the jobs of each tile height: 64 rows (VALU dot products up
-  // to kDotRows rows of x, MFMA above), 32 or 16 rows (MFMA)
+  return WC_OK;
+}
+
+// One launch per tile height (64 rows: VALU dot products up to kDotRows rows
+// of x, MFMA above, or the shared GEMM; 32 or 16 rows: MFMA).  xs: the x (or,
+// for the shared GEMM, packed x) of each job.
+wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
+                      const uint32_t* tensors, const uint64_t* xs, uint32_t m,
+                      float* const* dev_y, bool share, hipStream_t st, int32_t* dev_err) {
   for (uint32_t rows : {64u, 32u, 16u}) {
     LaunchArgs args{};
     fill_common(args, P, dev_blob, dev_err);
@@ -936,15 +1165,24 @@ extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t
       const wc::TensorInfo& T = P.tensors[tensors[i]];
       if (T.tile_r != rows) continue;
       fill_tensor(args.t[nt], T, dev_y[i], wgs);
-      args.t[nt].x = reinterpret_cast<uint64_t>(dev_x[i]);
-      wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
+      args.t[nt].x = xs[i];
+      if (share) {
+        // (pass, band, segment of kWaves tiles) per workgroup
+        const uint64_t ntc = T.cols / T.tile_c, bands = T.rows / 64;
+        const uint64_t segs = (ntc + kWaves - 1) / kWaves, passes = (m + kPassRows - 1) / kPassRows;
+        wgs += uint32_t(bands * segs * passes);
+      } else {
+        wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
+      }
       nt++;
     }
     if (!nt) continue;
     args.n_tensors = nt;
     args.m = m;
     const dim3 grid(wgs), block(kThreads);
-    if (rows == 64 && m > kDotRows) {
+    if (share) {
+      hipLaunchKernelGGL((wc_gemm_kernel<1>), grid, block, 0, st, args);
+    } else if (rows == 64 && m > kDotRows) {
       if (m <= 32) hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 64>), grid, block, 0, st, args);
       else hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 64>), grid, block, 0, st, args);
     } else if (rows == 64) {
@@ -970,4 +1208,89 @@ extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t
     if (hipGetLastError() != hipSuccess) return WC_EHIP;
   }
   return WC_OK;
+}
+
+// Packed-x slots of the jobs of a shared GEMM: jobs with the same x (pointer
+// and length) share one slot.  Returns the workspace bytes; slot[i] is job i's
+// byte offset in the workspace.
+uint64_t packed_slots(const wc::BlobPriv& P, uint32_t n, const uint32_t* tensors,
+                      const void* const* dev_x, uint32_t m, uint64_t* slot) {
+  uint64_t total = 0;
+  const uint64_t mpad = (m + 31) / 32 * 32;
+  for (uint32_t i = 0; i < n; i++) {
+    const uint64_t K = P.tensors[tensors[i]].cols;
+    slot[i] = ~uint64_t(0);
+    for (uint32_t j = 0; j < i; j++)
+      if (dev_x[j] == dev_x[i] && P.tensors[tensors[j]].cols == K) slot[i] = slot[j];
+    if (slot[i] == ~uint64_t(0)) {
+      slot[i] = total;
+      total += pad256(mpad * K * 2);
+    }
+  }
+  return total;
+}
+
+}  // namespace
+
+extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n,
+                             const uint32_t* tensors, const void* const* dev_x, uint32_t m,
+                             float* const* dev_y, void* stream, int32_t* dev_err) {
+  if (m < 1 || m > 64) return WC_EINVAL;
+  const wc_status rc = check_jobs(desc, dev_blob, n, tensors, dev_x, m, dev_y, false);
+  if (rc != WC_OK) return rc;
+  const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
+  uint64_t xs[kMaxLaunchTensors];
+  for (uint32_t i = 0; i < n; i++) xs[i] = reinterpret_cast<uint64_t>(dev_x[i]);
+  return launch_jobs(P, dev_blob, n, tensors, xs, m, dev_y, false,
+                     reinterpret_cast<hipStream_t>(stream), dev_err);
+}
+
+extern "C" wc_status wc_gemm_workspace_bytes(const wc_blob* desc, uint32_t n,
+                                             const uint32_t* tensors, const void* const* dev_x,
+                                             uint32_t m, uint64_t* bytes) {
+  if (!bytes) return WC_EINVAL;
+  *bytes = 0;
+  if (!desc || !desc->priv || !tensors || !dev_x || n == 0 || n > kMaxLaunchTensors ||
+      m < 1 || m > kMaxGemmRows)
+    return WC_EINVAL;
+  for (uint32_t i = 0; i < n; i++)
+    if (tensors[i] >= desc->n_tensors) return WC_EINVAL;
+  if (m <= kShareRows) return WC_OK;
+  const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
+  uint64_t slot[kMaxLaunchTensors];
+  *bytes = packed_slots(P, n, tensors, dev_x, m, slot);
+  return WC_OK;
+}
+
+extern "C" wc_status wc_gemm(const wc_blob* desc, const void* dev_blob, uint32_t n,
+                             const uint32_t* tensors, const void* const* dev_x, uint32_t m,
+                             float* const* dev_y, void* dev_workspace, uint64_t workspace_bytes,
+                             void* stream, int32_t* dev_err) {
+  if (m < 1 || m > kMaxGemmRows) return WC_EINVAL;
+  if (m <= kShareRows) return wc_gemv(desc, dev_blob, n, tensors, dev_x, m, dev_y, stream, dev_err);
+  const wc_status rc = check_jobs(desc, dev_blob, n, tensors, dev_x, m, dev_y, true);
+  if (rc != WC_OK) return rc;
+  const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
+  uint64_t slot[kMaxLaunchTensors];
+  const uint64_t need = packed_slots(P, n, tensors, dev_x, m, slot);
+  if (!dev_workspace || reinterpret_cast<uintptr_t>(dev_workspace) % 256 ||
+      workspace_bytes < need)
+    return WC_EINVAL;
+  const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  uint64_t xs[kMaxLaunchTensors];
+  const uint64_t mpad = (m + 31) / 32 * 32;
+  for (uint32_t i = 0; i < n; i++) {
+    const uint64_t K = P.tensors[tensors[i]].cols;
+    xs[i] = reinterpret_cast<uint64_t>(dev_workspace) + slot[i];
+    bool first = true;
+    for (uint32_t j = 0; j < i; j++) first = first && slot[j] != slot[i];
+    if (!first) continue;
+    const uint64_t units = mpad * K / 8;  // 16-byte units
+    const uint32_t blocks = uint32_t(std::min<uint64_t>((units + 255) / 256, 8192));
+    hipLaunchKernelGGL(pack_x_kernel, dim3(blocks), dim3(256), 0, st,
+                       static_cast<const uint16_t*>(dev_x[i]), m, uint32_t(K),
+                       reinterpret_cast<u32x4*>(xs[i]), units);
+    if (hipGetLastError() != hipSuccess) return WC_EHIP;
+  }
+  return launch_jobs(P, dev_blob, n, tensors, xs, m, dev_y, true, st, dev_err);
 }

@@ -22,7 +22,8 @@ DERR = {1: "WC_DERR_INDEX", 2: "WC_DERR_STATE", 4: "WC_DERR_CURSOR", 8: "WC_DERR
 
 # Every function the header declares; the library must export all of them.
 EXPORTS = ["wc_analyze", "wc_encode", "wc_open", "wc_decode", "wc_gemv", "wc_free",
-           "wc_version", "wc_analyze_device", "wc_encode_device_bounds", "wc_encode_device"]
+           "wc_version", "wc_analyze_device", "wc_encode_device_bounds", "wc_encode_device",
+           "wc_gemm_workspace_bytes", "wc_gemm"]
 
 ANALYZE_WORKSPACE_BYTES = 524288  # WC_ANALYZE_WORKSPACE_BYTES
 
@@ -88,6 +89,14 @@ def lib():
                               C.POINTER(C.c_uint32), C.POINTER(C.c_void_p), C.c_uint32,
                               C.POINTER(C.c_void_p), C.c_void_p, C.c_void_p]
         L.wc_gemv.restype = C.c_int
+        L.wc_gemm_workspace_bytes.argtypes = [C.POINTER(_Blob), C.c_uint32,
+                                              C.POINTER(C.c_uint32), C.POINTER(C.c_void_p),
+                                              C.c_uint32, C.POINTER(C.c_uint64)]
+        L.wc_gemm_workspace_bytes.restype = C.c_int
+        L.wc_gemm.argtypes = [C.POINTER(_Blob), C.c_void_p, C.c_uint32, C.POINTER(C.c_uint32),
+                              C.POINTER(C.c_void_p), C.c_uint32, C.POINTER(C.c_void_p),
+                              C.c_void_p, C.c_uint64, C.c_void_p, C.c_void_p]
+        L.wc_gemm.restype = C.c_int
         L.wc_analyze_device.argtypes = [C.POINTER(_Tensor), C.c_void_p, C.c_uint64, C.c_void_p,
                                         C.POINTER(_Stats)]
         L.wc_analyze_device.restype = C.c_int
@@ -235,6 +244,34 @@ def gemv(blob: Blob, dev_blob: int, tensors, dev_x, m: int, dev_y, stream: int =
         raise WcError("wc_gemv", rc)
 
 
+def gemm_workspace_bytes(blob: Blob, tensors, dev_x, m: int) -> int:
+    """wc_gemm_workspace_bytes: device bytes wc_gemm needs for these jobs (0 up
+    to 64 rows of x; jobs with the same x share its packed copy)."""
+    n = len(tensors)
+    ts = (C.c_uint32 * max(n, 1))(*tensors)
+    xs = (C.c_void_p * max(n, 1))(*[p or None for p in dev_x])
+    out = C.c_uint64(0)
+    rc = lib().wc_gemm_workspace_bytes(blob.ptr, n, ts, xs, m, C.byref(out))
+    if rc:
+        raise WcError("wc_gemm_workspace_bytes", rc)
+    return out.value
+
+
+def gemm(blob: Blob, dev_blob: int, tensors, dev_x, m: int, dev_y, workspace: int = 0,
+         workspace_bytes: int = 0, stream: int = 0, dev_err: int = 0) -> None:
+    """wc_gemm with raw device pointers: wc_gemv for up to 64 rows of x, the
+    shared fused GEMM (packed x in the caller's workspace) above."""
+    n = len(tensors)
+    ts = (C.c_uint32 * max(n, 1))(*tensors)
+    xs = (C.c_void_p * max(n, 1))(*[p or None for p in dev_x])
+    ys = (C.c_void_p * max(n, 1))(*[p or None for p in dev_y])
+    rc = lib().wc_gemm(blob.ptr, C.c_void_p(dev_blob), n, ts, xs, m, ys,
+                       C.c_void_p(workspace or None), workspace_bytes,
+                       C.c_void_p(stream or None), C.c_void_p(dev_err or None))
+    if rc:
+        raise WcError("wc_gemm", rc)
+
+
 # --- torch plumbing: device memory and streams only ---------------------------
 
 def to_device(blob: Blob, device="cuda"):
@@ -369,3 +406,25 @@ def encode_device(entries, chunk_bytes: int = 65536, lanes: int = 64, tile=(0, 0
     if rc:
         raise WcError("wc_encode_device", rc)
     return blob, size
+
+
+def gemm_torch(blob: Blob, dev_blob, tensors, xs, ys=None, workspace=None, stream=None, err=None):
+    """wc_gemm into float32 tensors: ys[i] += xs[i] @ W_i^T (ys zeroed and
+    returned if None; the workspace is allocated if None)."""
+    import torch
+    m = xs[0].shape[0]
+    for x in xs:
+        if x.dtype != torch.bfloat16 or not x.is_contiguous() or x.shape[0] != m:
+            raise ValueError("xs must be contiguous bfloat16 tensors with equal row counts")
+    if ys is None:
+        ys = [torch.zeros((m, int(blob.out_bytes[t] // 2 // x.shape[1])), dtype=torch.float32,
+                          device=x.device) for t, x in zip(tensors, xs)]
+    need = gemm_workspace_bytes(blob, list(tensors), [x.data_ptr() for x in xs], m)
+    if workspace is None:
+        workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=xs[0].device)
+    if stream is None:
+        stream = torch.cuda.current_stream(xs[0].device)
+    gemm(blob, dev_blob.data_ptr(), list(tensors), [x.data_ptr() for x in xs], m,
+         [y.data_ptr() for y in ys], workspace.data_ptr(), workspace.numel(), stream.cuda_stream,
+         err.data_ptr() if err is not None else 0)
+    return ys

@@ -2,9 +2,10 @@
 
 wc_gemv adds x * W^T to y, decoding W on the fly.  The reference is the
 oracle's fp64 product of the same bf16 values (orc_gemv_bf16, pinned on
-one-hot and small-integer inputs).  The GPU sums in fp32 (v_dot2_f32_bf16 for
-64-row tiles, v_mfma_f32_16x16x32_bf16 for 16-row tiles, then fp32 atomics
-across the tiles of a row band); bf16 products are exact in fp32, so with at
+one-hot and small-integer inputs).  The GPU sums in fp32 (v_dot2_f32_bf16 or
+v_mfma_f32_32x32x16_bf16 for 64-row tiles, v_mfma_f32_32x32x16_bf16 for 32-row
+and v_mfma_f32_16x16x32_bf16 for 16-row tiles, then fp32 atomics across the
+tiles or tile segments of a row band); bf16 products are exact in fp32, so with at
 most K roundings of relative size 2^-24 each, |y - y_ref| <= K * 2^-24 *
 sum_k |x_k w_k|.  The test allows twice that.
 """
@@ -44,6 +45,15 @@ def _run_gemv(blob, dev, t, x_bits, y0=None, expect_err=0):
     err = torch.zeros(1, dtype=torch.int32, device=dev)
     ys = None if y0 is None else [torch.from_numpy(y0).to(dev)]
     ys = wc.gemv_torch(blob, d, [t], [_dev_x(x_bits, dev)], ys=ys, err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == expect_err, wc.describe_errors(int(err.item()))
+    return ys[0].cpu().numpy().astype(np.float64)
+
+
+def _run_gemm(blob, dev, t, x_bits, expect_err=0):
+    d = wc.to_device(blob, dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ys = wc.gemm_torch(blob, d, [t], [_dev_x(x_bits, dev)], err=err)
     torch.cuda.synchronize()
     assert int(err.item()) == expect_err, wc.describe_errors(int(err.item()))
     return ys[0].cpu().numpy().astype(np.float64)
@@ -133,7 +143,7 @@ def test_gemv_reports_corruption(dev):
     assert int(err.item()) & 0x6
 
 
-@pytest.mark.parametrize("m", [1, 5])
+@pytest.mark.parametrize("m", [1, 5, 100])
 def test_gemv_many_jobs_in_one_launch(dev, m):
     """Every projection of a scaled 8B layer in one call; jobs with the same K
     share one x, as q/k/v and gate/up do in a transformer layer."""
@@ -147,7 +157,7 @@ def test_gemv_many_jobs_in_one_launch(dev, m):
         xbits.setdefault(t.shape[1], _bf16(rng.normal(0, 1.0, (m, t.shape[1]))))
     xdev = {k: _dev_x(v, dev) for k, v in xbits.items()}
     err = torch.zeros(1, dtype=torch.int32, device=dev)
-    ys = wc.gemv_torch(blob, d, list(range(len(ts))), [xdev[t.shape[1]] for t in ts], err=err)
+    ys = wc.gemm_torch(blob, d, list(range(len(ts))), [xdev[t.shape[1]] for t in ts], err=err)
     torch.cuda.synchronize()
     assert int(err.item()) == 0
     for t, y in zip(ts, ys):
@@ -214,9 +224,9 @@ def test_mfma_gemm_full_size_layer(dev, tile):
 
 
 def test_gemv_row_limits(dev):
-    """Up to 64 rows of x on every tile height (64-row tiles take the VALU dot
-    products up to 5 rows, the matrix cores above); 65 rows are refused, and
-    64-row tiles narrower than 16 columns take at most 5."""
+    """Up to 64 rows of x on 16-row tiles (65 are refused); 64-row tiles take the
+    VALU dot products up to 5 rows and the matrix cores above, and 64-row tiles
+    narrower than 16 columns take at most 5."""
     rng = np.random.default_rng(43)
     w = _bf16(rng.normal(0, 0.02, (128, 512)))
     b64 = wc.encode([("bf16", w, (128, 512))], tile=(64, 256), tile_order=1)
@@ -230,6 +240,146 @@ def test_gemv_row_limits(dev):
     _check(_run_gemv(narrow, dev, 0, x5), w, x5)
     with pytest.raises(wc.WcError):
         _run_gemv(narrow, dev, 0, x6)
-    for b in (b64, b16):
-        with pytest.raises(wc.WcError):
-            _run_gemv(b, dev, 0, _bf16(rng.normal(0, 1.0, (65, 512))))
+    with pytest.raises(wc.WcError):                 # 16-row tiles: at most 64 rows
+        _run_gemv(b16, dev, 0, _bf16(rng.normal(0, 1.0, (65, 512))))
+
+
+# --- many rows of x: wc_gemm, the shared fused GEMM on 64-row tiles ----------
+# The waves of a workgroup decode up to 8 tiles of one band once and multiply
+# every decoded pair of wave rows by their own 32 rows of packed x (256 per pass).
+
+@pytest.mark.parametrize("shape,tile", [((128, 5120), (64, 512)),   # 10 tiles: 2 + 6 idle waves
+                                        ((64, 4096), (64, 512)),    # one full segment
+                                        ((192, 1024), (64, 256)),   # 4 tiles, 4 idle waves
+                                        ((64, 128), (64, 16)),      # one pair per tile
+                                        ((128, 9216), (64, 512))])  # 18 tiles: 3 segments
+@pytest.mark.parametrize("m", [65, 100, 256, 300])
+def test_shared_gemm_matches_the_reference(dev, shape, tile, m):
+    say("shared gemm", shape, tile, m)
+    rng = np.random.default_rng(shape[1] + m)
+    w = _bf16(rng.normal(0, 0.02, shape))
+    x = _bf16(rng.normal(0, 1.0, (m, shape[1])))
+    blob = wc.encode([("bf16", w, shape)], tile=tile, tile_order=1)
+    _check(_run_gemm(blob, dev, 0, x), w, x)
+
+
+@pytest.mark.parametrize("m", [65, 513, 1000])
+def test_shared_gemm_small_integers_exact(dev, m):
+    """Exact small-integer products pin the operand exchange through LDS, the
+    x blocks of every wave and the passes over x."""
+    rng = np.random.default_rng(44 + m)
+    shape = (128, 5120)
+    w = _bf16(rng.integers(-4, 5, shape).astype(np.float32))
+    x = _bf16(rng.integers(-3, 4, (m, shape[1])).astype(np.float32))
+    blob = wc.encode([("bf16", w, shape)], tile=(64, 512), tile_order=1)
+    y = _run_gemm(blob, dev, 0, x)
+    ref, _ = oracle.gemv_bf16(w, x)
+    assert np.array_equal(y, ref)
+
+
+def test_shared_gemm_full_size_layer(dev):
+    """All seven projections of a Llama-3-70B layer (numpy draw), 64 x 512
+    tiles, 256 rows of x, one launch: sampled y within the fp32 bound."""
+    ts = synth.config(5)
+    blob = wc.encode([(t.dtype, t.data, t.shape) for t in ts], tile=(64, 512), tile_order=1)
+    d = wc.to_device(blob, dev)
+    rng = np.random.default_rng(45)
+    xbits = {}
+    for t in ts:
+        xbits.setdefault(t.shape[1], _bf16(rng.normal(0, 1.0, (256, t.shape[1]))))
+    xdev = {k: _dev_x(v, dev) for k, v in xbits.items()}
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ys = wc.gemm_torch(blob, d, list(range(len(ts))), [xdev[t.shape[1]] for t in ts], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    for t, y in zip(ts, ys):
+        rows = np.random.default_rng(t.shape[0]).choice(t.shape[0], 32, replace=False)
+        xr = xbits[t.shape[1]][::8]                      # 32 of the 256 x rows
+        ref, absref = oracle.gemv_bf16(np.ascontiguousarray(t.data[rows]), xr)
+        tol = 2.0 * t.shape[1] * 2.0 ** -24 * absref + 1e-30
+        got = y.cpu().numpy().astype(np.float64)[::8][:, rows]
+        assert (np.abs(got - ref) <= tol).all(), t.name
+
+
+def test_shared_gemm_reports_corruption(dev):
+    """A bad lane state and a bad index entry: the launch completes (the wave
+    with the bad entry still takes part in every exchange) and reports both."""
+    rng = np.random.default_rng(46)
+    w = _bf16(rng.normal(0, 0.02, (128, 5120)))
+    blob = wc.encode([("bf16", w, (128, 5120))], tile=(64, 512), tile_order=1)
+    raw = blob.tobytes()
+    idx = struct.unpack_from("<Q", raw, 32)[0]
+    x = _dev_x(_bf16(rng.normal(0, 1, (100, 5120))), dev)
+    off1 = struct.unpack_from("<I", raw, idx + 4)[0] * 16
+    d = wc.to_device(blob, dev)
+    d[off1 + 16 + 20] ^= 0x01                      # a lane state of tile 1
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    wc.gemm_torch(blob, d, [0], [x], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) & 0x6
+    d = wc.to_device(blob, dev)
+    d[idx + 4 * 3 + 3] = 0x7F                      # index entry of tile 3: far past the records
+    err.zero_()
+    wc.gemm_torch(blob, d, [0], [x], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) & 0x1
+
+
+def test_shared_gemm_limits(dev):
+    """Past 64 rows of x: 64-row tiles only, all full; at most 4096 rows;
+    wc_gemv stops at 64."""
+    rng = np.random.default_rng(47)
+    w = _bf16(rng.normal(0, 0.02, (128, 512)))
+    b16 = wc.encode([("bf16", w, (128, 512))], tile=(16, 256), tile_order=1)
+    ragged = wc.encode([("bf16", w[:100], (100, 512))], tile=(64, 256), tile_order=1)
+    b64 = wc.encode([("bf16", w, (128, 512))], tile=(64, 256), tile_order=1)
+    x65 = _bf16(rng.normal(0, 1.0, (65, 512)))
+    for b in (b16, ragged):
+        with pytest.raises(wc.WcError) as e:
+            _run_gemm(b, dev, 0, x65)
+        assert e.value.rc == -5
+    with pytest.raises(wc.WcError) as e:
+        _run_gemv(b64, dev, 0, x65)
+    assert e.value.rc == -1
+    _check(_run_gemm(b64, dev, 0, x65), w, x65)
+    x4096 = _bf16(rng.normal(0, 1.0, (4096, 512)))
+    _check(_run_gemm(b64, dev, 0, x4096), w, x4096)
+    with pytest.raises(wc.WcError) as e:
+        _run_gemm(b64, dev, 0, _bf16(rng.normal(0, 1.0, (4097, 512))))
+    assert e.value.rc == -1
+
+
+@pytest.mark.parametrize("m", [1, 37, 64])
+def test_gemm_up_to_64_rows_is_gemv(dev, m):
+    """wc_gemm below 65 rows runs wc_gemv's kernels, with no workspace."""
+    rng = np.random.default_rng(48 + m)
+    w = _bf16(rng.normal(0, 0.02, (128, 1024)))
+    x = _bf16(rng.normal(0, 1.0, (m, 1024)))
+    for tile in ((64, 512), (16, 1024)):
+        blob = wc.encode([("bf16", w, (128, 1024))], tile=tile, tile_order=1)
+        assert wc.gemm_workspace_bytes(blob, [0], [16], m) == 0
+        _check(_run_gemm(blob, dev, 0, x), w, x)
+
+
+def test_gemm_jobs_sharing_x(dev):
+    """q, k and v of one x and a second x: one packed copy per distinct x,
+    every product right, the workspace used as sized."""
+    rng = np.random.default_rng(49)
+    ws_ = [_bf16(rng.normal(0, 0.02, (n, 1024))) for n in (256, 64, 64)]
+    w2 = _bf16(rng.normal(0, 0.02, (128, 2048)))
+    blob = wc.encode([("bf16", w, w.shape) for w in ws_] + [("bf16", w2, w2.shape)],
+                     tile=(64, 256), tile_order=1, codebook="layer")
+    d = wc.to_device(blob, dev)
+    x1 = _bf16(rng.normal(0, 1.0, (130, 1024)))
+    x2 = _bf16(rng.normal(0, 1.0, (130, 2048)))
+    dx1, dx2 = _dev_x(x1, dev), _dev_x(x2, dev)
+    xs = [dx1, dx1, dx1, dx2]
+    need = wc.gemm_workspace_bytes(blob, [0, 1, 2, 3], [x.data_ptr() for x in xs], 130)
+    assert need == 160 * 1024 * 2 + 160 * 2048 * 2
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ys = wc.gemm_torch(blob, d, [0, 1, 2, 3], xs, workspace=ws, err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    for w, x, y in zip(ws_ + [w2], [x1, x1, x1, x2], ys):
+        _check(y.cpu().numpy().astype(np.float64), w, x)

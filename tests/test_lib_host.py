@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (wc_\w+)", out))
     assert set(names) <= exported
-    assert lib.wc_version() == 3
+    assert lib.wc_version() == 4
 
 
 @pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16), (6, 8), (7, 8),
@@ -172,6 +172,22 @@ def test_gemv_rejects_before_any_launch():
         with pytest.raises(wc.WcError) as e:
             wc.gemv(good, 16, [0], [16], m, [16])
         assert e.value.rc == -1
+    for m in (0, 4097):
+        with pytest.raises(wc.WcError) as e:
+            wc.gemm(good, 16, [0], [16], m, [16], 256, 1 << 20)
+        assert e.value.rc == -1
+    tile16 = wc.encode([("bf16", w, (128, 512))], tile=(16, 256), tile_order=1)
+    ragged = wc.encode([("bf16", w[:100], (100, 512))], tile=(64, 256), tile_order=1)
+    for b in (tile16, ragged):                    # past 64 rows: full 64-row tiles only
+        with pytest.raises(wc.WcError) as e:
+            wc.gemm(b, 16, [0], [16], 65, [16], 256, 1 << 20)
+        assert e.value.rc == -5
+    need = wc.gemm_workspace_bytes(good, [0], [16], 65)
+    for ws, size in ((0, need), (256, need - 1), (16, need)):   # none, too small, misaligned
+        with pytest.raises(wc.WcError) as e:
+            wc.gemm(good, 16, [0], [16], 65, [16], ws, size)
+        assert e.value.rc == -1
+
     narrow = wc.encode([("bf16", w, (128, 512))], tile=(64, 8), tile_order=1)
     with pytest.raises(wc.WcError) as e:          # 64-row tiles past 5 rows pair k-blocks
         wc.gemv(narrow, 16, [0], [16], 6, [16])
@@ -188,6 +204,24 @@ def test_gemv_rejects_before_any_launch():
         with pytest.raises(wc.WcError) as e:
             wc.gemv(b, 16, [0], [16], 1, [16])
         assert e.value.rc == -5
+
+
+def test_gemm_workspace_bytes():
+    """One packed x per distinct (pointer, K): rows rounded up to 32, bf16,
+    each slot rounded up to 256 bytes; nothing below 65 rows."""
+    w = (np.random.default_rng(5).normal(0, 0.02, (128, 512)).astype(np.float32)
+         .view(np.uint32) >> 16).astype(np.uint16)
+    w2 = np.ascontiguousarray(w[:, :496])
+    b = wc.encode([("bf16", w, (128, 512)), ("bf16", w2, (128, 496))], tile=(64, 16),
+                  tile_order=1)
+    assert wc.gemm_workspace_bytes(b, [0], [16], 64) == 0
+    assert wc.gemm_workspace_bytes(b, [0], [16], 65) == 96 * 512 * 2
+    assert wc.gemm_workspace_bytes(b, [0, 0], [16, 16], 100) == 128 * 512 * 2
+    assert wc.gemm_workspace_bytes(b, [0, 0], [16, 32], 100) == 2 * 128 * 512 * 2
+    assert wc.gemm_workspace_bytes(b, [0, 1], [16, 16], 33 + 64) == (
+        128 * 512 * 2 + ((128 * 496 * 2 + 255) // 256) * 256)
+    with pytest.raises(wc.WcError):
+        wc.gemm_workspace_bytes(b, [2], [16], 100)
 
 
 def _pad16(x):
