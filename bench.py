@@ -116,6 +116,50 @@ def oracle_baseline(blob, host_tensors, workload: str, min_seconds: float = 10.0
             "seconds": round(dt, 3), "cpu": cpu_model(), "host_cpus": os.cpu_count()}
 
 
+def oracle_gemv_baseline(blob, w0, M: int, layer_weight_bytes: int, min_seconds: float = 10.0):
+    """Single-thread oracle of the fused decode-GEMM on one host core, on a
+    bounded sample: the oracle decode of the first tensor's tiles and its fp64
+    product with up to 2 rows of x, repeated for at least `min_seconds`; the
+    per-byte decode time and the per-byte, per-row product time are scaled to
+    the whole layer at M rows."""
+    import numpy as np
+
+    import oracle
+    raw = blob.array()
+    info = oracle.tensor_info(raw)[0]
+    out = np.empty(info["out_bytes"], np.uint8)
+    rows = min(M, 2)
+    x = (np.random.default_rng(7).normal(0, 1, (rows, w0.shape[1])).astype(np.float32)
+         .view(np.uint32) >> 16).astype(np.uint16)
+    old = os.sched_getaffinity(0)
+    core = min(old)
+    os.sched_setaffinity(0, {core})
+    reps, t_dec, t_mul = 0, 0.0, 0.0
+    try:
+        while reps == 0 or t_dec + t_mul < min_seconds:
+            t0 = time.perf_counter()
+            oracle.decode_chunks(raw, 0, 0, info["n_chunks"], out=out)
+            t1 = time.perf_counter()
+            oracle.gemv_bf16(out.view(np.uint16).reshape(w0.shape), x)
+            t_mul += time.perf_counter() - t1
+            t_dec += t1 - t0
+            reps += 1
+    finally:
+        os.sched_setaffinity(0, old)
+    if not np.array_equal(out, np.ascontiguousarray(w0).view(np.uint8).reshape(-1)):
+        raise RuntimeError("oracle baseline decoded a different tensor")
+    wb = info["out_bytes"]
+    step_s = (t_dec / reps / wb + t_mul / reps / rows / wb * M) * layer_weight_bytes
+    return {"value": round(layer_weight_bytes / step_s / 1e9, 5), "unit": "GB/s", "cores": 1,
+            "kind": "oracle",
+            "sample": f"tensor 0 ({w0.shape[0]}x{w0.shape[1]} bf16, {info['n_chunks']} tiles): "
+                      f"oracle decode + fp64 product with {rows} x row(s), {reps}x; per-byte "
+                      f"decode and per-byte-per-row product times scaled to the layer's "
+                      f"{layer_weight_bytes} weight bytes at M = {M}; single thread pinned to "
+                      f"core {core}",
+            "seconds": round(t_dec + t_mul, 3), "cpu": cpu_model(), "host_cpus": os.cpu_count()}
+
+
 def counted_traffic(workload: str, chunk_bytes: int, lanes: int, tiled: bool = False):
     import hashlib
     src = os.path.join(ROOT, "paper_2606_15789_amd", "csrc", "wc_decode.hip")
@@ -541,6 +585,9 @@ def gemv_bench(args, dev) -> int:
                          "what": "torch.matmul on the bf16 weights"},
         "setup_s": round(setup_s, 1),
     }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = oracle_gemv_baseline(blob, W[0].cpu().view(torch.int16).numpy().view(np.uint16),
+                                                    M, wbytes)
     print(json.dumps(line), flush=True)
     return 0
 
