@@ -60,7 +60,7 @@ ROTATE_BYTES = 1 << 30   # resident bytes the small workloads rotate over
 # WRITE_SIZE runs, each scaled by the same counter on a 512 MiB device copy (FETCH_SIZE
 # reads half the copied bytes: factor 2.0; WRITE_SIZE is exact).  Valid only for
 # the kernel source they were taken on (sha256 prefix); otherwise reported as null.
-COUNTED_TRAFFIC = {"kernel_sha256": "66ecc7505236a3ca", "fetch_bytes": 1143544218,
+COUNTED_TRAFFIC = {"kernel_fingerprint": "5d6401ebff49316d", "fetch_bytes": 1143544218,
                    "write_bytes": 1711282176, "chunk_bytes": 65536, "lanes": 64}
 
 
@@ -160,14 +160,25 @@ def oracle_gemv_baseline(blob, w0, M: int, layer_weight_bytes: int, min_seconds:
             "seconds": round(t_dec + t_mul, 3), "cpu": cpu_model(), "host_cpus": os.cpu_count()}
 
 
+def decode_kernel_fingerprint():
+    """The fingerprint of wc_decode_kernel's gfx950 code in the loaded library
+    (written next to it by the build), or None."""
+    from paper_2606_15789_amd import wc
+    path = os.path.splitext(wc.library_path())[0] + ".kernels.json"
+    try:
+        with open(path) as fh:
+            prints = json.load(fh)
+    except (OSError, ValueError):
+        return None
+    return next((v for k, v in prints.items() if "wc_decode_kernel" in k), None)
+
+
 def counted_traffic(workload: str, chunk_bytes: int, lanes: int, tiled: bool = False):
-    import hashlib
-    src = os.path.join(ROOT, "paper_2606_15789_amd", "csrc", "wc_decode.hip")
-    with open(src, "rb") as fh:
-        sha = hashlib.sha256(fh.read()).hexdigest()[:16]
+    """HBM bytes per launch from the counter runs, if they were taken on this
+    workload and on the decode kernel as built now."""
     c = COUNTED_TRAFFIC
-    if (workload != WORKLOAD_DEFAULT or tiled or sha != c["kernel_sha256"]
-            or chunk_bytes != c["chunk_bytes"] or lanes != c["lanes"]):
+    if (workload != WORKLOAD_DEFAULT or tiled or chunk_bytes != c["chunk_bytes"]
+            or lanes != c["lanes"] or decode_kernel_fingerprint() != c["kernel_fingerprint"]):
         return None
     return c["fetch_bytes"] + c["write_bytes"]
 

@@ -30,18 +30,62 @@ def stale() -> bool:
     return any(os.path.getmtime(p) > t for p in SOURCES + HEADERS)
 
 
+# Fingerprints of the decode kernels' gfx950 code, written next to the library
+# by every build: the hash of each kernel's assembly with comments and label
+# numbers taken out.  Measurements taken on one kernel (counter runs) name the
+# fingerprint they were taken on, so they can tell when that kernel changed,
+# whatever else changed in its source file.
+KERNELS = os.path.join(HERE, "libwc.kernels.json")
+KERNEL_SOURCE = os.path.join(CSRC, "wc_decode.hip")
+
+
+def kernel_fingerprints(asm: str) -> dict:
+    import hashlib
+    import re
+    out = {}
+    for m in re.finditer(r"^(_Z\w+):", asm, re.M):
+        name = m.group(1)
+        end = asm.find(".Lfunc_end", m.end())
+        if end < 0:
+            continue
+        lines = []
+        for line in asm[m.end():end].splitlines():
+            line = line.split(";")[0].strip()
+            if not line:
+                continue
+            lines.append(re.sub(r"\.LBB\d+_", ".LBB_", line))
+        out[name] = hashlib.sha256("\n".join(lines).encode()).hexdigest()[:16]
+    return out
+
+
 def build(verbose: bool = False) -> str:
+    import json
+    import tempfile
     tmp = LIB + f".tmp{os.getpid()}"
     cmd = [HIPCC] + FLAGS + SOURCES + ["-o", tmp]
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError("libwc build failed: " + " ".join(cmd))
+    with tempfile.TemporaryDirectory() as td:
+        asm = os.path.join(td, "wc_decode.s")
+        acmd = ([HIPCC] + [f for f in FLAGS if f not in ("-shared", "-lpthread")] +
+                ["--cuda-device-only", "-S", KERNEL_SOURCE, "-o", asm])
+        ap = subprocess.Popen(acmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        aout, aerr = ap.communicate()
+        if res.returncode != 0:
+            sys.stderr.write(res.stdout + res.stderr)
+            raise RuntimeError("libwc build failed: " + " ".join(cmd))
+        if ap.returncode != 0:
+            sys.stderr.write(aout + aerr)
+            raise RuntimeError("kernel assembly failed: " + " ".join(acmd))
+        with open(asm) as fh:
+            prints = kernel_fingerprints(fh.read())
     if verbose:
         out = "\n".join(l for l in (res.stdout + res.stderr).splitlines()
                         if "packed-fp32-ops" not in l)
         if out.strip():
             print(out)
+    with open(KERNELS + ".tmp", "w") as fh:
+        json.dump(prints, fh, indent=1, sort_keys=True)
+    os.replace(KERNELS + ".tmp", KERNELS)
     os.replace(tmp, LIB)
     return LIB
 
