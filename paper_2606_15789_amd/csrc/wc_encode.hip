@@ -528,25 +528,39 @@ __device__ void pack_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, uin
     const uint8_t* src = reinterpret_cast<const uint8_t*>(T.src);
     const GroupAddr ga(T, c);
     const uint32_t groups = (n_c + W - 1) / W;
-    uint32_t gi = lane;
-    uint4 v = gi < groups ? load16(src, T.src_bytes, ga.at(gi * W)) : make_uint4(0u, 0u, 0u, 0u);
-    for (; gi < groups; gi += 64) {
-      const uint32_t i0 = gi * W;
-      // the next lane-group's load is in flight while this one is written
-      const uint4 cur = v;
-      if (gi + 64 < groups) v = load16(src, T.src_bytes, ga.at((gi + 64) * W));
-      uint32_t rb[2] = {0u, 0u};
+    // a lane takes pairs of lane-groups (16 raw bytes, one 16-byte store);
+    // kPairs pairs per lane per round, their source loads all in flight at once
+    constexpr uint32_t kPairs = 4;
+    const uint32_t pairs = (groups + 1) / 2;
+    for (uint32_t p0 = 0; p0 < pairs; p0 += 64 * kPairs) {
+      uint4 v[kPairs][2];
 #pragma unroll
-      for (uint32_t k = 0; k < 8; k++) {
-        const uint32_t w = (dword(cur, k >> 1) >> (16 * (k & 1))) & 0xFFFFu;
-        const uint32_t r = ((w >> 8) & 0x80u) | (w & 0x7Fu);
-        rb[k >> 2] |= r << (8 * (k & 3));
-      }
-      const uint32_t nv = min(W, n_c - i0);
-      if (nv == W) {
-        *reinterpret_cast<uint2*>(raw + i0) = make_uint2(rb[0], rb[1]);
-      } else {
-        for (uint32_t k = 0; k < nv; k++) raw[i0 + k] = uint8_t(rb[k >> 2] >> (8 * (k & 3)));
+      for (uint32_t b = 0; b < kPairs; b++)
+#pragma unroll
+        for (uint32_t h = 0; h < 2; h++) {
+          const uint32_t gi = 2 * (p0 + 64 * b + lane) + h;
+          v[b][h] = gi < groups ? load16(src, T.src_bytes, ga.at(gi * W)) : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+      for (uint32_t b = 0; b < kPairs; b++) {
+        const uint32_t p = p0 + 64 * b + lane;
+        if (p >= pairs) continue;
+        uint32_t rb[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+        for (uint32_t h = 0; h < 2; h++)
+#pragma unroll
+          for (uint32_t k = 0; k < 8; k++) {
+            const uint32_t w = (dword(v[b][h], k >> 1) >> (16 * (k & 1))) & 0xFFFFu;
+            const uint32_t r = ((w >> 8) & 0x80u) | (w & 0x7Fu);
+            rb[2 * h + (k >> 2)] |= r << (8 * (k & 3));
+          }
+        const uint32_t i0 = 2 * p * W;
+        const uint32_t nv = min(2 * W, n_c - i0);
+        if (nv == 2 * W && (reinterpret_cast<uintptr_t>(raw + i0) & 15u) == 0) {
+          *reinterpret_cast<uint4*>(raw + i0) = make_uint4(rb[0], rb[1], rb[2], rb[3]);
+        } else {
+          for (uint32_t k = 0; k < nv; k++) raw[i0 + k] = uint8_t(rb[k >> 2] >> (8 * (k & 3)));
+        }
       }
     }
     if (c + 1 == T.n_chunks) {
