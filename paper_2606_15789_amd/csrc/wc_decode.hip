@@ -514,6 +514,7 @@ template <int kXB>
 __device__ __forceinline__ void share_mma(const Share& s, uint32_t lane,
                                           const u32x4 (&xs)[kWaves][kXB],
                                           f32x16 (&acc)[kXB][2]) {
+  if (s.mrows == 0) return;  // no rows of x in this pass: no operand to read
 #pragma unroll
   for (int f = 0; f < kWaves; f++) {
     if (uint32_t(f) >= s.n_act) break;
