@@ -2,7 +2,10 @@
  * wc.h -- C ABI of libwc, the MI355X chunked rANS weight decoder.
  *
  * The library turns near-entropy-bound compressed weight streams back into
- * bit-identical bf16 / fp16 / int8 / int4 tensors in GPU memory.
+ * bit-identical bf16 / fp16 / int8 / int4 / fp8 / fp4 tensors in GPU memory
+ * (wc_decode), or multiplies bf16 weights into activations while decoding
+ * them, never writing them out (wc_gemv, wc_gemm).  Compression runs on the
+ * host (wc_encode) or on the GPU (wc_encode_device), to the same blob.
  *
  * Paper: "Approaching Shannon Bound with Lossless LLM Weight Compression"
  * (Tan, Chen, Alonso, Wong, He).
@@ -13,6 +16,8 @@
  *   - Alg. 2, Sec. V-C-3: lane-parallel rANS decode with a table lookup of
  *     (symbol, frequency, cumulative frequency) in on-chip memory and
  *     coalesced renormalisation reads.
+ *   - Alg. 1 / 3, Sec. V (pipeline overlap and the batch-size regime):
+ *     decoded tiles consumed by the GEMM on chip, never written to memory.
  *   - Sec. VI-F: metadata = 4 B per tile offset + one 2^12-entry codebook.
  *
  * All functions return a wc_status; no C++ exception crosses the ABI.  No

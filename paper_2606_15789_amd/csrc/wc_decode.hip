@@ -33,8 +33,12 @@
 //    four int8 or eight int4), and every 4G steps it stores the four with one
 //    16-byte non-temporal (streaming) store, so a wave writes a 1 KiB row;
 //  * the raw sign|mantissa bytes of bf16/fp16 rows (8 per lane per row) are
-//    loaded two rows ahead with one 8-byte load per lane;
-// No MFMA: the work is integer table decoding, not a contraction.
+//    loaded two rows ahead with one 8-byte load per lane.
+// The decode itself uses no MFMA: it is integer table decoding, not a
+// contraction.  The fused decode-GEMM kernels (wc_gemv_kernel, wc_gemm_kernel,
+// Alg. 1 / 3) run the same decoder and feed the decoded bf16 lane-groups to the
+// VALU dot products or to v_mfma_f32_16x16x32_bf16 / v_mfma_f32_32x32x16_bf16
+// operands instead of storing them.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -428,18 +432,6 @@ __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ 
   return lo;
 }
 
-// Decode the chunk(s) of one wave, one rANS lane per wave lane.  G symbols
-// make one output dword; a lane-group is 4G symbols, 16 output bytes, so a
-// lane's share of a row is stored with one 16-byte store.
-//
-// kGemv: instead of storing a row, multiply it into y (the fused decode-GEMM,
-// Alg. 1 / 3).  It needs column-block tiles of 64 rows decoded by 64 lanes:
-// lane l then holds 8 consecutive weights of tile row l in every wave row r
-// (columns b * tile_c + 8 r ..), so each lane accumulates whole dot products
-// of its row with v_dot2_f32_bf16, reading the matching x columns as scalar
-// (wave-uniform) loads, and adds them to y once per tile (fp32 atomics: the
-// tiles of one row band split K).
-//
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
@@ -570,6 +562,18 @@ __device__ void share_idle_wave(const LaunchArgs& a, const DevTensor& T, const S
   share_store<kXB>(s, lane, acc, reinterpret_cast<float*>(T.dst));
 }
 
+// Decode the chunk(s) of one wave, one rANS lane per wave lane.  G symbols
+// make one output dword; a lane-group is 4G symbols, 16 output bytes, so a
+// lane's share of a row is stored with one 16-byte store.
+//
+// kGemv: instead of storing a row, multiply it into y (the fused decode-GEMM,
+// Alg. 1 / 3).  It needs column-block tiles of 64 rows decoded by 64 lanes:
+// lane l then holds 8 consecutive weights of tile row l in every wave row r
+// (columns b * tile_c + 8 r ..), so each lane accumulates whole dot products
+// of its row with v_dot2_f32_bf16, reading the matching x columns as scalar
+// (wave-uniform) loads, and adds them to y once per tile (fp32 atomics: the
+// tiles of one row band split K).
+//
 // kMB: the fused GEMM on the matrix cores, for up to kMR kMB rows of x.  It
 // needs column-block tiles of kMR (16 or 32) rows decoded by 64 lanes: lane l
 // then holds, in every wave row r, the 8 weights of tile row l mod kMR at
@@ -590,6 +594,11 @@ __device__ void share_idle_wave(const LaunchArgs& a, const DevTensor& T, const S
 // B operands of v_mfma_f32_32x32x16_bf16 (rows 0..31 and 32..63: lanes 0..31
 // keep row r, lanes 32..63 take row r + 1 of the same W rows), which share
 // one A operand of x, so every x value loaded feeds 64 W rows.
+//
+// kShare (with kMR = 64): the shared fused GEMM.  The two B operands of each
+// pair go to this wave's slot in LDS instead, and after a workgroup barrier
+// every wave multiplies all decoding waves' operands by its own rows of packed
+// x (see Share).
 template <int G, int L, bool kTiled, int kM = 0, int kMB = 0, int kMR = 16, bool kShare = false>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
