@@ -81,6 +81,8 @@ def lib():
                                       C.POINTER(u8p), C.POINTER(C.c_uint64)]
         L.orc_gemv_bf16.argtypes = [C.c_void_p, C.c_uint64, C.c_uint64, C.c_void_p, C.c_uint32,
                                     C.c_void_p, C.c_void_p]
+        L.orc_gemm_i8.argtypes = [C.c_void_p, C.c_uint64, C.c_uint64, C.c_void_p, C.c_uint32,
+                                  C.c_void_p]
         L.orc_free.argtypes = [C.c_void_p]
         L.orc_free.restype = None
         L.orc_blob_tensors.argtypes = [C.c_void_p, C.c_uint64, C.POINTER(C.c_uint32)]
@@ -315,3 +317,18 @@ def gemv_bf16(w, x):
     if rc:
         raise OracleError(rc, "gemv")
     return y, a
+
+
+def gemm_i8(w, x):
+    """y[m, n] = sum_k x[m, k] * w[n, k] exactly (int64) for int8 w (rows x
+    cols) and int8 x (M x cols)."""
+    w = np.ascontiguousarray(w, dtype=np.int8)
+    x = np.ascontiguousarray(x, dtype=np.int8)
+    rows, cols = w.shape
+    M = x.shape[0]
+    assert x.shape[1] == cols
+    y = np.empty((M, rows), np.int64)
+    rc = lib().orc_gemm_i8(_ptr(w), rows, cols, _ptr(x), M, _ptr(y))
+    if rc:
+        raise OracleError(rc, "gemm_i8")
+    return y

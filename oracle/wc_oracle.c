@@ -984,3 +984,21 @@ int orc_gemv_bf16(const uint16_t* w, uint64_t rows, uint64_t cols, const uint16_
     }
   return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* What the fused int8 decode-GEMM computes (W8A8, the sq8 format of Sec.    */
+/* VI-A; Alg. 1 / 3): y[m][n] = sum_k x[m][k] * w[n][k] for int8 w (rows x   */
+/* cols, row-major) and int8 x (M x cols), exactly, in 64-bit integers.      */
+
+int orc_gemm_i8(const int8_t* w, uint64_t rows, uint64_t cols, const int8_t* x, uint32_t M,
+                int64_t* y) {
+  if (!w || !x || !y || M == 0) return ORC_EINVAL;
+  for (uint32_t m = 0; m < M; m++)
+    for (uint64_t n = 0; n < rows; n++) {
+      int64_t s = 0;
+      for (uint64_t k = 0; k < cols; k++)
+        s += (int64_t)x[(uint64_t)m * cols + k] * (int64_t)w[n * cols + k];
+      y[(uint64_t)m * rows + n] = s;
+    }
+  return ORC_OK;
+}

@@ -192,3 +192,50 @@ def test_gemv_reference_exact_on_small_integers():
     y, a = oracle.gemv_bf16(_bf16_of(wi.astype(np.float32)), _bf16_of(xi.astype(np.float32)))
     assert np.array_equal(y, (xi @ wi.T).astype(np.float64))
     assert np.array_equal(a, (np.abs(xi) @ np.abs(wi).T).astype(np.float64))
+
+
+def test_gemm_i8_reference_one_hot_rows_pick_columns():
+    rng = np.random.default_rng(15)
+    w = rng.integers(-128, 128, (24, 80)).astype(np.int8)
+    ks = [0, 33, 79]
+    x = np.zeros((3, 80), np.int8)
+    for m, k in enumerate(ks):
+        x[m, k] = 1
+    y = oracle.gemm_i8(w, x)
+    for m, k in enumerate(ks):
+        assert y[m].tolist() == [int(v) for v in w[:, k]]
+
+
+def test_gemm_i8_reference_is_signed_and_exact_at_the_extremes():
+    """int8 bytes are two's complement: -128 * 127 must give a negative sum
+    (an unsigned reading would give +16256 per term), and the extremes of
+    K = 4096 terms sum exactly."""
+    K = 4096
+    w = np.full((2, K), 127, np.int8)
+    w[1] = -128
+    x = np.full((2, K), -128, np.int8)
+    x[1] = 127
+    y = oracle.gemm_i8(w, x)
+    assert y.tolist() == [[-128 * 127 * K, 128 * 128 * K], [127 * 127 * K, -128 * 127 * K]]
+
+
+def test_gemm_i8_reference_rank_one_closed_form():
+    """w[n, k] = a_n b_k and x[m, k] = c_m d_k give y[m, n] = a_n c_m sum_k b_k d_k."""
+    rng = np.random.default_rng(16)
+    a, b = rng.integers(-9, 10, 7), rng.integers(-9, 10, 300)
+    c, d = rng.integers(-9, 10, 5), rng.integers(-9, 10, 300)
+    w = np.array([[int(an) * int(bk) for bk in b] for an in a], np.int8)
+    x = np.array([[int(cm) * int(dk) for dk in d] for cm in c], np.int8)
+    s = sum(int(bk) * int(dk) for bk, dk in zip(b, d))
+    y = oracle.gemm_i8(w, x)
+    assert y.tolist() == [[int(an) * int(cm) * s for an in a] for cm in c]
+
+
+def test_gemm_i8_reference_brute_force_small():
+    rng = np.random.default_rng(17)
+    for rows, cols, M in ((1, 1, 1), (3, 5, 2), (6, 17, 4)):
+        w = rng.integers(-128, 128, (rows, cols)).astype(np.int8)
+        x = rng.integers(-128, 128, (M, cols)).astype(np.int8)
+        want = [[sum(int(x[m, k]) * int(w[n, k]) for k in range(cols)) for n in range(rows)]
+                for m in range(M)]
+        assert oracle.gemm_i8(w, x).tolist() == want
