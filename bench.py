@@ -231,6 +231,11 @@ def main() -> int:
                     help="tile rows of the fused GEMM: 64 (VALU dot products for M <= 5, "
                          "matrix cores above), 32 or 16 (matrix cores); default 16 for "
                          "M <= 16, else 64")
+    ap.add_argument("--gemm-i8", type=int, default=0, metavar="M",
+                    help="time the fused int8 decode-GEMM (W8A8: int8 x, int32 y, "
+                         "v_mfma_i32_16x16x64_i8; M rows, 1..64) over the int8 projections of "
+                         "the 8B W8 layer in 16 x 2048 tiles, next to the same product unfused "
+                         "and uncompressed (torch._int_mm)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -250,6 +255,8 @@ def main() -> int:
     wc.lib()
     if args.gemv:
         return gemv_bench(args, dev)
+    if args.gemm_i8:
+        return gemm_i8_bench(args, dev)
     if args.encode:
         return encode_bench(args, dev)
     if args.sweep:
@@ -599,6 +606,137 @@ def gemv_bench(args, dev) -> int:
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = oracle_gemv_baseline(blob, W[0].cpu().view(torch.int16).numpy().view(np.uint16),
                                                     M, wbytes)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def gemm_i8_bench(args, dev) -> int:
+    """Fused int8 decode-GEMM (W8A8) over the seven int8 projections of the 8B
+    W8 layer: exact int32 y, checked against an fp64 product (exact here)."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15789_amd import synth, wc
+    M = args.gemm_i8
+    if not 1 <= M <= 64:
+        print("--gemm-i8 takes 1..64 rows of activations", file=sys.stderr)
+        return 2
+    tile = (16, 2048)
+    t0 = time.perf_counter()
+    ts = [t for t in synth.config(4) if t.dtype == "u8" and len(t.shape) == 2]
+    shapes = [t.shape for t in ts]
+    blob = wc.encode([(t.dtype, t.data, t.shape) for t in ts], lanes=64, tile=tile,
+                     tile_order=1, threads=args.threads)
+    dblob = wc.to_device(blob, dev)
+    W = [torch.from_numpy(np.ascontiguousarray(t.data).view(np.int8).reshape(t.shape)).to(dev)
+         for t in ts]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(54321)
+    xs = [torch.randint(-127, 128, (M, shp[1]), generator=gen, device=dev, dtype=torch.int8)
+          for shp in shapes]
+    ys = [torch.zeros(M, shp[0], dtype=torch.int32, device=dev) for shp in shapes]
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def fused():
+        wc.gemm_i8(blob, dblob.data_ptr(), list(range(len(W))), [x.data_ptr() for x in xs], M,
+                   [y.data_ptr() for y in ys], stream.cuda_stream, err.data_ptr())
+
+    fused()
+    torch.cuda.synchronize()
+    if int(err.item()):
+        raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
+    for t, (w, x, y) in enumerate(zip(W, xs, ys)):
+        # |y| < 2^30: the fp64 product is exact
+        if not torch.equal(y.double(), x.double() @ w.double().t()):
+            raise RuntimeError(f"int8 fused GEMM tensor {t} differs from the exact product")
+    setup_s = time.perf_counter() - t0
+
+    # uncompressed int8 GEMM: torch._int_mm (hipBLASLt) where it takes the shape
+    def int_mm(x, w):
+        return torch._int_mm(x, w.t())
+    try:
+        xp = torch.zeros(max(M, 32), shapes[0][1], dtype=torch.int8, device=dev)
+        int_mm(xp, W[0])
+        xs_mm = [torch.zeros(max(M, 32), shp[1], dtype=torch.int8, device=dev) for shp in shapes]
+        for xm, x in zip(xs_mm, xs):
+            xm[:M].copy_(x)
+        base_what = ("torch._int_mm (int8 x int8 -> int32) on the int8 weights" +
+                     (f", x padded to {max(M, 32)} rows (its smallest M)" if M < 32 else ""))
+        mm = int_mm
+    except RuntimeError:
+        xs_mm = [x.to(torch.bfloat16) for x in xs]
+        Wb = [w.to(torch.bfloat16) for w in W]
+        base_what = "torch.matmul in bf16 on the int8 weights (no int8 GEMM for this shape)"
+        mm = None
+
+    flat = wc.encode([("u8", np.ascontiguousarray(t.data).reshape(-1)) for t in ts], lanes=64,
+                     threads=args.threads)
+    dflat = wc.to_device(flat, dev)
+    outs = [torch.empty(n, dtype=torch.uint8, device=dev) for n in flat.out_bytes]
+
+    def product(i, w):
+        return mm(xs_mm[i], w) if mm else torch.matmul(xs_mm[i], w.t())
+
+    def unfused():
+        wc.decode(flat, dflat.data_ptr(), [o.data_ptr() for o in outs], stream.cuda_stream,
+                  err.data_ptr())
+        for i, (o, shp) in enumerate(zip(outs, shapes)):
+            w = o.view(torch.int8).view(shp)
+            product(i, w if mm else w.to(torch.bfloat16))
+
+    def uncompressed():
+        for i in range(len(W)):
+            product(i, W[i] if mm else Wb[i])
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / args.steps / 1e3
+
+    s_fused, s_unfused, s_plain = timed(fused), timed(unfused), timed(uncompressed)
+    if int(err.item()):
+        raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
+    wbytes = sum(blob.out_bytes)
+    alg = blob.size + sum(x.numel() for x in xs) + sum(2 * y.numel() * 4 for y in ys)
+    achieved = alg / s_fused / 1e9
+    line = {
+        "metric": METRIC + " [fused int8 decode-GEMM]",
+        "value": round(wbytes / s_fused / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(s_fused * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int8 x int8 -> int32",
+        "data": "synthetic",
+        "config": {"workload": "llama3-8b-layer-int8", "mode": "fused-gemm-i8", "m": M,
+                   "tile": f"{tile[0]}x{tile[1]}", "tile_order": "column-blocks",
+                   "product": "v_mfma_i32_16x16x64_i8", "lanes": 64,
+                   "weight_bytes_per_step": wbytes, "compressed_bytes_per_step": blob.size,
+                   "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "wc_gemv_kernel (int8)", "mean_step_us": round(s_fused * 1e6, 2),
+                     "algorithmic_bytes_per_step": int(alg)},
+        "unfused": {"value": round(wbytes / s_unfused / 1e9, 2), "unit": "GB/s",
+                    "ms_per_step": round(s_unfused * 1e3, 4),
+                    "what": "wc_decode of the weights (64 KiB byte-run chunks) into memory, then "
+                            + base_what},
+        "uncompressed": {"value": round(wbytes / s_plain / 1e9, 2), "unit": "GB/s",
+                         "ms_per_step": round(s_plain * 1e3, 4), "what": base_what},
+        "setup_s": round(setup_s, 1),
+    }
     print(json.dumps(line), flush=True)
     return 0
 

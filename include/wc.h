@@ -236,6 +236,30 @@ wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n, const u
                   const void* const* dev_x, uint32_t m, float* const* dev_y, void* stream,
                   int32_t* dev_err);
 
+/* wc_gemm_i8 -- the fused decode-GEMM for int8 weights and int8 activations
+ * (W8A8, the SmoothQuant-style sq8 format of Sec. VI-A; Alg. 1 / 3): for each
+ * of n jobs i, dev_y[i] += x_i * W_i^T in exact integer arithmetic, W_i =
+ * tensor tensors[i] decoded on the fly and never written.  With 16-row
+ * column-block tiles a decoded wave row (16 W rows x 64 columns) is the B
+ * operand of v_mfma_i32_16x16x64_i8 as it stands.  y is the integer product
+ * before dequantisation: the per-row scales of x and W stay with the caller.
+ *   tensors  host array of n tensor indices; each W must be WC_U8 (bytes read
+ *            as two's-complement int8), coded with 64 lanes in column-block
+ *            tiles (WC_TILE_COLUMN_BLOCKS) of 16 rows, K = cols <= 65536 (so
+ *            no int32 sum can overflow: |x w| <= 2^14);
+ *   dev_x    host array of n device pointers to int8 x, m x K row-major,
+ *            16-byte aligned (jobs may share one x);
+ *   m        1..64 rows of x, the same for every job;
+ *   dev_y    host array of n device pointers to int32 y, m x N row-major; the
+ *            products are added with integer atomics, so y is exact and the
+ *            same whatever order the tiles finish in;
+ *   stream, dev_err as for wc_decode.
+ * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument) or
+ * WC_EUNSUPPORTED (a tensor the path does not take). */
+wc_status wc_gemm_i8(const wc_blob* desc, const void* dev_blob, uint32_t n,
+                     const uint32_t* tensors, const void* const* dev_x, uint32_t m,
+                     int32_t* const* dev_y, void* stream, int32_t* dev_err);
+
 /* wc_gemm_workspace_bytes -- device workspace wc_gemm needs for these jobs
  * (host only, nothing launched): 0 for m <= 64; above, one packed copy of
  * each distinct x (jobs whose dev_x pointers and K are equal share it) of
@@ -326,7 +350,7 @@ wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_params* p, 
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);
 
-/* wc_version -- ABI version of this header (4). */
+/* wc_version -- ABI version of this header (5). */
 int32_t wc_version(void);
 
 #ifdef __cplusplus

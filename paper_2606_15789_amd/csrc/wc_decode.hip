@@ -608,7 +608,10 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   constexpr bool kMfma = kMB > 0;  // fused GEMM with kMB blocks of x rows, MFMA
   static_assert(!kShare || (kMfma && kMR == 64), "shared fused GEMM: 64-row tiles");
   static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
-  static_assert(!kMfma || (G == 2 && L == 64 && kTiled && !kGemv), "MFMA GEMM: bf16 tiles");
+  static_assert(!kMfma || (L == 64 && kTiled && !kGemv &&
+                           (G == 2 || (G == 4 && kMR == 16 && !kShare))),
+                "MFMA GEMM: bf16 tiles, or int8 tiles of 16 rows");
+  constexpr bool kInt8 = kMfma && G == 4;   // int8 W and x, int32 sums (W8A8)
   static_assert(kMR == 16 || kMR == 32 || kMR == 64, "MFMA tiles of 16, 32 or 64 rows");
   constexpr int kMM = kMR == 64 ? 32 : kMR;   // x rows per MFMA block
   constexpr int kNB = kMR == 64 ? 2 : 1;      // MFMA output blocks of W rows per tile
@@ -697,8 +700,12 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   typedef __attribute__((ext_vector_type(8))) __bf16 bf8;
   typedef __attribute__((ext_vector_type(kMM * kMM / 64))) float facc;
   typedef __attribute__((ext_vector_type(4))) unsigned int u4v;
-  constexpr uint32_t kRowXBytes = 1024u / kMR;  // bytes of an x row one wave row covers
-  facc macc[kMfma && !kShare ? kMB : 1][kNB];
+  constexpr uint32_t kXB = G == 2 ? 2u : 1u;  // bytes of one x element (bf16, int8)
+  // bytes of an x row one wave row covers: 64 lane-groups of W columns over kMR rows
+  constexpr uint32_t kRowXBytes = 64u * W / kMR * kXB;
+  typedef __attribute__((ext_vector_type(4))) int i32x4;
+  facc macc[kMfma && !kShare && !kInt8 ? kMB : 1][kNB];
+  i32x4 iacc[kInt8 ? kMB : 1];                   // int8 GEMM: 16 x 16 int32 sums per block
   f32x16 sacc[kShare ? kMB : 1][2];        // shared GEMM: this wave's x blocks x 64 W rows
   u32x4 xs[kShare ? kWaves : 1][kShare ? kMB : 1];  // shared GEMM: A operands of the pair
   uint32_t prev[kMR == 64 ? 4 : 1];             // 64-row tiles: the even row's dwords
@@ -708,19 +715,21 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   // (the shared GEMM reads packed x: rows rounded up to blocks of 32)
   const __amdgpu_buffer_rsrc_t xrs = make_rsrc(
       reinterpret_cast<const void*>(T.x),
-      kShare ? ((a.m + 31u) & ~31u) * K * 2u : (kMfma ? a.m * K * 2u : 0u));
+      kShare ? ((a.m + 31u) & ~31u) * K * 2u : (kMfma ? a.m * K * kXB : 0u));
   uint32_t xoff = 0, xblk = 0;
   if constexpr (kShare) {
 #pragma unroll
     for (int xb = 0; xb < kMB; xb++) sacc[xb][0] = sacc[xb][1] = f32x16{};
   } else if constexpr (kMfma) {
 #pragma unroll
-    for (int mb = 0; mb < kMB; mb++)
+    for (int mb = 0; mb < kMB; mb++) {
+      iacc[kInt8 ? mb : 0] = i32x4{};
 #pragma unroll
-      for (int nb = 0; nb < kNB; nb++) macc[mb][nb] = facc{};
-    // this lane's 8 x values of wave row 0: row sub mod kMM, columns 8 (sub div kMM) ..
-    xoff = ((sub % kMM) * K + (chunk0 % T.ntc) * (1u << T.log_tc) + 8u * (sub / kMM)) * 2u;
-    xblk = 2u * kMM * K;  // bytes of kMM rows of x
+      for (int nb = 0; nb < kNB; nb++) macc[kInt8 ? 0 : mb][nb] = facc{};
+    }
+    // this lane's W x values of wave row 0: row sub mod kMM, columns W (sub div kMM) ..
+    xoff = ((sub % kMM) * K + (chunk0 % T.ntc) * (1u << T.log_tc) + W * (sub / kMM)) * kXB;
+    xblk = kXB * kMM * K;  // bytes of kMM rows of x
   }
 
   // group g of the chunk, j = g mod kUnroll (static)
@@ -799,6 +808,15 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
             macc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, B1, macc[mb][1], 0, 0, 0);
           }
         }
+        return;
+      }
+      if constexpr (kInt8) {
+        // the lane-group's 16 int8 weights are the B operand as decoded
+        const i32x4 b = {int(ow[0]), int(ow[1]), int(ow[2]), int(ow[3])};
+#pragma unroll
+        for (int mb = 0; mb < kMB; mb++)
+          iacc[mb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, xa[mb]), b,
+                                                           iacc[mb], 0, 0, 0);
         return;
       }
       if constexpr (kMfma) {
@@ -883,7 +901,21 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
     for (int m = 0; m < kM; m++) unsafeAtomicAdd(y + uint64_t(m) * N + n, acc[m]);
   }
   if constexpr (kShare) share_store<kMB>(*sh, lane, sacc, reinterpret_cast<float*>(T.dst));
-  if constexpr (kMfma && !kShare) {
+  if constexpr (kInt8) {
+    // D[4 (sub div 16) + i][sub mod 16] of every x block, added to int32 y:
+    // integer adds commute, so y is the same whatever order the tiles finish in
+    const uint64_t N = uint64_t(T.n_chunks / T.ntc) * kMR;
+    int* y = reinterpret_cast<int*>(T.dst);
+    const uint32_t n = (chunk0 / T.ntc) * kMR + (sub % 16u);
+#pragma unroll
+    for (int mb = 0; mb < kMB; mb++)
+#pragma unroll
+      for (int i = 0; i < 4; i++) {
+        const uint32_t m = mb * 16u + 4u * (sub >> 4) + i;
+        if (m < a.m) atomicAdd(y + uint64_t(m) * N + n, iacc[mb][i]);
+      }
+  }
+  if constexpr (kMfma && !kShare && !kInt8) {
     // D[row][sub mod kMM] of every x block and W block: y row, W row = y column
     const uint64_t N = uint64_t(T.n_chunks / T.ntc) * kMR;
     float* y = reinterpret_cast<float*>(T.dst);
@@ -957,8 +989,9 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
 // The fused decode-GEMM of up to kMaxLaunchTensors tensors in one launch: one
 // wave per tile, y += x * W^T for each tensor's own x and y.  kM > 0: column-
 // block tiles of 64 x tile_c bf16, kM rows of x, dot products on the VALU;
-// kMB > 0: column-block tiles of kMR x tile_c, up to kMR kMB rows of x, MFMA.
-template <int kM, int kMB, int kMR = 16>
+// kMB > 0: column-block tiles of kMR x tile_c, up to kMR kMB rows of x, MFMA
+// (G = 2: bf16; G = 4: int8 W and x, 16-row tiles, int32 y).
+template <int kM, int kMB, int kMR = 16, int G = 2>
 __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   __shared__ uint2 tab[wc::kTableSize];
   __shared__ uint32_t cum[260];
@@ -976,7 +1009,7 @@ __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   build_table(a, T, tab, cum, tid);
   __syncthreads();
   if (chunk >= T.n_chunks) return;
-  decode_chunks<2, 64, true, kM, kMB, kMR>(a, T, chunk, lane, tab, ring[wave], pre);
+  decode_chunks<G, 64, true, kM, kMB, kMR>(a, T, chunk, lane, tab, ring[wave], pre);
 }
 
 // The shared fused GEMM: workgroup = (pass over 256 kXB rows of x, band of 64
@@ -1253,6 +1286,43 @@ extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t
   for (uint32_t i = 0; i < n; i++) xs[i] = reinterpret_cast<uint64_t>(dev_x[i]);
   return launch_jobs(P, dev_blob, n, tensors, xs, m, dev_y, false,
                      reinterpret_cast<hipStream_t>(stream), dev_err);
+}
+
+extern "C" wc_status wc_gemm_i8(const wc_blob* desc, const void* dev_blob, uint32_t n,
+                                const uint32_t* tensors, const void* const* dev_x, uint32_t m,
+                                int32_t* const* dev_y, void* stream, int32_t* dev_err) {
+  if (!desc || !desc->priv || !dev_blob || !tensors || !dev_x || !dev_y || n == 0 ||
+      n > kMaxLaunchTensors || m < 1 || m > 64)
+    return WC_EINVAL;
+  const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
+  LaunchArgs args{};
+  fill_common(args, P, dev_blob, dev_err);
+  uint32_t wgs = 0;
+  for (uint32_t i = 0; i < n; i++) {
+    if (tensors[i] >= desc->n_tensors || !dev_x[i] || !dev_y[i] ||
+        reinterpret_cast<uintptr_t>(dev_x[i]) % 16)
+      return WC_EINVAL;
+    const wc::TensorInfo& T = P.tensors[tensors[i]];
+    if (T.dtype != WC_U8 || T.lanes != 64 || T.tile_order != WC_TILE_COLUMN_BLOCKS ||
+        T.tile_r != 16)
+      return WC_EUNSUPPORTED;
+    // |x w| <= 2^14, so K <= 2^16 keeps every int32 sum below 2^30
+    if (T.cols > 65536 || T.rows > 0xFFFFFFFFull) return WC_EUNSUPPORTED;
+    fill_tensor(args.t[i], T, dev_y[i], wgs);
+    args.t[i].x = reinterpret_cast<uint64_t>(dev_x[i]);
+    wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
+  }
+  args.n_tensors = n;
+  args.m = m;
+  const dim3 grid(wgs), block(kThreads);
+  const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
+  switch ((m + 15) / 16) {
+    case 1: hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 16, 4>), grid, block, 0, st, args); break;
+    case 2: hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 16, 4>), grid, block, 0, st, args); break;
+    case 3: hipLaunchKernelGGL((wc_gemv_kernel<0, 3, 16, 4>), grid, block, 0, st, args); break;
+    default: hipLaunchKernelGGL((wc_gemv_kernel<0, 4, 16, 4>), grid, block, 0, st, args); break;
+  }
+  return hipGetLastError() == hipSuccess ? WC_OK : WC_EHIP;
 }
 
 extern "C" wc_status wc_gemm_workspace_bytes(const wc_blob* desc, uint32_t n,

@@ -23,7 +23,7 @@ DERR = {1: "WC_DERR_INDEX", 2: "WC_DERR_STATE", 4: "WC_DERR_CURSOR", 8: "WC_DERR
 # Every function the header declares; the library must export all of them.
 EXPORTS = ["wc_analyze", "wc_encode", "wc_open", "wc_decode", "wc_gemv", "wc_free",
            "wc_version", "wc_analyze_device", "wc_encode_device_bounds", "wc_encode_device",
-           "wc_gemm_workspace_bytes", "wc_gemm"]
+           "wc_gemm_workspace_bytes", "wc_gemm", "wc_gemm_i8"]
 
 ANALYZE_WORKSPACE_BYTES = 524288  # WC_ANALYZE_WORKSPACE_BYTES
 
@@ -97,6 +97,10 @@ def lib():
                               C.POINTER(C.c_void_p), C.c_uint32, C.POINTER(C.c_void_p),
                               C.c_void_p, C.c_uint64, C.c_void_p, C.c_void_p]
         L.wc_gemm.restype = C.c_int
+        L.wc_gemm_i8.argtypes = [C.POINTER(_Blob), C.c_void_p, C.c_uint32, C.POINTER(C.c_uint32),
+                                 C.POINTER(C.c_void_p), C.c_uint32, C.POINTER(C.c_void_p),
+                                 C.c_void_p, C.c_void_p]
+        L.wc_gemm_i8.restype = C.c_int
         L.wc_analyze_device.argtypes = [C.POINTER(_Tensor), C.c_void_p, C.c_uint64, C.c_void_p,
                                         C.POINTER(_Stats)]
         L.wc_analyze_device.restype = C.c_int
@@ -272,6 +276,20 @@ def gemm(blob: Blob, dev_blob: int, tensors, dev_x, m: int, dev_y, workspace: in
         raise WcError("wc_gemm", rc)
 
 
+def gemm_i8(blob: Blob, dev_blob: int, tensors, dev_x, m: int, dev_y, stream: int = 0,
+            dev_err: int = 0) -> None:
+    """wc_gemm_i8 with raw device pointers: y_i (m x N int32) += x_i (m x K int8)
+    * W_i^T (int8), exactly, in one launch."""
+    n = len(tensors)
+    ts = (C.c_uint32 * max(n, 1))(*tensors)
+    xs = (C.c_void_p * max(n, 1))(*[p or None for p in dev_x])
+    ys = (C.c_void_p * max(n, 1))(*[p or None for p in dev_y])
+    rc = lib().wc_gemm_i8(blob.ptr, C.c_void_p(dev_blob), n, ts, xs, m, ys,
+                          C.c_void_p(stream or None), C.c_void_p(dev_err or None))
+    if rc:
+        raise WcError("wc_gemm_i8", rc)
+
+
 # --- torch plumbing: device memory and streams only ---------------------------
 
 def to_device(blob: Blob, device="cuda"):
@@ -427,4 +445,22 @@ def gemm_torch(blob: Blob, dev_blob, tensors, xs, ys=None, workspace=None, strea
     gemm(blob, dev_blob.data_ptr(), list(tensors), [x.data_ptr() for x in xs], m,
          [y.data_ptr() for y in ys], workspace.data_ptr(), workspace.numel(), stream.cuda_stream,
          err.data_ptr() if err is not None else 0)
+    return ys
+
+
+def gemm_i8_torch(blob: Blob, dev_blob, tensors, xs, ys=None, stream=None, err=None):
+    """wc_gemm_i8 into int32 tensors: ys[i] += xs[i] @ W_i^T for int8 xs and
+    int8 W_i = tensor tensors[i] (ys zeroed and returned if None)."""
+    import torch
+    m = xs[0].shape[0]
+    for x in xs:
+        if x.dtype != torch.int8 or not x.is_contiguous() or x.shape[0] != m:
+            raise ValueError("xs must be contiguous int8 tensors with equal row counts")
+    if ys is None:
+        ys = [torch.zeros((m, int(blob.out_bytes[t] // x.shape[1])), dtype=torch.int32,
+                          device=x.device) for t, x in zip(tensors, xs)]
+    if stream is None:
+        stream = torch.cuda.current_stream(xs[0].device)
+    gemm_i8(blob, dev_blob.data_ptr(), list(tensors), [x.data_ptr() for x in xs], m,
+            [y.data_ptr() for y in ys], stream.cuda_stream, err.data_ptr() if err is not None else 0)
     return ys

@@ -383,3 +383,75 @@ def test_gemm_jobs_sharing_x(dev):
     assert int(err.item()) == 0
     for w, x, y in zip(ws_ + [w2], [x1, x1, x1, x2], ys):
         _check(y.cpu().numpy().astype(np.float64), w, x)
+
+
+# --- int8 weights, int8 x (W8A8): v_mfma_i32_16x16x64_i8, exact int32 --------
+
+def _run_gemm_i8(blob, dev, t, x, expect_err=0):
+    d = wc.to_device(blob, dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ys = wc.gemm_i8_torch(blob, d, [t], [torch.from_numpy(x).to(dev)], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == expect_err, wc.describe_errors(int(err.item()))
+    return ys[0].cpu().numpy().astype(np.int64)
+
+
+@pytest.mark.parametrize("shape,tile", [((64, 256), (16, 64)), ((48, 1024), (16, 256)),
+                                        ((256, 4096), (16, 4096)), ((32, 64), (16, 16)),
+                                        ((16, 2048), (16, 1024))])
+@pytest.mark.parametrize("m", [1, 5, 16, 17, 33, 64])
+def test_int8_gemm_is_exact(dev, shape, tile, m):
+    """Every int32 sum equals the oracle's exact product (tile (16, 16) leaves
+    three quarters of each wave row empty: those lanes contribute zero)."""
+    say("int8 gemm", shape, tile, m)
+    rng = np.random.default_rng(shape[1] + 7 * m)
+    w = rng.integers(-128, 128, shape).astype(np.int8)
+    x = rng.integers(-128, 128, (m, shape[1])).astype(np.int8)
+    blob = wc.encode([("u8", w, shape)], tile=tile, tile_order=1)
+    assert np.array_equal(_run_gemm_i8(blob, dev, 0, x), oracle.gemm_i8(w, x))
+
+
+def test_int8_gemm_quantised_layer(dev):
+    """The int8 projections of the scaled 8B W8 workload (Student-t weights,
+    per-row absmax scales) in 16 x 512 tiles, one launch, 16 rows of x."""
+    ts = [t for t in synth.config(4, div=4) if t.dtype == "u8" and len(t.shape) == 2]
+    assert ts
+    blob = wc.encode([(t.dtype, t.data, t.shape) for t in ts], tile=(16, 512), tile_order=1,
+                     codebook="layer")
+    d = wc.to_device(blob, dev)
+    rng = np.random.default_rng(50)
+    xs = {}
+    for t in ts:
+        xs.setdefault(t.shape[1], rng.integers(-127, 128, (16, t.shape[1])).astype(np.int8))
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ys = wc.gemm_i8_torch(blob, d, list(range(len(ts))),
+                          [torch.from_numpy(xs[t.shape[1]]).to(dev) for t in ts], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    for t, y in zip(ts, ys):
+        rows = np.random.default_rng(t.shape[0]).choice(t.shape[0], 48, replace=False)
+        want = oracle.gemm_i8(np.ascontiguousarray(t.data.view(np.int8).reshape(t.shape)[rows]),
+                             xs[t.shape[1]])
+        assert np.array_equal(y.cpu().numpy().astype(np.int64)[:, rows], want), t.name
+
+
+def test_int8_gemm_adds_and_rejects(dev):
+    rng = np.random.default_rng(51)
+    w = rng.integers(-128, 128, (64, 512)).astype(np.int8)
+    x = rng.integers(-128, 128, (8, 512)).astype(np.int8)
+    blob = wc.encode([("u8", w, (64, 512))], tile=(16, 128), tile_order=1)
+    d = wc.to_device(blob, dev)
+    y0 = torch.from_numpy(oracle.gemm_i8(w, x).astype(np.int32)).to(dev)
+    wc.gemm_i8_torch(blob, d, [0], [torch.from_numpy(x).to(dev)], ys=[y0])   # y += x W^T
+    torch.cuda.synchronize()
+    assert np.array_equal(y0.cpu().numpy().astype(np.int64), 2 * oracle.gemm_i8(w, x))
+    b64 = wc.encode([("u8", w, (64, 512))], tile=(64, 128), tile_order=1)
+    bf = wc.encode([("bf16", w.view(np.uint8).view(np.uint16).reshape(64, 256), (64, 256))],
+                   tile=(16, 128), tile_order=1)
+    for b in (b64, bf):
+        with pytest.raises(wc.WcError) as e:
+            _run_gemm_i8(b, dev, 0, x if b is b64 else x[:, :256])
+        assert e.value.rc == -5
+    with pytest.raises(wc.WcError) as e:
+        _run_gemm_i8(blob, dev, 0, rng.integers(-128, 128, (65, 512)).astype(np.int8))
+    assert e.value.rc == -1
