@@ -15,7 +15,7 @@
  *               an offset index table.
  *   Sec. V-B    offline compression: static frequency table, independent
  *               initial state per tile.
- *   Alg. 2      warp-cooperative rANS decode: slot = state mod 2^b, table
+ *   Alg. 2      lane-parallel rANS decode: slot = state mod 2^b, table
  *               lookup (symbol, freq, cumfreq), state <- f*floor(s/2^b)+slot-c,
  *               renormalise from the interleaved stream.
  *   Sec. VI-F   metadata closed form 4 B * N_tiles + 2^b * 4 B (Table 3).

@@ -2,7 +2,7 @@
 // chunk-parallel rANS encoder, blob assembly and validation.
 //
 // Paper: Sec. II-B (symbols defined by the numeric format, per-tensor
-// empirical entropy), Sec. V-B (offline, tile-addressable compression with a
+// empirical entropy), Sec. V-B (offline compression into independently addressable tiles, with a
 // static table and independently initialised states), Sec. VI-F (b = 12
 // probability bits; an offset entry per independently decodable unit).
 #include <math.h>

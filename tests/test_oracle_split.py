@@ -1,4 +1,4 @@
-"""Pins for the oracle's field split (symbols determined by the numeric format, Sec. II-B).
+"""Pins for the oracle's field split (the storage format fixes the symbols, Sec. II-B).
 
 The split of a 16-bit float word into a coded exponent byte and a raw
 sign|mantissa byte is pinned against IEEE semantics through library routines
