@@ -143,6 +143,31 @@ def test_gemv_reports_corruption(dev):
     assert int(err.item()) & 0x6
 
 
+def test_fused_gemms_on_a_side_stream(dev):
+    """wc_gemv, wc_gemm (shared path) and wc_gemm_i8 issued on a non-default
+    stream, with the inputs made on that stream: every launch, the x packing
+    included, follows the stream's order."""
+    rng = np.random.default_rng(61)
+    w = _bf16(rng.normal(0, 0.02, (128, 1024)))
+    wi = rng.integers(-128, 128, (64, 1024)).astype(np.int8)
+    b16 = wc.encode([("bf16", w, w.shape)], tile=(16, 1024), tile_order=1)
+    b64 = wc.encode([("bf16", w, w.shape)], tile=(64, 512), tile_order=1)
+    bi8 = wc.encode([("u8", wi, wi.shape)], tile=(16, 256), tile_order=1)
+    x16 = _bf16(rng.normal(0, 1.0, (16, 1024)))
+    x100 = _bf16(rng.normal(0, 1.0, (100, 1024)))
+    xi = rng.integers(-128, 128, (16, 1024)).astype(np.int8)
+    side = torch.cuda.Stream(dev)
+    with torch.cuda.stream(side):
+        d16, d64, di8 = wc.to_device(b16, dev), wc.to_device(b64, dev), wc.to_device(bi8, dev)
+        y16 = wc.gemv_torch(b16, d16, [0], [_dev_x(x16, dev)], stream=side)[0]
+        y100 = wc.gemm_torch(b64, d64, [0], [_dev_x(x100, dev)], stream=side)[0]
+        yi = wc.gemm_i8_torch(bi8, di8, [0], [torch.from_numpy(xi).to(dev)], stream=side)[0]
+    side.synchronize()
+    _check(y16.cpu().numpy().astype(np.float64), w, x16)
+    _check(y100.cpu().numpy().astype(np.float64), w, x100)
+    assert np.array_equal(yi.cpu().numpy().astype(np.int64), oracle.gemm_i8(wi, xi))
+
+
 @pytest.mark.parametrize("m", [1, 5, 100])
 def test_gemv_many_jobs_in_one_launch(dev, m):
     """Every projection of a scaled 8B layer in one call; jobs with the same K
