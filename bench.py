@@ -216,6 +216,9 @@ def main() -> int:
     ap.add_argument("--tile", default="", help="ROWSxCOLS 2-D tiles, e.g. 128x256 (default: "
                     "flat chunks of --chunk-bytes)")
     ap.add_argument("--codebook", choices=["tensor", "layer"], default="tensor")
+    ap.add_argument("--nibbles-as-bytes", action="store_true",
+                    help="code 4-bit tensors (int4, fp4 codes) by their packed bytes, two "
+                         "nibbles per symbol, instead of one symbol per nibble")
     ap.add_argument("--sweep", action="store_true",
                     help="one bf16 decoder layer of each model family of the paper (1.5B to "
                          "405B parameters), drawn on the GPU and compressed with the device "
@@ -320,8 +323,13 @@ def main() -> int:
         origs = lambda k: keep_orig[k % n_res]    # noqa: E731
     else:
         tens = synth.config(cfg)
-        host = [(t.dtype, t.data) for t in tens]
-        blob = wc.encode([shaped(t.dtype, t.data, t.shape) for t in tens],
+        # --nibbles-as-bytes: a packed 4-bit tensor becomes a byte tensor of half
+        # the columns (two nibbles per symbol); the decoded bytes are the same
+        nib = lambda t: args.nibbles_as_bytes and t.dtype in ("u4", "fp4_e2m1")  # noqa: E731
+        sym = lambda t: "u8" if nib(t) else t.dtype  # noqa: E731
+        shp = lambda t: (t.shape[0], t.shape[1] // 2) if nib(t) and len(t.shape) == 2 else t.shape  # noqa: E731
+        host = [(sym(t), t.data) for t in tens]
+        blob = wc.encode([shaped(sym(t), t.data, shp(t)) for t in tens],
                          chunk_bytes=args.chunk_bytes, lanes=args.lanes,
                          threads=args.threads, tile=tile, codebook=args.codebook)
         per = blob.size + sum(blob.out_bytes)
@@ -429,6 +437,8 @@ def main() -> int:
         config["tile"] = args.tile
     if args.codebook != "tensor":
         config["codebook"] = args.codebook
+    if args.nibbles_as_bytes:
+        config["symbols"] = "4-bit tensors coded by packed bytes (two nibbles per symbol)"
     if big:
         config["layers_resident"] = n_res
     else:

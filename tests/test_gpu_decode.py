@@ -108,6 +108,19 @@ def test_workloads_scaled(dev, cfg, div, lanes):
     check_exact(pairs, blob, gpu_decode(blob, dev))
 
 
+@pytest.mark.parametrize("cfg", [3, 7, 8])
+def test_nibble_tensors_coded_by_bytes(dev, cfg):
+    """4-bit tensors (int4, MXFP4, AWQ-style codes) coded by their packed bytes,
+    two nibbles per symbol: the host blob equals the oracle's and the GPU decode
+    is bit-exact."""
+    say("nibbles as bytes", cfg)
+    pairs = [("u8" if t.dtype in ("u4", "fp4_e2m1") else t.dtype, t.data)
+             for t in synth.config(cfg, div=8)]
+    blob = wc.encode(pairs)
+    assert blob.tobytes() == oracle.encode(pairs)
+    check_exact(pairs, blob, gpu_decode(blob, dev))
+
+
 def test_oracle_blob_decodes_on_gpu(dev):
     pairs = [(t.dtype, t.data) for t in synth.config(3, div=8)]
     blob = wc.open_blob(oracle.encode(pairs, chunk_bytes=32768))
