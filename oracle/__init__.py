@@ -83,6 +83,10 @@ def lib():
                                     C.c_void_p, C.c_void_p]
         L.orc_gemm_i8.argtypes = [C.c_void_p, C.c_uint64, C.c_uint64, C.c_void_p, C.c_uint32,
                                   C.c_void_p]
+        L.orc_gemv_fp8.argtypes = [C.c_void_p, C.c_uint64, C.c_uint64, C.c_void_p, C.c_uint32,
+                                   C.c_void_p, C.c_void_p]
+        L.orc_e4m3_value.argtypes = [C.c_uint8]
+        L.orc_e4m3_value.restype = C.c_double
         L.orc_free.argtypes = [C.c_void_p]
         L.orc_free.restype = None
         L.orc_blob_tensors.argtypes = [C.c_void_p, C.c_uint64, C.POINTER(C.c_uint32)]
@@ -332,3 +336,24 @@ def gemm_i8(w, x):
     if rc:
         raise OracleError(rc, "gemm_i8")
     return y
+
+
+def e4m3_value(v: int) -> float:
+    """The value of one OCP e4m3 byte (NaN for the two NaN patterns)."""
+    return lib().orc_e4m3_value(v)
+
+
+def gemv_fp8(w, x):
+    """(y, sum |x w|) in fp64: y[m, n] = sum_k x[m, k] * e4m3(w[n, k]) for fp8
+    e4m3 bytes w (rows x cols) and bf16 storage words x (M x cols)."""
+    w = np.ascontiguousarray(w, dtype=np.uint8)
+    x = np.ascontiguousarray(x, dtype=np.uint16)
+    rows, cols = w.shape
+    M = x.shape[0]
+    assert x.shape[1] == cols
+    y = np.empty((M, rows), np.float64)
+    a = np.empty((M, rows), np.float64)
+    rc = lib().orc_gemv_fp8(_ptr(w), rows, cols, _ptr(x), M, _ptr(y), _ptr(a))
+    if rc:
+        raise OracleError(rc, "gemv_fp8")
+    return y, a

@@ -1002,3 +1002,35 @@ int orc_gemm_i8(const int8_t* w, uint64_t rows, uint64_t cols, const int8_t* x, 
     }
   return ORC_OK;
 }
+
+/* ------------------------------------------------------------------------ */
+/* What the fused decode-GEMM computes for fp8 e4m3 weights with bf16         */
+/* activations (an fp8 weight format of Sec. VI-A): y[m][n] = sum_k x[m][k] *  */
+/* e4m3(w[n][k]), in fp64, summed in k order; abs_out as for orc_gemv_bf16.  */
+/* e4m3 (OCP 8-bit float, E4M3): sign, 4 exponent bits with bias 7, 3        */
+/* mantissa bits; exponent 0 is subnormal (m/8 * 2^-6); no infinities; the  */
+/* two patterns with all exponent and mantissa bits set are NaN.             */
+
+double orc_e4m3_value(uint8_t v) {
+  const int s = v >> 7, e = (v >> 3) & 15, m = v & 7;
+  if (e == 15 && m == 7) return NAN;
+  const double mag = e ? ldexp(1.0 + m / 8.0, e - 7) : ldexp(m / 8.0, -6);
+  return s ? -mag : mag;
+}
+
+int orc_gemv_fp8(const uint8_t* w, uint64_t rows, uint64_t cols, const uint16_t* x, uint32_t M,
+                 double* y, double* abs_out) {
+  if (!w || !x || !y || M == 0) return ORC_EINVAL;
+  for (uint32_t m = 0; m < M; m++)
+    for (uint64_t n = 0; n < rows; n++) {
+      double s = 0.0, a = 0.0;
+      for (uint64_t k = 0; k < cols; k++) {
+        double p = bf16_value(x[(uint64_t)m * cols + k]) * orc_e4m3_value(w[n * cols + k]);
+        s += p;
+        a += fabs(p);
+      }
+      y[(uint64_t)m * rows + n] = s;
+      if (abs_out) abs_out[(uint64_t)m * rows + n] = a;
+    }
+  return ORC_OK;
+}

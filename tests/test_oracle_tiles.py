@@ -239,3 +239,49 @@ def test_gemm_i8_reference_brute_force_small():
         want = [[sum(int(x[m, k]) * int(w[n, k]) for k in range(cols)) for n in range(rows)]
                 for m in range(M)]
         assert oracle.gemm_i8(w, x).tolist() == want
+
+
+def test_e4m3_values_match_an_independent_decoder():
+    """Every byte against torch's float8_e4m3fn (an implementation of the same
+    OCP format that shares nothing with the oracle), plus the constants the
+    format fixes: 1.0, 2.0, the largest normal 448, the smallest subnormal
+    2^-9, the smallest normal 2^-6, -0 and the NaN patterns."""
+    torch = pytest.importorskip("torch")
+    ref = torch.arange(256, dtype=torch.uint8).view(torch.float8_e4m3fn).to(torch.float64)
+    for v in range(256):
+        got, want = oracle.e4m3_value(v), float(ref[v])
+        if (v & 0x7F) == 0x7F:
+            assert np.isnan(got) and np.isnan(want)
+        else:
+            assert got == want, (v, got, want)
+    assert [oracle.e4m3_value(v) for v in (0x38, 0x40, 0x7E, 0x01, 0x08)] == \
+        [1.0, 2.0, 448.0, 2.0 ** -9, 2.0 ** -6]
+    assert np.signbit(oracle.e4m3_value(0x80)) and oracle.e4m3_value(0x80) == 0.0
+
+
+def test_gemv_fp8_reference_one_hot_and_small_integers():
+    """One-hot x rows pick e4m3 values; small integers (exact in e4m3 up to 16,
+    in bf16 and in fp64) give an integer product."""
+    rng = np.random.default_rng(18)
+    w = rng.integers(0, 256, (12, 64)).astype(np.uint8)
+    w[(w & 0x7F) == 0x7F] = 0x38
+    ks = [0, 9, 63]
+    x = np.zeros((3, 64), np.float32)
+    for m, k in enumerate(ks):
+        x[m, k] = 1.0
+    y, a = oracle.gemv_fp8(w, _bf16_of(x))
+    for m, k in enumerate(ks):
+        assert y[m].tolist() == [oracle.e4m3_value(int(v)) for v in w[:, k]]
+    # integers 0..16 and their negatives in e4m3
+    codes = {0: 0x00}
+    for v in range(1, 17):
+        e = v.bit_length() - 1
+        m = (v << 3 >> e) & 7
+        codes[v] = ((e + 7) << 3) | m
+        codes[-v] = 0x80 | codes[v]
+    wi = rng.integers(-16, 17, (9, 200))
+    xi = rng.integers(-40, 41, (4, 200))
+    wb = np.vectorize(codes.get)(wi).astype(np.uint8)
+    y, a = oracle.gemv_fp8(wb, _bf16_of(xi.astype(np.float32)))
+    assert np.array_equal(y, (xi @ wi.T).astype(np.float64))
+    assert np.array_equal(a, (np.abs(xi) @ np.abs(wi).T).astype(np.float64))
