@@ -210,10 +210,12 @@ wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_
  * on the fly and never written to memory.  Every job of one tile height runs
  * in one launch.
  *   n        1..32 jobs;
- *   tensors  host array of n tensor indices; each W must be bf16 with a shape
- *            (N = rows, K = cols, 64 * K * 2 bytes below 2 GiB), coded with 64
- *            lanes in column-block tiles (wc_params.tile_order =
- *            WC_TILE_COLUMN_BLOCKS) of 64, 32 or 16 rows.  64-row tiles take
+ *   tensors  host array of n tensor indices; each W must be bf16, or fp8 e4m3
+ *            (WC_FP8_E4M3, converted exactly to bf16 as it is decoded; 16-row
+ *            tiles only), with a shape (N = rows, K = cols, 64 * K * 2 bytes
+ *            below 2 GiB), coded with 64 lanes in column-block tiles
+ *            (wc_params.tile_order = WC_TILE_COLUMN_BLOCKS) of 64, 32 or 16
+ *            rows.  64-row tiles take
  *            the products on the VALU for m <= 5 and on the matrix cores above
  *            (v_mfma_f32_32x32x16_bf16 on pairs of k-blocks, which needs at
  *            least 16 columns per tile); 32-row tiles use
@@ -230,8 +232,8 @@ wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_
  *   stream, dev_err as for wc_decode.
  * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument), or
  * WC_EUNSUPPORTED (a tensor is not a bf16 64-lane column-block tensor of 64,
- * 32 or 16 rows per tile, has 64-row tiles of 8 columns with m > 5, or K is
- * too large). */
+ * 32 or 16 rows per tile or an fp8 e4m3 one of 16 rows, has 64-row tiles of 8
+ * columns with m > 5, or K is too large). */
 wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n, const uint32_t* tensors,
                   const void* const* dev_x, uint32_t m, float* const* dev_y, void* stream,
                   int32_t* dev_err);

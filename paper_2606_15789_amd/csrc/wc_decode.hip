@@ -599,7 +599,8 @@ __device__ void share_idle_wave(const LaunchArgs& a, const DevTensor& T, const S
 // pair go to this wave's slot in LDS instead, and after a workgroup barrier
 // every wave multiplies all decoding waves' operands by its own rows of packed
 // x (see Share).
-template <int G, int L, bool kTiled, int kM = 0, int kMB = 0, int kMR = 16, bool kShare = false>
+template <int G, int L, bool kTiled, int kM = 0, int kMB = 0, int kMR = 16, bool kShare = false,
+          bool kFp8 = false>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
                                               const uint2* __restrict__ tab, uint32_t* ring,
@@ -610,8 +611,10 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
   static_assert(!kMfma || (L == 64 && kTiled && !kGemv &&
                            (G == 2 || (G == 4 && kMR == 16 && !kShare))),
-                "MFMA GEMM: bf16 tiles, or int8 tiles of 16 rows");
-  constexpr bool kInt8 = kMfma && G == 4;   // int8 W and x, int32 sums (W8A8)
+                "MFMA GEMM: bf16 tiles, or int8 / fp8 tiles of 16 rows");
+  static_assert(!kFp8 || (kMfma && G == 4), "fp8 weights: the byte MFMA path");
+  constexpr bool kInt8 = kMfma && G == 4 && !kFp8;  // int8 W and x, int32 sums (W8A8)
+  constexpr bool kFp8W = kMfma && G == 4 && kFp8;   // fp8 e4m3 W as bf16, bf16 x, fp32 sums
   static_assert(kMR == 16 || kMR == 32 || kMR == 64, "MFMA tiles of 16, 32 or 64 rows");
   constexpr int kMM = kMR == 64 ? 32 : kMR;   // x rows per MFMA block
   constexpr int kNB = kMR == 64 ? 2 : 1;      // MFMA output blocks of W rows per tile
@@ -700,7 +703,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   typedef __attribute__((ext_vector_type(8))) __bf16 bf8;
   typedef __attribute__((ext_vector_type(kMM * kMM / 64))) float facc;
   typedef __attribute__((ext_vector_type(4))) unsigned int u4v;
-  constexpr uint32_t kXB = G == 2 ? 2u : 1u;  // bytes of one x element (bf16, int8)
+  constexpr uint32_t kXB = (G == 2 || kFp8) ? 2u : 1u;  // bytes of one x element (bf16, int8)
   // bytes of an x row one wave row covers: 64 lane-groups of W columns over kMR rows
   constexpr uint32_t kRowXBytes = 64u * W / kMR * kXB;
   typedef __attribute__((ext_vector_type(4))) int i32x4;
@@ -710,6 +713,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   u32x4 xs[kShare ? kWaves : 1][kShare ? kMB : 1];  // shared GEMM: A operands of the pair
   uint32_t prev[kMR == 64 ? 4 : 1];             // 64-row tiles: the even row's dwords
   u4v xa[kMfma ? kMB : 1];
+  u4v xa2[kFp8W ? kMB : 1];  // fp8 weights: x columns 8..15 of the lane's 16
   // the x rows (fused GEMM on the matrix cores): a.m rows of K bf16
   const uint32_t K = T.ntc << T.log_tc;  // columns of W = length of an x row
   // (the shared GEMM reads packed x: rows rounded up to blocks of 32)
@@ -753,10 +757,15 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
       // the A operands of this wave row (512 / kMR columns of each x row; for
       // 64-row tiles, of the even row of a pair: 16 columns)
 #pragma unroll
-      for (int mb = 0; mb < kMB; mb++)
+      for (int mb = 0; mb < kMB; mb++) {
         xa[mb] = __builtin_bit_cast(
             u4v, __builtin_amdgcn_raw_buffer_load_b128(xrs, xoff + mb * xblk + r * kRowXBytes,
                                                        0, 0));
+        if constexpr (kFp8W)
+          xa2[mb] = __builtin_bit_cast(
+              u4v, __builtin_amdgcn_raw_buffer_load_b128(
+                       xrs, xoff + mb * xblk + r * kRowXBytes + 16u, 0, 0));
+      }
     }
     const int nv = kTail ? max(0, min<int>(W, (int)n_lane - (int)(r * kRowSym + sub * W))) : W;
 #pragma unroll
@@ -807,6 +816,28 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
             macc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, B0, macc[mb][0], 0, 0, 0);
             macc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, B1, macc[mb][1], 0, 0, 0);
           }
+        }
+        return;
+      }
+      if constexpr (kFp8W) {
+        // 16 e4m3 weights -> 16 bf16 (exact), two B operands of 8: weights 0..7
+        // and 8..15 of the lane-group, against x columns 0..7 and 8..15 of its 16
+        uint32_t bw[8];
+#pragma unroll
+        for (int d = 0; d < 4; d++) {
+          bw[2 * d] = __builtin_bit_cast(
+              uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(ow[d], 1.0f, false));
+          bw[2 * d + 1] = __builtin_bit_cast(
+              uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(ow[d], 1.0f, true));
+        }
+        const bf8 b0 = __builtin_bit_cast(bf8, u4v{bw[0], bw[1], bw[2], bw[3]});
+        const bf8 b1 = __builtin_bit_cast(bf8, u4v{bw[4], bw[5], bw[6], bw[7]});
+#pragma unroll
+        for (int mb = 0; mb < kMB; mb++) {
+          macc[mb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, xa[mb]),
+                                                                b0, macc[mb][0], 0, 0, 0);
+          macc[mb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, xa2[mb]),
+                                                                b1, macc[mb][0], 0, 0, 0);
         }
         return;
       }
@@ -990,8 +1021,9 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
 // wave per tile, y += x * W^T for each tensor's own x and y.  kM > 0: column-
 // block tiles of 64 x tile_c bf16, kM rows of x, dot products on the VALU;
 // kMB > 0: column-block tiles of kMR x tile_c, up to kMR kMB rows of x, MFMA
-// (G = 2: bf16; G = 4: int8 W and x, 16-row tiles, int32 y).
-template <int kM, int kMB, int kMR = 16, int G = 2>
+// (G = 2: bf16; G = 4: int8 W and x, 16-row tiles, int32 y; G = 4 with kFp8:
+// fp8 e4m3 W converted to bf16, bf16 x, 16-row tiles, fp32 y).
+template <int kM, int kMB, int kMR = 16, int G = 2, bool kFp8 = false>
 __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   __shared__ uint2 tab[wc::kTableSize];
   __shared__ uint32_t cum[260];
@@ -1009,7 +1041,7 @@ __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   build_table(a, T, tab, cum, tid);
   __syncthreads();
   if (chunk >= T.n_chunks) return;
-  decode_chunks<G, 64, true, kM, kMB, kMR>(a, T, chunk, lane, tab, ring[wave], pre);
+  decode_chunks<G, 64, true, kM, kMB, kMR, false, kFp8>(a, T, chunk, lane, tab, ring[wave], pre);
 }
 
 // The shared fused GEMM: workgroup = (pass over 256 kXB rows of x, band of 64
@@ -1175,8 +1207,11 @@ wc_status check_jobs(const wc_blob* desc, const void* dev_blob, uint32_t n,
         reinterpret_cast<uintptr_t>(dev_x[i]) % 16)
       return WC_EINVAL;
     const wc::TensorInfo& T = P.tensors[tensors[i]];
-    if (T.dtype != WC_BF16 || T.lanes != 64 || T.tile_order != WC_TILE_COLUMN_BLOCKS ||
+    if (T.lanes != 64 || T.tile_order != WC_TILE_COLUMN_BLOCKS ||
         !(T.tile_r == 64 || T.tile_r == 32 || T.tile_r == 16))
+      return WC_EUNSUPPORTED;
+    // bf16 weights on every tile height; fp8 e4m3 on 16-row tiles (not shared)
+    if (!(T.dtype == WC_BF16 || (T.dtype == WC_FP8_E4M3 && T.tile_r == 16 && !share)))
       return WC_EUNSUPPORTED;
     // 64-row tiles past the dot-product rows pair k-blocks r and r+1 of one
     // tile: at least two k-blocks (16 columns) per tile
@@ -1194,19 +1229,23 @@ wc_status check_jobs(const wc_blob* desc, const void* dev_blob, uint32_t n,
   return WC_OK;
 }
 
-// One launch per tile height (64 rows: VALU dot products up to kDotRows rows
-// of x, MFMA above, or the shared GEMM; 32 or 16 rows: MFMA).  xs: the x (or,
-// for the shared GEMM, packed x) of each job.
+// One launch per tile height and weight type (bf16 on 64 rows: VALU dot
+// products up to kDotRows rows of x, MFMA above, or the shared GEMM; bf16 on
+// 32 or 16 rows: MFMA; fp8 e4m3 on 16 rows: converted to bf16, MFMA).  xs: the
+// x (or, for the shared GEMM, packed x) of each job.
 wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
                       const uint32_t* tensors, const uint64_t* xs, uint32_t m,
                       float* const* dev_y, bool share, hipStream_t st, int32_t* dev_err) {
-  for (uint32_t rows : {64u, 32u, 16u}) {
+  for (uint32_t kind = 0; kind < 4; kind++) {
+    // bf16 weights on 64-, 32- and 16-row tiles, then fp8 weights on 16-row tiles
+    const uint32_t rows = kind == 0 ? 64u : (kind == 1 ? 32u : 16u);
+    const bool fp8 = kind == 3;
     LaunchArgs args{};
     fill_common(args, P, dev_blob, dev_err);
     uint32_t wgs = 0, nt = 0;
     for (uint32_t i = 0; i < n; i++) {
       const wc::TensorInfo& T = P.tensors[tensors[i]];
-      if (T.tile_r != rows) continue;
+      if (T.tile_r != rows || (T.dtype == WC_FP8_E4M3) != fp8) continue;
       fill_tensor(args.t[nt], T, dev_y[i], wgs);
       args.t[nt].x = xs[i];
       if (share) {
@@ -1223,7 +1262,14 @@ wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
     args.n_tensors = nt;
     args.m = m;
     const dim3 grid(wgs), block(kThreads);
-    if (share) {
+    if (fp8) {
+      switch ((m + 15) / 16) {
+        case 1: hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 16, 4, true>), grid, block, 0, st, args); break;
+        case 2: hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 16, 4, true>), grid, block, 0, st, args); break;
+        case 3: hipLaunchKernelGGL((wc_gemv_kernel<0, 3, 16, 4, true>), grid, block, 0, st, args); break;
+        default: hipLaunchKernelGGL((wc_gemv_kernel<0, 4, 16, 4, true>), grid, block, 0, st, args); break;
+      }
+    } else if (share) {
       hipLaunchKernelGGL((wc_gemm_kernel<1>), grid, block, 0, st, args);
     } else if (rows == 64 && m > kDotRows) {
       if (m <= 32) hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 64>), grid, block, 0, st, args);

@@ -175,6 +175,13 @@ class Blob:
     def tobytes(self) -> bytes:
         return C.string_at(self.ptr.contents.data, self.size)
 
+    def shape(self, t: int):
+        """(rows, cols) of tensor t in symbol elements, from its descriptor in
+        the blob header (blob format: 64-byte header, 96-byte descriptors with
+        rows and cols at bytes 64 and 72); (0, 0) for an unshaped tensor."""
+        d = np.frombuffer(self.array()[64 + 96 * t: 64 + 96 * (t + 1)].tobytes(), np.uint64)
+        return int(d[8]), int(d[9])
+
     def payload_bytes(self) -> int:
         """Lane states + words + raw bytes (what the entropy bound is compared with)."""
         d = self.breakdown
@@ -332,8 +339,8 @@ def gemv_torch(blob: Blob, dev_blob, tensors, xs, ys=None, stream=None, err=None
         if x.dtype != torch.bfloat16 or not x.is_contiguous() or x.shape[0] != m:
             raise ValueError("xs must be contiguous bfloat16 tensors with equal row counts")
     if ys is None:
-        ys = [torch.zeros((m, int(blob.out_bytes[t] // 2 // x.shape[1])), dtype=torch.float32,
-                          device=x.device) for t, x in zip(tensors, xs)]
+        ys = [torch.zeros((m, blob.shape(t)[0]), dtype=torch.float32, device=x.device)
+              for t, x in zip(tensors, xs)]
     if stream is None:
         stream = torch.cuda.current_stream(xs[0].device)
     gemv(blob, dev_blob.data_ptr(), list(tensors), [x.data_ptr() for x in xs], m,
@@ -435,8 +442,8 @@ def gemm_torch(blob: Blob, dev_blob, tensors, xs, ys=None, workspace=None, strea
         if x.dtype != torch.bfloat16 or not x.is_contiguous() or x.shape[0] != m:
             raise ValueError("xs must be contiguous bfloat16 tensors with equal row counts")
     if ys is None:
-        ys = [torch.zeros((m, int(blob.out_bytes[t] // 2 // x.shape[1])), dtype=torch.float32,
-                          device=x.device) for t, x in zip(tensors, xs)]
+        ys = [torch.zeros((m, blob.shape(t)[0]), dtype=torch.float32, device=x.device)
+              for t, x in zip(tensors, xs)]
     need = gemm_workspace_bytes(blob, list(tensors), [x.data_ptr() for x in xs], m)
     if workspace is None:
         workspace = torch.empty(max(need, 256), dtype=torch.uint8, device=xs[0].device)
@@ -457,8 +464,8 @@ def gemm_i8_torch(blob: Blob, dev_blob, tensors, xs, ys=None, stream=None, err=N
         if x.dtype != torch.int8 or not x.is_contiguous() or x.shape[0] != m:
             raise ValueError("xs must be contiguous int8 tensors with equal row counts")
     if ys is None:
-        ys = [torch.zeros((m, int(blob.out_bytes[t] // x.shape[1])), dtype=torch.int32,
-                          device=x.device) for t, x in zip(tensors, xs)]
+        ys = [torch.zeros((m, blob.shape(t)[0]), dtype=torch.int32, device=x.device)
+              for t, x in zip(tensors, xs)]
     if stream is None:
         stream = torch.cuda.current_stream(xs[0].device)
     gemm_i8(blob, dev_blob.data_ptr(), list(tensors), [x.data_ptr() for x in xs], m,

@@ -480,3 +480,89 @@ def test_int8_gemm_adds_and_rejects(dev):
     with pytest.raises(wc.WcError) as e:
         _run_gemm_i8(blob, dev, 0, rng.integers(-128, 128, (65, 512)).astype(np.int8))
     assert e.value.rc == -1
+
+
+# --- fp8 e4m3 weights, bf16 x (W8A16): exact conversion, bf16 MFMA ------------
+
+def _fp8_codes(rng, shape):
+    w = rng.integers(0, 256, shape).astype(np.uint8)
+    w[(w & 0x7F) == 0x7F] ^= 0x01          # no NaN patterns
+    return w
+
+
+def _check_fp8(y, w, x):
+    ref, absref = oracle.gemv_fp8(w, x)
+    tol = 2.0 * w.shape[1] * 2.0 ** -24 * absref + 1e-30
+    bad = np.abs(y - ref) > tol
+    assert not bad.any(), (np.argwhere(bad)[:5], float(np.abs(y - ref).max()))
+
+
+@pytest.mark.parametrize("shape,tile", [((64, 256), (16, 64)), ((48, 1024), (16, 256)),
+                                        ((256, 4096), (16, 4096)), ((32, 64), (16, 16))])
+@pytest.mark.parametrize("m", [1, 5, 16, 17, 33, 64])
+def test_fp8_gemv_matches_the_reference(dev, shape, tile, m):
+    """fp8 e4m3 tiles of 16 rows, converted to bf16 while decoded: y within the
+    fp32 summation bound of the oracle's fp64 product (every e4m3 value is a
+    bf16 value, so the conversion adds no error)."""
+    say("fp8 gemv", shape, tile, m)
+    rng = np.random.default_rng(shape[1] + 11 * m)
+    w = _fp8_codes(rng, shape)
+    x = _bf16(rng.normal(0, 1.0, (m, shape[1])))
+    blob = wc.encode([("fp8_e4m3", w, shape)], tile=tile, tile_order=1)
+    _check_fp8(_run_gemv(blob, dev, 0, x), w, x)
+
+
+def test_fp8_gemv_small_integers_exact(dev):
+    """Small integers, exact in e4m3, bf16 and fp32 sums: y equals the integer
+    product, which pins the conversion's byte order and both MFMA halves."""
+    rng = np.random.default_rng(52)
+    codes = {0: 0x00}
+    for v in range(1, 17):
+        e = v.bit_length() - 1
+        codes[v] = ((e + 7) << 3) | ((v << 3 >> e) & 7)
+        codes[-v] = 0x80 | codes[v]
+    wi = rng.integers(-16, 17, (64, 512))
+    xi = rng.integers(-40, 41, (37, 512))
+    w = np.vectorize(codes.get)(wi).astype(np.uint8)
+    blob = wc.encode([("fp8_e4m3", w, w.shape)], tile=(16, 256), tile_order=1)
+    y = _run_gemv(blob, dev, 0, _bf16(xi.astype(np.float32)))
+    assert np.array_equal(y, (xi @ wi.T).astype(np.float64))
+
+
+def test_fp8_gemv_quantised_layer(dev):
+    """The fp8 codes of the scaled 8B fp8 workload (per-row scales stay with the
+    caller) in 16 x 512 tiles, one launch, 16 rows of x: sampled rows of y."""
+    ts = [t for t in synth.config(6, div=4) if t.dtype == "fp8_e4m3" and len(t.shape) == 2]
+    assert ts
+    blob = wc.encode([(t.dtype, t.data, t.shape) for t in ts], tile=(16, 512), tile_order=1)
+    d = wc.to_device(blob, dev)
+    rng = np.random.default_rng(53)
+    xbits = {}
+    for t in ts:
+        xbits.setdefault(t.shape[1], _bf16(rng.normal(0, 1.0, (16, t.shape[1]))))
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ys = wc.gemv_torch(blob, d, list(range(len(ts))), [_dev_x(xbits[t.shape[1]], dev) for t in ts],
+                       err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    for t, y in zip(ts, ys):
+        rows = np.random.default_rng(t.shape[0]).choice(t.shape[0], 32, replace=False)
+        w = np.ascontiguousarray(t.data.reshape(t.shape)[rows])
+        ref, absref = oracle.gemv_fp8(w, xbits[t.shape[1]])
+        tol = 2.0 * t.shape[1] * 2.0 ** -24 * absref + 1e-30
+        assert (np.abs(y.cpu().numpy().astype(np.float64)[:, rows] - ref) <= tol).all(), t.name
+
+
+def test_fp8_gemv_limits(dev):
+    rng = np.random.default_rng(54)
+    w = _fp8_codes(rng, (64, 512))
+    b64 = wc.encode([("fp8_e4m3", w, w.shape)], tile=(64, 256), tile_order=1)
+    b16 = wc.encode([("fp8_e4m3", w, w.shape)], tile=(16, 256), tile_order=1)
+    with pytest.raises(wc.WcError) as e:                 # 64-row fp8 tiles
+        _run_gemv(b64, dev, 0, _bf16(rng.normal(0, 1.0, (4, 512))))
+    assert e.value.rc == -5
+    with pytest.raises(wc.WcError) as e:                 # the shared path is bf16 only
+        _run_gemm(b16, dev, 0, _bf16(rng.normal(0, 1.0, (65, 512))))
+    assert e.value.rc == -5
+    x = _bf16(rng.normal(0, 1.0, (64, 512)))
+    _check_fp8(_run_gemm(b16, dev, 0, x), w, x)          # wc_gemm up to 64 rows is wc_gemv
