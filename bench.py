@@ -239,6 +239,11 @@ def main() -> int:
                          "v_mfma_i32_16x16x64_i8; M rows, 1..64) over the int8 projections of "
                          "the 8B W8 layer in 16 x 2048 tiles, next to the same product unfused "
                          "and uncompressed (torch._int_mm)")
+    ap.add_argument("--gemv-fp8", type=int, default=0, metavar="M",
+                    help="time the fused decode-GEMM on fp8 e4m3 weights (bf16 x, fp32 y; "
+                         "M rows, 1..64) over the fp8 projections of the 8B fp8 layer in "
+                         "16 x 2048 tiles, next to the same product unfused and on the "
+                         "weights kept as bf16")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -260,6 +265,8 @@ def main() -> int:
         return gemv_bench(args, dev)
     if args.gemm_i8:
         return gemm_i8_bench(args, dev)
+    if args.gemv_fp8:
+        return gemv_fp8_bench(args, dev)
     if args.encode:
         return encode_bench(args, dev)
     if args.sweep:
@@ -745,6 +752,118 @@ def gemm_i8_bench(args, dev) -> int:
                             + base_what},
         "uncompressed": {"value": round(wbytes / s_plain / 1e9, 2), "unit": "GB/s",
                          "ms_per_step": round(s_plain * 1e3, 4), "what": base_what},
+        "setup_s": round(setup_s, 1),
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def gemv_fp8_bench(args, dev) -> int:
+    """Fused decode-GEMM over the seven fp8 e4m3 projections of the 8B fp8 layer
+    (bf16 x, fp32 y), checked against torch's fp32 product of the same values."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15789_amd import synth, wc
+    M = args.gemv_fp8
+    if not 1 <= M <= 64:
+        print("--gemv-fp8 takes 1..64 rows of activations", file=sys.stderr)
+        return 2
+    tile = (16, 2048)
+    t0 = time.perf_counter()
+    ts = [t for t in synth.config(6) if t.dtype == "fp8_e4m3" and len(t.shape) == 2]
+    shapes = [t.shape for t in ts]
+    blob = wc.encode([(t.dtype, t.data, t.shape) for t in ts], lanes=64, tile=tile,
+                     tile_order=1, threads=args.threads)
+    dblob = wc.to_device(blob, dev)
+    W8 = [torch.from_numpy(np.ascontiguousarray(t.data).reshape(t.shape)).to(dev) for t in ts]
+    Wb = [w.view(torch.float8_e4m3fn).to(torch.bfloat16) for w in W8]   # exact
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(24680)
+    xs = [torch.randn(M, shp[1], generator=gen, device=dev).to(torch.bfloat16) for shp in shapes]
+    ys = [torch.zeros(M, shp[0], dtype=torch.float32, device=dev) for shp in shapes]
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def fused():
+        wc.gemv(blob, dblob.data_ptr(), list(range(len(ts))), [x.data_ptr() for x in xs], M,
+                [y.data_ptr() for y in ys], stream.cuda_stream, err.data_ptr())
+
+    fused()
+    torch.cuda.synchronize()
+    if int(err.item()):
+        raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
+    for t, (w, x, y) in enumerate(zip(Wb, xs, ys)):
+        ref = x.float() @ w.float().t()
+        bound = x.float().abs() @ w.float().abs().t()
+        if torch.any((y - ref).abs() > w.shape[1] * 2.0 ** -23 * bound + 1e-30):
+            raise RuntimeError(f"fp8 fused GEMM tensor {t} outside the fp32 summation bound")
+    setup_s = time.perf_counter() - t0
+
+    flat = wc.encode([("fp8_e4m3", np.ascontiguousarray(t.data).reshape(-1)) for t in ts],
+                     lanes=64, threads=args.threads)
+    dflat = wc.to_device(flat, dev)
+    outs = [torch.empty(n, dtype=torch.uint8, device=dev) for n in flat.out_bytes]
+
+    def unfused():
+        wc.decode(flat, dflat.data_ptr(), [o.data_ptr() for o in outs], stream.cuda_stream,
+                  err.data_ptr())
+        for o, x, shp in zip(outs, xs, shapes):
+            w = o.view(torch.float8_e4m3fn).view(shp).to(torch.bfloat16)
+            torch.matmul(x, w.t())
+
+    def uncompressed():
+        for w, x in zip(Wb, xs):
+            torch.matmul(x, w.t())
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / args.steps / 1e3
+
+    s_fused, s_unfused, s_plain = timed(fused), timed(unfused), timed(uncompressed)
+    if int(err.item()):
+        raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
+    wbytes = sum(blob.out_bytes)
+    alg = blob.size + sum(x.numel() * 2 for x in xs) + sum(2 * y.numel() * 4 for y in ys)
+    achieved = alg / s_fused / 1e9
+    line = {
+        "metric": METRIC + " [fused fp8 decode-GEMM]",
+        "value": round(wbytes / s_fused / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(s_fused * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp8 e4m3 (as bf16) x bf16 -> fp32",
+        "data": "synthetic",
+        "config": {"workload": "llama3-8b-layer-fp8-e4m3", "mode": "fused-gemv-fp8", "m": M,
+                   "tile": f"{tile[0]}x{tile[1]}", "tile_order": "column-blocks",
+                   "product": "v_cvt_scalef32_pk_bf16_fp8 + v_mfma_f32_16x16x32_bf16",
+                   "lanes": 64, "weight_bytes_per_step": wbytes,
+                   "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "wc_gemv_kernel (fp8)", "mean_step_us": round(s_fused * 1e6, 2),
+                     "algorithmic_bytes_per_step": int(alg)},
+        "unfused": {"value": round(wbytes / s_unfused / 1e9, 2), "unit": "GB/s",
+                    "ms_per_step": round(s_unfused * 1e3, 4),
+                    "what": "wc_decode of the fp8 weights (64 KiB byte-run chunks), torch "
+                            "conversion to bf16, torch.matmul per tensor"},
+        "uncompressed": {"value": round(wbytes / s_plain / 1e9, 2), "unit": "GB/s",
+                         "ms_per_step": round(s_plain * 1e3, 4),
+                         "what": "torch.matmul on the weights kept resident as bf16 (2x the "
+                                 "fp8 bytes)"},
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line), flush=True)
