@@ -10,8 +10,8 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libwc.so")
 SOURCES = [os.path.join(CSRC, "wc_host.cpp"), os.path.join(CSRC, "wc_decode.hip"),
-           os.path.join(CSRC, "wc_encode.hip")]
-HEADERS = [os.path.join(CSRC, "wc_internal.h"),
+           os.path.join(CSRC, "wc_gemm.hip"), os.path.join(CSRC, "wc_encode.hip")]
+HEADERS = [os.path.join(CSRC, "wc_internal.h"), os.path.join(CSRC, "wc_decoder.h"),
            os.path.join(os.path.dirname(HERE), "include", "wc.h")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = os.environ.get("WC_OFFLOAD_ARCH", "gfx950")

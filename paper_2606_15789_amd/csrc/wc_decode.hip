@@ -1,979 +1,9 @@
-// wc_decode.hip -- device half of libwc: chunked rANS decode for CDNA4 (gfx950).
-//
-// Paper: Alg. 2 (lane-parallel rANS tile decode: per-lane state, slot = state
-// mod 2^b, on-chip table lookup of (symbol, freq, cumfreq), state update
-// f * floor(x / 2^b) + slot - cum, renormalisation reads that are coalesced
-// because the lanes' words are interleaved in one stream), Sec. V-C-3, and
-// Sec. IV-A / V-B (independently decodable units located by an offset index).
-//
-// Mapping onto the MI355X:
-//  * a workgroup of kWaves wave64s decodes chunks of one tensor, one rANS lane
-//    per wave lane: a wave decodes one 64-lane chunk, or two adjacent 32-lane
-//    chunks, one per half-wave (each half keeps its own word ring and cursor;
-//    a lane's rank within its half is the wave's mbcnt minus the lower half's
-//    popcount);
-//  * the workgroup shares one 4096-entry decode table in LDS, built from the
-//    tensor's 2^12-normalised frequencies; an entry is {f | symbol << 24,
-//    slot - cum}, so the state update is one v_mad_u32_u24 (the 24-bit multiply
-//    ignores the symbol byte);
-//  * words reach a per-chunk 2 KiB LDS ring through a fixed-rate pipeline: every
-//    four decode steps a chain commits the 256-word unit (8 bytes per lane) it
-//    loaded eight steps earlier and issues one new bounds-checked buffer load
-//    (the next unit, or a load past the record that returns zeros when the ring
-//    is full).  Four steps consume at most 256 words, so the decoder never waits
-//    for a unit, and the fixed load pattern gives the compiler exact vmcnt
-//    waits.  The ring's first 64 words are mirrored past its end, so a lane's
-//    word address is one scalar base plus its rank (two 32-lane chunks per wave move
-//    one dword per lane of a half every two steps);
-//  * renormalisation: ballot of the lanes whose state fell below 2^16, mbcnt
-//    gives each of them its rank, the cursor advances by the popcount -- the
-//    lanes' words are consecutive in the stream;
-//  * a lane-group is 16 decoded bytes: every G steps a lane assembles a dword
-//    (two bf16 rebuilt from their coded and raw bytes with v_perm / v_bfi,
-//    four int8 or eight int4), and every 4G steps it stores the four with one
-//    16-byte non-temporal (streaming) store, so a wave writes a 1 KiB row;
-//  * the raw sign|mantissa bytes of bf16/fp16 rows (8 per lane per row) are
-//    loaded two rows ahead with one 8-byte load per lane.
-// The decode itself uses no MFMA: it is integer table decoding, not a
-// contraction.  The fused decode-GEMM kernels (wc_gemv_kernel, wc_gemm_kernel,
-// Alg. 1 / 3) run the same decoder and feed the decoded bf16 lane-groups to the
-// VALU dot products or to v_mfma_f32_16x16x32_bf16 / v_mfma_f32_32x32x16_bf16
-// operands instead of storing them.
-#include <hip/hip_runtime.h>
+// wc_decode.hip -- wc_decode: one launch decodes every chunk of a blob's
+// tensors into the caller's buffers (Alg. 2; the decoder is in wc_decoder.h).
 
-#include <algorithm>
-#include <utility>
-
-#include "wc_internal.h"
+#include "wc_decoder.h"
 
 namespace {
-
-constexpr int kWaves = 8;                  // waves (chunks) per workgroup
-constexpr int kThreads = kWaves * 64;
-constexpr int kWaveRingWords = 1024;       // words of a wave's ring (2 KiB)
-constexpr int kWaveMirrorWords = 64;       // a ring's first 64 words, mirrored past its end
-constexpr int kPipeSteps = 8;              // decode steps between a unit's load and its commit
-constexpr int kRawRows = 2;                // raw-byte rows in flight (16-bit formats)
-constexpr uint32_t kNoUnit = 0xFFFFFFFFu;
-// Offsets that can fall outside a buffer are always passed as the vector
-// offset, which the hardware range-checks against num_records; the scalar
-// offset carries only offsets that are in range by construction.
-constexpr uint32_t kFarOffset = 0x7FFFFF00u;  // past any record: loads return zeros
-constexpr int kMaxLaunchTensors = 32;
-constexpr int kStreamStore = 2;            // buffer-store cache policy: non-temporal
-
-enum Kind : uint32_t { kSplit16 = 0, kByte = 1, kNibble = 2 };
-
-struct DevTensor {
-  uint64_t dst;          // device pointer of the decoded tensor
-  uint64_t freq_off;     // u16 frequency table (blob offset)
-  uint64_t raw_off;      // raw bytes (blob offset), 16-bit formats only
-  uint64_t n_sym;        // coded symbols in the tensor
-  uint64_t raw_padded;   // bytes of the (16-B padded) raw region
-  uint64_t out_bytes;    // decoded bytes of the tensor
-  uint32_t first_chunk;  // global index of the tensor's first chunk
-  uint32_t n_chunks;
-  uint32_t wg0;          // first workgroup of the tensor in this launch
-  uint32_t per;          // symbols per chunk
-  uint32_t chunk_bytes;  // decoded bytes per full chunk
-  uint32_t kind;
-  uint32_t alphabet;
-  uint32_t lanes;        // rANS lanes per chunk: 64, or 32 (two chunks per wave)
-  uint32_t tiled;        // 1: chunk c is tile (c / ntc, c % ntc) of a row-major matrix
-  uint32_t tile_r;       // tile rows
-  uint32_t log_tc;       // log2 of the tile columns (symbols)
-  uint32_t ntc;          // tiles per band of tile_r rows
-  uint32_t pitch;        // decoded bytes of one matrix row
-  uint32_t tile_row_bytes;  // decoded bytes of one tile row
-  uint32_t order;        // tile order: 0 row-major, 1 column blocks
-  uint32_t log_tr;       // log2 of the tile rows (column-block order)
-  uint64_t x;            // fused GEMM: const bf16 x[M][K]; y[M][N] is float* dst
-};
-
-struct LaunchArgs {
-  uint64_t blob;
-  uint64_t index_off;
-  uint64_t records_off;
-  uint64_t records_end;
-  uint64_t err;          // int32_t* or 0
-  uint32_t n_tensors;
-  uint32_t m;            // fused GEMM: rows of x (and of y) in every job
-  DevTensor t[kMaxLaunchTensors];
-};
-
-constexpr uint32_t wc_ring_words() { return kWaveRingWords + kWaveMirrorWords; }
-
-__device__ __forceinline__ uint64_t dpad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-  // raw buffer: stride 0, num_records in bytes, default data format for gfx9-class parts
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes,
-                                           0x00020000);
-}
-
-__device__ __forceinline__ void report(const LaunchArgs& a, uint32_t bits) {
-  if (a.err && bits) atomicOr(reinterpret_cast<int32_t*>(a.err), (int32_t)bits);
-}
-
-// Decode table of one tensor: slot -> {f | sym << 24, slot - cum_sym}.
-__device__ void build_table(const LaunchArgs& a, const DevTensor& T, uint2* tab, uint32_t* cum,
-                            uint32_t tid) {
-  const uint16_t* fr = reinterpret_cast<const uint16_t*>(a.blob + T.freq_off);
-  if (tid < 64) {
-    uint32_t f[4];
-#pragma unroll
-    for (int k = 0; k < 4; k++) {
-      uint32_t s = tid * 4 + k;
-      f[k] = s < T.alphabet ? fr[s] : 0u;
-    }
-    uint32_t local = f[0] + f[1] + f[2] + f[3];
-    uint32_t incl = local;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
-      uint32_t v = __shfl_up(incl, d, 64);
-      if ((int)tid >= d) incl += v;
-    }
-    uint32_t base = incl - local;
-    cum[tid * 4 + 0] = base;
-    cum[tid * 4 + 1] = base + f[0];
-    cum[tid * 4 + 2] = base + f[0] + f[1];
-    cum[tid * 4 + 3] = base + f[0] + f[1] + f[2];
-    if (tid == 63) {
-      cum[256] = incl;
-      if (incl != wc::kTableSize) report(a, WC_DERR_TABLE);
-    }
-  }
-  __syncthreads();
-  constexpr uint32_t kPer = wc::kTableSize / kThreads;
-  const uint32_t j0 = tid * kPer;
-  uint32_t lo = 0, hi = 256;  // largest s with cum[s] <= j0
-  while (hi - lo > 1) {
-    uint32_t mid = (lo + hi) >> 1;
-    if (cum[mid] <= j0) lo = mid; else hi = mid;
-  }
-  uint32_t s = lo;
-#pragma unroll
-  for (uint32_t j = j0; j < j0 + kPer; j++) {
-    while (s < 255 && cum[s + 1] <= j) s++;
-    uint32_t f = cum[s + 1] - cum[s];
-    tab[j] = make_uint2(f | (s << 24), j - cum[s]);
-  }
-}
-
-// One decoded dword (G symbols) from the table entries' low words (symbol in
-// byte 3) and, for 16-bit formats, its two raw bytes.
-template <int G>
-__device__ __forceinline__ uint32_t assemble(const uint32_t (&lo)[G], uint32_t raw2) {
-  if constexpr (G == 2) {
-    // word = raw bit 7 -> bit 15 | coded byte -> bits 14..7 | raw bits 6..0
-    const uint32_t E = __builtin_amdgcn_perm(lo[1], lo[0], 0x0C070C03u);  // e0 | e1 << 16
-    const uint32_t P = __builtin_amdgcn_perm(0u, raw2, 0x01010000u);       // r0 r0 r1 r1
-    const uint32_t M = 0x807F807Fu;
-    return (P & M) | ((E << 7) & ~M);
-  } else if constexpr (G == 4) {
-    const uint32_t b01 = __builtin_amdgcn_perm(lo[1], lo[0], 0x0C0C0703u);
-    const uint32_t b23 = __builtin_amdgcn_perm(lo[3], lo[2], 0x0C0C0703u);
-    return b01 | (b23 << 16);
-  } else {
-    // nibbles: even symbols gathered into bytes, odd ones shifted in above them
-    const uint32_t e01 = __builtin_amdgcn_perm(lo[2], lo[0], 0x0C0C0703u);
-    const uint32_t e23 = __builtin_amdgcn_perm(lo[6], lo[4], 0x0C0C0703u);
-    const uint32_t o01 = __builtin_amdgcn_perm(lo[3], lo[1], 0x0C0C0703u);
-    const uint32_t o23 = __builtin_amdgcn_perm(lo[7], lo[5], 0x0C0C0703u);
-    return (e01 | (e23 << 16)) | ((o01 | (o23 << 16)) << 4);
-  }
-}
-
-// Everything a wave keeps about the kH chunks it decodes (kH = 64 / L: one
-// 64-lane chunk, or two adjacent 32-lane chunks, one per half-wave).  The
-// chunks' records, raw bytes and outputs are adjacent, so one buffer
-// descriptor spans both and a lane adds its half's base as a vector offset.
-template <int L>
-struct Chain {
-  static constexpr int kH = 64 / L;
-  __amdgpu_buffer_rsrc_t rs;  // the chunks' records
-  __amdgpu_buffer_rsrc_t rr;  // the chunks' raw bytes (16-bit formats)
-  __amdgpu_buffer_rsrc_t os;  // the chunks' decoded bytes
-  uint32_t* ring;             // LDS word rings, one per half (kHalfRing32 u32 each)
-  uint32_t x;                 // this lane's rANS state
-  uint32_t cursor[kH];        // words consumed, per half
-  uint32_t issued[kH];        // units loaded or in flight, per half
-  uint32_t nunits[kH], nw[kH], A[kH], n_c[kH], wbase[kH];
-  uint32_t rec1, raw1, out1;  // half 1's byte offsets within rs / rr / os
-  uint32_t n_exist;           // halves with a chunk
-  bool ok;
-};
-
-// The word pipeline of a wave.  One chunk per wave: a unit is two dwords per
-// lane (256 words), loaded and committed every two groups (four steps, which
-// read at most 256 words).  Two chunks per wave: a unit is one dword per lane
-// of a half (64 words of that half), every group (two steps, at most 64 words
-// of a half).  Either way a unit is committed kPipeSteps steps after its load,
-// and the ring keeps two spare units.
-template <int L>
-struct Shape {
-  static constexpr int kH = 64 / L;
-  static constexpr int kDw = kH == 1 ? 2 : 1;                 // dwords per lane per unit
-  static constexpr int kEvery = kDw;                          // groups per pipeline slot
-  static constexpr uint32_t kUnitWords = 2 * L * kDw;         // words per unit (per half)
-  static constexpr uint32_t kRingWords = kWaveRingWords / kH; // per half
-  static constexpr uint32_t kRingUnits = kRingWords / kUnitWords;
-  static constexpr int kPipe = kPipeSteps / (2 * kEvery);     // slots between load and commit
-  static constexpr uint32_t kMirrorWords = 64 / kH;           // a step reads at most L words
-  // a step's reads run at most 64 / kH words past a half's ring: mirrored
-  static_assert(kH * (kRingWords + kMirrorWords) <= wc_ring_words(), "ring shape");
-  static constexpr uint32_t kHalfRing32 = (kRingWords + kMirrorWords) / 2;
-  static_assert(kPipe >= 1 && kPipe <= int(kRingUnits) - 2, "two spare ring units");
-  static_assert(2 * kEvery * 64 <= kUnitWords * kH, "a slot's steps read at most one unit");
-};
-
-// The index entries of a wave's chunks: g, g + 1 and (two chunks per wave)
-// g + 2, clamped to the tensor's chunks.  Loaded before the table build so
-// that their latency overlaps it.
-struct IndexPre {
-  uint32_t v[3];
-};
-
-__device__ __forceinline__ IndexPre load_index(const LaunchArgs& a, const DevTensor& T,
-                                               uint32_t chunk0, uint32_t per_wave) {
-  IndexPre p{};
-  if (chunk0 < T.n_chunks) {
-    const uint32_t* index = reinterpret_cast<const uint32_t*>(a.blob + a.index_off);
-    const uint32_t g = T.first_chunk + chunk0;
-    const uint32_t n_exist = min<uint32_t>(per_wave, T.n_chunks - chunk0);
-#pragma unroll
-    for (uint32_t h = 0; h < 3; h++)
-      p.v[h] = __builtin_amdgcn_readfirstlane(index[g + min<uint32_t>(h, n_exist)]);
-  }
-  return p;
-}
-
-template <int L>
-__device__ __forceinline__ Chain<L> open_chain(const LaunchArgs& a, const DevTensor& T,
-                                               uint32_t chunk0, uint32_t W, uint32_t lane,
-                                               uint32_t* ring, const IndexPre& pre) {
-  constexpr int kH = Chain<L>::kH;
-  Chain<L> c;
-  const uint8_t* blob = reinterpret_cast<const uint8_t*>(a.blob);
-  c.n_exist = min<uint32_t>(kH, T.n_chunks - chunk0);
-  // per-chunk values are wave-uniform; readfirstlane keeps them (and the
-  // buffer descriptors built from them) in scalar registers
-  uint64_t o[kH + 1];
-#pragma unroll
-  for (int h = 0; h <= kH; h++) o[h] = 16ull * pre.v[h];
-  c.ring = ring;
-  c.ok = true;
-  uint64_t end = o[0];
-#pragma unroll
-  for (int h = 0; h < kH; h++) {
-    c.cursor[h] = c.issued[h] = 0;
-    c.nw[h] = c.nunits[h] = c.wbase[h] = c.A[h] = c.n_c[h] = 0;
-    if ((uint32_t)h >= c.n_exist) continue;
-    const uint64_t s0 = uint64_t(chunk0 + h) * T.per;
-    c.n_c[h] = (uint32_t)min<uint64_t>(T.per, T.n_sym - s0);
-    c.A[h] = min<uint32_t>(L, (c.n_c[h] + W - 1) / W);
-    bool ok = o[h] >= a.records_off && o[h + 1] <= a.records_end && o[h + 1] >= o[h] + 16;
-    if (ok) {
-      const uint32_t* rec = reinterpret_cast<const uint32_t*>(blob + o[h]);
-      c.nw[h] = __builtin_amdgcn_readfirstlane(rec[0]);
-      const uint32_t recA = __builtin_amdgcn_readfirstlane(rec[1]);
-      const uint32_t recN = __builtin_amdgcn_readfirstlane(rec[2]);
-      c.wbase[h] = (uint32_t)(o[h] - o[0]) + 16u + (uint32_t)dpad16(4ull * c.A[h]);
-      ok = recA == c.A[h] && recN == c.n_c[h] &&
-           c.wbase[h] + dpad16(2ull * c.nw[h]) == o[h + 1] - o[0];
-    }
-    c.nunits[h] = ok ? (c.nw[h] + Shape<L>::kUnitWords - 1) / Shape<L>::kUnitWords : 0u;
-    c.ok = c.ok && ok;
-    end = o[h + 1];
-  }
-  c.rs = make_rsrc(blob + o[0], c.ok ? (uint32_t)(end - o[0]) : 0u);
-  c.rec1 = kH == 2 ? (uint32_t)(o[1] - o[0]) : 0u;
-  // lane -> half h, lane within the half
-  const uint32_t h = kH == 2 ? lane / L : 0u;
-  const uint32_t sub = lane % L;
-  const uint32_t A_h = kH == 2 && h ? c.A[kH - 1] : c.A[0];
-  c.x = __builtin_amdgcn_raw_buffer_load_b32(c.rs, (h ? c.rec1 : 0u) + 16u + 4u * sub, 0, 0);
-  if (sub >= A_h) c.x = wc::kStateLow;  // lanes without symbols keep the initial state
-  const uint64_t s0 = uint64_t(chunk0) * T.per;
-  if (T.tiled) {
-    // a tile's bytes start at its band's first row plus its column offset;
-    // the descriptor spans from the first tile's start to the last one's end
-    auto base = [&](uint32_t ch) {
-      return uint64_t(ch / T.ntc) * T.tile_r * T.pitch + uint64_t(ch % T.ntc) * T.tile_row_bytes;
-    };
-    const uint64_t out0 = base(chunk0);
-    c.out1 = c.n_exist == 2 ? (uint32_t)(base(chunk0 + 1) - out0) : 0u;
-    const uint32_t span = c.out1 + (T.tile_r - 1) * T.pitch + T.tile_row_bytes;
-    c.os = make_rsrc(reinterpret_cast<const void*>(T.dst + out0), span);
-  } else {
-    const uint64_t out0 = uint64_t(chunk0) * T.chunk_bytes;
-    const uint32_t out_len =
-        (uint32_t)min<uint64_t>(uint64_t(kH) * T.chunk_bytes, T.out_bytes - out0);
-    c.os = make_rsrc(reinterpret_cast<const void*>(T.dst + out0), out_len);
-    c.out1 = T.chunk_bytes;
-  }
-  const uint32_t raw_len = T.kind == kSplit16
-                               ? (uint32_t)min<uint64_t>(uint64_t(kH) * T.per, T.raw_padded - s0)
-                               : 0u;
-  c.rr = make_rsrc(blob + T.raw_off + s0, raw_len);
-  c.raw1 = T.per;
-  return c;
-}
-
-// Next unit of half h to issue, or kNoUnit when its stream is done or its
-// ring is full.
-template <int L>
-__device__ __forceinline__ uint32_t next_unit(Chain<L>& c, int h) {
-  if (c.issued[h] < c.nunits[h] &&
-      c.issued[h] < c.cursor[h] / Shape<L>::kUnitWords + Shape<L>::kRingUnits)
-    return c.issued[h]++;
-  return kNoUnit;
-}
-
-// The unit load of one pipeline slot, per lane: unit `u` of the lane's half,
-// or (kNoUnit) a load past the records that returns zeros and touches no memory.
-template <int L>
-__device__ __forceinline__ uint32_t load_unit(const Chain<L>& c, uint32_t u, uint32_t wb,
-                                              uint32_t sub) {
-  const uint32_t off = u == kNoUnit ? kFarOffset : wb + u * (4u * L);
-  return __builtin_amdgcn_raw_buffer_load_b32(c.rs, sub * 4u + off, 0, 0);
-}
-
-// One pipeline slot: the unit of each half issued together (one load).
-template <int L>
-struct Slot {
-  uint32_t u;                  // this lane's unit (its half's), or kNoUnit
-  uint32_t v[Shape<L>::kDw];   // the loaded dwords
-};
-
-template <int L>
-__device__ __forceinline__ void commit_unit(const Chain<L>& c, const Slot<L>& s, uint32_t h,
-                                            uint32_t sub) {
-  const uint32_t u = s.u;
-  if (u == kNoUnit) return;
-  const uint32_t slot = u % Shape<L>::kRingUnits;
-  if constexpr (Chain<L>::kH == 1) {
-    // u is wave-uniform here, so both unit tests are scalar branches; the
-    // mirror takes the unit's first 64 words (lanes 0..15), all the reads need
-    uint2* r = reinterpret_cast<uint2*>(c.ring);
-    const uint2 v = make_uint2(s.v[0], s.v[1]);
-    r[slot * L + sub] = v;
-    if (slot == 0 && sub < Shape<L>::kMirrorWords / 4) r[Shape<L>::kRingWords / 4 + sub] = v;
-  } else {
-    uint32_t* r = c.ring + h * Shape<L>::kHalfRing32;
-    r[slot * L + sub] = s.v[0];
-    if (slot == 0 && sub < Shape<L>::kMirrorWords / 2) r[Shape<L>::kRingWords / 2 + sub] = s.v[0];
-  }
-}
-
-template <int L>
-__device__ __forceinline__ Slot<L> issue(Chain<L>& c, uint32_t h, uint32_t sub) {
-  Slot<L> s;
-  if constexpr (Chain<L>::kH == 1) {
-    // wave-uniform, in integer arithmetic (no boolean, which the compiler
-    // would carry as a lane mask): the next unit while the stream has one and
-    // the ring room.  issued <= lim always: both only grow, issued only below lim.
-    using S = Shape<L>;
-    const uint32_t lim = min(c.nunits[0], c.cursor[0] / S::kUnitWords + S::kRingUnits);
-    const uint32_t take = (c.issued[0] - lim) >> 31;  // lim - issued < 2^31
-    const uint32_t none = take - 1u;  // 0, or all ones when nothing is issued
-    s.u = c.issued[0] | none;         // the unit, or kNoUnit
-    // the unit's offset (below 2^31), or one at least kFarOffset: zeros, no access
-    const uint32_t off = (c.wbase[0] + c.issued[0] * (2u * S::kUnitWords)) | (none & kFarOffset);
-    c.issued[0] += take;
-    const uint2 v = __builtin_bit_cast(
-        uint2, __builtin_amdgcn_raw_buffer_load_b64(c.rs, sub * 8u + off, 0, 0));
-    s.v[0] = v.x;
-    s.v[1] = v.y;
-  } else {
-    const uint32_t u0 = next_unit(c, 0), u1 = next_unit(c, 1);
-    s.u = h ? u1 : u0;
-    s.v[0] = load_unit(c, s.u, h ? c.wbase[1] : c.wbase[0], sub);
-  }
-  return s;
-}
-
-// One decode step for the lanes with `active` set; returns the table entry's
-// low word (symbol in byte 3).  Branch-free: every lane reads a word and
-// v_perm either shifts it in or keeps the state, so a group of steps stays
-// one basic block.
-template <bool kAll, int L>
-__device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ tab, bool active,
-                                         uint32_t h) {
-  using S = Shape<L>;
-  const uint2 e = tab[c.x & (wc::kTableSize - 1)];
-  uint32_t xn = __umul24(e.x, c.x >> wc::kProbBits) + e.y;
-  uint32_t lo = e.x;
-  if (!kAll) {
-    xn = active ? xn : c.x;
-    lo = active ? lo : 0u;
-  }
-  const bool need = (kAll || active) && xn < wc::kStateLow;
-  const uint64_t m = __ballot(need);
-  const uint32_t rank =
-      __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-  const uint16_t* words = reinterpret_cast<const uint16_t*>(c.ring);
-  uint32_t idx;
-  if constexpr (Chain<L>::kH == 1) {
-    idx = (c.cursor[0] & (S::kRingWords - 1)) + rank;
-    c.cursor[0] += (uint32_t)__popcll(m);
-  } else {
-    // the upper half's rank counts the lower half's lanes too: subtract them
-    const uint32_t p0 = (uint32_t)__popc((uint32_t)m);
-    const uint32_t b0 = c.cursor[0] & (S::kRingWords - 1);
-    const uint32_t b1 = 2 * S::kHalfRing32 + (c.cursor[1] & (S::kRingWords - 1)) - p0;
-    idx = (h ? b1 : b0) + rank;
-    c.cursor[0] += p0;
-    c.cursor[1] += (uint32_t)__popc((uint32_t)(m >> 32));
-  }
-  const uint32_t w = words[idx];
-  // bytes {w0, w1, x0, x1} = (x << 16) | w, or {x0, x1, x2, x3} = x
-  c.x = __builtin_amdgcn_perm(xn, w, need ? 0x05040100u : 0x07060504u);
-  return lo;
-}
-
-typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(16))) float f32x16;
-
-// The shared fused GEMM, for many rows of x on column-block tiles of 64 rows:
-// the waves of a workgroup decode up to kWaves consecutive tiles of one band
-// of 64 W rows (one tile each), so every weight is decoded once per pass over
-// the rows of x.  After each pair of wave rows a decoding wave leaves its two
-// v_mfma_f32_32x32x16_bf16 B operands (64 W rows x 16 columns) in LDS, and
-// every wave multiplies all of them by its own kXB blocks of 32 x rows.
-struct Share {
-  u32x4* frag;     // LDS [kWaves][2][64]: each wave's B operands of the current pair
-  uint32_t wave;   // this wave's slot
-  uint32_t n_act;  // waves of the workgroup that decode a tile (operands per pair)
-  uint32_t xoff;   // this lane's byte offset in packed x: tile 0, pair 0, x block 0
-  uint32_t xtile;  // packed x bytes between two consecutive tiles
-  uint32_t xblk;   // packed x bytes between blocks of 32 rows
-  uint32_t mrows;  // rows of x from this wave's first (0: none)
-  uint32_t first;  // this wave's first row of x (and of y)
-  uint32_t n0;     // first W row of the band (column of y)
-  uint32_t pairs;  // pairs of wave rows per tile
-  uint64_t N;      // columns of y (rows of W)
-};
-
-// LDS writes of every wave before the barrier are seen by every wave after it;
-// global loads in flight stay in flight.
-__device__ __forceinline__ void lds_barrier() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-  __builtin_amdgcn_s_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-// Packed x: the A operands of v_mfma_f32_32x32x16_bf16 in the order the shared
-// GEMM reads them.  Unit (b, p, l) (16 bytes, at ((b K/16 + p) 64 + l) 16) holds
-// x row 32 b + l mod 32, columns 16 p + 8 (l div 32) .. + 8, zero past row M, so
-// the operand of one block of 32 rows and one pair of wave rows is 1 KiB in a
-// row: one fully used load per lane.
-__global__ __launch_bounds__(256) void pack_x_kernel(const uint16_t* __restrict__ x, uint32_t m,
-                                                    uint32_t K, u32x4* __restrict__ xp,
-                                                    uint64_t units) {
-  const __amdgpu_buffer_rsrc_t xr = make_rsrc(x, m * K * 2u);
-  const uint32_t pairs = K / 16u;
-  for (uint64_t u = uint64_t(blockIdx.x) * blockDim.x + threadIdx.x; u < units;
-       u += uint64_t(gridDim.x) * blockDim.x) {
-    const uint32_t l = uint32_t(u & 63u);
-    const uint64_t bp = u >> 6;
-    const uint32_t p = uint32_t(bp % pairs), b = uint32_t(bp / pairs);
-    const uint32_t row = 32u * b + (l & 31u), col = 16u * p + 8u * (l >> 5);
-    xp[u] = __builtin_bit_cast(
-        u32x4, __builtin_amdgcn_raw_buffer_load_b128(xr, (row * K + col) * 2u, 0, 0));
-  }
-}
-
-// A operands of one pair for every decoding wave's tile, from packed x: lane l
-// holds x row (first + l mod 32), columns 16 pair + 8 (l div 32) .. of the
-// tile; absent tiles and x blocks load nothing.
-template <int kXB>
-__device__ __forceinline__ void share_load_x(const Share& s, __amdgpu_buffer_rsrc_t xrs,
-                                             uint32_t pair, u32x4 (&xs)[kWaves][kXB]) {
-#pragma unroll
-  for (int f = 0; f < kWaves; f++)
-#pragma unroll
-    for (int xb = 0; xb < kXB; xb++) {
-      const bool use = uint32_t(f) < s.n_act && 32u * xb < s.mrows;
-      const uint32_t off = use ? s.xoff + f * s.xtile + xb * s.xblk + pair * 1024u : kFarOffset;
-      xs[f][xb] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(xrs, off, 0, 0));
-    }
-}
-
-// acc[xb][nb] += x block xb times W rows 32 nb .. 32 nb + 31 of every tile's pair
-template <int kXB>
-__device__ __forceinline__ void share_mma(const Share& s, uint32_t lane,
-                                          const u32x4 (&xs)[kWaves][kXB],
-                                          f32x16 (&acc)[kXB][2]) {
-  if (s.mrows == 0) return;  // no rows of x in this pass: no operand to read
-#pragma unroll
-  for (int f = 0; f < kWaves; f++) {
-    if (uint32_t(f) >= s.n_act) break;
-    const bf16x8 b0 = __builtin_bit_cast(bf16x8, s.frag[(2 * f) * 64 + lane]);
-    const bf16x8 b1 = __builtin_bit_cast(bf16x8, s.frag[(2 * f + 1) * 64 + lane]);
-#pragma unroll
-    for (int xb = 0; xb < kXB; xb++) {
-      if (32u * xb >= s.mrows) break;
-      const bf16x8 A = __builtin_bit_cast(bf16x8, xs[f][xb]);
-      acc[xb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, b0, acc[xb][0], 0, 0, 0);
-      acc[xb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, b1, acc[xb][1], 0, 0, 0);
-    }
-  }
-}
-
-// y[first + row][n0 + 32 nb + l mod 32] += acc: lane l holds rows
-// 8 (i div 4) + 4 (l div 32) + i mod 4 of each 32 x 32 block
-template <int kXB>
-__device__ __forceinline__ void share_store(const Share& s, uint32_t lane,
-                                            const f32x16 (&acc)[kXB][2], float* y) {
-#pragma unroll
-  for (int xb = 0; xb < kXB; xb++)
-#pragma unroll
-    for (int nb = 0; nb < 2; nb++)
-#pragma unroll
-      for (int i = 0; i < 16; i++) {
-        const uint32_t row = 32u * xb + 8u * (i >> 2) + 4u * (lane >> 5) + (i & 3);
-        if (row < s.mrows)
-          unsafeAtomicAdd(y + uint64_t(s.first + row) * s.N + s.n0 + 32u * nb + (lane & 31u),
-                          acc[xb][nb][i]);
-      }
-}
-
-// A wave of the workgroup with no tile to decode (or whose tile's index entry
-// is bad): it takes part in every pair's barriers and multiplies the decoding
-// waves' operands by its own rows of x.
-template <int kXB>
-__device__ void share_idle_wave(const LaunchArgs& a, const DevTensor& T, const Share& s,
-                                uint32_t lane) {
-  const uint32_t K = T.ntc << T.log_tc;
-  const __amdgpu_buffer_rsrc_t xrs =
-      make_rsrc(reinterpret_cast<const void*>(T.x), ((a.m + 31u) & ~31u) * K * 2u);
-  f32x16 acc[kXB][2];
-#pragma unroll
-  for (int xb = 0; xb < kXB; xb++) acc[xb][0] = acc[xb][1] = f32x16{};
-  u32x4 xs[kWaves][kXB];
-  for (uint32_t p = 0; p < s.pairs; p++) {
-    share_load_x<kXB>(s, xrs, p, xs);
-    lds_barrier();
-    share_mma<kXB>(s, lane, xs, acc);
-    lds_barrier();
-  }
-  share_store<kXB>(s, lane, acc, reinterpret_cast<float*>(T.dst));
-}
-
-// Decode the chunk(s) of one wave, one rANS lane per wave lane.  G symbols
-// make one output dword; a lane-group is 4G symbols, 16 output bytes, so a
-// lane's share of a row is stored with one 16-byte store.
-//
-// kGemv: instead of storing a row, multiply it into y (the fused decode-GEMM,
-// Alg. 1 / 3).  It needs column-block tiles of 64 rows decoded by 64 lanes:
-// lane l then holds 8 consecutive weights of tile row l in every wave row r
-// (columns b * tile_c + 8 r ..), so each lane accumulates whole dot products
-// of its row with v_dot2_f32_bf16, reading the matching x columns as scalar
-// (wave-uniform) loads, and adds them to y once per tile (fp32 atomics: the
-// tiles of one row band split K).
-//
-// kMB: the fused GEMM on the matrix cores, for up to kMR kMB rows of x.  It
-// needs column-block tiles of kMR (16 or 32) rows decoded by 64 lanes: lane l
-// then holds, in every wave row r, the 8 weights of tile row l mod kMR at
-// columns b * tile_c + (512 / kMR) r + 8 (l div kMR) .., which is exactly the
-// B operand of v_mfma_f32_16x16x32_bf16 (kMR = 16) or
-// v_mfma_f32_32x32x16_bf16 (kMR = 32): B[k][n] = W[n][k], lane l holding
-// column n = l mod kMR, rows 8 (l div kMR) ...  Each lane loads the matching
-// 8 x values of row l mod kMR of every block of kMR x rows (the A operand;
-// rows past M read as zeros through the buffer range check) at the start of
-// the wave row, and every wave row issues one MFMA per x block.  At the end
-// of the tile each lane adds its kMR * kMR / 64 accumulators per block to y
-// (fp32 atomics): lane l holds D[row][l mod kMR] with row = 4 (l div 16) + i
-// (kMR = 16) or 8 (i div 4) + 4 (l div 32) + i mod 4 (kMR = 32).
-//
-// kMR = 64: the same on column-block tiles of 64 rows (the dot-product
-// layout: lane l holds row l, columns 8 r ..).  Two wave rows r, r + 1 hold
-// 64 rows x 16 columns; one v_permlane32_swap per dword turns them into two
-// B operands of v_mfma_f32_32x32x16_bf16 (rows 0..31 and 32..63: lanes 0..31
-// keep row r, lanes 32..63 take row r + 1 of the same W rows), which share
-// one A operand of x, so every x value loaded feeds 64 W rows.
-//
-// kShare (with kMR = 64): the shared fused GEMM.  The two B operands of each
-// pair go to this wave's slot in LDS instead, and after a workgroup barrier
-// every wave multiplies all decoding waves' operands by its own rows of packed
-// x (see Share).
-template <int G, int L, bool kTiled, int kM = 0, int kMB = 0, int kMR = 16, bool kShare = false,
-          bool kFp8 = false>
-__device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
-                                              uint32_t chunk0, uint32_t lane,
-                                              const uint2* __restrict__ tab, uint32_t* ring,
-                                              const IndexPre& pre, const Share* sh = nullptr) {
-  constexpr bool kGemv = kM > 0;   // fused GEMM with kM rows of x, dot products
-  constexpr bool kMfma = kMB > 0;  // fused GEMM with kMB blocks of x rows, MFMA
-  static_assert(!kShare || (kMfma && kMR == 64), "shared fused GEMM: 64-row tiles");
-  static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
-  static_assert(!kMfma || (L == 64 && kTiled && !kGemv &&
-                           (G == 2 || (G == 4 && kMR == 16 && !kShare))),
-                "MFMA GEMM: bf16 tiles, or int8 / fp8 tiles of 16 rows");
-  static_assert(!kFp8 || (kMfma && G == 4), "fp8 weights: the byte MFMA path");
-  constexpr bool kInt8 = kMfma && G == 4 && !kFp8;  // int8 W and x, int32 sums (W8A8)
-  constexpr bool kFp8W = kMfma && G == 4 && kFp8;   // fp8 e4m3 W as bf16, bf16 x, fp32 sums
-  static_assert(kMR == 16 || kMR == 32 || kMR == 64, "MFMA tiles of 16, 32 or 64 rows");
-  constexpr int kMM = kMR == 64 ? 32 : kMR;   // x rows per MFMA block
-  constexpr int kNB = kMR == 64 ? 2 : 1;      // MFMA output blocks of W rows per tile
-  constexpr int kH = Chain<L>::kH;
-  constexpr int W = 4 * G;                    // symbols per lane-group
-  constexpr int kGroupsPerRow = W / 2;        // groups of two steps in a row
-  constexpr int kUnroll = G == 2 ? kGroupsPerRow * kRawRows : kGroupsPerRow;  // groups per body
-  constexpr uint32_t kRowSym = L * W;          // symbols of one half-row
-  constexpr uint32_t kRowBytes = 16u * L;      // decoded bytes of one half-row
-  constexpr uint32_t kRawRowBytes = 8u * L;    // raw bytes of one half-row (16-bit formats)
-  constexpr uint32_t kLogW = G == 2 ? 3 : (G == 4 ? 4 : 5);
-  constexpr int kPipe = Shape<L>::kPipe, kEvery = Shape<L>::kEvery;
-  static_assert(!kMfma || kMR != 64 || kUnroll == 2 * kGroupsPerRow, "row pairs per body");
-  static_assert(kUnroll % (kPipe * kEvery) == 0 && kUnroll % kGroupsPerRow == 0,
-                "pipeline shape");
-
-  Chain<L> c = open_chain<L>(a, T, chunk0, W, lane, ring, pre);
-  if (!c.ok) {
-    if (lane == 0) report(a, WC_DERR_INDEX);
-    if constexpr (kShare) share_idle_wave<kMB>(a, T, *sh, lane);
-    return;
-  }
-  const uint32_t h = kH == 2 ? lane / L : 0u;
-  const uint32_t sub = lane % L;
-  // rows every lane of every half decodes in full, and rows in total
-  uint32_t rows_full = c.n_c[0] / kRowSym, rows = (c.n_c[0] + kRowSym - 1) / kRowSym;
-  if constexpr (kH == 2) {
-    rows_full = min(rows_full, c.n_c[1] / kRowSym);
-    rows = max(rows, (c.n_c[1] + kRowSym - 1) / kRowSym);
-  }
-  const uint32_t n_lane = kH == 2 && h ? c.n_c[kH - 1] : c.n_c[0];  // symbols of this lane's chunk
-  const uint32_t groups = rows * kGroupsPerRow;
-  const uint32_t out_v = (kH == 2 && h ? c.out1 : 0u) + sub * 16u;  // lane's output offset
-  const uint32_t half_v = kH == 2 && h ? c.out1 : 0u;                // tiled: half's base
-  const uint32_t tc_mask = (1u << T.log_tc) - 1u;
-  // output offset (voffset, soffset) of this lane's lane-group in row r: a
-  // byte run, or the lane-group's place in the tile of a row-major matrix
-  auto out_at = [&](uint32_t r, uint32_t& vo, uint32_t& so) {
-    if constexpr (kTiled) {
-      const uint32_t i0 = r * kRowSym + sub * W;
-      if (T.order == 0) {
-        vo = half_v + (i0 >> T.log_tc) * T.pitch + ((i0 & tc_mask) >> kLogW) * 16u;
-      } else {
-        // lane-group g = i0 / W is row g mod tile_r of k-block g div tile_r
-        const uint32_t g = i0 >> kLogW;
-        vo = half_v + (g & ((1u << T.log_tr) - 1u)) * T.pitch + (g >> T.log_tr) * 16u;
-      }
-      so = 0;
-    } else {
-      vo = out_v;
-      so = r * kRowBytes;
-    }
-  };
-  const uint32_t raw_v = (kH == 2 && h ? c.raw1 : 0u) + sub * 8u;   // lane's raw offset
-
-  // prologue: unit 0 committed now, then kPipe units in flight
-  Slot<L> pipe[kPipe];
-  {
-    const Slot<L> s0 = issue(c, h, sub);
-    commit_unit(c, s0, h, sub);
-  }
-#pragma unroll
-  for (int j = 0; j < kPipe; j++) pipe[j] = issue(c, h, sub);
-  __builtin_amdgcn_wave_barrier();
-
-  // raw bytes (8 per lane per row) of the first kRawRows rows (16-bit formats)
-  uint2 rq[G == 2 ? kRawRows : 1];
-  if constexpr (G == 2) {
-#pragma unroll
-    for (int j = 0; j < kRawRows; j++)
-      rq[j] = __builtin_bit_cast(
-          uint2, __builtin_amdgcn_raw_buffer_load_b64(c.rr, j * kRawRowBytes + raw_v, 0, 0));
-  }
-  uint32_t lo[G];   // entries of the dword being assembled
-  uint32_t ow[4];   // the row's four output dwords
-  float acc[kGemv ? kM : 1];
-  // x columns of this tile (fused GEMM), read through the constant address
-  // space: the addresses are wave-uniform, so the loads are scalar
-  typedef __attribute__((address_space(4))) const uint32_t cu32;
-  uint64_t xrow = 0;
-  if constexpr (kGemv) {
-#pragma unroll
-    for (int m = 0; m < kM; m++) acc[m] = 0.0f;
-    xrow = T.x + 2ull * (chunk0 % T.ntc) * (1u << T.log_tc);
-  }
-  typedef __attribute__((ext_vector_type(8))) __bf16 bf8;
-  typedef __attribute__((ext_vector_type(kMM * kMM / 64))) float facc;
-  typedef __attribute__((ext_vector_type(4))) unsigned int u4v;
-  constexpr uint32_t kXB = (G == 2 || kFp8) ? 2u : 1u;  // bytes of one x element (bf16, int8)
-  // bytes of an x row one wave row covers: 64 lane-groups of W columns over kMR rows
-  constexpr uint32_t kRowXBytes = 64u * W / kMR * kXB;
-  typedef __attribute__((ext_vector_type(4))) int i32x4;
-  facc macc[kMfma && !kShare && !kInt8 ? kMB : 1][kNB];
-  i32x4 iacc[kInt8 ? kMB : 1];                   // int8 GEMM: 16 x 16 int32 sums per block
-  f32x16 sacc[kShare ? kMB : 1][2];        // shared GEMM: this wave's x blocks x 64 W rows
-  u32x4 xs[kShare ? kWaves : 1][kShare ? kMB : 1];  // shared GEMM: A operands of the pair
-  uint32_t prev[kMR == 64 ? 4 : 1];             // 64-row tiles: the even row's dwords
-  u4v xa[kMfma ? kMB : 1];
-  u4v xa2[kFp8W ? kMB : 1];  // fp8 weights: x columns 8..15 of the lane's 16
-  // the x rows (fused GEMM on the matrix cores): a.m rows of K bf16
-  const uint32_t K = T.ntc << T.log_tc;  // columns of W = length of an x row
-  // (the shared GEMM reads packed x: rows rounded up to blocks of 32)
-  const __amdgpu_buffer_rsrc_t xrs = make_rsrc(
-      reinterpret_cast<const void*>(T.x),
-      kShare ? ((a.m + 31u) & ~31u) * K * 2u : (kMfma ? a.m * K * kXB : 0u));
-  uint32_t xoff = 0, xblk = 0;
-  if constexpr (kShare) {
-#pragma unroll
-    for (int xb = 0; xb < kMB; xb++) sacc[xb][0] = sacc[xb][1] = f32x16{};
-  } else if constexpr (kMfma) {
-#pragma unroll
-    for (int mb = 0; mb < kMB; mb++) {
-      iacc[kInt8 ? mb : 0] = i32x4{};
-#pragma unroll
-      for (int nb = 0; nb < kNB; nb++) macc[kInt8 ? 0 : mb][nb] = facc{};
-    }
-    // this lane's W x values of wave row 0: row sub mod kMM, columns W (sub div kMM) ..
-    xoff = ((sub % kMM) * K + (chunk0 % T.ntc) * (1u << T.log_tc) + W * (sub / kMM)) * kXB;
-    xblk = kXB * kMM * K;  // bytes of kMM rows of x
-  }
-
-  // group g of the chunk, j = g mod kUnroll (static)
-  auto group = [&](uint32_t g, auto jc, auto tailc) {
-    constexpr int j = decltype(jc)::value;
-    constexpr bool kTail = decltype(tailc)::value;
-    constexpr int k0 = (j % kGroupsPerRow) * 2;  // first step of this group in its lane-group
-    if constexpr (j % kEvery == 0) {
-      // every kEvery groups: commit the unit loaded kPipe slots ago, load the next
-      constexpr int slot = (j / kEvery) % kPipe;
-      commit_unit(c, pipe[slot], h, sub);
-      pipe[slot] = issue(c, h, sub);
-    }
-    __builtin_amdgcn_wave_barrier();
-    const uint32_t r = g / kGroupsPerRow;
-    if constexpr (kShare) {
-      if constexpr (j == 0) share_load_x<kMB>(*sh, xrs, r >> 1, xs);
-    }
-    if constexpr (kMfma && !kShare && j % kGroupsPerRow == 0 &&
-                  (kMR != 64 || j < kGroupsPerRow)) {
-      // the A operands of this wave row (512 / kMR columns of each x row; for
-      // 64-row tiles, of the even row of a pair: 16 columns)
-#pragma unroll
-      for (int mb = 0; mb < kMB; mb++) {
-        xa[mb] = __builtin_bit_cast(
-            u4v, __builtin_amdgcn_raw_buffer_load_b128(xrs, xoff + mb * xblk + r * kRowXBytes,
-                                                       0, 0));
-        if constexpr (kFp8W)
-          xa2[mb] = __builtin_bit_cast(
-              u4v, __builtin_amdgcn_raw_buffer_load_b128(
-                       xrs, xoff + mb * xblk + r * kRowXBytes + 16u, 0, 0));
-      }
-    }
-    const int nv = kTail ? max(0, min<int>(W, (int)n_lane - (int)(r * kRowSym + sub * W))) : W;
-#pragma unroll
-    for (int k = k0; k < k0 + 2; k++) lo[k % G] = step<!kTail, L>(c, tab, k < nv, h);
-    if constexpr ((k0 + 2) % G == 0) {
-      constexpr int d = (k0 + 1) / G;             // the dword these G steps complete
-      uint32_t raw2 = 0;
-      if constexpr (G == 2) {
-        const uint2 rv = rq[(j / kGroupsPerRow) % kRawRows];
-        const uint32_t src = d < 2 ? rv.x : rv.y;
-        raw2 = d & 1 ? src >> 16 : src;
-      }
-      ow[d] = assemble<G>(lo, raw2);
-    }
-    if constexpr (j % kGroupsPerRow == kGroupsPerRow - 1) {
-      if constexpr (G == 2) {
-        rq[(j / kGroupsPerRow) % kRawRows] = __builtin_bit_cast(
-            uint2, __builtin_amdgcn_raw_buffer_load_b64(c.rr, (r + kRawRows) * kRawRowBytes + raw_v,
-                                                        0, 0));
-      }
-      if constexpr (kMfma && kMR == 64) {
-        if constexpr (j < kGroupsPerRow) {
-#pragma unroll
-          for (int d = 0; d < 4; d++) prev[d] = ow[d];  // the even row waits for its pair
-        } else {
-          uint32_t b0[4], b1[4];
-#pragma unroll
-          for (int d = 0; d < 4; d++) {
-            const auto sw = __builtin_amdgcn_permlane32_swap(prev[d], ow[d], false, false);
-            b0[d] = sw[0];  // W rows 0..31: lanes 0..31 row r, lanes 32..63 row r + 1
-            b1[d] = sw[1];  // W rows 32..63
-          }
-          if constexpr (kShare) {
-            // this wave's operands to every wave of the workgroup, then all of them
-            // times this wave's rows of x; the second barrier frees the slots
-            sh->frag[(2 * sh->wave) * 64 + lane] = u32x4{b0[0], b0[1], b0[2], b0[3]};
-            sh->frag[(2 * sh->wave + 1) * 64 + lane] = u32x4{b1[0], b1[1], b1[2], b1[3]};
-            lds_barrier();
-            share_mma<kMB>(*sh, lane, xs, sacc);
-            lds_barrier();
-            return;
-          }
-          const bf8 B0 = __builtin_bit_cast(bf8, u4v{b0[0], b0[1], b0[2], b0[3]});
-          const bf8 B1 = __builtin_bit_cast(bf8, u4v{b1[0], b1[1], b1[2], b1[3]});
-#pragma unroll
-          for (int mb = 0; mb < kMB; mb++) {
-            const bf8 A = __builtin_bit_cast(bf8, xa[mb]);
-            macc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, B0, macc[mb][0], 0, 0, 0);
-            macc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, B1, macc[mb][1], 0, 0, 0);
-          }
-        }
-        return;
-      }
-      if constexpr (kFp8W) {
-        // 16 e4m3 weights -> 16 bf16 (exact), two B operands of 8: weights 0..7
-        // and 8..15 of the lane-group, against x columns 0..7 and 8..15 of its 16
-        uint32_t bw[8];
-#pragma unroll
-        for (int d = 0; d < 4; d++) {
-          bw[2 * d] = __builtin_bit_cast(
-              uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(ow[d], 1.0f, false));
-          bw[2 * d + 1] = __builtin_bit_cast(
-              uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(ow[d], 1.0f, true));
-        }
-        const bf8 b0 = __builtin_bit_cast(bf8, u4v{bw[0], bw[1], bw[2], bw[3]});
-        const bf8 b1 = __builtin_bit_cast(bf8, u4v{bw[4], bw[5], bw[6], bw[7]});
-#pragma unroll
-        for (int mb = 0; mb < kMB; mb++) {
-          macc[mb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, xa[mb]),
-                                                                b0, macc[mb][0], 0, 0, 0);
-          macc[mb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, xa2[mb]),
-                                                                b1, macc[mb][0], 0, 0, 0);
-        }
-        return;
-      }
-      if constexpr (kInt8) {
-        // the lane-group's 16 int8 weights are the B operand as decoded
-        const i32x4 b = {int(ow[0]), int(ow[1]), int(ow[2]), int(ow[3])};
-#pragma unroll
-        for (int mb = 0; mb < kMB; mb++)
-          iacc[mb] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, xa[mb]), b,
-                                                           iacc[mb], 0, 0, 0);
-        return;
-      }
-      if constexpr (kMfma) {
-        const bf8 b = __builtin_bit_cast(bf8, u4v{ow[0], ow[1], ow[2], ow[3]});
-#pragma unroll
-        for (int mb = 0; mb < kMB; mb++) {
-          if constexpr (kMR == 16)
-            macc[mb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf8, xa[mb]),
-                                                                  b, macc[mb][0], 0, 0, 0);
-          else
-            macc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf8, xa[mb]),
-                                                                  b, macc[mb][0], 0, 0, 0);
-        }
-        return;
-      }
-      if constexpr (kGemv) {
-        // this lane: weights [8 r, 8 r + 8) of its tile row; x rows m < M
-        typedef __attribute__((ext_vector_type(2))) __bf16 bf2;
-        uint32_t xv[kM][4];
-#pragma unroll
-        for (int m = 0; m < kM; m++) {
-          cu32* xp = reinterpret_cast<cu32*>(
-              xrow + 2ull * (uint64_t(m) * (T.ntc << T.log_tc) + r * 8u));
-#pragma unroll
-          for (int d = 0; d < 4; d++) xv[m][d] = xp[d];
-        }
-#pragma unroll
-        for (int m = 0; m < kM; m++)
-#pragma unroll
-          for (int d = 0; d < 4; d++)
-            acc[m] = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf2, ow[d]),
-                                                     __builtin_bit_cast(bf2, xv[m][d]), acc[m],
-                                                     false);
-        return;
-      }
-      using v4u = __attribute__((ext_vector_type(4))) unsigned int;
-      const v4u o = {ow[0], ow[1], ow[2], ow[3]};
-      const int nb = nv * 4 / G;  // valid output bytes of this lane
-      uint32_t vo, so;
-      out_at(r, vo, so);
-      if (!kTail || nb == 16) {
-        __builtin_amdgcn_raw_buffer_store_b128(o, c.os, vo, so, kStreamStore);
-      } else {
-#pragma unroll
-        for (int d = 0; d < 4; d++) {
-          if (4 * d + 4 <= nb) {
-            __builtin_amdgcn_raw_buffer_store_b32(ow[d], c.os, vo + 4u * d, so, 0);
-          } else {
-            for (int b = 4 * d; b < nb; b++)
-              __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(ow[d] >> (8 * (b - 4 * d))), c.os,
-                                                   vo + b, so, 0);
-          }
-        }
-      }
-    }
-  };
-
-  const uint32_t groups_full = rows_full * kGroupsPerRow;
-  uint32_t g0 = 0;
-  for (; g0 + kUnroll <= groups_full; g0 += kUnroll) {
-    [&]<int... J>(std::integer_sequence<int, J...>) {
-      (group(g0 + J, std::integral_constant<int, J>{}, std::false_type{}), ...);
-    }(std::make_integer_sequence<int, kUnroll>{});
-  }
-  // the remaining full groups, then the rows some lanes decode only in part
-  // (the last row of a chunk; with two chunks per wave, every row past the
-  // shorter chunk's full rows)
-  for (; g0 < groups; g0 += kUnroll) {
-    [&]<int... J>(std::integer_sequence<int, J...>) {
-      ((g0 + J < groups ? group(g0 + J, std::integral_constant<int, J>{}, std::true_type{})
-                        : void()),
-       ...);
-    }(std::make_integer_sequence<int, kUnroll>{});
-  }
-
-  if constexpr (kGemv) {
-    // tile (band, column) adds its partial dot products to y
-    const uint32_t n = (chunk0 / T.ntc) * 64u + sub;
-    const uint64_t N = uint64_t(T.n_chunks / T.ntc) * 64u;
-    float* y = reinterpret_cast<float*>(T.dst);
-#pragma unroll
-    for (int m = 0; m < kM; m++) unsafeAtomicAdd(y + uint64_t(m) * N + n, acc[m]);
-  }
-  if constexpr (kShare) share_store<kMB>(*sh, lane, sacc, reinterpret_cast<float*>(T.dst));
-  if constexpr (kInt8) {
-    // D[4 (sub div 16) + i][sub mod 16] of every x block, added to int32 y:
-    // integer adds commute, so y is the same whatever order the tiles finish in
-    const uint64_t N = uint64_t(T.n_chunks / T.ntc) * kMR;
-    int* y = reinterpret_cast<int*>(T.dst);
-    const uint32_t n = (chunk0 / T.ntc) * kMR + (sub % 16u);
-#pragma unroll
-    for (int mb = 0; mb < kMB; mb++)
-#pragma unroll
-      for (int i = 0; i < 4; i++) {
-        const uint32_t m = mb * 16u + 4u * (sub >> 4) + i;
-        if (m < a.m) atomicAdd(y + uint64_t(m) * N + n, iacc[mb][i]);
-      }
-  }
-  if constexpr (kMfma && !kShare && !kInt8) {
-    // D[row][sub mod kMM] of every x block and W block: y row, W row = y column
-    const uint64_t N = uint64_t(T.n_chunks / T.ntc) * kMR;
-    float* y = reinterpret_cast<float*>(T.dst);
-#pragma unroll
-    for (int nb = 0; nb < kNB; nb++) {
-      const uint32_t n = (chunk0 / T.ntc) * kMR + nb * kMM + (sub % kMM);
-#pragma unroll
-      for (int mb = 0; mb < kMB; mb++)
-#pragma unroll
-        for (int i = 0; i < kMM * kMM / 64; i++) {
-          const uint32_t row = kMM == 16 ? 4u * (sub >> 4) + i
-                                         : 8u * (i >> 2) + 4u * (sub >> 5) + (i & 3);
-          const uint32_t m = mb * kMM + row;
-          if (m < a.m) unsafeAtomicAdd(y + uint64_t(m) * N + n, macc[mb][nb][i]);
-        }
-    }
-  }
-
-  // --- end-of-chunk checks: every lane back at 2^16, every word consumed ----
-  uint32_t bits = 0;
-  const uint32_t A_h = kH == 2 && h ? c.A[kH - 1] : c.A[0];
-  if (__ballot(sub < A_h && c.x != wc::kStateLow)) bits |= WC_DERR_STATE;
-#pragma unroll
-  for (int k = 0; k < kH; k++)
-    if (c.cursor[k] != c.nw[k]) bits |= WC_DERR_CURSOR;
-  if (lane == 0) report(a, bits);
-}
 
 __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
   __shared__ uint2 tab[wc::kTableSize];
@@ -1017,131 +47,12 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
     by_kind(std::integral_constant<int, 64>{});
 }
 
-// The fused decode-GEMM of up to kMaxLaunchTensors tensors in one launch: one
-// wave per tile, y += x * W^T for each tensor's own x and y.  kM > 0: column-
-// block tiles of 64 x tile_c bf16, kM rows of x, dot products on the VALU;
-// kMB > 0: column-block tiles of kMR x tile_c, up to kMR kMB rows of x, MFMA
-// (G = 2: bf16; G = 4: int8 W and x, 16-row tiles, int32 y; G = 4 with kFp8:
-// fp8 e4m3 W converted to bf16, bf16 x, 16-row tiles, fp32 y).
-template <int kM, int kMB, int kMR = 16, int G = 2, bool kFp8 = false>
-__global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
-  __shared__ uint2 tab[wc::kTableSize];
-  __shared__ uint32_t cum[260];
-  __shared__ uint32_t ring[kWaves][wc_ring_words() / 2];
-  const uint32_t wg = blockIdx.x;
-  uint32_t ti = 0;
-  for (uint32_t k = 1; k < a.n_tensors; k++)
-    if (wg >= a.t[k].wg0) ti = k;
-  const DevTensor& T = a.t[ti];
-  const uint32_t tid = threadIdx.x;
-  const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const uint32_t lane = __lane_id();
-  const uint32_t chunk = (wg - T.wg0) * kWaves + wave;
-  const IndexPre pre = load_index(a, T, chunk, 1u);
-  build_table(a, T, tab, cum, tid);
-  __syncthreads();
-  if (chunk >= T.n_chunks) return;
-  decode_chunks<G, 64, true, kM, kMB, kMR, false, kFp8>(a, T, chunk, lane, tab, ring[wave], pre);
-}
-
-// The shared fused GEMM: workgroup = (pass over 256 kXB rows of x, band of 64
-// W rows, segment of kWaves consecutive tiles of the band); wave w decodes tile
-// w of the segment (when the band has one) and owns x rows 32 kXB w .. of the
-// pass.  Every tile must be full: 64 rows, tile_c columns.  DevTensor::x is the
-// packed x of the job (pack_x_kernel).
-template <int kXB>
-__global__ __launch_bounds__(kThreads) void wc_gemm_kernel(LaunchArgs a) {
-  __shared__ uint2 tab[wc::kTableSize];
-  __shared__ uint32_t cum[260];
-  __shared__ uint32_t ring[kWaves][wc_ring_words() / 2];
-  __shared__ u32x4 frag[kWaves * 2 * 64];
-  const uint32_t wg = blockIdx.x;
-  uint32_t ti = 0;
-  for (uint32_t k = 1; k < a.n_tensors; k++)
-    if (wg >= a.t[k].wg0) ti = k;
-  const DevTensor& T = a.t[ti];
-  const uint32_t tid = threadIdx.x;
-  const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const uint32_t lane = __lane_id();
-  const uint32_t bands = T.n_chunks / T.ntc;
-  const uint32_t segs = (T.ntc + kWaves - 1) / kWaves;
-  const uint32_t local = wg - T.wg0;
-  const uint32_t pass = local / (bands * segs), rest = local % (bands * segs);
-  const uint32_t band = rest / segs, seg = rest % segs;
-  Share s;
-  s.frag = frag;
-  s.wave = wave;
-  s.n_act = min<uint32_t>(kWaves, T.ntc - seg * kWaves);
-  const uint32_t K = T.ntc << T.log_tc;
-  s.first = (pass * kWaves + wave) * 32u * kXB;
-  s.mrows = s.first < a.m ? a.m - s.first : 0u;
-  // packed x: 1 KiB per (block of 32 rows, pair of columns 16 p ..)
-  s.xoff = s.mrows ? ((s.first / 32u) * (K / 16u) * 64u + lane) * 16u +
-                         seg * kWaves * ((1u << T.log_tc) / 16u) * 1024u
-                   : 0u;
-  s.xtile = (1u << T.log_tc) * 64u;
-  s.xblk = K * 64u;
-  s.n0 = band * 64u;
-  s.pairs = (1u << T.log_tc) / 16u;
-  s.N = uint64_t(bands) * 64u;
-  // waves past the band's last tile decode nothing; they index a tile that exists
-  const bool decodes = wave < s.n_act;
-  const uint32_t chunk = band * T.ntc + seg * kWaves + (decodes ? wave : 0u);
-  const IndexPre pre = load_index(a, T, chunk, 1u);
-  build_table(a, T, tab, cum, tid);
-  __syncthreads();
-  if (decodes)
-    decode_chunks<2, 64, true, 0, kXB, 64, true>(a, T, chunk, lane, tab, ring[wave], pre, &s);
-  else
-    share_idle_wave<kXB>(a, T, s, lane);
-}
-
-}  // namespace
-
-namespace {
-
 // A tiled tensor whose widest output descriptor (two tiles of a 32-lane wave)
 // would not fit the 32-bit range the buffer descriptors address.
 bool tile_span_ok(const wc::TensorInfo& T) {
   if (!T.tile_r) return true;
   const uint64_t pitch = T.cols * 16 / T.group;
   return (2 * uint64_t(T.tile_r) + 1) * pitch < (1ull << 31);
-}
-
-void fill_tensor(DevTensor& D, const wc::TensorInfo& T, const void* dst, uint32_t wg0) {
-  D = DevTensor{};
-  D.dst = reinterpret_cast<uint64_t>(dst);
-  D.freq_off = T.freq_off;
-  D.raw_off = T.raw_off;
-  D.n_sym = T.n_sym;
-  D.out_bytes = T.out_bytes;
-  D.raw_padded = wc::has_raw(T.dtype) ? wc::pad16(T.n_sym) : 0;
-  D.first_chunk = (uint32_t)T.first_chunk;
-  D.n_chunks = (uint32_t)T.n_chunks;
-  D.wg0 = wg0;
-  D.per = (uint32_t)T.sym_per_chunk();
-  D.chunk_bytes = T.chunk_bytes;
-  D.kind = wc::is_nibble(T.dtype) ? kNibble : (wc::is_byte(T.dtype) ? kByte : kSplit16);
-  D.alphabet = T.alphabet;
-  D.lanes = T.lanes;
-  D.tiled = T.tile_r ? 1u : 0u;
-  if (D.tiled) {
-    D.tile_r = T.tile_r;
-    D.log_tc = uint32_t(__builtin_ctz(T.tile_c));
-    D.ntc = uint32_t(T.cols / T.tile_c);
-    D.pitch = uint32_t(T.cols * 16 / T.group);
-    D.tile_row_bytes = uint32_t(uint64_t(T.tile_c) * 16 / T.group);
-    D.order = T.tile_order;
-    D.log_tr = T.tile_order == WC_TILE_COLUMN_BLOCKS ? uint32_t(__builtin_ctz(T.tile_r)) : 0u;
-  }
-}
-
-void fill_common(LaunchArgs& args, const wc::BlobPriv& P, const void* dev_blob, int32_t* dev_err) {
-  args.blob = reinterpret_cast<uint64_t>(dev_blob);
-  args.index_off = P.index_off;
-  args.records_off = P.records_off;
-  args.records_end = P.raw_off;
-  args.err = reinterpret_cast<uint64_t>(dev_err);
 }
 
 }  // namespace
@@ -1177,246 +88,4 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
     if (hipGetLastError() != hipSuccess) return WC_EHIP;
   }
   return WC_OK;
-}
-
-// Rows of x up to which 64-row tiles take the VALU dot products; above, the
-// matrix cores (row pairs swapped into 32 x 32 x 16 MFMA operands).
-constexpr uint32_t kDotRows = 5;
-// Rows of x up to which wc_gemm runs wc_gemv's kernels; above, the shared
-// fused GEMM (one decode of every tile per pass of kPassRows x rows) over
-// packed x.  kMaxGemmRows: the most rows of x wc_gemm takes.
-constexpr uint32_t kShareRows = 64;
-constexpr uint32_t kMaxGemmRows = 4096;
-constexpr uint32_t kPassRows = kWaves * 32u;
-
-namespace {
-
-uint64_t pad256(uint64_t v) { return (v + 255) & ~uint64_t(255); }
-
-// Arguments of a fused GEMM call, before anything is launched.  share: the
-// jobs go to the shared fused GEMM (64-row tiles, every tile full).
-wc_status check_jobs(const wc_blob* desc, const void* dev_blob, uint32_t n,
-                     const uint32_t* tensors, const void* const* dev_x, uint32_t m,
-                     float* const* dev_y, bool share) {
-  if (!desc || !desc->priv || !dev_blob || !tensors || !dev_x || !dev_y || n == 0 ||
-      n > kMaxLaunchTensors)
-    return WC_EINVAL;
-  const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
-  for (uint32_t i = 0; i < n; i++) {
-    if (tensors[i] >= desc->n_tensors || !dev_x[i] || !dev_y[i] ||
-        reinterpret_cast<uintptr_t>(dev_x[i]) % 16)
-      return WC_EINVAL;
-    const wc::TensorInfo& T = P.tensors[tensors[i]];
-    if (T.lanes != 64 || T.tile_order != WC_TILE_COLUMN_BLOCKS ||
-        !(T.tile_r == 64 || T.tile_r == 32 || T.tile_r == 16))
-      return WC_EUNSUPPORTED;
-    // bf16 weights on every tile height; fp8 e4m3 on 16-row tiles (not shared)
-    if (!(T.dtype == WC_BF16 || (T.dtype == WC_FP8_E4M3 && T.tile_r == 16 && !share)))
-      return WC_EUNSUPPORTED;
-    // 64-row tiles past the dot-product rows pair k-blocks r and r+1 of one
-    // tile: at least two k-blocks (16 columns) per tile
-    if (T.tile_r == 64 && m > kDotRows && T.tile_c < 16) return WC_EUNSUPPORTED;
-    if (T.rows > 0xFFFFFFFFull || T.cols > 0xFFFFFFFFull) return WC_EUNSUPPORTED;
-    // x offsets of a lane reach 64 rows (4 blocks of 16) of 2 * cols bytes
-    if (64ull * T.cols * 2 > 0x7FFFFFFFull) return WC_EUNSUPPORTED;
-    if (share) {
-      // every wave of a workgroup takes the same number of pairs of wave rows:
-      // 64-row tiles, all full; packed x addressed below kFarOffset
-      if (T.tile_r != 64 || T.rows % 64 || T.cols % T.tile_c) return WC_EUNSUPPORTED;
-      if (uint64_t((m + 31) / 32 * 32) * T.cols * 2 > kFarOffset) return WC_EUNSUPPORTED;
-    }
-  }
-  return WC_OK;
-}
-
-// One launch per tile height and weight type (bf16 on 64 rows: VALU dot
-// products up to kDotRows rows of x, MFMA above, or the shared GEMM; bf16 on
-// 32 or 16 rows: MFMA; fp8 e4m3 on 16 rows: converted to bf16, MFMA).  xs: the
-// x (or, for the shared GEMM, packed x) of each job.
-wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
-                      const uint32_t* tensors, const uint64_t* xs, uint32_t m,
-                      float* const* dev_y, bool share, hipStream_t st, int32_t* dev_err) {
-  for (uint32_t kind = 0; kind < 4; kind++) {
-    // bf16 weights on 64-, 32- and 16-row tiles, then fp8 weights on 16-row tiles
-    const uint32_t rows = kind == 0 ? 64u : (kind == 1 ? 32u : 16u);
-    const bool fp8 = kind == 3;
-    LaunchArgs args{};
-    fill_common(args, P, dev_blob, dev_err);
-    uint32_t wgs = 0, nt = 0;
-    for (uint32_t i = 0; i < n; i++) {
-      const wc::TensorInfo& T = P.tensors[tensors[i]];
-      if (T.tile_r != rows || (T.dtype == WC_FP8_E4M3) != fp8) continue;
-      fill_tensor(args.t[nt], T, dev_y[i], wgs);
-      args.t[nt].x = xs[i];
-      if (share) {
-        // (pass, band, segment of kWaves tiles) per workgroup
-        const uint64_t ntc = T.cols / T.tile_c, bands = T.rows / 64;
-        const uint64_t segs = (ntc + kWaves - 1) / kWaves, passes = (m + kPassRows - 1) / kPassRows;
-        wgs += uint32_t(bands * segs * passes);
-      } else {
-        wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
-      }
-      nt++;
-    }
-    if (!nt) continue;
-    args.n_tensors = nt;
-    args.m = m;
-    const dim3 grid(wgs), block(kThreads);
-    if (fp8) {
-      switch ((m + 15) / 16) {
-        case 1: hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 16, 4, true>), grid, block, 0, st, args); break;
-        case 2: hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 16, 4, true>), grid, block, 0, st, args); break;
-        case 3: hipLaunchKernelGGL((wc_gemv_kernel<0, 3, 16, 4, true>), grid, block, 0, st, args); break;
-        default: hipLaunchKernelGGL((wc_gemv_kernel<0, 4, 16, 4, true>), grid, block, 0, st, args); break;
-      }
-    } else if (share) {
-      hipLaunchKernelGGL((wc_gemm_kernel<1>), grid, block, 0, st, args);
-    } else if (rows == 64 && m > kDotRows) {
-      if (m <= 32) hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 64>), grid, block, 0, st, args);
-      else hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 64>), grid, block, 0, st, args);
-    } else if (rows == 64) {
-      switch (m) {
-        case 1: hipLaunchKernelGGL((wc_gemv_kernel<1, 0>), grid, block, 0, st, args); break;
-        case 2: hipLaunchKernelGGL((wc_gemv_kernel<2, 0>), grid, block, 0, st, args); break;
-        case 3: hipLaunchKernelGGL((wc_gemv_kernel<3, 0>), grid, block, 0, st, args); break;
-        case 4: hipLaunchKernelGGL((wc_gemv_kernel<4, 0>), grid, block, 0, st, args); break;
-        default: hipLaunchKernelGGL((wc_gemv_kernel<5, 0>), grid, block, 0, st, args); break;
-      }
-      static_assert(kDotRows == 5, "one dot-product instance per row count up to kDotRows");
-    } else if (rows == 32) {
-      if (m <= 32) hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 32>), grid, block, 0, st, args);
-      else hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 32>), grid, block, 0, st, args);
-    } else {
-      switch ((m + 15) / 16) {
-        case 1: hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 16>), grid, block, 0, st, args); break;
-        case 2: hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 16>), grid, block, 0, st, args); break;
-        case 3: hipLaunchKernelGGL((wc_gemv_kernel<0, 3, 16>), grid, block, 0, st, args); break;
-        default: hipLaunchKernelGGL((wc_gemv_kernel<0, 4, 16>), grid, block, 0, st, args); break;
-      }
-    }
-    if (hipGetLastError() != hipSuccess) return WC_EHIP;
-  }
-  return WC_OK;
-}
-
-// Packed-x slots of the jobs of a shared GEMM: jobs with the same x (pointer
-// and length) share one slot.  Returns the workspace bytes; slot[i] is job i's
-// byte offset in the workspace.
-uint64_t packed_slots(const wc::BlobPriv& P, uint32_t n, const uint32_t* tensors,
-                      const void* const* dev_x, uint32_t m, uint64_t* slot) {
-  uint64_t total = 0;
-  const uint64_t mpad = (m + 31) / 32 * 32;
-  for (uint32_t i = 0; i < n; i++) {
-    const uint64_t K = P.tensors[tensors[i]].cols;
-    slot[i] = ~uint64_t(0);
-    for (uint32_t j = 0; j < i; j++)
-      if (dev_x[j] == dev_x[i] && P.tensors[tensors[j]].cols == K) slot[i] = slot[j];
-    if (slot[i] == ~uint64_t(0)) {
-      slot[i] = total;
-      total += pad256(mpad * K * 2);
-    }
-  }
-  return total;
-}
-
-}  // namespace
-
-extern "C" wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n,
-                             const uint32_t* tensors, const void* const* dev_x, uint32_t m,
-                             float* const* dev_y, void* stream, int32_t* dev_err) {
-  if (m < 1 || m > 64) return WC_EINVAL;
-  const wc_status rc = check_jobs(desc, dev_blob, n, tensors, dev_x, m, dev_y, false);
-  if (rc != WC_OK) return rc;
-  const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
-  uint64_t xs[kMaxLaunchTensors];
-  for (uint32_t i = 0; i < n; i++) xs[i] = reinterpret_cast<uint64_t>(dev_x[i]);
-  return launch_jobs(P, dev_blob, n, tensors, xs, m, dev_y, false,
-                     reinterpret_cast<hipStream_t>(stream), dev_err);
-}
-
-extern "C" wc_status wc_gemm_i8(const wc_blob* desc, const void* dev_blob, uint32_t n,
-                                const uint32_t* tensors, const void* const* dev_x, uint32_t m,
-                                int32_t* const* dev_y, void* stream, int32_t* dev_err) {
-  if (!desc || !desc->priv || !dev_blob || !tensors || !dev_x || !dev_y || n == 0 ||
-      n > kMaxLaunchTensors || m < 1 || m > 64)
-    return WC_EINVAL;
-  const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
-  LaunchArgs args{};
-  fill_common(args, P, dev_blob, dev_err);
-  uint32_t wgs = 0;
-  for (uint32_t i = 0; i < n; i++) {
-    if (tensors[i] >= desc->n_tensors || !dev_x[i] || !dev_y[i] ||
-        reinterpret_cast<uintptr_t>(dev_x[i]) % 16)
-      return WC_EINVAL;
-    const wc::TensorInfo& T = P.tensors[tensors[i]];
-    if (T.dtype != WC_U8 || T.lanes != 64 || T.tile_order != WC_TILE_COLUMN_BLOCKS ||
-        T.tile_r != 16)
-      return WC_EUNSUPPORTED;
-    // |x w| <= 2^14, so K <= 2^16 keeps every int32 sum below 2^30
-    if (T.cols > 65536 || T.rows > 0xFFFFFFFFull) return WC_EUNSUPPORTED;
-    fill_tensor(args.t[i], T, dev_y[i], wgs);
-    args.t[i].x = reinterpret_cast<uint64_t>(dev_x[i]);
-    wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
-  }
-  args.n_tensors = n;
-  args.m = m;
-  const dim3 grid(wgs), block(kThreads);
-  const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  switch ((m + 15) / 16) {
-    case 1: hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 16, 4>), grid, block, 0, st, args); break;
-    case 2: hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 16, 4>), grid, block, 0, st, args); break;
-    case 3: hipLaunchKernelGGL((wc_gemv_kernel<0, 3, 16, 4>), grid, block, 0, st, args); break;
-    default: hipLaunchKernelGGL((wc_gemv_kernel<0, 4, 16, 4>), grid, block, 0, st, args); break;
-  }
-  return hipGetLastError() == hipSuccess ? WC_OK : WC_EHIP;
-}
-
-extern "C" wc_status wc_gemm_workspace_bytes(const wc_blob* desc, uint32_t n,
-                                             const uint32_t* tensors, const void* const* dev_x,
-                                             uint32_t m, uint64_t* bytes) {
-  if (!bytes) return WC_EINVAL;
-  *bytes = 0;
-  if (!desc || !desc->priv || !tensors || !dev_x || n == 0 || n > kMaxLaunchTensors ||
-      m < 1 || m > kMaxGemmRows)
-    return WC_EINVAL;
-  for (uint32_t i = 0; i < n; i++)
-    if (tensors[i] >= desc->n_tensors) return WC_EINVAL;
-  if (m <= kShareRows) return WC_OK;
-  const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
-  uint64_t slot[kMaxLaunchTensors];
-  *bytes = packed_slots(P, n, tensors, dev_x, m, slot);
-  return WC_OK;
-}
-
-extern "C" wc_status wc_gemm(const wc_blob* desc, const void* dev_blob, uint32_t n,
-                             const uint32_t* tensors, const void* const* dev_x, uint32_t m,
-                             float* const* dev_y, void* dev_workspace, uint64_t workspace_bytes,
-                             void* stream, int32_t* dev_err) {
-  if (m < 1 || m > kMaxGemmRows) return WC_EINVAL;
-  if (m <= kShareRows) return wc_gemv(desc, dev_blob, n, tensors, dev_x, m, dev_y, stream, dev_err);
-  const wc_status rc = check_jobs(desc, dev_blob, n, tensors, dev_x, m, dev_y, true);
-  if (rc != WC_OK) return rc;
-  const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
-  uint64_t slot[kMaxLaunchTensors];
-  const uint64_t need = packed_slots(P, n, tensors, dev_x, m, slot);
-  if (!dev_workspace || reinterpret_cast<uintptr_t>(dev_workspace) % 256 ||
-      workspace_bytes < need)
-    return WC_EINVAL;
-  const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  uint64_t xs[kMaxLaunchTensors];
-  const uint64_t mpad = (m + 31) / 32 * 32;
-  for (uint32_t i = 0; i < n; i++) {
-    const uint64_t K = P.tensors[tensors[i]].cols;
-    xs[i] = reinterpret_cast<uint64_t>(dev_workspace) + slot[i];
-    bool first = true;
-    for (uint32_t j = 0; j < i; j++) first = first && slot[j] != slot[i];
-    if (!first) continue;
-    const uint64_t units = mpad * K / 8;  // 16-byte units
-    const uint32_t blocks = uint32_t(std::min<uint64_t>((units + 255) / 256, 8192));
-    hipLaunchKernelGGL(pack_x_kernel, dim3(blocks), dim3(256), 0, st,
-                       static_cast<const uint16_t*>(dev_x[i]), m, uint32_t(K),
-                       reinterpret_cast<u32x4*>(xs[i]), units);
-    if (hipGetLastError() != hipSuccess) return WC_EHIP;
-  }
-  return launch_jobs(P, dev_blob, n, tensors, xs, m, dev_y, true, st, dev_err);
 }
