@@ -36,7 +36,7 @@ def stale() -> bool:
 # fingerprint they were taken on, so they can tell when that kernel changed,
 # whatever else changed in its source file.
 KERNELS = os.path.join(HERE, "libwc.kernels.json")
-KERNEL_SOURCE = os.path.join(CSRC, "wc_decode.hip")
+KERNEL_SOURCES = [os.path.join(CSRC, "wc_decode.hip"), os.path.join(CSRC, "wc_gemm.hip")]
 
 
 def kernel_fingerprints(asm: str) -> dict:
@@ -64,20 +64,25 @@ def build(verbose: bool = False) -> str:
     tmp = LIB + f".tmp{os.getpid()}"
     cmd = [HIPCC] + FLAGS + SOURCES + ["-o", tmp]
     with tempfile.TemporaryDirectory() as td:
-        asm = os.path.join(td, "wc_decode.s")
-        acmd = ([HIPCC] + [f for f in FLAGS if f not in ("-shared", "-lpthread")] +
-                ["--cuda-device-only", "-S", KERNEL_SOURCE, "-o", asm])
-        ap = subprocess.Popen(acmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)
+        jobs = []
+        for src in KERNEL_SOURCES:
+            asm = os.path.join(td, os.path.basename(src) + ".s")
+            acmd = ([HIPCC] + [f for f in FLAGS if f not in ("-shared", "-lpthread")] +
+                    ["--cuda-device-only", "-S", src, "-o", asm])
+            jobs.append((asm, acmd, subprocess.Popen(acmd, stdout=subprocess.PIPE,
+                                                     stderr=subprocess.PIPE, text=True)))
         res = subprocess.run(cmd, capture_output=True, text=True)
-        aout, aerr = ap.communicate()
         if res.returncode != 0:
             sys.stderr.write(res.stdout + res.stderr)
             raise RuntimeError("libwc build failed: " + " ".join(cmd))
-        if ap.returncode != 0:
-            sys.stderr.write(aout + aerr)
-            raise RuntimeError("kernel assembly failed: " + " ".join(acmd))
-        with open(asm) as fh:
-            prints = kernel_fingerprints(fh.read())
+        prints = {}
+        for asm, acmd, ap in jobs:
+            aout, aerr = ap.communicate()
+            if ap.returncode != 0:
+                sys.stderr.write(aout + aerr)
+                raise RuntimeError("kernel assembly failed: " + " ".join(acmd))
+            with open(asm) as fh:
+                prints.update(kernel_fingerprints(fh.read()))
     if verbose:
         out = "\n".join(l for l in (res.stdout + res.stderr).splitlines()
                         if "packed-fp32-ops" not in l)
