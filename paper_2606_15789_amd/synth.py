@@ -440,6 +440,26 @@ def layer_torch_device(shapes, sigma: float, seed: int, layer: int = 0, device: 
     return out
 
 
+def int8_rows_torch_device(rows: int, cols: int, seed: int, device: str = "cuda",
+                           block_rows: int = 4096):
+    """Per-row symmetric int8 codes of Normal(0, 1) draws on the GPU: scale =
+    absmax(row) / 127, q = round(w / scale), stored as uint8 (two's complement).
+    Row block b is drawn with torch's Philox generator seeded (seed, b).
+    Returns a uint8 device tensor of rows * cols bytes."""
+    import torch
+    out = torch.empty(rows * cols, dtype=torch.uint8, device=device)
+    for b, r0 in enumerate(range(0, rows, block_rows)):
+        r1 = min(rows, r0 + block_rows)
+        g = torch.Generator(device=device)
+        g.manual_seed((seed << 40) | b)
+        w = torch.randn((r1 - r0, cols), generator=g, device=device, dtype=torch.float32)
+        scale = w.abs().amax(dim=1, keepdim=True).clamp_min(1e-30) / 127.0
+        q = torch.round(w / scale).clamp_(-127, 127).to(torch.int8)
+        out[r0 * cols:r1 * cols] = q.view(torch.uint8).reshape(-1)
+        del w, q
+    return out
+
+
 def config_torch_device(cfg: int, layer: int, device: str = "cuda"):
     """70B-layer bf16 tensors drawn on the GPU with torch's device generator.
 

@@ -192,6 +192,53 @@ def test_workloads_full_size(dev, cfg):
     torch.cuda.empty_cache()
 
 
+def test_tensors_past_4_gib(dev):
+    """The largest sizes: one blob of an int8 matrix of 65 541 x 65 533 symbols
+    and a bf16 matrix of 131 073 x 16 384 (4 GiB + 32 KiB): symbol counts and
+    output offsets pass 2^32, the bf16 chunk records straddle 4 GiB of blob and
+    the raw region lies past it, and both tensors end in a partial chunk.  Encoded on the device,
+    decoded on the GPU to the original bytes; sampled chunks (the first, the
+    last, the two around 4 GiB of output, random ones) decoded by the oracle."""
+    say("tensors past 4 GiB")
+    i8 = synth.int8_rows_torch_device(65541, 65533, seed=11, device=dev)
+    bf = synth.layer_torch_device([("w", 131073, 16384)], 0.02, 12, device=dev)[0][1]
+    dents = [("u8", i8), ("bf16", bf)]
+    blob, size = wc.encode_device(dents)
+    torch.cuda.synchronize()
+    n = int(size.item())
+    host = blob[:n].cpu().numpy()
+    desc = wc.open_blob(host)
+    assert list(desc.out_bytes) == [65541 * 65533, 131073 * 32768]
+    info = oracle.tensor_info(host)
+    # header bytes 32 and 48: u64 offsets of the index (record offsets / 16)
+    # and of the raw region; the bf16 tensor's chunks follow the int8 tensor's
+    index, raw = (int(host[o:o + 8].view(np.uint64)[0]) for o in (32, 48))
+    g = info[0]["n_chunks"]
+    first_bf16 = 16 * int(host[index + 4 * g:index + 4 * g + 4].view(np.uint32)[0])
+    assert first_bf16 < 2**32 < raw < n, (first_bf16, raw, n)
+    say("blob bytes", n, "bf16 records from", first_bf16, "raw region from", raw)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    outs = wc.decode_torch(desc, blob, err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    for t, (x, out) in enumerate(zip((i8, bf), outs)):
+        assert torch.equal(out, x), t
+    del outs, blob
+    torch.cuda.empty_cache()
+    rng = np.random.default_rng(12)
+    for t, x in enumerate((i8, bf)):
+        ob, nc = info[t]["out_bytes"], info[t]["n_chunks"]
+        c4 = 2**32 // 65536
+        picks = sorted({0, nc - 1, c4 - 1, c4} | set(int(c) for c in rng.choice(nc, 6, False)))
+        buf = np.zeros(ob, np.uint8)
+        for c in picks:
+            oracle.decode_chunks(host, t, c, c + 1, out=buf)
+            lo, hi = c * 65536, min((c + 1) * 65536, ob)
+            assert np.array_equal(buf[lo:hi], x[lo:hi].cpu().numpy()), (t, c)
+    del i8, bf
+    torch.cuda.empty_cache()
+
+
 def test_round_trip_on_device_only(dev):
     """Encode and decode without the blob leaving the GPU (bar the descriptor)."""
     ts = synth.config(2, div=4)
