@@ -84,9 +84,11 @@ def lib():
         L.orc_gemm_i8.argtypes = [C.c_void_p, C.c_uint64, C.c_uint64, C.c_void_p, C.c_uint32,
                                   C.c_void_p]
         L.orc_gemv_fp8.argtypes = [C.c_void_p, C.c_uint64, C.c_uint64, C.c_void_p, C.c_uint32,
-                                   C.c_void_p, C.c_void_p]
+                                   C.c_uint32, C.c_void_p, C.c_void_p]
         L.orc_e4m3_value.argtypes = [C.c_uint8]
         L.orc_e4m3_value.restype = C.c_double
+        L.orc_e5m2_value.argtypes = [C.c_uint8]
+        L.orc_e5m2_value.restype = C.c_double
         L.orc_free.argtypes = [C.c_void_p]
         L.orc_free.restype = None
         L.orc_blob_tensors.argtypes = [C.c_void_p, C.c_uint64, C.POINTER(C.c_uint32)]
@@ -343,9 +345,18 @@ def e4m3_value(v: int) -> float:
     return lib().orc_e4m3_value(v)
 
 
-def gemv_fp8(w, x):
-    """(y, sum |x w|) in fp64: y[m, n] = sum_k x[m, k] * e4m3(w[n, k]) for fp8
-    e4m3 bytes w (rows x cols) and bf16 storage words x (M x cols)."""
+def e5m2_value(v: int) -> float:
+    """The value of one OCP e5m2 byte (+-inf, NaN for the exponent-31 patterns)."""
+    return lib().orc_e5m2_value(v)
+
+
+FP8_FORMATS = {"e4m3": 0, "e5m2": 1}
+
+
+def gemv_fp8(w, x, fmt: str = "e4m3"):
+    """(y, sum |x w|) in fp64: y[m, n] = sum_k x[m, k] * fp8(w[n, k]) for fp8
+    bytes w (rows x cols) of format `fmt` ("e4m3" or "e5m2") and bf16 storage
+    words x (M x cols)."""
     w = np.ascontiguousarray(w, dtype=np.uint8)
     x = np.ascontiguousarray(x, dtype=np.uint16)
     rows, cols = w.shape
@@ -353,7 +364,7 @@ def gemv_fp8(w, x):
     assert x.shape[1] == cols
     y = np.empty((M, rows), np.float64)
     a = np.empty((M, rows), np.float64)
-    rc = lib().orc_gemv_fp8(_ptr(w), rows, cols, _ptr(x), M, _ptr(y), _ptr(a))
+    rc = lib().orc_gemv_fp8(_ptr(w), rows, cols, _ptr(x), M, FP8_FORMATS[fmt], _ptr(y), _ptr(a))
     if rc:
         raise OracleError(rc, "gemv_fp8")
     return y, a

@@ -1004,12 +1004,15 @@ int orc_gemm_i8(const int8_t* w, uint64_t rows, uint64_t cols, const int8_t* x, 
 }
 
 /* ------------------------------------------------------------------------ */
-/* What the fused decode-GEMM computes for fp8 e4m3 weights with bf16         */
-/* activations (an fp8 weight format of Sec. VI-A): y[m][n] = sum_k x[m][k] *  */
-/* e4m3(w[n][k]), in fp64, summed in k order; abs_out as for orc_gemv_bf16.  */
+/* What the fused decode-GEMM computes for fp8 weights with bf16 activations */
+/* (the fp8 weight formats of Sec. VI-A): y[m][n] = sum_k x[m][k] *          */
+/* fp8(w[n][k]), in fp64, summed in k order; abs_out as for orc_gemv_bf16.   */
 /* e4m3 (OCP 8-bit float, E4M3): sign, 4 exponent bits with bias 7, 3        */
 /* mantissa bits; exponent 0 is subnormal (m/8 * 2^-6); no infinities; the  */
 /* two patterns with all exponent and mantissa bits set are NaN.             */
+/* e5m2 (OCP 8-bit float, E5M2, the paper's FP8-E5M2): sign, 5 exponent bits */
+/* with bias 15, 2 mantissa bits; exponent 0 is subnormal (m/4 * 2^-14);     */
+/* exponent 31 is infinity (mantissa 0) or NaN (mantissa not 0).             */
 
 double orc_e4m3_value(uint8_t v) {
   const int s = v >> 7, e = (v >> 3) & 15, m = v & 7;
@@ -1018,14 +1021,25 @@ double orc_e4m3_value(uint8_t v) {
   return s ? -mag : mag;
 }
 
+double orc_e5m2_value(uint8_t v) {
+  const int s = v >> 7, e = (v >> 2) & 31, m = v & 3;
+  double mag;
+  if (e == 31) mag = m ? NAN : INFINITY;
+  else mag = e ? ldexp(1.0 + m / 4.0, e - 15) : ldexp(m / 4.0, -14);
+  return s ? -mag : mag;
+}
+
+/* fmt: 0 = e4m3, 1 = e5m2 */
 int orc_gemv_fp8(const uint8_t* w, uint64_t rows, uint64_t cols, const uint16_t* x, uint32_t M,
-                 double* y, double* abs_out) {
-  if (!w || !x || !y || M == 0) return ORC_EINVAL;
+                 uint32_t fmt, double* y, double* abs_out) {
+  if (!w || !x || !y || M == 0 || fmt > 1) return ORC_EINVAL;
   for (uint32_t m = 0; m < M; m++)
     for (uint64_t n = 0; n < rows; n++) {
       double s = 0.0, a = 0.0;
       for (uint64_t k = 0; k < cols; k++) {
-        double p = bf16_value(x[(uint64_t)m * cols + k]) * orc_e4m3_value(w[n * cols + k]);
+        const uint8_t c = w[n * cols + k];
+        double p = bf16_value(x[(uint64_t)m * cols + k]) *
+                   (fmt ? orc_e5m2_value(c) : orc_e4m3_value(c));
         s += p;
         a += fabs(p);
       }

@@ -259,29 +259,60 @@ def test_e4m3_values_match_an_independent_decoder():
     assert np.signbit(oracle.e4m3_value(0x80)) and oracle.e4m3_value(0x80) == 0.0
 
 
-def test_gemv_fp8_reference_one_hot_and_small_integers():
-    """One-hot x rows pick e4m3 values; small integers (exact in e4m3 up to 16,
-    in bf16 and in fp64) give an integer product."""
+def test_e5m2_values_match_an_independent_decoder():
+    """Every byte against torch's float8_e5m2 (the same OCP format, an
+    implementation that shares nothing with the oracle), plus the constants
+    the format fixes: 1.0, 2.0, 3.0, the largest normal 57344, the smallest
+    subnormal 2^-16, the smallest normal 2^-14, -0, the infinities and NaN."""
+    torch = pytest.importorskip("torch")
+    ref = torch.arange(256, dtype=torch.uint8).view(torch.float8_e5m2).to(torch.float64)
+    for v in range(256):
+        got, want = oracle.e5m2_value(v), float(ref[v])
+        if (v & 0x7C) == 0x7C and (v & 3):
+            assert np.isnan(got) and np.isnan(want)
+        else:
+            assert got == want, (v, got, want)
+    assert [oracle.e5m2_value(v) for v in (0x3C, 0x40, 0x42, 0x7B, 0x01, 0x04)] == \
+        [1.0, 2.0, 3.0, 57344.0, 2.0 ** -16, 2.0 ** -14]
+    assert oracle.e5m2_value(0x7C) == np.inf and oracle.e5m2_value(0xFC) == -np.inf
+    assert np.signbit(oracle.e5m2_value(0x80)) and oracle.e5m2_value(0x80) == 0.0
+
+
+def _fp8_int_codes(fmt):
+    """Codes of the integers a format holds exactly: -16..16 in e4m3 (3
+    mantissa bits), -8..8 in e5m2 (2 bits), from sign, exponent and mantissa."""
+    mbits, bias, top = (3, 7, 16) if fmt == "e4m3" else (2, 15, 8)
+    codes = {0: 0x00}
+    for v in range(1, top + 1):
+        e = v.bit_length() - 1
+        m = (v << mbits >> e) & ((1 << mbits) - 1)
+        codes[v] = ((e + bias) << mbits) | m
+        codes[-v] = 0x80 | codes[v]
+    return codes, top
+
+
+@pytest.mark.parametrize("fmt", ["e4m3", "e5m2"])
+def test_gemv_fp8_reference_one_hot_and_small_integers(fmt):
+    """One-hot x rows pick fp8 values; small integers (exact in the format, in
+    bf16 and in fp64) give an integer product."""
+    value = oracle.e4m3_value if fmt == "e4m3" else oracle.e5m2_value
     rng = np.random.default_rng(18)
     w = rng.integers(0, 256, (12, 64)).astype(np.uint8)
-    w[(w & 0x7F) == 0x7F] = 0x38
+    special = (w & 0x7F) == 0x7F if fmt == "e4m3" else (w & 0x7C) == 0x7C
+    w[special] = 0x38
     ks = [0, 9, 63]
     x = np.zeros((3, 64), np.float32)
     for m, k in enumerate(ks):
         x[m, k] = 1.0
-    y, a = oracle.gemv_fp8(w, _bf16_of(x))
+    y, a = oracle.gemv_fp8(w, _bf16_of(x), fmt)
     for m, k in enumerate(ks):
-        assert y[m].tolist() == [oracle.e4m3_value(int(v)) for v in w[:, k]]
-    # integers 0..16 and their negatives in e4m3
-    codes = {0: 0x00}
-    for v in range(1, 17):
-        e = v.bit_length() - 1
-        m = (v << 3 >> e) & 7
-        codes[v] = ((e + 7) << 3) | m
-        codes[-v] = 0x80 | codes[v]
-    wi = rng.integers(-16, 17, (9, 200))
+        assert y[m].tolist() == [value(int(v)) for v in w[:, k]]
+    codes, top = _fp8_int_codes(fmt)
+    for v, c in codes.items():
+        assert value(c) == v
+    wi = rng.integers(-top, top + 1, (9, 200))
     xi = rng.integers(-40, 41, (4, 200))
     wb = np.vectorize(codes.get)(wi).astype(np.uint8)
-    y, a = oracle.gemv_fp8(wb, _bf16_of(xi.astype(np.float32)))
+    y, a = oracle.gemv_fp8(wb, _bf16_of(xi.astype(np.float32)), fmt)
     assert np.array_equal(y, (xi @ wi.T).astype(np.float64))
     assert np.array_equal(a, (np.abs(xi) @ np.abs(wi).T).astype(np.float64))
