@@ -53,7 +53,7 @@ WORKLOAD_DEFAULT = "llama3-70b-layer-bf16"
 WORKLOADS = {WORKLOAD_DEFAULT: 5, "bf16-matrix-4096": 1, "llama3-8b-layer-bf16": 2,
              "llama3-8b-layer-int4": 3, "llama3-8b-layer-int8": 4,
              "llama3-8b-layer-fp8-e4m3": 6, "llama3-8b-layer-mxfp4": 7,
-             "llama3-8b-layer-awq4": 8}
+             "llama3-8b-layer-awq4": 8, "llama3-8b-layer-fp8-e5m2": 9}
 ROTATE_BYTES = 1 << 30   # resident bytes the small workloads rotate over
 
 # HBM bytes per launch of the 70B-layer decode from rocprofv3 --pmc FETCH_SIZE and
@@ -240,10 +240,13 @@ def main() -> int:
                          "the 8B W8 layer in 16 x 2048 tiles, next to the same product unfused "
                          "and uncompressed (torch._int_mm)")
     ap.add_argument("--gemv-fp8", type=int, default=0, metavar="M",
-                    help="time the fused decode-GEMM on fp8 e4m3 weights (bf16 x, fp32 y; "
+                    help="time the fused decode-GEMM on fp8 weights (bf16 x, fp32 y; "
                          "M rows, 1..64) over the fp8 projections of the 8B fp8 layer in "
                          "16 x 2048 tiles, next to the same product unfused and on the "
                          "weights kept as bf16")
+    ap.add_argument("--fp8-format", choices=["e4m3", "e5m2"], default="e4m3",
+                    help="fp8 format of --gemv-fp8 (the llama3-8b-layer-fp8-e4m3 or "
+                         "-fp8-e5m2 workload)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
@@ -759,8 +762,9 @@ def gemm_i8_bench(args, dev) -> int:
 
 
 def gemv_fp8_bench(args, dev) -> int:
-    """Fused decode-GEMM over the seven fp8 e4m3 projections of the 8B fp8 layer
-    (bf16 x, fp32 y), checked against torch's fp32 product of the same values."""
+    """Fused decode-GEMM over the seven fp8 (e4m3 or e5m2) projections of the 8B
+    fp8 layer (bf16 x, fp32 y), checked against torch's fp32 product of the
+    same values."""
     import numpy as np
     import torch
 
@@ -769,15 +773,19 @@ def gemv_fp8_bench(args, dev) -> int:
     if not 1 <= M <= 64:
         print("--gemv-fp8 takes 1..64 rows of activations", file=sys.stderr)
         return 2
+    fmt = args.fp8_format
+    dtype = "fp8_" + fmt
+    tdt = torch.float8_e4m3fn if fmt == "e4m3" else torch.float8_e5m2
+    workload = "llama3-8b-layer-fp8-" + fmt
     tile = (16, 2048)
     t0 = time.perf_counter()
-    ts = [t for t in synth.config(6) if t.dtype == "fp8_e4m3" and len(t.shape) == 2]
+    ts = [t for t in synth.config(WORKLOADS[workload]) if t.dtype == dtype and len(t.shape) == 2]
     shapes = [t.shape for t in ts]
     blob = wc.encode([(t.dtype, t.data, t.shape) for t in ts], lanes=64, tile=tile,
                      tile_order=1, threads=args.threads)
     dblob = wc.to_device(blob, dev)
     W8 = [torch.from_numpy(np.ascontiguousarray(t.data).reshape(t.shape)).to(dev) for t in ts]
-    Wb = [w.view(torch.float8_e4m3fn).to(torch.bfloat16) for w in W8]   # exact
+    Wb = [w.view(tdt).to(torch.bfloat16) for w in W8]   # exact
     gen = torch.Generator(device=dev)
     gen.manual_seed(24680)
     xs = [torch.randn(M, shp[1], generator=gen, device=dev).to(torch.bfloat16) for shp in shapes]
@@ -800,7 +808,7 @@ def gemv_fp8_bench(args, dev) -> int:
             raise RuntimeError(f"fp8 fused GEMM tensor {t} outside the fp32 summation bound")
     setup_s = time.perf_counter() - t0
 
-    flat = wc.encode([("fp8_e4m3", np.ascontiguousarray(t.data).reshape(-1)) for t in ts],
+    flat = wc.encode([(dtype, np.ascontiguousarray(t.data).reshape(-1)) for t in ts],
                      lanes=64, threads=args.threads)
     dflat = wc.to_device(flat, dev)
     outs = [torch.empty(n, dtype=torch.uint8, device=dev) for n in flat.out_bytes]
@@ -809,7 +817,7 @@ def gemv_fp8_bench(args, dev) -> int:
         wc.decode(flat, dflat.data_ptr(), [o.data_ptr() for o in outs], stream.cuda_stream,
                   err.data_ptr())
         for o, x, shp in zip(outs, xs, shapes):
-            w = o.view(torch.float8_e4m3fn).view(shp).to(torch.bfloat16)
+            w = o.view(tdt).view(shp).to(torch.bfloat16)
             torch.matmul(x, w.t())
 
     def uncompressed():
@@ -845,11 +853,12 @@ def gemv_fp8_bench(args, dev) -> int:
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "fp8 e4m3 (as bf16) x bf16 -> fp32",
+        "dtype": f"fp8 {fmt} (as bf16) x bf16 -> fp32",
         "data": "synthetic",
-        "config": {"workload": "llama3-8b-layer-fp8-e4m3", "mode": "fused-gemv-fp8", "m": M,
+        "config": {"workload": workload, "mode": "fused-gemv-fp8", "m": M,
                    "tile": f"{tile[0]}x{tile[1]}", "tile_order": "column-blocks",
-                   "product": "v_cvt_scalef32_pk_bf16_fp8 + v_mfma_f32_16x16x32_bf16",
+                   "product": ("v_cvt_scalef32_pk_bf16_" + ("fp8" if fmt == "e4m3" else "bf8") +
+                               " + v_mfma_f32_16x16x32_bf16"),
                    "lanes": 64, "weight_bytes_per_step": wbytes,
                    "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,

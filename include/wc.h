@@ -210,9 +210,9 @@ wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_
  * on the fly and never written to memory.  Every job of one tile height runs
  * in one launch.
  *   n        1..32 jobs;
- *   tensors  host array of n tensor indices; each W must be bf16, or fp8 e4m3
- *            (WC_FP8_E4M3, converted exactly to bf16 as it is decoded; 16-row
- *            tiles only), with a shape (N = rows, K = cols, 64 * K * 2 bytes
+ *   tensors  host array of n tensor indices; each W must be bf16, or fp8
+ *            (WC_FP8_E4M3 or WC_FP8_E5M2, the formats of Sec. VI-A, converted
+ *            exactly to bf16 as it is decoded; 16-row tiles only), with a shape (N = rows, K = cols, 64 * K * 2 bytes
  *            below 2 GiB), coded with 64 lanes in column-block tiles
  *            (wc_params.tile_order = WC_TILE_COLUMN_BLOCKS) of 64, 32 or 16
  *            rows.  64-row tiles take
@@ -232,7 +232,7 @@ wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_
  *   stream, dev_err as for wc_decode.
  * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument), or
  * WC_EUNSUPPORTED (a tensor is not a bf16 64-lane column-block tensor of 64,
- * 32 or 16 rows per tile or an fp8 e4m3 one of 16 rows, has 64-row tiles of 8
+ * 32 or 16 rows per tile or an fp8 (e4m3, e5m2) one of 16 rows, has 64-row tiles of 8
  * columns with m > 5, or K is too large). */
 wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n, const uint32_t* tensors,
                   const void* const* dev_x, uint32_t m, float* const* dev_y, void* stream,
@@ -352,7 +352,7 @@ wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_params* p, 
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);
 
-/* wc_version -- ABI version of this header (5). */
+/* wc_version -- ABI version of this header (6). */
 int32_t wc_version(void);
 
 #ifdef __cplusplus

@@ -583,7 +583,7 @@ __device__ void share_idle_wave(const LaunchArgs& a, const DevTensor& T, const S
 // every wave multiplies all decoding waves' operands by its own rows of packed
 // x (see Share).
 template <int G, int L, bool kTiled, int kM = 0, int kMB = 0, int kMR = 16, bool kShare = false,
-          bool kFp8 = false>
+          int kF8 = 0>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
                                               const uint2* __restrict__ tab, uint32_t* ring,
@@ -595,9 +595,11 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   static_assert(!kMfma || (L == 64 && kTiled && !kGemv &&
                            (G == 2 || (G == 4 && kMR == 16 && !kShare))),
                 "MFMA GEMM: bf16 tiles, or int8 / fp8 tiles of 16 rows");
-  static_assert(!kFp8 || (kMfma && G == 4), "fp8 weights: the byte MFMA path");
-  constexpr bool kInt8 = kMfma && G == 4 && !kFp8;  // int8 W and x, int32 sums (W8A8)
-  constexpr bool kFp8W = kMfma && G == 4 && kFp8;   // fp8 e4m3 W as bf16, bf16 x, fp32 sums
+  // kF8: 0 no fp8; fp8 weights as bf16 (bf16 x, fp32 sums) of format 1 e4m3, 2 e5m2
+  static_assert(kF8 == 0 || ((kF8 == 1 || kF8 == 2) && kMfma && G == 4),
+                "fp8 weights: the byte MFMA path, e4m3 or e5m2");
+  constexpr bool kInt8 = kMfma && G == 4 && kF8 == 0;  // int8 W and x, int32 sums (W8A8)
+  constexpr bool kFp8W = kMfma && G == 4 && kF8 != 0;  // fp8 W as bf16, bf16 x, fp32 sums
   static_assert(kMR == 16 || kMR == 32 || kMR == 64, "MFMA tiles of 16, 32 or 64 rows");
   constexpr int kMM = kMR == 64 ? 32 : kMR;   // x rows per MFMA block
   constexpr int kNB = kMR == 64 ? 2 : 1;      // MFMA output blocks of W rows per tile
@@ -686,7 +688,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   typedef __attribute__((ext_vector_type(8))) __bf16 bf8;
   typedef __attribute__((ext_vector_type(kMM * kMM / 64))) float facc;
   typedef __attribute__((ext_vector_type(4))) unsigned int u4v;
-  constexpr uint32_t kXB = (G == 2 || kFp8) ? 2u : 1u;  // bytes of one x element (bf16, int8)
+  constexpr uint32_t kXB = (G == 2 || kFp8W) ? 2u : 1u;  // bytes of one x element (bf16, int8)
   // bytes of an x row one wave row covers: 64 lane-groups of W columns over kMR rows
   constexpr uint32_t kRowXBytes = 64u * W / kMR * kXB;
   typedef __attribute__((ext_vector_type(4))) int i32x4;
@@ -803,15 +805,23 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
         return;
       }
       if constexpr (kFp8W) {
-        // 16 e4m3 weights -> 16 bf16 (exact), two B operands of 8: weights 0..7
-        // and 8..15 of the lane-group, against x columns 0..7 and 8..15 of its 16
+        // 16 fp8 weights -> 16 bf16 (exact: every e4m3 and e5m2 value is a bf16
+        // value; scale 1), two B operands of 8: weights 0..7 and 8..15 of the
+        // lane-group, against x columns 0..7 and 8..15 of its 16
         uint32_t bw[8];
 #pragma unroll
         for (int d = 0; d < 4; d++) {
-          bw[2 * d] = __builtin_bit_cast(
-              uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(ow[d], 1.0f, false));
-          bw[2 * d + 1] = __builtin_bit_cast(
-              uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(ow[d], 1.0f, true));
+          if constexpr (kF8 == 1) {
+            bw[2 * d] = __builtin_bit_cast(
+                uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(ow[d], 1.0f, false));
+            bw[2 * d + 1] = __builtin_bit_cast(
+                uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(ow[d], 1.0f, true));
+          } else {
+            bw[2 * d] = __builtin_bit_cast(
+                uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_bf8(ow[d], 1.0f, false));
+            bw[2 * d + 1] = __builtin_bit_cast(
+                uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_bf8(ow[d], 1.0f, true));
+          }
         }
         const bf8 b0 = __builtin_bit_cast(bf8, u4v{bw[0], bw[1], bw[2], bw[3]});
         const bf8 b1 = __builtin_bit_cast(bf8, u4v{bw[4], bw[5], bw[6], bw[7]});

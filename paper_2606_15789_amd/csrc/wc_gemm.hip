@@ -51,7 +51,31 @@ __global__ __launch_bounds__(kThreads) void wc_gemv_kernel(LaunchArgs a) {
   build_table(a, T, tab, cum, tid);
   __syncthreads();
   if (chunk >= T.n_chunks) return;
-  decode_chunks<G, 64, true, kM, kMB, kMR, false, kFp8>(a, T, chunk, lane, tab, ring[wave], pre);
+  decode_chunks<G, 64, true, kM, kMB, kMR, false, kFp8 ? 1 : 0>(a, T, chunk, lane, tab, ring[wave],
+                                                                pre);
+}
+
+// The same fused decode-GEMM for fp8 e5m2 weights on 16-row tiles: kMB blocks
+// of 16 x rows, each lane-group converted to bf16 as it is decoded.
+template <int kMB>
+__global__ __launch_bounds__(kThreads) void wc_gemv_e5m2_kernel(LaunchArgs a) {
+  __shared__ uint2 tab[wc::kTableSize];
+  __shared__ uint32_t cum[260];
+  __shared__ uint32_t ring[kWaves][wc_ring_words() / 2];
+  const uint32_t wg = blockIdx.x;
+  uint32_t ti = 0;
+  for (uint32_t k = 1; k < a.n_tensors; k++)
+    if (wg >= a.t[k].wg0) ti = k;
+  const DevTensor& T = a.t[ti];
+  const uint32_t tid = threadIdx.x;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t lane = __lane_id();
+  const uint32_t chunk = (wg - T.wg0) * kWaves + wave;
+  const IndexPre pre = load_index(a, T, chunk, 1u);
+  build_table(a, T, tab, cum, tid);
+  __syncthreads();
+  if (chunk >= T.n_chunks) return;
+  decode_chunks<4, 64, true, 0, kMB, 16, false, 2>(a, T, chunk, lane, tab, ring[wave], pre);
 }
 
 // The shared fused GEMM: workgroup = (pass over 256 kXB rows of x, band of 64
@@ -139,8 +163,9 @@ wc_status check_jobs(const wc_blob* desc, const void* dev_blob, uint32_t n,
     if (T.lanes != 64 || T.tile_order != WC_TILE_COLUMN_BLOCKS ||
         !(T.tile_r == 64 || T.tile_r == 32 || T.tile_r == 16))
       return WC_EUNSUPPORTED;
-    // bf16 weights on every tile height; fp8 e4m3 on 16-row tiles (not shared)
-    if (!(T.dtype == WC_BF16 || (T.dtype == WC_FP8_E4M3 && T.tile_r == 16 && !share)))
+    // bf16 weights on every tile height; fp8 e4m3 or e5m2 on 16-row tiles (not shared)
+    const bool fp8 = T.dtype == WC_FP8_E4M3 || T.dtype == WC_FP8_E5M2;
+    if (!(T.dtype == WC_BF16 || (fp8 && T.tile_r == 16 && !share)))
       return WC_EUNSUPPORTED;
     // 64-row tiles past the dot-product rows pair k-blocks r and r+1 of one
     // tile: at least two k-blocks (16 columns) per tile
@@ -160,21 +185,23 @@ wc_status check_jobs(const wc_blob* desc, const void* dev_blob, uint32_t n,
 
 // One launch per tile height and weight type (bf16 on 64 rows: VALU dot
 // products up to kDotRows rows of x, MFMA above, or the shared GEMM; bf16 on
-// 32 or 16 rows: MFMA; fp8 e4m3 on 16 rows: converted to bf16, MFMA).  xs: the
-// x (or, for the shared GEMM, packed x) of each job.
+// 32 or 16 rows: MFMA; fp8 e4m3, then e5m2, on 16 rows: converted to bf16,
+// MFMA).  xs: the x (or, for the shared GEMM, packed x) of each job.
 wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
                       const uint32_t* tensors, const uint64_t* xs, uint32_t m,
                       float* const* dev_y, bool share, hipStream_t st, int32_t* dev_err) {
-  for (uint32_t kind = 0; kind < 4; kind++) {
-    // bf16 weights on 64-, 32- and 16-row tiles, then fp8 weights on 16-row tiles
+  for (uint32_t kind = 0; kind < 5; kind++) {
+    // bf16 weights on 64-, 32- and 16-row tiles, then fp8 e4m3 and e5m2 weights
+    // on 16-row tiles
     const uint32_t rows = kind == 0 ? 64u : (kind == 1 ? 32u : 16u);
-    const bool fp8 = kind == 3;
+    const uint32_t f8 = kind < 3 ? 0u : kind - 2u;  // 0 bf16, 1 e4m3, 2 e5m2
+    const uint32_t dtype = f8 == 0 ? WC_BF16 : (f8 == 1 ? WC_FP8_E4M3 : WC_FP8_E5M2);
     LaunchArgs args{};
     fill_common(args, P, dev_blob, dev_err);
     uint32_t wgs = 0, nt = 0;
     for (uint32_t i = 0; i < n; i++) {
       const wc::TensorInfo& T = P.tensors[tensors[i]];
-      if (T.tile_r != rows || (T.dtype == WC_FP8_E4M3) != fp8) continue;
+      if (T.tile_r != rows || T.dtype != dtype) continue;
       fill_tensor(args.t[nt], T, dev_y[i], wgs);
       args.t[nt].x = xs[i];
       if (share) {
@@ -191,12 +218,19 @@ wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
     args.n_tensors = nt;
     args.m = m;
     const dim3 grid(wgs), block(kThreads);
-    if (fp8) {
+    if (f8 == 1) {
       switch ((m + 15) / 16) {
         case 1: hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 16, 4, true>), grid, block, 0, st, args); break;
         case 2: hipLaunchKernelGGL((wc_gemv_kernel<0, 2, 16, 4, true>), grid, block, 0, st, args); break;
         case 3: hipLaunchKernelGGL((wc_gemv_kernel<0, 3, 16, 4, true>), grid, block, 0, st, args); break;
         default: hipLaunchKernelGGL((wc_gemv_kernel<0, 4, 16, 4, true>), grid, block, 0, st, args); break;
+      }
+    } else if (f8 == 2) {
+      switch ((m + 15) / 16) {
+        case 1: hipLaunchKernelGGL((wc_gemv_e5m2_kernel<1>), grid, block, 0, st, args); break;
+        case 2: hipLaunchKernelGGL((wc_gemv_e5m2_kernel<2>), grid, block, 0, st, args); break;
+        case 3: hipLaunchKernelGGL((wc_gemv_e5m2_kernel<3>), grid, block, 0, st, args); break;
+        default: hipLaunchKernelGGL((wc_gemv_e5m2_kernel<4>), grid, block, 0, st, args); break;
       }
     } else if (share) {
       hipLaunchKernelGGL((wc_gemm_kernel<1>), grid, block, 0, st, args);

@@ -317,7 +317,7 @@ def _norms(seed: int, div: int):
 
 
 def config(cfg: int, layer: int = 0, div: int = 1) -> list:
-    """Tensors of workload `cfg` (1..5).
+    """Tensors of workload `cfg` (1..9).
 
     `div` > 1 shrinks every matrix dimension by that factor (same recipe,
     same distribution) so CPU-only tests stay fast; `layer` selects the
@@ -363,6 +363,14 @@ def config(cfg: int, layer: int = 0, div: int = 1) -> list:
             ts.append(Tensor(name + ".weight", "fp8_e4m3", codes.reshape(-1), (o, i)))
             ts.append(Tensor(name + ".scale", "bf16", scales.reshape(-1), (o,)))
         return ts + _norms(6, div)
+    if cfg == 9:
+        ts = []
+        for j, (name, o, i) in enumerate(_scaled(LLAMA3_8B, div)):
+            w = normal_weight(o, i, 0.02, _key(9, j), outliers=True)
+            codes, scales = quant_fp8_rows(w, "e5m2")
+            ts.append(Tensor(name + ".weight", "fp8_e5m2", codes.reshape(-1), (o, i)))
+            ts.append(Tensor(name + ".scale", "bf16", scales.reshape(-1), (o,)))
+        return ts + _norms(9, div)
     if cfg == 7:
         ts = []
         for j, (name, o, i) in enumerate(_scaled(LLAMA3_8B, div)):
@@ -392,6 +400,7 @@ CONFIG_NAMES = {
     6: "Llama-3-8B layer fp8 e4m3, per-row bf16 scales (outlier channels)",
     7: "Llama-3-8B layer MXFP4: e2m1 codes + e8m0 scales per 32 inputs",
     8: "Llama-3-8B layer AWQ-style int4 g128: codes + 4-bit zero points + fp16 scales",
+    9: "Llama-3-8B layer fp8 e5m2, per-row bf16 scales (outlier channels)",
 }
 
 

@@ -99,7 +99,7 @@ def test_degenerate_tables(dev, lanes):
 
 
 @pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16), (6, 8), (7, 8),
-                                     (8, 8)])
+                                     (8, 8), (9, 8)])
 @pytest.mark.parametrize("lanes", [64, 32])
 def test_workloads_scaled(dev, cfg, div, lanes):
     say("workload", cfg, "div", div, "lanes", lanes)
@@ -151,7 +151,7 @@ def _sample_chunks(n, k, rng):
 
 
 @pytest.mark.parametrize("cfg,lanes", [(1, 64), (2, 64), (3, 64), (4, 64), (5, 64), (4, 32),
-                                       (5, 32), (6, 64), (7, 64), (8, 64)])
+                                       (5, 32), (6, 64), (7, 64), (8, 64), (9, 64)])
 def test_workloads_full_size(dev, cfg, lanes):
     """Full workload sizes in the benchmark's launch configuration (one launch)."""
     say("full workload", cfg, "lanes", lanes)

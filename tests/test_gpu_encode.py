@@ -116,7 +116,7 @@ def test_excess_normalisation(dev):
 
 
 @pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16), (6, 8), (7, 8),
-                                     (8, 8)])
+                                     (8, 8), (9, 8)])
 def test_workloads_scaled(dev, cfg, div):
     say("workload", cfg, "div", div)
     entries = [(t.dtype, t.data) for t in synth.config(cfg, div=div)]

@@ -482,57 +482,97 @@ def test_int8_gemm_adds_and_rejects(dev):
     assert e.value.rc == -1
 
 
-# --- fp8 e4m3 weights, bf16 x (W8A16): exact conversion, bf16 MFMA ------------
+# --- fp8 weights (e4m3, e5m2), bf16 x (W8A16): exact conversion, bf16 MFMA ----
 
-def _fp8_codes(rng, shape):
+FP8 = ["e4m3", "e5m2"]
+
+
+def _fp8_special(w, fmt):
+    """NaN patterns (e4m3), infinities and NaN (e5m2)."""
+    return (w & 0x7F) == 0x7F if fmt == "e4m3" else (w & 0x7C) == 0x7C
+
+
+def _fp8_codes(rng, shape, fmt):
     w = rng.integers(0, 256, shape).astype(np.uint8)
-    w[(w & 0x7F) == 0x7F] ^= 0x01          # no NaN patterns
+    w[_fp8_special(w, fmt)] &= 0xFB      # e4m3: exponent 15 -> mantissa 3; e5m2: exponent 30
     return w
 
 
-def _check_fp8(y, w, x):
-    ref, absref = oracle.gemv_fp8(w, x)
+def _fp8_value(fmt):
+    return oracle.e4m3_value if fmt == "e4m3" else oracle.e5m2_value
+
+
+def _check_fp8(y, w, x, fmt):
+    ref, absref = oracle.gemv_fp8(w, x, fmt)
     tol = 2.0 * w.shape[1] * 2.0 ** -24 * absref + 1e-30
     bad = np.abs(y - ref) > tol
     assert not bad.any(), (np.argwhere(bad)[:5], float(np.abs(y - ref).max()))
 
 
+@pytest.mark.parametrize("fmt", FP8)
 @pytest.mark.parametrize("shape,tile", [((64, 256), (16, 64)), ((48, 1024), (16, 256)),
                                         ((256, 4096), (16, 4096)), ((32, 64), (16, 16))])
 @pytest.mark.parametrize("m", [1, 5, 16, 17, 33, 64])
-def test_fp8_gemv_matches_the_reference(dev, shape, tile, m):
-    """fp8 e4m3 tiles of 16 rows, converted to bf16 while decoded: y within the
-    fp32 summation bound of the oracle's fp64 product (every e4m3 value is a
-    bf16 value, so the conversion adds no error)."""
-    say("fp8 gemv", shape, tile, m)
-    rng = np.random.default_rng(shape[1] + 11 * m)
-    w = _fp8_codes(rng, shape)
+def test_fp8_gemv_matches_the_reference(dev, fmt, shape, tile, m):
+    """fp8 tiles of 16 rows, converted to bf16 while decoded: y within the fp32
+    summation bound of the oracle's fp64 product (every e4m3 and e5m2 value is
+    a bf16 value, so the conversion adds no error)."""
+    say("fp8 gemv", fmt, shape, tile, m)
+    rng = np.random.default_rng(shape[1] + 11 * m + (7 if fmt == "e5m2" else 0))
+    w = _fp8_codes(rng, shape, fmt)
     x = _bf16(rng.normal(0, 1.0, (m, shape[1])))
-    blob = wc.encode([("fp8_e4m3", w, shape)], tile=tile, tile_order=1)
-    _check_fp8(_run_gemv(blob, dev, 0, x), w, x)
+    blob = wc.encode([("fp8_" + fmt, w, shape)], tile=tile, tile_order=1)
+    _check_fp8(_run_gemv(blob, dev, 0, x), w, x, fmt)
 
 
-def test_fp8_gemv_small_integers_exact(dev):
-    """Small integers, exact in e4m3, bf16 and fp32 sums: y equals the integer
-    product, which pins the conversion's byte order and both MFMA halves."""
+@pytest.mark.parametrize("fmt", FP8)
+def test_fp8_gemv_every_code_exact(dev, fmt):
+    """Every finite code of the format, picked out by one-hot rows of x: y[m][n]
+    must be the code's value exactly (fp32 holds every fp8 value), which pins
+    the conversion of every byte (subnormals and signed zero included), its
+    byte order within the lane-group and both halves of the MFMA operand, in
+    the first and the last k-block of a tile."""
+    value = _fp8_value(fmt)
+    K = 256
+    k = np.arange(K)[None, :]
+    n = np.arange(16)[:, None]
+    w = ((16 * k + n) % 256).astype(np.uint8)   # columns 0..15 and 240..255 hold every code
+    w[_fp8_special(w, fmt)] = 0
+    cols = list(range(16)) + list(range(240, 256))
+    x = np.zeros((len(cols), K), np.float32)
+    for m, c in enumerate(cols):
+        x[m, c] = 1.0
+    blob = wc.encode([("fp8_" + fmt, w, w.shape)], tile=(16, 256), tile_order=1)
+    y = _run_gemv(blob, dev, 0, _bf16(x))
+    want = np.array([[value(int(w[r, c])) for r in range(16)] for c in cols])
+    assert np.array_equal(y, want), np.argwhere(y != want)[:8]
+
+
+@pytest.mark.parametrize("fmt", FP8)
+def test_fp8_gemv_small_integers_exact(dev, fmt):
+    """Small integers, exact in the format, bf16 and fp32 sums: y equals the
+    integer product, which pins the conversion's byte order and both MFMA
+    halves."""
     rng = np.random.default_rng(52)
+    mbits, bias, top = (3, 7, 16) if fmt == "e4m3" else (2, 15, 8)
     codes = {0: 0x00}
-    for v in range(1, 17):
+    for v in range(1, top + 1):
         e = v.bit_length() - 1
-        codes[v] = ((e + 7) << 3) | ((v << 3 >> e) & 7)
+        codes[v] = ((e + bias) << mbits) | ((v << mbits >> e) & ((1 << mbits) - 1))
         codes[-v] = 0x80 | codes[v]
-    wi = rng.integers(-16, 17, (64, 512))
+    wi = rng.integers(-top, top + 1, (64, 512))
     xi = rng.integers(-40, 41, (37, 512))
     w = np.vectorize(codes.get)(wi).astype(np.uint8)
-    blob = wc.encode([("fp8_e4m3", w, w.shape)], tile=(16, 256), tile_order=1)
+    blob = wc.encode([("fp8_" + fmt, w, w.shape)], tile=(16, 256), tile_order=1)
     y = _run_gemv(blob, dev, 0, _bf16(xi.astype(np.float32)))
     assert np.array_equal(y, (xi @ wi.T).astype(np.float64))
 
 
-def test_fp8_gemv_quantised_layer(dev):
+@pytest.mark.parametrize("fmt,cfg", [("e4m3", 6), ("e5m2", 9)])
+def test_fp8_gemv_quantised_layer(dev, fmt, cfg):
     """The fp8 codes of the scaled 8B fp8 workload (per-row scales stay with the
     caller) in 16 x 512 tiles, one launch, 16 rows of x: sampled rows of y."""
-    ts = [t for t in synth.config(6, div=4) if t.dtype == "fp8_e4m3" and len(t.shape) == 2]
+    ts = [t for t in synth.config(cfg, div=4) if t.dtype == "fp8_" + fmt and len(t.shape) == 2]
     assert ts
     blob = wc.encode([(t.dtype, t.data, t.shape) for t in ts], tile=(16, 512), tile_order=1)
     d = wc.to_device(blob, dev)
@@ -548,16 +588,37 @@ def test_fp8_gemv_quantised_layer(dev):
     for t, y in zip(ts, ys):
         rows = np.random.default_rng(t.shape[0]).choice(t.shape[0], 32, replace=False)
         w = np.ascontiguousarray(t.data.reshape(t.shape)[rows])
-        ref, absref = oracle.gemv_fp8(w, xbits[t.shape[1]])
+        ref, absref = oracle.gemv_fp8(w, xbits[t.shape[1]], fmt)
         tol = 2.0 * t.shape[1] * 2.0 ** -24 * absref + 1e-30
         assert (np.abs(y.cpu().numpy().astype(np.float64)[:, rows] - ref) <= tol).all(), t.name
 
 
-def test_fp8_gemv_limits(dev):
+def test_fp8_formats_in_one_call(dev):
+    """e4m3 and e5m2 jobs (and a bf16 one) in one wc_gemv call: one launch per
+    weight type, each job converted by its own format."""
+    rng = np.random.default_rng(55)
+    w4 = _fp8_codes(rng, (32, 512), "e4m3")
+    w5 = _fp8_codes(rng, (48, 512), "e5m2")
+    wb = _bf16(rng.normal(0, 0.02, (16, 512)))
+    blob = wc.encode([("fp8_e4m3", w4, w4.shape), ("fp8_e5m2", w5, w5.shape),
+                      ("bf16", wb, wb.shape)], tile=(16, 256), tile_order=1)
+    x = _bf16(rng.normal(0, 1.0, (8, 512)))
+    d = wc.to_device(blob, dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ys = wc.gemv_torch(blob, d, [0, 1, 2], [_dev_x(x, dev)] * 3, err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    _check_fp8(ys[0].cpu().numpy().astype(np.float64), w4, x, "e4m3")
+    _check_fp8(ys[1].cpu().numpy().astype(np.float64), w5, x, "e5m2")
+    _check(ys[2].cpu().numpy().astype(np.float64), wb, x)
+
+
+@pytest.mark.parametrize("fmt", FP8)
+def test_fp8_gemv_limits(dev, fmt):
     rng = np.random.default_rng(54)
-    w = _fp8_codes(rng, (64, 512))
-    b64 = wc.encode([("fp8_e4m3", w, w.shape)], tile=(64, 256), tile_order=1)
-    b16 = wc.encode([("fp8_e4m3", w, w.shape)], tile=(16, 256), tile_order=1)
+    w = _fp8_codes(rng, (64, 512), fmt)
+    b64 = wc.encode([("fp8_" + fmt, w, w.shape)], tile=(64, 256), tile_order=1)
+    b16 = wc.encode([("fp8_" + fmt, w, w.shape)], tile=(16, 256), tile_order=1)
     with pytest.raises(wc.WcError) as e:                 # 64-row fp8 tiles
         _run_gemv(b64, dev, 0, _bf16(rng.normal(0, 1.0, (4, 512))))
     assert e.value.rc == -5
@@ -565,4 +626,4 @@ def test_fp8_gemv_limits(dev):
         _run_gemm(b16, dev, 0, _bf16(rng.normal(0, 1.0, (65, 512))))
     assert e.value.rc == -5
     x = _bf16(rng.normal(0, 1.0, (64, 512)))
-    _check_fp8(_run_gemm(b16, dev, 0, x), w, x)          # wc_gemm up to 64 rows is wc_gemv
+    _check_fp8(_run_gemm(b16, dev, 0, x), w, x, fmt)     # wc_gemm up to 64 rows is wc_gemv

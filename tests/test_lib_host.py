@@ -35,11 +35,11 @@ def test_library_exports_every_declared_symbol():
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (wc_\w+)", out))
     assert set(names) <= exported
-    assert lib.wc_version() == 5
+    assert lib.wc_version() == 6
 
 
 @pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16), (6, 8), (7, 8),
-                                     (8, 8)])
+                                     (8, 8), (9, 8)])
 @pytest.mark.parametrize("lanes", [64, 32])
 def test_blobs_identical_to_oracle(cfg, div, lanes):
     ts = synth.config(cfg, div=div)

@@ -123,7 +123,8 @@ def _payload(blob):
     return states + words + (len(blob) - raw)
 
 
-@pytest.mark.parametrize("cfg,div", [(1, 1), (2, 4), (3, 4), (4, 4), (6, 4), (7, 4), (8, 4)])
+@pytest.mark.parametrize("cfg,div", [(1, 1), (2, 4), (3, 4), (4, 4), (6, 4), (7, 4), (8, 4),
+                                     (9, 4)])
 def test_size_within_one_percent_of_entropy_bound(cfg, div):
     ts = synth.config(cfg, div=div)
     pairs = [(t.dtype, t.data) for t in ts]
