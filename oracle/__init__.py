@@ -89,6 +89,12 @@ def lib():
         L.orc_e4m3_value.restype = C.c_double
         L.orc_e5m2_value.argtypes = [C.c_uint8]
         L.orc_e5m2_value.restype = C.c_double
+        L.orc_e2m1_value.argtypes = [C.c_uint8]
+        L.orc_e2m1_value.restype = C.c_double
+        L.orc_e8m0_value.argtypes = [C.c_uint8]
+        L.orc_e8m0_value.restype = C.c_double
+        L.orc_gemv_mxfp4.argtypes = [C.c_void_p, C.c_void_p, C.c_uint64, C.c_uint64, C.c_void_p,
+                                     C.c_uint32, C.c_void_p, C.c_void_p]
         L.orc_free.argtypes = [C.c_void_p]
         L.orc_free.restype = None
         L.orc_blob_tensors.argtypes = [C.c_void_p, C.c_uint64, C.POINTER(C.c_uint32)]
@@ -348,6 +354,34 @@ def e4m3_value(v: int) -> float:
 def e5m2_value(v: int) -> float:
     """The value of one OCP e5m2 byte (+-inf, NaN for the exponent-31 patterns)."""
     return lib().orc_e5m2_value(v)
+
+
+def e2m1_value(nibble: int) -> float:
+    """The value of one fp4 e2m1 code (low 4 bits)."""
+    return lib().orc_e2m1_value(nibble)
+
+
+def e8m0_value(e: int) -> float:
+    """The value of one e8m0 scale byte: 2^(e - 127), NaN for 255."""
+    return lib().orc_e8m0_value(e)
+
+
+def gemv_mxfp4(w, scales, x):
+    """(y, sum |x w|) in fp64 for MXFP4 weights: w the packed e2m1 codes
+    (rows x cols/2 bytes, even element in the low nibble), scales the e8m0
+    bytes (rows x cols/32), x bf16 storage words (M x cols)."""
+    w = np.ascontiguousarray(w, dtype=np.uint8)
+    scales = np.ascontiguousarray(scales, dtype=np.uint8)
+    x = np.ascontiguousarray(x, dtype=np.uint16)
+    rows, cols = w.shape[0], 2 * w.shape[1]
+    M = x.shape[0]
+    assert x.shape[1] == cols and scales.shape == (rows, cols // 32)
+    y = np.empty((M, rows), np.float64)
+    a = np.empty((M, rows), np.float64)
+    rc = lib().orc_gemv_mxfp4(_ptr(w), _ptr(scales), rows, cols, _ptr(x), M, _ptr(y), _ptr(a))
+    if rc:
+        raise OracleError(rc, "gemv_mxfp4")
+    return y, a
 
 
 FP8_FORMATS = {"e4m3": 0, "e5m2": 1}

@@ -1029,6 +1029,43 @@ double orc_e5m2_value(uint8_t v) {
   return s ? -mag : mag;
 }
 
+/* ------------------------------------------------------------------------ */
+/* MXFP4 weights (OCP microscaling; the paper's fp4 format, Sec. VI-A):      */
+/* e2m1 codes (sign, 2 exponent bits with bias 1, 1 mantissa bit: 0, 0.5, 1, */
+/* 1.5, 2, 3, 4, 6), two per byte with the even element in the low nibble,   */
+/* and one e8m0 scale byte E per 32 consecutive weights of a row, worth      */
+/* 2^(E - 127) (E = 255 is NaN).  What the fused decode-GEMM computes:       */
+/* y[m][n] = sum_k x[m][k] * e2m1(w[n][k]) * 2^(E[n][k / 32] - 127), in fp64, */
+/* summed in k order; abs_out as for orc_gemv_bf16.                         */
+
+double orc_e2m1_value(uint8_t nibble) {
+  const int s = (nibble >> 3) & 1, e = (nibble >> 1) & 3, m = nibble & 1;
+  const double mag = e ? ldexp(1.0 + m / 2.0, e - 1) : m / 2.0;
+  return s ? -mag : mag;
+}
+
+double orc_e8m0_value(uint8_t e) { return e == 255 ? NAN : ldexp(1.0, (int)e - 127); }
+
+int orc_gemv_mxfp4(const uint8_t* w, const uint8_t* scales, uint64_t rows, uint64_t cols,
+                   const uint16_t* x, uint32_t M, double* y, double* abs_out) {
+  if (!w || !scales || !x || !y || M == 0 || cols % 32) return ORC_EINVAL;
+  for (uint32_t m = 0; m < M; m++)
+    for (uint64_t n = 0; n < rows; n++) {
+      double s = 0.0, a = 0.0;
+      for (uint64_t k = 0; k < cols; k++) {
+        const uint8_t byte = w[(n * cols + k) / 2];
+        const uint8_t code = (k & 1) ? byte >> 4 : byte & 15;
+        const double v = orc_e2m1_value(code) * orc_e8m0_value(scales[n * (cols / 32) + k / 32]);
+        double p = bf16_value(x[(uint64_t)m * cols + k]) * v;
+        s += p;
+        a += fabs(p);
+      }
+      y[(uint64_t)m * rows + n] = s;
+      if (abs_out) abs_out[(uint64_t)m * rows + n] = a;
+    }
+  return ORC_OK;
+}
+
 /* fmt: 0 = e4m3, 1 = e5m2 */
 int orc_gemv_fp8(const uint8_t* w, uint64_t rows, uint64_t cols, const uint16_t* x, uint32_t M,
                  uint32_t fmt, double* y, double* abs_out) {

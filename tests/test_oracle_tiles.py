@@ -316,3 +316,59 @@ def test_gemv_fp8_reference_one_hot_and_small_integers(fmt):
     y, a = oracle.gemv_fp8(wb, _bf16_of(xi.astype(np.float32)), fmt)
     assert np.array_equal(y, (xi @ wi.T).astype(np.float64))
     assert np.array_equal(a, (np.abs(xi) @ np.abs(wi).T).astype(np.float64))
+
+
+def test_e2m1_and_e8m0_values():
+    """fp4 e2m1: the eight magnitudes the OCP format defines, each code
+    against the input generator's own e2m1 encoder (a separate implementation:
+    quantising a representable value must give back its code, and the code's
+    value must be that value), and the sign bit.  e8m0: powers of two and NaN."""
+    from paper_2606_15789_amd import synth
+    mags = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]
+    assert [oracle.e2m1_value(c) for c in range(8)] == mags
+    assert [oracle.e2m1_value(8 + c) for c in range(1, 8)] == [-v for v in mags[1:]]
+    assert np.signbit(oracle.e2m1_value(8)) and oracle.e2m1_value(8) == 0.0
+    vals = np.array(mags[1:] + [-v for v in mags[1:]], np.float32)
+    codes = synth.fp4_e2m1_codes(vals)
+    assert [oracle.e2m1_value(int(c)) for c in codes] == vals.tolist()
+    assert [oracle.e8m0_value(e) for e in (127, 128, 126, 0, 254)] == \
+        [1.0, 2.0, 0.5, 2.0 ** -127, 2.0 ** 127]
+    assert np.isnan(oracle.e8m0_value(255))
+
+
+def test_gemv_mxfp4_reference():
+    """One-hot x rows pick single weights (code value times its block's scale);
+    small integers (e2m1 0..4 and 6 at scale 1, exact everywhere) give the
+    integer product; and a power-of-two scale on one block scales exactly that
+    block's share of the product."""
+    rng = np.random.default_rng(19)
+    rows, cols = 6, 96
+    codes = rng.integers(0, 16, (rows, cols)).astype(np.uint8)
+    w = codes[:, 0::2] | (codes[:, 1::2] << 4)
+    sc = rng.integers(120, 135, (rows, cols // 32)).astype(np.uint8)
+    ks = [0, 31, 32, 95]
+    x = np.zeros((len(ks), cols), np.float32)
+    for m, k in enumerate(ks):
+        x[m, k] = 1.0
+    y, _ = oracle.gemv_mxfp4(w, sc, _bf16_of(x))
+    for m, k in enumerate(ks):
+        assert y[m].tolist() == [oracle.e2m1_value(int(codes[n, k])) * 2.0 ** (int(sc[n, k // 32]) - 127)
+                                 for n in range(rows)]
+    # small integers at scale 1 (E = 127)
+    table = {0: 0, 1: 2, 2: 4, 3: 5, 4: 6, 6: 7}
+    for v, c in table.items():
+        assert oracle.e2m1_value(c) == v and oracle.e2m1_value(8 | c) == -v
+    vals = rng.choice([0, 1, 2, 3, 4, 6, -1, -2, -3, -4, -6], (rows, cols))
+    ci = np.vectorize(lambda v: table[abs(v)] | (8 if v < 0 else 0))(vals).astype(np.uint8)
+    wi = ci[:, 0::2] | (ci[:, 1::2] << 4)
+    xi = rng.integers(-20, 21, (3, cols))
+    one = np.full((rows, cols // 32), 127, np.uint8)
+    y, a = oracle.gemv_mxfp4(wi, one, _bf16_of(xi.astype(np.float32)))
+    assert np.array_equal(y, (xi @ vals.T).astype(np.float64))
+    assert np.array_equal(a, (np.abs(xi) @ np.abs(vals).T).astype(np.float64))
+    # scale block 1 of every row by 2^3: its columns' share of y scales by 8
+    sc3 = one.copy()
+    sc3[:, 1] = 130
+    y3, _ = oracle.gemv_mxfp4(wi, sc3, _bf16_of(xi.astype(np.float32)))
+    part = (xi[:, 32:64] @ vals[:, 32:64].T).astype(np.float64)
+    assert np.array_equal(y3, y + 7 * part)
