@@ -244,6 +244,11 @@ def main() -> int:
                          "M rows, 1..64) over the fp8 projections of the 8B fp8 layer in "
                          "16 x 2048 tiles, next to the same product unfused and on the "
                          "weights kept as bf16")
+    ap.add_argument("--gemv-mx", type=int, default=0, metavar="M",
+                    help="time the fused decode-GEMM on MXFP4 weights (wc_gemv_mx: e2m1 codes "
+                         "with e8m0 scales per 32, bf16 x, fp32 y; M rows, 1..64) over the "
+                         "seven projections of the 8B MXFP4 layer in 16 x 2048 tiles, next to "
+                         "the same product unfused and on the weights kept as bf16")
     ap.add_argument("--fp8-format", choices=["e4m3", "e5m2"], default="e4m3",
                     help="fp8 format of --gemv-fp8 (the llama3-8b-layer-fp8-e4m3 or "
                          "-fp8-e5m2 workload)")
@@ -270,6 +275,8 @@ def main() -> int:
         return gemm_i8_bench(args, dev)
     if args.gemv_fp8:
         return gemv_fp8_bench(args, dev)
+    if args.gemv_mx:
+        return gemv_mx_bench(args, dev)
     if args.encode:
         return encode_bench(args, dev)
     if args.sweep:
@@ -873,6 +880,137 @@ def gemv_fp8_bench(args, dev) -> int:
                          "ms_per_step": round(s_plain * 1e3, 4),
                          "what": "torch.matmul on the weights kept resident as bf16 (2x the "
                                  "fp8 bytes)"},
+        "setup_s": round(setup_s, 1),
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def gemv_mx_bench(args, dev) -> int:
+    """Fused decode-GEMM over the seven MXFP4 projections of the 8B MXFP4 layer
+    (e2m1 codes in the blob, e8m0 scales decoded once, bf16 x, fp32 y), checked
+    against torch's fp32 product of the same values."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15789_amd import synth, wc
+    M = args.gemv_mx
+    if not 1 <= M <= 64:
+        print("--gemv-mx takes 1..64 rows of activations", file=sys.stderr)
+        return 2
+    workload = "llama3-8b-layer-mxfp4"
+    tile = (16, 2048)
+    t0 = time.perf_counter()
+    ts = synth.config(WORKLOADS[workload])
+    blocks = [t for t in ts if t.dtype == "fp4_e2m1"]
+    scales = [t for t in ts if t.name.endswith(".scales")]
+    shapes = [t.shape for t in blocks]
+    blob = wc.encode([(t.dtype, t.data, t.shape) for t in blocks], lanes=64, tile=tile,
+                     tile_order=1, threads=args.threads)
+    dblob = wc.to_device(blob, dev)
+    dsc = [torch.from_numpy(np.ascontiguousarray(s.data).reshape(-1)).to(dev) for s in scales]
+    lut = torch.tensor([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0,
+                        -0.0, -0.5, -1.0, -1.5, -2.0, -3.0, -4.0, -6.0],
+                       dtype=torch.float32, device=dev)
+
+    def dequant(packed, sc, shp):
+        """bf16 weights of packed e2m1 codes and e8m0 scales (exact)."""
+        p = packed.view(shp[0], shp[1] // 2)
+        codes = torch.stack([p & 15, p >> 4], dim=2).reshape(shp).long()
+        e = sc.view(shp[0], shp[1] // 32).int() - 127
+        scale = torch.pow(2.0, e.float()).repeat_interleave(32, dim=1)
+        return (lut[codes] * scale).to(torch.bfloat16)
+
+    Wb = [dequant(torch.from_numpy(np.ascontiguousarray(t.data).reshape(-1)).to(dev), s, shp)
+          for t, s, shp in zip(blocks, dsc, shapes)]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(13579)
+    xs = [torch.randn(M, shp[1], generator=gen, device=dev).to(torch.bfloat16) for shp in shapes]
+    ys = [torch.zeros(M, shp[0], dtype=torch.float32, device=dev) for shp in shapes]
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def fused():
+        wc.gemv_mx(blob, dblob.data_ptr(), list(range(len(blocks))), [s.data_ptr() for s in dsc],
+                   [x.data_ptr() for x in xs], M, [y.data_ptr() for y in ys],
+                   stream.cuda_stream, err.data_ptr())
+
+    fused()
+    torch.cuda.synchronize()
+    if int(err.item()):
+        raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
+    for t, (w, x, y) in enumerate(zip(Wb, xs, ys)):
+        ref = x.float() @ w.float().t()
+        bound = x.float().abs() @ w.float().abs().t()
+        if torch.any((y - ref).abs() > w.shape[1] * 2.0 ** -23 * bound + 1e-30):
+            raise RuntimeError(f"MXFP4 fused GEMM tensor {t} outside the fp32 summation bound")
+    setup_s = time.perf_counter() - t0
+
+    flat = wc.encode([("fp4_e2m1", np.ascontiguousarray(t.data).reshape(-1)) for t in blocks],
+                     lanes=64, threads=args.threads)
+    dflat = wc.to_device(flat, dev)
+    outs = [torch.empty(n, dtype=torch.uint8, device=dev) for n in flat.out_bytes]
+
+    def unfused():
+        wc.decode(flat, dflat.data_ptr(), [o.data_ptr() for o in outs], stream.cuda_stream,
+                  err.data_ptr())
+        for o, s, x, shp in zip(outs, dsc, xs, shapes):
+            torch.matmul(x, dequant(o, s, shp).t())
+
+    def uncompressed():
+        for w, x in zip(Wb, xs):
+            torch.matmul(x, w.t())
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / args.steps / 1e3
+
+    s_fused, s_unfused, s_plain = timed(fused), timed(unfused), timed(uncompressed)
+    if int(err.item()):
+        raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
+    wbytes = sum(blob.out_bytes)
+    sbytes = sum(s.numel() for s in dsc)
+    alg = (blob.size + sbytes + sum(x.numel() * 2 for x in xs) +
+           sum(2 * y.numel() * 4 for y in ys))
+    achieved = alg / s_fused / 1e9
+    line = {
+        "metric": METRIC + " [fused MXFP4 decode-GEMM]",
+        "value": round(wbytes / s_fused / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(s_fused * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp4 e2m1 x e8m0 (as bf16) x bf16 -> fp32",
+        "data": "synthetic",
+        "config": {"workload": workload, "mode": "fused-gemv-mx", "m": M,
+                   "tile": f"{tile[0]}x{tile[1]}", "tile_order": "column-blocks",
+                   "product": "v_cvt_scalef32_pk_bf16_fp4 + v_mfma_f32_16x16x32_bf16",
+                   "lanes": 64, "code_bytes_per_step": wbytes, "scale_bytes_per_step": sbytes,
+                   "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "wc_gemv_mx_kernel", "mean_step_us": round(s_fused * 1e6, 2),
+                     "algorithmic_bytes_per_step": int(alg)},
+        "unfused": {"value": round(wbytes / s_unfused / 1e9, 2), "unit": "GB/s",
+                    "ms_per_step": round(s_unfused * 1e3, 4),
+                    "what": "wc_decode of the codes (64 KiB byte-run chunks), torch dequantisation "
+                            "to bf16 with the scales, torch.matmul per tensor"},
+        "uncompressed": {"value": round(wbytes / s_plain / 1e9, 2), "unit": "GB/s",
+                         "ms_per_step": round(s_plain * 1e3, 4),
+                         "what": "torch.matmul on the weights kept resident as bf16 (4x the "
+                                 "fp4 bytes)"},
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line), flush=True)

@@ -238,6 +238,33 @@ wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n, const u
                   const void* const* dev_x, uint32_t m, float* const* dev_y, void* stream,
                   int32_t* dev_err);
 
+/* wc_gemv_mx -- the fused decode-GEMM for MXFP4 weights (OCP microscaling,
+ * the paper's fp4 format of Sec. VI-A; Alg. 1 / 3): for each of n jobs i,
+ * dev_y[i] += x_i * W_i^T with W_i[n][k] = e2m1(code[n][k]) *
+ * 2^(scale[n][k / 32] - 127), the codes decoded on the fly and never written.
+ * A lane-group of a 16-row column-block tile is 32 codes of one row, one MX
+ * block: v_cvt_scalef32_pk_bf16_fp4 turns it into bf16 with its scale (exact
+ * while the weights stay in bf16's normal range) and four
+ * v_mfma_f32_16x16x32_bf16 multiply it by x.
+ *   tensors    host array of n tensor indices; each W must be WC_FP4_E2M1
+ *              with a shape (N = rows, K = cols in codes), coded with 64 lanes
+ *              in column-block tiles (WC_TILE_COLUMN_BLOCKS) of 16 rows and a
+ *              multiple of 128 columns;
+ *   dev_scales host array of n device pointers to the e8m0 scale bytes of
+ *              each W, N x K/32 row-major (e.g. decoded by wc_decode from the
+ *              same blob); 255 reads as NaN;
+ *   dev_x      host array of n device pointers to bf16 x, m x K row-major,
+ *              16-byte aligned (jobs may share one x);
+ *   m          1..64 rows of x, the same for every job;
+ *   dev_y      host array of n device pointers to float y, m x N row-major;
+ *              the products are added with fp32 atomics, as in wc_gemv;
+ *   stream, dev_err as for wc_decode.
+ * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument) or
+ * WC_EUNSUPPORTED (a tensor the path does not take). */
+wc_status wc_gemv_mx(const wc_blob* desc, const void* dev_blob, uint32_t n, const uint32_t* tensors,
+                     const uint8_t* const* dev_scales, const void* const* dev_x, uint32_t m,
+                     float* const* dev_y, void* stream, int32_t* dev_err);
+
 /* wc_gemm_i8 -- the fused decode-GEMM for int8 weights and int8 activations
  * (W8A8, the SmoothQuant-style sq8 format of Sec. VI-A; Alg. 1 / 3): for each
  * of n jobs i, dev_y[i] += x_i * W_i^T in exact integer arithmetic, W_i =
@@ -352,7 +379,7 @@ wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_params* p, 
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);
 
-/* wc_version -- ABI version of this header (6). */
+/* wc_version -- ABI version of this header (7). */
 int32_t wc_version(void);
 
 #ifdef __cplusplus

@@ -73,7 +73,10 @@ struct DevTensor {
   uint64_t freq_off;     // u16 frequency table (blob offset)
   uint64_t raw_off;      // raw bytes (blob offset), 16-bit formats only
   uint64_t n_sym;        // coded symbols in the tensor
-  uint64_t raw_padded;   // bytes of the (16-B padded) raw region
+  union {
+    uint64_t raw_padded;  // bytes of the (16-B padded) raw region, 16-bit formats only
+    uint64_t scales;      // fused MXFP4 GEMM: device e8m0 scales, [N][K / 32] bytes
+  };
   uint64_t out_bytes;    // decoded bytes of the tensor
   uint32_t first_chunk;  // global index of the tensor's first chunk
   uint32_t n_chunks;
@@ -593,13 +596,17 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   static_assert(!kShare || (kMfma && kMR == 64), "shared fused GEMM: 64-row tiles");
   static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
   static_assert(!kMfma || (L == 64 && kTiled && !kGemv &&
-                           (G == 2 || (G == 4 && kMR == 16 && !kShare))),
-                "MFMA GEMM: bf16 tiles, or int8 / fp8 tiles of 16 rows");
-  // kF8: 0 no fp8; fp8 weights as bf16 (bf16 x, fp32 sums) of format 1 e4m3, 2 e5m2
-  static_assert(kF8 == 0 || ((kF8 == 1 || kF8 == 2) && kMfma && G == 4),
-                "fp8 weights: the byte MFMA path, e4m3 or e5m2");
+                           (G == 2 || ((G == 4 || (G == 8 && kF8 == 3)) && kMR == 16 &&
+                                       !kShare))),
+                "MFMA GEMM: bf16 tiles, or int8 / fp8 / MXFP4 tiles of 16 rows");
+  // kF8: 0 no fp8; fp8 weights as bf16 (bf16 x, fp32 sums) of format 1 e4m3, 2 e5m2;
+  // 3 MXFP4 weights (e2m1 nibbles, an e8m0 scale per 32-weight lane-group) as bf16
+  static_assert(kF8 == 0 || ((kF8 == 1 || kF8 == 2) && kMfma && G == 4) ||
+                    (kF8 == 3 && kMfma && G == 8 && kMR == 16 && !kShare),
+                "fp8 weights: the byte MFMA path, e4m3 or e5m2; MXFP4: the nibble path");
   constexpr bool kInt8 = kMfma && G == 4 && kF8 == 0;  // int8 W and x, int32 sums (W8A8)
   constexpr bool kFp8W = kMfma && G == 4 && kF8 != 0;  // fp8 W as bf16, bf16 x, fp32 sums
+  constexpr bool kMx = kMfma && G == 8;                // MXFP4 W as bf16, bf16 x, fp32 sums
   static_assert(kMR == 16 || kMR == 32 || kMR == 64, "MFMA tiles of 16, 32 or 64 rows");
   constexpr int kMM = kMR == 64 ? 32 : kMR;   // x rows per MFMA block
   constexpr int kNB = kMR == 64 ? 2 : 1;      // MFMA output blocks of W rows per tile
@@ -688,7 +695,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   typedef __attribute__((ext_vector_type(8))) __bf16 bf8;
   typedef __attribute__((ext_vector_type(kMM * kMM / 64))) float facc;
   typedef __attribute__((ext_vector_type(4))) unsigned int u4v;
-  constexpr uint32_t kXB = (G == 2 || kFp8W) ? 2u : 1u;  // bytes of one x element (bf16, int8)
+  constexpr uint32_t kXB = (G == 2 || kFp8W || kMx) ? 2u : 1u;  // bytes of an x element
   // bytes of an x row one wave row covers: 64 lane-groups of W columns over kMR rows
   constexpr uint32_t kRowXBytes = 64u * W / kMR * kXB;
   typedef __attribute__((ext_vector_type(4))) int i32x4;
@@ -699,6 +706,8 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   uint32_t prev[kMR == 64 ? 4 : 1];             // 64-row tiles: the even row's dwords
   u4v xa[kMfma ? kMB : 1];
   u4v xa2[kFp8W ? kMB : 1];  // fp8 weights: x columns 8..15 of the lane's 16
+  u4v xm[kMx ? kMB : 1][3];  // MXFP4 weights: x columns 8..31 of the lane's 32
+  uint32_t mxe = 0;          // MXFP4: the e8m0 scale byte of this lane's lane-group
   // the x rows (fused GEMM on the matrix cores): a.m rows of K bf16
   const uint32_t K = T.ntc << T.log_tc;  // columns of W = length of an x row
   // (the shared GEMM reads packed x: rows rounded up to blocks of 32)
@@ -720,6 +729,14 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
     xoff = ((sub % kMM) * K + (chunk0 % T.ntc) * (1u << T.log_tc) + W * (sub / kMM)) * kXB;
     xblk = kXB * kMM * K;  // bytes of kMM rows of x
   }
+  // MXFP4: the scales of W row n, one per 32 columns; the lane-group of this
+  // lane in wave row r is k-block (chunk0 mod ntc) tile_c / 32 + 4 r + sub div 16
+  const __amdgpu_buffer_rsrc_t mrs = make_rsrc(
+      reinterpret_cast<const void*>(kMx ? T.scales : 0ull),
+      kMx ? (T.n_chunks / T.ntc) * 16u * (K / 32u) : 0u);
+  const uint32_t moff = kMx ? ((chunk0 / T.ntc) * 16u + sub % 16u) * (K / 32u) +
+                                  (chunk0 % T.ntc) * ((1u << T.log_tc) / 32u) + sub / 16u
+                            : 0u;
 
   // group g of the chunk, j = g mod kUnroll (static)
   auto group = [&](uint32_t g, auto jc, auto tailc) {
@@ -750,7 +767,15 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
           xa2[mb] = __builtin_bit_cast(
               u4v, __builtin_amdgcn_raw_buffer_load_b128(
                        xrs, xoff + mb * xblk + r * kRowXBytes + 16u, 0, 0));
+        if constexpr (kMx) {
+#pragma unroll
+          for (int q = 0; q < 3; q++)
+            xm[mb][q] = __builtin_bit_cast(
+                u4v, __builtin_amdgcn_raw_buffer_load_b128(
+                         xrs, xoff + mb * xblk + r * kRowXBytes + 16u * (q + 1), 0, 0));
+        }
       }
+      if constexpr (kMx) mxe = __builtin_amdgcn_raw_buffer_load_b8(mrs, moff + 4u * r, 0, 0);
     }
     const int nv = kTail ? max(0, min<int>(W, (int)n_lane - (int)(r * kRowSym + sub * W))) : W;
 #pragma unroll
@@ -801,6 +826,34 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
             macc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, B0, macc[mb][0], 0, 0, 0);
             macc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, B1, macc[mb][1], 0, 0, 0);
           }
+        }
+        return;
+      }
+      if constexpr (kMx) {
+        // 32 e2m1 weights -> 32 bf16 times the block's scale 2^(E - 127) (exact
+        // while the products stay in bf16's range); byte b of dword d holds
+        // weights 8 d + 2 b (low nibble) and 8 d + 2 b + 1.  Four B operands
+        // of 8 weights, against x columns 8 q .. 8 q + 7 of the lane's 32.
+        const uint32_t e = mxe & 0xFFu;
+        const float sc =
+            __builtin_bit_cast(float, e == 255u ? 0x7FC00000u : (e ? e << 23 : 0x00400000u));
+        uint32_t bw[16];
+#pragma unroll
+        for (int d = 0; d < 4; d++) {
+          bw[4 * d] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(ow[d], sc, 0));
+          bw[4 * d + 1] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(ow[d], sc, 1));
+          bw[4 * d + 2] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(ow[d], sc, 2));
+          bw[4 * d + 3] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(ow[d], sc, 3));
+        }
+#pragma unroll
+        for (int q = 0; q < 4; q++) {
+          const bf8 b =
+              __builtin_bit_cast(bf8, u4v{bw[4 * q], bw[4 * q + 1], bw[4 * q + 2], bw[4 * q + 3]});
+#pragma unroll
+          for (int mb = 0; mb < kMB; mb++)
+            macc[mb][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                __builtin_bit_cast(bf8, q == 0 ? xa[mb] : xm[mb][q > 0 ? q - 1 : 0]), b, macc[mb][0], 0,
+                0, 0);
         }
         return;
       }

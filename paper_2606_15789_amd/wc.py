@@ -23,7 +23,7 @@ DERR = {1: "WC_DERR_INDEX", 2: "WC_DERR_STATE", 4: "WC_DERR_CURSOR", 8: "WC_DERR
 # Every function the header declares; the library must export all of them.
 EXPORTS = ["wc_analyze", "wc_encode", "wc_open", "wc_decode", "wc_gemv", "wc_free",
            "wc_version", "wc_analyze_device", "wc_encode_device_bounds", "wc_encode_device",
-           "wc_gemm_workspace_bytes", "wc_gemm", "wc_gemm_i8"]
+           "wc_gemm_workspace_bytes", "wc_gemm", "wc_gemm_i8", "wc_gemv_mx"]
 
 ANALYZE_WORKSPACE_BYTES = 524288  # WC_ANALYZE_WORKSPACE_BYTES
 
@@ -101,6 +101,10 @@ def lib():
                                  C.POINTER(C.c_void_p), C.c_uint32, C.POINTER(C.c_void_p),
                                  C.c_void_p, C.c_void_p]
         L.wc_gemm_i8.restype = C.c_int
+        L.wc_gemv_mx.argtypes = [C.POINTER(_Blob), C.c_void_p, C.c_uint32, C.POINTER(C.c_uint32),
+                                 C.POINTER(C.c_void_p), C.POINTER(C.c_void_p), C.c_uint32,
+                                 C.POINTER(C.c_void_p), C.c_void_p, C.c_void_p]
+        L.wc_gemv_mx.restype = C.c_int
         L.wc_analyze_device.argtypes = [C.POINTER(_Tensor), C.c_void_p, C.c_uint64, C.c_void_p,
                                         C.POINTER(_Stats)]
         L.wc_analyze_device.restype = C.c_int
@@ -297,6 +301,21 @@ def gemm_i8(blob: Blob, dev_blob: int, tensors, dev_x, m: int, dev_y, stream: in
         raise WcError("wc_gemm_i8", rc)
 
 
+def gemv_mx(blob: Blob, dev_blob: int, tensors, dev_scales, dev_x, m: int, dev_y,
+            stream: int = 0, dev_err: int = 0) -> None:
+    """wc_gemv_mx with raw device pointers: y_i (m x N float) += x_i (m x K bf16)
+    * W_i^T for MXFP4 W_i (e2m1 codes in the blob, e8m0 scales at dev_scales[i])."""
+    n = len(tensors)
+    ts = (C.c_uint32 * max(n, 1))(*tensors)
+    ss = (C.c_void_p * max(n, 1))(*[p or None for p in dev_scales])
+    xs = (C.c_void_p * max(n, 1))(*[p or None for p in dev_x])
+    ys = (C.c_void_p * max(n, 1))(*[p or None for p in dev_y])
+    rc = lib().wc_gemv_mx(blob.ptr, C.c_void_p(dev_blob), n, ts, ss, xs, m, ys,
+                          C.c_void_p(stream or None), C.c_void_p(dev_err or None))
+    if rc:
+        raise WcError("wc_gemv_mx", rc)
+
+
 # --- torch plumbing: device memory and streams only ---------------------------
 
 def to_device(blob: Blob, device="cuda"):
@@ -470,4 +489,27 @@ def gemm_i8_torch(blob: Blob, dev_blob, tensors, xs, ys=None, stream=None, err=N
         stream = torch.cuda.current_stream(xs[0].device)
     gemm_i8(blob, dev_blob.data_ptr(), list(tensors), [x.data_ptr() for x in xs], m,
             [y.data_ptr() for y in ys], stream.cuda_stream, err.data_ptr() if err is not None else 0)
+    return ys
+
+
+def gemv_mx_torch(blob: Blob, dev_blob, tensors, scales, xs, ys=None, stream=None, err=None):
+    """wc_gemv_mx into float32 tensors: ys[i] += xs[i] @ W_i^T for MXFP4 W_i =
+    tensor tensors[i] with e8m0 scales `scales[i]` (uint8 device tensors of
+    N x K/32); ys zeroed and returned if None."""
+    import torch
+    m = xs[0].shape[0]
+    for x in xs:
+        if x.dtype != torch.bfloat16 or not x.is_contiguous() or x.shape[0] != m:
+            raise ValueError("xs must be contiguous bfloat16 tensors with equal row counts")
+    for sc in scales:
+        if sc.dtype != torch.uint8 or not sc.is_contiguous():
+            raise ValueError("scales must be contiguous uint8 tensors")
+    if ys is None:
+        ys = [torch.zeros((m, blob.shape(t)[0]), dtype=torch.float32, device=x.device)
+              for t, x in zip(tensors, xs)]
+    if stream is None:
+        stream = torch.cuda.current_stream(xs[0].device)
+    gemv_mx(blob, dev_blob.data_ptr(), list(tensors), [sc.data_ptr() for sc in scales],
+            [x.data_ptr() for x in xs], m, [y.data_ptr() for y in ys], stream.cuda_stream,
+            err.data_ptr() if err is not None else 0)
     return ys

@@ -627,3 +627,140 @@ def test_fp8_gemv_limits(dev, fmt):
     assert e.value.rc == -5
     x = _bf16(rng.normal(0, 1.0, (64, 512)))
     _check_fp8(_run_gemm(b16, dev, 0, x), w, x, fmt)     # wc_gemm up to 64 rows is wc_gemv
+
+
+# --- MXFP4 weights (e2m1 codes, e8m0 scale per 32), bf16 x: wc_gemv_mx --------
+
+def _mx_pack(codes):
+    """Nibble codes (rows x cols) packed two per byte, even element low."""
+    return (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
+
+
+def _run_mx(blob, dev, t, scales, x_bits, expect_err=0):
+    d = wc.to_device(blob, dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    sc = torch.from_numpy(np.ascontiguousarray(scales, np.uint8).reshape(-1).copy()).to(dev)
+    ys = wc.gemv_mx_torch(blob, d, [t], [sc], [_dev_x(x_bits, dev)], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == expect_err, wc.describe_errors(int(err.item()))
+    return ys[0].cpu().numpy().astype(np.float64)
+
+
+def _check_mx(y, w, sc, x):
+    ref, absref = oracle.gemv_mxfp4(w, sc, x)
+    tol = 2.0 * 2 * w.shape[1] * 2.0 ** -24 * absref + 1e-30
+    bad = np.abs(y - ref) > tol
+    assert not bad.any(), (np.argwhere(bad)[:5], float(np.abs(y - ref).max()))
+
+
+@pytest.mark.parametrize("varied", [False, True])
+def test_mx_gemv_every_code_exact(dev, varied):
+    """Every e2m1 code in every position of a lane-group, picked out by one-hot
+    rows of x in the first and the last MX block of a tile row: y must be the
+    code's value times its block's scale exactly (fp32 holds every product),
+    which pins the nibble order of the conversion, the four MFMA operands of a
+    lane-group and the scale each lane-group reads."""
+    rows, cols = 16, 256
+    k = np.arange(cols)[None, :]
+    n = np.arange(rows)[:, None]
+    codes = ((n + k) % 16).astype(np.uint8)
+    rng = np.random.default_rng(81)
+    sc = (rng.integers(118, 137, (rows, cols // 32)) if varied
+          else np.full((rows, cols // 32), 127)).astype(np.uint8)
+    picks = list(range(32)) + list(range(224, 256))
+    x = np.zeros((len(picks), cols), np.float32)
+    for m, c in enumerate(picks):
+        x[m, c] = 1.0
+    blob = wc.encode([("fp4_e2m1", _mx_pack(codes), (rows, cols))], tile=(16, 256), tile_order=1)
+    y = _run_mx(blob, dev, 0, sc, _bf16(x))
+    want = np.array([[oracle.e2m1_value(int(codes[r, c])) * oracle.e8m0_value(int(sc[r, c // 32]))
+                      for r in range(rows)] for c in picks])
+    assert np.array_equal(y, want), np.argwhere(y != want)[:8]
+
+
+@pytest.mark.parametrize("shape,tile", [((64, 512), (16, 128)), ((48, 1024), (16, 256)),
+                                        ((256, 4096), (16, 4096))])
+@pytest.mark.parametrize("m", [1, 5, 16, 17, 33, 64])
+def test_mx_gemv_matches_the_reference(dev, shape, tile, m):
+    """MXFP4 tiles of 16 rows, converted to bf16 with their block scales while
+    decoded: y within the fp32 summation bound of the oracle's fp64 product."""
+    say("mx gemv", shape, tile, m)
+    rng = np.random.default_rng(shape[1] + 13 * m)
+    codes = rng.integers(0, 16, shape).astype(np.uint8)
+    sc = rng.integers(112, 140, (shape[0], shape[1] // 32)).astype(np.uint8)
+    x = _bf16(rng.normal(0, 1.0, (m, shape[1])))
+    w = _mx_pack(codes)
+    blob = wc.encode([("fp4_e2m1", w, shape)], tile=tile, tile_order=1)
+    _check_mx(_run_mx(blob, dev, 0, sc, x), w, sc, x)
+
+
+def test_mx_gemv_small_integers_exact(dev):
+    """e2m1 integers (0..4, 6) at scale 1 and small integer x: every sum is an
+    integer below 2^24, so y must equal the integer product exactly."""
+    rng = np.random.default_rng(82)
+    table = {0: 0, 1: 2, 2: 4, 3: 5, 4: 6, 6: 7}
+    vals = rng.choice([0, 1, 2, 3, 4, 6, -1, -2, -3, -4, -6], (64, 512))
+    codes = np.vectorize(lambda v: table[abs(v)] | (8 if v < 0 else 0))(vals).astype(np.uint8)
+    xi = rng.integers(-40, 41, (37, 512))
+    sc = np.full((64, 512 // 32), 127, np.uint8)
+    blob = wc.encode([("fp4_e2m1", _mx_pack(codes), codes.shape)], tile=(16, 256), tile_order=1)
+    y = _run_mx(blob, dev, 0, sc, _bf16(xi.astype(np.float32)))
+    assert np.array_equal(y, (xi @ vals.T).astype(np.float64))
+
+
+def test_mx_gemv_quantised_layer(dev):
+    """The scaled 8B MXFP4 workload as a serving step would run it: one blob
+    holds the codes (16 x 512 tiles) and the scale bytes; wc_decode brings the
+    scales back, one wc_gemv_mx launch multiplies all seven projections by 16
+    rows of x; sampled rows of y against the oracle."""
+    ts = synth.config(7, div=4)
+    blocks = [t for t in ts if t.dtype == "fp4_e2m1"]
+    scales = [t for t in ts if t.name.endswith(".scales")]
+    assert len(blocks) == len(scales) == 7
+    entries = [(t.dtype, t.data, t.shape) for t in blocks] + [(t.dtype, t.data) for t in scales]
+    blob = wc.encode(entries, tile=(16, 512), tile_order=1)
+    d = wc.to_device(blob, dev)
+    outs = wc.decode_torch(blob, d)
+    dsc = outs[len(blocks):]
+    rng = np.random.default_rng(83)
+    xbits = {}
+    for t in blocks:
+        xbits.setdefault(t.shape[1], _bf16(rng.normal(0, 1.0, (16, t.shape[1]))))
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ys = wc.gemv_mx_torch(blob, d, list(range(len(blocks))), dsc,
+                          [_dev_x(xbits[t.shape[1]], dev) for t in blocks], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    for t, s, y in zip(blocks, scales, ys):
+        rows = np.random.default_rng(t.shape[0]).choice(t.shape[0], 32, replace=False)
+        w = np.ascontiguousarray(t.data.reshape(t.shape[0], -1)[rows])
+        sc = np.ascontiguousarray(s.data.reshape(t.shape[0], -1)[rows])
+        ref, absref = oracle.gemv_mxfp4(w, sc, xbits[t.shape[1]])
+        tol = 2.0 * t.shape[1] * 2.0 ** -24 * absref + 1e-30
+        assert (np.abs(y.cpu().numpy().astype(np.float64)[:, rows] - ref) <= tol).all(), t.name
+
+
+def test_mx_gemv_limits(dev):
+    rng = np.random.default_rng(84)
+    codes = rng.integers(0, 16, (64, 512)).astype(np.uint8)
+    w = _mx_pack(codes)
+    sc = np.full((64, 16), 127, np.uint8)
+    x = _bf16(rng.normal(0, 1.0, (4, 512)))
+    for tile in [(64, 256), (16, 64), (32, 128)]:        # not 16 rows x 128k columns
+        blob = wc.encode([("fp4_e2m1", w, codes.shape)], tile=tile, tile_order=1)
+        with pytest.raises(wc.WcError) as e:
+            _run_mx(blob, dev, 0, sc, x)
+        assert e.value.rc == -5, tile
+    blob = wc.encode([("u4", w, codes.shape)], tile=(16, 128), tile_order=1)
+    with pytest.raises(wc.WcError) as e:                 # int4 codes are not e2m1
+        _run_mx(blob, dev, 0, sc, x)
+    assert e.value.rc == -5
+    blob = wc.encode([("fp4_e2m1", w, codes.shape)], tile=(16, 128), tile_order=1)
+    d = wc.to_device(blob, dev)
+    y = torch.zeros((4, 64), dtype=torch.float32, device=dev)
+    with pytest.raises(wc.WcError) as e:                 # no scales
+        wc.gemv_mx(blob, d.data_ptr(), [0], [0], [_dev_x(x, dev).data_ptr()], 4, [y.data_ptr()])
+    assert e.value.rc == -1
+    with pytest.raises(wc.WcError) as e:                 # 65 rows of x
+        wc.gemv_mx(blob, d.data_ptr(), [0], [1], [_dev_x(x, dev).data_ptr()], 65, [y.data_ptr()])
+    assert e.value.rc == -1
