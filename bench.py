@@ -249,6 +249,9 @@ def main() -> int:
                          "with e8m0 scales per 32, bf16 x, fp32 y; M rows, 1..64) over the "
                          "seven projections of the 8B MXFP4 layer in 16 x 2048 tiles, next to "
                          "the same product unfused and on the weights kept as bf16")
+    ap.add_argument("--mx-bytes", action="store_true",
+                    help="--gemv-mx: code the packed e2m1 bytes as byte symbols (WC_U8) "
+                         "instead of nibble symbols: half the decode steps")
     ap.add_argument("--fp8-format", choices=["e4m3", "e5m2"], default="e4m3",
                     help="fp8 format of --gemv-fp8 (the llama3-8b-layer-fp8-e4m3 or "
                          "-fp8-e5m2 workload)")
@@ -905,8 +908,13 @@ def gemv_mx_bench(args, dev) -> int:
     blocks = [t for t in ts if t.dtype == "fp4_e2m1"]
     scales = [t for t in ts if t.name.endswith(".scales")]
     shapes = [t.shape for t in blocks]
-    blob = wc.encode([(t.dtype, t.data, t.shape) for t in blocks], lanes=64, tile=tile,
-                     tile_order=1, threads=args.threads)
+    if args.mx_bytes:
+        blob = wc.encode([("u8", t.data, (t.shape[0], t.shape[1] // 2)) for t in blocks],
+                         lanes=64, tile=(tile[0], tile[1] // 2), tile_order=1,
+                         threads=args.threads)
+    else:
+        blob = wc.encode([(t.dtype, t.data, t.shape) for t in blocks], lanes=64, tile=tile,
+                         tile_order=1, threads=args.threads)
     dblob = wc.to_device(blob, dev)
     dsc = [torch.from_numpy(np.ascontiguousarray(s.data).reshape(-1)).to(dev) for s in scales]
     lut = torch.tensor([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0,
@@ -995,7 +1003,8 @@ def gemv_mx_bench(args, dev) -> int:
         "dtype": "fp4 e2m1 x e8m0 (as bf16) x bf16 -> fp32",
         "data": "synthetic",
         "config": {"workload": workload, "mode": "fused-gemv-mx", "m": M,
-                   "tile": f"{tile[0]}x{tile[1]}", "tile_order": "column-blocks",
+                   "tile": f"{tile[0]}x{tile[1]} codes", "tile_order": "column-blocks",
+                   "symbols": "bytes (two codes)" if args.mx_bytes else "e2m1 nibbles",
                    "product": "v_cvt_scalef32_pk_bf16_fp4 + v_mfma_f32_16x16x32_bf16",
                    "lanes": 64, "code_bytes_per_step": wbytes, "scale_bytes_per_step": sbytes,
                    "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},

@@ -247,9 +247,11 @@ wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n, const u
  * while the weights stay in bf16's normal range) and four
  * v_mfma_f32_16x16x32_bf16 multiply it by x.
  *   tensors    host array of n tensor indices; each W must be WC_FP4_E2M1
- *              with a shape (N = rows, K = cols in codes), coded with 64 lanes
- *              in column-block tiles (WC_TILE_COLUMN_BLOCKS) of 16 rows and a
- *              multiple of 128 columns;
+ *              with a shape (N = rows, K = cols in codes), or WC_U8 holding
+ *              the same packed bytes (two codes per byte symbol, even code in
+ *              the low nibble: half the decode steps; shape N x K/2 bytes),
+ *              coded with 64 lanes in column-block tiles
+ *              (WC_TILE_COLUMN_BLOCKS) of 16 rows and a multiple of 128 codes;
  *   dev_scales host array of n device pointers to the e8m0 scale bytes of
  *              each W, N x K/32 row-major (e.g. decoded by wc_decode from the
  *              same blob); 255 reads as NaN;

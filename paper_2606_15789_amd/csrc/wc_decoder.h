@@ -602,11 +602,14 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   // kF8: 0 no fp8; fp8 weights as bf16 (bf16 x, fp32 sums) of format 1 e4m3, 2 e5m2;
   // 3 MXFP4 weights (e2m1 nibbles, an e8m0 scale per 32-weight lane-group) as bf16
   static_assert(kF8 == 0 || ((kF8 == 1 || kF8 == 2) && kMfma && G == 4) ||
-                    (kF8 == 3 && kMfma && G == 8 && kMR == 16 && !kShare),
+                    (kF8 == 3 && kMfma && (G == 8 || G == 4) && kMR == 16 && !kShare),
                 "fp8 weights: the byte MFMA path, e4m3 or e5m2; MXFP4: the nibble path");
   constexpr bool kInt8 = kMfma && G == 4 && kF8 == 0;  // int8 W and x, int32 sums (W8A8)
-  constexpr bool kFp8W = kMfma && G == 4 && kF8 != 0;  // fp8 W as bf16, bf16 x, fp32 sums
-  constexpr bool kMx = kMfma && G == 8;                // MXFP4 W as bf16, bf16 x, fp32 sums
+  constexpr bool kFp8W = kMfma && G == 4 && (kF8 == 1 || kF8 == 2);  // fp8 W as bf16, bf16 x
+  // MXFP4 W as bf16, bf16 x: e2m1 nibble symbols (G = 8), or the packed bytes
+  // of two codes as byte symbols (G = 4: two x columns per symbol)
+  constexpr bool kMx = kMfma && kF8 == 3;
+  constexpr uint32_t kEPS = kMx && G == 4 ? 2u : 1u;  // x columns per symbol
   static_assert(kMR == 16 || kMR == 32 || kMR == 64, "MFMA tiles of 16, 32 or 64 rows");
   constexpr int kMM = kMR == 64 ? 32 : kMR;   // x rows per MFMA block
   constexpr int kNB = kMR == 64 ? 2 : 1;      // MFMA output blocks of W rows per tile
@@ -697,7 +700,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   typedef __attribute__((ext_vector_type(4))) unsigned int u4v;
   constexpr uint32_t kXB = (G == 2 || kFp8W || kMx) ? 2u : 1u;  // bytes of an x element
   // bytes of an x row one wave row covers: 64 lane-groups of W columns over kMR rows
-  constexpr uint32_t kRowXBytes = 64u * W / kMR * kXB;
+  constexpr uint32_t kRowXBytes = 64u * W * kEPS / kMR * kXB;
   typedef __attribute__((ext_vector_type(4))) int i32x4;
   facc macc[kMfma && !kShare && !kInt8 ? kMB : 1][kNB];
   i32x4 iacc[kInt8 ? kMB : 1];                   // int8 GEMM: 16 x 16 int32 sums per block
@@ -709,7 +712,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   u4v xm[kMx ? kMB : 1][3];  // MXFP4 weights: x columns 8..31 of the lane's 32
   uint32_t mxe = 0;          // MXFP4: the e8m0 scale byte of this lane's lane-group
   // the x rows (fused GEMM on the matrix cores): a.m rows of K bf16
-  const uint32_t K = T.ntc << T.log_tc;  // columns of W = length of an x row
+  const uint32_t K = (T.ntc << T.log_tc) * kEPS;  // columns of W = length of an x row
   // (the shared GEMM reads packed x: rows rounded up to blocks of 32)
   const __amdgpu_buffer_rsrc_t xrs = make_rsrc(
       reinterpret_cast<const void*>(T.x),
@@ -726,7 +729,8 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
       for (int nb = 0; nb < kNB; nb++) macc[kInt8 ? 0 : mb][nb] = facc{};
     }
     // this lane's W x values of wave row 0: row sub mod kMM, columns W (sub div kMM) ..
-    xoff = ((sub % kMM) * K + (chunk0 % T.ntc) * (1u << T.log_tc) + W * (sub / kMM)) * kXB;
+    xoff = ((sub % kMM) * K + (chunk0 % T.ntc) * (kEPS << T.log_tc) + W * kEPS * (sub / kMM)) *
+           kXB;
     xblk = kXB * kMM * K;  // bytes of kMM rows of x
   }
   // MXFP4: the scales of W row n, one per 32 columns; the lane-group of this
@@ -735,7 +739,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
       reinterpret_cast<const void*>(kMx ? T.scales : 0ull),
       kMx ? (T.n_chunks / T.ntc) * 16u * (K / 32u) : 0u);
   const uint32_t moff = kMx ? ((chunk0 / T.ntc) * 16u + sub % 16u) * (K / 32u) +
-                                  (chunk0 % T.ntc) * ((1u << T.log_tc) / 32u) + sub / 16u
+                                  (chunk0 % T.ntc) * ((kEPS << T.log_tc) / 32u) + sub / 16u
                             : 0u;
 
   // group g of the chunk, j = g mod kUnroll (static)

@@ -636,6 +636,18 @@ def _mx_pack(codes):
     return (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
 
 
+CODINGS = ["nibbles", "bytes"]
+
+
+def _mx_encode(packed, rows, cols, tile, coding, **kw):
+    """Blob of MXFP4 codes as e2m1 nibble symbols, or their packed bytes as u8
+    byte symbols (tile columns in bytes)."""
+    if coding == "nibbles":
+        return wc.encode([("fp4_e2m1", packed, (rows, cols))], tile=tile, tile_order=1, **kw)
+    return wc.encode([("u8", packed, (rows, cols // 2))], tile=(tile[0], tile[1] // 2),
+                     tile_order=1, **kw)
+
+
 def _run_mx(blob, dev, t, scales, x_bits, expect_err=0):
     d = wc.to_device(blob, dev)
     err = torch.zeros(1, dtype=torch.int32, device=dev)
@@ -653,8 +665,9 @@ def _check_mx(y, w, sc, x):
     assert not bad.any(), (np.argwhere(bad)[:5], float(np.abs(y - ref).max()))
 
 
+@pytest.mark.parametrize("coding", CODINGS)
 @pytest.mark.parametrize("varied", [False, True])
-def test_mx_gemv_every_code_exact(dev, varied):
+def test_mx_gemv_every_code_exact(dev, varied, coding):
     """Every e2m1 code in every position of a lane-group, picked out by one-hot
     rows of x in the first and the last MX block of a tile row: y must be the
     code's value times its block's scale exactly (fp32 holds every product),
@@ -671,7 +684,7 @@ def test_mx_gemv_every_code_exact(dev, varied):
     x = np.zeros((len(picks), cols), np.float32)
     for m, c in enumerate(picks):
         x[m, c] = 1.0
-    blob = wc.encode([("fp4_e2m1", _mx_pack(codes), (rows, cols))], tile=(16, 256), tile_order=1)
+    blob = _mx_encode(_mx_pack(codes), rows, cols, (16, 256), coding)
     y = _run_mx(blob, dev, 0, sc, _bf16(x))
     want = np.array([[oracle.e2m1_value(int(codes[r, c])) * oracle.e8m0_value(int(sc[r, c // 32]))
                       for r in range(rows)] for c in picks])
@@ -681,20 +694,22 @@ def test_mx_gemv_every_code_exact(dev, varied):
 @pytest.mark.parametrize("shape,tile", [((64, 512), (16, 128)), ((48, 1024), (16, 256)),
                                         ((256, 4096), (16, 4096))])
 @pytest.mark.parametrize("m", [1, 5, 16, 17, 33, 64])
-def test_mx_gemv_matches_the_reference(dev, shape, tile, m):
+@pytest.mark.parametrize("coding", CODINGS)
+def test_mx_gemv_matches_the_reference(dev, shape, tile, m, coding):
     """MXFP4 tiles of 16 rows, converted to bf16 with their block scales while
     decoded: y within the fp32 summation bound of the oracle's fp64 product."""
-    say("mx gemv", shape, tile, m)
+    say("mx gemv", shape, tile, m, coding)
     rng = np.random.default_rng(shape[1] + 13 * m)
     codes = rng.integers(0, 16, shape).astype(np.uint8)
     sc = rng.integers(112, 140, (shape[0], shape[1] // 32)).astype(np.uint8)
     x = _bf16(rng.normal(0, 1.0, (m, shape[1])))
     w = _mx_pack(codes)
-    blob = wc.encode([("fp4_e2m1", w, shape)], tile=tile, tile_order=1)
+    blob = _mx_encode(w, shape[0], shape[1], tile, coding)
     _check_mx(_run_mx(blob, dev, 0, sc, x), w, sc, x)
 
 
-def test_mx_gemv_small_integers_exact(dev):
+@pytest.mark.parametrize("coding", CODINGS)
+def test_mx_gemv_small_integers_exact(dev, coding):
     """e2m1 integers (0..4, 6) at scale 1 and small integer x: every sum is an
     integer below 2^24, so y must equal the integer product exactly."""
     rng = np.random.default_rng(82)
@@ -703,12 +718,13 @@ def test_mx_gemv_small_integers_exact(dev):
     codes = np.vectorize(lambda v: table[abs(v)] | (8 if v < 0 else 0))(vals).astype(np.uint8)
     xi = rng.integers(-40, 41, (37, 512))
     sc = np.full((64, 512 // 32), 127, np.uint8)
-    blob = wc.encode([("fp4_e2m1", _mx_pack(codes), codes.shape)], tile=(16, 256), tile_order=1)
+    blob = _mx_encode(_mx_pack(codes), 64, 512, (16, 256), coding)
     y = _run_mx(blob, dev, 0, sc, _bf16(xi.astype(np.float32)))
     assert np.array_equal(y, (xi @ vals.T).astype(np.float64))
 
 
-def test_mx_gemv_quantised_layer(dev):
+@pytest.mark.parametrize("coding", CODINGS)
+def test_mx_gemv_quantised_layer(dev, coding):
     """The scaled 8B MXFP4 workload as a serving step would run it: one blob
     holds the codes (16 x 512 tiles) and the scale bytes; wc_decode brings the
     scales back, one wc_gemv_mx launch multiplies all seven projections by 16
@@ -717,8 +733,12 @@ def test_mx_gemv_quantised_layer(dev):
     blocks = [t for t in ts if t.dtype == "fp4_e2m1"]
     scales = [t for t in ts if t.name.endswith(".scales")]
     assert len(blocks) == len(scales) == 7
-    entries = [(t.dtype, t.data, t.shape) for t in blocks] + [(t.dtype, t.data) for t in scales]
-    blob = wc.encode(entries, tile=(16, 512), tile_order=1)
+    if coding == "nibbles":
+        entries = [(t.dtype, t.data, t.shape) for t in blocks]
+    else:
+        entries = [("u8", t.data, (t.shape[0], t.shape[1] // 2)) for t in blocks]
+    entries += [(t.dtype, t.data) for t in scales]
+    blob = wc.encode(entries, tile=(16, 512 if coding == "nibbles" else 256), tile_order=1)
     d = wc.to_device(blob, dev)
     outs = wc.decode_torch(blob, d)
     dsc = outs[len(blocks):]
@@ -751,6 +771,10 @@ def test_mx_gemv_limits(dev):
         with pytest.raises(wc.WcError) as e:
             _run_mx(blob, dev, 0, sc, x)
         assert e.value.rc == -5, tile
+    blob = wc.encode([("u8", w, (64, 256))], tile=(16, 32), tile_order=1)
+    with pytest.raises(wc.WcError) as e:                 # byte-coded tile of 64 codes
+        _run_mx(blob, dev, 0, sc, x)
+    assert e.value.rc == -5
     blob = wc.encode([("u4", w, codes.shape)], tile=(16, 128), tile_order=1)
     with pytest.raises(wc.WcError) as e:                 # int4 codes are not e2m1
         _run_mx(blob, dev, 0, sc, x)
