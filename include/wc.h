@@ -3,9 +3,10 @@
  *
  * The library turns near-entropy-bound compressed weight streams back into
  * bit-identical bf16 / fp16 / int8 / int4 / fp8 / fp4 tensors in GPU memory
- * (wc_decode), or multiplies bf16 weights into activations while decoding
- * them, never writing them out (wc_gemv, wc_gemm).  Compression runs on the
- * host (wc_encode) or on the GPU (wc_encode_device), to the same blob.
+ * (wc_decode), or multiplies weights into activations while decoding them,
+ * never writing them out (wc_gemv, wc_gemm: bf16 and fp8; wc_gemm_i8: int8;
+ * wc_gemv_mx: MXFP4).  Compression runs on the host (wc_encode) or on the GPU
+ * (wc_encode_device), to the same blob.
  *
  * Paper: "Approaching Shannon Bound with Lossless LLM Weight Compression"
  * (Tan, Chen, Alonso, Wong, He).
