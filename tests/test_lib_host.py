@@ -206,6 +206,40 @@ def test_gemv_rejects_before_any_launch():
         assert e.value.rc == -5
 
 
+def test_gemv_mx_rejects_before_any_launch():
+    """wc_gemv_mx validates every argument and tensor on the host and returns
+    before any HIP call; the fake device addresses are never touched."""
+    codes = np.random.default_rng(4).integers(0, 16, (64, 512)).astype(np.uint8)
+    w = (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
+    nib = wc.encode([("fp4_e2m1", w, (64, 512))], tile=(16, 256), tile_order=1)
+    for m in (0, 65):
+        with pytest.raises(wc.WcError) as e:
+            wc.gemv_mx(nib, 16, [0], [16], [16], m, [16])
+        assert e.value.rc == -1
+    for args in (([0], [0], [16], [16]),           # no scales
+                 ([0], [16], [8], [16]),           # x not 16-byte aligned
+                 ([1], [16], [16], [16]),          # no such tensor
+                 ([0], [16], [16], [0]),           # no y
+                 ([], [], [], []),                 # no jobs
+                 ([0] * 33, [16] * 33, [16] * 33, [16] * 33)):
+        with pytest.raises(wc.WcError) as e:
+            wc.gemv_mx(nib, 16, args[0], args[1], args[2], 1, args[3])
+        assert e.value.rc == -1, args
+    unsupported = [
+        wc.encode([("fp4_e2m1", w, (64, 512))], tile=(64, 256), tile_order=1),   # 64-row tiles
+        wc.encode([("fp4_e2m1", w, (64, 512))], tile=(16, 64), tile_order=1),    # 64 codes wide
+        wc.encode([("fp4_e2m1", w, (64, 512))], tile=(16, 256), tile_order=0),   # row-major tiles
+        wc.encode([("fp4_e2m1", w, (64, 512))]),                                 # byte runs
+        wc.encode([("u4", w, (64, 512))], tile=(16, 256), tile_order=1),         # int4 codes
+        wc.encode([("u8", w, (64, 256))], tile=(16, 32), tile_order=1),          # 64 codes as bytes
+        wc.encode([("fp4_e2m1", w, (64, 512))], lanes=32, tile=(16, 256), tile_order=1),
+    ]
+    for b in unsupported:
+        with pytest.raises(wc.WcError) as e:
+            wc.gemv_mx(b, 16, [0], [16], [16], 1, [16])
+        assert e.value.rc == -5
+
+
 def test_gemm_workspace_bytes():
     """One packed x per distinct (pointer, K): rows rounded up to 32, bf16,
     each slot rounded up to 256 bytes; nothing below 65 rows."""
