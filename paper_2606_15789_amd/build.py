@@ -58,6 +58,24 @@ def kernel_fingerprints(asm: str) -> dict:
     return out
 
 
+# A plain-C client of the ABI (no Python), built next to the library.
+EXAMPLE_SRC = os.path.join(CSRC, "wc_example.c")
+EXAMPLE = os.path.join(HERE, "wc_example")
+
+
+def build_example() -> str:
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(HIPCC)))
+    cmd = ["gcc", "-std=c99", "-O2", "-Wall", "-D__HIP_PLATFORM_AMD__",
+           f"-I{rocm}/include", EXAMPLE_SRC, "-o", EXAMPLE + ".tmp", f"-L{HERE}", "-lwc",
+           f"-L{rocm}/lib", "-lamdhip64", "-lm", "-Wl,-rpath,$ORIGIN", f"-Wl,-rpath,{rocm}/lib"]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError("C example build failed: " + " ".join(cmd))
+    os.replace(EXAMPLE + ".tmp", EXAMPLE)
+    return EXAMPLE
+
+
 def build(verbose: bool = False) -> str:
     import json
     import tempfile
@@ -92,6 +110,7 @@ def build(verbose: bool = False) -> str:
         json.dump(prints, fh, indent=1, sort_keys=True)
     os.replace(KERNELS + ".tmp", KERNELS)
     os.replace(tmp, LIB)
+    build_example()
     return LIB
 
 
