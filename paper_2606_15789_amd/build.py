@@ -114,6 +114,14 @@ def build(verbose: bool = False) -> str:
     return LIB
 
 
+def ensure_example() -> str:
+    """The C example, built (host code only, seconds) when it is missing."""
+    ensure_built()
+    if not os.path.exists(EXAMPLE):
+        build_example()
+    return EXAMPLE
+
+
 def ensure_built() -> str:
     """Build only when nothing is built yet (tests and benches call this)."""
     if not os.path.exists(LIB):

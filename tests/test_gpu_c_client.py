@@ -7,17 +7,17 @@ import subprocess
 
 import pytest
 
-pytestmark = pytest.mark.gpu
+from paper_2606_15789_amd import build
 
-EXE = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))),
-                   "paper_2606_15789_amd", "wc_example")
+pytestmark = pytest.mark.gpu
 
 
 def test_plain_c_client():
     torch = pytest.importorskip("torch")
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
-    assert os.path.exists(EXE), "build the package first (it builds the C example)"
-    r = subprocess.run([EXE], capture_output=True, text=True, timeout=120)
+    exe = build.ensure_example()
+    assert os.path.exists(exe)
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, (r.stdout, r.stderr)
     assert "bit-exact" in r.stdout and "matches fp64" in r.stdout, r.stdout
