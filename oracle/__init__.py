@@ -93,6 +93,10 @@ def lib():
         L.orc_e2m1_value.restype = C.c_double
         L.orc_e8m0_value.argtypes = [C.c_uint8]
         L.orc_e8m0_value.restype = C.c_double
+        L.orc_fp16_value.argtypes = [C.c_uint16]
+        L.orc_fp16_value.restype = C.c_double
+        L.orc_gemv_int4.argtypes = [C.c_void_p, C.c_void_p, C.c_void_p, C.c_uint64, C.c_uint64,
+                                    C.c_void_p, C.c_uint32, C.c_void_p, C.c_void_p]
         L.orc_gemv_mxfp4.argtypes = [C.c_void_p, C.c_void_p, C.c_uint64, C.c_uint64, C.c_void_p,
                                      C.c_uint32, C.c_void_p, C.c_void_p]
         L.orc_free.argtypes = [C.c_void_p]
@@ -381,6 +385,36 @@ def gemv_mxfp4(w, scales, x):
     rc = lib().orc_gemv_mxfp4(_ptr(w), _ptr(scales), rows, cols, _ptr(x), M, _ptr(y), _ptr(a))
     if rc:
         raise OracleError(rc, "gemv_mxfp4")
+    return y, a
+
+
+def fp16_value(h: int) -> float:
+    """The value of one IEEE binary16 storage word."""
+    return lib().orc_fp16_value(h)
+
+
+def gemv_int4(w, scales, zeros, x):
+    """(y, sum |x w|) in fp64 for group-quantised int4 weights: w the packed
+    codes (rows x cols/2 bytes, even element low), scales fp16 storage words
+    (rows x cols/128), zeros one byte per group (rows x cols/128; codes
+    unsigned, weight s (q - z)) or None (two's-complement codes, weight s q),
+    x bf16 storage words (M x cols)."""
+    w = np.ascontiguousarray(w, dtype=np.uint8)
+    scales = np.ascontiguousarray(scales, dtype=np.uint16)
+    x = np.ascontiguousarray(x, dtype=np.uint16)
+    rows, cols = w.shape[0], 2 * w.shape[1]
+    M = x.shape[0]
+    assert x.shape[1] == cols and scales.shape == (rows, cols // 128)
+    zp = None
+    if zeros is not None:
+        zeros = np.ascontiguousarray(zeros, dtype=np.uint8)
+        assert zeros.shape == (rows, cols // 128)
+        zp = _ptr(zeros)
+    y = np.empty((M, rows), np.float64)
+    a = np.empty((M, rows), np.float64)
+    rc = lib().orc_gemv_int4(_ptr(w), _ptr(scales), zp, rows, cols, _ptr(x), M, _ptr(y), _ptr(a))
+    if rc:
+        raise OracleError(rc, "gemv_int4")
     return y, a
 
 

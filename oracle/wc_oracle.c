@@ -1066,6 +1066,44 @@ int orc_gemv_mxfp4(const uint8_t* w, const uint8_t* scales, uint64_t rows, uint6
   return ORC_OK;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Group-quantised int4 weights (the paper's int4 and awq4 formats, Sec.     */
+/* VI-A): codes two per byte (even element in the low nibble), one fp16      */
+/* scale per 128 consecutive weights of a row, and either a zero point per   */
+/* group (unsigned codes q, weight s (q - z); zeros one byte per group) or   */
+/* none (two's-complement codes, weight s q).  What the fused decode-GEMM    */
+/* computes: y[m][n] = sum_k x[m][k] * w[n][k], in fp64, summed in k order;  */
+/* abs_out as for orc_gemv_bf16.                                             */
+
+double orc_fp16_value(uint16_t h) {
+  const int s = h >> 15, e = (h >> 10) & 31, m = h & 1023;
+  double mag;
+  if (e == 31) mag = m ? NAN : INFINITY;
+  else mag = e ? ldexp(1.0 + m / 1024.0, e - 15) : ldexp(m / 1024.0, -14);
+  return s ? -mag : mag;
+}
+
+int orc_gemv_int4(const uint8_t* w, const uint16_t* scales, const uint8_t* zeros, uint64_t rows,
+                  uint64_t cols, const uint16_t* x, uint32_t M, double* y, double* abs_out) {
+  if (!w || !scales || !x || !y || M == 0 || cols % 128) return ORC_EINVAL;
+  for (uint32_t m = 0; m < M; m++)
+    for (uint64_t n = 0; n < rows; n++) {
+      double s = 0.0, a = 0.0;
+      for (uint64_t k = 0; k < cols; k++) {
+        const uint8_t byte = w[(n * cols + k) / 2];
+        const int code = (k & 1) ? byte >> 4 : byte & 15;
+        const uint64_t g = n * (cols / 128) + k / 128;
+        const int q = zeros ? code - (int)zeros[g] : (code ^ 8) - 8;
+        double p = bf16_value(x[(uint64_t)m * cols + k]) * (orc_fp16_value(scales[g]) * q);
+        s += p;
+        a += fabs(p);
+      }
+      y[(uint64_t)m * rows + n] = s;
+      if (abs_out) abs_out[(uint64_t)m * rows + n] = a;
+    }
+  return ORC_OK;
+}
+
 /* fmt: 0 = e4m3, 1 = e5m2 */
 int orc_gemv_fp8(const uint8_t* w, uint64_t rows, uint64_t cols, const uint16_t* x, uint32_t M,
                  uint32_t fmt, double* y, double* abs_out) {

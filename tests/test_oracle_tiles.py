@@ -372,3 +372,48 @@ def test_gemv_mxfp4_reference():
     y3, _ = oracle.gemv_mxfp4(wi, sc3, _bf16_of(xi.astype(np.float32)))
     part = (xi[:, 32:64] @ vals[:, 32:64].T).astype(np.float64)
     assert np.array_equal(y3, y + 7 * part)
+
+
+def test_fp16_values_match_numpy():
+    """Every binary16 pattern against numpy's float16 (an independent
+    implementation of the IEEE format)."""
+    ref = np.arange(65536, dtype=np.uint32).astype(np.uint16).view(np.float16).astype(np.float64)
+    got = np.array([oracle.fp16_value(h) for h in range(65536)])
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+
+
+@pytest.mark.parametrize("with_zeros", [False, True])
+def test_gemv_int4_reference(with_zeros):
+    """One-hot x rows pick scale times (code - zero) or the signed code; small
+    integers at scale 1 give the integer product; a scale of 2^3 on one group
+    scales exactly that group's share of y."""
+    rng = np.random.default_rng(20)
+    rows, cols = 5, 256
+    codes = rng.integers(0, 16, (rows, cols)).astype(np.uint8)
+    w = codes[:, 0::2] | (codes[:, 1::2] << 4)
+    sc = (rng.uniform(0.5, 2.0, (rows, cols // 128)).astype(np.float16)).view(np.uint16)
+    z = rng.integers(0, 16, (rows, cols // 128)).astype(np.uint8) if with_zeros else None
+    def weight(n, k):
+        q = int(codes[n, k]) - int(z[n, k // 128]) if with_zeros else (int(codes[n, k]) ^ 8) - 8
+        return oracle.fp16_value(int(sc[n, k // 128])) * q
+    ks = [0, 127, 128, 255]
+    x = np.zeros((len(ks), cols), np.float32)
+    for m, k in enumerate(ks):
+        x[m, k] = 1.0
+    y, _ = oracle.gemv_int4(w, sc, z, _bf16_of(x))
+    for m, k in enumerate(ks):
+        assert y[m].tolist() == [weight(n, k) for n in range(rows)]
+    # small integers at scale 1
+    one = np.full((rows, cols // 128), 0x3C00, np.uint16)
+    q = np.array([[(int(codes[n, k]) - int(z[n, k // 128]) if with_zeros
+                    else (int(codes[n, k]) ^ 8) - 8) for k in range(cols)] for n in range(rows)])
+    xi = rng.integers(-30, 31, (3, cols))
+    y, a = oracle.gemv_int4(w, one, z, _bf16_of(xi.astype(np.float32)))
+    assert np.array_equal(y, (xi @ q.T).astype(np.float64))
+    assert np.array_equal(a, (np.abs(xi) @ np.abs(q).T).astype(np.float64))
+    sc8 = one.copy()
+    sc8[:, 1] = 0x4800                                   # 8.0 in binary16
+    y8, _ = oracle.gemv_int4(w, sc8, z, _bf16_of(xi.astype(np.float32)))
+    assert np.array_equal(y8, y + 7 * (xi[:, 128:] @ q[:, 128:].T).astype(np.float64))
