@@ -249,6 +249,15 @@ def main() -> int:
                          "with e8m0 scales per 32, bf16 x, fp32 y; M rows, 1..64) over the "
                          "seven projections of the 8B MXFP4 layer in 16 x 2048 tiles, next to "
                          "the same product unfused and on the weights kept as bf16")
+    ap.add_argument("--gemv-w4", type=int, default=0, metavar="M",
+                    help="time the fused decode-GEMM on group-quantised int4 weights "
+                         "(wc_gemv_w4: codes as bytes, fp16 scales per 128, zero points; "
+                         "bf16 x, fp32 y; M rows, 1..64) over the seven projections of the "
+                         "8B AWQ-style layer (--w4-signed: the symmetric int4 layer) in "
+                         "16 x 1024-byte tiles, next to the same product unfused and on the "
+                         "weights kept as bf16")
+    ap.add_argument("--w4-signed", action="store_true",
+                    help="--gemv-w4 on the two's-complement int4 layer (no zero points)")
     ap.add_argument("--mx-bytes", action="store_true",
                     help="--gemv-mx: code the packed e2m1 bytes as byte symbols (WC_U8) "
                          "instead of nibble symbols: half the decode steps")
@@ -280,6 +289,8 @@ def main() -> int:
         return gemv_fp8_bench(args, dev)
     if args.gemv_mx:
         return gemv_mx_bench(args, dev)
+    if args.gemv_w4:
+        return gemv_w4_bench(args, dev)
     if args.encode:
         return encode_bench(args, dev)
     if args.sweep:
@@ -1020,6 +1031,155 @@ def gemv_mx_bench(args, dev) -> int:
                          "ms_per_step": round(s_plain * 1e3, 4),
                          "what": "torch.matmul on the weights kept resident as bf16 (4x the "
                                  "fp4 bytes)"},
+        "setup_s": round(setup_s, 1),
+    }
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def gemv_w4_bench(args, dev) -> int:
+    """Fused decode-GEMM over the seven int4 projections of the 8B AWQ-style layer
+    (or the symmetric int4 layer): codes as the blob's bytes, fp16 scales and
+    zero points decoded once, bf16 x, fp32 y; checked against torch's fp32
+    product of the same values."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15789_amd import synth, wc
+    M = args.gemv_w4
+    if not 1 <= M <= 64:
+        print("--gemv-w4 takes 1..64 rows of activations", file=sys.stderr)
+        return 2
+    workload = "llama3-8b-layer-int4" if args.w4_signed else "llama3-8b-layer-awq4"
+    tile = (16, 1024)   # bytes: 2048 codes
+    t0 = time.perf_counter()
+    ts = synth.config(WORKLOADS[workload])
+    codes = [t for t in ts if t.name.endswith(".qweight")]
+    scales = [t for t in ts if t.name.endswith(".scales")]
+    zeros = [t for t in ts if t.name.endswith(".qzeros")]
+    shapes = [t.shape for t in codes]
+    blob = wc.encode([("u8", t.data, (t.shape[0], t.shape[1] // 2)) for t in codes], lanes=64,
+                     tile=tile, tile_order=1, threads=args.threads)
+    dblob = wc.to_device(blob, dev)
+    dsc = [torch.from_numpy(np.ascontiguousarray(s.data).reshape(-1).view(np.int16)).to(dev)
+           for s in scales]
+    dz = None
+    if zeros:
+        dz = []
+        for z in zeros:
+            zp = torch.from_numpy(np.ascontiguousarray(z.data).reshape(-1)).to(dev)
+            dz.append(torch.stack([zp & 15, zp >> 4], dim=1).reshape(-1).contiguous())
+
+    def dequant(packed, j, shp):
+        """bf16 weights s (q - z) or s q of packed codes (as exact as bf16 allows)."""
+        p = packed.view(shp[0], shp[1] // 2)
+        q = torch.stack([p & 15, p >> 4], dim=2).reshape(shp).int()
+        if dz is None:
+            q = (q ^ 8) - 8
+        else:
+            q = q - dz[j].view(shp[0], shp[1] // 128).int().repeat_interleave(128, dim=1)
+        s = dsc[j].view(torch.float16).float().view(shp[0], shp[1] // 128)
+        return (q.float() * s.repeat_interleave(128, dim=1)).to(torch.bfloat16)
+
+    Wb = [dequant(torch.from_numpy(np.ascontiguousarray(t.data).reshape(-1)).to(dev), j, shp)
+          for j, (t, shp) in enumerate(zip(codes, shapes))]
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(24601)
+    xs = [torch.randn(M, shp[1], generator=gen, device=dev).to(torch.bfloat16) for shp in shapes]
+    ys = [torch.zeros(M, shp[0], dtype=torch.float32, device=dev) for shp in shapes]
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    def fused():
+        wc.gemv_w4(blob, dblob.data_ptr(), list(range(len(codes))), [s.data_ptr() for s in dsc],
+                   None if dz is None else [z.data_ptr() for z in dz],
+                   [x.data_ptr() for x in xs], M, [y.data_ptr() for y in ys],
+                   stream.cuda_stream, err.data_ptr())
+
+    fused()
+    torch.cuda.synchronize()
+    if int(err.item()):
+        raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
+    for t, (x, y, shp) in enumerate(zip(xs, ys, shapes)):
+        # reference in fp32 from the exact weights s (q - z) (the bf16 copy rounds them)
+        p = torch.from_numpy(np.ascontiguousarray(codes[t].data).reshape(-1)).to(dev)
+        p = p.view(shp[0], shp[1] // 2)
+        q = torch.stack([p & 15, p >> 4], dim=2).reshape(shp).int()
+        q = (q ^ 8) - 8 if dz is None else \
+            q - dz[t].view(shp[0], shp[1] // 128).int().repeat_interleave(128, dim=1)
+        s = dsc[t].view(torch.float16).float().view(shp[0], shp[1] // 128).repeat_interleave(128, 1)
+        w = q.float() * s
+        ref = x.float() @ w.t()
+        bound = x.float().abs() @ (s.abs() * 40.0).t()
+        if torch.any((y - ref).abs() > 1e4 * 2.0 ** -24 * bound + 1e-30):
+            raise RuntimeError(f"int4 fused GEMM tensor {t} outside the fp32 error bound")
+    setup_s = time.perf_counter() - t0
+
+    flat = wc.encode([("u8", np.ascontiguousarray(t.data).reshape(-1)) for t in codes],
+                     lanes=64, threads=args.threads)
+    dflat = wc.to_device(flat, dev)
+    outs = [torch.empty(n, dtype=torch.uint8, device=dev) for n in flat.out_bytes]
+
+    def unfused():
+        wc.decode(flat, dflat.data_ptr(), [o.data_ptr() for o in outs], stream.cuda_stream,
+                  err.data_ptr())
+        for j, (o, x, shp) in enumerate(zip(outs, xs, shapes)):
+            torch.matmul(x, dequant(o, j, shp).t())
+
+    def uncompressed():
+        for w, x in zip(Wb, xs):
+            torch.matmul(x, w.t())
+
+    def timed(fn):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(args.steps):
+            fn()
+        b.record(stream)
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / args.steps / 1e3
+
+    s_fused, s_unfused, s_plain = timed(fused), timed(unfused), timed(uncompressed)
+    if int(err.item()):
+        raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
+    wbytes = sum(blob.out_bytes)
+    aux = sum(s.numel() * 2 for s in dsc) + (sum(z.numel() for z in dz) if dz else 0)
+    alg = blob.size + aux + sum(x.numel() * 2 for x in xs) + sum(2 * y.numel() * 4 for y in ys)
+    achieved = alg / s_fused / 1e9
+    line = {
+        "metric": METRIC + " [fused int4 decode-GEMM]",
+        "value": round(wbytes / s_fused / 1e9, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(s_fused * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "int4 x fp16 scale (as bf16 16 + t) x bf16 -> fp32",
+        "data": "synthetic",
+        "config": {"workload": workload, "mode": "fused-gemv-w4", "m": M,
+                   "tile": f"{tile[0]}x{tile[1]} bytes", "tile_order": "column-blocks",
+                   "zero_points": dz is not None,
+                   "product": "v_perm + v_lshl_or to bf16 + v_mfma_f32_16x16x32_bf16 (x and ones)",
+                   "lanes": 64, "code_bytes_per_step": wbytes, "aux_bytes_per_step": aux,
+                   "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "kernel": "wc_gemv_w4_kernel", "mean_step_us": round(s_fused * 1e6, 2),
+                     "algorithmic_bytes_per_step": int(alg)},
+        "unfused": {"value": round(wbytes / s_unfused / 1e9, 2), "unit": "GB/s",
+                    "ms_per_step": round(s_unfused * 1e3, 4),
+                    "what": "wc_decode of the codes (64 KiB byte-run chunks), torch dequantisation "
+                            "to bf16 with scales and zero points, torch.matmul per tensor"},
+        "uncompressed": {"value": round(wbytes / s_plain / 1e9, 2), "unit": "GB/s",
+                         "ms_per_step": round(s_plain * 1e3, 4),
+                         "what": "torch.matmul on the dequantised weights kept resident as bf16 "
+                                 "(4x the int4 bytes)"},
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line), flush=True)

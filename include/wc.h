@@ -5,7 +5,7 @@
  * bit-identical bf16 / fp16 / int8 / int4 / fp8 / fp4 tensors in GPU memory
  * (wc_decode), or multiplies weights into activations while decoding them,
  * never writing them out (wc_gemv, wc_gemm: bf16 and fp8; wc_gemm_i8: int8;
- * wc_gemv_mx: MXFP4).  Compression runs on the host (wc_encode) or on the GPU
+ * wc_gemv_mx: MXFP4; wc_gemv_w4: int4 with group scales).  Compression runs on the host (wc_encode) or on the GPU
  * (wc_encode_device), to the same blob.
  *
  * Paper: "Approaching Shannon Bound with Lossless LLM Weight Compression"
@@ -268,6 +268,37 @@ wc_status wc_gemv_mx(const wc_blob* desc, const void* dev_blob, uint32_t n, cons
                      const uint8_t* const* dev_scales, const void* const* dev_x, uint32_t m,
                      float* const* dev_y, void* stream, int32_t* dev_err);
 
+/* wc_gemv_w4 -- the fused decode-GEMM for group-quantised int4 weights (the
+ * paper's int4 and awq4 formats, Sec. VI-A; Alg. 1 / 3): for each of n jobs
+ * i, dev_y[i] += x_i * W_i^T with W_i[n][k] = s[n][k / 128] * (q - z[n][k /
+ * 128]) for unsigned codes q and zero points z, or s * q for two's-complement
+ * codes, the codes decoded on the fly and never written.  Each code becomes the
+ * bf16 value 16 + t exactly (t = q, or the signed code + 8); the products with
+ * x and with ones (the group's sums of x) go through v_mfma_f32_16x16x32_bf16,
+ * and y gains s (sum x (16 + t) - (16 + z or 24) sum x) per group, in fp32.
+ *   tensors    host array of n tensor indices; each W must be WC_U8 holding
+ *              the packed codes (two per byte, even element in the low nibble;
+ *              shape N x K/2 bytes), coded with 64 lanes in column-block tiles
+ *              (WC_TILE_COLUMN_BLOCKS) of 16 rows and a multiple of 64 bytes
+ *              (128 codes: a 16-row wave row is one group of each row);
+ *   dev_scales host array of n device pointers to the fp16 scales of each W,
+ *              N x K/128 row-major, 2-byte aligned;
+ *   dev_zeros  NULL (every W has two's-complement codes), or a host array of
+ *              n device pointers: NULL for a W with two's-complement codes, or
+ *              its zero points, one byte (0..15) per group, N x K/128;
+ *   dev_x      host array of n device pointers to bf16 x, m x K row-major,
+ *              16-byte aligned;
+ *   m          1..64 rows of x, the same for every job;
+ *   dev_y      host array of n device pointers to float y, m x N row-major;
+ *              the products are added with fp32 atomics, as in wc_gemv;
+ *   stream, dev_err as for wc_decode.
+ * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument) or
+ * WC_EUNSUPPORTED (a tensor the path does not take). */
+wc_status wc_gemv_w4(const wc_blob* desc, const void* dev_blob, uint32_t n, const uint32_t* tensors,
+                     const uint16_t* const* dev_scales, const uint8_t* const* dev_zeros,
+                     const void* const* dev_x, uint32_t m, float* const* dev_y, void* stream,
+                     int32_t* dev_err);
+
 /* wc_gemm_i8 -- the fused decode-GEMM for int8 weights and int8 activations
  * (W8A8, the SmoothQuant-style sq8 format of Sec. VI-A; Alg. 1 / 3): for each
  * of n jobs i, dev_y[i] += x_i * W_i^T in exact integer arithmetic, W_i =
@@ -382,7 +413,7 @@ wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_params* p, 
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);
 
-/* wc_version -- ABI version of this header (7). */
+/* wc_version -- ABI version of this header (8). */
 int32_t wc_version(void);
 
 #ifdef __cplusplus

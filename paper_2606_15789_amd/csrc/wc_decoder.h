@@ -71,7 +71,10 @@ enum Kind : uint32_t { kSplit16 = 0, kByte = 1, kNibble = 2 };
 struct DevTensor {
   uint64_t dst;          // device pointer of the decoded tensor
   uint64_t freq_off;     // u16 frequency table (blob offset)
-  uint64_t raw_off;      // raw bytes (blob offset), 16-bit formats only
+  union {
+    uint64_t raw_off;    // raw bytes (blob offset), 16-bit formats only
+    uint64_t zeros;      // fused int4 GEMM: device zero points, [N][K / 128] bytes, or 0
+  };
   uint64_t n_sym;        // coded symbols in the tensor
   union {
     uint64_t raw_padded;  // bytes of the (16-B padded) raw region, 16-bit formats only
@@ -600,16 +603,21 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
                                        !kShare))),
                 "MFMA GEMM: bf16 tiles, or int8 / fp8 / MXFP4 tiles of 16 rows");
   // kF8: 0 no fp8; fp8 weights as bf16 (bf16 x, fp32 sums) of format 1 e4m3, 2 e5m2;
-  // 3 MXFP4 weights (e2m1 nibbles, an e8m0 scale per 32-weight lane-group) as bf16
+  // 3 MXFP4 weights (e2m1 nibbles, an e8m0 scale per 32-weight lane-group) as bf16;
+  // 4 group-quantised int4 weights (codes as bytes, fp16 scale per 128) as bf16
   static_assert(kF8 == 0 || ((kF8 == 1 || kF8 == 2) && kMfma && G == 4) ||
-                    (kF8 == 3 && kMfma && (G == 8 || G == 4) && kMR == 16 && !kShare),
-                "fp8 weights: the byte MFMA path, e4m3 or e5m2; MXFP4: the nibble path");
+                    (kF8 == 3 && kMfma && (G == 8 || G == 4) && kMR == 16 && !kShare) ||
+                    (kF8 == 4 && kMfma && G == 4 && kMR == 16 && !kShare),
+                "fp8 weights: the byte MFMA path; MXFP4: nibbles or bytes; int4: bytes");
   constexpr bool kInt8 = kMfma && G == 4 && kF8 == 0;  // int8 W and x, int32 sums (W8A8)
   constexpr bool kFp8W = kMfma && G == 4 && (kF8 == 1 || kF8 == 2);  // fp8 W as bf16, bf16 x
   // MXFP4 W as bf16, bf16 x: e2m1 nibble symbols (G = 8), or the packed bytes
   // of two codes as byte symbols (G = 4: two x columns per symbol)
   constexpr bool kMx = kMfma && kF8 == 3;
-  constexpr uint32_t kEPS = kMx && G == 4 ? 2u : 1u;  // x columns per symbol
+  // int4 W (two codes per byte symbol) as bf16 16 + t, bf16 x, fp32 sums corrected
+  // per 128-column group: y += s (sum x (16 + t) - c sum x), c = 16 + z or 24
+  constexpr bool kI4 = kMfma && kF8 == 4;
+  constexpr uint32_t kEPS = (kMx || kI4) && G == 4 ? 2u : 1u;  // x columns per symbol
   static_assert(kMR == 16 || kMR == 32 || kMR == 64, "MFMA tiles of 16, 32 or 64 rows");
   constexpr int kMM = kMR == 64 ? 32 : kMR;   // x rows per MFMA block
   constexpr int kNB = kMR == 64 ? 2 : 1;      // MFMA output blocks of W rows per tile
@@ -698,7 +706,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   typedef __attribute__((ext_vector_type(8))) __bf16 bf8;
   typedef __attribute__((ext_vector_type(kMM * kMM / 64))) float facc;
   typedef __attribute__((ext_vector_type(4))) unsigned int u4v;
-  constexpr uint32_t kXB = (G == 2 || kFp8W || kMx) ? 2u : 1u;  // bytes of an x element
+  constexpr uint32_t kXB = (G == 2 || kFp8W || kMx || kI4) ? 2u : 1u;  // bytes of an x element
   // bytes of an x row one wave row covers: 64 lane-groups of W columns over kMR rows
   constexpr uint32_t kRowXBytes = 64u * W * kEPS / kMR * kXB;
   typedef __attribute__((ext_vector_type(4))) int i32x4;
@@ -709,8 +717,10 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   uint32_t prev[kMR == 64 ? 4 : 1];             // 64-row tiles: the even row's dwords
   u4v xa[kMfma ? kMB : 1];
   u4v xa2[kFp8W ? kMB : 1];  // fp8 weights: x columns 8..15 of the lane's 16
-  u4v xm[kMx ? kMB : 1][3];  // MXFP4 weights: x columns 8..31 of the lane's 32
-  uint32_t mxe = 0;          // MXFP4: the e8m0 scale byte of this lane's lane-group
+  u4v xm[kMx || kI4 ? kMB : 1][3];  // MXFP4 / int4 weights: x columns 8..31 of the lane's 32
+  uint32_t mxe = 0;   // MXFP4: the e8m0 scale byte of this lane's lane-group
+  uint32_t i4s = 0;   // int4: the fp16 scale of this lane's W row in this wave row's group
+  uint32_t i4z = 0;   // int4: its zero point
   // the x rows (fused GEMM on the matrix cores): a.m rows of K bf16
   const uint32_t K = (T.ntc << T.log_tc) * kEPS;  // columns of W = length of an x row
   // (the shared GEMM reads packed x: rows rounded up to blocks of 32)
@@ -740,6 +750,17 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
       kMx ? (T.n_chunks / T.ntc) * 16u * (K / 32u) : 0u);
   const uint32_t moff = kMx ? ((chunk0 / T.ntc) * 16u + sub % 16u) * (K / 32u) +
                                   (chunk0 % T.ntc) * ((kEPS << T.log_tc) / 32u) + sub / 16u
+                            : 0u;
+  // int4: fp16 scales and zero points of W row n, one per 128 columns; wave row r
+  // of tile (band, column c) is group c tile_c / 128 + r of the row
+  const bool i4zp = kI4 && T.zeros != 0;
+  const uint32_t i4n = kI4 ? (T.n_chunks / T.ntc) * 16u * (K / 128u) : 0u;  // groups of W
+  const __amdgpu_buffer_rsrc_t srs =
+      make_rsrc(reinterpret_cast<const void*>(kI4 ? T.scales : 0ull), 2u * i4n);
+  const __amdgpu_buffer_rsrc_t zrs =
+      make_rsrc(reinterpret_cast<const void*>(kI4 ? T.zeros : 0ull), i4zp ? i4n : 0u);
+  const uint32_t ioff = kI4 ? ((chunk0 / T.ntc) * 16u + sub % 16u) * (K / 128u) +
+                                  (chunk0 % T.ntc) * ((kEPS << T.log_tc) / 128u)
                             : 0u;
 
   // group g of the chunk, j = g mod kUnroll (static)
@@ -771,7 +792,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
           xa2[mb] = __builtin_bit_cast(
               u4v, __builtin_amdgcn_raw_buffer_load_b128(
                        xrs, xoff + mb * xblk + r * kRowXBytes + 16u, 0, 0));
-        if constexpr (kMx) {
+        if constexpr (kMx || kI4) {
 #pragma unroll
           for (int q = 0; q < 3; q++)
             xm[mb][q] = __builtin_bit_cast(
@@ -780,6 +801,10 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
         }
       }
       if constexpr (kMx) mxe = __builtin_amdgcn_raw_buffer_load_b8(mrs, moff + 4u * r, 0, 0);
+      if constexpr (kI4) {
+        i4s = __builtin_amdgcn_raw_buffer_load_b16(srs, 2u * (ioff + r), 0, 0);
+        i4z = __builtin_amdgcn_raw_buffer_load_b8(zrs, ioff + r, 0, 0);
+      }
     }
     const int nv = kTail ? max(0, min<int>(W, (int)n_lane - (int)(r * kRowSym + sub * W))) : W;
 #pragma unroll
@@ -830,6 +855,45 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
             macc[mb][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, B0, macc[mb][0], 0, 0, 0);
             macc[mb][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(A, B1, macc[mb][1], 0, 0, 0);
           }
+        }
+        return;
+      }
+      if constexpr (kI4) {
+        // 32 int4 codes -> 32 bf16 16 + t (t = q, or the signed code + 8; exact:
+        // t sits in the top 4 fraction bits of 2^4), four B operands of 8
+        // against x columns 8 q .. of the lane's 32, and four more against ones,
+        // which give the group's sums of x in the same layout.  Then
+        // y += s (sum x (16 + t) - c sum x) with c = 16 + z, or 24 for signed codes.
+        const uint32_t flip = i4zp ? 0u : 0x88888888u;
+        uint32_t bw[16];
+#pragma unroll
+        for (int d = 0; d < 4; d++) {
+          const uint32_t v = ow[d] ^ flip;
+          const uint32_t lo = v & 0x0F0F0F0Fu, hi = (v >> 4) & 0x0F0F0F0Fu;
+#pragma unroll
+          for (int b = 0; b < 4; b++) {
+            // bytes {lo.b, 0, hi.b, 0}: codes 8 d + 2 b and 8 d + 2 b + 1
+            const uint32_t pr = __builtin_amdgcn_perm(hi, lo, 0x0C000C00u | ((4u + b) << 16) | b);
+            bw[4 * d + b] = (pr << 3) | 0x41804180u;
+          }
+        }
+        const bf8 ones = __builtin_bit_cast(bf8, u4v{0x3F803F80u, 0x3F803F80u, 0x3F803F80u,
+                                                     0x3F803F80u});
+        const float sc = (float)__builtin_bit_cast(_Float16, (uint16_t)(i4s & 0xFFFFu));
+        const float cc = i4zp ? 16.0f + (float)(i4z & 0xFFu) : 24.0f;
+#pragma unroll
+        for (int mb = 0; mb < kMB; mb++) {
+          facc t{}, u{};
+#pragma unroll
+          for (int q = 0; q < 4; q++) {
+            const bf8 b =
+                __builtin_bit_cast(bf8, u4v{bw[4 * q], bw[4 * q + 1], bw[4 * q + 2], bw[4 * q + 3]});
+            const bf8 xq = __builtin_bit_cast(bf8, q == 0 ? xa[mb] : xm[mb][q > 0 ? q - 1 : 0]);
+            t = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xq, b, t, 0, 0, 0);
+            u = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xq, ones, u, 0, 0, 0);
+          }
+#pragma unroll
+          for (int i = 0; i < 4; i++) macc[mb][0][i] += sc * (t[i] - cc * u[i]);
         }
         return;
       }

@@ -23,7 +23,7 @@ DERR = {1: "WC_DERR_INDEX", 2: "WC_DERR_STATE", 4: "WC_DERR_CURSOR", 8: "WC_DERR
 # Every function the header declares; the library must export all of them.
 EXPORTS = ["wc_analyze", "wc_encode", "wc_open", "wc_decode", "wc_gemv", "wc_free",
            "wc_version", "wc_analyze_device", "wc_encode_device_bounds", "wc_encode_device",
-           "wc_gemm_workspace_bytes", "wc_gemm", "wc_gemm_i8", "wc_gemv_mx"]
+           "wc_gemm_workspace_bytes", "wc_gemm", "wc_gemm_i8", "wc_gemv_mx", "wc_gemv_w4"]
 
 ANALYZE_WORKSPACE_BYTES = 524288  # WC_ANALYZE_WORKSPACE_BYTES
 
@@ -105,6 +105,11 @@ def lib():
                                  C.POINTER(C.c_void_p), C.POINTER(C.c_void_p), C.c_uint32,
                                  C.POINTER(C.c_void_p), C.c_void_p, C.c_void_p]
         L.wc_gemv_mx.restype = C.c_int
+        L.wc_gemv_w4.argtypes = [C.POINTER(_Blob), C.c_void_p, C.c_uint32, C.POINTER(C.c_uint32),
+                                 C.POINTER(C.c_void_p), C.POINTER(C.c_void_p),
+                                 C.POINTER(C.c_void_p), C.c_uint32, C.POINTER(C.c_void_p),
+                                 C.c_void_p, C.c_void_p]
+        L.wc_gemv_w4.restype = C.c_int
         L.wc_analyze_device.argtypes = [C.POINTER(_Tensor), C.c_void_p, C.c_uint64, C.c_void_p,
                                         C.POINTER(_Stats)]
         L.wc_analyze_device.restype = C.c_int
@@ -316,6 +321,24 @@ def gemv_mx(blob: Blob, dev_blob: int, tensors, dev_scales, dev_x, m: int, dev_y
         raise WcError("wc_gemv_mx", rc)
 
 
+def gemv_w4(blob: Blob, dev_blob: int, tensors, dev_scales, dev_zeros, dev_x, m: int, dev_y,
+            stream: int = 0, dev_err: int = 0) -> None:
+    """wc_gemv_w4 with raw device pointers: y_i += x_i * W_i^T for int4 W_i (packed
+    codes as the blob's byte tensor, fp16 scales per 128 at dev_scales[i], zero
+    points at dev_zeros[i] or 0 for two's-complement codes; dev_zeros None: all
+    two's-complement)."""
+    n = len(tensors)
+    ts = (C.c_uint32 * max(n, 1))(*tensors)
+    ss = (C.c_void_p * max(n, 1))(*[p or None for p in dev_scales])
+    zs = None if dev_zeros is None else (C.c_void_p * max(n, 1))(*[p or None for p in dev_zeros])
+    xs = (C.c_void_p * max(n, 1))(*[p or None for p in dev_x])
+    ys = (C.c_void_p * max(n, 1))(*[p or None for p in dev_y])
+    rc = lib().wc_gemv_w4(blob.ptr, C.c_void_p(dev_blob), n, ts, ss, zs, xs, m, ys,
+                          C.c_void_p(stream or None), C.c_void_p(dev_err or None))
+    if rc:
+        raise WcError("wc_gemv_w4", rc)
+
+
 # --- torch plumbing: device memory and streams only ---------------------------
 
 def to_device(blob: Blob, device="cuda"):
@@ -510,6 +533,29 @@ def gemv_mx_torch(blob: Blob, dev_blob, tensors, scales, xs, ys=None, stream=Non
     if stream is None:
         stream = torch.cuda.current_stream(xs[0].device)
     gemv_mx(blob, dev_blob.data_ptr(), list(tensors), [sc.data_ptr() for sc in scales],
+            [x.data_ptr() for x in xs], m, [y.data_ptr() for y in ys], stream.cuda_stream,
+            err.data_ptr() if err is not None else 0)
+    return ys
+
+
+def gemv_w4_torch(blob: Blob, dev_blob, tensors, scales, zeros, xs, ys=None, stream=None,
+                  err=None):
+    """wc_gemv_w4 into float32 tensors: ys[i] += xs[i] @ W_i^T for int4 W_i with fp16
+    scales `scales[i]` (float16 or uint16 device tensors, N x K/128) and zero points
+    `zeros[i]` (uint8 device tensors, or None for two's-complement codes; `zeros`
+    None: all two's-complement); ys zeroed and returned if None."""
+    import torch
+    m = xs[0].shape[0]
+    for x in xs:
+        if x.dtype != torch.bfloat16 or not x.is_contiguous() or x.shape[0] != m:
+            raise ValueError("xs must be contiguous bfloat16 tensors with equal row counts")
+    if ys is None:
+        ys = [torch.zeros((m, blob.shape(t)[0]), dtype=torch.float32, device=x.device)
+              for t, x in zip(tensors, xs)]
+    if stream is None:
+        stream = torch.cuda.current_stream(xs[0].device)
+    zp = None if zeros is None else [z.data_ptr() if z is not None else 0 for z in zeros]
+    gemv_w4(blob, dev_blob.data_ptr(), list(tensors), [s.data_ptr() for s in scales], zp,
             [x.data_ptr() for x in xs], m, [y.data_ptr() for y in ys], stream.cuda_stream,
             err.data_ptr() if err is not None else 0)
     return ys

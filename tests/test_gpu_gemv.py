@@ -788,3 +788,162 @@ def test_mx_gemv_limits(dev):
     with pytest.raises(wc.WcError) as e:                 # 65 rows of x
         wc.gemv_mx(blob, d.data_ptr(), [0], [1], [_dev_x(x, dev).data_ptr()], 65, [y.data_ptr()])
     assert e.value.rc == -1
+
+
+# --- group-quantised int4 weights (codes as bytes), bf16 x: wc_gemv_w4 ---------
+
+def _w4_pack(codes):
+    return (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
+
+
+def _run_w4(blob, dev, scales, zeros, x_bits, expect_err=0):
+    d = wc.to_device(blob, dev)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    sc = torch.from_numpy(np.ascontiguousarray(scales, np.uint16).view(np.int16).reshape(-1).copy()).to(dev)
+    zs = None if zeros is None else [torch.from_numpy(np.ascontiguousarray(zeros, np.uint8).reshape(-1).copy()).to(dev)]
+    ys = wc.gemv_w4_torch(blob, d, [0], [sc], zs, [_dev_x(x_bits, dev)], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == expect_err, wc.describe_errors(int(err.item()))
+    return ys[0].cpu().numpy().astype(np.float64)
+
+
+def _w4_tolerance(w, sc, zeros, x_bits, absref):
+    """fp32 error bound of y: per group, sums of 128 products with x of
+    (16 + t) and of ones, the correction (16 + z or 24) times the second, the
+    scale, and the fp32 accumulation over groups and tiles (u = 2^-24):
+    u (10^4 sum_g |s_g| sum_{k in g} |x_k| + (K/128 + 64) sum |x w|)."""
+    K = 2 * w.shape[1]
+    xv = (np.asarray(x_bits, np.uint32) << 16).view(np.float32).astype(np.float64)
+    gx = np.abs(xv).reshape(xv.shape[0], K // 128, 128).sum(axis=2)            # M x G
+    s = np.abs(np.ascontiguousarray(sc, np.uint16).view(np.float16).astype(np.float64))  # N x G
+    return 2.0 ** -24 * (1e4 * (gx @ s.T) + (K / 128 + 64) * absref) + 1e-30
+
+
+@pytest.mark.parametrize("with_zeros", [False, True])
+def test_w4_gemv_every_code_exact(dev, with_zeros):
+    """Every code in every position of a lane-group and in the first and last
+    group of a tile row, picked by one-hot x rows at scale 1: y must be q - z
+    (or the signed code) exactly, which pins the nibble order, the +16 / +8
+    offsets, the sums of x through the ones operand and the group of each
+    wave row."""
+    rows, cols = 16, 512
+    k = np.arange(cols)[None, :]
+    n = np.arange(rows)[:, None]
+    codes = ((n + k) % 16).astype(np.uint8)
+    rng = np.random.default_rng(91)
+    zeros = rng.integers(0, 16, (rows, cols // 128)).astype(np.uint8) if with_zeros else None
+    sc = np.full((rows, cols // 128), 0x3C00, np.uint16)
+    picks = list(range(32)) + list(range(480, 512))
+    x = np.zeros((len(picks), cols), np.float32)
+    for m, c in enumerate(picks):
+        x[m, c] = 1.0
+    w = _w4_pack(codes)
+    blob = wc.encode([("u8", w, (rows, cols // 2))], tile=(16, 256), tile_order=1)
+    y = _run_w4(blob, dev, sc, zeros, _bf16(x))
+    want = np.array([[(int(codes[r, c]) - int(zeros[r, c // 128])) if with_zeros
+                      else (int(codes[r, c]) ^ 8) - 8 for r in range(rows)] for c in picks],
+                    np.float64)
+    assert np.array_equal(y, want), np.argwhere(y != want)[:8]
+
+
+@pytest.mark.parametrize("with_zeros", [False, True])
+@pytest.mark.parametrize("shape,tile", [((64, 512), (16, 64)), ((48, 1024), (16, 128)),
+                                        ((256, 4096), (16, 2048))])
+@pytest.mark.parametrize("m", [1, 5, 16, 17, 33, 64])
+def test_w4_gemv_matches_the_reference(dev, with_zeros, shape, tile, m):
+    """Random codes, fp16 scales and zero points: y within the derived fp32
+    bound of the oracle's fp64 product."""
+    say("w4 gemv", with_zeros, shape, tile, m)
+    rng = np.random.default_rng(shape[1] + 17 * m + with_zeros)
+    codes = rng.integers(0, 16, shape).astype(np.uint8)
+    sc = rng.uniform(0.002, 0.05, (shape[0], shape[1] // 128)).astype(np.float16).view(np.uint16)
+    zeros = rng.integers(0, 16, (shape[0], shape[1] // 128)).astype(np.uint8) if with_zeros else None
+    x = _bf16(rng.normal(0, 1.0, (m, shape[1])))
+    w = _w4_pack(codes)
+    blob = wc.encode([("u8", w, (shape[0], shape[1] // 2))], tile=tile, tile_order=1)
+    y = _run_w4(blob, dev, sc, zeros, x)
+    ref, absref = oracle.gemv_int4(w, sc, zeros, x)
+    tol = _w4_tolerance(w, sc, zeros, x, absref)
+    bad = np.abs(y - ref) > tol
+    assert not bad.any(), (np.argwhere(bad)[:5], float(np.abs(y - ref).max()))
+
+
+def test_w4_gemv_small_integers_exact(dev):
+    """Scale 1, zero points, small integer x: every partial sum is an integer
+    below 2^24, so y must equal the oracle's integer product exactly."""
+    rng = np.random.default_rng(92)
+    codes = rng.integers(0, 16, (64, 1024)).astype(np.uint8)
+    zeros = rng.integers(0, 16, (64, 8)).astype(np.uint8)
+    sc = np.full((64, 8), 0x3C00, np.uint16)
+    xi = rng.integers(-40, 41, (37, 1024))
+    w = _w4_pack(codes)
+    blob = wc.encode([("u8", w, (64, 512))], tile=(16, 256), tile_order=1)
+    y = _run_w4(blob, dev, sc, zeros, _bf16(xi.astype(np.float32)))
+    ref, _ = oracle.gemv_int4(w, sc, zeros, _bf16(xi.astype(np.float32)))
+    assert np.array_equal(y, ref)
+
+
+@pytest.mark.parametrize("cfg", [3, 8])
+def test_w4_gemv_quantised_layer(dev, cfg):
+    """The scaled 8B int4 (two's-complement codes) and AWQ-style (zero points)
+    workloads as a serving step: one blob holds the codes as bytes (16 x 256-byte
+    tiles), the fp16 scales and the packed zero points; wc_decode brings the
+    scales and zeros back, torch unpacks the zero nibbles to bytes, one
+    wc_gemv_w4 launch multiplies all seven projections by 16 rows of x; sampled
+    rows of y against the oracle."""
+    ts = synth.config(cfg, div=4)
+    codes = [t for t in ts if t.name.endswith(".qweight")]
+    scales = [t for t in ts if t.name.endswith(".scales")]
+    zeros = [t for t in ts if t.name.endswith(".qzeros")]
+    assert len(codes) == len(scales) == 7 and len(zeros) in (0, 7)
+    entries = [("u8", t.data, (t.shape[0], t.shape[1] // 2)) for t in codes]
+    entries += [(t.dtype, t.data) for t in scales + zeros]
+    blob = wc.encode(entries, tile=(16, 256), tile_order=1)
+    d = wc.to_device(blob, dev)
+    outs = wc.decode_torch(blob, d)
+    dsc = outs[7:14]
+    dz = None
+    if zeros:
+        dz = [torch.stack([o & 15, o >> 4], dim=1).reshape(-1).contiguous() for o in outs[14:21]]
+    rng = np.random.default_rng(93)
+    xbits = {}
+    for t in codes:
+        xbits.setdefault(t.shape[1], _bf16(rng.normal(0, 1.0, (16, t.shape[1]))))
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    ys = wc.gemv_w4_torch(blob, d, list(range(7)), dsc, dz,
+                          [_dev_x(xbits[t.shape[1]], dev) for t in codes], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    for j, (t, s, y) in enumerate(zip(codes, scales, ys)):
+        rows = np.random.default_rng(t.shape[0]).choice(t.shape[0], 32, replace=False)
+        w = np.ascontiguousarray(t.data.reshape(t.shape[0], -1)[rows])
+        sc = np.ascontiguousarray(s.data.reshape(t.shape[0], -1)[rows]).view(np.uint16)
+        z = None
+        if zeros:
+            zp = zeros[j].data.reshape(t.shape[0], -1)
+            z = np.ascontiguousarray(np.stack([zp & 15, zp >> 4], axis=2).reshape(t.shape[0], -1)[rows])
+        ref, absref = oracle.gemv_int4(w, sc, z, xbits[t.shape[1]])
+        tol = _w4_tolerance(w, sc, z, xbits[t.shape[1]], absref)
+        assert (np.abs(y.cpu().numpy().astype(np.float64)[:, rows] - ref) <= tol).all(), t.name
+
+
+def test_w4_gemv_limits(dev):
+    rng = np.random.default_rng(94)
+    codes = rng.integers(0, 16, (64, 512)).astype(np.uint8)
+    w = _w4_pack(codes)
+    sc = np.full((64, 4), 0x3C00, np.uint16)
+    x = _bf16(rng.normal(0, 1.0, (4, 512)))
+    for entry, tile in [(("u8", w, (64, 256)), (16, 32)),     # 64 codes per tile row
+                        (("u8", w, (64, 256)), (64, 128)),    # 64-row tiles
+                        (("u4", w, (64, 512)), (16, 128))]:   # nibble symbols
+        blob = wc.encode([entry], tile=tile, tile_order=1)
+        with pytest.raises(wc.WcError) as e:
+            _run_w4(blob, dev, sc, None, x)
+        assert e.value.rc == -5, tile
+    blob = wc.encode([("u8", w, (64, 256))], tile=(16, 128), tile_order=1)
+    d = wc.to_device(blob, dev)
+    y = torch.zeros((4, 64), dtype=torch.float32, device=dev)
+    with pytest.raises(wc.WcError) as e:                 # scales not 2-byte aligned
+        wc.gemv_w4(blob, d.data_ptr(), [0], [17], None, [_dev_x(x, dev).data_ptr()], 4,
+                   [y.data_ptr()])
+    assert e.value.rc == -1

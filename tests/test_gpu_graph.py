@@ -1,5 +1,5 @@
-"""wc_decode, wc_gemv, wc_gemm (with its x packing), wc_gemm_i8, wc_gemv_mx
-and wc_encode_device only launch kernels on the caller's stream: no allocation,
+"""wc_decode, wc_gemv, wc_gemm (with its x packing), wc_gemm_i8, wc_gemv_mx,
+wc_gemv_w4 and wc_encode_device only launch kernels on the caller's stream: no allocation,
 no memset node, no synchronisation.  So a HIP graph can capture them, the way
 a serving loop replays one step.
 
@@ -94,8 +94,8 @@ def test_decode_replayed_from_a_graph(dev):
 
 def test_fused_gemms_replayed_from_a_graph(dev):
     """wc_gemv (16-row MFMA tiles, 8 rows of x), wc_gemm (64-row tiles, 100
-    rows: x packing + shared GEMM), wc_gemm_i8 (16 rows) and wc_gemv_mx (MXFP4,
-    8 rows), all in one graph, on small integers so that every replay must
+    rows: x packing + shared GEMM), wc_gemm_i8 (16 rows), wc_gemv_mx (MXFP4,
+    8 rows) and wc_gemv_w4 (int4 with zero points, 8 rows), all in one graph, on small integers so that every replay must
     equal the exact product."""
     say("graph: fused GEMMs")
     rng = np.random.default_rng(72)
@@ -110,6 +110,14 @@ def test_fused_gemms_replayed_from_a_graph(dev):
     ref8, _ = oracle.gemv_bf16(w, x8)
     ref100, _ = oracle.gemv_bf16(w, x100)
     refi = oracle.gemm_i8(wi, xi)
+    # int4 with zero points at scale 1 (binary16 0x3C00)
+    c4 = rng.integers(0, 16, (32, 1024)).astype(np.uint8)
+    z4 = rng.integers(0, 16, (32, 8)).astype(np.uint8)
+    p4 = (c4[:, 0::2] | (c4[:, 1::2] << 4)).astype(np.uint8)
+    bw4 = wc.encode([("u8", p4, (32, 512))], tile=(16, 256), tile_order=1)
+    s4 = torch.full((32 * 8,), 0x3C00, dtype=torch.int16, device=dev)
+    dz4 = torch.from_numpy(z4.reshape(-1).copy()).to(dev)
+    ref4, _ = oracle.gemv_int4(p4, np.full((32, 8), 0x3C00, np.uint16), z4, x8)
     # MXFP4: e2m1 integers at scale 1 (e8m0 127)
     table = {0: 0, 1: 2, 2: 4, 3: 5, 4: 6, 6: 7}
     vals = rng.choice([0, 1, 2, 3, 4, 6, -1, -2, -3, -4, -6], (32, 1024))
@@ -123,12 +131,14 @@ def test_fused_gemms_replayed_from_a_graph(dev):
                           @ vals.T.astype(np.float64))
     d16, d64, di8 = wc.to_device(b16, dev), wc.to_device(b64, dev), wc.to_device(bi8, dev)
     dmx = wc.to_device(bmx, dev)
+    dw4 = wc.to_device(bw4, dev)
     dx8, dx100 = _dev_bf16(x8, dev), _dev_bf16(x100, dev)
     dxi = torch.from_numpy(xi).to(dev)
     y8 = torch.empty((8, 128), dtype=torch.float32, device=dev)
     y100 = torch.empty((100, 128), dtype=torch.float32, device=dev)
     yi = torch.empty((16, 64), dtype=torch.int32, device=dev)
     ymx = torch.empty((8, 32), dtype=torch.float32, device=dev)
+    y4 = torch.empty((8, 32), dtype=torch.float32, device=dev)
     need = wc.gemm_workspace_bytes(b64, [0], [dx100.data_ptr()], 100)
     ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
     err = torch.zeros(1, dtype=torch.int32, device=dev)
@@ -139,7 +149,9 @@ def test_fused_gemms_replayed_from_a_graph(dev):
         y100.zero_()
         yi.zero_()
         ymx.zero_()
+        y4.zero_()
         wc.gemv_torch(b16, d16, [0], [dx8], ys=[y8], err=err)
+        wc.gemv_w4_torch(bw4, dw4, [0], [s4], [dz4], [dx8], ys=[y4], err=err)
         wc.gemv_mx_torch(bmx, dmx, [0], [smx], [dx8], ys=[ymx], err=err)
         wc.gemm_torch(b64, d64, [0], [dx100], ys=[y100], workspace=ws, err=err)
         wc.gemm_i8_torch(bi8, di8, [0], [dxi], ys=[yi], err=err)
@@ -150,6 +162,7 @@ def test_fused_gemms_replayed_from_a_graph(dev):
         y100.fill_(float("nan"))
         yi.fill_(-7)
         ymx.fill_(float("nan"))
+        y4.fill_(float("nan"))
         ws.fill_(0xEE)
         torch.cuda.synchronize()
         g.replay()
@@ -159,6 +172,7 @@ def test_fused_gemms_replayed_from_a_graph(dev):
         assert np.array_equal(y100.cpu().numpy().astype(np.float64), ref100), k
         assert np.array_equal(yi.cpu().numpy().astype(np.int64), refi), k
         assert np.array_equal(ymx.cpu().numpy().astype(np.float64), refmx), k
+        assert np.array_equal(y4.cpu().numpy().astype(np.float64), ref4), k
 
 
 def test_device_encoder_replayed_from_a_graph(dev):

@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (wc_\w+)", out))
     assert set(names) <= exported
-    assert lib.wc_version() == 7
+    assert lib.wc_version() == 8
 
 
 @pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16), (6, 8), (7, 8),
@@ -237,6 +237,39 @@ def test_gemv_mx_rejects_before_any_launch():
     for b in unsupported:
         with pytest.raises(wc.WcError) as e:
             wc.gemv_mx(b, 16, [0], [16], [16], 1, [16])
+        assert e.value.rc == -5
+
+
+def test_gemv_w4_rejects_before_any_launch():
+    """wc_gemv_w4 validates every argument and tensor on the host and returns
+    before any HIP call; the fake device addresses are never touched."""
+    codes = np.random.default_rng(5).integers(0, 16, (64, 512)).astype(np.uint8)
+    w = (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
+    good = wc.encode([("u8", w, (64, 256))], tile=(16, 128), tile_order=1)
+    for m in (0, 65):
+        with pytest.raises(wc.WcError) as e:
+            wc.gemv_w4(good, 16, [0], [16], None, [16], m, [16])
+        assert e.value.rc == -1
+    for args in (([0], [0], [16], [16]),           # no scales
+                 ([0], [17], [16], [16]),          # scales not 2-byte aligned
+                 ([0], [16], [8], [16]),           # x not 16-byte aligned
+                 ([1], [16], [16], [16]),          # no such tensor
+                 ([0], [16], [16], [0]),           # no y
+                 ([], [], [], [])):                # no jobs
+        with pytest.raises(wc.WcError) as e:
+            wc.gemv_w4(good, 16, args[0], args[1], None, args[2], 1, args[3])
+        assert e.value.rc == -1, args
+    unsupported = [
+        wc.encode([("u8", w, (64, 256))], tile=(64, 128), tile_order=1),   # 64-row tiles
+        wc.encode([("u8", w, (64, 256))], tile=(16, 32), tile_order=1),    # 64 codes wide
+        wc.encode([("u8", w, (64, 256))], tile=(16, 128), tile_order=0),   # row-major tiles
+        wc.encode([("u8", w, (64, 256))]),                                 # byte runs
+        wc.encode([("u4", w, (64, 512))], tile=(16, 256), tile_order=1),   # nibble symbols
+        wc.encode([("u8", w, (64, 256))], lanes=32, tile=(16, 128), tile_order=1),
+    ]
+    for b in unsupported:
+        with pytest.raises(wc.WcError) as e:
+            wc.gemv_w4(b, 16, [0], [16], None, [16], 1, [16])
         assert e.value.rc == -5
 
 
