@@ -276,11 +276,13 @@ wc_status wc_gemv_mx(const wc_blob* desc, const void* dev_blob, uint32_t n, cons
  * bf16 value 16 + t exactly (t = q, or the signed code + 8); the products with
  * x and with ones (the group's sums of x) go through v_mfma_f32_16x16x32_bf16,
  * and y gains s (sum x (16 + t) - (16 + z or 24) sum x) per group, in fp32.
- *   tensors    host array of n tensor indices; each W must be WC_U8 holding
- *              the packed codes (two per byte, even element in the low nibble;
- *              shape N x K/2 bytes), coded with 64 lanes in column-block tiles
- *              (WC_TILE_COLUMN_BLOCKS) of 16 rows and a multiple of 64 bytes
- *              (128 codes: a 16-row wave row is one group of each row);
+ *   tensors    host array of n tensor indices; each W must be WC_U4 with a
+ *              shape (N = rows, K = cols in codes), or WC_U8 holding the same
+ *              packed bytes (two codes per byte symbol, even element in the
+ *              low nibble: half the decode steps; shape N x K/2 bytes), coded
+ *              with 64 lanes in column-block tiles (WC_TILE_COLUMN_BLOCKS) of
+ *              16 rows and a multiple of 128 codes (a 16-row wave row is one
+ *              group of each row);
  *   dev_scales host array of n device pointers to the fp16 scales of each W,
  *              N x K/128 row-major, 2-byte aligned;
  *   dev_zeros  NULL (every W has two's-complement codes), or a host array of

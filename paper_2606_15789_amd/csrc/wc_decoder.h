@@ -599,16 +599,16 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   static_assert(!kShare || (kMfma && kMR == 64), "shared fused GEMM: 64-row tiles");
   static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
   static_assert(!kMfma || (L == 64 && kTiled && !kGemv &&
-                           (G == 2 || ((G == 4 || (G == 8 && kF8 == 3)) && kMR == 16 &&
-                                       !kShare))),
-                "MFMA GEMM: bf16 tiles, or int8 / fp8 / MXFP4 tiles of 16 rows");
+                           (G == 2 || ((G == 4 || (G == 8 && (kF8 == 3 || kF8 == 4))) &&
+                                       kMR == 16 && !kShare))),
+                "MFMA GEMM: bf16 tiles, or int8 / fp8 / MXFP4 / int4 tiles of 16 rows");
   // kF8: 0 no fp8; fp8 weights as bf16 (bf16 x, fp32 sums) of format 1 e4m3, 2 e5m2;
   // 3 MXFP4 weights (e2m1 nibbles, an e8m0 scale per 32-weight lane-group) as bf16;
   // 4 group-quantised int4 weights (codes as bytes, fp16 scale per 128) as bf16
   static_assert(kF8 == 0 || ((kF8 == 1 || kF8 == 2) && kMfma && G == 4) ||
                     (kF8 == 3 && kMfma && (G == 8 || G == 4) && kMR == 16 && !kShare) ||
-                    (kF8 == 4 && kMfma && G == 4 && kMR == 16 && !kShare),
-                "fp8 weights: the byte MFMA path; MXFP4: nibbles or bytes; int4: bytes");
+                    (kF8 == 4 && kMfma && (G == 4 || G == 8) && kMR == 16 && !kShare),
+                "fp8 weights: the byte MFMA path; MXFP4 and int4: nibbles or bytes");
   constexpr bool kInt8 = kMfma && G == 4 && kF8 == 0;  // int8 W and x, int32 sums (W8A8)
   constexpr bool kFp8W = kMfma && G == 4 && (kF8 == 1 || kF8 == 2);  // fp8 W as bf16, bf16 x
   // MXFP4 W as bf16, bf16 x: e2m1 nibble symbols (G = 8), or the packed bytes

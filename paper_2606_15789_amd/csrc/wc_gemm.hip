@@ -148,6 +148,28 @@ __global__ __launch_bounds__(kThreads) void wc_gemv_w4_kernel(LaunchArgs a) {
   decode_chunks<4, 64, true, 0, kMB, 16, false, 4>(a, T, chunk, lane, tab, ring[wave], pre);
 }
 
+// The same for int4 codes as nibble symbols (WC_U4 tensors).
+template <int kMB>
+__global__ __launch_bounds__(kThreads) void wc_gemv_w4n_kernel(LaunchArgs a) {
+  __shared__ uint2 tab[wc::kTableSize];
+  __shared__ uint32_t cum[260];
+  __shared__ uint32_t ring[kWaves][wc_ring_words() / 2];
+  const uint32_t wg = blockIdx.x;
+  uint32_t ti = 0;
+  for (uint32_t k = 1; k < a.n_tensors; k++)
+    if (wg >= a.t[k].wg0) ti = k;
+  const DevTensor& T = a.t[ti];
+  const uint32_t tid = threadIdx.x;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t lane = __lane_id();
+  const uint32_t chunk = (wg - T.wg0) * kWaves + wave;
+  const IndexPre pre = load_index(a, T, chunk, 1u);
+  build_table(a, T, tab, cum, tid);
+  __syncthreads();
+  if (chunk >= T.n_chunks) return;
+  decode_chunks<8, 64, true, 0, kMB, 16, false, 4>(a, T, chunk, lane, tab, ring[wave], pre);
+}
+
 // The shared fused GEMM: workgroup = (pass over 256 kXB rows of x, band of 64
 // W rows, segment of kWaves consecutive tiles of the band); wave w decodes tile
 // w of the segment (when the band has one) and owns x rows 32 kXB w .. of the
@@ -477,41 +499,62 @@ extern "C" wc_status wc_gemv_w4(const wc_blob* desc, const void* dev_blob, uint3
       n > kMaxLaunchTensors || m < 1 || m > 64)
     return WC_EINVAL;
   const wc::BlobPriv& P = static_cast<const wc::BlobHandle*>(desc->priv)->priv;
-  LaunchArgs args{};
-  fill_common(args, P, dev_blob, dev_err);
-  uint32_t wgs = 0;
   for (uint32_t i = 0; i < n; i++) {
     if (tensors[i] >= desc->n_tensors || !dev_x[i] || !dev_y[i] || !dev_scales[i] ||
         reinterpret_cast<uintptr_t>(dev_x[i]) % 16 || reinterpret_cast<uintptr_t>(dev_scales[i]) % 2)
       return WC_EINVAL;
     const wc::TensorInfo& T = P.tensors[tensors[i]];
-    // the packed codes as byte symbols; a wave row of a 16-row tile is 4
-    // lane-groups of 32 codes of each row: one 128-column group per row
-    if (T.dtype != WC_U8 || T.lanes != 64 || T.tile_order != WC_TILE_COLUMN_BLOCKS ||
-        T.tile_r != 16 || (T.tile_c * 2) % 128)
+    // the codes as nibble symbols (WC_U4), or the packed bytes as byte symbols
+    // (WC_U8); a wave row of a 16-row tile is 4 lane-groups of 32 codes of each
+    // row: one 128-column group per row
+    const uint64_t per = T.dtype == WC_U8 ? 2 : 1;  // codes per symbol
+    if ((T.dtype != WC_U8 && T.dtype != WC_U4) || T.lanes != 64 ||
+        T.tile_order != WC_TILE_COLUMN_BLOCKS || T.tile_r != 16 || (T.tile_c * per) % 128)
       return WC_EUNSUPPORTED;
-    const uint64_t K = T.cols * 2;
+    const uint64_t K = T.cols * per;
     if (T.rows > 0xFFFFFFFFull || K > 0xFFFFFFFFull) return WC_EUNSUPPORTED;
     // x offsets of a lane reach 64 rows of 2 K bytes; scale offsets 2 N K / 128
     if (64ull * K * 2 > 0x7FFFFFFFull || T.rows * (K / 128) * 2 > 0xFFFFFFFFull)
       return WC_EUNSUPPORTED;
-    fill_tensor(args.t[i], T, dev_y[i], wgs);
-    args.t[i].x = reinterpret_cast<uint64_t>(dev_x[i]);
-    args.t[i].scales = reinterpret_cast<uint64_t>(dev_scales[i]);
-    args.t[i].zeros = dev_zeros ? reinterpret_cast<uint64_t>(dev_zeros[i]) : 0ull;
-    wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
   }
-  args.n_tensors = n;
-  args.m = m;
-  const dim3 grid(wgs), block(kThreads);
   const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  switch ((m + 15) / 16) {
-    case 1: hipLaunchKernelGGL((wc_gemv_w4_kernel<1>), grid, block, 0, st, args); break;
-    case 2: hipLaunchKernelGGL((wc_gemv_w4_kernel<2>), grid, block, 0, st, args); break;
-    case 3: hipLaunchKernelGGL((wc_gemv_w4_kernel<3>), grid, block, 0, st, args); break;
-    default: hipLaunchKernelGGL((wc_gemv_w4_kernel<4>), grid, block, 0, st, args); break;
+  // one launch for the byte-coded jobs, one for the nibble-coded ones
+  for (int nibbles = 0; nibbles < 2; nibbles++) {
+    LaunchArgs args{};
+    fill_common(args, P, dev_blob, dev_err);
+    uint32_t wgs = 0, nt = 0;
+    for (uint32_t i = 0; i < n; i++) {
+      const wc::TensorInfo& T = P.tensors[tensors[i]];
+      if ((T.dtype == WC_U4) != (nibbles == 1)) continue;
+      fill_tensor(args.t[nt], T, dev_y[i], wgs);
+      args.t[nt].x = reinterpret_cast<uint64_t>(dev_x[i]);
+      args.t[nt].scales = reinterpret_cast<uint64_t>(dev_scales[i]);
+      args.t[nt].zeros = dev_zeros ? reinterpret_cast<uint64_t>(dev_zeros[i]) : 0ull;
+      wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
+      nt++;
+    }
+    if (!nt) continue;
+    args.n_tensors = nt;
+    args.m = m;
+    const dim3 grid(wgs), block(kThreads);
+    if (nibbles) {
+      switch ((m + 15) / 16) {
+        case 1: hipLaunchKernelGGL((wc_gemv_w4n_kernel<1>), grid, block, 0, st, args); break;
+        case 2: hipLaunchKernelGGL((wc_gemv_w4n_kernel<2>), grid, block, 0, st, args); break;
+        case 3: hipLaunchKernelGGL((wc_gemv_w4n_kernel<3>), grid, block, 0, st, args); break;
+        default: hipLaunchKernelGGL((wc_gemv_w4n_kernel<4>), grid, block, 0, st, args); break;
+      }
+    } else {
+      switch ((m + 15) / 16) {
+        case 1: hipLaunchKernelGGL((wc_gemv_w4_kernel<1>), grid, block, 0, st, args); break;
+        case 2: hipLaunchKernelGGL((wc_gemv_w4_kernel<2>), grid, block, 0, st, args); break;
+        case 3: hipLaunchKernelGGL((wc_gemv_w4_kernel<3>), grid, block, 0, st, args); break;
+        default: hipLaunchKernelGGL((wc_gemv_w4_kernel<4>), grid, block, 0, st, args); break;
+      }
+    }
+    if (hipGetLastError() != hipSuccess) return WC_EHIP;
   }
-  return hipGetLastError() == hipSuccess ? WC_OK : WC_EHIP;
+  return WC_OK;
 }
 
 extern "C" wc_status wc_gemm_workspace_bytes(const wc_blob* desc, uint32_t n,

@@ -819,8 +819,16 @@ def _w4_tolerance(w, sc, zeros, x_bits, absref):
     return 2.0 ** -24 * (1e4 * (gx @ s.T) + (K / 128 + 64) * absref) + 1e-30
 
 
+def _w4_encode(w, rows, cols, tile_bytes, coding):
+    """Blob of int4 codes as u8 byte symbols (tile columns in bytes) or u4 nibbles."""
+    if coding == "bytes":
+        return wc.encode([("u8", w, (rows, cols // 2))], tile=(16, tile_bytes), tile_order=1)
+    return wc.encode([("u4", w, (rows, cols))], tile=(16, 2 * tile_bytes), tile_order=1)
+
+
+@pytest.mark.parametrize("coding", CODINGS)
 @pytest.mark.parametrize("with_zeros", [False, True])
-def test_w4_gemv_every_code_exact(dev, with_zeros):
+def test_w4_gemv_every_code_exact(dev, with_zeros, coding):
     """Every code in every position of a lane-group and in the first and last
     group of a tile row, picked by one-hot x rows at scale 1: y must be q - z
     (or the signed code) exactly, which pins the nibble order, the +16 / +8
@@ -838,7 +846,7 @@ def test_w4_gemv_every_code_exact(dev, with_zeros):
     for m, c in enumerate(picks):
         x[m, c] = 1.0
     w = _w4_pack(codes)
-    blob = wc.encode([("u8", w, (rows, cols // 2))], tile=(16, 256), tile_order=1)
+    blob = _w4_encode(w, rows, cols, 256, coding)
     y = _run_w4(blob, dev, sc, zeros, _bf16(x))
     want = np.array([[(int(codes[r, c]) - int(zeros[r, c // 128])) if with_zeros
                       else (int(codes[r, c]) ^ 8) - 8 for r in range(rows)] for c in picks],
@@ -850,17 +858,18 @@ def test_w4_gemv_every_code_exact(dev, with_zeros):
 @pytest.mark.parametrize("shape,tile", [((64, 512), (16, 64)), ((48, 1024), (16, 128)),
                                         ((256, 4096), (16, 2048))])
 @pytest.mark.parametrize("m", [1, 5, 16, 17, 33, 64])
-def test_w4_gemv_matches_the_reference(dev, with_zeros, shape, tile, m):
+@pytest.mark.parametrize("coding", CODINGS)
+def test_w4_gemv_matches_the_reference(dev, with_zeros, shape, tile, m, coding):
     """Random codes, fp16 scales and zero points: y within the derived fp32
     bound of the oracle's fp64 product."""
-    say("w4 gemv", with_zeros, shape, tile, m)
+    say("w4 gemv", with_zeros, shape, tile, m, coding)
     rng = np.random.default_rng(shape[1] + 17 * m + with_zeros)
     codes = rng.integers(0, 16, shape).astype(np.uint8)
     sc = rng.uniform(0.002, 0.05, (shape[0], shape[1] // 128)).astype(np.float16).view(np.uint16)
     zeros = rng.integers(0, 16, (shape[0], shape[1] // 128)).astype(np.uint8) if with_zeros else None
     x = _bf16(rng.normal(0, 1.0, (m, shape[1])))
     w = _w4_pack(codes)
-    blob = wc.encode([("u8", w, (shape[0], shape[1] // 2))], tile=tile, tile_order=1)
+    blob = _w4_encode(w, shape[0], shape[1], tile[1], coding)
     y = _run_w4(blob, dev, sc, zeros, x)
     ref, absref = oracle.gemv_int4(w, sc, zeros, x)
     tol = _w4_tolerance(w, sc, zeros, x, absref)
@@ -883,8 +892,9 @@ def test_w4_gemv_small_integers_exact(dev):
     assert np.array_equal(y, ref)
 
 
+@pytest.mark.parametrize("coding", CODINGS)
 @pytest.mark.parametrize("cfg", [3, 8])
-def test_w4_gemv_quantised_layer(dev, cfg):
+def test_w4_gemv_quantised_layer(dev, cfg, coding):
     """The scaled 8B int4 (two's-complement codes) and AWQ-style (zero points)
     workloads as a serving step: one blob holds the codes as bytes (16 x 256-byte
     tiles), the fp16 scales and the packed zero points; wc_decode brings the
@@ -896,9 +906,12 @@ def test_w4_gemv_quantised_layer(dev, cfg):
     scales = [t for t in ts if t.name.endswith(".scales")]
     zeros = [t for t in ts if t.name.endswith(".qzeros")]
     assert len(codes) == len(scales) == 7 and len(zeros) in (0, 7)
-    entries = [("u8", t.data, (t.shape[0], t.shape[1] // 2)) for t in codes]
+    if coding == "bytes":
+        entries = [("u8", t.data, (t.shape[0], t.shape[1] // 2)) for t in codes]
+    else:
+        entries = [(t.dtype, t.data, t.shape) for t in codes]
     entries += [(t.dtype, t.data) for t in scales + zeros]
-    blob = wc.encode(entries, tile=(16, 256), tile_order=1)
+    blob = wc.encode(entries, tile=(16, 256 if coding == "bytes" else 512), tile_order=1)
     d = wc.to_device(blob, dev)
     outs = wc.decode_torch(blob, d)
     dsc = outs[7:14]
@@ -935,7 +948,7 @@ def test_w4_gemv_limits(dev):
     x = _bf16(rng.normal(0, 1.0, (4, 512)))
     for entry, tile in [(("u8", w, (64, 256)), (16, 32)),     # 64 codes per tile row
                         (("u8", w, (64, 256)), (64, 128)),    # 64-row tiles
-                        (("u4", w, (64, 512)), (16, 128))]:   # nibble symbols
+                        (("u4", w, (64, 512)), (16, 64))]:    # 64 nibbles wide
         blob = wc.encode([entry], tile=tile, tile_order=1)
         with pytest.raises(wc.WcError) as e:
             _run_w4(blob, dev, sc, None, x)

@@ -264,7 +264,8 @@ def test_gemv_w4_rejects_before_any_launch():
         wc.encode([("u8", w, (64, 256))], tile=(16, 32), tile_order=1),    # 64 codes wide
         wc.encode([("u8", w, (64, 256))], tile=(16, 128), tile_order=0),   # row-major tiles
         wc.encode([("u8", w, (64, 256))]),                                 # byte runs
-        wc.encode([("u4", w, (64, 512))], tile=(16, 256), tile_order=1),   # nibble symbols
+        wc.encode([("u4", w, (64, 512))], tile=(16, 64), tile_order=1),    # 64 nibbles wide
+        wc.encode([("fp4_e2m1", w, (64, 512))], tile=(16, 256), tile_order=1),  # e2m1 codes
         wc.encode([("u8", w, (64, 256))], lanes=32, tile=(16, 128), tile_order=1),
     ]
     for b in unsupported:
