@@ -258,6 +258,8 @@ def main() -> int:
                          "weights kept as bf16")
     ap.add_argument("--w4-signed", action="store_true",
                     help="--gemv-w4 on the two's-complement int4 layer (no zero points)")
+    ap.add_argument("--w4-nibbles", action="store_true",
+                    help="--gemv-w4 with the codes as nibble symbols (WC_U4) instead of bytes")
     ap.add_argument("--mx-bytes", action="store_true",
                     help="--gemv-mx: code the packed e2m1 bytes as byte symbols (WC_U8) "
                          "instead of nibble symbols: half the decode steps")
@@ -1058,8 +1060,12 @@ def gemv_w4_bench(args, dev) -> int:
     scales = [t for t in ts if t.name.endswith(".scales")]
     zeros = [t for t in ts if t.name.endswith(".qzeros")]
     shapes = [t.shape for t in codes]
-    blob = wc.encode([("u8", t.data, (t.shape[0], t.shape[1] // 2)) for t in codes], lanes=64,
-                     tile=tile, tile_order=1, threads=args.threads)
+    if args.w4_nibbles:
+        blob = wc.encode([("u4", t.data, t.shape) for t in codes], lanes=64,
+                         tile=(tile[0], 2 * tile[1]), tile_order=1, threads=args.threads)
+    else:
+        blob = wc.encode([("u8", t.data, (t.shape[0], t.shape[1] // 2)) for t in codes],
+                         lanes=64, tile=tile, tile_order=1, threads=args.threads)
     dblob = wc.to_device(blob, dev)
     dsc = [torch.from_numpy(np.ascontiguousarray(s.data).reshape(-1).view(np.int16)).to(dev)
            for s in scales]
@@ -1163,7 +1169,8 @@ def gemv_w4_bench(args, dev) -> int:
         "dtype": "int4 x fp16 scale (as bf16 16 + t) x bf16 -> fp32",
         "data": "synthetic",
         "config": {"workload": workload, "mode": "fused-gemv-w4", "m": M,
-                   "tile": f"{tile[0]}x{tile[1]} bytes", "tile_order": "column-blocks",
+                   "tile": f"{tile[0]}x{2 * tile[1]} codes", "tile_order": "column-blocks",
+                   "symbols": "nibbles" if args.w4_nibbles else "bytes (two codes)",
                    "zero_points": dz is not None,
                    "product": "v_perm + v_lshl_or to bf16 + v_mfma_f32_16x16x32_bf16 (x and ones)",
                    "lanes": 64, "code_bytes_per_step": wbytes, "aux_bytes_per_step": aux,
