@@ -39,10 +39,12 @@
 //  * the raw sign|mantissa bytes of bf16/fp16 rows (8 per lane per row) are
 //    loaded two rows ahead with one 8-byte load per lane.
 // The decode itself uses no MFMA: it is integer table decoding, not a
-// contraction.  The fused decode-GEMM kernels (wc_gemv_kernel, wc_gemm_kernel,
-// Alg. 1 / 3) run the same decoder and feed the decoded bf16 lane-groups to the
-// VALU dot products or to v_mfma_f32_16x16x32_bf16 / v_mfma_f32_32x32x16_bf16
-// operands instead of storing them.
+// contraction.  The fused decode-GEMM kernels (wc_gemm.hip, Alg. 1 / 3) run the
+// same decoder and feed the decoded lane-groups to the VALU dot products or to
+// MFMA operands instead of storing them: bf16 as decoded, int8 to
+// v_mfma_i32_16x16x64_i8, and fp8, MXFP4 and int4 weights after an exact
+// conversion to bf16 (hardware conversions for fp8 / fp4, bit operations for
+// int4).
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -589,7 +591,7 @@ __device__ void share_idle_wave(const LaunchArgs& a, const DevTensor& T, const S
 // every wave multiplies all decoding waves' operands by its own rows of packed
 // x (see Share).
 template <int G, int L, bool kTiled, int kM = 0, int kMB = 0, int kMR = 16, bool kShare = false,
-          int kF8 = 0>
+          int kWF = 0>
 __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTensor& T,
                                               uint32_t chunk0, uint32_t lane,
                                               const uint2* __restrict__ tab, uint32_t* ring,
@@ -599,24 +601,25 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   static_assert(!kShare || (kMfma && kMR == 64), "shared fused GEMM: 64-row tiles");
   static_assert(!kGemv || (G == 2 && L == 64 && kTiled), "fused GEMM: bf16, 64-lane tiles");
   static_assert(!kMfma || (L == 64 && kTiled && !kGemv &&
-                           (G == 2 || ((G == 4 || (G == 8 && (kF8 == 3 || kF8 == 4))) &&
+                           (G == 2 || ((G == 4 || (G == 8 && (kWF == 3 || kWF == 4))) &&
                                        kMR == 16 && !kShare))),
                 "MFMA GEMM: bf16 tiles, or int8 / fp8 / MXFP4 / int4 tiles of 16 rows");
-  // kF8: 0 no fp8; fp8 weights as bf16 (bf16 x, fp32 sums) of format 1 e4m3, 2 e5m2;
-  // 3 MXFP4 weights (e2m1 nibbles, an e8m0 scale per 32-weight lane-group) as bf16;
-  // 4 group-quantised int4 weights (codes as bytes, fp16 scale per 128) as bf16
-  static_assert(kF8 == 0 || ((kF8 == 1 || kF8 == 2) && kMfma && G == 4) ||
-                    (kF8 == 3 && kMfma && (G == 8 || G == 4) && kMR == 16 && !kShare) ||
-                    (kF8 == 4 && kMfma && (G == 4 || G == 8) && kMR == 16 && !kShare),
+  // kWF, the weight format the MFMA path converts to bf16 (bf16 x, fp32 sums):
+  // 0 none (bf16 weights, or int8 with int8 x); 1 fp8 e4m3; 2 fp8 e5m2;
+  // 3 MXFP4 (e2m1 codes, an e8m0 scale per 32-weight lane-group);
+  // 4 group-quantised int4 (fp16 scale per 128, zero points or signed codes)
+  static_assert(kWF == 0 || ((kWF == 1 || kWF == 2) && kMfma && G == 4) ||
+                    (kWF == 3 && kMfma && (G == 8 || G == 4) && kMR == 16 && !kShare) ||
+                    (kWF == 4 && kMfma && (G == 4 || G == 8) && kMR == 16 && !kShare),
                 "fp8 weights: the byte MFMA path; MXFP4 and int4: nibbles or bytes");
-  constexpr bool kInt8 = kMfma && G == 4 && kF8 == 0;  // int8 W and x, int32 sums (W8A8)
-  constexpr bool kFp8W = kMfma && G == 4 && (kF8 == 1 || kF8 == 2);  // fp8 W as bf16, bf16 x
+  constexpr bool kInt8 = kMfma && G == 4 && kWF == 0;  // int8 W and x, int32 sums (W8A8)
+  constexpr bool kFp8W = kMfma && G == 4 && (kWF == 1 || kWF == 2);  // fp8 W as bf16, bf16 x
   // MXFP4 W as bf16, bf16 x: e2m1 nibble symbols (G = 8), or the packed bytes
   // of two codes as byte symbols (G = 4: two x columns per symbol)
-  constexpr bool kMx = kMfma && kF8 == 3;
+  constexpr bool kMx = kMfma && kWF == 3;
   // int4 W (two codes per byte symbol) as bf16 16 + t, bf16 x, fp32 sums corrected
   // per 128-column group: y += s (sum x (16 + t) - c sum x), c = 16 + z or 24
-  constexpr bool kI4 = kMfma && kF8 == 4;
+  constexpr bool kI4 = kMfma && kWF == 4;
   constexpr uint32_t kEPS = (kMx || kI4) && G == 4 ? 2u : 1u;  // x columns per symbol
   static_assert(kMR == 16 || kMR == 32 || kMR == 64, "MFMA tiles of 16, 32 or 64 rows");
   constexpr int kMM = kMR == 64 ? 32 : kMR;   // x rows per MFMA block
@@ -932,7 +935,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
         uint32_t bw[8];
 #pragma unroll
         for (int d = 0; d < 4; d++) {
-          if constexpr (kF8 == 1) {
+          if constexpr (kWF == 1) {
             bw[2 * d] = __builtin_bit_cast(
                 uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(ow[d], 1.0f, false));
             bw[2 * d + 1] = __builtin_bit_cast(
