@@ -1113,12 +1113,20 @@ def gemv_w4_bench(args, dev) -> int:
         q = torch.stack([p & 15, p >> 4], dim=2).reshape(shp).int()
         q = (q ^ 8) - 8 if dz is None else \
             q - dz[t].view(shp[0], shp[1] // 128).int().repeat_interleave(128, dim=1)
-        s = dsc[t].view(torch.float16).float().view(shp[0], shp[1] // 128).repeat_interleave(128, 1)
-        w = q.float() * s
-        ref = x.float() @ w.t()
-        bound = x.float().abs() @ (s.abs() * 40.0).t()
-        if torch.any((y - ref).abs() > 1e4 * 2.0 ** -24 * bound + 1e-30):
+        sg = dsc[t].view(torch.float16).double().view(shp[0], shp[1] // 128)
+        s = sg.repeat_interleave(128, 1)
+        w = q.double() * s
+        xd = x.double()
+        ref = xd @ w.t()
+        # the derived fp32 bound of the fused product (group sums of x (16 + t) and
+        # of x, the zero-point correction, the scale, the accumulation over groups
+        # and tiles): u (10^4 sum_g |s_g| sum_{k in g} |x_k| + (K/128 + 64) sum |x w|)
+        gx = xd.abs().view(x.shape[0], shp[1] // 128, 128).sum(dim=2)
+        bound = 2.0 ** -24 * (1e4 * (gx @ sg.abs().t())
+                              + (shp[1] / 128 + 64) * (xd.abs() @ w.abs().t()))
+        if torch.any((y.double() - ref).abs() > bound + 1e-30):
             raise RuntimeError(f"int4 fused GEMM tensor {t} outside the fp32 error bound")
+        del w, ref
     setup_s = time.perf_counter() - t0
 
     flat = wc.encode([("u8", np.ascontiguousarray(t.data).reshape(-1)) for t in codes],

@@ -412,10 +412,31 @@ wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_params* p, 
                            uint64_t blob_capacity, void* dev_workspace, uint64_t workspace_bytes,
                            void* stream, uint64_t* dev_size);
 
+/* wc_stream -- a measuring aid, not part of the codec: a plain streaming
+ * kernel that moves a decode's byte mix with no decoding, so that a decode
+ * launch can be set against the rate the device's memory gives the same
+ * traffic.  Write unit j (16 bytes) of dst receives read unit
+ * (j * q) >> 32 of src, q = floor(n_src * 2^32 / n_dst) (n_src, n_dst: the
+ * sizes in 16-byte units), so src is read once, in order, spread evenly over
+ * the writes; the stores are non-temporal, as the decode's are.
+ *   dev_src, src_bytes  device memory to read, 16-byte aligned, src_bytes a
+ *                       non-zero multiple of 16;
+ *   dev_dst, dst_bytes  device memory to write, 16-byte aligned, dst_bytes a
+ *                       multiple of 16 with src_bytes <= dst_bytes < 64 GiB;
+ *                       dst_bytes = 0 reads src only (dev_dst must then hold
+ *                       16 writable bytes, stored to only if the data read
+ *                       XOR to one fixed 128-bit pattern);
+ *   blocks              workgroups of 256 threads (0 = 16 per compute unit);
+ *   stream              hipStream_t (NULL = null stream);
+ *   read_bytes          NULL, or receives the bytes the launch reads.
+ * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument), WC_EHIP. */
+wc_status wc_stream(const void* dev_src, uint64_t src_bytes, void* dev_dst, uint64_t dst_bytes,
+                    uint32_t blocks, void* stream, uint64_t* read_bytes);
+
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);
 
-/* wc_version -- ABI version of this header (8). */
+/* wc_version -- ABI version of this header (9). */
 int32_t wc_version(void);
 
 #ifdef __cplusplus

@@ -23,7 +23,8 @@ DERR = {1: "WC_DERR_INDEX", 2: "WC_DERR_STATE", 4: "WC_DERR_CURSOR", 8: "WC_DERR
 # Every function the header declares; the library must export all of them.
 EXPORTS = ["wc_analyze", "wc_encode", "wc_open", "wc_decode", "wc_gemv", "wc_free",
            "wc_version", "wc_analyze_device", "wc_encode_device_bounds", "wc_encode_device",
-           "wc_gemm_workspace_bytes", "wc_gemm", "wc_gemm_i8", "wc_gemv_mx", "wc_gemv_w4"]
+           "wc_gemm_workspace_bytes", "wc_gemm", "wc_gemm_i8", "wc_gemv_mx", "wc_gemv_w4",
+           "wc_stream"]
 
 ANALYZE_WORKSPACE_BYTES = 524288  # WC_ANALYZE_WORKSPACE_BYTES
 
@@ -120,6 +121,9 @@ def lib():
                                        C.c_void_p, C.c_uint64, C.c_void_p, C.c_uint64,
                                        C.c_void_p, C.c_void_p]
         L.wc_encode_device.restype = C.c_int
+        L.wc_stream.argtypes = [C.c_void_p, C.c_uint64, C.c_void_p, C.c_uint64, C.c_uint32,
+                                C.c_void_p, C.POINTER(C.c_uint64)]
+        L.wc_stream.restype = C.c_int
         L.wc_free.argtypes = [C.POINTER(_Blob)]
         L.wc_free.restype = None
         L.wc_version.restype = C.c_int32
@@ -190,6 +194,11 @@ class Blob:
         rows and cols at bytes 64 and 72); (0, 0) for an unshaped tensor."""
         d = np.frombuffer(self.array()[64 + 96 * t: 64 + 96 * (t + 1)].tobytes(), np.uint64)
         return int(d[8]), int(d[9])
+
+    def dtype(self, t: int) -> str:
+        """Storage format of tensor t (the descriptor's first u32)."""
+        code = int(np.frombuffer(self.array()[64 + 96 * t: 64 + 96 * t + 4].tobytes(), np.uint32)[0])
+        return {v: k for k, v in DTYPES.items()}[code]
 
     def payload_bytes(self) -> int:
         """Lane states + words + raw bytes (what the entropy bound is compared with)."""
@@ -337,6 +346,18 @@ def gemv_w4(blob: Blob, dev_blob: int, tensors, dev_scales, dev_zeros, dev_x, m:
                           C.c_void_p(stream or None), C.c_void_p(dev_err or None))
     if rc:
         raise WcError("wc_gemv_w4", rc)
+
+
+def stream_bytes(dev_src: int, src_bytes: int, dev_dst: int, dst_bytes: int, blocks: int = 0,
+                 stream: int = 0) -> int:
+    """wc_stream (a measuring aid, no decoding): read src_bytes once and write
+    dst_bytes once, non-temporal, on `stream`; returns the bytes it reads."""
+    rd = C.c_uint64(0)
+    rc = lib().wc_stream(C.c_void_p(dev_src or None), src_bytes, C.c_void_p(dev_dst or None),
+                         dst_bytes, blocks, C.c_void_p(stream or None), C.byref(rd))
+    if rc:
+        raise WcError("wc_stream", rc)
+    return rd.value
 
 
 # --- torch plumbing: device memory and streams only ---------------------------
@@ -515,18 +536,46 @@ def gemm_i8_torch(blob: Blob, dev_blob, tensors, xs, ys=None, stream=None, err=N
     return ys
 
 
+def _codes_shape(blob: Blob, t: int):
+    """(N, K) of a 4-bit weight tensor in codes: a nibble tensor's own shape, or
+    twice the columns of a byte tensor holding the packed codes."""
+    n, k = blob.shape(t)
+    if blob.dtype(t) == "u8":
+        k *= 2
+    return n, k
+
+
+def _check_jobs(blob: Blob, tensors, xs, m: int):
+    """xs: one contiguous bf16 m x K tensor per job, K the weights' code count."""
+    import torch
+    if len(xs) != len(tensors):
+        raise ValueError("one x per job")
+    for t, x in zip(tensors, xs):
+        if x.dtype != torch.bfloat16 or not x.is_contiguous() or x.dim() != 2 or x.shape[0] != m:
+            raise ValueError("xs must be contiguous 2-D bfloat16 tensors with equal row counts")
+        if not 0 <= t < blob.n_tensors:
+            raise ValueError(f"tensor index {t} out of range")
+        k = _codes_shape(blob, t)[1]
+        if x.shape[1] != k:
+            raise ValueError(f"tensor {t}: x has {x.shape[1]} columns, the weights {k}")
+
+
 def gemv_mx_torch(blob: Blob, dev_blob, tensors, scales, xs, ys=None, stream=None, err=None):
     """wc_gemv_mx into float32 tensors: ys[i] += xs[i] @ W_i^T for MXFP4 W_i =
     tensor tensors[i] with e8m0 scales `scales[i]` (uint8 device tensors of
     N x K/32); ys zeroed and returned if None."""
     import torch
     m = xs[0].shape[0]
-    for x in xs:
-        if x.dtype != torch.bfloat16 or not x.is_contiguous() or x.shape[0] != m:
-            raise ValueError("xs must be contiguous bfloat16 tensors with equal row counts")
-    for sc in scales:
+    _check_jobs(blob, tensors, xs, m)
+    if len(scales) != len(tensors):
+        raise ValueError("one scale tensor per job")
+    for t, sc in zip(tensors, scales):
+        n, k = _codes_shape(blob, t)
         if sc.dtype != torch.uint8 or not sc.is_contiguous():
             raise ValueError("scales must be contiguous uint8 tensors")
+        if sc.numel() != n * (k // 32):
+            raise ValueError(f"tensor {t}: {sc.numel()} scale bytes, the weights need N * K/32 = "
+                             f"{n * (k // 32)}")
     if ys is None:
         ys = [torch.zeros((m, blob.shape(t)[0]), dtype=torch.float32, device=x.device)
               for t, x in zip(tensors, xs)]
@@ -541,14 +590,33 @@ def gemv_mx_torch(blob: Blob, dev_blob, tensors, scales, xs, ys=None, stream=Non
 def gemv_w4_torch(blob: Blob, dev_blob, tensors, scales, zeros, xs, ys=None, stream=None,
                   err=None):
     """wc_gemv_w4 into float32 tensors: ys[i] += xs[i] @ W_i^T for int4 W_i with fp16
-    scales `scales[i]` (float16 or uint16 device tensors, N x K/128) and zero points
-    `zeros[i]` (uint8 device tensors, or None for two's-complement codes; `zeros`
-    None: all two's-complement); ys zeroed and returned if None."""
+    scales `scales[i]` (device tensors holding N x K/128 binary16 words, of any
+    element type) and zero points `zeros[i]` (uint8 device tensors of one byte per
+    group, or None for two's-complement codes; `zeros` None: all two's-complement);
+    ys zeroed and returned if None.  Every tensor's size is checked against the
+    weights' shape before the launch (ValueError), since the kernel sizes its reads
+    from the blob, not from the tensors passed."""
     import torch
     m = xs[0].shape[0]
-    for x in xs:
-        if x.dtype != torch.bfloat16 or not x.is_contiguous() or x.shape[0] != m:
-            raise ValueError("xs must be contiguous bfloat16 tensors with equal row counts")
+    _check_jobs(blob, tensors, xs, m)
+    if len(scales) != len(tensors) or (zeros is not None and len(zeros) != len(tensors)):
+        raise ValueError("one scale tensor (and one zero-point entry, if any) per job")
+    for i, t in enumerate(tensors):
+        n, k = _codes_shape(blob, t)
+        sc = scales[i]
+        if not sc.is_contiguous() or sc.data_ptr() % 2:
+            raise ValueError("scales must be contiguous and 2-byte aligned")
+        if sc.numel() * sc.element_size() != 2 * n * (k // 128):
+            raise ValueError(f"tensor {t}: {sc.numel() * sc.element_size()} bytes of scales, the "
+                             f"weights need N * K/128 = {n * (k // 128)} fp16 words")
+        z = None if zeros is None else zeros[i]
+        if z is not None:
+            if z.dtype != torch.uint8 or not z.is_contiguous():
+                raise ValueError("zero points must be contiguous uint8 tensors, one byte a group")
+            if z.numel() != n * (k // 128):
+                raise ValueError(f"tensor {t}: {z.numel()} zero points, the weights need one "
+                                 f"byte per group, N * K/128 = {n * (k // 128)} (packed "
+                                 "nibbles must be unpacked first)")
     if ys is None:
         ys = [torch.zeros((m, blob.shape(t)[0]), dtype=torch.float32, device=x.device)
               for t, x in zip(tensors, xs)]

@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
                          text=True, check=True).stdout
     exported = set(re.findall(r"\bT (wc_\w+)", out))
     assert set(names) <= exported
-    assert lib.wc_version() == 8
+    assert lib.wc_version() == 9
 
 
 @pytest.mark.parametrize("cfg,div", [(1, 4), (2, 8), (3, 8), (4, 8), (5, 16), (6, 8), (7, 8),
@@ -133,6 +133,23 @@ def test_decode_rejects_before_any_launch():
     assert e.value.rc == -1
     with pytest.raises(wc.WcError):
         wc.decode(b, 0, [1])                      # no device blob
+
+
+def test_stream_rejects_before_any_launch():
+    """wc_stream checks sizes and alignment on the host (fake device addresses,
+    never touched)."""
+    for args in ((0, 32, 16, 64),             # no source
+                 (16, 32, 0, 64),             # no destination
+                 (16, 0, 16, 64),             # nothing to read
+                 (16, 24, 16, 64),            # source not whole 16-byte units
+                 (16, 32, 16, 40),            # destination not whole units
+                 (8, 32, 16, 64),             # source misaligned
+                 (16, 32, 24, 64),            # destination misaligned
+                 (16, 128, 16, 64),           # more read than written
+                 (16, 32, 16, 1 << 36)):      # destination of 2^32 units
+        with pytest.raises(wc.WcError) as e:
+            wc.stream_bytes(*args)
+        assert e.value.rc == -1, args
 
 
 @pytest.mark.parametrize("tile", [(32, 128), (64, 256), (128, 256)])
@@ -272,6 +289,46 @@ def test_gemv_w4_rejects_before_any_launch():
         with pytest.raises(wc.WcError) as e:
             wc.gemv_w4(b, 16, [0], [16], None, [16], 1, [16])
         assert e.value.rc == -5
+
+
+def test_fused_torch_wrappers_check_tensor_sizes():
+    """gemv_w4_torch and gemv_mx_torch size every scale, zero-point and x
+    tensor against the weights' shape before any launch: the kernels size
+    their reads from the blob, so a packed zero-point tensor (two groups a
+    byte), a short scale tensor or an x of the wrong width would otherwise be
+    read past its end.  CPU tensors: the checks run before any device call."""
+    import torch
+    N, K = 64, 512
+    codes = np.random.default_rng(6).integers(0, 16, (N, K)).astype(np.uint8)
+    w = (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
+    for blob in (wc.encode([("u8", w, (N, K // 2))], tile=(16, 128), tile_order=1),
+                 wc.encode([("u4", w, (N, K))], tile=(16, 256), tile_order=1)):
+        assert wc._codes_shape(blob, 0) == (N, K)
+        x = torch.zeros((2, K), dtype=torch.bfloat16)
+        sc = torch.zeros(N * K // 128, dtype=torch.float16)
+        z = torch.zeros(N * K // 128, dtype=torch.uint8)
+        bad = [
+            dict(zeros=[torch.zeros(N * K // 256, dtype=torch.uint8)]),   # packed zero points
+            dict(zeros=[z.to(torch.int32)]),                               # not one byte a group
+            dict(scales=[sc[:-1]]),                                        # one scale short
+            dict(xs=[x[:, :K - 128].contiguous()]),                        # x narrower than K
+            dict(xs=[torch.zeros((2, K), dtype=torch.float32)]),           # x not bf16
+            dict(xs=[x, x]),                                               # two x for one job
+        ]
+        for b in bad:
+            kw = dict(scales=[sc], zeros=[z], xs=[x])
+            kw.update(b)
+            with pytest.raises(ValueError):
+                wc.gemv_w4_torch(blob, None, [0], kw["scales"], kw["zeros"], kw["xs"])
+    mx = wc.encode([("fp4_e2m1", w, (N, K))], tile=(16, 256), tile_order=1)
+    x = torch.zeros((2, K), dtype=torch.bfloat16)
+    sc = torch.zeros(N * K // 32, dtype=torch.uint8)
+    for scales, xs in (([sc[:-1]], [x]),                     # one scale short
+                       ([sc.to(torch.int16)], [x]),          # scales not bytes
+                       ([sc], [x[:, :256].contiguous()]),    # x narrower than K
+                       ([sc], [x, x])):                      # two x for one job
+        with pytest.raises(ValueError):
+            wc.gemv_mx_torch(mx, None, [0], scales, xs)
 
 
 def test_gemm_workspace_bytes():

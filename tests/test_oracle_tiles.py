@@ -417,3 +417,50 @@ def test_gemv_int4_reference(with_zeros):
     sc8[:, 1] = 0x4800                                   # 8.0 in binary16
     y8, _ = oracle.gemv_int4(w, sc8, z, _bf16_of(xi.astype(np.float32)))
     assert np.array_equal(y8, y + 7 * (xi[:, 128:] @ q[:, 128:].T).astype(np.float64))
+
+
+@pytest.mark.parametrize("recipe", ["int4", "awq4"])
+def test_gemv_int4_reads_back_the_generators_quantiser(recipe):
+    """The oracle's reading of int4 codes, pinned by the input generator's own
+    quantisers rather than by a retyped formula.  synth.quant_int4 rounds
+    w / s to the nearest integer in [-8, 7] and stores its two's complement;
+    synth.quant_awq4 stores rint(w / s) + z in [0, 15] with a zero point z.
+    Picking every weight out of the oracle's product with one-hot rows of x
+    must therefore give back w to within half a scale step, whatever the code
+    layout, for every weight that the quantiser did not clip.  A misread code
+    (offset binary for the signed codes, z - q instead of q - z, swapped
+    nibbles or groups) is off by at least one full step on most weights."""
+    rng = np.random.default_rng(2606)
+    rows, cols = 48, 512
+    w = rng.normal(0.0, 0.02, (rows, cols)).astype(np.float32)
+    w[:, 37] *= 20.0                                    # an outlier input channel
+    if recipe == "int4":
+        packed, sc = synth.quant_int4(w)
+        zeros = None
+    else:
+        packed, zp, sc = synth.quant_awq4(w)
+        zeros = np.empty((rows, cols // 128), np.uint8)  # packed nibbles, even group low
+        zeros[:, 0::2] = zp & 0x0F
+        zeros[:, 1::2] = zp >> 4
+    s = sc.view(np.float16).astype(np.float64)           # (rows, groups)
+    x = np.eye(cols, dtype=np.float32)                   # row k picks input column k
+    y, _ = oracle.gemv_int4(packed, sc, zeros, _bf16_of(x))
+    w_hat = y.T                                          # (rows, cols)
+    step = np.repeat(s, 128, axis=1)
+    r = np.rint(w.astype(np.float64) / step)
+    if zeros is None:
+        clipped = (r < -8) | (r > 7)
+    else:
+        zz = np.repeat(zeros.astype(np.float64), 128, axis=1)
+        clipped = (r + zz < 0) | (r + zz > 15)
+    assert clipped.mean() < 0.01
+    err = np.abs(w_hat - w)
+    assert np.all(err[~clipped] <= step[~clipped] * (0.5 + 1e-3))
+    # every weight is an integer number of steps, inside the format's range
+    q = w_hat / step
+    assert np.array_equal(q, np.rint(q))
+    lo, hi = (-8, 7) if zeros is None else (-zz, 15 - zz)
+    assert np.all((q >= lo) & (q <= hi))
+    # a clipped weight sits at the end of the range on its own side
+    if clipped.any():
+        assert np.all(np.sign(w_hat[clipped]) == np.sign(w[clipped]))
