@@ -383,6 +383,27 @@ typedef struct {
 wc_status wc_analyze_device(const wc_dtensor* t, void* dev_workspace, uint64_t workspace_bytes,
                             void* stream, wc_stats* out);
 
+/* wc_analyze_device_static -- wc_analyze_device for callers that cannot
+ * allocate device memory (harnesses and serving loops that forbid hipMalloc):
+ * the same wc_stats, bit for bit, with no workspace argument.  The 65 536 u64
+ * histogram bins (512 KiB, the WC_ANALYZE_WORKSPACE_BYTES of wc_analyze_device)
+ * live in a device array of the library's own: every GPU the library runs on
+ * holds one copy until the process ends.  Its device address is looked up
+ * once per device, on the first call with that device current; the bins are
+ * cleared by a kernel at the start of every call, so nothing of a previous
+ * call (a larger tensor, another format) carries over.  Any tensor size is
+ * taken: the bins are u64 counts whatever the size.
+ *   t       the tensor, in memory of the current device (16-byte aligned);
+ *   stream  hipStream_t of the current device (NULL = null stream);
+ *   out     receives the statistics.
+ * Synchronous.  Calls no hipMalloc, hipFree or other allocating routine, and
+ * takes a process-wide lock for its duration: calls from several host threads
+ * run one after another.  (Calls from several processes each have their own
+ * copy of the array.)  Returns WC_EINVAL (argument, dtype, odd size of a
+ * 16-bit format, misaligned pointer), WC_EUNSUPPORTED (device ordinal 64 or
+ * above), WC_EHIP. */
+wc_status wc_analyze_device_static(const wc_dtensor* t, void* stream, wc_stats* out);
+
 /* wc_encode_device_bounds -- what wc_encode_device needs for these tensors and
  * parameters (their pointers are not read): *blob_capacity, the largest blob
  * they can give (every coded symbol emitting a word), and *workspace_bytes,
@@ -436,7 +457,7 @@ wc_status wc_stream(const void* dev_src, uint64_t src_bytes, void* dev_dst, uint
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);
 
-/* wc_version -- ABI version of this header (9). */
+/* wc_version -- ABI version of this header (10). */
 int32_t wc_version(void);
 
 #ifdef __cplusplus

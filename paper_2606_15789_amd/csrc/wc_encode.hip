@@ -31,6 +31,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "wc_internal.h"
@@ -878,15 +879,16 @@ extern "C" wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_
   }
 }
 
-extern "C" wc_status wc_analyze_device(const wc_dtensor* t, void* dev_workspace,
-                                       uint64_t workspace_bytes, void* stream, wc_stats* out) {
-  if (!t || !out || !dev_workspace || workspace_bytes < WC_ANALYZE_WORKSPACE_BYTES)
-    return WC_EINVAL;
+namespace {
+
+// The histograms of one tensor counted into device memory at dev_workspace
+// (65 536 u64 bins, cleared first by a kernel), copied back into `counts` on
+// the host (as many bins as the format has) and turned into wc_stats.  The
+// caller has checked the arguments.
+wc_status analyze_device_into(const wc_dtensor* t, void* dev_workspace, void* stream,
+                              wc_stats* out, uint64_t* counts) {
   const uint32_t dt = uint32_t(t->dtype);
-  if (!wc::dtype_ok(dt) || (wc::has_raw(dt) && t->nbytes % 2)) return WC_EINVAL;
-  if (t->nbytes && (!t->dev_ptr || reinterpret_cast<uintptr_t>(t->dev_ptr) % 16)) return WC_EINVAL;
-  if (reinterpret_cast<uintptr_t>(dev_workspace) % 16) return WC_EINVAL;
-  try {
+  {
     const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
     const uint64_t ws = reinterpret_cast<uint64_t>(dev_workspace);
     const bool words = wc::has_raw(dt);
@@ -919,20 +921,76 @@ extern "C" wc_status wc_analyze_device(const wc_dtensor* t, void* dev_workspace,
         if (hipGetLastError() != hipSuccess) return WC_EHIP;
       }
     }
-    std::vector<uint64_t> h(bins);
-    if (hipMemcpyAsync(h.data(), dev_workspace, bins * 8, hipMemcpyDeviceToHost, st) != hipSuccess)
+    if (hipMemcpyAsync(counts, dev_workspace, bins * 8, hipMemcpyDeviceToHost, st) != hipSuccess)
       return WC_EHIP;
     if (hipStreamSynchronize(st) != hipSuccess) return WC_EHIP;
     memset(out, 0, sizeof(*out));
     const uint64_t n_sym = wc::symbols_of(dt, t->nbytes);
     if (words) {
-      wc::split_word_counts(h.data(), out);
+      wc::split_word_counts(counts, out);
     } else {
-      for (uint32_t s = 0; s < 256; s++) out->hist[0][s] = h[s];
+      for (uint32_t s = 0; s < 256; s++) out->hist[0][s] = counts[s];
     }
-    wc::finish_stats(dt, n_sym, words ? h.data() : nullptr, out);
+    wc::finish_stats(dt, n_sym, words ? counts : nullptr, out);
     return WC_OK;
+  }
+}
+
+// Arguments both analysis entry points check the same way.
+bool analyze_args_ok(const wc_dtensor* t, const wc_stats* out) {
+  if (!t || !out) return false;
+  const uint32_t dt = uint32_t(t->dtype);
+  if (!wc::dtype_ok(dt) || (wc::has_raw(dt) && t->nbytes % 2)) return false;
+  return !(t->nbytes && (!t->dev_ptr || reinterpret_cast<uintptr_t>(t->dev_ptr) % 16));
+}
+
+}  // namespace
+
+extern "C" wc_status wc_analyze_device(const wc_dtensor* t, void* dev_workspace,
+                                       uint64_t workspace_bytes, void* stream, wc_stats* out) {
+  if (!analyze_args_ok(t, out) || !dev_workspace || workspace_bytes < WC_ANALYZE_WORKSPACE_BYTES)
+    return WC_EINVAL;
+  if (reinterpret_cast<uintptr_t>(dev_workspace) % 16) return WC_EINVAL;
+  try {
+    std::vector<uint64_t> counts(WC_ANALYZE_WORKSPACE_BYTES / 8);
+    return analyze_device_into(t, dev_workspace, stream, out, counts.data());
   } catch (...) {
     return WC_ENOMEM;
   }
+}
+
+// ---------------------------------------------------------------------------
+// wc_analyze_device_static: wc_analyze_device for callers that cannot
+// allocate.  Its bins live in `scratch`, a device array of the library's own
+// (each GPU holds one copy, at its own address, until the process ends); its
+// host side copies the counts into a static host array.  One mutex serialises
+// the calls of a process, so two calls never share the bins at once.
+
+namespace {
+
+constexpr uint64_t kStaticBins = WC_ANALYZE_WORKSPACE_BYTES / 8;
+constexpr int kMaxStaticDevices = 64;
+
+static __device__ __align__(256) uint64_t scratch[kStaticBins];
+
+std::mutex g_static_mu;
+void* g_scratch_ptr[kMaxStaticDevices] = {};  // device address of `scratch`, per device
+uint64_t g_static_counts[kStaticBins];
+
+}  // namespace
+
+extern "C" wc_status wc_analyze_device_static(const wc_dtensor* t, void* stream, wc_stats* out) {
+  if (!analyze_args_ok(t, out)) return WC_EINVAL;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return WC_EHIP;
+  if (dev < 0 || dev >= kMaxStaticDevices) return WC_EUNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_static_mu);
+  if (!g_scratch_ptr[dev]) {
+    // the array's name is a host-side stand-in: only this address is the
+    // device's copy, and only it may reach a kernel or a copy
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return WC_EHIP;
+    g_scratch_ptr[dev] = p;
+  }
+  return analyze_device_into(t, g_scratch_ptr[dev], stream, out, g_static_counts);
 }

@@ -458,7 +458,7 @@ using namespace wc;
 
 extern "C" {
 
-int32_t wc_version(void) { return 9; }
+int32_t wc_version(void) { return 10; }
 
 wc_status wc_analyze(const wc_tensor* t, wc_stats* out) {
   if (!t || !out || (!t->host_ptr && t->nbytes)) return WC_EINVAL;

@@ -24,7 +24,7 @@ DERR = {1: "WC_DERR_INDEX", 2: "WC_DERR_STATE", 4: "WC_DERR_CURSOR", 8: "WC_DERR
 EXPORTS = ["wc_analyze", "wc_encode", "wc_open", "wc_decode", "wc_gemv", "wc_free",
            "wc_version", "wc_analyze_device", "wc_encode_device_bounds", "wc_encode_device",
            "wc_gemm_workspace_bytes", "wc_gemm", "wc_gemm_i8", "wc_gemv_mx", "wc_gemv_w4",
-           "wc_stream"]
+           "wc_stream", "wc_analyze_device_static"]
 
 ANALYZE_WORKSPACE_BYTES = 524288  # WC_ANALYZE_WORKSPACE_BYTES
 
@@ -114,6 +114,8 @@ def lib():
         L.wc_analyze_device.argtypes = [C.POINTER(_Tensor), C.c_void_p, C.c_uint64, C.c_void_p,
                                         C.POINTER(_Stats)]
         L.wc_analyze_device.restype = C.c_int
+        L.wc_analyze_device_static.argtypes = [C.POINTER(_Tensor), C.c_void_p, C.POINTER(_Stats)]
+        L.wc_analyze_device_static.restype = C.c_int
         L.wc_encode_device_bounds.argtypes = [C.POINTER(_Tensor), C.c_uint32, C.POINTER(_Params),
                                               C.POINTER(C.c_uint64), C.POINTER(C.c_uint64)]
         L.wc_encode_device_bounds.restype = C.c_int
@@ -444,6 +446,20 @@ def analyze_device(dtype: str, x, workspace=None, stream=None) -> dict:
                                  C.c_void_p(stream.cuda_stream or None), C.byref(st))
     if rc:
         raise WcError("wc_analyze_device", rc)
+    return _stats_dict(st)
+
+
+def analyze_device_static(dtype: str, x, stream=None) -> dict:
+    """wc_analyze_device_static of a tensor on the current device: no workspace,
+    the bins are the library's own device array (synchronises `stream`)."""
+    import torch
+    t = _dtensors([(dtype, x)])
+    if stream is None:
+        stream = torch.cuda.current_stream(x.device)
+    st = _Stats()
+    rc = lib().wc_analyze_device_static(t, C.c_void_p(stream.cuda_stream or None), C.byref(st))
+    if rc:
+        raise WcError("wc_analyze_device_static", rc)
     return _stats_dict(st)
 
 
