@@ -20,17 +20,20 @@ Blobs are encoded on the host with libwc's threaded encoder (64 KiB chunks,
 64 lanes by default) and kept resident in HBM; every resident blob is decoded
 once and checked byte-exact against its original before timing.
 
-A step is one wc_decode launch that decodes every tensor of one blob into a
-resident output set.  The 70B workload rotates over its layer seeds (each blob
-~1.13 GB, several times the 256 MB Infinity Cache); the smaller workloads
-rotate over enough resident copies of their blob and output set (at least
-1 GiB together) that every step streams from HBM.  The JSON line reports
-decoded GB/s over the K timed steps, the roofline of the decode kernel
-(algorithmic bytes = blob bytes read + decoded bytes written, per launch, over
-its mean event-timed duration, against 8 TB/s), the compression ratio next to
-the order-0 entropy bound, a device-to-device copy ceiling, the same K steps
-issued alternately on two streams (so one launch's tail overlaps the next
-launch's start), and the CPU oracle's single-thread decode rate on the host.
+A step of the 70B workload decodes every resident layer (80 by default, the
+whole model), one wc_decode launch per layer, back to back on one stream into
+two ping-ponged output sets: the sustained run.  Each layer blob is ~1.13 GB,
+several times the 256 MB Infinity Cache.  A step of the smaller workloads is
+one wc_decode launch of one of enough resident copies of the blob and output
+set (at least 1 GiB together) that every launch streams from HBM.  A launch
+decodes every tensor of its blob.  The JSON line reports decoded GB/s over the
+K timed steps; the roofline of the decode kernel (algorithmic bytes = blob
+bytes read + decoded bytes written, per launch, over the median of the
+event-timed launch durations, against 8 TB/s); the ceiling that a plain
+streaming kernel (wc_stream) reaches on the same byte mix, and torch's device
+copy; the compression ratio next to the order-0 entropy bound; the same steps
+with consecutive launches on two streams; and the CPU oracle's decode rate on
+one host core and on all of them.
 """
 
 from __future__ import annotations
@@ -69,51 +72,123 @@ def log(*a):
 
 
 def cpu_model() -> str:
+    """The host CPU as /proc/cpuinfo names it, with its family / model /
+    stepping numbers (some hosts report only a short vendor name)."""
+    info = {}
     try:
         with open("/proc/cpuinfo") as fh:
             for line in fh:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
+                if ":" in line:
+                    k, v = (x.strip() for x in line.split(":", 1))
+                    if k in ("model name", "cpu family", "model", "stepping", "vendor_id") \
+                            and k not in info:
+                        info[k] = v
+                if not line.strip() and info:
+                    break
     except OSError:
         pass
-    return platform.processor() or "unknown"
+    name = info.get("model name") or platform.processor() or "unknown"
+    ids = ", ".join(f"{k} {info[k]}" for k in ("vendor_id", "cpu family", "model", "stepping")
+                    if k in info)
+    return f"{name} ({ids})" if ids else name
 
 
-def oracle_baseline(blob, host_tensors, workload: str, min_seconds: float = 10.0):
-    """Single-thread oracle decode of one whole blob on one host core.
+def oracle_baseline(blob, host_tensors, workload: str, rep_seconds: float = 3.0):
+    """The oracle's decode of one whole blob, timed around the decode calls only.
 
-    The blob is decoded whole, repeatedly until `min_seconds` have elapsed
-    (at least once), timed around the decode calls only.
+    One core: the process pinned to one host core, three repetitions, each
+    decoding the blob as many times as it takes to pass `rep_seconds` (at
+    least once); the median of the three rates.  All cores: the chunks of every
+    tensor split into one contiguous range per available core, one thread per
+    range (the oracle's C calls release the interpreter lock), three timed
+    whole-blob decodes, the median.  Both outputs are checked against the
+    original tensors.
     """
+    import threading
+
     import numpy as np
 
     import oracle
     raw = blob.array()
     info = oracle.tensor_info(raw)
     outs = [np.empty(i["out_bytes"], np.uint8) for i in info]
+    n_out = sum(i["out_bytes"] for i in info)
+    n_chunks = sum(i["n_chunks"] for i in info)
     old = os.sched_getaffinity(0)
     core = min(old)
+
+    def check():
+        for o, h in zip(outs, host_tensors):
+            if not np.array_equal(o, np.ascontiguousarray(h).view(np.uint8).reshape(-1)):
+                raise RuntimeError("oracle baseline decoded a different blob")
+
     os.sched_setaffinity(0, {core})
-    reps, dt = 0, 0.0
+    rates, total, reps_each = [], 0.0, []
     try:
-        while reps == 0 or dt < min_seconds:
-            t0 = time.perf_counter()
-            for t, i in enumerate(info):
-                oracle.decode_chunks(raw, t, 0, i["n_chunks"], out=outs[t])
-            dt += time.perf_counter() - t0
-            reps += 1
+        for _ in range(3):
+            reps, dt = 0, 0.0
+            while reps == 0 or dt < rep_seconds:
+                t0 = time.perf_counter()
+                for t, i in enumerate(info):
+                    oracle.decode_chunks(raw, t, 0, i["n_chunks"], out=outs[t])
+                dt += time.perf_counter() - t0
+                reps += 1
+            rates.append(reps * n_out / dt / 1e9)
+            reps_each.append(reps)
+            total += dt
     finally:
         os.sched_setaffinity(0, old)
-    for o, h in zip(outs, host_tensors):
-        if not np.array_equal(o, np.ascontiguousarray(h).view(np.uint8).reshape(-1)):
-            raise RuntimeError("oracle baseline decoded a different blob")
-    n_out = sum(i["out_bytes"] for i in info)
+    check()
     what = "layer 0 of the 70B bf16 workload" if workload == WORKLOAD_DEFAULT else workload
-    return {"value": round(reps * n_out / dt / 1e9, 4), "unit": "GB/s", "cores": 1,
-            "kind": "oracle",
-            "sample": f"{what}: all {sum(i['n_chunks'] for i in info)} chunks, {n_out} decoded "
-                      f"bytes, decoded {reps}x, single thread pinned to core {core}",
-            "seconds": round(dt, 3), "cpu": cpu_model(), "host_cpus": os.cpu_count()}
+    one = {"value": round(float(np.median(rates)), 4), "unit": "GB/s", "cores": 1,
+           "kind": "oracle",
+           "sample": f"{what}: all {n_chunks} chunks, {n_out} decoded bytes; three timed "
+                     f"repetitions of {reps_each} whole-blob decodes, median rate; single "
+                     f"thread pinned to core {core}",
+           "runs_GBps": [round(r, 4) for r in rates], "seconds": round(total, 3),
+           "cpu": cpu_model(), "host_cpus": os.cpu_count()}
+
+    # all cores: disjoint chunk ranges, one thread each
+    cores = sorted(old)
+    jobs = [[] for _ in cores]
+    for t, i in enumerate(info):
+        n = i["n_chunks"]
+        for k in range(len(cores)):
+            c0, c1 = n * k // len(cores), n * (k + 1) // len(cores)
+            if c1 > c0:
+                jobs[k].append((t, c0, c1))
+    for o in outs:
+        o.fill(0)
+    errs = []
+
+    def work(k):
+        try:
+            os.sched_setaffinity(0, {cores[k]})
+            for t, c0, c1 in jobs[k]:
+                oracle.decode_chunks(raw, t, c0, c1, out=outs[t])
+        except Exception as e:  # noqa: BLE001
+            errs.append(e)
+
+    walls = []
+    for _ in range(3):
+        ths = [threading.Thread(target=work, args=(k,)) for k in range(len(cores))]
+        t0 = time.perf_counter()
+        for th in ths:
+            th.start()
+        for th in ths:
+            th.join()
+        walls.append(time.perf_counter() - t0)
+    os.sched_setaffinity(0, old)
+    if errs:
+        raise errs[0]
+    check()
+    allc = {"value": round(n_out / float(np.median(walls)) / 1e9, 4), "unit": "GB/s",
+            "cores": len(cores), "kind": "oracle",
+            "sample": f"{what}: the same blob, its chunks split into {len(cores)} contiguous "
+                      "ranges per tensor, one thread per range pinned to its own core; three "
+                      "timed whole-blob decodes, median",
+            "seconds": round(sum(walls), 3)}
+    return one, allc
 
 
 def oracle_gemv_baseline(blob, w0, M: int, layer_weight_bytes: int, min_seconds: float = 10.0):
@@ -160,6 +235,52 @@ def oracle_gemv_baseline(blob, w0, M: int, layer_weight_bytes: int, min_seconds:
             "seconds": round(t_dec + t_mul, 3), "cpu": cpu_model(), "host_cpus": os.cpu_count()}
 
 
+def rotation_copies(nbytes_per_copy: int) -> int:
+    """Resident copies of a step's operands so that consecutive steps never
+    find them in the 256 MB Infinity Cache: at least ROTATE_BYTES together,
+    and at least two."""
+    return max(2, -(-ROTATE_BYTES // max(1, int(nbytes_per_copy))))
+
+
+def timed_rotating(fn, warmup: int, steps: int, stream) -> float:
+    """Mean seconds per step of fn(k), k counting the steps (warm-up first),
+    between two events on `stream`."""
+    import torch
+    for k in range(warmup):
+        fn(k)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record(stream)
+    for k in range(steps):
+        fn(warmup + k)
+    b.record(stream)
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / steps / 1e3
+
+
+def hbm_read_rate(dev, stream) -> float:
+    """GB/s of wc_stream reading 1 GiB once (no writes), median of 10."""
+    import numpy as np
+    import torch
+
+    from paper_2606_15789_amd import wc
+    buf = torch.zeros(1 << 30, dtype=torch.uint8, device=dev)
+    sink = torch.zeros(16, dtype=torch.uint8, device=dev)
+    for _ in range(2):
+        wc.stream_bytes(buf.data_ptr(), buf.numel(), sink.data_ptr(), 0, 0, stream.cuda_stream)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(10)]
+    for e0, e1 in ev:
+        e0.record(stream)
+        wc.stream_bytes(buf.data_ptr(), buf.numel(), sink.data_ptr(), 0, 0, stream.cuda_stream)
+        e1.record(stream)
+    torch.cuda.synchronize()
+    med = float(np.median([e0.elapsed_time(e1) for e0, e1 in ev])) / 1e3
+    del buf
+    torch.cuda.empty_cache()
+    return (1 << 30) / med / 1e9
+
+
 def decode_kernel_fingerprint():
     """The fingerprint of wc_decode_kernel's gfx950 code in the loaded library
     (written next to it by the build), or None."""
@@ -203,11 +324,12 @@ def compression_stats(blob, typed_host):
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.splitlines()[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=80)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", choices=list(WORKLOADS), default=WORKLOAD_DEFAULT)
-    ap.add_argument("--layers", type=int, default=8,
-                    help="distinct 70B layer seeds resident in HBM")
+    ap.add_argument("--layers", type=int, default=80,
+                    help="distinct 70B layer seeds resident in HBM; a step decodes all of "
+                         "them (80: every layer of the 70B model)")
     ap.add_argument("--chunk-bytes", type=int, default=65536)
     ap.add_argument("--lanes", type=int, default=64)
     ap.add_argument("--threads", type=int, default=int(os.environ.get("OMP_NUM_THREADS", "16")))
@@ -303,12 +425,14 @@ def main() -> int:
     shaped = lambda t, d, shape: (t, d, shape if len(shape) == 2 else None)  # noqa: E731
 
     # --- setup: draw, encode, upload, verify ---------------------------------
-    # The 70B workload keeps `--layers` distinct layer blobs; the others keep
-    # copies of one blob.  Either way `n_res` blobs rotate through the steps.
+    # The 70B workload keeps `--layers` distinct layer blobs and a step decodes
+    # every one of them, back to back (80 layers: the sustained run over a whole
+    # model's layers); the others keep copies of one blob and a step decodes one
+    # copy.  Launch g decodes resident blob g mod n_res.
     err = torch.zeros(1, dtype=torch.int32, device=dev)
     blobs, dblobs, sets = [], [], []
     keep_orig = {}
-    comp = cpu = None
+    comp = cpu = cpu_all = None
     t_setup = time.perf_counter()
 
     def check(blob, dblob, outs, originals, what):
@@ -321,16 +445,18 @@ def main() -> int:
                 raise RuntimeError(f"{what}: decoded bytes differ from the original")
 
     def first_blob(typed_host):
-        nonlocal comp, cpu
+        nonlocal comp, cpu, cpu_all
         comp = compression_stats(blobs[0], typed_host)
         if not args.no_cpu_baseline:
-            log("cpu baseline: oracle decode on one core ...")
-            cpu = oracle_baseline(blobs[0], [h for _, h in typed_host], args.workload)
-            log(f"cpu baseline: {cpu['value']} GB/s in {cpu['seconds']} s")
+            log("cpu baseline: oracle decode, one core, then all cores ...")
+            cpu, cpu_all = oracle_baseline(blobs[0], [h for _, h in typed_host], args.workload)
+            log(f"cpu baseline: {cpu['value']} GB/s on one core ({cpu['seconds']} s), "
+                f"{cpu_all['value']} GB/s on {cpu_all['cores']} cores")
 
     if big:
         n_res = max(1, args.layers)
-        last = {(args.warmup + args.steps - j) % n_res for j in (1, 2)}
+        per_step = n_res
+        last = {(n_res - j) % n_res for j in (1, 2)}
         for layer in range(n_res):
             t0 = time.perf_counter()
             tens = synth.config_torch_device(5, layer, device="cuda")
@@ -352,9 +478,10 @@ def main() -> int:
             log(f"layer {layer + 1}/{n_res}: {blob.size / 1e9:.3f} GB compressed, "
                 f"{sum(blob.out_bytes) / 1e9:.3f} GB decoded, verified, "
                 f"{time.perf_counter() - t0:.1f} s")
-        out_sets = lambda k: sets[k % 2]          # noqa: E731
-        origs = lambda k: keep_orig[k % n_res]    # noqa: E731
+        out_sets = lambda g: sets[g % 2]          # noqa: E731
+        origs = lambda g: keep_orig[g % n_res]    # noqa: E731
     else:
+        per_step = 1
         tens = synth.config(cfg)
         # --nibbles-as-bytes: a packed 4-bit tensor becomes a byte tensor of half
         # the columns (two nibbles per symbol); the decoded bytes are the same
@@ -377,66 +504,100 @@ def main() -> int:
         first_blob(host)
         log(f"{args.workload}: {blob.size / 1e6:.1f} MB compressed, "
             f"{sum(blob.out_bytes) / 1e6:.1f} MB decoded, {n_res} resident copies, verified")
-        out_sets = lambda k: sets[k % n_res]      # noqa: E731
-        origs = lambda k: dev_orig                # noqa: E731
+        out_sets = lambda g: sets[g % n_res]      # noqa: E731
+        origs = lambda g: dev_orig                # noqa: E731
         del tens
     torch.cuda.empty_cache()
     setup_s = time.perf_counter() - t_setup
-    out_per_step = sum(blobs[0].out_bytes)
-    in_per_step = float(np.mean([b.size for b in blobs]))
+    out_per_launch = sum(blobs[0].out_bytes)
+    in_per_launch = float(np.mean([b.size for b in blobs]))
+    out_per_step = per_step * out_per_launch
+    stream = torch.cuda.current_stream(dev)
 
-    # --- device-to-device copy ceiling: 512 MiB, twice the Infinity Cache ------
-    src = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
-    dst = torch.empty_like(src)
+    # --- ceilings: the same byte mix through a plain streaming kernel ---------
+    # wc_stream reads the compressed bytes of one launch once and writes its
+    # decoded bytes once (non-temporal stores), with no decoding in between;
+    # the best of a few grid sizes.  Beside it, torch's device-to-device copy
+    # of 512 MiB (twice the Infinity Cache).
+    n_in = int(in_per_launch) // 16 * 16
+    src = torch.empty(n_in, dtype=torch.uint8, device=dev)
+    src.random_(0, 256)
+    dst = torch.empty(out_per_launch // 16 * 16, dtype=torch.uint8, device=dev)
+    sweep = {}
+    for blocks in (8192, 16384, 32768, 65536, 131072):
+        for _ in range(2):
+            rd = wc.stream_bytes(src.data_ptr(), n_in, dst.data_ptr(), dst.numel(), blocks,
+                                 stream.cuda_stream)
+        sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(10)]
+        for e0, e1 in sev:
+            e0.record(stream)
+            wc.stream_bytes(src.data_ptr(), n_in, dst.data_ptr(), dst.numel(), blocks,
+                            stream.cuda_stream)
+            e1.record(stream)
+        torch.cuda.synchronize()
+        med = float(np.median([e0.elapsed_time(e1) for e0, e1 in sev])) / 1e3
+        sweep[blocks] = ((rd + dst.numel()) / med / 1e9, med, rd)
+    best = max(sweep, key=lambda k: sweep[k][0])
+    ceiling = {"kernel": "wc_stream_kernel", "GBps": round(sweep[best][0], 1),
+               "frac": round(sweep[best][0] / HBM_PEAK_GBPS, 4),
+               "read_bytes": sweep[best][2], "write_bytes": dst.numel(),
+               "median_launch_us": round(sweep[best][1] * 1e6, 2),
+               "blocks": best,
+               "sweep_GBps": {str(k): round(v[0], 1) for k, v in sweep.items()},
+               "timing": "median of 10 event-timed launches per grid size; best grid"}
+    del src, dst
+    csrc = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    cdst = torch.empty_like(csrc)
     for _ in range(3):
-        dst.copy_(src)
+        cdst.copy_(csrc)
     torch.cuda.synchronize()
     c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     c0.record()
     for _ in range(10):
-        dst.copy_(src)
+        cdst.copy_(csrc)
     c1.record()
     torch.cuda.synchronize()
-    copy_gbps = 10 * 2 * src.numel() / (c0.elapsed_time(c1) / 1e3) / 1e9
-    del src, dst
+    copy_gbps = 10 * 2 * csrc.numel() / (c0.elapsed_time(c1) / 1e3) / 1e9
+    del csrc, cdst
     torch.cuda.empty_cache()
 
     # --- timed decode ---------------------------------------------------------
-    stream = torch.cuda.current_stream(dev)
     err.zero_()
 
-    def step(k, s):
-        r = k % n_res
-        wc.decode(blobs[r], dblobs[r].data_ptr(), [o.data_ptr() for o in out_sets(k)],
+    def launch(g, s):
+        r = g % n_res
+        wc.decode(blobs[r], dblobs[r].data_ptr(), [o.data_ptr() for o in out_sets(g)],
                   s.cuda_stream, err.data_ptr())
 
-    for k in range(args.warmup):
-        step(k, stream)
+    W, K = args.warmup, args.steps
+    for g in range(W * per_step):
+        launch(g, stream)
     torch.cuda.synchronize()
-    K = args.steps
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(K)]
+    G = K * per_step
+    # one event between consecutive launches: launch j runs between ev[j] and ev[j + 1]
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(G + 1)]
     start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
-    for k in range(K):
-        ev[k][0].record(stream)
-        step(args.warmup + k, stream)
-        ev[k][1].record(stream)
+    for j in range(G):
+        ev[j].record(stream)
+        launch(W * per_step + j, stream)
+    ev[G].record(stream)
     end.record(stream)
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(end)
-    launch_ms = [a.elapsed_time(b) for a, b in ev]
+    launch_ms = [ev[j].elapsed_time(ev[j + 1]) for j in range(G)]
 
     def verify_last(what):
         if int(err.item()) != 0:
             raise RuntimeError(f"device errors during {what}: "
                                f"{wc.describe_errors(int(err.item()))}")
         for j in (1, 2):
-            k = args.warmup + K - j
-            if k < args.warmup:
+            g = (W + K) * per_step - j
+            if g < W * per_step:
                 continue
-            for o, r in zip(out_sets(k), origs(k)):
+            for o, r in zip(out_sets(g), origs(g)):
                 if not torch.equal(o[:r.numel() * r.element_size()], r.reshape(-1).view(torch.uint8)):
                     raise RuntimeError(f"{what}: decode output differs from the original")
 
@@ -446,25 +607,29 @@ def main() -> int:
     two = None
     if not args.no_two_stream:
         streams = [torch.cuda.Stream(dev), torch.cuda.Stream(dev)]
-        for k in range(args.warmup):
-            step(k, streams[k % 2])
+        for g in range(W * per_step):
+            launch(g, streams[g % 2])
         torch.cuda.synchronize()
         t0 = time.perf_counter()
-        for k in range(K):
-            step(args.warmup + k, streams[k % 2])
+        for j in range(G):
+            g = W * per_step + j
+            launch(g, streams[g % 2])
         torch.cuda.synchronize()
         dt2 = time.perf_counter() - t0
         verify_last("the two-stream decode")
         two = {"value": round(K * out_per_step / dt2 / 1e9, 2), "unit": "GB/s",
                "ms_per_step": round(dt2 / K * 1e3, 4),
-               "timing": "host clock around K steps issued alternately on two streams"}
+               "timing": "host clock around the K steps with consecutive launches issued "
+                         "alternately on two streams"}
 
     value = K * out_per_step / (total_ms / 1e3) / 1e9
+    med_launch_s = float(np.median(launch_ms)) / 1e3
     mean_launch_s = float(np.mean(launch_ms)) / 1e3
-    achieved = (in_per_step + out_per_step) / mean_launch_s / 1e9
-    config = {"workload": args.workload, "tensors_per_step": len(blobs[0].out_bytes),
+    achieved = (in_per_launch + out_per_launch) / med_launch_s / 1e9
+    config = {"workload": args.workload, "tensors_per_launch": len(blobs[0].out_bytes),
+              "launches_per_step": per_step,
               "decoded_bytes_per_step": out_per_step,
-              "compressed_bytes_per_step": int(in_per_step),
+              "compressed_bytes_per_step": int(per_step * in_per_launch),
               "chunk_bytes": args.chunk_bytes, "lanes": args.lanes, "parallelism": "single-gpu"}
     if args.tile:
         config["tile"] = args.tile
@@ -474,15 +639,17 @@ def main() -> int:
         config["symbols"] = "4-bit tensors coded by packed bytes (two nibbles per symbol)"
     if big:
         config["layers_resident"] = n_res
+        config["step"] = f"one wc_decode launch per resident layer, {n_res} back to back"
     else:
         config["copies_resident"] = n_res
+        config["step"] = "one wc_decode launch of one resident copy"
     line = {
         "metric": METRIC,
         "value": round(value, 2),
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": K,
-        "warmup": args.warmup,
+        "warmup": W,
         "ms_per_step": round(total_ms / K, 4),
         "higher_is_better": True,
         "scaling": "weak",
@@ -495,13 +662,18 @@ def main() -> int:
                      "traffic": counted_traffic(args.workload, args.chunk_bytes, args.lanes,
                                                 bool(args.tile) or args.codebook != "tensor"),
                      "kernel": "wc_decode_kernel",
+                     "median_launch_us": round(med_launch_s * 1e6, 2),
                      "mean_launch_us": round(mean_launch_s * 1e6, 2),
-                     "algorithmic_bytes_per_launch": int(in_per_step + out_per_step)},
+                     "launches_timed": G,
+                     "algorithmic_bytes_per_launch": int(in_per_launch + out_per_launch),
+                     "of_ceiling": round(achieved / ceiling["GBps"], 4)},
         "hbm_pct": round(100 * achieved / HBM_PEAK_GBPS, 2),
+        "ceiling": ceiling,
         "d2d_copy_GBps": round(copy_gbps, 1),
         "two_stream": two,
         "compression": comp,
         "cpu_baseline": cpu,
+        "cpu_baseline_all_cores": cpu_all,
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line), flush=True)
@@ -624,7 +796,8 @@ def gemv_bench(args, dev) -> int:
                    "decoded_once_per": ("256 rows of x (operands shared through LDS)"
                                         if shared else "call"),
                    "lanes": 64, "weight_bytes_per_step": wbytes,
-                   "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},
+                   "compressed_bytes_per_step": blob.size,
+                   "parallelism": "single-gpu"},
         "roofline": ({"bound": "mfma", "achieved": round(tflops, 1),
                       "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                       "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None}
@@ -721,30 +894,35 @@ def gemm_i8_bench(args, dev) -> int:
     def product(i, w):
         return mm(xs_mm[i], w) if mm else torch.matmul(xs_mm[i], w.t())
 
-    def unfused():
-        wc.decode(flat, dflat.data_ptr(), [o.data_ptr() for o in outs], stream.cuda_stream,
-                  err.data_ptr())
-        for i, (o, shp) in enumerate(zip(outs, shapes)):
+    # every variant rotates over resident copies of its weights (>= 1 GiB)
+    n_f = rotation_copies(blob.size)
+    dblobs = [dblob] + [dblob.clone() for _ in range(n_f - 1)]
+    n_u = rotation_copies(flat.size + sum(flat.out_bytes))
+    dflats = [dflat] + [dflat.clone() for _ in range(n_u - 1)]
+    outss = [outs] + [[torch.empty_like(o) for o in outs] for _ in range(n_u - 1)]
+    Wp = W if mm else Wb
+    n_p = rotation_copies(sum(w.numel() * w.element_size() for w in Wp))
+    Wps = [Wp] + [[w.clone() for w in Wp] for _ in range(n_p - 1)]
+
+    def fused_k(k):
+        wc.gemm_i8(blob, dblobs[k % n_f].data_ptr(), list(range(len(W))),
+                   [x.data_ptr() for x in xs], M, [y.data_ptr() for y in ys], stream.cuda_stream,
+                   err.data_ptr())
+
+    def unfused(k):
+        o_k = outss[k % n_u]
+        wc.decode(flat, dflats[k % n_u].data_ptr(), [o.data_ptr() for o in o_k],
+                  stream.cuda_stream, err.data_ptr())
+        for i, (o, shp) in enumerate(zip(o_k, shapes)):
             w = o.view(torch.int8).view(shp)
             product(i, w if mm else w.to(torch.bfloat16))
 
-    def uncompressed():
-        for i in range(len(W)):
-            product(i, W[i] if mm else Wb[i])
+    def uncompressed(k):
+        for i, w in enumerate(Wps[k % n_p]):
+            product(i, w)
 
-    def timed(fn):
-        for _ in range(args.warmup):
-            fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(args.steps):
-            fn()
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / args.steps / 1e3
-
-    s_fused, s_unfused, s_plain = timed(fused), timed(unfused), timed(uncompressed)
+    s_fused, s_unfused, s_plain = (timed_rotating(f, args.warmup, args.steps, stream)
+                                   for f in (fused_k, unfused, uncompressed))
     if int(err.item()):
         raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
     wbytes = sum(blob.out_bytes)
@@ -767,6 +945,7 @@ def gemm_i8_bench(args, dev) -> int:
                    "tile": f"{tile[0]}x{tile[1]}", "tile_order": "column-blocks",
                    "product": "v_mfma_i32_16x16x64_i8", "lanes": 64,
                    "weight_bytes_per_step": wbytes, "compressed_bytes_per_step": blob.size,
+                   "copies_resident": {"fused": n_f, "unfused": n_u, "uncompressed": n_p},
                    "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
@@ -836,30 +1015,34 @@ def gemv_fp8_bench(args, dev) -> int:
     dflat = wc.to_device(flat, dev)
     outs = [torch.empty(n, dtype=torch.uint8, device=dev) for n in flat.out_bytes]
 
-    def unfused():
-        wc.decode(flat, dflat.data_ptr(), [o.data_ptr() for o in outs], stream.cuda_stream,
-                  err.data_ptr())
-        for o, x, shp in zip(outs, xs, shapes):
+    # every variant rotates over resident copies of its weights (>= 1 GiB)
+    n_f = rotation_copies(blob.size)
+    dblobs = [dblob] + [dblob.clone() for _ in range(n_f - 1)]
+    n_u = rotation_copies(flat.size + sum(flat.out_bytes))
+    dflats = [dflat] + [dflat.clone() for _ in range(n_u - 1)]
+    outss = [outs] + [[torch.empty_like(o) for o in outs] for _ in range(n_u - 1)]
+    n_p = rotation_copies(sum(w.numel() * 2 for w in Wb))
+    Wbs = [Wb] + [[w.clone() for w in Wb] for _ in range(n_p - 1)]
+
+    def fused_k(k):
+        wc.gemv(blob, dblobs[k % n_f].data_ptr(), list(range(len(ts))),
+                [x.data_ptr() for x in xs], M, [y.data_ptr() for y in ys], stream.cuda_stream,
+                err.data_ptr())
+
+    def unfused(k):
+        o_k = outss[k % n_u]
+        wc.decode(flat, dflats[k % n_u].data_ptr(), [o.data_ptr() for o in o_k],
+                  stream.cuda_stream, err.data_ptr())
+        for o, x, shp in zip(o_k, xs, shapes):
             w = o.view(tdt).view(shp).to(torch.bfloat16)
             torch.matmul(x, w.t())
 
-    def uncompressed():
-        for w, x in zip(Wb, xs):
+    def uncompressed(k):
+        for w, x in zip(Wbs[k % n_p], xs):
             torch.matmul(x, w.t())
 
-    def timed(fn):
-        for _ in range(args.warmup):
-            fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(args.steps):
-            fn()
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / args.steps / 1e3
-
-    s_fused, s_unfused, s_plain = timed(fused), timed(unfused), timed(uncompressed)
+    s_fused, s_unfused, s_plain = (timed_rotating(f, args.warmup, args.steps, stream)
+                                   for f in (fused_k, unfused, uncompressed))
     if int(err.item()):
         raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
     wbytes = sum(blob.out_bytes)
@@ -883,7 +1066,9 @@ def gemv_fp8_bench(args, dev) -> int:
                    "product": ("v_cvt_scalef32_pk_bf16_" + ("fp8" if fmt == "e4m3" else "bf8") +
                                " + v_mfma_f32_16x16x32_bf16"),
                    "lanes": 64, "weight_bytes_per_step": wbytes,
-                   "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},
+                   "compressed_bytes_per_step": blob.size,
+                   "copies_resident": {"fused": n_f, "unfused": n_u, "uncompressed": n_p},
+                   "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
                      "kernel": "wc_gemv_kernel (fp8)", "mean_step_us": round(s_fused * 1e6, 2),
@@ -972,33 +1157,40 @@ def gemv_mx_bench(args, dev) -> int:
     dflat = wc.to_device(flat, dev)
     outs = [torch.empty(n, dtype=torch.uint8, device=dev) for n in flat.out_bytes]
 
-    def unfused():
-        wc.decode(flat, dflat.data_ptr(), [o.data_ptr() for o in outs], stream.cuda_stream,
+    # every variant rotates over resident copies of its weights (>= 1 GiB): the
+    # fused one over copies of the blob and the scales
+    sbytes = sum(s.numel() for s in dsc)
+    n_f = rotation_copies(blob.size + sbytes)
+    fcop = [(dblob, dsc)] + [(dblob.clone(), [s.clone() for s in dsc]) for _ in range(n_f - 1)]
+    n_u = rotation_copies(flat.size + sum(flat.out_bytes) + sbytes)
+    ucop = [(dflat, outs, dsc)] + [(dflat.clone(), [torch.empty_like(o) for o in outs],
+                                    [s.clone() for s in dsc]) for _ in range(n_u - 1)]
+    n_p = rotation_copies(sum(w.numel() * 2 for w in Wb))
+    Wbs = [Wb] + [[w.clone() for w in Wb] for _ in range(n_p - 1)]
+
+    def fused_k(k):
+        d, sc = fcop[k % n_f]
+        wc.gemv_mx(blob, d.data_ptr(), list(range(len(blocks))), [s.data_ptr() for s in sc],
+                   [x.data_ptr() for x in xs], M, [y.data_ptr() for y in ys],
+                   stream.cuda_stream, err.data_ptr())
+
+    def unfused(k):
+        d, o_k, sc = ucop[k % n_u]
+        wc.decode(flat, d.data_ptr(), [o.data_ptr() for o in o_k], stream.cuda_stream,
                   err.data_ptr())
-        for o, s, x, shp in zip(outs, dsc, xs, shapes):
+        for o, s, x, shp in zip(o_k, sc, xs, shapes):
             torch.matmul(x, dequant(o, s, shp).t())
 
-    def uncompressed():
-        for w, x in zip(Wb, xs):
+    def uncompressed(k):
+        for w, x in zip(Wbs[k % n_p], xs):
             torch.matmul(x, w.t())
 
-    def timed(fn):
-        for _ in range(args.warmup):
-            fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(args.steps):
-            fn()
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / args.steps / 1e3
-
-    s_fused, s_unfused, s_plain = timed(fused), timed(unfused), timed(uncompressed)
+    s_fused, s_unfused, s_plain = (timed_rotating(f, args.warmup, args.steps, stream)
+                                   for f in (fused_k, unfused, uncompressed))
+    read_gbps = hbm_read_rate(dev, stream)
     if int(err.item()):
         raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
     wbytes = sum(blob.out_bytes)
-    sbytes = sum(s.numel() for s in dsc)
     alg = (blob.size + sbytes + sum(x.numel() * 2 for x in xs) +
            sum(2 * y.numel() * 4 for y in ys))
     achieved = alg / s_fused / 1e9
@@ -1020,7 +1212,9 @@ def gemv_mx_bench(args, dev) -> int:
                    "symbols": "bytes (two codes)" if args.mx_bytes else "e2m1 nibbles",
                    "product": "v_cvt_scalef32_pk_bf16_fp4 + v_mfma_f32_16x16x32_bf16",
                    "lanes": 64, "code_bytes_per_step": wbytes, "scale_bytes_per_step": sbytes,
-                   "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},
+                   "compressed_bytes_per_step": blob.size,
+                   "copies_resident": {"fused": n_f, "unfused": n_u, "uncompressed": n_p},
+                   "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
                      "kernel": "wc_gemv_mx_kernel", "mean_step_us": round(s_fused * 1e6, 2),
@@ -1033,6 +1227,11 @@ def gemv_mx_bench(args, dev) -> int:
                          "ms_per_step": round(s_plain * 1e3, 4),
                          "what": "torch.matmul on the weights kept resident as bf16 (4x the "
                                  "fp4 bytes)"},
+        "raw_codes_read": {"bytes": wbytes + sbytes,
+                           "ms": round((wbytes + sbytes) / read_gbps / 1e6, 4),
+                           "read_GBps": round(read_gbps, 1),
+                           "what": "the uncompressed format's floor: its packed e2m1 codes and "
+                                   "scales read once at the rate wc_stream reads 1 GiB"},
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line), flush=True)
@@ -1134,33 +1333,43 @@ def gemv_w4_bench(args, dev) -> int:
     dflat = wc.to_device(flat, dev)
     outs = [torch.empty(n, dtype=torch.uint8, device=dev) for n in flat.out_bytes]
 
-    def unfused():
-        wc.decode(flat, dflat.data_ptr(), [o.data_ptr() for o in outs], stream.cuda_stream,
+    # every variant rotates over resident copies of its weights (>= 1 GiB): the
+    # fused one over copies of the blob, the scales and the zero points
+    aux = sum(s.numel() * 2 for s in dsc) + (sum(z.numel() for z in dz) if dz else 0)
+    n_f = rotation_copies(blob.size + aux)
+    fcop = [(dblob, dsc, dz)] + [(dblob.clone(), [s.clone() for s in dsc],
+                                  None if dz is None else [z.clone() for z in dz])
+                                 for _ in range(n_f - 1)]
+    n_u = rotation_copies(flat.size + sum(flat.out_bytes) + aux)
+    ucop = [(dflat, outs)] + [(dflat.clone(), [torch.empty_like(o) for o in outs])
+                              for _ in range(n_u - 1)]
+    n_p = rotation_copies(sum(w.numel() * 2 for w in Wb))
+    Wbs = [Wb] + [[w.clone() for w in Wb] for _ in range(n_p - 1)]
+
+    def fused_k(k):
+        d, sc, zp = fcop[k % n_f]
+        wc.gemv_w4(blob, d.data_ptr(), list(range(len(codes))), [s.data_ptr() for s in sc],
+                   None if zp is None else [z.data_ptr() for z in zp],
+                   [x.data_ptr() for x in xs], M, [y.data_ptr() for y in ys],
+                   stream.cuda_stream, err.data_ptr())
+
+    def unfused(k):
+        d, o_k = ucop[k % n_u]
+        wc.decode(flat, d.data_ptr(), [o.data_ptr() for o in o_k], stream.cuda_stream,
                   err.data_ptr())
-        for j, (o, x, shp) in enumerate(zip(outs, xs, shapes)):
+        for j, (o, x, shp) in enumerate(zip(o_k, xs, shapes)):
             torch.matmul(x, dequant(o, j, shp).t())
 
-    def uncompressed():
-        for w, x in zip(Wb, xs):
+    def uncompressed(k):
+        for w, x in zip(Wbs[k % n_p], xs):
             torch.matmul(x, w.t())
 
-    def timed(fn):
-        for _ in range(args.warmup):
-            fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(args.steps):
-            fn()
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / args.steps / 1e3
-
-    s_fused, s_unfused, s_plain = timed(fused), timed(unfused), timed(uncompressed)
+    s_fused, s_unfused, s_plain = (timed_rotating(f, args.warmup, args.steps, stream)
+                                   for f in (fused_k, unfused, uncompressed))
+    read_gbps = hbm_read_rate(dev, stream)
     if int(err.item()):
         raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
     wbytes = sum(blob.out_bytes)
-    aux = sum(s.numel() * 2 for s in dsc) + (sum(z.numel() for z in dz) if dz else 0)
     alg = blob.size + aux + sum(x.numel() * 2 for x in xs) + sum(2 * y.numel() * 4 for y in ys)
     achieved = alg / s_fused / 1e9
     line = {
@@ -1182,7 +1391,9 @@ def gemv_w4_bench(args, dev) -> int:
                    "zero_points": dz is not None,
                    "product": "v_perm + v_lshl_or to bf16 + v_mfma_f32_16x16x32_bf16 (x and ones)",
                    "lanes": 64, "code_bytes_per_step": wbytes, "aux_bytes_per_step": aux,
-                   "compressed_bytes_per_step": blob.size, "parallelism": "single-gpu"},
+                   "compressed_bytes_per_step": blob.size,
+                   "copies_resident": {"fused": n_f, "unfused": n_u, "uncompressed": n_p},
+                   "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
                      "kernel": "wc_gemv_w4_kernel", "mean_step_us": round(s_fused * 1e6, 2),
@@ -1195,6 +1406,12 @@ def gemv_w4_bench(args, dev) -> int:
                          "ms_per_step": round(s_plain * 1e3, 4),
                          "what": "torch.matmul on the dequantised weights kept resident as bf16 "
                                  "(4x the int4 bytes)"},
+        "raw_codes_read": {"bytes": wbytes + aux,
+                           "ms": round((wbytes + aux) / read_gbps / 1e6, 4),
+                           "read_GBps": round(read_gbps, 1),
+                           "what": "the uncompressed format's floor: its packed int4 codes, "
+                                   "scales and zero points read once at the rate wc_stream "
+                                   "reads 1 GiB"},
         "setup_s": round(setup_s, 1),
     }
     print(json.dumps(line), flush=True)
