@@ -31,9 +31,9 @@ K timed steps; the roofline of the decode kernel (algorithmic bytes = blob
 bytes read + decoded bytes written, per launch, over the median of the
 event-timed launch durations, against 8 TB/s); the ceiling that a plain
 streaming kernel (wc_stream) reaches on the same byte mix, and torch's device
-copy; the compression ratio next to the order-0 entropy bound; the same steps
-with consecutive launches on two streams; and the CPU oracle's decode rate on
-one host core and on all of them.
+copy; the compression ratio next to the order-0 entropy bound; the CPU
+oracle's decode rate on one host core and on all of them; and, with
+--two-stream, the same steps with consecutive launches on two streams.
 """
 
 from __future__ import annotations
@@ -334,7 +334,11 @@ def main() -> int:
     ap.add_argument("--lanes", type=int, default=64)
     ap.add_argument("--threads", type=int, default=int(os.environ.get("OMP_NUM_THREADS", "16")))
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-two-stream", action="store_true")
+    ap.add_argument("--two-stream", action="store_true",
+                    help="also time the same steps with consecutive launches issued "
+                         "alternately on two streams (supplementary; launches overlap, so a "
+                         "kernel trace of such a run no longer gives per-launch durations)")
+    ap.add_argument("--no-two-stream", action="store_true", help=argparse.SUPPRESS)
     ap.add_argument("--tile", default="", help="ROWSxCOLS 2-D tiles, e.g. 128x256 (default: "
                     "flat chunks of --chunk-bytes)")
     ap.add_argument("--codebook", choices=["tensor", "layer"], default="tensor")
@@ -519,34 +523,42 @@ def main() -> int:
     # decoded bytes once (non-temporal stores), with no decoding in between;
     # the best of a few grid sizes.  Beside it, torch's device-to-device copy
     # of 512 MiB (twice the Infinity Cache).
+    # Launches rotate over enough (source, destination) pairs (>= 1 GiB) that
+    # none finds its bytes in the Infinity Cache, as the decode launches do.
     n_in = int(in_per_launch) // 16 * 16
-    src = torch.empty(n_in, dtype=torch.uint8, device=dev)
-    src.random_(0, 256)
-    dst = torch.empty(out_per_launch // 16 * 16, dtype=torch.uint8, device=dev)
+    n_out = out_per_launch // 16 * 16
+    n_cp = 1 if big else rotation_copies(n_in + n_out)
+    pairs = []
+    for _ in range(n_cp):
+        src = torch.empty(n_in, dtype=torch.uint8, device=dev)
+        src.random_(0, 256)
+        pairs.append((src, torch.empty(n_out, dtype=torch.uint8, device=dev)))
     sweep = {}
     for blocks in (8192, 16384, 32768, 65536, 131072):
-        for _ in range(2):
-            rd = wc.stream_bytes(src.data_ptr(), n_in, dst.data_ptr(), dst.numel(), blocks,
-                                 stream.cuda_stream)
+        def sl(k):
+            src, dst = pairs[k % n_cp]
+            return wc.stream_bytes(src.data_ptr(), n_in, dst.data_ptr(), n_out, blocks,
+                                   stream.cuda_stream)
+        for k in range(2):
+            rd = sl(k)
         sev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(10)]
-        for e0, e1 in sev:
+        for k, (e0, e1) in enumerate(sev):
             e0.record(stream)
-            wc.stream_bytes(src.data_ptr(), n_in, dst.data_ptr(), dst.numel(), blocks,
-                            stream.cuda_stream)
+            sl(k)
             e1.record(stream)
         torch.cuda.synchronize()
         med = float(np.median([e0.elapsed_time(e1) for e0, e1 in sev])) / 1e3
-        sweep[blocks] = ((rd + dst.numel()) / med / 1e9, med, rd)
+        sweep[blocks] = ((rd + n_out) / med / 1e9, med, rd)
     best = max(sweep, key=lambda k: sweep[k][0])
     ceiling = {"kernel": "wc_stream_kernel", "GBps": round(sweep[best][0], 1),
                "frac": round(sweep[best][0] / HBM_PEAK_GBPS, 4),
-               "read_bytes": sweep[best][2], "write_bytes": dst.numel(),
+               "read_bytes": sweep[best][2], "write_bytes": n_out,
                "median_launch_us": round(sweep[best][1] * 1e6, 2),
-               "blocks": best,
+               "blocks": best, "copies_resident": n_cp,
                "sweep_GBps": {str(k): round(v[0], 1) for k, v in sweep.items()},
                "timing": "median of 10 event-timed launches per grid size; best grid"}
-    del src, dst
+    del pairs
     csrc = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     cdst = torch.empty_like(csrc)
     for _ in range(3):
@@ -605,7 +617,7 @@ def main() -> int:
 
     # --- the same steps on two streams (supplementary) --------------------------
     two = None
-    if not args.no_two_stream:
+    if args.two_stream:
         streams = [torch.cuda.Stream(dev), torch.cuda.Stream(dev)]
         for g in range(W * per_step):
             launch(g, streams[g % 2])

@@ -9,6 +9,7 @@ the host library's whole blob and decoded back on the GPU, and sampled chunks
 are decoded one by one by the oracle.  The statistics must equal the oracle's
 (integer histograms exactly, entropies to the last bit of the same formula).
 """
+import struct
 import sys
 
 import numpy as np
@@ -333,23 +334,76 @@ def test_analyze_device_edges(dev):
         _same_stats(wc.analyze_device(dt, x), oracle.analyze(dt, d))
 
 
-@pytest.mark.parametrize("model", ["qwen2-1.5b", "mistral-7b"])
+def _records_match_oracle(raw, t, host, rng, n_sample=3):
+    """For tensor t of a blob of bf16 tensors (64 lanes, flat 64 KiB chunks):
+    its frequency table is the oracle's normalisation of the oracle's
+    histogram of the whole tensor; sampled chunk records (the first, the last,
+    and random ones) are byte for byte the oracle's encode of that chunk's
+    symbols; and the oracle decodes those chunks back to the original bytes."""
+    d = 64 + 96 * t
+    first = struct.unpack_from("<Q", raw, d + 24)[0]
+    n_chunks = struct.unpack_from("<Q", raw, d + 32)[0]
+    freq_off = struct.unpack_from("<Q", raw, d + 48)[0]
+    index_off = struct.unpack_from("<Q", raw, 32)[0]
+    coded, _ = oracle.symbols("bf16", host)
+    freq = oracle.normalise(oracle.histogram(coded))
+    assert np.array_equal(np.frombuffer(raw[freq_off:freq_off + 512].tobytes(), np.uint16), freq)
+    E = 65536 // 2
+    picks = sorted({0, n_chunks - 1} | set(rng.choice(n_chunks, n_sample, replace=False).tolist()))
+    out = np.empty(host.size * 2, np.uint8)
+    orig = host.view(np.uint8).reshape(-1)
+    for c in picks:
+        states, words = oracle.encode_stream(coded[c * E:(c + 1) * E], freq, 64, 8)
+        off = 16 * struct.unpack_from("<I", raw, index_off + 4 * (first + c))[0]
+        nw, na, nsym, zero = struct.unpack_from("<IIII", raw, off)
+        assert (nw, na, zero) == (words.size, states.size, 0), (t, c)
+        assert nsym == min(E, coded.size - c * E), (t, c)
+        got_states = np.frombuffer(raw[off + 16:off + 16 + 4 * na].tobytes(), np.uint32)
+        w0 = off + 16 + (4 * na + 15) // 16 * 16
+        got_words = np.frombuffer(raw[w0:w0 + 2 * nw].tobytes(), np.uint16)
+        assert np.array_equal(got_states, states) and np.array_equal(got_words, words), (t, c)
+        oracle.decode_chunks(raw, t, c, c + 1, out=out)
+        lo, hi = 2 * c * E, min(2 * (c + 1) * E, out.size)
+        assert np.array_equal(out[lo:hi], orig[lo:hi]), (t, c)
+
+
+@pytest.mark.parametrize("model", list(synth.MODEL_LAYERS))
 def test_model_family_layer(dev, model):
-    """A whole decoder layer of a model family (the benchmark's sweep draw):
-    the device blob equals the oracle's, and decodes on the GPU to the layer."""
+    """A whole bf16 decoder layer of each model family of the paper (1.5B to
+    405B parameters; the benchmark's sweep draw), at its real shapes.  The
+    device encoder's blob decodes on the GPU to the layer, bit for bit.
+    Against the oracle: for the two smallest families the whole blob equals
+    the oracle's encode; for every family each tensor's table equals the
+    oracle's, sampled chunk records equal the oracle's encode of those chunks,
+    and the oracle decodes them back to the original bytes."""
     say("model layer", model)
     shapes, sigma = synth.MODEL_LAYERS[model]
-    tens = synth.layer_torch_device(shapes, sigma, 20, device="cuda")
+    seed = 20 + list(synth.MODEL_LAYERS).index(model)
+    tens = synth.layer_torch_device(shapes, sigma, seed, device="cuda")
     dents = [("bf16", t, shape) for _, t, shape in tens]
     blob, size = wc.encode_device(dents)
     torch.cuda.synchronize()
-    got = blob[: int(size.item())].cpu().numpy().tobytes()
-    host = [("bf16", t.cpu().numpy(), shape) for _, t, shape in tens]
-    assert got == oracle.encode(host)
-    desc = wc.open_blob(got)
+    n = int(size.item())
+    raw = blob[:n].cpu().numpy()
+    desc = wc.open_blob(raw)
     err = torch.zeros(1, dtype=torch.int32, device=dev)
     outs = wc.decode_torch(desc, blob, err=err)
     torch.cuda.synchronize()
     assert int(err.item()) == 0
     for (_, t, _), out in zip(tens, outs):
         assert torch.equal(out, t)
+    del outs
+    say(f"  {model}: {n / 1e9:.3f} GB blob, {sum(t.numel() for _, t, _ in tens) / 1e9:.3f} GB "
+        "decoded bit-exact on the GPU")
+    rng = np.random.default_rng(seed)
+    host = []
+    for j, (name, t, shape) in enumerate(tens):
+        h = t.cpu().numpy().view(np.uint16)
+        _records_match_oracle(raw, j, h, rng)
+        if model in ("qwen2-1.5b", "mistral-7b"):
+            host.append(("bf16", h, shape))
+        say(f"  {model} {name} {shape}: table and sampled records equal the oracle's")
+    if host:
+        assert raw.tobytes() == oracle.encode(host)
+    del tens, blob
+    torch.cuda.empty_cache()
