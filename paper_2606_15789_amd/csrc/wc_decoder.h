@@ -409,7 +409,13 @@ __device__ __forceinline__ Slot<L> issue(Chain<L>& c, uint32_t h, uint32_t sub) 
 // low word (symbol in byte 3).  Branch-free: every lane reads a word and
 // v_perm either shifts it in or keeps the state, so a group of steps stays
 // one basic block.
-template <bool kAll, int L>
+// kFoldBase: the ring position of the step's first word rides in the mbcnt
+// (its second operand is added to the count), which saves two scalar
+// instructions a step and costs one vector move to put the position in a
+// VGPR (gfx9 reads one scalar operand per vector instruction).  The decode
+// takes it; the fused products, which are bound by their vector instruction
+// count, add the position afterwards instead.
+template <bool kAll, int L, bool kFoldBase = true>
 __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ tab, bool active,
                                          uint32_t h) {
   using S = Shape<L>;
@@ -422,12 +428,15 @@ __device__ __forceinline__ uint32_t step(Chain<L>& c, const uint2* __restrict__ 
   }
   const bool need = (kAll || active) && xn < wc::kStateLow;
   const uint64_t m = __ballot(need);
+  // the lane's rank among the renormalising lanes (with kFoldBase, on top of
+  // the ring position of the step's first word)
+  const uint32_t fold = kFoldBase && Chain<L>::kH == 1 ? c.cursor[0] & (S::kRingWords - 1) : 0u;
   const uint32_t rank =
-      __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, fold));
   const uint16_t* words = reinterpret_cast<const uint16_t*>(c.ring);
   uint32_t idx;
   if constexpr (Chain<L>::kH == 1) {
-    idx = (c.cursor[0] & (S::kRingWords - 1)) + rank;
+    idx = kFoldBase ? rank : (c.cursor[0] & (S::kRingWords - 1)) + rank;
     c.cursor[0] += (uint32_t)__popcll(m);
   } else {
     // the upper half's rank counts the lower half's lanes too: subtract them
@@ -811,7 +820,8 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
     }
     const int nv = kTail ? max(0, min<int>(W, (int)n_lane - (int)(r * kRowSym + sub * W))) : W;
 #pragma unroll
-    for (int k = k0; k < k0 + 2; k++) lo[k % G] = step<!kTail, L>(c, tab, k < nv, h);
+    for (int k = k0; k < k0 + 2; k++)
+      lo[k % G] = step<!kTail, L, !(kGemv || kMfma)>(c, tab, k < nv, h);
     if constexpr ((k0 + 2) % G == 0) {
       constexpr int d = (k0 + 1) / G;             // the dword these G steps complete
       uint32_t raw2 = 0;
