@@ -26,7 +26,7 @@
  * passed as plain pointers (`void*`), so any allocator (torch, hipMalloc)
  * can own them.
  *
- * Blob format version 3 (little-endian; every offset absolute from the blob
+ * Blob format version 4 (little-endian; every offset absolute from the blob
  * start): header 64 B, then one 96-B descriptor per tensor (type, chunk size,
  * sizes, lanes, table and raw offsets, shape and tile), then the u16 frequency
  * tables (16-B padded; tensors sharing a codebook point to one table), the
@@ -38,6 +38,12 @@
  *     u32 state[A] (16-B padded), u16 word[n_words] (16-B padded).
  *   Symbol i of a chunk belongs to lane (i mod L*W) div W at step
  *   (i div L*W)*W + i mod W, with W symbols = 16 output bytes per lane-group.
+ *   Start states: a lane of a tiled chunk starts the encoder at 2^16 and its
+ *   decode ends there.  A lane of an untiled chunk starts at 2^S + D, where D
+ *   packs the lane's first K symbols (b bits each, the first lowest; fewer if
+ *   the lane has fewer), which are not coded: K, b, S = 2, 8, 16 for the coded
+ *   bytes of bf16 / fp16, 3, 8, 24 for byte symbols, 7, 4, 28 for nibbles.
+ *   Its decode ends in that state and reads those symbols back from it.
  */
 #ifndef WC_H_
 #define WC_H_
@@ -464,7 +470,7 @@ wc_status wc_stream(const void* dev_src, uint64_t src_bytes, void* dev_dst, uint
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);
 
-/* wc_version -- ABI version of this header (10). */
+/* wc_version -- ABI version of this header (11). */
 int32_t wc_version(void);
 
 #ifdef __cplusplus

@@ -70,12 +70,12 @@ def lib():
         L.orc_analyze.argtypes = [C.c_uint32, C.c_void_p, C.c_uint64, C.POINTER(Stats)]
         L.orc_normalise.argtypes = [C.c_void_p, C.c_uint32, C.c_void_p]
         L.orc_encode_stream.argtypes = [C.c_void_p, C.c_uint64, C.c_void_p, C.c_uint32,
-                                        C.c_uint32, C.c_uint32, C.c_void_p, C.c_void_p,
-                                        C.c_uint64, C.POINTER(C.c_uint64),
-                                        C.POINTER(C.c_uint32)]
+                                        C.c_uint32, C.c_uint32, C.c_void_p, C.c_uint32,
+                                        C.c_void_p, C.c_void_p, C.c_uint64,
+                                        C.POINTER(C.c_uint64), C.POINTER(C.c_uint32)]
         L.orc_decode_stream.argtypes = [C.c_void_p, C.c_uint32, C.c_void_p, C.c_uint64,
                                         C.c_uint64, C.c_void_p, C.c_uint32, C.c_uint32,
-                                        C.c_uint32, C.c_void_p]
+                                        C.c_uint32, C.c_uint32, C.c_void_p, C.c_void_p]
         L.orc_encode_blob.argtypes = [C.POINTER(_Tensor), C.c_uint32, C.c_uint32, C.c_uint32,
                                       C.c_uint32, C.c_uint32, C.c_uint32, C.c_uint32,
                                       C.POINTER(u8p), C.POINTER(C.c_uint64)]
@@ -201,33 +201,42 @@ def normalise(hist, alphabet: int | None = None) -> np.ndarray:
 
 # --- one interleaved rANS stream --------------------------------------------
 
-def encode_stream(sym, freq, lanes: int, group: int):
-    """(states, words) of one chunk coded with `lanes` lanes of `group` symbols."""
+def encode_stream(sym, freq, lanes: int, group: int, init=None, skip: int = 0):
+    """(states, words) of one chunk coded with `lanes` lanes of `group` symbols.
+
+    `init`: each lane's start state (default 2^16); steps below `skip` of
+    every lane are left out of the coding."""
     s = np.ascontiguousarray(sym, dtype=np.uint8)
     f = np.ascontiguousarray(freq, dtype=np.uint32)
     cap = s.size + 1
     words = np.empty(cap, np.uint16)
     states = np.empty(max(lanes, 1), np.uint32)
+    ini = None if init is None else np.ascontiguousarray(init, dtype=np.uint32)
     nw = C.c_uint64()
     na = C.c_uint32()
-    rc = lib().orc_encode_stream(_ptr(s), s.size, _ptr(f), f.size, lanes, group, _ptr(states),
+    rc = lib().orc_encode_stream(_ptr(s), s.size, _ptr(f), f.size, lanes, group,
+                                 None if ini is None else _ptr(ini), skip, _ptr(states),
                                  _ptr(words), cap, C.byref(nw), C.byref(na))
     if rc:
         raise OracleError(rc, "encode_stream")
     return states[:na.value].copy(), words[:nw.value].copy()
 
 
-def decode_stream(states, words, n: int, freq, lanes: int, group: int):
-    """Decoded symbols, or raises OracleError(-3) if the final-state checks fail."""
+def decode_stream(states, words, n: int, freq, lanes: int, group: int, skip: int = 0,
+                  want_final: bool = False):
+    """Decoded symbols (steps below `skip` left at 0), or raises OracleError(-3)
+    if the checks fail.  Every lane must end at 2^16, unless want_final: then
+    the end states are returned too, (symbols, states), for the caller to check."""
     st = np.ascontiguousarray(states, dtype=np.uint32)
     w = np.ascontiguousarray(words, dtype=np.uint16)
     f = np.ascontiguousarray(freq, dtype=np.uint32)
     out = np.zeros(max(n, 1), np.uint8)
+    fin = np.zeros(max(st.size, 1), np.uint32)
     rc = lib().orc_decode_stream(_ptr(st), st.size, _ptr(w), w.size, n, _ptr(f), f.size, lanes,
-                                 group, _ptr(out))
+                                 group, skip, _ptr(fin) if want_final else None, _ptr(out))
     if rc:
         raise OracleError(rc, "decode_stream")
-    return out[:n]
+    return (out[:n], fin[:st.size].copy()) if want_final else out[:n]
 
 
 # --- blobs -------------------------------------------------------------------

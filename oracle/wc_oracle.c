@@ -43,7 +43,7 @@
 #define ORC_M (1u << ORC_PROB_BITS)   /* table total 2^12 (Sec. VI-F, b = 12) */
 #define ORC_STATE_LOW (1u << 16)       /* rANS lower bound of the state        */
 #define ORC_MAGIC 0x31424357u          /* bytes 'W','C','B','1'                */
-#define ORC_VERSION 3u
+#define ORC_VERSION 4u
 
 #define ORC_OK 0
 #define ORC_EINVAL (-1)
@@ -358,6 +358,70 @@ static uint32_t states_of(uint64_t n, uint32_t L, uint32_t W) {
 }
 
 /* ------------------------------------------------------------------------ */
+/* Lane states that carry data (format version 4; a reading of ours, the     */
+/* paper's encoder starts every lane from the same fixed state, Sec. V-B).   */
+/* The encoder's start state is information the decoder gets back for free  */
+/* at the end of the lane, so an untiled chunk spends it: lane l starts at   */
+/* 2^S + D, D packing the lane's first K_l = min(K, its symbols) symbols     */
+/* (step t's symbol in bits [b t, b t + b)), and those steps are not coded.   */
+/*   exponent bytes of a 16-bit format   K = 2, b = 8, S = 16                */
+/*   byte symbols                        K = 3, b = 8, S = 24                */
+/*   nibble symbols                      K = 7, b = 4, S = 28                */
+/* K b <= S and 2^S + D < 2^32, so the start state is a valid state; a       */
+/* decoded lane must end with x div 2^S = 1 and D below 2^(b K_l).  Tiled     */
+/* chunks (the fused products' input) keep the plain start 2^16, K = 0.      */
+
+typedef struct {
+  uint32_t K, b, S;
+} orc_carry;
+
+static orc_carry carry_of(uint32_t dt, int tiled) {
+  orc_carry c = {0, 8, 16};
+  if (tiled) return c;
+  if (has_raw(dt)) {
+    c.K = 2;
+  } else if (is_nibble(dt)) {
+    c.K = 7;
+    c.b = 4;
+    c.S = 28;
+  } else {
+    c.K = 3;
+    c.S = 24;
+  }
+  return c;
+}
+
+/* start state of lane l of a chunk of n symbols (sym in coding order) */
+static uint32_t carry_state(orc_carry c, const uint8_t* sym, uint64_t n, uint32_t l, uint32_t L,
+                            uint32_t W) {
+  if (c.K == 0) return ORC_STATE_LOW;
+  uint32_t D = 0;
+  for (uint32_t t = 0; t < c.K; t++) {
+    uint64_t i = symbol_at(t, l, L, W);
+    if (i < n) D |= (uint32_t)sym[i] << (c.b * t);
+  }
+  return (1u << c.S) + D;
+}
+
+/* the carried symbols back from lane l's end state; ORC_ECORRUPT if the
+   state is not 2^S + D with D inside the lane's K_l symbols */
+static int carry_read(orc_carry c, uint32_t x, uint8_t* sym, uint64_t n, uint32_t l, uint32_t L,
+                      uint32_t W) {
+  if (c.K == 0) return x == ORC_STATE_LOW ? ORC_OK : ORC_ECORRUPT;
+  if ((x >> c.S) != 1) return ORC_ECORRUPT;
+  uint32_t D = x - (1u << c.S);
+  uint32_t used = 0;
+  for (uint32_t t = 0; t < c.K; t++) {
+    uint64_t i = symbol_at(t, l, L, W);
+    if (i >= n) continue;
+    sym[i] = (uint8_t)((D >> (c.b * t)) & ((1u << c.b) - 1));
+    used += c.b;
+  }
+  if (used < 32 && (D >> used) != 0) return ORC_ECORRUPT;
+  return ORC_OK;
+}
+
+/* ------------------------------------------------------------------------ */
 /* rANS coding of one chunk.                                                 */
 /*
  * State x is a 32-bit integer kept in [2^16, 2^32); 16-bit words are moved
@@ -367,8 +431,10 @@ static uint32_t states_of(uint64_t n, uint32_t L, uint32_t W) {
  *   decode:    slot = x mod 2^12; s = the symbol with cum_s <= slot < cum_s+f_s
  *              x = f_s * floor(x / 2^12) + slot - cum_s          (Alg. 2)
  *              if x < 2^16: x = x * 2^16 + next word
- * Every lane starts the encoder at 2^16, so a correct decode ends with every
- * lane back at 2^16 and the whole word stream consumed.
+ * Lane l starts the encoder at init[l] (2^16 when init is NULL), any value in
+ * [2^16, 2^32); decoding lane l ends in that same state, so a correct decode
+ * ends with every lane back at its start and the whole word stream consumed.
+ * Steps t < skip of every lane are left out of the coding on both sides.
  *
  * Word order: the encoder runs steps T-1..0 and, within a step, lanes L-1..0,
  * pushing words on a stack; the stream is that stack read from the top, so
@@ -377,17 +443,21 @@ static uint32_t states_of(uint64_t n, uint32_t L, uint32_t W) {
  */
 
 int orc_encode_stream(const uint8_t* sym, uint64_t n, const uint32_t* freq, uint32_t alphabet,
-                      uint32_t L, uint32_t W, uint32_t* states /*[L]*/, uint16_t* words,
+                      uint32_t L, uint32_t W, const uint32_t* init /*[L] or NULL*/,
+                      uint32_t skip, uint32_t* states /*[L]*/, uint16_t* words,
                       uint64_t words_cap, uint64_t* n_words, uint32_t* n_states) {
   if (L == 0 || W == 0) return ORC_EINVAL;
   uint32_t cum[256];
   cumulative(freq, alphabet, cum);
   uint32_t A = states_of(n, L, W);
   uint64_t T = steps_of(n, L, W);
-  for (uint32_t l = 0; l < A; l++) states[l] = ORC_STATE_LOW;
+  for (uint32_t l = 0; l < A; l++) {
+    states[l] = init ? init[l] : ORC_STATE_LOW;
+    if (states[l] < ORC_STATE_LOW) return ORC_EINVAL;
+  }
   /* the stack is written top-down at the end of `words` and moved later */
   uint64_t pushed = 0;
-  for (uint64_t tt = T; tt-- > 0;) {
+  for (uint64_t tt = T; tt-- > skip;) {
     for (uint32_t l = A; l-- > 0;) {
       uint64_t i = symbol_at(tt, l, L, W);
       if (i >= n) continue;
@@ -412,9 +482,13 @@ int orc_encode_stream(const uint8_t* sym, uint64_t n, const uint32_t* freq, uint
   return ORC_OK;
 }
 
+/* Decodes steps skip..T-1 of every lane.  With final == NULL every lane must
+   end at 2^16; otherwise the end states are returned there for the caller to
+   check.  Either way the whole word stream must be consumed. */
 int orc_decode_stream(const uint32_t* states_in, uint32_t n_states, const uint16_t* words,
                       uint64_t n_words, uint64_t n, const uint32_t* freq, uint32_t alphabet,
-                      uint32_t L, uint32_t W, uint8_t* sym_out) {
+                      uint32_t L, uint32_t W, uint32_t skip, uint32_t* final /*[L] or NULL*/,
+                      uint8_t* sym_out) {
   if (L == 0 || W == 0 || L > 4096) return ORC_EINVAL;
   uint32_t A = states_of(n, L, W);
   if (n_states != A) return ORC_ECORRUPT;
@@ -433,7 +507,7 @@ int orc_decode_stream(const uint32_t* states_in, uint32_t n_states, const uint16
   uint64_t cursor = 0;
   uint64_t T = steps_of(n, L, W);
   int bad = 0;
-  for (uint64_t t = 0; t < T; t++) {
+  for (uint64_t t = skip; t < T; t++) {
     for (uint32_t l = 0; l < A; l++) {
       uint64_t i = symbol_at(t, l, L, W);
       if (i >= n) continue;
@@ -452,8 +526,12 @@ int orc_decode_stream(const uint32_t* states_in, uint32_t n_states, const uint16
       }
     }
   }
-  for (uint32_t l = 0; l < A; l++)
-    if (x[l] != ORC_STATE_LOW) bad = 1;
+  for (uint32_t l = 0; l < A; l++) {
+    if (final)
+      final[l] = x[l];
+    else if (x[l] != ORC_STATE_LOW)
+      bad = 1;
+  }
   if (cursor != n_words) bad = 1;
   return bad ? ORC_ECORRUPT : ORC_OK;
 }
@@ -607,15 +685,17 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
       /* each symbol pushes at most one word */
       uint64_t cap = len + 1;
       uint16_t* words = (uint16_t*)malloc(cap * sizeof(uint16_t));
-      uint32_t states[64];
+      uint32_t states[64], init[64];
       uint64_t nw = 0;
       uint32_t A = 0;
       if (!words) {
         rc = ORC_ENOMEM;
         break;
       }
-      rc = orc_encode_stream(codeds[t] + s0, len, freqs + (size_t)t * 256, alpha, L, W, states,
-                             words, cap, &nw, &A);
+      orc_carry cy = carry_of(dt, tiled[t]);
+      for (uint32_t l = 0; l < L; l++) init[l] = carry_state(cy, codeds[t] + s0, len, l, L, W);
+      rc = orc_encode_stream(codeds[t] + s0, len, freqs + (size_t)t * 256, alpha, L, W, init,
+                             cy.K, states, words, cap, &nw, &A);
       if (rc != ORC_OK) {
         free(words);
         break;
@@ -871,8 +951,14 @@ static int decode_one(const uint8_t* b, uint64_t size, const orc_desc* d, uint64
   for (uint32_t k = 0; k < nw; k++) words[k] = (uint16_t)get16(wp + 2 * k);
   uint32_t freq[256];
   for (uint32_t s = 0; s < d->alphabet; s++) freq[s] = get16(b + d->freq_off + 2 * s);
-  int rc = orc_decode_stream(states, A, words, nw, len, freq, d->alphabet, d->L, d->W, sym);
+  orc_carry cy = carry_of(d->dtype, d->tile_r != 0);
+  uint32_t fin[64];
+  memset(sym, 0, len ? len : 1);
+  int rc = orc_decode_stream(states, A, words, nw, len, freq, d->alphabet, d->L, d->W, cy.K, fin,
+                             sym);
   if (rc == ORC_OK || rc == ORC_ECORRUPT) {
+    for (uint32_t l = 0; l < A; l++)
+      if (carry_read(cy, fin[l], sym, len, l, d->L, d->W) != ORC_OK) rc = ORC_ECORRUPT;
     const uint8_t* raw = has_raw(d->dtype) ? b + d->raw_off + s0 : NULL;
     put_symbols(d->dtype, sym, raw, s0, len, out, d->tile_r ? d->cols : 0, d->tile_r, d->tile_c,
                 d->tile_order);

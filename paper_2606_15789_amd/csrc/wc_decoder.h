@@ -643,6 +643,14 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   constexpr uint32_t kLogW = G == 2 ? 3 : (G == 4 ? 4 : 5);
   constexpr int kPipe = Shape<L>::kPipe, kEvery = Shape<L>::kEvery;
   static_assert(!kMfma || kMR != 64 || kUnroll == 2 * kGroupsPerRow, "row pairs per body");
+  // Start states that carry data (untiled chunks): a lane's first kCK
+  // symbols (kCB bits each, the first lowest) are not coded; the lane ends at
+  // 2^kCS + D and they are read back from D.  They all lie in the lane's first
+  // output dword.  Tiled chunks (every fused GEMM) carry nothing.
+  constexpr uint32_t kCK = kTiled ? 0u : (G == 2 ? 2u : (G == 4 ? 3u : 7u));
+  constexpr uint32_t kCB = G == 8 ? 4u : 8u;
+  constexpr uint32_t kCS = G == 2 ? 16u : (G == 4 ? 24u : 28u);
+  static_assert(kCK <= uint32_t(G) && kCK * kCB <= kCS, "carried symbols fit the first dword");
   static_assert(kUnroll % (kPipe * kEvery) == 0 && kUnroll % kGroupsPerRow == 0,
                 "pipeline shape");
 
@@ -705,6 +713,7 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   }
   uint32_t lo[G];   // entries of the dword being assembled
   uint32_t ow[4];   // the row's four output dwords
+  uint32_t first_dw = 0;  // row 0's first dword without the carried symbols
   float acc[kGemv ? kM : 1];
   // x columns of this tile (fused GEMM), read through the constant address
   // space: the addresses are wave-uniform, so the loads are scalar
@@ -776,9 +785,11 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
                             : 0u;
 
   // group g of the chunk, j = g mod kUnroll (static)
-  auto group = [&](uint32_t g, auto jc, auto tailc) {
+  auto group = [&](uint32_t g, auto jc, auto tailc, auto firstc) {
     constexpr int j = decltype(jc)::value;
     constexpr bool kTail = decltype(tailc)::value;
+    // the first body of full rows: row 0's carried steps are known here
+    constexpr bool kFirst = decltype(firstc)::value && j < kGroupsPerRow;
     constexpr int k0 = (j % kGroupsPerRow) * 2;  // first step of this group in its lane-group
     if constexpr (j % kEvery == 0) {
       // every kEvery groups: commit the unit loaded kPipe slots ago, load the next
@@ -819,9 +830,15 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
       }
     }
     const int nv = kTail ? max(0, min<int>(W, (int)n_lane - (int)(r * kRowSym + sub * W))) : W;
+    // in the tail, a runtime row: its carried steps are masked off
+    const int kc = kTail && kCK > 0 && r == 0 ? int(kCK) : 0;
 #pragma unroll
-    for (int k = k0; k < k0 + 2; k++)
-      lo[k % G] = step<!kTail, L, !(kGemv || kMfma)>(c, tab, k < nv, h);
+    for (int k = k0; k < k0 + 2; k++) {
+      if (kFirst && uint32_t(k) < kCK)
+        lo[k % G] = 0u;  // carried in the start state: not coded
+      else
+        lo[k % G] = step<!kTail, L, !(kGemv || kMfma)>(c, tab, k < nv && k >= kc, h);
+    }
     if constexpr ((k0 + 2) % G == 0) {
       constexpr int d = (k0 + 1) / G;             // the dword these G steps complete
       uint32_t raw2 = 0;
@@ -831,6 +848,9 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
         raw2 = d & 1 ? src >> 16 : src;
       }
       ow[d] = assemble<G>(lo, raw2);
+      if constexpr (kCK > 0 && d == 0) {
+        if (kFirst || (kTail && r == 0)) first_dw = ow[0];
+      }
     }
     if constexpr (j % kGroupsPerRow == kGroupsPerRow - 1) {
       if constexpr (G == 2) {
@@ -1034,9 +1054,19 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
 
   const uint32_t groups_full = rows_full * kGroupsPerRow;
   uint32_t g0 = 0;
+  if constexpr (kCK > 0) {
+    // the first body apart: it leaves row 0's carried steps out
+    if (kUnroll <= groups_full) {
+      [&]<int... J>(std::integer_sequence<int, J...>) {
+        (group(J, std::integral_constant<int, J>{}, std::false_type{}, std::true_type{}), ...);
+      }(std::make_integer_sequence<int, kUnroll>{});
+      g0 = kUnroll;
+    }
+  }
   for (; g0 + kUnroll <= groups_full; g0 += kUnroll) {
     [&]<int... J>(std::integer_sequence<int, J...>) {
-      (group(g0 + J, std::integral_constant<int, J>{}, std::false_type{}), ...);
+      (group(g0 + J, std::integral_constant<int, J>{}, std::false_type{}, std::false_type{}),
+       ...);
     }(std::make_integer_sequence<int, kUnroll>{});
   }
   // the remaining full groups, then the rows some lanes decode only in part
@@ -1044,7 +1074,8 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
   // shorter chunk's full rows)
   for (; g0 < groups; g0 += kUnroll) {
     [&]<int... J>(std::integer_sequence<int, J...>) {
-      ((g0 + J < groups ? group(g0 + J, std::integral_constant<int, J>{}, std::true_type{})
+      ((g0 + J < groups ? group(g0 + J, std::integral_constant<int, J>{}, std::true_type{},
+                                std::false_type{})
                         : void()),
        ...);
     }(std::make_integer_sequence<int, kUnroll>{});
@@ -1092,10 +1123,36 @@ __device__ __forceinline__ void decode_chunks(const LaunchArgs& a, const DevTens
     }
   }
 
-  // --- end-of-chunk checks: every lane back at 2^16, every word consumed ----
+  // --- end-of-chunk checks: every lane back at its start, every word consumed
   uint32_t bits = 0;
   const uint32_t A_h = kH == 2 && h ? c.A[kH - 1] : c.A[0];
-  if (__ballot(sub < A_h && c.x != wc::kStateLow)) bits |= WC_DERR_STATE;
+  if constexpr (kCK > 0) {
+    // the carried symbols: the lane's first min(kCK, n0) symbols from D
+    const uint32_t n0 = n_lane > sub * W ? min<uint32_t>(W, n_lane - sub * W) : 0u;
+    const uint32_t kl = min(kCK, n0);
+    const uint32_t D = c.x - (1u << kCS);
+    const bool bad = (c.x >> kCS) != 1u || (D >> (kCB * kl)) != 0u;
+    if (__ballot(sub < A_h && bad)) bits |= WC_DERR_STATE;
+    if (n0 > 0) {
+      uint32_t lc[G];
+#pragma unroll
+      for (int t = 0; t < G; t++)
+        lc[t] = uint32_t(t) < kl ? ((D >> (kCB * t)) & ((1u << kCB) - 1u)) << 24 : 0u;
+      const uint32_t dw = first_dw | assemble<G>(lc, 0u);
+      // the lane's first dword again, now whole (only its valid bytes)
+      const uint32_t nb = min(4u, n0 * 4u / G + (G == 8 ? (n0 & 1u) : 0u));
+      uint32_t vo, so;
+      out_at(0, vo, so);
+      if (nb == 4) {
+        __builtin_amdgcn_raw_buffer_store_b32(dw, c.os, vo, so, 0);
+      } else {
+        for (uint32_t b = 0; b < nb; b++)
+          __builtin_amdgcn_raw_buffer_store_b8((uint8_t)(dw >> (8 * b)), c.os, vo + b, so, 0);
+      }
+    }
+  } else {
+    if (__ballot(sub < A_h && c.x != wc::kStateLow)) bits |= WC_DERR_STATE;
+  }
 #pragma unroll
   for (int k = 0; k < kH; k++)
     if (c.cursor[k] != c.nw[k]) bits |= WC_DERR_CURSOR;

@@ -343,18 +343,33 @@ __device__ void encode_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, u
     if (lane < L && i0 < n_c) v = load16(src, src_bytes, ga.at(i0));
     return v;
   };
+  // an untiled chunk's lane starts at 2^S + D, D its first ck symbols (cb
+  // bits each, the first lowest), which are not coded; tiled chunks at 2^16
+  const uint32_t ck = T.tiled ? 0u : (K == kSplit16 ? 2u : (K == kByte ? 3u : 7u));
+  constexpr uint32_t cb = K == kNibble ? 4u : 8u;
+  constexpr uint32_t cs = K == kSplit16 ? 16u : (K == kByte ? 24u : 28u);
+  const uint4 zero = make_uint4(0u, 0u, 0u, 0u);
+  const uint4 first = rows ? load_row(0) : zero;  // row 0, kept for the last row coded
   uint32_t x = wc::kStateLow;
+  if (ck) {
+    const uint32_t nv0 = lane < L && lane * W < n_c ? min(W, n_c - lane * W) : 0u;
+    uint32_t D = 0;
+#pragma unroll
+    for (uint32_t k = 0; k < 7; k++)
+      if (k < ck && k < nv0) D |= symbol<K>(first, k) << (cb * k);
+    x = (1u << cs) + D;
+  }
   uint32_t top = 0;  // words pushed
-  uint4 cur = rows ? load_row(rows - 1) : make_uint4(0u, 0u, 0u, 0u);
+  uint4 cur = rows > 1 ? load_row(rows - 1) : first;
   for (uint32_t r = rows; r-- > 0;) {
     // the next row's load is in flight while this row is coded
-    const uint4 nxt = r ? load_row(r - 1) : make_uint4(0u, 0u, 0u, 0u);
+    const uint4 nxt = r > 1 ? load_row(r - 1) : (r == 1 ? first : zero);
     const uint32_t i0 = r * LW + lane * W;
     const uint32_t nv = lane < L && i0 < n_c ? min(W, n_c - i0) : 0u;
 #pragma unroll
     for (uint32_t kk = 0; kk < W; kk++) {
       const uint32_t k = W - 1 - kk;
-      const bool active = k < nv;
+      const bool active = k < nv && (r != 0 || k >= ck);
       const uint4 e = tab[symbol<K>(cur, k)];  // {f, cum, r_lo, r_hi}
       const bool emit = active && (x >> 20) >= e.x;
       const uint64_t m = __ballot(emit);

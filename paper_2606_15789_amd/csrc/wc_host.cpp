@@ -180,16 +180,22 @@ struct Record {
 };
 
 void encode_chunk(const uint8_t* sym, uint64_t n, const EncSym* tab, uint32_t L, uint32_t W,
-                  Record& rec, std::vector<uint16_t>& stack) {
+                  Carry cy, Record& rec, std::vector<uint16_t>& stack) {
   uint32_t A = uint32_t(std::min<uint64_t>(L, (n + W - 1) / W));
   uint32_t x[kMaxLanes];
-  for (uint32_t l = 0; l < A; l++) x[l] = kStateLow;
+  for (uint32_t l = 0; l < A; l++) {
+    // the lane's first K symbols (row 0, steps 0..K-1) ride in its start state
+    uint32_t D = 0;
+    for (uint32_t k = 0; k < cy.K; k++)
+      if (uint64_t(l) * W + k < n) D |= uint32_t(sym[uint64_t(l) * W + k]) << (cy.b * k);
+    x[l] = cy.K ? (1u << cy.S) + D : kStateLow;
+  }
   stack.resize(n + 1);
   uint16_t* top = stack.data() + stack.size();  // grows downwards
   const uint64_t LW = uint64_t(L) * W;
   const uint64_t rows = (n + LW - 1) / LW;
   for (uint64_t r = rows; r-- > 0;) {
-    for (uint32_t k = W; k-- > 0;) {
+    for (uint32_t k = W; k-- > (r == 0 ? cy.K : 0u);) {
       for (uint32_t l = A; l-- > 0;) {
         uint64_t i = r * LW + uint64_t(l) * W + k;
         if (i >= n) continue;
@@ -458,7 +464,7 @@ using namespace wc;
 
 extern "C" {
 
-int32_t wc_version(void) { return 10; }
+int32_t wc_version(void) { return 11; }
 
 wc_status wc_analyze(const wc_tensor* t, wc_stats* out) {
   if (!t || !out || (!t->host_ptr && t->nbytes)) return WC_EINVAL;
@@ -584,7 +590,8 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
       parallel_for(T.n_chunks, threads, [&](uint64_t c) {
         thread_local std::vector<uint16_t> stack;
         uint64_t s0 = c * per, len = std::min(per, T.n_sym - s0);
-        encode_chunk(coded.data() + s0, len, tab, L, T.group, recs[T.first_chunk + c], stack);
+        encode_chunk(coded.data() + s0, len, tab, L, T.group, carry_of(T.dtype, T.tile_r != 0),
+                     recs[T.first_chunk + c], stack);
       });
       std::vector<uint8_t>().swap(codeds[t]);
     }

@@ -11,7 +11,7 @@
 namespace wc {
 
 constexpr uint32_t kMagic = 0x31424357u;  // "WCB1"
-constexpr uint32_t kVersion = 3;        // blob format version
+constexpr uint32_t kVersion = 4;        // blob format version
 constexpr uint32_t kProbBits = 12;        // b = 12 (Sec. VI-F)
 constexpr uint32_t kTableSize = 1u << kProbBits;
 constexpr uint32_t kStateLow = 1u << 16;  // lower end of the state interval
@@ -31,6 +31,22 @@ inline uint64_t symbols_of(uint32_t dt, uint64_t bytes) {
   return is_nibble(dt) ? 2 * bytes : (is_byte(dt) ? bytes : bytes / 2);
 }
 inline uint64_t pad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
+
+// Start states that carry data (blob version 4).  The encoder's start state
+// comes back to the decoder for free at the end of a lane, so an untiled
+// chunk spends it: lane l starts at 2^S + D, D packing the lane's first K
+// symbols (b bits each, the first lowest), and those steps are not coded.  A
+// decoded lane must end at 2^S + D with D within the symbols it carries.
+// Tiled chunks, the fused GEMMs' input, start at 2^16 and carry nothing.
+struct Carry {
+  uint32_t K, b, S;
+};
+inline Carry carry_of(uint32_t dt, bool tiled) {
+  if (tiled) return {0, 8, 16};
+  if (has_raw(dt)) return {2, 8, 16};    // exponent bytes of bf16 / fp16
+  if (is_nibble(dt)) return {7, 4, 28};  // int4 / fp4 nibbles
+  return {3, 8, 24};                     // int8 / fp8 bytes
+}
 inline bool pow2(uint64_t x) { return x && !(x & (x - 1)); }
 
 // A tensor is cut into tile_r x tile_c tiles (one chunk each) when its shape

@@ -353,7 +353,13 @@ def _records_match_oracle(raw, t, host, rng, n_sample=3):
     out = np.empty(host.size * 2, np.uint8)
     orig = host.view(np.uint8).reshape(-1)
     for c in picks:
-        states, words = oracle.encode_stream(coded[c * E:(c + 1) * E], freq, 64, 8)
+        # an untiled bf16 chunk: each lane starts at 2^16 plus its first two
+        # exponent bytes (the first lowest), which are not coded
+        sym = coded[c * E:(c + 1) * E]
+        init = [(1 << 16) + sum(int(sym[lane * 8 + t]) << (8 * t) for t in range(2)
+                                if lane * 8 + t < sym.size) for lane in range(64)]
+        states, words = oracle.encode_stream(sym, freq, 64, 8, init=np.array(init, np.uint32),
+                                             skip=2)
         off = 16 * struct.unpack_from("<I", raw, index_off + 4 * (first + c))[0]
         nw, na, nsym, zero = struct.unpack_from("<IIII", raw, off)
         assert (nw, na, zero) == (words.size, states.size, 0), (t, c)

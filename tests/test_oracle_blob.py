@@ -18,7 +18,8 @@ from paper_2606_15789_amd import synth
 def roundtrip(tensors, **kw):
     blob = oracle.encode(tensors, **kw)
     outs = oracle.decode(blob)
-    for (dt, data), out in zip(tensors, outs):
+    for entry, out in zip(tensors, outs):
+        dt, data = entry[0], entry[1]
         assert np.array_equal(out, np.ascontiguousarray(data).view(np.uint8).reshape(-1)), dt
     return blob
 
@@ -54,17 +55,112 @@ def test_edge_sizes(dtype, esize, cb):
             roundtrip([(dtype, data)], chunk_bytes=cb, lanes=lanes)
 
 
-def test_single_symbol_tensor_has_no_words():
-    blob = roundtrip([("u8", np.full(100_000, 42, np.uint8))], chunk_bytes=65536, lanes=64)
-    # 2 chunks: each record is 16 B header + 64 states, no words
+def _records(blob):
+    """(word count, states, words) of every chunk record, in index order."""
     n_c = struct.unpack_from("<Q", blob, 16)[0]
     idx = struct.unpack_from("<Q", blob, 32)[0]
+    out = []
     for c in range(n_c):
         off = struct.unpack_from("<I", blob, idx + 4 * c)[0] * 16
         nw, A, ns, _ = struct.unpack_from("<IIII", blob, off)
+        states = np.array(struct.unpack_from(f"<{A}I", blob, off + 16), np.uint32)
+        wpos = off + 16 + ((4 * A + 15) // 16) * 16
+        words = np.frombuffer(bytes(blob[wpos:wpos + 2 * nw]), np.uint16)
+        out.append((nw, states, words))
+    return out
+
+
+def test_single_symbol_tensor_has_no_words():
+    blob = roundtrip([("u8", np.full(100_000, 42, np.uint8))], chunk_bytes=65536, lanes=64)
+    # 2 chunks: each record is 16 B header + 64 states, no words.  A one-symbol
+    # table (f = 2^12) leaves every state as it starts, and a lane of byte
+    # symbols starts at 2^24 plus its first three bytes: 0x012A2A2A
+    for nw, states, _ in _records(blob):
         assert nw == 0
-        states = struct.unpack_from(f"<{A}I", blob, off + 16)
-        assert all(s == 65536 for s in states)
+        assert all(int(s) == (1 << 24) + 0x2A2A2A for s in states)
+
+
+# --- lane states that carry data (format version 4) --------------------------
+# An untiled chunk's lane l starts the encoder at 2^S + D, D holding the lane's
+# first K symbols (b bits each, the first in the lowest bits), and those steps
+# are not coded: K, b, S = 2, 8, 16 for the exponent bytes of bf16 / fp16,
+# 3, 8, 24 for byte symbols, 7, 4, 28 for nibbles.
+
+CARRY = {"bf16": (2, 8, 16), "u8": (3, 8, 24), "fp8_e5m2": (3, 8, 24), "u4": (7, 4, 28)}
+
+
+def test_carried_states_written_out():
+    # one lane, exactly K symbols: nothing is coded and the state is 2^S + D,
+    # worked out by hand from the symbols
+    blob = roundtrip([("u8", np.array([5, 6, 7], np.uint8))], lanes=1)
+    assert [(nw, list(st)) for nw, st, _ in _records(blob)] == [(0, [0x01070605])]
+    # nibbles 1..6 (low nibble first)
+    blob = roundtrip([("u4", np.array([0x21, 0x43, 0x65], np.uint8))], lanes=1)
+    assert [list(st) for _, st, _ in _records(blob)] == [[(1 << 28) + 0x654321]]
+    # bf16 1.0 (exponent byte 127) and -2.0 (exponent byte 128): 2^16 + 127 + 128 * 256
+    blob = roundtrip([("bf16", np.array([0x3F80, 0xC000], np.uint16))], lanes=1)
+    assert [list(st) for _, st, _ in _records(blob)] == [[(1 << 16) + 127 + 128 * 256]]
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "u8", "u4"])
+@pytest.mark.parametrize("lanes", [64, 7])
+def test_carry_equals_the_stream_coder_from_those_states(dtype, lanes):
+    """Each record equals the (separately pinned) stream coder started from
+    2^S + D with steps below K left out, D assembled here from the symbols."""
+    K, b, S = CARRY[dtype]
+    rng = np.random.default_rng(3)
+    n_bytes = 3 * 4096 + 1234
+    if dtype == "bf16":
+        data = (rng.standard_normal(n_bytes // 2) * 0.02).astype(np.float32)
+        data = (data.view(np.uint32) >> 16).astype(np.uint16)
+    else:
+        data = np.minimum(rng.geometric(0.15, n_bytes), 255).astype(np.uint8)
+    cb = 4096
+    blob = roundtrip([(dtype, data)], chunk_bytes=cb, lanes=lanes)
+    coded, _ = oracle.symbols(dtype, data)
+    freq = np.array(struct.unpack_from(f"<{16 if dtype == 'u4' else 256}H", blob,
+                                       struct.unpack_from("<Q", blob, 64 + 48)[0]), np.uint32)
+    W = {"bf16": 8, "u8": 16, "u4": 32}[dtype]
+    per = {"bf16": cb // 2, "u8": cb, "u4": 2 * cb}[dtype]
+    for c, (nw, states, words) in enumerate(_records(blob)):
+        sym = coded[c * per:(c + 1) * per]
+        init = []
+        for lane in range(lanes):
+            D = 0
+            for t in range(K):
+                i = (t // W) * lanes * W + lane * W + t % W
+                if i < sym.size:
+                    D |= int(sym[i]) << (b * t)
+            init.append((1 << S) + D)
+        st2, w2 = oracle.encode_stream(sym, freq, lanes, W, init=np.array(init, np.uint32),
+                                       skip=K)
+        assert np.array_equal(states, st2) and np.array_equal(words, w2), c
+
+
+def test_carried_state_corruption_is_reported():
+    data = np.minimum(np.random.default_rng(5).geometric(0.2, 40000), 255).astype(np.uint8)
+    blob = bytearray(oracle.encode([("u8", data)], chunk_bytes=16384, lanes=64))
+    idx = struct.unpack_from("<Q", blob, 32)[0]
+    off = struct.unpack_from("<I", blob, idx + 4)[0] * 16             # chunk 1
+    blob[off + 16 + 4 * 5 + 3] ^= 0x02                                 # lane 5: bit 25 of its state
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.decode(bytes(blob))
+    assert e.value.rc == -3
+
+
+def test_tiled_chunks_keep_the_plain_start():
+    # one 64 x 512 tile = the whole matrix, row-major: its record is the plain
+    # stream coder's output (every lane from 2^16, nothing left out)
+    w = (np.random.default_rng(6).standard_normal(64 * 512) * 0.02).astype(np.float32)
+    w = (w.view(np.uint32) >> 16).astype(np.uint16)
+    blob = roundtrip([("bf16", w, (64, 512))], lanes=64, tile=(64, 512))
+    assert oracle.tensor_info(blob)[0]["tile"] == (64, 512)
+    coded, _ = oracle.symbols("bf16", w)
+    freq = np.array(struct.unpack_from("<256H", blob, struct.unpack_from("<Q", blob, 64 + 48)[0]),
+                    np.uint32)
+    (nw, states, words), = _records(blob)
+    st2, w2 = oracle.encode_stream(coded, freq, 64, 8)
+    assert np.array_equal(states, st2) and np.array_equal(words, w2)
 
 
 def test_multi_tensor_layer_and_chunk_decode():
