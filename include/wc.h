@@ -26,12 +26,12 @@
  * passed as plain pointers (`void*`), so any allocator (torch, hipMalloc)
  * can own them.
  *
- * Blob format version 4 (little-endian; every offset absolute from the blob
+ * Blob format version 5 (little-endian; every offset absolute from the blob
  * start): header 64 B, then one 96-B descriptor per tensor (type, chunk size,
  * sizes, lanes, table and raw offsets, shape and tile), then the u16 frequency
  * tables (16-B padded; tensors sharing a codebook point to one table), the
- * chunk index (u32 per chunk + 1: record offset / 16), the chunk records and
- * the raw bytes.  A chunk covers `chunk_bytes` of decoded output (a tile of a
+ * chunk index (u32 per chunk + 1: record offset / 16), the raw bytes and the
+ * chunk records (the raw regions' places depend on the sizes only).  A chunk covers `chunk_bytes` of decoded output (a tile of a
  * tiled tensor, whose symbols and raw bytes are stored tile by tile); its
  * record is
  *     u32 n_words, u32 n_states (A), u32 n_symbols, u32 0,
@@ -470,7 +470,7 @@ wc_status wc_stream(const void* dev_src, uint64_t src_bytes, void* dev_dst, uint
 /* wc_free -- release a blob from wc_encode / wc_open.  NULL is a no-op. */
 void wc_free(wc_blob* b);
 
-/* wc_version -- ABI version of this header (11). */
+/* wc_version -- ABI version of this header (12). */
 int32_t wc_version(void);
 
 #ifdef __cplusplus

@@ -43,7 +43,7 @@
 #define ORC_M (1u << ORC_PROB_BITS)   /* table total 2^12 (Sec. VI-F, b = 12) */
 #define ORC_STATE_LOW (1u << 16)       /* rANS lower bound of the state        */
 #define ORC_MAGIC 0x31424357u          /* bytes 'W','C','B','1'                */
-#define ORC_VERSION 4u
+#define ORC_VERSION 5u
 
 #define ORC_OK 0
 #define ORC_EINVAL (-1)
@@ -537,9 +537,9 @@ int orc_decode_stream(const uint32_t* states_in, uint32_t n_states, const uint16
 }
 
 /* ------------------------------------------------------------------------ */
-/* Blob: header, tensor descriptors, tables, chunk index, chunk records and  */
-/* the raw bytes (layout readings in the design notes; Sec. IV-A / V-B give  */
-/* per-tile substreams plus an offset table).                                */
+/* Blob: header, tensor descriptors, tables, chunk index, the raw bytes and  */
+/* the chunk records (layout readings in the design notes; Sec. IV-A / V-B   */
+/* give per-tile substreams plus an offset table).                           */
 
 typedef struct {
   const uint8_t* data;
@@ -741,17 +741,19 @@ int orc_encode_blob(const orc_tensor* ts, uint32_t n_tensors, uint32_t chunk_byt
       freq_off[t] = freq_off[owner];
     }
   }
+  /* the raw regions come before the records (format 5): their places depend
+     on the tensor sizes only, not on how well the chunks code */
   uint64_t off_index = round16(pos);
-  uint64_t off_records = round16(off_index + 4ull * (n_chunks + 1));
-  pos = off_records;
-  for (uint64_t c = 0; c < n_chunks && rc == ORC_OK; c++) pos += rec_size[c];
-  uint64_t off_raw = pos;
+  uint64_t off_raw = round16(off_index + 4ull * (n_chunks + 1));
+  pos = off_raw;
   for (uint32_t t = 0; t < n_tensors && rc == ORC_OK; t++) {
     if (has_raw(ts[t].dtype)) {
       raw_off_t[t] = pos;
       pos += round16(n_symbols_of(ts[t].dtype, ts[t].nbytes));
     }
   }
+  uint64_t off_records = pos;
+  for (uint64_t c = 0; c < n_chunks && rc == ORC_OK; c++) pos += rec_size[c];
   uint64_t total = pos;
   if (rc == ORC_OK && total / 16 > 0xFFFFFFFFull) rc = ORC_EINVAL;
 
@@ -900,13 +902,16 @@ static int check_header(const uint8_t* b, uint64_t size) {
   uint64_t off_index = get64(b + 32), off_rec = get64(b + 40), off_raw = get64(b + 48);
   if (n_t == 0 || 64 + (uint64_t)ORC_DESC * n_t > size) return ORC_EINVAL;
   if (off_index > size || n_c + 1 > (size - off_index) / 4) return ORC_EINVAL;
-  if (off_rec > off_raw || off_raw > size) return ORC_EINVAL;
+  if (off_index + 4 * (n_c + 1) > off_raw || off_raw > off_rec || off_rec > size)
+    return ORC_EINVAL;
   uint64_t first = 0;
   for (uint32_t t = 0; t < n_t; t++) {
     orc_desc d;
     int rc = read_desc(b, size, t, &d);
     if (rc) return rc;
     if (d.first_chunk != first) return ORC_EINVAL;
+    if (has_raw(d.dtype) && (d.raw_off < off_raw || d.n_sym > off_rec - d.raw_off))
+      return ORC_EINVAL;
     first += d.n_chunks;
     if (d.n_sym > 0) {
       uint32_t sum = 0;
@@ -917,7 +922,7 @@ static int check_header(const uint8_t* b, uint64_t size) {
   if (first != n_c) return ORC_EINVAL;
   for (uint64_t c = 0; c <= n_c; c++) {
     uint64_t o = 16ull * get32(b + off_index + 4 * c);
-    if (o < off_rec || o > off_raw) return ORC_EINVAL;
+    if (o < off_rec || o > size) return ORC_EINVAL;
     if (c > 0 && o < 16ull * get32(b + off_index + 4 * (c - 1))) return ORC_EINVAL;
   }
   return ORC_OK;

@@ -1191,7 +1191,7 @@ inline void fill_common(LaunchArgs& args, const wc::BlobPriv& P, const void* dev
   args.blob = reinterpret_cast<uint64_t>(dev_blob);
   args.index_off = P.index_off;
   args.records_off = P.records_off;
-  args.records_end = P.raw_off;
+  args.records_end = P.size;
   args.err = reinterpret_cast<uint64_t>(dev_err);
 }
 

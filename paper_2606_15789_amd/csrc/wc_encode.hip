@@ -68,8 +68,9 @@ struct EncTensor {
 
 struct EncArgs {
   uint64_t blob, ws;
-  uint64_t hist_off, tab_off, rsz_off, misc_off;
+  uint64_t hist_off, tab_off, rsz_off;
   uint64_t index_off;  // blob offset of the chunk index
+  uint64_t raw_start;  // blob offset of the raw regions (after the index)
   uint32_t n_tensors, pad;
   EncTensor t[kMaxLaunch];
 };
@@ -360,12 +361,35 @@ __device__ void encode_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, u
     x = (1u << cs) + D;
   }
   uint32_t top = 0;  // words pushed
+  // 16-bit formats: the raw byte of every word goes straight to its
+  // coding-order place in the raw region, which precedes the records.  The
+  // stores go through a buffer descriptor: a flat store would also hold the
+  // LDS counter that every step's table read waits on.
+  const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
+      reinterpret_cast<uint8_t*>(a.blob) + a.raw_start + T.raw_rel + s0, (short)0,
+      K == kSplit16 ? (int)n_c : 0, 0x00020000);
   uint4 cur = rows > 1 ? load_row(rows - 1) : first;
   for (uint32_t r = rows; r-- > 0;) {
     // the next row's load is in flight while this row is coded
     const uint4 nxt = r > 1 ? load_row(r - 1) : (r == 1 ? first : zero);
     const uint32_t i0 = r * LW + lane * W;
     const uint32_t nv = lane < L && i0 < n_c ? min(W, n_c - i0) : 0u;
+    if constexpr (K == kSplit16) {
+      // raw byte of a word: bit 15 -> bit 7, bits 6..0 kept
+      uint32_t rb[2] = {0u, 0u};
+#pragma unroll
+      for (uint32_t k = 0; k < 8; k++) {
+        const uint32_t w = (dword(cur, k >> 1) >> (16 * (k & 1))) & 0xFFFFu;
+        rb[k >> 2] |= (((w >> 8) & 0x80u) | (w & 0x7Fu)) << (8 * (k & 3));
+      }
+      if (nv == 8) {
+        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+        __builtin_amdgcn_raw_buffer_store_b64(u32x2{rb[0], rb[1]}, rr, i0, 0, 0);
+      } else {
+        for (uint32_t k = 0; k < nv; k++)
+          __builtin_amdgcn_raw_buffer_store_b8(uint8_t(rb[k >> 2] >> (8 * (k & 3))), rr, i0 + k, 0, 0);
+      }
+    }
 #pragma unroll
     for (uint32_t kk = 0; kk < W; kk++) {
       const uint32_t k = W - 1 - kk;
@@ -386,6 +410,11 @@ __device__ void encode_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, u
       x = active ? xn : x;
     }
     cur = nxt;
+  }
+  if (K == kSplit16 && c + 1 == T.n_chunks) {
+    // the raw region's zero padding to 16 bytes
+    uint8_t* end = reinterpret_cast<uint8_t*>(a.blob) + a.raw_start + T.raw_rel;
+    if (lane < dpad16(T.n_sym) - T.n_sym) end[T.n_sym + lane] = 0;
   }
   // record header, states and their padding at the slot's start
   uint32_t* hdr = reinterpret_cast<uint32_t*>(slot);
@@ -415,12 +444,12 @@ __global__ __launch_bounds__(kThreads) void encode_kernel(EncArgs a) {
 
 // ---------------------------------------------------------------------------
 // 5. offset index: exclusive scan of the record sizes (16-byte units) from the
-// records' start; then the header, with the size and raw offset it implies.
+// records' start; then the header, with the size it implies.
 
 struct ScanArgs {
-  uint64_t blob, ws, rsz_off, misc_off, size_out;
-  uint64_t index_off, records_off, raw_region_bytes, n_chunks;
-  uint32_t header[16];  // the header with size and raw offset still 0
+  uint64_t blob, ws, rsz_off, size_out;
+  uint64_t index_off, raw_start, records_off, n_chunks;
+  uint32_t header[16];  // the header with the size still 0
 };
 
 __global__ __launch_bounds__(kScanThreads) void scan_kernel(ScanArgs a) {
@@ -451,69 +480,51 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(ScanArgs a) {
     if (tid == kScanThreads - 1) carry_s = carry + before + incl;
     __syncthreads();
   }
-  const uint64_t raw_start = a.records_off + 16 * carry_s;
-  const uint64_t size = raw_start + a.raw_region_bytes;
+  const uint64_t size = a.records_off + 16 * carry_s;
   if (tid == 0) {
-    index[a.n_chunks] = uint32_t(raw_start / 16);
-    reinterpret_cast<uint64_t*>(a.ws + a.misc_off)[0] = raw_start;
+    index[a.n_chunks] = uint32_t(size / 16);
     *reinterpret_cast<uint64_t*>(a.size_out) = size;
   }
-  // zeros between the index and the records
+  // zeros between the index and the raw regions
   uint8_t* b = reinterpret_cast<uint8_t*>(a.blob);
-  for (uint64_t o = a.index_off + 4 * (a.n_chunks + 1) + tid; o < a.records_off; o += kScanThreads)
+  for (uint64_t o = a.index_off + 4 * (a.n_chunks + 1) + tid; o < a.raw_start; o += kScanThreads)
     b[o] = 0;
   if (tid < 16) {
     uint32_t h = a.header[tid];
     if (tid == 6) h = uint32_t(size);  // bytes 24..31: size
     if (tid == 7) h = uint32_t(size >> 32);
-    if (tid == 12) h = uint32_t(raw_start);  // bytes 48..55: raw region
-    if (tid == 13) h = uint32_t(raw_start >> 32);
     reinterpret_cast<uint32_t*>(a.blob)[tid] = h;
   }
 }
 
 // ---------------------------------------------------------------------------
-// 6. descriptors: 96 bytes per tensor from the host, raw offsets rebased on
-// the raw regions' start.
+// 6. descriptors: 96 bytes per tensor, as the host wrote them.
 
 struct DescArgs {
-  uint64_t blob, ws, misc_off;
+  uint64_t blob;
   uint32_t first, n;
-  uint32_t raw_mask;  // tensors (bit i: first + i) with a raw region
-  uint32_t pad;
   uint32_t d[kMaxLaunch * 2][24];
 };
 
 __global__ void desc_kernel(DescArgs a) {
   const uint32_t t = threadIdx.x / 24, j = threadIdx.x % 24;
   if (t >= a.n) return;
-  const uint64_t raw_start = reinterpret_cast<const uint64_t*>(a.ws + a.misc_off)[0];
-  uint32_t v = a.d[t][j];
-  if ((a.raw_mask >> t) & 1u) {
-    // bytes 56..63: raw offset (relative to the raw regions' start in d)
-    const uint64_t rel = uint64_t(a.d[t][14]) | (uint64_t(a.d[t][15]) << 32);
-    const uint64_t abs = raw_start + rel;
-    if (j == 14) v = uint32_t(abs);
-    if (j == 15) v = uint32_t(abs >> 32);
-  }
   reinterpret_cast<uint32_t*>(a.blob + wc::kHeaderBytes + uint64_t(wc::kDescBytes) * (a.first + t))[j] =
-      v;
+      a.d[t][j];
 }
 
 // ---------------------------------------------------------------------------
 // 7. packing: one wave per chunk moves its record from the slot to the offset
-// the index gives (words re-based from the stack's end, zero padding), and
-// for 16-bit formats writes the chunk's raw bytes at their coding-order place.
+// the index gives (words re-based from the stack's end, zero padding).
 
 template <uint32_t K>
 __device__ void pack_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, uint32_t lane) {
-  constexpr uint32_t W = K == kSplit16 ? 8u : (K == kByte ? 16u : 32u);
   const uint32_t g = T.first_chunk + c;
   uint8_t* blob = reinterpret_cast<uint8_t*>(a.blob);
   const uint64_t o = 16ull * reinterpret_cast<const uint32_t*>(a.blob + a.index_off)[g];
   const uint8_t* slot = reinterpret_cast<const uint8_t*>(a.ws + T.slot_off) + uint64_t(c) * T.slot_bytes;
   const uint4 hdr = *reinterpret_cast<const uint4*>(slot);
-  const uint32_t nw = hdr.x, A = hdr.y, n_c = hdr.z;
+  const uint32_t nw = hdr.x, A = hdr.y;
   const uint32_t head = 16u + uint32_t(dpad16(4ull * A));
   // header and states (16-byte units)
   for (uint32_t j = lane; j < head / 16; j += 64)
@@ -536,55 +547,6 @@ __device__ void pack_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, uin
 #pragma unroll
     for (uint32_t q = 0; q < 4; q++) w[q] = sh ? __builtin_amdgcn_alignbit(d[q + 1], d[q], 16) : d[q];
     *reinterpret_cast<uint4*>(blob + o + head + 16ull * j) = make_uint4(w[0], w[1], w[2], w[3]);
-  }
-  if constexpr (K == kSplit16) {
-    // raw byte of a word: bit 15 -> bit 7, bits 6..0 kept
-    const uint64_t raw_start = reinterpret_cast<const uint64_t*>(a.ws + a.misc_off)[0];
-    uint8_t* raw = blob + raw_start + T.raw_rel + uint64_t(c) * T.per;
-    const uint8_t* src = reinterpret_cast<const uint8_t*>(T.src);
-    const GroupAddr ga(T, c);
-    const uint32_t groups = (n_c + W - 1) / W;
-    // a lane takes pairs of lane-groups (16 raw bytes, one 16-byte store);
-    // kPairs pairs per lane per round, their source loads all in flight at once
-    constexpr uint32_t kPairs = 4;
-    const uint32_t pairs = (groups + 1) / 2;
-    for (uint32_t p0 = 0; p0 < pairs; p0 += 64 * kPairs) {
-      uint4 v[kPairs][2];
-#pragma unroll
-      for (uint32_t b = 0; b < kPairs; b++)
-#pragma unroll
-        for (uint32_t h = 0; h < 2; h++) {
-          const uint32_t gi = 2 * (p0 + 64 * b + lane) + h;
-          v[b][h] = gi < groups ? load16(src, T.src_bytes, ga.at(gi * W)) : make_uint4(0u, 0u, 0u, 0u);
-        }
-#pragma unroll
-      for (uint32_t b = 0; b < kPairs; b++) {
-        const uint32_t p = p0 + 64 * b + lane;
-        if (p >= pairs) continue;
-        uint32_t rb[4] = {0u, 0u, 0u, 0u};
-#pragma unroll
-        for (uint32_t h = 0; h < 2; h++)
-#pragma unroll
-          for (uint32_t k = 0; k < 8; k++) {
-            const uint32_t w = (dword(v[b][h], k >> 1) >> (16 * (k & 1))) & 0xFFFFu;
-            const uint32_t r = ((w >> 8) & 0x80u) | (w & 0x7Fu);
-            rb[2 * h + (k >> 2)] |= r << (8 * (k & 3));
-          }
-        const uint32_t i0 = 2 * p * W;
-        const uint32_t nv = min(2 * W, n_c - i0);
-        if (nv == 2 * W && (reinterpret_cast<uintptr_t>(raw + i0) & 15u) == 0) {
-          *reinterpret_cast<uint4*>(raw + i0) = make_uint4(rb[0], rb[1], rb[2], rb[3]);
-        } else {
-          for (uint32_t k = 0; k < nv; k++) raw[i0 + k] = uint8_t(rb[k >> 2] >> (8 * (k & 3)));
-        }
-      }
-    }
-    if (c + 1 == T.n_chunks) {
-      // the raw region's zero padding to 16 bytes
-      uint8_t* end = blob + raw_start + T.raw_rel;
-      const uint64_t padded = dpad16(T.n_sym);
-      if (lane < padded - T.n_sym) end[T.n_sym + lane] = 0;
-    }
   }
 }
 
@@ -610,7 +572,7 @@ using wc::Plan;
 using wc::TensorInfo;
 
 struct WsLayout {
-  uint64_t hist_off, tab_off, rsz_off, misc_off, slots_off, total;
+  uint64_t hist_off, tab_off, rsz_off, slots_off, total;
   std::vector<uint64_t> slot_off;     // per tensor
   std::vector<uint32_t> table_of;     // per tensor: its table's index
   uint32_t n_tables;
@@ -633,8 +595,6 @@ void layout_ws(const Plan& P, WsLayout& L) {
   pos = up256(pos + 16ull * 256 * L.n_tables);
   L.rsz_off = pos;
   pos = up256(pos + 4 * (P.n_chunks + 1));
-  L.misc_off = pos;
-  pos = up256(pos + 16);
   L.slots_off = pos;
   L.slot_off.assign(n, 0);
   for (uint32_t t = 0; t < n; t++) {
@@ -683,8 +643,8 @@ void put64(uint32_t* d, uint32_t byte, uint64_t v) {
   d[byte / 4 + 1] = uint32_t(v >> 32);
 }
 
-// The 96-byte descriptor of T as dwords (raw_off still relative).
-void descriptor(const TensorInfo& T, uint32_t* d) {
+// The 96-byte descriptor of T as dwords (raw_off relative to raw_start).
+void descriptor(const TensorInfo& T, uint64_t raw_start, uint32_t* d) {
   memset(d, 0, 96);
   put32(d, 0, T.dtype);
   put32(d, 4, T.chunk_bytes);
@@ -695,7 +655,7 @@ void descriptor(const TensorInfo& T, uint32_t* d) {
   d[10] = T.lanes | (T.group << 16) | (wc::kProbBits << 24);
   d[11] = T.alphabet;
   put64(d, 48, T.freq_off);
-  put64(d, 56, wc::has_raw(T.dtype) ? T.raw_off : 0);
+  put64(d, 56, wc::has_raw(T.dtype) ? raw_start + T.raw_off : 0);
   put64(d, 64, T.rows);
   put64(d, 72, T.cols);
   put32(d, 80, T.tile_r);
@@ -712,9 +672,7 @@ wc_status plan_device(const wc_dtensor* t, uint32_t n, const wc_params* p, Plan&
   return wc::plan_blob(hs.data(), n, p, P);
 }
 
-uint64_t capacity_of(const Plan& P) {
-  return P.records_off + P.worst_record_bytes + P.raw_region_bytes;
-}
+uint64_t capacity_of(const Plan& P) { return P.records_off + P.worst_record_bytes; }
 
 // Launch `kern` over the tensors in groups of kMaxLaunch, each tensor getting
 // `wgs_of(T)` workgroups.
@@ -801,8 +759,8 @@ extern "C" wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_
     args.hist_off = L.hist_off;
     args.tab_off = L.tab_off;
     args.rsz_off = L.rsz_off;
-    args.misc_off = L.misc_off;
     args.index_off = P.index_off;
+    args.raw_start = P.raw_start;
     // 2. histograms
     if (!launch_groups(
             P, t, L, args,
@@ -833,7 +791,7 @@ extern "C" wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_
         }
       }
     }
-    // 4. chunk encoder
+    // 4. chunk encoder (and the raw bytes of 16-bit formats)
     if (!launch_groups(
             P, t, L, args,
             [](const TensorInfo& T) { return uint32_t((T.n_chunks + kWaves - 1) / kWaves); },
@@ -847,11 +805,10 @@ extern "C" wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_
       sa.blob = blob;
       sa.ws = ws;
       sa.rsz_off = L.rsz_off;
-      sa.misc_off = L.misc_off;
       sa.size_out = reinterpret_cast<uint64_t>(dev_size);
       sa.index_off = P.index_off;
+      sa.raw_start = P.raw_start;
       sa.records_off = P.records_off;
-      sa.raw_region_bytes = P.raw_region_bytes;
       sa.n_chunks = P.n_chunks;
       uint32_t* h = sa.header;
       put32(h, 0, wc::kMagic);
@@ -861,6 +818,7 @@ extern "C" wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_
       put64(h, 16, P.n_chunks);
       put64(h, 32, P.index_off);
       put64(h, 40, P.records_off);
+      put64(h, 48, P.raw_start);
       hipLaunchKernelGGL(scan_kernel, dim3(1), dim3(kScanThreads), 0, st, sa);
       if (hipGetLastError() != hipSuccess) return WC_EHIP;
     }
@@ -868,19 +826,13 @@ extern "C" wc_status wc_encode_device(const wc_dtensor* t, uint32_t n, const wc_
     for (uint32_t t0 = 0; t0 < n; t0 += 2 * kMaxLaunch) {
       DescArgs da{};
       da.blob = blob;
-      da.ws = ws;
-      da.misc_off = L.misc_off;
       da.first = t0;
       da.n = std::min<uint32_t>(2 * kMaxLaunch, n - t0);
-      for (uint32_t i = 0; i < da.n; i++) {
-        const TensorInfo& T = P.tensors[t0 + i];
-        descriptor(T, da.d[i]);
-        if (wc::has_raw(T.dtype)) da.raw_mask |= 1u << i;
-      }
+      for (uint32_t i = 0; i < da.n; i++) descriptor(P.tensors[t0 + i], P.raw_start, da.d[i]);
       hipLaunchKernelGGL(desc_kernel, dim3(1), dim3(24 * 2 * kMaxLaunch), 0, st, da);
       if (hipGetLastError() != hipSuccess) return WC_EHIP;
     }
-    // 7. records and raw bytes
+    // 7. records
     if (!launch_groups(
             P, t, L, args,
             [](const TensorInfo& T) { return uint32_t((T.n_chunks + kWaves - 1) / kWaves); },

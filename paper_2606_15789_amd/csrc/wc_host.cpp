@@ -238,7 +238,7 @@ wc_blob* make_handle(BlobPriv&& bp) {
   b.priv = h;
   // size breakdown
   const uint8_t* base = P.bytes.data();
-  b.meta_bytes = P.records_off;
+  b.meta_bytes = P.raw_off;  // header, descriptors, tables and index
   for (uint64_t c = 0; c < P.n_chunks; c++) {
     uint64_t o0 = 16ull * ld32(base + P.index_off + 4 * c);
     uint64_t o1 = 16ull * ld32(base + P.index_off + 4 * (c + 1));
@@ -248,7 +248,7 @@ wc_blob* make_handle(BlobPriv&& bp) {
     b.word_bytes += 2ull * nw;
     b.pad_bytes += (o1 - o0) - 16 - 4ull * A - 2ull * nw;
   }
-  b.raw_bytes = P.bytes.size() - P.raw_off;
+  b.raw_bytes = P.records_off - P.raw_off;
   return &b;
 }
 
@@ -353,13 +353,15 @@ wc_status plan_blob(const wc_tensor* ts, uint32_t n, const wc_params* prm, Plan&
   }
   out.n_chunks = nc_total;
   out.index_off = pad16(pos);
-  out.records_off = pad16(out.index_off + 4 * (nc_total + 1));
+  // the raw regions follow the index; their places depend on the sizes only
+  out.raw_start = pad16(out.index_off + 4 * (nc_total + 1));
   for (uint32_t t = 0; t < n; t++) {
     TensorInfo& T = out.tensors[t];
     if (!has_raw(T.dtype)) continue;
     T.raw_off = out.raw_region_bytes;
     out.raw_region_bytes += pad16(T.n_sym);
   }
+  out.records_off = out.raw_start + out.raw_region_bytes;
   return WC_OK;
 }
 
@@ -377,7 +379,7 @@ wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out) {
   if (nt == 0 || kHeaderBytes + uint64_t(kDescBytes) * nt > size) return WC_EINVAL;
   if (idx % 16 || rec % 16 || raw % 16) return WC_EINVAL;
   if (idx > size || nc >= (size - idx) / 4) return WC_EINVAL;
-  if (rec < idx + 4 * (nc + 1) || rec > raw || raw > size) return WC_EINVAL;
+  if (raw < idx + 4 * (nc + 1) || raw > rec || rec > size) return WC_EINVAL;
   out.tensors.assign(nt, TensorInfo());
   out.out_bytes.assign(nt, 0);
   uint64_t first = 0, raw_pos = raw;
@@ -426,13 +428,13 @@ wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out) {
       if (sum != kTableSize) return WC_EINVAL;
     }
     if (has_raw(T.dtype)) {
-      if (T.raw_off != raw_pos || T.raw_off + T.n_sym > size) return WC_EINVAL;
+      if (T.raw_off != raw_pos || T.raw_off + T.n_sym > rec) return WC_EINVAL;
       raw_pos += pad16(T.n_sym);
     }
     first += T.n_chunks;
     out.out_bytes[t] = T.out_bytes;
   }
-  if (first != nc || raw_pos != size) return WC_EINVAL;
+  if (first != nc || raw_pos != rec) return WC_EINVAL;
   // index and chunk records
   uint64_t prev = rec;
   for (uint32_t t = 0; t < nt; t++) {
@@ -441,7 +443,7 @@ wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out) {
     for (uint64_t c = 0; c < T.n_chunks; c++) {
       uint64_t g = T.first_chunk + c;
       uint64_t o0 = 16ull * ld32(p + idx + 4 * g), o1 = 16ull * ld32(p + idx + 4 * (g + 1));
-      if (o0 != prev || o1 < o0 + 16 || o1 > raw) return WC_EINVAL;
+      if (o0 != prev || o1 < o0 + 16 || o1 > size) return WC_EINVAL;
       uint64_t n_c = std::min(per, T.n_sym - c * per);
       uint32_t nw = ld32(p + o0), A = ld32(p + o0 + 4), ns = ld32(p + o0 + 8);
       uint32_t wantA = uint32_t(std::min<uint64_t>(T.lanes, (n_c + T.group - 1) / T.group));
@@ -450,11 +452,12 @@ wc_status parse_blob(const uint8_t* p, uint64_t size, BlobPriv& out) {
       prev = o1;
     }
   }
-  if (prev != raw || 16ull * ld32(p + idx + 4 * nc) != raw) return WC_EINVAL;
+  if (prev != size || 16ull * ld32(p + idx + 4 * nc) != size) return WC_EINVAL;
   out.n_chunks = nc;
   out.index_off = idx;
   out.records_off = rec;
   out.raw_off = raw;
+  out.size = size;
   return WC_OK;
 }
 
@@ -464,7 +467,7 @@ using namespace wc;
 
 extern "C" {
 
-int32_t wc_version(void) { return 11; }
+int32_t wc_version(void) { return 12; }
 
 wc_status wc_analyze(const wc_tensor* t, wc_stats* out) {
   if (!t || !out || (!t->host_ptr && t->nbytes)) return WC_EINVAL;
@@ -596,16 +599,15 @@ wc_status wc_encode(const wc_tensor* ts, uint32_t n, const wc_params* prm, wc_bl
       std::vector<uint8_t>().swap(codeds[t]);
     }
 
-    // layout: the plan fixed everything up to the records; the raw regions
-    // follow the records in tensor order
+    // layout: the plan fixed everything up to the records (the raw regions
+    // sit between the index and the records); the records follow in order
     const uint64_t idx = plan.index_off;
+    const uint64_t raw = plan.raw_start;
     const uint64_t rec = plan.records_off;
-    uint64_t pos = rec;
-    for (auto& r : recs) pos += r.bytes.size();
-    const uint64_t raw = pos;
     for (uint32_t t = 0; t < n; t++)
       if (has_raw(P.tensors[t].dtype)) P.tensors[t].raw_off += raw;
-    pos = raw + plan.raw_region_bytes;
+    uint64_t pos = rec;
+    for (auto& r : recs) pos += r.bytes.size();
     const uint64_t total = pos;
     if (total / 16 >= 0xFFFFFFFFull) return WC_EINVAL;
 

@@ -11,7 +11,7 @@
 namespace wc {
 
 constexpr uint32_t kMagic = 0x31424357u;  // "WCB1"
-constexpr uint32_t kVersion = 4;        // blob format version
+constexpr uint32_t kVersion = 5;        // blob format version
 constexpr uint32_t kProbBits = 12;        // b = 12 (Sec. VI-F)
 constexpr uint32_t kTableSize = 1u << kProbBits;
 constexpr uint32_t kStateLow = 1u << 16;  // lower end of the state interval
@@ -78,7 +78,8 @@ struct BlobPriv {
   std::vector<uint8_t> bytes;
   std::vector<uint64_t> out_bytes;
   std::vector<TensorInfo> tensors;
-  uint64_t n_chunks = 0, index_off = 0, records_off = 0, raw_off = 0;
+  // raw regions at [raw_off, records_off), records at [records_off, size)
+  uint64_t n_chunks = 0, index_off = 0, raw_off = 0, records_off = 0, size = 0;
 };
 
 // What a wc_blob's `priv` points at: the public struct and the parsed blob.
@@ -90,12 +91,13 @@ struct BlobHandle {
 // The data-independent part of a blob's layout, shared by the host encoder
 // (wc_encode) and the device encoder (wc_encode_device): per-tensor chunking
 // and tiling, the table each tensor uses and where it sits, the chunk index,
-// and where each raw region starts relative to the first one.  Everything
-// after the index depends on the coded data only through the records' total.
+// the raw regions (right after the index) and where the records start.  Only
+// the records' sizes, and with them the index and the blob's end, depend on
+// the coded data.
 struct Plan {
   std::vector<TensorInfo> tensors;  // freq_off absolute; raw_off relative to the raw regions' start
   std::vector<uint32_t> owner;      // tensor whose table a tensor uses (itself unless a layer codebook)
-  uint64_t n_chunks = 0, index_off = 0, records_off = 0;
+  uint64_t n_chunks = 0, index_off = 0, raw_start = 0, records_off = 0;
   uint64_t raw_region_bytes = 0;    // sum of pad16(n_sym) over the 16-bit tensors
   uint64_t worst_record_bytes = 0;  // all records if every symbol emitted a word
 };

@@ -212,11 +212,12 @@ def test_tensors_past_4_gib(dev):
     assert list(desc.out_bytes) == [65541 * 65533, 131073 * 32768]
     info = oracle.tensor_info(host)
     # header bytes 32 and 48: u64 offsets of the index (record offsets / 16)
-    # and of the raw region; the bf16 tensor's chunks follow the int8 tensor's
+    # and of the raw region, which sits between the index and the records; the
+    # bf16 tensor's chunk records follow the int8 tensor's, all past 4 GiB
     index, raw = (int(host[o:o + 8].view(np.uint64)[0]) for o in (32, 48))
     g = info[0]["n_chunks"]
     first_bf16 = 16 * int(host[index + 4 * g:index + 4 * g + 4].view(np.uint32)[0])
-    assert first_bf16 < 2**32 < raw < n, (first_bf16, raw, n)
+    assert raw < 2**32 < first_bf16 < n, (raw, first_bf16, n)
     say("blob bytes", n, "bf16 records from", first_bf16, "raw region from", raw)
     err = torch.zeros(1, dtype=torch.int32, device=dev)
     outs = wc.decode_torch(desc, blob, err=err)

@@ -216,7 +216,7 @@ def _payload(blob):
         nw, A = struct.unpack_from("<II", blob, off)
         states += 4 * A
         words += 2 * nw
-    return states + words + (len(blob) - raw)
+    return states + words + (rec - raw)   # the raw regions sit between index and records
 
 
 @pytest.mark.parametrize("cfg,div", [(1, 1), (2, 4), (3, 4), (4, 4), (6, 4), (7, 4), (8, 4),

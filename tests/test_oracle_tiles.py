@@ -122,10 +122,11 @@ def test_tiled_index_matches_the_per_tile_metadata_term():
     d, s = _matrix("bf16", 256, 1024, 8)
     for tr, tc in ((32, 128), (64, 256)):
         blob = oracle.encode([("bf16", d, s)], tile=(tr, tc), codebook="layer")
-        off_index, off_rec = struct.unpack_from("<QQ", blob, 32)
+        # the index runs from its offset to the raw region, which follows it
+        off_index, off_rec, off_raw = struct.unpack_from("<QQQ", blob, 32)
         n_tiles = (256 // tr) * (1024 // tc)
         index_bytes = 4 * (n_tiles + 1)
-        assert off_rec - off_index == (index_bytes + 15) // 16 * 16
+        assert off_raw - off_index == (index_bytes + 15) // 16 * 16
         closed = oracle.metadata_bytes(256, 1024, tr, tc, 12) - (1 << 12) * 4
         assert index_bytes - 4 == closed
 
