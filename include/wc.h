@@ -357,8 +357,8 @@ wc_status wc_gemm_workspace_bytes(const wc_blob* desc, uint32_t n, const uint32_
  * so the fused call pays off up to about 256 rows.  Above that, decode the
  * weights once with wc_decode and multiply with a library GEMM: on one
  * MI355X, for the seven products of a Llama-3-70B layer, the fused call took
- * 0.925 ms at m = 256 against 1.380 ms decode-then-multiply, but 1.786 ms at
- * m = 512 against 1.471 ms, and 3.483 ms at m = 1024 against 1.998 ms.  The
+ * 0.918 ms at m = 256 against 1.356 ms decode-then-multiply, but 1.779 ms at
+ * m = 512 against 1.468 ms, and 3.499 ms at m = 1024 against 1.978 ms.  The
  * call does not switch by itself.
  * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument, or a
  * workspace too small or misaligned) or WC_EUNSUPPORTED (a tensor the path
