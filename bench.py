@@ -61,10 +61,11 @@ ROTATE_BYTES = 1 << 30   # resident bytes the small workloads rotate over
 
 # HBM bytes per launch of the 70B-layer decode from rocprofv3 --pmc FETCH_SIZE and
 # WRITE_SIZE runs, each scaled by the same counter on a 512 MiB device copy (FETCH_SIZE
-# reads half the copied bytes: factor 2.0; WRITE_SIZE is exact).  Valid only for
-# the kernel source they were taken on (sha256 prefix); otherwise reported as null.
-COUNTED_TRAFFIC = {"kernel_fingerprint": "760f453da281aca2", "fetch_bytes": 1143526810,
-                   "write_bytes": 1711288934, "chunk_bytes": 65536, "lanes": 64}
+# reads half the copied bytes: factor 2.0; WRITE_SIZE is exact).  Valid only for the
+# decode kernel's code they were taken on (its fingerprint, the hash of its gfx950
+# assembly that the build writes); otherwise reported as null.
+COUNTED_TRAFFIC = {"kernel_fingerprint": "e31179740fecb6db", "fetch_bytes": 1143115162,
+                   "write_bytes": 1738021274, "chunk_bytes": 65536, "lanes": 64}
 
 
 def log(*a):
