@@ -10,7 +10,7 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
   __shared__ uint32_t cum[260];
   __shared__ uint32_t ring[kWaves][wc_ring_words() / 2];
 
-  const uint32_t wg = blockIdx.x;
+  const uint32_t wg = xcd_order(blockIdx.x, gridDim.x);
   uint32_t ti = 0;
   for (uint32_t k = 1; k < a.n_tensors; k++)
     if (wg >= a.t[k].wg0) ti = k;

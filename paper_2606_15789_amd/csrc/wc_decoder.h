@@ -115,6 +115,16 @@ struct LaunchArgs {
 
 constexpr uint32_t wc_ring_words() { return kWaveRingWords + kWaveMirrorWords; }
 
+// Workgroup b of a launch runs on XCD b mod 8 (the eight dies take workgroups
+// round-robin, each with its own L2).  Renumber them so that each XCD gets one
+// contiguous block of the launch's workgroups: consecutive chunks, whose
+// records, raw bytes and outputs are adjacent, then share an XCD.  A
+// bijection of [0, n).
+__device__ __forceinline__ uint32_t xcd_order(uint32_t b, uint32_t n) {
+  const uint32_t x = b % 8u, k = b / 8u, q = n / 8u, r = n % 8u;
+  return x * q + min(x, r) + k;
+}
+
 __device__ __forceinline__ uint64_t dpad16(uint64_t x) { return (x + 15) & ~uint64_t(15); }
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {

@@ -131,6 +131,15 @@ struct GroupAddr {
   }
 };
 
+// Workgroup b runs on XCD b mod 8; renumbered so that each XCD takes one
+// contiguous block of the launch's workgroups (a bijection of [0, n)).  The
+// chunk encoder uses it (about 3 % faster); the histogram and pack passes
+// measured no better or worse with it.
+__device__ __forceinline__ uint32_t xcd_order(uint32_t b, uint32_t n) {
+  const uint32_t x = b % 8u, k = b / 8u, q = n / 8u, r = n % 8u;
+  return x * q + min(x, r) + k;
+}
+
 __device__ __forceinline__ uint32_t tensor_of(const EncArgs& a, uint32_t wg) {
   uint32_t ti = 0;
   for (uint32_t k = 1; k < a.n_tensors; k++)
@@ -429,12 +438,13 @@ __device__ void encode_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, u
 
 __global__ __launch_bounds__(kThreads) void encode_kernel(EncArgs a) {
   __shared__ uint4 tab[256];
-  const EncTensor& T = a.t[tensor_of(a, blockIdx.x)];
+  const uint32_t wg = xcd_order(blockIdx.x, gridDim.x);
+  const EncTensor& T = a.t[tensor_of(a, wg)];
   const uint4* tg = reinterpret_cast<const uint4*>(a.ws + a.tab_off) + uint64_t(T.table) * 256u;
   if (threadIdx.x < 256) tab[threadIdx.x] = tg[threadIdx.x];
   __syncthreads();
   const uint32_t wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const uint32_t c = (blockIdx.x - T.wg0) * kWaves + wave;
+  const uint32_t c = (wg - T.wg0) * kWaves + wave;
   if (c >= T.n_chunks) return;
   const uint32_t lane = __lane_id();
   if (T.kind == kSplit16) encode_chunk<kSplit16>(a, T, c, lane, tab);
