@@ -13,17 +13,18 @@
 //      flushed with 64-bit atomics), into the table each tensor uses;
 //   3. normalisation to 2^12 (one workgroup per table, integer largest
 //      remainder exactly as the host does it), the u16 tables written into the
-//      blob, and per symbol {f, cum, ceil(2^64 / f)} for the encoder;
+//      blob, and per symbol {2^12 - f, cum, ceil(2^64 / f)} for the encoder;
 //   4. the chunk encoder: one wave per chunk, one rANS lane per wave lane,
 //      steps in reverse.  Within a step the lanes that emit a word push it in
 //      decreasing lane order (ballot; a lane's place is the number of emitting
 //      lanes above it), so the word stack, written downwards from the end of
-//      the chunk's worst-case workspace slot, is the chunk's stream in order;
+//      the chunk's worst-case workspace slot, is the chunk's stream in order.
+//      The raw sign|mantissa bytes of 16-bit formats go straight to their
+//      place in the blob;
 //   5. the offset index: one workgroup scans the record sizes and writes the
 //      index and the header;
-//   6. the descriptors (their raw-region offsets follow from the scan);
-//   7. packing: every chunk's record copied from its slot to its place, and
-//      the raw sign|mantissa bytes of 16-bit formats written in coding order.
+//   6. the descriptors (copied from the host's layout plan);
+//   7. packing: every chunk's record copied from its slot to its place.
 // The symbols' loads follow the decoder's layout: a lane-group of W symbols
 // is 16 bytes of the source, wherever the tiling puts it.
 #include <hip/hip_runtime.h>
@@ -32,6 +33,7 @@
 
 #include <algorithm>
 #include <mutex>
+#include <type_traits>
 #include <vector>
 
 #include "wc_internal.h"
@@ -40,12 +42,12 @@ namespace {
 
 constexpr int kWaves = 8;  // chunks (waves) per encoder / packer workgroup
 constexpr int kThreads = kWaves * 64;
-constexpr int kHistThreads = 256;
-constexpr int kHistReps = 16;                // LDS histogram copies (lane & 15)
-constexpr int kHistStride = 257;             // odd stride: copies of a bin in different banks
+constexpr int kHistThreads = 1024;           // 16 waves share one set of lane histograms
+constexpr int kHistLoads = 2;                // 16-byte loads in flight per lane
 constexpr uint64_t kHistSpan = 256u << 10;   // source bytes per histogram workgroup
 constexpr int kMaxLaunch = 16;               // tensors per launch
 constexpr int kScanThreads = 1024;
+constexpr int kScanPer = 32;  // record sizes per scan thread and round
 constexpr uint32_t kFarOffset = 0x7FFFFF00u;  // past any slot: buffer stores are dropped
 
 enum Kind : uint32_t { kSplit16 = 0, kByte = 1, kNibble = 2 };
@@ -95,6 +97,15 @@ __device__ __forceinline__ uint4 load16(const uint8_t* base, uint64_t bytes, uin
 
 __device__ __forceinline__ uint32_t dword(const uint4& v, uint32_t j) {
   return j == 0 ? v.x : (j == 1 ? v.y : (j == 2 ? v.z : v.w));
+}
+
+// m's lane bit ? a : b, as one v_cndmask.  Written out because the compiler
+// turns the equivalent conditional expression around a store into a branch,
+// whose skipped path leaves the number of stores in flight unknown to it.
+__device__ __forceinline__ uint32_t lane_select(uint64_t m, uint32_t a, uint32_t b) {
+  uint32_t r;
+  asm("v_cndmask_b32_e64 %0, %1, %2, %3" : "=v"(r) : "v"(b), "v"(a), "s"(m));
+  return r;
 }
 
 // Coded symbol k of a lane-group (k a compile-time constant after unrolling).
@@ -158,23 +169,28 @@ __global__ void zero_kernel(uint4* p, uint64_t n16) {
 
 // ---------------------------------------------------------------------------
 // 2. coded-symbol histograms.  Workgroup w of a tensor counts source bytes
-// [w * kHistSpan, +kHistSpan); symbol order does not matter here.
+// [w * kHistSpan, +kHistSpan); symbol order does not matter here.  Every wave
+// lane has its own histogram in LDS, laid out bin-major (bin * 64 + lane):
+// the lanes of one atomic add never share an address, each lane stays in its
+// own bank, and the waves of the workgroup share the 64 histograms.
 
 template <uint32_t K>
 __device__ void count_span(const EncTensor& T, uint64_t off0, uint64_t off1, uint32_t* h) {
   const uint8_t* src = reinterpret_cast<const uint8_t*>(T.src);
-  const uint32_t rep = (threadIdx.x & (kHistReps - 1)) * kHistStride;
+  const uint32_t lane = threadIdx.x & 63u;
   constexpr uint32_t W = K == kSplit16 ? 8u : (K == kByte ? 16u : 32u);
   constexpr uint64_t kStep = kHistThreads * 16ull;
-  // whole lane-groups, two loads in flight; then the tensor's last bytes
+  // whole lane-groups, kHistLoads loads in flight; then the tensor's last bytes
   const uint64_t full_end = off0 + (off1 - off0) / 16 * 16;
   uint64_t off = off0 + threadIdx.x * 16ull;
-  for (; off + kStep < full_end; off += 2 * kStep) {
-    const uint4 v0 = load16(src, full_end, off), v1 = load16(src, full_end, off + kStep);
+  for (; off + (kHistLoads - 1) * kStep < full_end; off += kHistLoads * kStep) {
+    uint4 v[kHistLoads];
 #pragma unroll
-    for (uint32_t k = 0; k < W; k++) atomicAdd(&h[rep + symbol<K>(v0, k)], 1u);
+    for (int u = 0; u < kHistLoads; u++) v[u] = load16(src, full_end, off + u * kStep);
 #pragma unroll
-    for (uint32_t k = 0; k < W; k++) atomicAdd(&h[rep + symbol<K>(v1, k)], 1u);
+    for (int u = 0; u < kHistLoads; u++)
+#pragma unroll
+      for (uint32_t k = 0; k < W; k++) atomicAdd(&h[symbol<K>(v[u], k) * 64u + lane], 1u);
   }
   for (; off < off1; off += kStep) {
     const uint4 v = load16(src, T.src_bytes, off);
@@ -183,13 +199,13 @@ __device__ void count_span(const EncTensor& T, uint64_t off0, uint64_t off1, uin
     const uint32_t nv = left >= 16 ? W : uint32_t(left * W / 16);
 #pragma unroll
     for (uint32_t k = 0; k < W; k++)
-      if (k < nv) atomicAdd(&h[rep + symbol<K>(v, k)], 1u);
+      if (k < nv) atomicAdd(&h[symbol<K>(v, k) * 64u + lane], 1u);
   }
 }
 
 __global__ __launch_bounds__(kHistThreads) void hist_kernel(EncArgs a) {
-  __shared__ uint32_t h[kHistReps * kHistStride];
-  for (uint32_t i = threadIdx.x; i < kHistReps * kHistStride; i += kHistThreads) h[i] = 0;
+  __shared__ uint32_t h[256 * 64];
+  for (uint32_t i = threadIdx.x; i < 256 * 64; i += kHistThreads) h[i] = 0;
   __syncthreads();
   const EncTensor& T = a.t[tensor_of(a, blockIdx.x)];
   const uint64_t off0 = uint64_t(blockIdx.x - T.wg0) * kHistSpan;
@@ -198,11 +214,15 @@ __global__ __launch_bounds__(kHistThreads) void hist_kernel(EncArgs a) {
   else if (T.kind == kByte) count_span<kByte>(T, off0, off1, h);
   else count_span<kNibble>(T, off0, off1, h);
   __syncthreads();
-  uint32_t c = 0;
-  for (int r = 0; r < kHistReps; r++) c += h[r * kHistStride + threadIdx.x];
-  unsigned long long* g =
-      reinterpret_cast<unsigned long long*>(a.ws + a.hist_off) + uint64_t(T.table) * 256u;
-  if (c) atomicAdd(g + threadIdx.x, (unsigned long long)c);
+  if (threadIdx.x < 256) {
+    // bin threadIdx.x over the 64 lanes, starting at a different lane in
+    // every thread so that the wave's reads fall in different banks
+    uint32_t c = 0;
+    for (uint32_t r = 0; r < 64; r++) c += h[threadIdx.x * 64u + ((r + threadIdx.x) & 63u)];
+    unsigned long long* g =
+        reinterpret_cast<unsigned long long*>(a.ws + a.hist_off) + uint64_t(T.table) * 256u;
+    if (c) atomicAdd(g + threadIdx.x, (unsigned long long)c);
+  }
 }
 
 // Whole 16-bit words of a 16-bit tensor, bins [part * 16384, +16384) counted
@@ -303,31 +323,45 @@ __global__ __launch_bounds__(256) void norm_kernel(NormArgs a) {
     d++;
     __syncthreads();
   }
-  // u16 table into the blob; cum and the reciprocal for the encoder
+  // u16 table into the blob; g = 2^12 - f, cum and 1/f for the encoder
   if (s < NT.alphabet) reinterpret_cast<uint16_t*>(a.blob + NT.freq_off)[s] = uint16_t(f);
   red[s] = f;
   __syncthreads();
   uint32_t cum = 0;
   for (uint32_t t = 0; t < s; t++) cum += red[t];
-  // ceil(2^64 / f) = floor((2^64 - 1) / f) + 1 for f >= 2.  For f == 1 the
-  // reciprocal 2^64 - 1 gives the quotient x - 1 instead of x, which leaves
-  // the new state 2^12 - 1 short; the encoder's cum for that symbol carries it.
-  const unsigned long long rc = f > 1 ? ~0ull / f + 1 : (f == 1 ? ~0ull : 0ull);
-  const uint32_t cum_enc = f == 1 ? cum + wc::kTableSize - 1 : cum;
+  // 1/f rounded up to a double: the correctly rounded quotient, raised by one
+  // unit in the last place when it is below 1/f (the sign of the exact
+  // fma(r, f, -1) says which)
+  double rcp = 0.0;
+  if (f) {
+    rcp = 1.0 / double(f);
+    if (fma(rcp, double(f), -1.0) < 0.0)
+      rcp = __longlong_as_double(__double_as_longlong(rcp) + 1);
+  }
+  const uint32_t g = f ? wc::kTableSize - f : 0u;
+  const unsigned long long rb = __double_as_longlong(rcp);
   uint4* tab = reinterpret_cast<uint4*>(a.ws + a.tab_off) + uint64_t(NT.table) * 256u;
-  tab[s] = make_uint4(f, cum_enc, uint32_t(rc), uint32_t(rc >> 32));
+  tab[s] = make_uint4(g, cum, uint32_t(rb), uint32_t(rb >> 32));
 }
 
 // ---------------------------------------------------------------------------
 // 4. chunk encoder.  Symbol i of a chunk is lane (i mod L*W) div W's symbol at
 // step (i div L*W)*W + i mod W.  Steps run from the last to the first; in a
 // step every active lane with x >= f * 2^20 emits its low 16 bits (x >>= 16)
-// and then x = floor(x / f) * 2^12 + x mod f + cum.  The quotient uses the
-// 64-bit reciprocal r = ceil(2^64 / f): floor(x * r / 2^64) = floor(x / f) for
-// x < 2^32 (the error x * (r - 2^64 / f) / 2^64 is below 1 / f), computed as
-// (x * r_hi + mulhi(x, r_lo)) >> 32.  q < 2^20 and f <= 2^12, so q * f is a
-// 24-bit multiply.  Every step is branch-free: a lane that emits nothing
-// stores its word at an offset past the slot, which the buffer range check drops.
+// and then x = floor(x / f) * 2^12 + x mod f + cum.  The step works from
+// Q = floor(x / f), computed as x * r in double precision with r = 1/f
+// rounded up, truncated: the product is never below x / f (so not below Q,
+// an integer), and it exceeds x / f by at most (x / f) * 2^-52 < 2^-20,
+// while x / f is at least 1/f >= 2^-12 below Q + 1, so it stays below Q + 1.
+//   * x >= f * 2^20 exactly when Q >= 2^20; the emitting lane then codes
+//     from x >> 16, whose quotient is Q >> 16;
+//   * with g = 2^12 - f and q the quotient of the value coded from, the new
+//     state is that value + cum + q * g (q < 2^20, g < 2^12: a 24-bit
+//     multiply-add).
+// A row in which every lane codes all W
+// symbols takes a step without any masks; the chunk's last row (row 0, whose
+// first symbols the start states carry) and a ragged final row mask inactive
+// lanes.
 
 template <uint32_t K>
 __device__ void encode_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, uint32_t lane,
@@ -341,11 +375,14 @@ __device__ void encode_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, u
   const uint32_t A = min(L, (n_c + W - 1) / W);
   const uint32_t LW = L * W;
   const uint32_t rows = (n_c + LW - 1) / LW;
+  // rows [1, full) have every lane coding all W symbols
+  const uint32_t full = L == 64 ? n_c / LW : 0u;
   const GroupAddr ga(T, c);
-  uint8_t* slot = reinterpret_cast<uint8_t*>(a.ws + T.slot_off) + uint64_t(c) * T.slot_bytes;
+  const uint32_t slot_bytes = T.slot_bytes;
+  uint8_t* slot = reinterpret_cast<uint8_t*>(a.ws + T.slot_off) + uint64_t(c) * slot_bytes;
   // the slot as a buffer: word k from its end sits at byte slot_bytes - 2k
   const __amdgpu_buffer_rsrc_t rs =
-      __builtin_amdgcn_make_buffer_rsrc(slot, (short)0, (int)T.slot_bytes, 0x00020000);
+      __builtin_amdgcn_make_buffer_rsrc(slot, (short)0, (int)slot_bytes, 0x00020000);
   // this lane's lane-group of row r (zeros past the chunk's symbols)
   auto load_row = [&](uint32_t r) {
     const uint32_t i0 = r * LW + lane * W;
@@ -377,49 +414,108 @@ __device__ void encode_chunk(const EncArgs& a, const EncTensor& T, uint32_t c, u
   const __amdgpu_buffer_rsrc_t rr = __builtin_amdgcn_make_buffer_rsrc(
       reinterpret_cast<uint8_t*>(a.blob) + a.raw_start + T.raw_rel + s0, (short)0,
       K == kSplit16 ? (int)n_c : 0, 0x00020000);
-  uint4 cur = rows > 1 ? load_row(rows - 1) : first;
-  for (uint32_t r = rows; r-- > 0;) {
-    // the next row's load is in flight while this row is coded
-    const uint4 nxt = r > 1 ? load_row(r - 1) : (r == 1 ? first : zero);
+  // One step: symbol k of every lane in `active` (all lanes when kAll).
+  auto step = [&](auto all, const uint4& v, uint32_t k, bool active) {
+    constexpr bool kAll = decltype(all)::value;
+    const uint4 e = tab[symbol<K>(v, k)];  // {g, cum, 1/f rounded up (double)}
+    const uint32_t Q = uint32_t(double(x) * __hiloint2double(int(e.w), int(e.z)));
+    bool emit = Q >= (1u << 20);
+    if constexpr (!kAll) emit = emit && active;
+    const uint64_t m = __ballot(emit);
+    const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+        uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
+    const uint32_t total = uint32_t(__popcll(m));
+    // pushed after the emitting lanes above this one (total - below - 1)
+    // Every lane stores (a lane that emits nothing past the slot, where the
+    // buffer range check drops it), so that each row issues a fixed number of
+    // stores and the wait for the next row's load counts exactly.
+    const uint32_t base = __builtin_amdgcn_readfirstlane(slot_bytes - 2u * (top + total));
+    __builtin_amdgcn_raw_buffer_store_b16(uint16_t(x), rs,
+                                          lane_select(m, base + 2u * below, kFarOffset), 0, 0);
+    top += total;
+    const uint32_t v2 = emit ? x >> 16 : x;
+    const uint32_t q = emit ? Q >> 16 : Q;
+    const uint32_t xn = __umul24(q, e.x) + v2 + e.y;
+    if constexpr (kAll) x = xn;
+    else x = active ? xn : x;
+  };
+  // A row in which every lane codes all W symbols (every row of a 64-lane
+  // chunk but row 0 and a ragged last row).
+  auto code_full = [&](uint32_t r, const uint4& cur) {
+    if constexpr (K == kSplit16) {
+      // raw byte of a word: bit 15 -> bit 7, bits 6..0 kept; the high and the
+      // low bytes of four words gathered, then merged bit by bit
+      typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+      const uint32_t h0 = __builtin_amdgcn_perm(cur.y, cur.x, 0x07050301u);
+      const uint32_t l0 = __builtin_amdgcn_perm(cur.y, cur.x, 0x06040200u);
+      const uint32_t h1 = __builtin_amdgcn_perm(cur.w, cur.z, 0x07050301u);
+      const uint32_t l1 = __builtin_amdgcn_perm(cur.w, cur.z, 0x06040200u);
+      const uint32_t m8 = 0x80808080u;
+      __builtin_amdgcn_raw_buffer_store_b64(
+          u32x2{(h0 & m8) | (l0 & ~m8), (h1 & m8) | (l1 & ~m8)}, rr, r * LW + lane * W, 0, 0);
+    }
+#pragma unroll
+    for (uint32_t kk = 0; kk < W; kk++) step(std::true_type{}, cur, W - 1 - kk, true);
+  };
+  // Any row: lanes past the chunk's symbols, and in row 0 the symbols the
+  // start states carry, are inactive.
+  auto code_any = [&](uint32_t r, const uint4& cur) {
     const uint32_t i0 = r * LW + lane * W;
     const uint32_t nv = lane < L && i0 < n_c ? min(W, n_c - i0) : 0u;
     if constexpr (K == kSplit16) {
-      // raw byte of a word: bit 15 -> bit 7, bits 6..0 kept
       uint32_t rb[2] = {0u, 0u};
 #pragma unroll
       for (uint32_t k = 0; k < 8; k++) {
         const uint32_t w = (dword(cur, k >> 1) >> (16 * (k & 1))) & 0xFFFFu;
         rb[k >> 2] |= (((w >> 8) & 0x80u) | (w & 0x7Fu)) << (8 * (k & 3));
       }
-      if (nv == 8) {
-        typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-        __builtin_amdgcn_raw_buffer_store_b64(u32x2{rb[0], rb[1]}, rr, i0, 0, 0);
-      } else {
-        for (uint32_t k = 0; k < nv; k++)
-          __builtin_amdgcn_raw_buffer_store_b8(uint8_t(rb[k >> 2] >> (8 * (k & 3))), rr, i0 + k, 0, 0);
-      }
+#pragma unroll
+      for (uint32_t k = 0; k < 8; k++)
+        __builtin_amdgcn_raw_buffer_store_b8(uint8_t(rb[k >> 2] >> (8 * (k & 3))), rr,
+                                             k < nv ? i0 + k : kFarOffset, 0, 0);
     }
 #pragma unroll
     for (uint32_t kk = 0; kk < W; kk++) {
       const uint32_t k = W - 1 - kk;
-      const bool active = k < nv && (r != 0 || k >= ck);
-      const uint4 e = tab[symbol<K>(cur, k)];  // {f, cum, r_lo, r_hi}
-      const bool emit = active && (x >> 20) >= e.x;
-      const uint64_t m = __ballot(emit);
-      const uint32_t below = __builtin_amdgcn_mbcnt_hi(
-          uint32_t(m >> 32), __builtin_amdgcn_mbcnt_lo(uint32_t(m), 0u));
-      const uint32_t total = uint32_t(__popcll(m));
-      // pushed after the emitting lanes above this one (total - below - 1)
-      const uint32_t off = emit ? T.slot_bytes - 2u * (top + total - below) : kFarOffset;
-      __builtin_amdgcn_raw_buffer_store_b16(uint16_t(x), rs, off, 0, 0);
-      top += total;
-      const uint32_t v2 = emit ? x >> 16 : x;
-      const uint32_t q = uint32_t((uint64_t(v2) * e.w + __umulhi(v2, e.z)) >> 32);
-      const uint32_t xn = (q << wc::kProbBits) + v2 - __umul24(q, e.x) + e.y;
-      x = active ? xn : x;
+      step(std::false_type{}, cur, k, k < nv && (r != 0 || k >= ck));
     }
+  };
+  // Rows are coded from the last to the first, in three runs: rows that are
+  // not full (from the top down to row 1), the full rows, row 0.  Each row's
+  // successor is loaded before the row is coded.  The empty statement after
+  // that load keeps the compiler from merging it with the load before the
+  // loop into one load at the top of the loop, which would wait for each
+  // row's data as it is needed; the explicit vmcnt(0) before the runs
+  // leaves, inside them, only the wait for the next row's load at the end of
+  // each row.  Every row issues a fixed number of stores, so that wait counts
+  // exactly.
+  auto next_row = [&](uint32_t r) { return r > 1 ? load_row(r - 1) : (r == 1 ? first : zero); };
+  // the same for a row below `full` (every lane-group inside the tensor): a
+  // plain load, with no branch for the tensor's end
+  auto next_full = [&](uint32_t r) {
+    if (r > 1) {
+      const v4u v = *(gu4*)(uint64_t)(src + ga.at((r - 1) * LW + lane * W));
+      return make_uint4(v.x, v.y, v.z, v.w);
+    }
+    return r == 1 ? first : zero;
+  };
+  uint4 cur = rows > 1 ? load_row(rows - 1) : first;
+  __builtin_amdgcn_s_waitcnt(0x0F70);
+  uint32_t r = rows;
+  const uint32_t lo = max(full, 1u);
+  for (; r > lo; r--) {
+    const uint4 nxt = next_row(r - 1);
+    asm volatile("" ::: "memory");
+    code_any(r - 1, cur);
     cur = nxt;
   }
+  for (; r > 1; r--) {
+    const uint4 nxt = next_full(r - 1);
+    asm volatile("" ::: "memory");
+    code_full(r - 1, cur);
+    cur = nxt;
+  }
+  if (r == 1) code_any(0, cur);
   if (K == kSplit16 && c + 1 == T.n_chunks) {
     // the raw region's zero padding to 16 bytes
     uint8_t* end = reinterpret_cast<uint8_t*>(a.blob) + a.raw_start + T.raw_rel;
@@ -469,12 +565,30 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(ScanArgs a) {
   const uint32_t* rsz = reinterpret_cast<const uint32_t*>(a.ws + a.rsz_off);
   uint32_t* index = reinterpret_cast<uint32_t*>(a.blob + a.index_off);
   const uint64_t rec16 = a.records_off / 16;
+  const uint64_t n = a.n_chunks;
   if (tid == 0) carry_s = 0;
   __syncthreads();
-  for (uint64_t base = 0; base < a.n_chunks; base += kScanThreads) {
-    const uint64_t g = base + tid;
-    const uint32_t v = g < a.n_chunks ? rsz[g] : 0u;
-    uint32_t incl = v;
+  // rounds of kScanThreads * kScanPer sizes; thread tid takes kScanPer
+  // consecutive ones, all loaded before any is added
+  constexpr uint64_t kRound = uint64_t(kScanThreads) * kScanPer;
+  for (uint64_t base = 0; base < n; base += kRound) {
+    const uint64_t g0 = base + uint64_t(tid) * kScanPer;
+    uint32_t v[kScanPer];
+    if (g0 + kScanPer <= n) {
+      const uint4* r4 = reinterpret_cast<const uint4*>(rsz + g0);  // 128-byte aligned
+#pragma unroll
+      for (int j = 0; j < kScanPer / 4; j++) {
+        const uint4 q = r4[j];
+        v[4 * j] = q.x, v[4 * j + 1] = q.y, v[4 * j + 2] = q.z, v[4 * j + 3] = q.w;
+      }
+    } else {
+#pragma unroll
+      for (int j = 0; j < kScanPer; j++) v[j] = g0 + j < n ? rsz[g0 + j] : 0u;
+    }
+    uint32_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < kScanPer; j++) sum += v[j];
+    uint32_t incl = sum;
 #pragma unroll
     for (int d = 1; d < 64; d <<= 1) {
       const uint32_t u = __shfl_up(incl, d, 64);
@@ -485,7 +599,12 @@ __global__ __launch_bounds__(kScanThreads) void scan_kernel(ScanArgs a) {
     uint32_t before = 0;
     for (uint32_t w = 0; w < wave; w++) before += wsum[w];
     const uint64_t carry = carry_s;
-    if (g < a.n_chunks) index[g] = uint32_t(rec16 + carry + before + incl - v);
+    uint64_t run = rec16 + carry + before + incl - sum;
+#pragma unroll
+    for (int j = 0; j < kScanPer; j++) {
+      if (g0 + j < n) index[g0 + j] = uint32_t(run);
+      run += v[j];
+    }
     __syncthreads();
     if (tid == kScanThreads - 1) carry_s = carry + before + incl;
     __syncthreads();
