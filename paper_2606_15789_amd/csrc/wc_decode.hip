@@ -1,6 +1,10 @@
 // wc_decode.hip -- wc_decode: one launch decodes every chunk of a blob's
 // tensors into the caller's buffers (Alg. 2; the decoder is in wc_decoder.h).
 
+#include <mutex>
+#include <utility>
+#include <vector>
+
 #include "wc_decoder.h"
 
 namespace {
@@ -47,6 +51,31 @@ __global__ __launch_bounds__(kThreads) void wc_decode_kernel(LaunchArgs a) {
     by_kind(std::integral_constant<int, 64>{});
 }
 
+// Waves of the general kernel and of the 16-bit wide kernel resident on the
+// current device at once, from the runtime's occupancy calculation, worked
+// out once per device ({0, 0} when unknown: the general kernel is used).
+struct Capacity {
+  uint64_t general, wide;
+};
+
+Capacity capacity() {
+  static std::mutex mu;
+  static std::vector<std::pair<int, Capacity>> known;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return Capacity{0, 0};
+  std::lock_guard<std::mutex> lock(mu);
+  for (const auto& k : known)
+    if (k.first == dev) return k.second;
+  Capacity c{0, 0};
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(
+          &per_cu, reinterpret_cast<const void*>(wc_decode_kernel), kThreads, 0) == hipSuccess)
+    c = Capacity{uint64_t(cus) * uint64_t(per_cu) * uint64_t(kWaves), wc::wide_resident_waves()};
+  known.push_back({dev, c});
+  return c;
+}
+
 // A tiled tensor whose widest output descriptor (two tiles of a 32-lane wave)
 // would not fit the 32-bit range the buffer descriptors address.
 bool tile_span_ok(const wc::TensorInfo& T) {
@@ -73,19 +102,42 @@ extern "C" wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* 
   fill_common(args, P, dev_blob, dev_err);
   uint32_t t = 0;
   while (t < n) {
-    uint32_t nt = 0, wgs = 0;
-    for (; t < n && nt < kMaxLaunchTensors; t++) {
+    // the tensors of one launch: the next kMaxLaunchTensors that have chunks
+    uint32_t end = t, nt = 0;
+    uint64_t chunks = 0;
+    bool wide_fits = true;
+    for (; end < n && nt < kMaxLaunchTensors; end++) {
+      const wc::TensorInfo& T = P.tensors[end];
+      if (T.n_chunks == 0) continue;
+      nt++;
+      chunks += T.n_chunks;
+      wide_fits = wide_fits && wc::has_raw(T.dtype) &&
+                  T.lanes == 64 && !T.tile_r;
+    }
+    if (nt == 0) break;
+    bool wide = false;
+    if (wide_fits) {
+      const Capacity cap = capacity();
+      wide = cap.general && cap.wide > cap.general && chunks > cap.general && chunks <= cap.wide;
+    }
+    const uint64_t waves = wide ? uint64_t(wc::kWideWaves) : uint64_t(kWaves);
+    uint32_t wgs = 0;
+    nt = 0;
+    for (; t < end; t++) {
       const wc::TensorInfo& T = P.tensors[t];
       if (T.n_chunks == 0) continue;
       fill_tensor(args.t[nt++], T, dev_dst[t], wgs);
-      const uint64_t per_group = uint64_t(kWaves) * (T.lanes == 32 ? 2u : 1u);
+      const uint64_t per_group = waves * (T.lanes == 32 ? 2u : 1u);
       wgs += (uint32_t)((T.n_chunks + per_group - 1) / per_group);
     }
-    if (nt == 0) break;
     args.n_tensors = nt;
-    hipLaunchKernelGGL(wc_decode_kernel, dim3(wgs), dim3(kThreads), 0,
-                       reinterpret_cast<hipStream_t>(stream), args);
-    if (hipGetLastError() != hipSuccess) return WC_EHIP;
+    if (wide) {
+      if (!wc::wide_launch(&args, sizeof args, wgs, stream)) return WC_EHIP;
+    } else {
+      hipLaunchKernelGGL(wc_decode_kernel, dim3(wgs), dim3(kThreads), 0,
+                         reinterpret_cast<hipStream_t>(stream), args);
+      if (hipGetLastError() != hipSuccess) return WC_EHIP;
+    }
   }
   return WC_OK;
 }

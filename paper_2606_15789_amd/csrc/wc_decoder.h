@@ -137,7 +137,9 @@ __device__ __forceinline__ void report(const LaunchArgs& a, uint32_t bits) {
   if (a.err && bits) atomicOr(reinterpret_cast<int32_t*>(a.err), (int32_t)bits);
 }
 
-// Decode table of one tensor: slot -> {f | sym << 24, slot - cum_sym}.
+// Decode table of one tensor: slot -> {f | sym << 24, slot - cum_sym}, built
+// by a workgroup of kT threads.
+template <int kT = kThreads>
 __device__ void build_table(const LaunchArgs& a, const DevTensor& T, uint2* tab, uint32_t* cum,
                             uint32_t tid) {
   const uint16_t* fr = reinterpret_cast<const uint16_t*>(a.blob + T.freq_off);
@@ -166,7 +168,7 @@ __device__ void build_table(const LaunchArgs& a, const DevTensor& T, uint2* tab,
     }
   }
   __syncthreads();
-  constexpr uint32_t kPer = wc::kTableSize / kThreads;
+  constexpr uint32_t kPer = wc::kTableSize / kT;
   const uint32_t j0 = tid * kPer;
   uint32_t lo = 0, hi = 256;  // largest s with cum[s] <= j0
   while (hi - lo > 1) {

@@ -18,6 +18,14 @@ constexpr uint32_t kStateLow = 1u << 16;  // lower end of the state interval
 constexpr uint32_t kHeaderBytes = 64;
 constexpr uint32_t kDescBytes = 96;
 constexpr uint32_t kMaxLanes = 64;
+constexpr int kWideWaves = 16;  // waves to a workgroup of the 16-bit decode kernel
+
+// The 16-wave decode kernel for bf16 / fp16 tensors in untiled 64-lane chunks
+// (wc_decode_wide.hip): the waves of it resident on the current device at
+// once (0 when unknown), and a launch of it with wc_decode's launch arguments
+// (`bytes` their size; false on a launch error).
+uint64_t wide_resident_waves();
+bool wide_launch(const void* launch_args, uint64_t bytes, uint32_t workgroups, void* stream);
 
 inline bool dtype_ok(uint32_t dt) { return dt >= WC_BF16 && dt <= WC_FP4_E2M1; }
 inline bool has_raw(uint32_t dt) { return dt == WC_BF16 || dt == WC_FP16; }

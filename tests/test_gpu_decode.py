@@ -174,6 +174,51 @@ def test_workloads_full_size(dev, cfg, lanes):
     torch.cuda.empty_cache()
 
 
+@pytest.mark.parametrize("rows,cols", [(6144, 32768), (6145, 32768), (7000, 32704),
+                                       (8192, 32768), (8193, 32768)])
+def test_launches_around_the_wide_kernels_window(dev, rows, cols):
+    """wc_decode runs a bf16 launch of untiled 64-lane chunks on its 16-wave
+    kernel when the chunks overflow the general kernel's resident waves (6144
+    on a 256-CU MI355X) but fit in the 16-wave kernel's (8192).  Chunk counts
+    on both edges of that window (the 7000-row case ends in a partial chunk)
+    decode bit-exact; sampled chunks equal the oracle's decode; a flipped word
+    in the wide launch is reported like in the general one."""
+    say("wide window", rows, cols)
+    (_, t, shape), = synth.layer_torch_device([("w", rows, cols)], 0.02, 40 + rows % 97)
+    blob, size = wc.encode_device([("bf16", t, shape)])
+    torch.cuda.synchronize()
+    raw = blob[:int(size.item())].cpu().numpy()
+    desc = wc.open_blob(raw)
+    rawb = raw.tobytes()
+    info = oracle.tensor_info(rawb)
+    say(f"  {info[0]['n_chunks']} chunks, {t.numel() / 1e9:.3f} GB")
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    out, = wc.decode_torch(desc, blob, err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    assert torch.equal(out, t)
+    got = out.cpu().numpy()
+    rng = np.random.default_rng(rows)
+    for c in _sample_chunks(info[0]["n_chunks"], 6, rng):
+        ref = oracle.decode_chunks(rawb, 0, c, c + 1)
+        lo, hi = c * 65536, min((c + 1) * 65536, info[0]["out_bytes"])
+        assert np.array_equal(got[lo:hi], ref[lo:hi]), c
+    del out
+    # a flipped word in the middle chunk's record
+    c = info[0]["n_chunks"] // 2
+    idx = struct.unpack_from("<Q", rawb, 32)[0]
+    off = struct.unpack_from("<I", rawb, idx + 4 * c)[0] * 16
+    nw, na = struct.unpack_from("<II", rawb, off)
+    wpos = off + 16 + ((4 * na + 15) // 16) * 16 + 2 * (nw // 2)
+    blob[wpos] ^= 0x40
+    err.zero_()
+    wc.decode_torch(desc, blob, err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) & 0x6
+    del blob, t
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("lanes", [64, 32])
 def test_device_side_corruption_flags(dev, lanes):
     """The kernel's own checks turn corrupted device bytes into error bits."""
