@@ -295,6 +295,20 @@ def decode_kernel_fingerprint():
     return next((v for k, v in prints.items() if "wc_decode_kernel" in k), None)
 
 
+def decode_kernel_for(dtypes, n_chunks: int, lanes: int, tiled: bool) -> str:
+    """The kernel wc_decode runs for one launch of these tensors: its 16-wave
+    kernel for bf16/fp16 tensors in untiled 64-lane chunks when the chunks
+    exceed the general kernel's resident waves (24 a compute unit: the LDS of
+    three 8-wave workgroups) but fit the 16-wave kernel's (32 a compute unit),
+    the general kernel otherwise.  The library takes the same decision from the
+    runtime's occupancy figures."""
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    if (all(d in ("bf16", "fp16") for d in dtypes) and lanes == 64 and not tiled
+            and 24 * cus < n_chunks <= 32 * cus):
+        return "wc_decode_wide_kernel"
+    return "wc_decode_kernel"
+
+
 def counted_traffic(workload: str, chunk_bytes: int, lanes: int, tiled: bool = False):
     """HBM bytes per launch from the counter runs, if they were taken on this
     workload and on the decode kernel as built now."""
@@ -674,7 +688,9 @@ def main() -> int:
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": counted_traffic(args.workload, args.chunk_bytes, args.lanes,
                                                 bool(args.tile) or args.codebook != "tensor"),
-                     "kernel": "wc_decode_kernel",
+                     "kernel": decode_kernel_for(
+                         [blobs[0].dtype(t) for t in range(blobs[0].n_tensors)],
+                         blobs[0].n_chunks, args.lanes, bool(args.tile)),
                      "median_launch_us": round(med_launch_s * 1e6, 2),
                      "mean_launch_us": round(mean_launch_s * 1e6, 2),
                      "launches_timed": G,
@@ -1629,7 +1645,9 @@ def sweep_bench(args, dev) -> int:
                        "copies_resident": n_res, "parallelism": "single-gpu"},
             "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                          "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
-                         "traffic": None, "kernel": "wc_decode_kernel",
+                         "traffic": None,
+                         "kernel": decode_kernel_for(["bf16"] * len(entries), blob.n_chunks,
+                                                     args.lanes, False),
                          "mean_launch_us": round(mean_s * 1e6, 2),
                          "algorithmic_bytes_per_launch": int(n + out_b)},
             "compression": {"ratio": round(out_b / n, 5), "bound_ratio": round(out_b / bound, 5),

@@ -166,7 +166,8 @@ typedef struct wc_blob {
 
 /* Device-side error bits ORed into *dev_err by wc_decode. */
 #define WC_DERR_INDEX 1u  /* chunk record offset or header inconsistent */
-#define WC_DERR_STATE 2u  /* a lane did not end at the initial state 2^16 */
+#define WC_DERR_STATE 2u  /* a lane did not end at its start state (2^16, or 2^S plus the
+                             symbols it carries) */
 #define WC_DERR_CURSOR 4u /* a chunk's word stream was not consumed exactly */
 #define WC_DERR_TABLE 8u  /* a frequency table does not sum to 2^12 */
 
@@ -207,6 +208,10 @@ wc_status wc_open(const void* data, uint64_t size, wc_blob** out);
  * Asynchronous with respect to the host; allocates nothing.  Reads only
  * inside [dev_blob, dev_blob + desc->size) and writes only the decoded byte
  * ranges.  A wave decodes one 64-lane chunk, or two adjacent 32-lane chunks.
+ * A launch of bf16/fp16 tensors in untiled 64-lane chunks whose chunks exceed
+ * the general kernel's resident waves on the current device but fit those of
+ * a 16-wave-workgroup kernel for that format runs on the latter (the device's
+ * occupancy figures are read once per device, with no allocation).
  * Returns WC_EINVAL (argument mismatch), WC_EUNSUPPORTED (a tensor coded with
  * a lane count other than 64 or 32), WC_EHIP (launch failure). */
 wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_dst, uint32_t n,

@@ -1,5 +1,7 @@
 // wc_decode.hip -- wc_decode: one launch decodes every chunk of a blob's
 // tensors into the caller's buffers (Alg. 2; the decoder is in wc_decoder.h).
+// The general kernel is here; bf16/fp16 launches that just overflow its
+// resident waves run on the 16-wave kernel of wc_decode_wide.hip.
 
 #include <mutex>
 #include <utility>
