@@ -302,6 +302,7 @@ def decode_kernel_for(dtypes, n_chunks: int, lanes: int, tiled: bool) -> str:
     three 8-wave workgroups) but fit the 16-wave kernel's (32 a compute unit),
     the general kernel otherwise.  The library takes the same decision from the
     runtime's occupancy figures."""
+    import torch
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     if (all(d in ("bf16", "fp16") for d in dtypes) and lanes == 64 and not tiled
             and 24 * cus < n_chunks <= 32 * cus):
