@@ -26,6 +26,13 @@
  * passed as plain pointers (`void*`), so any allocator (torch, hipMalloc)
  * can own them.
  *
+ * Library state: per device, the address of wc_analyze_device_static's
+ * scratch array and the decode kernels' resident-wave counts (wc_decode's
+ * choice of kernel), each worked out once, under a lock, on the first call
+ * on that device.  Nothing else persists between calls; calls on different
+ * streams or devices may run concurrently, except wc_analyze_device_static,
+ * whose calls share its scratch and are serialised by a process-wide lock.
+ *
  * Blob format version 5 (little-endian; every offset absolute from the blob
  * start): header 64 B, then one 96-B descriptor per tensor (type, chunk size,
  * sizes, lanes, table and raw offsets, shape and tile), then the u16 frequency
