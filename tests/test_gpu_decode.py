@@ -174,18 +174,20 @@ def test_workloads_full_size(dev, cfg, lanes):
     torch.cuda.empty_cache()
 
 
-@pytest.mark.parametrize("rows,cols", [(6144, 32768), (6145, 32768), (7000, 32704),
-                                       (8192, 32768), (8193, 32768)])
-def test_launches_around_the_wide_kernels_window(dev, rows, cols):
+@pytest.mark.parametrize("rows,cols,dtype", [(6144, 32768, "bf16"), (6145, 32768, "bf16"),
+                                             (7000, 32704, "bf16"), (7000, 32704, "fp16"),
+                                             (8192, 32768, "bf16"), (8193, 32768, "bf16")])
+def test_launches_around_the_wide_kernels_window(dev, rows, cols, dtype):
     """wc_decode runs a bf16 launch of untiled 64-lane chunks on its 16-wave
     kernel when the chunks overflow the general kernel's resident waves (6144
     on a 256-CU MI355X) but fit in the 16-wave kernel's (8192).  Chunk counts
     on both edges of that window (the 7000-row case ends in a partial chunk)
     decode bit-exact; sampled chunks equal the oracle's decode; a flipped word
-    in the wide launch is reported like in the general one."""
-    say("wide window", rows, cols)
+    in the wide launch is reported like in the general one.  The fp16 case
+    codes the same 16-bit words as fp16 (the split is the same bit fields)."""
+    say("wide window", rows, cols, dtype)
     (_, t, shape), = synth.layer_torch_device([("w", rows, cols)], 0.02, 40 + rows % 97)
-    blob, size = wc.encode_device([("bf16", t, shape)])
+    blob, size = wc.encode_device([(dtype, t, shape)])
     torch.cuda.synchronize()
     raw = blob[:int(size.item())].cpu().numpy()
     desc = wc.open_blob(raw)
