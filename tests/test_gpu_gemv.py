@@ -436,6 +436,32 @@ def test_int8_gemm_is_exact(dev, shape, tile, m):
     assert np.array_equal(_run_gemm_i8(blob, dev, 0, x), oracle.gemm_i8(w, x))
 
 
+@pytest.mark.parametrize("tiles,m", [(6144, 16), (6145, 16), (7000, 1), (8192, 16), (8193, 16),
+                                     (7000, 17)])
+def test_int8_gemm_around_the_wide_kernels_window(dev, tiles, m):
+    """wc_gemm_i8 runs on its 16-wave kernel when the launch has one block of x
+    rows (m <= 16) and its tiles overflow the 8-wave kernel's resident waves
+    (6144 on a 256-CU MI355X) but fit the 16-wave kernel's (8192).  Tile counts
+    on both edges of that window, and m = 17 (outside it), give y equal to the
+    oracle's int8 product on sampled rows."""
+    say("int8 wide window", tiles, m)
+    rows, cols = 16 * tiles, 512
+    codes = synth.int8_rows_torch_device(rows, cols, 60 + tiles % 89)
+    blob = wc.encode([("u8", codes.cpu().numpy(), (rows, cols))], tile=(16, 512), tile_order=1)
+    d = wc.to_device(blob, dev)
+    x = np.random.default_rng(tiles).integers(-127, 128, (m, cols)).astype(np.int8)
+    err = torch.zeros(1, dtype=torch.int32, device=dev)
+    y, = wc.gemm_i8_torch(blob, d, [0], [torch.from_numpy(x).to(dev)], err=err)
+    torch.cuda.synchronize()
+    assert int(err.item()) == 0
+    w = codes.cpu().numpy().view(np.int8).reshape(rows, cols)
+    pick = np.random.default_rng(rows).choice(rows, 64, replace=False)
+    pick = np.concatenate([pick, [0, rows - 1]])
+    want = oracle.gemm_i8(np.ascontiguousarray(w[pick]), x)
+    assert np.array_equal(y.cpu().numpy().astype(np.int64)[:, pick], want)
+    del codes, d
+
+
 def test_int8_gemm_quantised_layer(dev):
     """The int8 projections of the scaled 8B W8 workload (Student-t weights,
     per-row absmax scales) in 16 x 512 tiles, one launch, 16 rows of x."""
