@@ -310,6 +310,22 @@ def decode_kernel_for(dtypes, n_chunks: int, lanes: int, tiled: bool) -> str:
     return "wc_decode_kernel"
 
 
+def gemv_kernel_for(weights: str, n_tiles: int, m: int) -> str:
+    """The kernel of a fused-GEMM launch of 16-row int8 or fp8 tiles (weights:
+    "int8", "e4m3" or "e5m2"): its 16-wave kernel when there is one block of x
+    rows (m <= 16) and the tiles exceed the 8-wave kernel's resident waves (24 a
+    compute unit) but fit the 16-wave kernel's (32 a compute unit), the 8-wave
+    kernel otherwise.  The library takes the same decision from the runtime's
+    occupancy figures."""
+    import torch
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    wide = m <= 16 and 24 * cus < n_tiles <= 32 * cus
+    if weights == "e5m2":
+        return "wc_gemv_wide_e5m2_kernel" if wide else "wc_gemv_e5m2_kernel"
+    what = "int8" if weights == "int8" else "fp8 e4m3"
+    return f"wc_gemv_wide_kernel ({what})" if wide else f"wc_gemv_kernel ({what})"
+
+
 def counted_traffic(workload: str, chunk_bytes: int, lanes: int, tiled: bool = False):
     """HBM bytes per launch from the counter runs, if they were taken on this
     workload and on the decode kernel as built now."""
@@ -979,7 +995,8 @@ def gemm_i8_bench(args, dev) -> int:
                    "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
-                     "kernel": "wc_gemv_kernel (int8)", "mean_step_us": round(s_fused * 1e6, 2),
+                     "kernel": gemv_kernel_for("int8", blob.n_chunks, M),
+                     "mean_step_us": round(s_fused * 1e6, 2),
                      "algorithmic_bytes_per_step": int(alg)},
         "unfused": {"value": round(wbytes / s_unfused / 1e9, 2), "unit": "GB/s",
                     "ms_per_step": round(s_unfused * 1e3, 4),
@@ -1101,7 +1118,8 @@ def gemv_fp8_bench(args, dev) -> int:
                    "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
-                     "kernel": "wc_gemv_kernel (fp8)", "mean_step_us": round(s_fused * 1e6, 2),
+                     "kernel": gemv_kernel_for(fmt, blob.n_chunks, M),
+                     "mean_step_us": round(s_fused * 1e6, 2),
                      "algorithmic_bytes_per_step": int(alg)},
         "unfused": {"value": round(wbytes / s_unfused / 1e9, 2), "unit": "GB/s",
                     "ms_per_step": round(s_unfused * 1e3, 4),

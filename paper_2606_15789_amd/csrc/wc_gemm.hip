@@ -283,34 +283,37 @@ wc_status check_jobs(const wc_blob* desc, const void* dev_blob, uint32_t n,
 // products up to kDotRows rows of x, MFMA above, or the shared GEMM; bf16 on
 // 32 or 16 rows: MFMA; fp8 e4m3, then e5m2, on 16 rows: converted to bf16,
 // MFMA).  xs: the x (or, for the shared GEMM, packed x) of each job.
-// Resident waves of the 8-wave fused-GEMM kernel for 16-row int8 (fp8 =
-// false) or fp8 e4m3 tiles with one block of x rows, and of its 16-wave
-// counterpart in wc_gemm_wide.hip, worked out once per device ({0, 0} when
-// unknown).  A launch whose tiles overflow the first but fit the second runs
-// on the 16-wave kernel, in one round.
-bool gemv_wide(bool fp8, uint64_t tiles) {
+// Resident waves of the 8-wave fused-GEMM kernel for 16-row tiles with one
+// block of x rows (kind: 0 int8, 1 fp8 e4m3, 2 fp8 e5m2 weights), and of its
+// 16-wave counterpart in wc_gemm_wide.hip, worked out once per device ({0, 0}
+// when unknown).  A launch whose tiles overflow the first but fit the second
+// runs on the 16-wave kernel, in one round.
+bool gemv_wide(int kind, uint64_t tiles) {
   struct Cap {
     uint64_t general, wide;
   };
+  if (kind < 0 || kind > 2) return false;
   static std::mutex mu;
-  static std::vector<std::pair<int, Cap>> known[2];
+  static std::vector<std::pair<int, Cap>> known[3];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return false;
   Cap c{0, 0};
   {
     std::lock_guard<std::mutex> lock(mu);
     bool found = false;
-    for (const auto& k : known[fp8])
+    for (const auto& k : known[kind])
       if (k.first == dev) c = k.second, found = true;
     if (!found) {
       int cus = 0, per_cu = 0;
-      const void* k8 = fp8 ? reinterpret_cast<const void*>(wc_gemv_kernel<0, 1, 16, 4, true>)
-                          : reinterpret_cast<const void*>(wc_gemv_kernel<0, 1, 16, 4, false>);
+      const void* k8 =
+          kind == 2   ? reinterpret_cast<const void*>(wc_gemv_e5m2_kernel<1>)
+          : kind == 1 ? reinterpret_cast<const void*>(wc_gemv_kernel<0, 1, 16, 4, true>)
+                      : reinterpret_cast<const void*>(wc_gemv_kernel<0, 1, 16, 4, false>);
       if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
           hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k8, kThreads, 0) == hipSuccess)
         c = Cap{uint64_t(cus) * uint64_t(per_cu) * uint64_t(kWaves),
-                wc::gemv_wide_resident_waves(fp8)};
-      known[fp8].push_back({dev, c});
+                wc::gemv_wide_resident_waves(kind)};
+      known[kind].push_back({dev, c});
     }
   }
   return c.general && c.wide > c.general && tiles > c.general && tiles <= c.wide;
@@ -327,15 +330,15 @@ wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
     const uint32_t dtype = f8 == 0 ? WC_BF16 : (f8 == 1 ? WC_FP8_E4M3 : WC_FP8_E5M2);
     LaunchArgs args{};
     fill_common(args, P, dev_blob, dev_err);
-    // fp8 e4m3 with one block of x rows: the 16-wave kernel when its tiles fit it
+    // fp8 with one block of x rows: the 16-wave kernel when its tiles fit it
     bool wide = false;
-    if (f8 == 1 && m <= 16) {
+    if (f8 != 0 && m <= 16) {
       uint64_t tiles = 0;
       for (uint32_t i = 0; i < n; i++) {
         const wc::TensorInfo& T = P.tensors[tensors[i]];
         if (T.tile_r == rows && T.dtype == dtype) tiles += T.n_chunks;
       }
-      wide = tiles && gemv_wide(true, tiles);
+      wide = tiles && gemv_wide(int(f8), tiles);
     }
     const uint64_t per_wg = wide ? uint64_t(wc::kWideWaves) : uint64_t(kWaves);
     uint32_t wgs = 0, nt = 0;
@@ -358,7 +361,7 @@ wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
     args.n_tensors = nt;
     args.m = m;
     if (wide) {
-      if (!wc::gemv_wide_launch(true, &args, sizeof args, wgs, st)) return WC_EHIP;
+      if (!wc::gemv_wide_launch(int(f8), &args, sizeof args, wgs, st)) return WC_EHIP;
       continue;
     }
     const dim3 grid(wgs), block(kThreads);
@@ -464,7 +467,7 @@ extern "C" wc_status wc_gemm_i8(const wc_blob* desc, const void* dev_blob, uint3
     tiles += T.n_chunks;
   }
   // one block of x rows: the 16-wave kernel when the tiles fit it
-  const bool wide = m <= 16 && gemv_wide(false, tiles);
+  const bool wide = m <= 16 && gemv_wide(0, tiles);
   const uint64_t per_wg = wide ? uint64_t(wc::kWideWaves) : uint64_t(kWaves);
   uint32_t wgs = 0;
   for (uint32_t i = 0; i < n; i++) {
@@ -476,7 +479,7 @@ extern "C" wc_status wc_gemm_i8(const wc_blob* desc, const void* dev_blob, uint3
   args.n_tensors = n;
   args.m = m;
   const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (wide) return wc::gemv_wide_launch(false, &args, sizeof args, wgs, st) ? WC_OK : WC_EHIP;
+  if (wide) return wc::gemv_wide_launch(0, &args, sizeof args, wgs, st) ? WC_OK : WC_EHIP;
   const dim3 grid(wgs), block(kThreads);
   switch ((m + 15) / 16) {
     case 1: hipLaunchKernelGGL((wc_gemv_kernel<0, 1, 16, 4>), grid, block, 0, st, args); break;

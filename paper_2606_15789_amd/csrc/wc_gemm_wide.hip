@@ -1,6 +1,7 @@
 // wc_gemm_wide.hip -- 16-wave-workgroup instances of the fused decode-GEMM
 // (Alg. 1 / 3; the decoder is in wc_decoder.h) for int8 weights (wc_gemm_i8)
-// and fp8 e4m3 weights (wc_gemv) on 16-row tiles with up to 16 rows of x.  One
+// and fp8 e4m3 and e5m2 weights (wc_gemv) on 16-row tiles with up to 16 rows
+// of x.  One
 // decode table serves 16 waves, so a compute unit holds 32 of these waves
 // against 24 of the 8-wave kernels in wc_gemm.hip; the launches of those
 // entry points whose tiles overflow the 8-wave kernel's resident waves but
@@ -35,37 +36,62 @@ __global__ __launch_bounds__(wc::kWideWaves * 64) void wc_gemv_wide_kernel(Launc
                                                              pre);
 }
 
-const void* wide_kernel(bool fp8) {
-  return fp8 ? reinterpret_cast<const void*>(wc_gemv_wide_kernel<true>)
-             : reinterpret_cast<const void*>(wc_gemv_wide_kernel<false>);
+// e5m2 weights: the exponent bits are coded and the rest travel raw, as for
+// bf16 (the decoder's fp8 mode 2).
+__global__ __launch_bounds__(wc::kWideWaves * 64) void wc_gemv_wide_e5m2_kernel(LaunchArgs a) {
+  __shared__ uint2 tab[wc::kTableSize];
+  __shared__ uint32_t cum[260];
+  __shared__ uint32_t ring[wc::kWideWaves][wc_ring_words() / 2];
+  const uint32_t wg = blockIdx.x;
+  uint32_t ti = 0;
+  for (uint32_t k = 1; k < a.n_tensors; k++)
+    if (wg >= a.t[k].wg0) ti = k;
+  const DevTensor& T = a.t[ti];
+  const uint32_t tid = threadIdx.x;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t lane = __lane_id();
+  const uint32_t chunk = (wg - T.wg0) * wc::kWideWaves + wave;
+  const IndexPre pre = load_index(a, T, chunk, 1u);
+  build_table<wc::kWideWaves * 64>(a, T, tab, cum, tid);
+  __syncthreads();
+  if (chunk >= T.n_chunks) return;
+  decode_chunks<4, 64, true, 0, 1, 16, false, 2>(a, T, chunk, lane, tab, ring[wave], pre);
+}
+
+// kind: 0 int8, 1 fp8 e4m3, 2 fp8 e5m2
+const void* wide_kernel(int kind) {
+  if (kind == 2) return reinterpret_cast<const void*>(wc_gemv_wide_e5m2_kernel);
+  return kind == 1 ? reinterpret_cast<const void*>(wc_gemv_wide_kernel<true>)
+                   : reinterpret_cast<const void*>(wc_gemv_wide_kernel<false>);
 }
 
 }  // namespace
 
 namespace wc {
 
-uint64_t gemv_wide_resident_waves(bool fp8) {
+uint64_t gemv_wide_resident_waves(int kind) {
   int dev = 0, cus = 0, per_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess ||
+  if (kind < 0 || kind > 2 || hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wide_kernel(fp8), kWideWaves * 64,
+      hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wide_kernel(kind), kWideWaves * 64,
                                                    0) != hipSuccess)
     return 0;
   return uint64_t(cus) * uint64_t(per_cu) * uint64_t(kWideWaves);
 }
 
-bool gemv_wide_launch(bool fp8, const void* launch_args, uint64_t bytes, uint32_t workgroups,
+bool gemv_wide_launch(int kind, const void* launch_args, uint64_t bytes, uint32_t workgroups,
                       void* stream) {
-  if (bytes != sizeof(LaunchArgs)) return false;
+  if (bytes != sizeof(LaunchArgs) || kind < 0 || kind > 2) return false;
   LaunchArgs args;
   memcpy(&args, launch_args, sizeof args);
   const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  if (fp8)
-    hipLaunchKernelGGL((wc_gemv_wide_kernel<true>), dim3(workgroups), dim3(kWideWaves * 64), 0,
-                       st, args);
+  const dim3 grid(workgroups), block(kWideWaves * 64);
+  if (kind == 2)
+    hipLaunchKernelGGL(wc_gemv_wide_e5m2_kernel, grid, block, 0, st, args);
+  else if (kind == 1)
+    hipLaunchKernelGGL((wc_gemv_wide_kernel<true>), grid, block, 0, st, args);
   else
-    hipLaunchKernelGGL((wc_gemv_wide_kernel<false>), dim3(workgroups), dim3(kWideWaves * 64), 0,
-                       st, args);
+    hipLaunchKernelGGL((wc_gemv_wide_kernel<false>), grid, block, 0, st, args);
   return hipGetLastError() == hipSuccess;
 }
 

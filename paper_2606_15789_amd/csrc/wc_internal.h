@@ -26,10 +26,11 @@ constexpr int kWideWaves = 16;  // waves to a workgroup of the 16-bit decode ker
 // (`bytes` their size; false on a launch error).
 uint64_t wide_resident_waves();
 bool wide_launch(const void* launch_args, uint64_t bytes, uint32_t workgroups, void* stream);
-// The same for the fused decode-GEMM on 16-row int8 (fp8 = false) or fp8
-// e4m3 (fp8 = true) tiles with up to 16 rows of x (wc_gemm_wide.hip).
-uint64_t gemv_wide_resident_waves(bool fp8);
-bool gemv_wide_launch(bool fp8, const void* launch_args, uint64_t bytes, uint32_t workgroups,
+// The same for the fused decode-GEMM on 16-row tiles with up to 16 rows of x
+// (wc_gemm_wide.hip); kind: 0 int8, 1 fp8 e4m3, 2 fp8 e5m2 weights (0
+// resident waves, or false, for any other kind).
+uint64_t gemv_wide_resident_waves(int kind);
+bool gemv_wide_launch(int kind, const void* launch_args, uint64_t bytes, uint32_t workgroups,
                       void* stream);
 
 inline bool dtype_ok(uint32_t dt) { return dt >= WC_BF16 && dt <= WC_FP4_E2M1; }

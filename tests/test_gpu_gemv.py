@@ -640,6 +640,27 @@ def test_fp8_formats_in_one_call(dev):
 
 
 @pytest.mark.parametrize("fmt", FP8)
+@pytest.mark.parametrize("tiles,m", [(6144, 16), (6145, 1), (8192, 16), (8193, 16), (7000, 17)])
+def test_fp8_gemv_around_the_wide_kernels_window(dev, fmt, tiles, m):
+    """wc_gemv runs fp8 weights on a 16-wave kernel when the launch has one
+    block of x rows (m <= 16) and its 16-row tiles overflow the 8-wave
+    kernel's resident waves (6144 on a 256-CU MI355X) but fit the 16-wave
+    kernel's (8192).  Per-row scaled fp8 codes of Normal(0, 1) draws, tile
+    counts on both edges of that window and m = 17 (outside it): sampled rows
+    of y within the fp32 summation bound of the oracle's product."""
+    say("fp8 wide window", fmt, tiles, m)
+    rows, cols = 16 * tiles, 512
+    rng = np.random.default_rng(tiles + (3 if fmt == "e5m2" else 0))
+    w, _ = synth.quant_fp8_rows(rng.standard_normal((rows, cols), dtype=np.float32), fmt)
+    w[_fp8_special(w, fmt)] &= 0xFB
+    blob = wc.encode([("fp8_" + fmt, w, w.shape)], tile=(16, 512), tile_order=1)
+    x = _bf16(rng.normal(0, 1.0, (m, cols)))
+    y = _run_gemv(blob, dev, 0, x)
+    pick = np.concatenate([rng.choice(rows, 64, replace=False), [0, rows - 1]])
+    _check_fp8(y[:, pick], np.ascontiguousarray(w[pick]), x, fmt)
+
+
+@pytest.mark.parametrize("fmt", FP8)
 def test_fp8_gemv_limits(dev, fmt):
     rng = np.random.default_rng(54)
     w = _fp8_codes(rng, (64, 512), fmt)
