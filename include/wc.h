@@ -101,7 +101,10 @@ typedef struct {
 } wc_tensor;
 
 /* Encoder parameters.  chunk_bytes: decoded bytes per chunk, a multiple of
- * 256 in [256, 1 MiB] (16, 32 or 64 KiB in practice).  lanes: interleaved
+ * 256 in [256, 1 MiB] (16, 32 or 64 KiB in practice; each chunk is a serial
+ * chain per lane, so a launch with too few chunks to fill the device is bound
+ * by the chain length: smaller chunks decode such a launch faster, at the
+ * cost of more lane states in the blob).  lanes: interleaved
  * rANS lanes per chunk, 1..64 (the GPU decoder takes 64 or 32).  prob_bits:
  * must be 12 (Sec. VI-F, b = 12).  n_threads: host encoder threads, 0 = all
  * cores.
