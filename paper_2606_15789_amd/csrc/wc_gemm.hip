@@ -279,10 +279,6 @@ wc_status check_jobs(const wc_blob* desc, const void* dev_blob, uint32_t n,
   return WC_OK;
 }
 
-// One launch per tile height and weight type (bf16 on 64 rows: VALU dot
-// products up to kDotRows rows of x, MFMA above, or the shared GEMM; bf16 on
-// 32 or 16 rows: MFMA; fp8 e4m3, then e5m2, on 16 rows: converted to bf16,
-// MFMA).  xs: the x (or, for the shared GEMM, packed x) of each job.
 // Resident waves of the 8-wave fused-GEMM kernel for 16-row tiles with one
 // block of x rows (kind: 0 int8, 1 fp8 e4m3, 2 fp8 e5m2 weights), and of its
 // 16-wave counterpart in wc_gemm_wide.hip, worked out once per device ({0, 0}
@@ -319,6 +315,11 @@ bool gemv_wide(int kind, uint64_t tiles) {
   return c.general && c.wide > c.general && tiles > c.general && tiles <= c.wide;
 }
 
+// One launch per tile height and weight type (bf16 on 64 rows: VALU dot
+// products up to kDotRows rows of x, MFMA above, or the shared GEMM; bf16 on
+// 32 or 16 rows: MFMA; fp8 e4m3, then e5m2, on 16 rows: converted to bf16,
+// MFMA; fp8 launches with one block of x rows may take the 16-wave kernel,
+// see gemv_wide).  xs: the x (or, for the shared GEMM, packed x) of each job.
 wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
                       const uint32_t* tensors, const uint64_t* xs, uint32_t m,
                       float* const* dev_y, bool share, hipStream_t st, int32_t* dev_err) {
