@@ -311,19 +311,26 @@ def decode_kernel_for(dtypes, n_chunks: int, lanes: int, tiled: bool) -> str:
 
 
 def gemv_kernel_for(weights: str, n_tiles: int, m: int) -> str:
-    """The kernel of a fused-GEMM launch of 16-row int8 or fp8 tiles (weights:
-    "int8", "e4m3" or "e5m2"): its 16-wave kernel when there is one block of x
-    rows (m <= 16) and the tiles exceed the 8-wave kernel's resident waves (24 a
-    compute unit) but fit the 16-wave kernel's (32 a compute unit), the 8-wave
-    kernel otherwise.  The library takes the same decision from the runtime's
-    occupancy figures."""
+    """The kernel of a fused-GEMM launch of 16-row tiles (weights: "int8",
+    "e4m3", "e5m2", or "mxfp4" / "int4" with "-bytes" when the 4-bit codes are
+    coded as bytes).  int8, fp8 and byte-coded 4-bit launches take a 16-wave
+    kernel when they have up to 16 rows of x (8 for the 4-bit codes) and their
+    tiles exceed the 8-wave kernel's resident waves (24 a compute unit) but fit
+    the 16-wave kernel's (32 a compute unit).  The library takes the same
+    decision from the runtime's occupancy figures."""
     import torch
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    wide = m <= 16 and 24 * cus < n_tiles <= 32 * cus
-    if weights == "e5m2":
-        return "wc_gemv_wide_e5m2_kernel" if wide else "wc_gemv_e5m2_kernel"
-    what = "int8" if weights == "int8" else "fp8 e4m3"
-    return f"wc_gemv_wide_kernel ({what})" if wide else f"wc_gemv_kernel ({what})"
+    wide_rows = {"int8": 16, "e4m3": 16, "e5m2": 16, "mxfp4-bytes": 8, "int4-bytes": 8}
+    wide = m <= wide_rows.get(weights, 0) and 24 * cus < n_tiles <= 32 * cus
+    general = {"int8": "wc_gemv_kernel (int8)", "e4m3": "wc_gemv_kernel (fp8 e4m3)",
+               "e5m2": "wc_gemv_e5m2_kernel", "mxfp4": "wc_gemv_mx_kernel",
+               "mxfp4-bytes": "wc_gemv_mxb_kernel", "int4": "wc_gemv_w4n_kernel",
+               "int4-bytes": "wc_gemv_w4_kernel"}[weights]
+    if not wide:
+        return general
+    return {"int8": "wc_gemv_wide_kernel (int8)", "e4m3": "wc_gemv_wide_kernel (fp8 e4m3)",
+            "e5m2": "wc_gemv_wide_e5m2_kernel", "mxfp4-bytes": "wc_gemv_wide_q4_kernel (MXFP4)",
+            "int4-bytes": "wc_gemv_wide_q4_kernel (int4)"}[weights]
 
 
 def counted_traffic(workload: str, chunk_bytes: int, lanes: int, tiled: bool = False):
@@ -1265,7 +1272,9 @@ def gemv_mx_bench(args, dev) -> int:
                    "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
-                     "kernel": "wc_gemv_mx_kernel", "mean_step_us": round(s_fused * 1e6, 2),
+                     "kernel": gemv_kernel_for("mxfp4-bytes" if args.mx_bytes else "mxfp4",
+                                               blob.n_chunks, M),
+                     "mean_step_us": round(s_fused * 1e6, 2),
                      "algorithmic_bytes_per_step": int(alg)},
         "unfused": {"value": round(wbytes / s_unfused / 1e9, 2), "unit": "GB/s",
                     "ms_per_step": round(s_unfused * 1e3, 4),
@@ -1444,7 +1453,9 @@ def gemv_w4_bench(args, dev) -> int:
                    "parallelism": "single-gpu"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
-                     "kernel": "wc_gemv_w4_kernel", "mean_step_us": round(s_fused * 1e6, 2),
+                     "kernel": gemv_kernel_for("int4" if args.w4_nibbles else "int4-bytes",
+                                               blob.n_chunks, M),
+                     "mean_step_us": round(s_fused * 1e6, 2),
                      "algorithmic_bytes_per_step": int(alg)},
         "unfused": {"value": round(wbytes / s_unfused / 1e9, 2), "unit": "GB/s",
                     "ms_per_step": round(s_unfused * 1e3, 4),

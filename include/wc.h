@@ -286,6 +286,10 @@ wc_status wc_gemv(const wc_blob* desc, const void* dev_blob, uint32_t n, const u
  *   dev_y      host array of n device pointers to float y, m x N row-major;
  *              the products are added with fp32 atomics, as in wc_gemv;
  *   stream, dev_err as for wc_decode.
+ * Byte-coded jobs with m <= 8 whose tiles exceed the 8-wave kernel's resident
+ * waves on the current device but fit those of a 16-wave-workgroup kernel run
+ * on the latter, as in wc_decode; that kernel keeps one or two values per lane
+ * in scratch (at most 12 bytes), which the HIP runtime provides.
  * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument) or
  * WC_EUNSUPPORTED (a tensor the path does not take). */
 wc_status wc_gemv_mx(const wc_blob* desc, const void* dev_blob, uint32_t n, const uint32_t* tensors,
@@ -318,6 +322,10 @@ wc_status wc_gemv_mx(const wc_blob* desc, const void* dev_blob, uint32_t n, cons
  *   dev_y      host array of n device pointers to float y, m x N row-major;
  *              the products are added with fp32 atomics, as in wc_gemv;
  *   stream, dev_err as for wc_decode.
+ * Byte-coded jobs with m <= 8 whose tiles exceed the 8-wave kernel's resident
+ * waves on the current device but fit those of a 16-wave-workgroup kernel run
+ * on the latter, as in wc_decode; that kernel keeps one or two values per lane
+ * in scratch (at most 12 bytes), which the HIP runtime provides.
  * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument) or
  * WC_EUNSUPPORTED (a tensor the path does not take). */
 wc_status wc_gemv_w4(const wc_blob* desc, const void* dev_blob, uint32_t n, const uint32_t* tensors,

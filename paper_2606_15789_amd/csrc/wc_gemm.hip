@@ -280,7 +280,8 @@ wc_status check_jobs(const wc_blob* desc, const void* dev_blob, uint32_t n,
 }
 
 // Resident waves of the 8-wave fused-GEMM kernel for 16-row tiles with one
-// block of x rows (kind: 0 int8, 1 fp8 e4m3, 2 fp8 e5m2 weights), and of its
+// block of x rows (kind: 0 int8, 1 fp8 e4m3, 2 fp8 e5m2 weights, 3 MXFP4 and
+// 4 int4 codes coded as bytes), and of its
 // 16-wave counterpart in wc_gemm_wide.hip, worked out once per device ({0, 0}
 // when unknown).  A launch whose tiles overflow the first but fit the second
 // runs on the 16-wave kernel, in one round.
@@ -288,9 +289,9 @@ bool gemv_wide(int kind, uint64_t tiles) {
   struct Cap {
     uint64_t general, wide;
   };
-  if (kind < 0 || kind > 2) return false;
+  if (kind < 0 || kind > 4) return false;
   static std::mutex mu;
-  static std::vector<std::pair<int, Cap>> known[3];
+  static std::vector<std::pair<int, Cap>> known[5];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return false;
   Cap c{0, 0};
@@ -302,7 +303,9 @@ bool gemv_wide(int kind, uint64_t tiles) {
     if (!found) {
       int cus = 0, per_cu = 0;
       const void* k8 =
-          kind == 2   ? reinterpret_cast<const void*>(wc_gemv_e5m2_kernel<1>)
+          kind == 4   ? reinterpret_cast<const void*>(wc_gemv_w4_kernel<1>)
+          : kind == 3 ? reinterpret_cast<const void*>(wc_gemv_mxb_kernel<1>)
+          : kind == 2 ? reinterpret_cast<const void*>(wc_gemv_e5m2_kernel<1>)
           : kind == 1 ? reinterpret_cast<const void*>(wc_gemv_kernel<0, 1, 16, 4, true>)
                       : reinterpret_cast<const void*>(wc_gemv_kernel<0, 1, 16, 4, false>);
       if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
@@ -314,6 +317,12 @@ bool gemv_wide(int kind, uint64_t tiles) {
   }
   return c.general && c.wide > c.general && tiles > c.general && tiles <= c.wide;
 }
+
+// Rows of x up to which the byte-coded MXFP4 and int4 launches take the 16-wave
+// kernel (in its window): on the 8B layers it gains 3-9 % up to 8 rows, nothing
+// at 12 and loses at 16 rows, where each wave row's conversions and products
+// weigh more than the extra waves.
+constexpr uint32_t kWideQ4Rows = 8;
 
 // One launch per tile height and weight type (bf16 on 64 rows: VALU dot
 // products up to kDotRows rows of x, MFMA above, or the shared GEMM; bf16 on
@@ -518,10 +527,19 @@ extern "C" wc_status wc_gemv_mx(const wc_blob* desc, const void* dev_blob, uint3
       return WC_EUNSUPPORTED;
   }
   const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  // one launch for the nibble-coded jobs, one for the byte-coded ones
+  // one launch for the nibble-coded jobs, one for the byte-coded ones (the
+  // latter on the 16-wave kernel when it has up to kWideQ4Rows rows of x and
+  // its tiles fit it)
   for (int bytes = 0; bytes < 2; bytes++) {
     LaunchArgs args{};
     fill_common(args, P, dev_blob, dev_err);
+    uint64_t tiles = 0;
+    for (uint32_t i = 0; i < n; i++) {
+      const wc::TensorInfo& T = P.tensors[tensors[i]];
+      if ((T.dtype == WC_U8) == (bytes == 1)) tiles += T.n_chunks;
+    }
+    const bool wide = bytes && m <= kWideQ4Rows && tiles && gemv_wide(3, tiles);
+    const uint64_t per_wg = wide ? uint64_t(wc::kWideWaves) : uint64_t(kWaves);
     uint32_t wgs = 0, nt = 0;
     for (uint32_t i = 0; i < n; i++) {
       const wc::TensorInfo& T = P.tensors[tensors[i]];
@@ -529,12 +547,16 @@ extern "C" wc_status wc_gemv_mx(const wc_blob* desc, const void* dev_blob, uint3
       fill_tensor(args.t[nt], T, dev_y[i], wgs);
       args.t[nt].x = reinterpret_cast<uint64_t>(dev_x[i]);
       args.t[nt].scales = reinterpret_cast<uint64_t>(dev_scales[i]);
-      wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
+      wgs += uint32_t((T.n_chunks + per_wg - 1) / per_wg);
       nt++;
     }
     if (!nt) continue;
     args.n_tensors = nt;
     args.m = m;
+    if (wide) {
+      if (!wc::gemv_wide_launch(3, &args, sizeof args, wgs, st)) return WC_EHIP;
+      continue;
+    }
     const dim3 grid(wgs), block(kThreads);
     if (bytes) {
       switch ((m + 15) / 16) {
@@ -583,10 +605,19 @@ extern "C" wc_status wc_gemv_w4(const wc_blob* desc, const void* dev_blob, uint3
       return WC_EUNSUPPORTED;
   }
   const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
-  // one launch for the byte-coded jobs, one for the nibble-coded ones
+  // one launch for the byte-coded jobs (on the 16-wave kernel when it has up
+  // to kWideQ4Rows rows of x and its tiles fit it), one for the nibble-coded
+  // ones
   for (int nibbles = 0; nibbles < 2; nibbles++) {
     LaunchArgs args{};
     fill_common(args, P, dev_blob, dev_err);
+    uint64_t tiles = 0;
+    for (uint32_t i = 0; i < n; i++) {
+      const wc::TensorInfo& T = P.tensors[tensors[i]];
+      if ((T.dtype == WC_U4) == (nibbles == 1)) tiles += T.n_chunks;
+    }
+    const bool wide = !nibbles && m <= kWideQ4Rows && tiles && gemv_wide(4, tiles);
+    const uint64_t per_wg = wide ? uint64_t(wc::kWideWaves) : uint64_t(kWaves);
     uint32_t wgs = 0, nt = 0;
     for (uint32_t i = 0; i < n; i++) {
       const wc::TensorInfo& T = P.tensors[tensors[i]];
@@ -595,12 +626,16 @@ extern "C" wc_status wc_gemv_w4(const wc_blob* desc, const void* dev_blob, uint3
       args.t[nt].x = reinterpret_cast<uint64_t>(dev_x[i]);
       args.t[nt].scales = reinterpret_cast<uint64_t>(dev_scales[i]);
       args.t[nt].zeros = dev_zeros ? reinterpret_cast<uint64_t>(dev_zeros[i]) : 0ull;
-      wgs += uint32_t((T.n_chunks + kWaves - 1) / kWaves);
+      wgs += uint32_t((T.n_chunks + per_wg - 1) / per_wg);
       nt++;
     }
     if (!nt) continue;
     args.n_tensors = nt;
     args.m = m;
+    if (wide) {
+      if (!wc::gemv_wide_launch(4, &args, sizeof args, wgs, st)) return WC_EHIP;
+      continue;
+    }
     const dim3 grid(wgs), block(kThreads);
     if (nibbles) {
       switch ((m + 15) / 16) {

@@ -1,7 +1,7 @@
 // wc_gemm_wide.hip -- 16-wave-workgroup instances of the fused decode-GEMM
-// (Alg. 1 / 3; the decoder is in wc_decoder.h) for int8 weights (wc_gemm_i8)
-// and fp8 e4m3 and e5m2 weights (wc_gemv) on 16-row tiles with up to 16 rows
-// of x.  One
+// (Alg. 1 / 3; the decoder is in wc_decoder.h) for int8 weights (wc_gemm_i8),
+// fp8 e4m3 and e5m2 weights (wc_gemv) and MXFP4 and int4 codes coded as bytes
+// (wc_gemv_mx, wc_gemv_w4) on 16-row tiles with up to 16 rows of x.  One
 // decode table serves 16 waves, so a compute unit holds 32 of these waves
 // against 24 of the 8-wave kernels in wc_gemm.hip; the launches of those
 // entry points whose tiles overflow the 8-wave kernel's resident waves but
@@ -58,8 +58,37 @@ __global__ __launch_bounds__(wc::kWideWaves * 64) void wc_gemv_wide_e5m2_kernel(
   decode_chunks<4, 64, true, 0, 1, 16, false, 2>(a, T, chunk, lane, tab, ring[wave], pre);
 }
 
-// kind: 0 int8, 1 fp8 e4m3, 2 fp8 e5m2
+// 4-bit codes coded as bytes (the packed pairs): MXFP4 (kF8 = 3, e8m0 scale
+// per 32 codes) or group-quantised int4 (kF8 = 4, scale and zero point per
+// 128).  Their 8-wave kernels need 68-73 registers; held to 64 here, for 8
+// waves per SIMD, the compiler keeps two values of the chunk's set-up in
+// scratch across the decode loop (8-12 bytes per lane, outside the loop).
+template <int kF8>
+__global__ __launch_bounds__(wc::kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(8)))
+void wc_gemv_wide_q4_kernel(LaunchArgs a) {
+  __shared__ uint2 tab[wc::kTableSize];
+  __shared__ uint32_t cum[260];
+  __shared__ uint32_t ring[wc::kWideWaves][wc_ring_words() / 2];
+  const uint32_t wg = blockIdx.x;
+  uint32_t ti = 0;
+  for (uint32_t k = 1; k < a.n_tensors; k++)
+    if (wg >= a.t[k].wg0) ti = k;
+  const DevTensor& T = a.t[ti];
+  const uint32_t tid = threadIdx.x;
+  const uint32_t wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const uint32_t lane = __lane_id();
+  const uint32_t chunk = (wg - T.wg0) * wc::kWideWaves + wave;
+  const IndexPre pre = load_index(a, T, chunk, 1u);
+  build_table<wc::kWideWaves * 64>(a, T, tab, cum, tid);
+  __syncthreads();
+  if (chunk >= T.n_chunks) return;
+  decode_chunks<4, 64, true, 0, 1, 16, false, kF8>(a, T, chunk, lane, tab, ring[wave], pre);
+}
+
+// kind: 0 int8, 1 fp8 e4m3, 2 fp8 e5m2, 3 MXFP4 as bytes, 4 int4 as bytes
 const void* wide_kernel(int kind) {
+  if (kind == 4) return reinterpret_cast<const void*>(wc_gemv_wide_q4_kernel<4>);
+  if (kind == 3) return reinterpret_cast<const void*>(wc_gemv_wide_q4_kernel<3>);
   if (kind == 2) return reinterpret_cast<const void*>(wc_gemv_wide_e5m2_kernel);
   return kind == 1 ? reinterpret_cast<const void*>(wc_gemv_wide_kernel<true>)
                    : reinterpret_cast<const void*>(wc_gemv_wide_kernel<false>);
@@ -71,7 +100,7 @@ namespace wc {
 
 uint64_t gemv_wide_resident_waves(int kind) {
   int dev = 0, cus = 0, per_cu = 0;
-  if (kind < 0 || kind > 2 || hipGetDevice(&dev) != hipSuccess ||
+  if (kind < 0 || kind > 4 || hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
       hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, wide_kernel(kind), kWideWaves * 64,
                                                    0) != hipSuccess)
@@ -81,12 +110,16 @@ uint64_t gemv_wide_resident_waves(int kind) {
 
 bool gemv_wide_launch(int kind, const void* launch_args, uint64_t bytes, uint32_t workgroups,
                       void* stream) {
-  if (bytes != sizeof(LaunchArgs) || kind < 0 || kind > 2) return false;
+  if (bytes != sizeof(LaunchArgs) || kind < 0 || kind > 4) return false;
   LaunchArgs args;
   memcpy(&args, launch_args, sizeof args);
   const hipStream_t st = reinterpret_cast<hipStream_t>(stream);
   const dim3 grid(workgroups), block(kWideWaves * 64);
-  if (kind == 2)
+  if (kind == 4)
+    hipLaunchKernelGGL((wc_gemv_wide_q4_kernel<4>), grid, block, 0, st, args);
+  else if (kind == 3)
+    hipLaunchKernelGGL((wc_gemv_wide_q4_kernel<3>), grid, block, 0, st, args);
+  else if (kind == 2)
     hipLaunchKernelGGL(wc_gemv_wide_e5m2_kernel, grid, block, 0, st, args);
   else if (kind == 1)
     hipLaunchKernelGGL((wc_gemv_wide_kernel<true>), grid, block, 0, st, args);

@@ -807,6 +807,25 @@ def test_mx_gemv_quantised_layer(dev, coding):
         assert (np.abs(y.cpu().numpy().astype(np.float64)[:, rows] - ref) <= tol).all(), t.name
 
 
+@pytest.mark.parametrize("tiles,m", [(6144, 8), (6145, 1), (8192, 8), (8193, 8), (7000, 9)])
+def test_mx_gemv_bytes_around_the_wide_kernels_window(dev, tiles, m):
+    """MXFP4 codes coded as bytes run on a 16-wave kernel when the launch has
+    up to 8 rows of x and its 16-row tiles overflow the 8-wave
+    kernel's resident waves (6144 on a 256-CU MI355X) but fit the 16-wave
+    kernel's (8192).  Tile counts on both edges of that window and m = 9
+    (outside it): sampled rows of y within the fp32 summation bound of the
+    oracle's product."""
+    say("mx bytes wide window", tiles, m)
+    rows, cols = 16 * tiles, 512
+    rng = np.random.default_rng(tiles + 5)
+    w = _mx_pack(rng.integers(0, 16, (rows, cols)).astype(np.uint8))
+    sc = rng.integers(112, 140, (rows, cols // 32)).astype(np.uint8)
+    x = _bf16(rng.normal(0, 1.0, (m, cols)))
+    y = _run_mx(_mx_encode(w, rows, cols, (16, 512), "bytes"), dev, 0, sc, x)
+    pick = np.concatenate([rng.choice(rows, 64, replace=False), [0, rows - 1]])
+    _check_mx(y[:, pick], np.ascontiguousarray(w[pick]), np.ascontiguousarray(sc[pick]), x)
+
+
 def test_mx_gemv_limits(dev):
     rng = np.random.default_rng(84)
     codes = rng.integers(0, 16, (64, 512)).astype(np.uint8)
@@ -985,6 +1004,30 @@ def test_w4_gemv_quantised_layer(dev, cfg, coding):
         ref, absref = oracle.gemv_int4(w, sc, z, xbits[t.shape[1]])
         tol = _w4_tolerance(w, sc, z, xbits[t.shape[1]], absref)
         assert (np.abs(y.cpu().numpy().astype(np.float64)[:, rows] - ref) <= tol).all(), t.name
+
+
+@pytest.mark.parametrize("tiles,m", [(6144, 8), (6145, 1), (8192, 8), (8193, 8), (7000, 9)])
+def test_w4_gemv_bytes_around_the_wide_kernels_window(dev, tiles, m):
+    """int4 codes coded as bytes run on a 16-wave kernel when the launch has
+    up to 8 rows of x and its 16-row tiles overflow the 8-wave
+    kernel's resident waves (6144 on a 256-CU MI355X) but fit the 16-wave
+    kernel's (8192).  Tile counts on both edges of that window and m = 9
+    (outside it), with zero points on odd tile counts: sampled rows of y
+    within the derived bound of the oracle's product."""
+    say("w4 bytes wide window", tiles, m)
+    rows, cols = 16 * tiles, 512
+    rng = np.random.default_rng(tiles + 9)
+    w = _w4_pack(rng.integers(0, 16, (rows, cols)).astype(np.uint8))
+    sc = rng.uniform(0.002, 0.05, (rows, cols // 128)).astype(np.float16).view(np.uint16)
+    zeros = rng.integers(0, 16, (rows, cols // 128)).astype(np.uint8) if tiles % 2 else None
+    x = _bf16(rng.normal(0, 1.0, (m, cols)))
+    y = _run_w4(_w4_encode(w, rows, cols, 256, "bytes"), dev, sc, zeros, x)
+    pick = np.concatenate([rng.choice(rows, 64, replace=False), [0, rows - 1]])
+    wp, sp = np.ascontiguousarray(w[pick]), np.ascontiguousarray(sc[pick])
+    zp = None if zeros is None else np.ascontiguousarray(zeros[pick])
+    ref, absref = oracle.gemv_int4(wp, sp, zp, x)
+    tol = _w4_tolerance(wp, sp, zp, x, absref)
+    assert (np.abs(y[:, pick] - ref) <= tol).all()
 
 
 def test_w4_gemv_limits(dev):
