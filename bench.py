@@ -311,24 +311,28 @@ def decode_kernel_for(dtypes, n_chunks: int, lanes: int, tiled: bool) -> str:
 
 
 def gemv_kernel_for(weights: str, n_tiles: int, m: int) -> str:
-    """The kernel of a fused-GEMM launch of 16-row tiles (weights: "int8",
-    "e4m3", "e5m2", or "mxfp4" / "int4" with "-bytes" when the 4-bit codes are
-    coded as bytes).  int8, fp8 and byte-coded 4-bit launches take a 16-wave
+    """The kernel of a fused-GEMM launch of 16-row tiles (weights: "bf16",
+    "int8", "e4m3", "e5m2", or "mxfp4" / "int4" with "-bytes" when the 4-bit
+    codes are coded as bytes).  bf16, int8, fp8 and byte-coded 4-bit launches
+    take a 16-wave
     kernel when they have up to 16 rows of x (8 for the 4-bit codes) and their
     tiles exceed the 8-wave kernel's resident waves (24 a compute unit) but fit
     the 16-wave kernel's (32 a compute unit).  The library takes the same
     decision from the runtime's occupancy figures."""
     import torch
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    wide_rows = {"int8": 16, "e4m3": 16, "e5m2": 16, "mxfp4-bytes": 8, "int4-bytes": 8}
+    wide_rows = {"bf16": 16, "int8": 16, "e4m3": 16, "e5m2": 16, "mxfp4-bytes": 8,
+                 "int4-bytes": 8}
     wide = m <= wide_rows.get(weights, 0) and 24 * cus < n_tiles <= 32 * cus
-    general = {"int8": "wc_gemv_kernel (int8)", "e4m3": "wc_gemv_kernel (fp8 e4m3)",
+    general = {"bf16": "wc_gemv_kernel (bf16)", "int8": "wc_gemv_kernel (int8)",
+               "e4m3": "wc_gemv_kernel (fp8 e4m3)",
                "e5m2": "wc_gemv_e5m2_kernel", "mxfp4": "wc_gemv_mx_kernel",
                "mxfp4-bytes": "wc_gemv_mxb_kernel", "int4": "wc_gemv_w4n_kernel",
                "int4-bytes": "wc_gemv_w4_kernel"}[weights]
     if not wide:
         return general
-    return {"int8": "wc_gemv_wide_kernel (int8)", "e4m3": "wc_gemv_wide_kernel (fp8 e4m3)",
+    return {"bf16": "wc_gemv_wide_bf16_kernel", "int8": "wc_gemv_wide_kernel (int8)",
+            "e4m3": "wc_gemv_wide_kernel (fp8 e4m3)",
             "e5m2": "wc_gemv_wide_e5m2_kernel", "mxfp4-bytes": "wc_gemv_wide_q4_kernel (MXFP4)",
             "int4-bytes": "wc_gemv_wide_q4_kernel (int4)"}[weights]
 
@@ -392,13 +396,17 @@ def main() -> int:
                     help="time the device encoder (wc_encode_device) on the resident 70B "
                          "layer instead of the decode")
     ap.add_argument("--gemv", type=int, default=0, metavar="M",
-                    help="time the fused decode-GEMM y += x W^T (x: M rows, 1..4096) over the "
-                         "70B layer instead of the decode, next to the same product unfused "
-                         "(wc_decode, then torch.matmul) and uncompressed (torch.matmul)")
+                    help="time the fused decode-GEMM y += x W^T (x: M rows, 1..4096) over a "
+                         "bf16 layer (--gemv-layer) instead of the decode, next to the same "
+                         "product unfused (wc_decode, then torch.matmul) and uncompressed "
+                         "(torch.matmul)")
     ap.add_argument("--gemv-rows", type=int, choices=[64, 32, 16], default=0,
                     help="tile rows of the fused GEMM: 64 (VALU dot products for M <= 5, "
                          "matrix cores above), 32 or 16 (matrix cores); default 16 for "
                          "M <= 16, else 64")
+    ap.add_argument("--gemv-layer", choices=["70b", "8b"], default="70b",
+                    help="the bf16 layer of --gemv: the Llama-3-70B layer (default) or the "
+                         "Llama-3-8B layer, the latter rotated over resident copies")
     ap.add_argument("--gemm-i8", type=int, default=0, metavar="M",
                     help="time the fused int8 decode-GEMM (W8A8: int8 x, int32 y, "
                          "v_mfma_i32_16x16x64_i8; M rows, 1..64) over the int8 projections of "
@@ -734,7 +742,9 @@ def main() -> int:
 
 
 def gemv_bench(args, dev) -> int:
-    """Fused decode-GEMM over the seven projections of one 70B layer."""
+    """Fused decode-GEMM over the seven projections of one bf16 layer: the 70B
+    layer (one copy, 1.7 GB of weights), or with --gemv-layer 8b the 8B layer,
+    whose variants rotate over resident copies (>= 1 GiB each)."""
     import numpy as np
     import torch
 
@@ -749,7 +759,12 @@ def gemv_bench(args, dev) -> int:
     # 16 x 2048 (a wave row per MFMA operand)
     tile = {64: (64, 512), 32: (32, 1024), 16: (16, 2048)}[rows]
     t0 = time.perf_counter()
-    tens = synth.config_torch_device(5, 0, device="cuda")
+    if args.gemv_layer == "8b":
+        workload = "llama3-8b-layer-bf16"
+        tens = synth.layer_torch_device(synth.LLAMA3_8B, 0.02, 1, 0, device="cuda")
+    else:
+        workload = "llama3-70b-layer-bf16"
+        tens = synth.config_torch_device(5, 0, device="cuda")
     shapes = [shape for _, _, shape in tens]
     host = [t.cpu().numpy() for _, t, _ in tens]
     blob = wc.encode([("bf16", h, shp) for h, shp in zip(host, shapes)], lanes=64, tile=tile,
@@ -769,9 +784,9 @@ def gemv_bench(args, dev) -> int:
     need = wc.gemm_workspace_bytes(blob, list(range(len(W))), [x.data_ptr() for x in xs], M)
     ws = torch.empty(max(need, 256), dtype=torch.uint8, device=dev)
 
-    def fused():
+    def fused(d=dblob):
         # one launch per tile height for the seven projections (plus the x packing)
-        wc.gemm(blob, dblob.data_ptr(), list(range(len(W))), [x.data_ptr() for x in xs], M,
+        wc.gemm(blob, d.data_ptr(), list(range(len(W))), [x.data_ptr() for x in xs], M,
                 [y.data_ptr() for y in ys], ws.data_ptr(), ws.numel(), stream.cuda_stream,
                 err.data_ptr())
 
@@ -795,29 +810,35 @@ def gemv_bench(args, dev) -> int:
     dflat = wc.to_device(flat, dev)
     outs = [torch.empty(n, dtype=torch.uint8, device=dev) for n in flat.out_bytes]
 
-    def unfused():
-        wc.decode(flat, dflat.data_ptr(), [o.data_ptr() for o in outs], stream.cuda_stream,
-                  err.data_ptr())
-        for t, (o, x, shp) in enumerate(zip(outs, xs, shapes)):
+    # the 70B layer is well past the 256 MB Infinity Cache in one copy; the 8B
+    # layer's variants rotate over resident copies of their operands
+    if args.gemv_layer == "8b":
+        n_f = rotation_copies(blob.size)
+        n_u = rotation_copies(flat.size + sum(flat.out_bytes))
+        n_p = rotation_copies(sum(w.numel() * 2 for w in W))
+    else:
+        n_f = n_u = n_p = 1
+    dblobs = [dblob] + [dblob.clone() for _ in range(n_f - 1)]
+    dflats = [dflat] + [dflat.clone() for _ in range(n_u - 1)]
+    outss = [outs] + [[torch.empty_like(o) for o in outs] for _ in range(n_u - 1)]
+    Ws = [W] + [[w.clone() for w in W] for _ in range(n_p - 1)]
+
+    def fused_k(k):
+        fused(dblobs[k % n_f])
+
+    def unfused(k):
+        o_k = outss[k % n_u]
+        wc.decode(flat, dflats[k % n_u].data_ptr(), [o.data_ptr() for o in o_k],
+                  stream.cuda_stream, err.data_ptr())
+        for t, (o, x, shp) in enumerate(zip(o_k, xs, shapes)):
             torch.matmul(x, o.view(torch.bfloat16).view(shp).t())
 
-    def uncompressed():
-        for w, x in zip(W, xs):
+    def uncompressed(k):
+        for w, x in zip(Ws[k % n_p], xs):
             torch.matmul(x, w.t())
 
-    def timed(fn):
-        for _ in range(args.warmup):
-            fn()
-        torch.cuda.synchronize()
-        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        a.record(stream)
-        for _ in range(args.steps):
-            fn()
-        b.record(stream)
-        torch.cuda.synchronize()
-        return a.elapsed_time(b) / args.steps / 1e3
-
-    s_fused, s_unfused, s_plain = timed(fused), timed(unfused), timed(uncompressed)
+    s_fused, s_unfused, s_plain = (timed_rotating(f, args.warmup, args.steps, stream)
+                                   for f in (fused_k, unfused, uncompressed))
     if int(err.item()):
         raise RuntimeError(f"device errors: {wc.describe_errors(int(err.item()))}")
     wbytes = sum(blob.out_bytes)
@@ -841,7 +862,7 @@ def gemv_bench(args, dev) -> int:
         "vs_baseline": None,
         "dtype": "bf16 x bf16 -> fp32",
         "data": "synthetic",
-        "config": {"workload": "llama3-70b-layer-bf16", "mode": "fused-gemv", "m": M,
+        "config": {"workload": workload, "mode": "fused-gemv", "m": M,
                    "tile": f"{tile[0]}x{tile[1]}", "tile_order": "column-blocks",
                    "product": ("v_dot2_f32_bf16" if rows == 64 and M <= 5 else
                                "v_mfma_f32_16x16x32_bf16" if rows == 16 else
@@ -850,6 +871,7 @@ def gemv_bench(args, dev) -> int:
                                         if shared else "call"),
                    "lanes": 64, "weight_bytes_per_step": wbytes,
                    "compressed_bytes_per_step": blob.size,
+                   "copies_resident": {"fused": n_f, "unfused": n_u, "uncompressed": n_p},
                    "parallelism": "single-gpu"},
         "roofline": ({"bound": "mfma", "achieved": round(tflops, 1),
                       "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
@@ -858,7 +880,9 @@ def gemv_bench(args, dev) -> int:
                      {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                       "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                       "traffic": None})
-                    | {"kernel": "wc_gemm_kernel" if shared else "wc_gemv_kernel",
+                    | {"kernel": ("wc_gemm_kernel" if shared else
+                                  gemv_kernel_for("bf16", blob.n_chunks, M) if rows == 16 else
+                                  "wc_gemv_kernel"),
                        "mean_step_us": round(s_fused * 1e6, 2),
                        "algorithmic_bytes_per_step": int(alg), "flops_per_step": flops,
                        "hbm_frac": round(achieved / HBM_PEAK_GBPS, 4),

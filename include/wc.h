@@ -252,9 +252,9 @@ wc_status wc_decode(const wc_blob* desc, const void* dev_blob, void* const* dev_
  *            tiles of one band of rows add with fp32 atomics, so the
  *            summation order, and the last bits of y, can differ between runs;
  *   stream, dev_err as for wc_decode.
- * fp8 jobs with m <= 16 whose tiles exceed the 8-wave kernel's resident waves
- * on the current device but fit those of a 16-wave-workgroup kernel for that
- * format run on the latter, as in wc_decode.
+ * bf16 and fp8 jobs on 16-row tiles with m <= 16 whose tiles exceed the
+ * 8-wave kernel's resident waves on the current device but fit those of a
+ * 16-wave-workgroup kernel for that format run on the latter, as in wc_decode.
  * Asynchronous; allocates nothing.  Returns WC_EINVAL (argument), or
  * WC_EUNSUPPORTED (a tensor is not a bf16 64-lane column-block tensor of 64,
  * 32 or 16 rows per tile or an fp8 (e4m3, e5m2) one of 16 rows, has 64-row tiles of 8

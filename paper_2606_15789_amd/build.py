@@ -11,8 +11,8 @@ CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libwc.so")
 SOURCES = [os.path.join(CSRC, "wc_host.cpp"), os.path.join(CSRC, "wc_decode.hip"),
            os.path.join(CSRC, "wc_decode_wide.hip"), os.path.join(CSRC, "wc_gemm.hip"),
-           os.path.join(CSRC, "wc_gemm_wide.hip"), os.path.join(CSRC, "wc_encode.hip"),
-           os.path.join(CSRC, "wc_stream.hip")]
+           os.path.join(CSRC, "wc_gemm_wide.hip"), os.path.join(CSRC, "wc_gemm_wide_bf16.hip"),
+           os.path.join(CSRC, "wc_encode.hip"), os.path.join(CSRC, "wc_stream.hip")]
 HEADERS = [os.path.join(CSRC, "wc_internal.h"), os.path.join(CSRC, "wc_decoder.h"),
            os.path.join(os.path.dirname(HERE), "include", "wc.h")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
@@ -40,7 +40,7 @@ def stale() -> bool:
 KERNELS = os.path.join(HERE, "libwc.kernels.json")
 KERNEL_SOURCES = [os.path.join(CSRC, "wc_decode.hip"), os.path.join(CSRC, "wc_decode_wide.hip"),
                   os.path.join(CSRC, "wc_gemm.hip"), os.path.join(CSRC, "wc_gemm_wide.hip"),
-                  os.path.join(CSRC, "wc_stream.hip")]
+                  os.path.join(CSRC, "wc_gemm_wide_bf16.hip"), os.path.join(CSRC, "wc_stream.hip")]
 
 
 def kernel_fingerprints(asm: str) -> dict:

@@ -281,7 +281,7 @@ wc_status check_jobs(const wc_blob* desc, const void* dev_blob, uint32_t n,
 
 // Resident waves of the 8-wave fused-GEMM kernel for 16-row tiles with one
 // block of x rows (kind: 0 int8, 1 fp8 e4m3, 2 fp8 e5m2 weights, 3 MXFP4 and
-// 4 int4 codes coded as bytes), and of its
+// 4 int4 codes coded as bytes, 5 bf16 weights), and of its
 // 16-wave counterpart in wc_gemm_wide.hip, worked out once per device ({0, 0}
 // when unknown).  A launch whose tiles overflow the first but fit the second
 // runs on the 16-wave kernel, in one round.
@@ -289,9 +289,9 @@ bool gemv_wide(int kind, uint64_t tiles) {
   struct Cap {
     uint64_t general, wide;
   };
-  if (kind < 0 || kind > 4) return false;
+  if (kind < 0 || kind > 5) return false;
   static std::mutex mu;
-  static std::vector<std::pair<int, Cap>> known[5];
+  static std::vector<std::pair<int, Cap>> known[6];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return false;
   Cap c{0, 0};
@@ -303,7 +303,8 @@ bool gemv_wide(int kind, uint64_t tiles) {
     if (!found) {
       int cus = 0, per_cu = 0;
       const void* k8 =
-          kind == 4   ? reinterpret_cast<const void*>(wc_gemv_w4_kernel<1>)
+          kind == 5   ? reinterpret_cast<const void*>(wc_gemv_kernel<0, 1, 16>)
+          : kind == 4 ? reinterpret_cast<const void*>(wc_gemv_w4_kernel<1>)
           : kind == 3 ? reinterpret_cast<const void*>(wc_gemv_mxb_kernel<1>)
           : kind == 2 ? reinterpret_cast<const void*>(wc_gemv_e5m2_kernel<1>)
           : kind == 1 ? reinterpret_cast<const void*>(wc_gemv_kernel<0, 1, 16, 4, true>)
@@ -327,7 +328,7 @@ constexpr uint32_t kWideQ4Rows = 8;
 // One launch per tile height and weight type (bf16 on 64 rows: VALU dot
 // products up to kDotRows rows of x, MFMA above, or the shared GEMM; bf16 on
 // 32 or 16 rows: MFMA; fp8 e4m3, then e5m2, on 16 rows: converted to bf16,
-// MFMA; fp8 launches with one block of x rows may take the 16-wave kernel,
+// MFMA; 16-row launches with one block of x rows may take the 16-wave kernel,
 // see gemv_wide).  xs: the x (or, for the shared GEMM, packed x) of each job.
 wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
                       const uint32_t* tensors, const uint64_t* xs, uint32_t m,
@@ -340,15 +341,17 @@ wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
     const uint32_t dtype = f8 == 0 ? WC_BF16 : (f8 == 1 ? WC_FP8_E4M3 : WC_FP8_E5M2);
     LaunchArgs args{};
     fill_common(args, P, dev_blob, dev_err);
-    // fp8 with one block of x rows: the 16-wave kernel when its tiles fit it
+    // bf16 or fp8 on 16-row tiles with one block of x rows: the 16-wave
+    // kernel when its tiles fit it
+    const int wide_kind = f8 ? int(f8) : 5;
     bool wide = false;
-    if (f8 != 0 && m <= 16) {
+    if (rows == 16 && !share && m <= 16) {
       uint64_t tiles = 0;
       for (uint32_t i = 0; i < n; i++) {
         const wc::TensorInfo& T = P.tensors[tensors[i]];
         if (T.tile_r == rows && T.dtype == dtype) tiles += T.n_chunks;
       }
-      wide = tiles && gemv_wide(int(f8), tiles);
+      wide = tiles && gemv_wide(wide_kind, tiles);
     }
     const uint64_t per_wg = wide ? uint64_t(wc::kWideWaves) : uint64_t(kWaves);
     uint32_t wgs = 0, nt = 0;
@@ -371,7 +374,7 @@ wc_status launch_jobs(const wc::BlobPriv& P, const void* dev_blob, uint32_t n,
     args.n_tensors = nt;
     args.m = m;
     if (wide) {
-      if (!wc::gemv_wide_launch(int(f8), &args, sizeof args, wgs, st)) return WC_EHIP;
+      if (!wc::gemv_wide_launch(wide_kind, &args, sizeof args, wgs, st)) return WC_EHIP;
       continue;
     }
     const dim3 grid(wgs), block(kThreads);

@@ -1,7 +1,8 @@
 // wc_gemm_wide.hip -- 16-wave-workgroup instances of the fused decode-GEMM
 // (Alg. 1 / 3; the decoder is in wc_decoder.h) for int8 weights (wc_gemm_i8),
 // fp8 e4m3 and e5m2 weights (wc_gemv) and MXFP4 and int4 codes coded as bytes
-// (wc_gemv_mx, wc_gemv_w4) on 16-row tiles with up to 16 rows of x.  One
+// (wc_gemv_mx, wc_gemv_w4) on 16-row tiles with up to 16 rows of x (bf16
+// weights: wc_gemm_wide_bf16.hip).  One
 // decode table serves 16 waves, so a compute unit holds 32 of these waves
 // against 24 of the 8-wave kernels in wc_gemm.hip; the launches of those
 // entry points whose tiles overflow the 8-wave kernel's resident waves but
@@ -86,6 +87,7 @@ void wc_gemv_wide_q4_kernel(LaunchArgs a) {
 }
 
 // kind: 0 int8, 1 fp8 e4m3, 2 fp8 e5m2, 3 MXFP4 as bytes, 4 int4 as bytes
+// (5, bf16, is in wc_gemm_wide_bf16.hip)
 const void* wide_kernel(int kind) {
   if (kind == 4) return reinterpret_cast<const void*>(wc_gemv_wide_q4_kernel<4>);
   if (kind == 3) return reinterpret_cast<const void*>(wc_gemv_wide_q4_kernel<3>);
@@ -99,6 +101,7 @@ const void* wide_kernel(int kind) {
 namespace wc {
 
 uint64_t gemv_wide_resident_waves(int kind) {
+  if (kind == 5) return gemv_wide_bf16_resident_waves();
   int dev = 0, cus = 0, per_cu = 0;
   if (kind < 0 || kind > 4 || hipGetDevice(&dev) != hipSuccess ||
       hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
@@ -110,6 +113,7 @@ uint64_t gemv_wide_resident_waves(int kind) {
 
 bool gemv_wide_launch(int kind, const void* launch_args, uint64_t bytes, uint32_t workgroups,
                       void* stream) {
+  if (kind == 5) return gemv_wide_bf16_launch(launch_args, bytes, workgroups, stream);
   if (bytes != sizeof(LaunchArgs) || kind < 0 || kind > 4) return false;
   LaunchArgs args;
   memcpy(&args, launch_args, sizeof args);

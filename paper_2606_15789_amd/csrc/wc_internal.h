@@ -28,11 +28,15 @@ uint64_t wide_resident_waves();
 bool wide_launch(const void* launch_args, uint64_t bytes, uint32_t workgroups, void* stream);
 // The same for the fused decode-GEMM on 16-row tiles with up to 16 rows of x
 // (wc_gemm_wide.hip); kind: 0 int8, 1 fp8 e4m3, 2 fp8 e5m2 weights, 3 MXFP4
-// and 4 int4 codes coded as bytes (0 resident waves, or false, for any other
-// kind).
+// and 4 int4 codes coded as bytes, 5 bf16 weights (0 resident waves, or
+// false, for any other kind).
 uint64_t gemv_wide_resident_waves(int kind);
 bool gemv_wide_launch(int kind, const void* launch_args, uint64_t bytes, uint32_t workgroups,
                       void* stream);
+// kind 5 of the two above (wc_gemm_wide_bf16.hip)
+uint64_t gemv_wide_bf16_resident_waves();
+bool gemv_wide_bf16_launch(const void* launch_args, uint64_t bytes, uint32_t workgroups,
+                           void* stream);
 
 inline bool dtype_ok(uint32_t dt) { return dt >= WC_BF16 && dt <= WC_FP4_E2M1; }
 inline bool has_raw(uint32_t dt) { return dt == WC_BF16 || dt == WC_FP16; }

@@ -127,6 +127,25 @@ def test_gemv_full_size_projection(dev):
     _check(y, w, x)
 
 
+@pytest.mark.parametrize("tiles,m", [(6144, 16), (6145, 1), (8192, 16), (8193, 16), (7000, 17)])
+def test_gemv_bf16_around_the_wide_kernels_window(dev, tiles, m):
+    """bf16 weights on 16-row tiles run on a 16-wave kernel when the launch has
+    one block of x rows (m <= 16) and its tiles overflow the 8-wave kernel's
+    resident waves (6144 on a 256-CU MI355X) but fit the 16-wave kernel's
+    (8192).  Tile counts on both edges of that window and m = 17 (outside it):
+    sampled rows of y within the fp32 summation bound of the oracle's
+    product."""
+    say("bf16 wide window", tiles, m)
+    rows, cols = 16 * tiles, 512
+    rng = np.random.default_rng(tiles + 1)
+    w = _bf16(rng.standard_normal((rows, cols), dtype=np.float32) * np.float32(0.02))
+    blob = wc.encode([("bf16", w, w.shape)], tile=(16, 512), tile_order=1)
+    x = _bf16(rng.normal(0, 1.0, (m, cols)))
+    y = _run_gemv(blob, dev, 0, x)
+    pick = np.concatenate([rng.choice(rows, 64, replace=False), [0, rows - 1]])
+    _check(y[:, pick], np.ascontiguousarray(w[pick]), x)
+
+
 def test_gemv_reports_corruption(dev):
     rng = np.random.default_rng(23)
     w = _bf16(rng.normal(0, 0.02, (128, 512)))
