@@ -62,8 +62,9 @@ __global__ __launch_bounds__(wc::kWideWaves * 64) void wc_gemv_wide_e5m2_kernel(
 // 4-bit codes coded as bytes (the packed pairs): MXFP4 (kF8 = 3, e8m0 scale
 // per 32 codes) or group-quantised int4 (kF8 = 4, scale and zero point per
 // 128).  Their 8-wave kernels need 68-73 registers; held to 64 here, for 8
-// waves per SIMD, the compiler keeps two values of the chunk's set-up in
-// scratch across the decode loop (8-12 bytes per lane, outside the loop).
+// waves per SIMD, the compiler keeps one or two values of the chunk's set-up
+// in scratch across the decode loop (8-12 bytes per lane, stored before the
+// loop and read after it).
 template <int kF8>
 __global__ __launch_bounds__(wc::kWideWaves * 64) __attribute__((amdgpu_waves_per_eu(8)))
 void wc_gemv_wide_q4_kernel(LaunchArgs a) {
