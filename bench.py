@@ -59,13 +59,19 @@ WORKLOADS = {WORKLOAD_DEFAULT: 5, "bf16-matrix-4096": 1, "llama3-8b-layer-bf16":
              "llama3-8b-layer-awq4": 8, "llama3-8b-layer-fp8-e5m2": 9}
 ROTATE_BYTES = 1 << 30   # resident bytes the small workloads rotate over
 
-# HBM bytes per launch of the 70B-layer decode from rocprofv3 --pmc FETCH_SIZE and
-# WRITE_SIZE runs, each scaled by the same counter on a 512 MiB device copy (FETCH_SIZE
-# reads half the copied bytes: factor 2.0; WRITE_SIZE is exact).  Valid only for the
-# decode kernel's code they were taken on (its fingerprint, the hash of its gfx950
-# assembly that the build writes); otherwise reported as null.
-COUNTED_TRAFFIC = {"kernel_fingerprint": "26a86b454521e29a", "fetch_bytes": 1141265856,
-                   "write_bytes": 1738020407, "chunk_bytes": 65536, "lanes": 64}
+# HBM bytes per launch of a workload's decode (64 KiB chunks, 64 lanes, untiled,
+# per-tensor tables) from rocprofv3 --pmc FETCH_SIZE and WRITE_SIZE runs, each scaled
+# by the same counter on a 512 MiB device copy (FETCH_SIZE reads half the copied
+# bytes: factor 2.0; WRITE_SIZE is exact).  Valid only for the kernel and code they
+# were taken on (its fingerprint, the hash of its gfx950 assembly that the build
+# writes); otherwise reported as null.
+COUNTED_TRAFFIC = {
+    "llama3-70b-layer-bf16": {"kernel": "wc_decode_kernel", "kernel_fingerprint": "26a86b454521e29a",
+                              "fetch_bytes": 1141265856, "write_bytes": 1738020407},
+    "llama3-8b-layer-bf16": {"kernel": "wc_decode_wide_kernel",
+                             "kernel_fingerprint": "f89c395c2a6474d3",
+                             "fetch_bytes": 291863961, "write_bytes": 443041996},
+}
 
 
 def log(*a):
@@ -282,9 +288,9 @@ def hbm_read_rate(dev, stream) -> float:
     return (1 << 30) / med / 1e9
 
 
-def decode_kernel_fingerprint():
-    """The fingerprint of wc_decode_kernel's gfx950 code in the loaded library
-    (written next to it by the build), or None."""
+def kernel_fingerprint(name: str = "wc_decode_kernel"):
+    """The fingerprint of a kernel's gfx950 code in the loaded library (written
+    next to it by the build), or None."""
     from paper_2606_15789_amd import wc
     path = os.path.splitext(wc.library_path())[0] + ".kernels.json"
     try:
@@ -292,7 +298,7 @@ def decode_kernel_fingerprint():
             prints = json.load(fh)
     except (OSError, ValueError):
         return None
-    return next((v for k, v in prints.items() if "wc_decode_kernel" in k), None)
+    return next((v for k, v in prints.items() if name in k), None)
 
 
 def decode_kernel_for(dtypes, n_chunks: int, lanes: int, tiled: bool) -> str:
@@ -337,12 +343,12 @@ def gemv_kernel_for(weights: str, n_tiles: int, m: int) -> str:
             "int4-bytes": "wc_gemv_wide_q4_kernel (int4)"}[weights]
 
 
-def counted_traffic(workload: str, chunk_bytes: int, lanes: int, tiled: bool = False):
+def counted_traffic(workload: str, chunk_bytes: int, lanes: int, tiled: bool, kernel: str):
     """HBM bytes per launch from the counter runs, if they were taken on this
-    workload and on the decode kernel as built now."""
-    c = COUNTED_TRAFFIC
-    if (workload != WORKLOAD_DEFAULT or tiled or chunk_bytes != c["chunk_bytes"]
-            or lanes != c["lanes"] or decode_kernel_fingerprint() != c["kernel_fingerprint"]):
+    workload and layout and on the kernel the launch runs on, as built now."""
+    c = COUNTED_TRAFFIC.get(workload)
+    if (c is None or tiled or chunk_bytes != 65536 or lanes != 64 or kernel != c["kernel"]
+            or kernel_fingerprint(kernel) != c["kernel_fingerprint"]):
         return None
     return c["fetch_bytes"] + c["write_bytes"]
 
@@ -702,6 +708,8 @@ def main() -> int:
     else:
         config["copies_resident"] = n_res
         config["step"] = "one wc_decode launch of one resident copy"
+    kname = decode_kernel_for([blobs[0].dtype(t) for t in range(blobs[0].n_tensors)],
+                              blobs[0].n_chunks, args.lanes, bool(args.tile))
     line = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -719,10 +727,9 @@ def main() -> int:
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBPS, 4),
                      "traffic": counted_traffic(args.workload, args.chunk_bytes, args.lanes,
-                                                bool(args.tile) or args.codebook != "tensor"),
-                     "kernel": decode_kernel_for(
-                         [blobs[0].dtype(t) for t in range(blobs[0].n_tensors)],
-                         blobs[0].n_chunks, args.lanes, bool(args.tile)),
+                                                bool(args.tile) or args.codebook != "tensor",
+                                                kname),
+                     "kernel": kname,
                      "median_launch_us": round(med_launch_s * 1e6, 2),
                      "mean_launch_us": round(mean_launch_s * 1e6, 2),
                      "launches_timed": G,

@@ -63,3 +63,19 @@ def test_gemv_kernel_window(bench, cus_256, weights, rows):
 def test_nibble_coded_4_bit_codes_keep_the_8_wave_kernels(bench, cus_256):
     assert bench.gemv_kernel_for("mxfp4", 6656, 1) == "wc_gemv_mx_kernel"
     assert bench.gemv_kernel_for("int4", 6656, 1) == "wc_gemv_w4n_kernel"
+
+
+def test_counted_traffic_only_for_the_kernel_and_layout_it_was_taken_on(bench, monkeypatch):
+    for workload, c in bench.COUNTED_TRAFFIC.items():
+        prints = {c["kernel"]: c["kernel_fingerprint"]}
+        monkeypatch.setattr(bench, "kernel_fingerprint", lambda name: prints.get(name))
+        want = c["fetch_bytes"] + c["write_bytes"]
+        assert bench.counted_traffic(workload, 65536, 64, False, c["kernel"]) == want
+        assert bench.counted_traffic(workload, 32768, 64, False, c["kernel"]) is None
+        assert bench.counted_traffic(workload, 65536, 32, False, c["kernel"]) is None
+        assert bench.counted_traffic(workload, 65536, 64, True, c["kernel"]) is None
+        other = "wc_decode_kernel" if c["kernel"] != "wc_decode_kernel" else "wc_decode_wide_kernel"
+        assert bench.counted_traffic(workload, 65536, 64, False, other) is None
+        prints[c["kernel"]] = "0000000000000000"          # the kernel's code changed
+        assert bench.counted_traffic(workload, 65536, 64, False, c["kernel"]) is None
+    assert bench.counted_traffic("bf16-matrix-4096", 65536, 64, False, "wc_decode_kernel") is None
